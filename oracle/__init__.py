@@ -1,0 +1,142 @@
+"""CPU oracle for the chunkwise GLA hot path.
+
+TEST INFRASTRUCTURE ONLY: the tests, ``__graft_entry__.smoke()`` and the CPU
+baseline leg of ``bench.py`` may use this package; the product library never
+does. It shares no code with the HIP path (the two meet only through the seeded
+input module, which holds no arithmetic of the method).
+
+* :func:`scan_order` - the four directional scan orders (paper Sec. 3.1,
+  "Directional scanning": left-to-right, right-to-left, top-to-bottom,
+  bottom-to-top), as the permutation "scan position -> spatial index".
+* :func:`permute` - gather / scatter of token rows by that permutation.
+* :func:`gla` - the key-only GLA recurrence (Sec. 3.1), float64, token by token,
+  in ``gla_oracle.c``.
+
+Readings taken where the paper is not explicit (each is listed with its reason
+in the design notes of the repository):
+
+* right-to-left is the full reversal of the row-major sequence, bottom-to-top
+  the full reversal of the column-major one (not per-row "snakes");
+* column-major visits column 0 top to bottom, then column 1, ...;
+* S0 is applied before the first token in scan order and S_final is the state
+  after the last token in scan order;
+* ``scale`` is explicit; the paper's value is d_k^{-1/2}.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+from typing import Optional
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "gla_oracle.c")
+_LIB = os.path.join(_HERE, "_build", "liboracle.so")
+
+SCAN_IDS = {"row": 0, "col": 1, "row_rev": 2, "col_rev": 3}
+
+
+def build(force: bool = True) -> str:
+    """Compile ``gla_oracle.c`` with gcc into ``oracle/_build/liboracle.so``."""
+    if not force and os.path.exists(_LIB) and os.path.getmtime(_LIB) >= os.path.getmtime(_SRC):
+        return _LIB
+    os.makedirs(os.path.dirname(_LIB), exist_ok=True)
+    tmp = _LIB + f".tmp{os.getpid()}"
+    # Plain -O2, no fast-math: the oracle keeps IEEE float64 semantics.
+    subprocess.check_call(["gcc", "-O2", "-fPIC", "-shared", "-std=c11", "-Wall",
+                           "-o", tmp, _SRC, "-lm", "-lpthread"])
+    os.replace(tmp, _LIB)
+    return _LIB
+
+
+_lib = None
+
+
+def _load():
+    global _lib
+    if _lib is None:
+        if not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
+            build()
+        lib = ctypes.CDLL(_LIB)
+        fn = lib.oracle_gla_forward
+        P = ctypes.c_void_p
+        fn.argtypes = [P, P, P, P, P, P, P, ctypes.c_long, ctypes.c_long, ctypes.c_int,
+                       ctypes.c_int, ctypes.c_double, P, ctypes.c_int]
+        fn.restype = ctypes.c_int
+        _lib = lib
+    return _lib
+
+
+def scan_order(H: int, W: int, scan: str) -> np.ndarray:
+    """order[s] = spatial (row-major) index of the token visited at scan step s.
+
+    row:     s -> s                         (left-to-right, rows top to bottom)
+    col:     s = j*H + i -> i*W + j         (top-to-bottom, columns left to right)
+    row_rev: s -> L-1-s                     (right-to-left = reversed row scan)
+    col_rev: s -> col(L-1-s)                (bottom-to-top = reversed column scan)
+    """
+    L = H * W
+    s = np.arange(L, dtype=np.int64)
+    if scan == "row":
+        return s
+    if scan == "col":
+        j, i = np.divmod(s, H)
+        return i * W + j
+    if scan == "row_rev":
+        return (L - 1) - s
+    if scan == "col_rev":
+        return scan_order(H, W, "col")[::-1].copy()
+    raise ValueError(f"unknown scan {scan!r}")
+
+
+def permute(x: np.ndarray, H: int, W: int, scan: str, inverse: bool = False) -> np.ndarray:
+    """Reorder the token axis (axis -2) of ``x`` [..., L, E].
+
+    forward: out[..., s, :] = x[..., order[s], :]   (spatial -> scan order)
+    inverse: out[..., order[s], :] = x[..., s, :]   (scan order -> spatial)
+    """
+    order = scan_order(H, W, scan)
+    if not inverse:
+        return x[..., order, :].copy()
+    out = np.empty_like(x)
+    out[..., order, :] = x
+    return out
+
+
+def _f64(a) -> np.ndarray:
+    if a is None:
+        return None
+    if hasattr(a, "detach"):  # torch tensor: take the exact values it holds
+        a = a.detach().to("cpu").double().numpy()
+    return np.ascontiguousarray(a, dtype=np.float64)
+
+
+def gla(q, k, v, g, s0=None, *, scale: float, H: int, W: int, scan: str = "row",
+        threads: Optional[int] = None, want_final: bool = True):
+    """Float64 recurrence over [B, heads, L, d] inputs in spatial order.
+
+    Returns ``(o [B, heads, L, d_v], s_final [B, heads, d_k, d_v] or None)`` as
+    float64 numpy arrays, ``o`` in spatial order.
+    """
+    q, k, v, g, s0 = (_f64(x) for x in (q, k, v, g, s0))
+    B, Hh, L, dk = q.shape
+    dv = v.shape[-1]
+    if L != H * W:
+        raise ValueError("L must equal H*W")
+    if k.shape != q.shape or g.shape != q.shape or v.shape[:3] != q.shape[:3]:
+        raise ValueError("shape mismatch")
+    if s0 is not None and s0.shape != (B, Hh, dk, dv):
+        raise ValueError("s0 shape mismatch")
+    order = np.ascontiguousarray(scan_order(H, W, scan), dtype=np.int64)
+    o = np.empty((B, Hh, L, dv), dtype=np.float64)
+    sf = np.empty((B, Hh, dk, dv), dtype=np.float64) if want_final else None
+    if threads is None:
+        threads = max(1, len(os.sched_getaffinity(0)))
+    ptr = lambda a: None if a is None else a.ctypes.data_as(ctypes.c_void_p)
+    rc = _load().oracle_gla_forward(ptr(q), ptr(k), ptr(v), ptr(g), ptr(s0), ptr(o), ptr(sf),
+                                    B * Hh, L, dk, dv, float(scale), ptr(order), int(threads))
+    if rc != 0:
+        raise RuntimeError(f"oracle_gla_forward failed with {rc}")
+    return o, sf

@@ -1,0 +1,351 @@
+"""Pins for the CPU oracle: it is checked against things other than itself.
+
+* brute force: the quadratic masked form of the recurrence with *explicit
+  products* of the gates (not exponentials of sums), pure-Python loops, tiny
+  shapes - the unrolled form of the paper's Sec. 3.1 recurrence;
+* closed forms: all gates 1 (g = 0) is causal linear attention
+  ``tril(Q K^T) V``; gates ~ 0 (g = -60) leaves ``o_t = (q_t . k_t) v_t``; one
+  scalar gate shared by all dimensions is retention ``sum_j gamma^(t-j) ...``;
+* direction identities: the reversed scans are flip - run - flip, the
+  column scan is the row scan of the transposed grid;
+* state split: run the first L1 tokens, resume from the returned final state;
+* L = 1 and linearity in v and in S0;
+* a hand-written scan-order fixture (tests/golden/scan_order.txt).
+
+``test_pins_reject_planted_mistakes`` shows that each pin family has power: a
+Python copy of the recurrence with one planted mistake (wrong gate placement,
+wrong exponent sign, swapped q/k, dropped S0, dropped scale, the previous token's gate)
+fails at least one of the same checks the oracle passes.
+"""
+import math
+import os
+
+import numpy as np
+import pytest
+
+import oracle
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+TOL = 1e-11
+
+
+def rel_err(a, b):
+    a = np.asarray(a, dtype=np.float64)
+    b = np.asarray(b, dtype=np.float64)
+    return float(np.max(np.abs(a - b)) / (np.max(np.abs(b)) + 1e-300))
+
+
+def rand_inputs(rng, BH, L, dk, dv, gate_lo=-2.0, gate_hi=0.0, with_s0=True):
+    q = rng.standard_normal((1, BH, L, dk))
+    k = rng.standard_normal((1, BH, L, dk))
+    v = rng.standard_normal((1, BH, L, dv))
+    g = rng.uniform(gate_lo, gate_hi, size=(1, BH, L, dk))
+    s0 = rng.standard_normal((1, BH, dk, dv)) if with_s0 else None
+    return q, k, v, g, s0
+
+
+# ----------------------------------------------------------------------------
+# independent references
+# ----------------------------------------------------------------------------
+
+def brute_force(q, k, v, g, s0, scale):
+    """One sequence already in scan order: quadratic form, explicit gate products."""
+    L, dk = q.shape
+    dv = v.shape[1]
+    gam = [[math.exp(g[t][i]) for i in range(dk)] for t in range(L)]
+    o = [[0.0] * dv for _ in range(L)]
+    for t in range(L):
+        for j in range(t + 1):
+            for i in range(dk):
+                w = 1.0
+                for u in range(j + 1, t + 1):
+                    w *= gam[u][i]
+                c = q[t][i] * w * k[j][i]
+                for m in range(dv):
+                    o[t][m] += c * v[j][m]
+        if s0 is not None:
+            for i in range(dk):
+                w = 1.0
+                for u in range(0, t + 1):
+                    w *= gam[u][i]
+                for m in range(dv):
+                    o[t][m] += q[t][i] * w * s0[i][m]
+        for m in range(dv):
+            o[t][m] *= scale
+    S = [[0.0] * dv for _ in range(dk)]
+    for j in range(L):
+        for i in range(dk):
+            w = 1.0
+            for u in range(j + 1, L):
+                w *= gam[u][i]
+            for m in range(dv):
+                S[i][m] += w * k[j][i] * v[j][m]
+    if s0 is not None:
+        for i in range(dk):
+            w = 1.0
+            for u in range(L):
+                w *= gam[u][i]
+            for m in range(dv):
+                S[i][m] += w * s0[i][m]
+    return np.array(o), np.array(S)
+
+
+def brute_force_grid(q, k, v, g, s0, scale, H, W, scan):
+    """Brute force on [1, BH, L, d] spatial-order inputs for a scan direction."""
+    order = oracle.scan_order(H, W, scan)
+    BH = q.shape[1]
+    o = np.zeros(v.shape)
+    S = np.zeros((1, BH, q.shape[-1], v.shape[-1]))
+    for b in range(BH):
+        ob, Sb = brute_force(q[0, b][order], k[0, b][order], v[0, b][order], g[0, b][order],
+                             None if s0 is None else s0[0, b], scale)
+        o[0, b][order] = ob
+        S[0, b] = Sb
+    return o, S
+
+
+# ----------------------------------------------------------------------------
+# pin checks, parameterised by the implementation under test
+# ----------------------------------------------------------------------------
+
+def pin_brute_force(fn, seed):
+    rng = np.random.default_rng(100 + seed)
+    cases = [(2, 3, 2, "row"), (3, 2, 3, "col"), (2, 3, 3, "row_rev"), (3, 3, 2, "col_rev"),
+             (1, 5, 4, "row")]
+    for (H, W, dk, scan) in cases:
+        dv = dk + 1
+        q, k, v, g, s0 = rand_inputs(rng, 2, H * W, dk, dv, -1.5, 0.0)
+        scale = 0.7
+        o, S = fn(q, k, v, g, s0, scale=scale, H=H, W=W, scan=scan)
+        ob, Sb = brute_force_grid(q, k, v, g, s0, scale, H, W, scan)
+        if rel_err(o, ob) > TOL or rel_err(S, Sb) > TOL:
+            return False
+    return True
+
+
+def pin_linear_attention(fn):
+    rng = np.random.default_rng(7)
+    H, W, dk, dv = 4, 5, 6, 3
+    q, k, v, _, _ = rand_inputs(rng, 2, H * W, dk, dv, with_s0=False)
+    g = np.zeros_like(q)
+    o, S = fn(q, k, v, g, None, scale=1.0, H=H, W=W, scan="row")
+    for b in range(2):
+        ref = np.tril(q[0, b] @ k[0, b].T) @ v[0, b]
+        if rel_err(o[0, b], ref) > TOL:
+            return False
+        if rel_err(S[0, b], k[0, b].T @ v[0, b]) > TOL:
+            return False
+    return True
+
+
+def pin_forgetting(fn):
+    rng = np.random.default_rng(8)
+    H, W, dk, dv = 3, 4, 5, 4
+    q, k, v, _, s0 = rand_inputs(rng, 2, H * W, dk, dv)
+    g = np.full_like(q, -60.0)
+    o, S = fn(q, k, v, g, s0, scale=0.5, H=H, W=W, scan="row")
+    for b in range(2):
+        ref = 0.5 * np.sum(q[0, b] * k[0, b], axis=1, keepdims=True) * v[0, b]
+        if rel_err(o[0, b], ref) > 1e-9:
+            return False
+        if rel_err(S[0, b], np.outer(k[0, b, -1], v[0, b, -1])) > 1e-9:
+            return False
+    return True
+
+
+def pin_retention(fn):
+    rng = np.random.default_rng(9)
+    H, W, dk, dv = 3, 5, 4, 5
+    q, k, v, _, _ = rand_inputs(rng, 1, H * W, dk, dv, with_s0=False)
+    gamma = 0.83
+    g = np.full_like(q, math.log(gamma))
+    o, _ = fn(q, k, v, g, None, scale=1.0, H=H, W=W, scan="row")
+    L = H * W
+    t = np.arange(L)[:, None]
+    j = np.arange(L)[None, :]
+    decay = np.where(t >= j, np.power(gamma, np.maximum(t - j, 0)), 0.0)
+    ref = ((q[0, 0] @ k[0, 0].T) * decay) @ v[0, 0]
+    return rel_err(o[0, 0], ref) <= TOL
+
+
+def pin_directions(fn):
+    rng = np.random.default_rng(10)
+    H, W, dk, dv = 3, 5, 4, 3
+    q, k, v, g, s0 = rand_inputs(rng, 2, H * W, dk, dv, -1.0, 0.0)
+    sc = 0.9
+    run = lambda xs, scan, HH, WW: fn(*xs, s0, scale=sc, H=HH, W=WW, scan=scan)
+    flip = lambda x: x[:, :, ::-1, :].copy()
+    o_row, S_row = run((q, k, v, g), "row", H, W)
+    o_rr, S_rr = run((q, k, v, g), "row_rev", H, W)
+    o_fl, S_fl = run((flip(q), flip(k), flip(v), flip(g)), "row", H, W)
+    if rel_err(o_rr, flip(o_fl)) > TOL or rel_err(S_rr, S_fl) > TOL:
+        return False
+
+    def tgrid(x, HH, WW):  # spatial [.., H*W, E] -> transposed grid [.., W*H, E]
+        sh = x.shape
+        return x.reshape(sh[0], sh[1], HH, WW, sh[-1]).transpose(0, 1, 3, 2, 4).reshape(sh)
+
+    o_col, S_col = run((q, k, v, g), "col", H, W)
+    o_t, S_t = run(tuple(tgrid(x, H, W) for x in (q, k, v, g)), "row", W, H)
+    if rel_err(o_col, tgrid(o_t, W, H)) > TOL or rel_err(S_col, S_t) > TOL:
+        return False
+    o_cr, S_cr = run((q, k, v, g), "col_rev", H, W)
+    o_tr, S_tr = run(tuple(tgrid(x, H, W) for x in (q, k, v, g)), "row_rev", W, H)
+    return rel_err(o_cr, tgrid(o_tr, W, H)) <= TOL and rel_err(S_cr, S_tr) <= TOL
+
+
+def pin_state_split(fn):
+    rng = np.random.default_rng(11)
+    L, dk, dv = 23, 5, 6
+    q, k, v, g, s0 = rand_inputs(rng, 2, L, dk, dv, -0.8, 0.0)
+    o, S = fn(q, k, v, g, s0, scale=0.3, H=1, W=L, scan="row")
+    for L1 in (1, 9, 22):
+        o1, S1 = fn(q[:, :, :L1], k[:, :, :L1], v[:, :, :L1], g[:, :, :L1], s0,
+                    scale=0.3, H=1, W=L1, scan="row")
+        L2 = L - L1
+        o2, S2 = fn(q[:, :, L1:], k[:, :, L1:], v[:, :, L1:], g[:, :, L1:], S1,
+                    scale=0.3, H=1, W=L2, scan="row")
+        if rel_err(np.concatenate([o1, o2], axis=2), o) > TOL or rel_err(S2, S) > TOL:
+            return False
+    return True
+
+
+def pin_single_token(fn):
+    rng = np.random.default_rng(12)
+    dk, dv = 4, 3
+    q, k, v, g, s0 = rand_inputs(rng, 3, 1, dk, dv)
+    o, S = fn(q, k, v, g, s0, scale=1.3, H=1, W=1, scan="col_rev")
+    for b in range(3):
+        Sb = np.exp(g[0, b, 0])[:, None] * s0[0, b] + np.outer(k[0, b, 0], v[0, b, 0])
+        if rel_err(S[0, b], Sb) > TOL or rel_err(o[0, b, 0], 1.3 * q[0, b, 0] @ Sb) > TOL:
+            return False
+    return True
+
+
+def pin_linearity(fn):
+    rng = np.random.default_rng(13)
+    H, W, dk, dv = 2, 6, 3, 4
+    q, k, v, g, s0 = rand_inputs(rng, 1, H * W, dk, dv)
+    _, _, v2, _, s02 = rand_inputs(rng, 1, H * W, dk, dv)
+    a, b = 0.37, -1.9
+    run = lambda vv, ss: fn(q, k, vv, g, ss, scale=1.0, H=H, W=W, scan="col")
+    o1, S1 = run(v, s0)
+    o2, S2 = run(v2, s02)
+    o3, S3 = run(a * v + b * v2, a * s0 + b * s02)
+    return rel_err(o3, a * o1 + b * o2) <= 1e-10 and rel_err(S3, a * S1 + b * S2) <= 1e-10
+
+
+ALL_PINS = {
+    "brute_force": lambda fn: all(pin_brute_force(fn, s) for s in range(2)),
+    "linear_attention": pin_linear_attention,
+    "forgetting": pin_forgetting,
+    "retention": pin_retention,
+    "directions": pin_directions,
+    "state_split": pin_state_split,
+    "single_token": pin_single_token,
+    "linearity": pin_linearity,
+}
+
+
+def oracle_fn(q, k, v, g, s0, *, scale, H, W, scan):
+    return oracle.gla(q, k, v, g, s0, scale=scale, H=H, W=W, scan=scan, threads=2)
+
+
+# ----------------------------------------------------------------------------
+# the oracle passes every pin
+# ----------------------------------------------------------------------------
+
+@pytest.mark.parametrize("name", sorted(ALL_PINS))
+def test_oracle_pin(name):
+    assert ALL_PINS[name](oracle_fn), name
+
+
+def test_scan_order_golden():
+    with open(os.path.join(GOLDEN, "scan_order.txt")) as f:
+        rows = [ln for ln in f if ln.strip() and not ln.startswith("#")]
+    assert len(rows) == 8
+    for ln in rows:
+        head, idx = ln.split(":")
+        H, W, scan = head.split()
+        want = np.array([int(x) for x in idx.split()])
+        np.testing.assert_array_equal(oracle.scan_order(int(H), int(W), scan), want)
+
+
+@pytest.mark.parametrize("H,W", [(1, 1), (1, 7), (7, 1), (7, 9), (40, 40), (16, 5)])
+def test_scan_order_properties(H, W):
+    L = H * W
+    row = oracle.scan_order(H, W, "row")
+    col = oracle.scan_order(H, W, "col")
+    np.testing.assert_array_equal(row, np.arange(L))
+    for scan in oracle.SCAN_IDS:
+        o = oracle.scan_order(H, W, scan)
+        np.testing.assert_array_equal(np.sort(o), np.arange(L))  # a bijection
+    # column-major order is the row-major order of the transposed grid
+    np.testing.assert_array_equal(col, np.arange(L).reshape(H, W).T.reshape(-1))
+    np.testing.assert_array_equal(oracle.scan_order(H, W, "row_rev"), row[::-1])
+    np.testing.assert_array_equal(oracle.scan_order(H, W, "col_rev"), col[::-1])
+
+
+@pytest.mark.parametrize("scan", sorted(oracle.SCAN_IDS))
+def test_permute_roundtrip(scan):
+    rng = np.random.default_rng(3)
+    x = rng.standard_normal((2, 3, 7 * 9, 5))
+    y = oracle.permute(x, 7, 9, scan)
+    np.testing.assert_array_equal(oracle.permute(y, 7, 9, scan, inverse=True), x)
+    order = oracle.scan_order(7, 9, scan)
+    for s in (0, 11, 62):
+        np.testing.assert_array_equal(y[:, :, s], x[:, :, order[s]])
+
+
+def test_oracle_threads_do_not_change_results():
+    rng = np.random.default_rng(5)
+    q, k, v, g, s0 = rand_inputs(rng, 7, 40, 8, 8, -0.5, 0.0)
+    o1, S1 = oracle.gla(q, k, v, g, s0, scale=0.2, H=5, W=8, scan="col", threads=1)
+    o4, S4 = oracle.gla(q, k, v, g, s0, scale=0.2, H=5, W=8, scan="col", threads=4)
+    np.testing.assert_array_equal(o1, o4)
+    np.testing.assert_array_equal(S1, S4)
+
+
+# ----------------------------------------------------------------------------
+# the pins have power: planted mistakes are caught
+# ----------------------------------------------------------------------------
+
+def py_recurrence(q, k, v, g, s0, *, scale, H, W, scan, mistake=None):
+    """A Python copy of the recurrence in which one mistake can be planted."""
+    order = oracle.scan_order(H, W, scan)
+    B, BH, L, dk = q.shape
+    dv = v.shape[-1]
+    o = np.zeros((B, BH, L, dv))
+    Sf = np.zeros((B, BH, dk, dv))
+    for b in range(BH):
+        S = np.zeros((dk, dv)) if (s0 is None or mistake == "drop_s0") else s0[0, b].copy()
+        for s in range(L):
+            t = order[s]
+            qt, kt, vt, gt = q[0, b, t], k[0, b, t], v[0, b, t], g[0, b, t]
+            if mistake == "swap_qk":
+                qt, kt = kt, qt
+            gam = np.exp(-gt) if mistake == "neg_exp" else np.exp(gt)
+            if mistake == "gate_after_add":
+                S = gam[:, None] * (S + np.outer(kt, vt))
+            elif mistake == "previous_gate":
+                gp = np.exp(g[0, b, order[s - 1]]) if s > 0 else np.ones(dk)
+                S = gp[:, None] * S + np.outer(kt, vt)
+            else:
+                S = gam[:, None] * S + np.outer(kt, vt)
+            o[0, b, t] = (1.0 if mistake == "drop_scale" else scale) * (qt @ S)
+        Sf[0, b] = S
+    return o, Sf
+
+
+@pytest.mark.parametrize("mistake", ["gate_after_add", "neg_exp", "swap_qk", "drop_s0",
+                                     "drop_scale", "previous_gate"])
+def test_pins_reject_planted_mistakes(mistake):
+    fn = lambda *a, **kw: py_recurrence(*a, mistake=mistake, **kw)
+    failed = [n for n, pin in ALL_PINS.items() if not pin(fn)]
+    assert failed, f"no pin caught the planted mistake {mistake!r}"
+
+
+def test_py_recurrence_without_mistake_passes_pins():
+    # guards the mutation test itself: the unmutated copy passes every pin
+    fn = lambda *a, **kw: py_recurrence(*a, **kw)
+    assert all(pin(fn) for pin in ALL_PINS.values())
