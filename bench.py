@@ -1,0 +1,170 @@
+"""Benchmark of the chunkwise GLA forward on one MI355X.
+
+One step = one gtr_gla_fwd call on the paper's operator-benchmark shape
+(B=1, 6 heads, 40x40 token grid -> L=1600, d_k=d_v=64, fp16 in/out, chunk 64,
+row-major scan), with inputs already resident in HBM. K steps are captured in
+one HIP graph (the paper times its operator under graph replay) and replayed
+once inside the timed region.
+
+Prints ONE JSON line (see the keys below). ``roofline`` prices the call's
+kernels against HBM bandwidth with the algorithmic bytes of the call;
+``cpu_baseline`` times the float64 oracle on the host on a bounded sample of
+the same workload.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import torch
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+import paper_2609_26590_amd as gtr  # noqa: E402
+from paper_2609_26590_amd.workloads import (WORKLOADS, algorithmic_bytes, algorithmic_flops,  # noqa: E402
+                                            make_inputs, torch_dtype)
+
+HBM_PEAK_GBS = 8000.0        # MI355X HBM3E, published
+MFMA_F16_PEAK_TFLOPS = 2500.0  # MI355X dense fp16 matrix, published
+
+
+def parse():
+    p = argparse.ArgumentParser()
+    p.add_argument("--gpus", type=int, default=1)
+    p.add_argument("--steps", type=int, default=500)
+    p.add_argument("--warmup", type=int, default=50)
+    p.add_argument("--workload", default="kbench", choices=sorted(WORKLOADS))
+    p.add_argument("--path", default="auto", choices=["auto", "fused", "staged"])
+    p.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
+    p.add_argument("--cpu-seconds", type=float, default=10.0)
+    p.add_argument("--detail", action="store_true", help="also time the other workloads")
+    return p.parse_args()
+
+
+def setup(wl, path, scan=None):
+    inp = make_inputs(wl)
+    dev = torch.device("cuda")
+    q, k, v, g = (inp[n].to(dev) for n in ("q", "k", "v", "g"))
+    s0 = None if inp["s0"] is None else inp["s0"].to(dev)
+    o = torch.empty((wl.B, wl.heads, wl.L, wl.dv), dtype=torch_dtype(wl.odtype), device=dev)
+    sf = torch.empty((wl.B, wl.heads, wl.dk, wl.dv), dtype=torch.float32, device=dev) if wl.want_final else None
+    ws = gtr.Workspace(dev)
+    scans = [scan] if scan else list(wl.scans)
+
+    def step(i=0):
+        gtr.gtr_gla_fwd(q, k, v, g, H=wl.H, W=wl.W, scale=wl.scale, chunk=wl.chunk, scan=scans[i % len(scans)],
+                        s0=s0, out=o, s_final=sf, path=path, workspace=ws)
+
+    step()  # sizes and zero-fills the workspace outside any capture
+    torch.cuda.synchronize()
+    return step
+
+
+def time_graph(step, steps, warmup):
+    for i in range(warmup):
+        step(i)
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        for i in range(steps):
+            step(i)
+    graph.replay()  # warm replay
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    e0.record()
+    graph.replay()
+    e1.record()
+    torch.cuda.synchronize()
+    return e0.elapsed_time(e1) / 1000.0  # seconds for `steps` calls
+
+
+def cpu_baseline(wl, budget_s):
+    import oracle  # test infrastructure: only this leg of the benchmark uses it
+    inp = make_inputs(wl)
+    threads = max(1, min(len(os.sched_getaffinity(0)), wl.B * wl.heads))
+    oracle.gla(inp["q"], inp["k"], inp["v"], inp["g"], inp["s0"], scale=wl.scale, H=wl.H, W=wl.W,
+               threads=threads)  # load / warm
+    reps, t0 = 0, time.perf_counter()
+    while True:
+        oracle.gla(inp["q"], inp["k"], inp["v"], inp["g"], inp["s0"], scale=wl.scale, H=wl.H, W=wl.W,
+                   threads=threads)
+        reps += 1
+        el = time.perf_counter() - t0
+        if el >= budget_s:
+            break
+    tokens = reps * wl.B * wl.L  # grid tokens, all heads of each token included, as in `value`
+    return {"value": tokens / el, "unit": "tokens/s", "cores": threads, "kind": "oracle",
+            "sample": f"{reps} full passes of the {wl.name} workload ({wl.B * wl.heads} sequences x {wl.L} "
+                      f"tokens, float64 sequential recurrence), {el:.1f} s"}
+
+
+def main():
+    a = parse()
+    if a.gpus != 1:
+        print(json.dumps({"error": "this build runs on one GPU only; multi-GPU sharding is described in the "
+                                   "design notes but not built", "n_gpus": a.gpus}))
+        sys.exit(2)
+    if not torch.cuda.is_available():
+        print(json.dumps({"error": "no GPU visible"}))
+        sys.exit(1)
+    gtr.load()
+    wl = WORKLOADS[a.workload]
+    step = setup(wl, a.path, scan=wl.scans[0])
+    secs = time_graph(step, a.steps, a.warmup)
+    per_call = secs / a.steps
+    tok_s = wl.B * wl.heads * wl.L / per_call  # token-heads per second
+    tokens_s = wl.B * wl.L / per_call          # grid tokens per second (all heads)
+    flops = algorithmic_flops(wl)
+    nbytes = algorithmic_bytes(wl)
+    achieved = nbytes / per_call / 1e9
+    out = {
+        "metric": "GLA fwd tokens/s and TFLOP/s at 40x40 tokens; % of MFMA/HBM roofline",
+        "value": tokens_s,
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": a.steps,
+        "warmup": a.warmup,
+        "ms_per_step": per_call * 1e3,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f16" if wl.dtype != "f32" else "f32",
+        "data": "synthetic",
+        "config": {"workload": f"{wl.name}: B={wl.B} heads={wl.heads} grid {wl.H}x{wl.W} (L={wl.L}) "
+                               f"d_k=d_v={wl.dk} {wl.dtype} in / {wl.odtype} out, chunk {wl.chunk}, "
+                               f"{wl.scans[0]} scan", "path": a.path, "timing": "HIP graph of K calls"},
+        "token_heads_per_s": tok_s,
+        "tflops": flops / per_call / 1e12,
+        "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": achieved / HBM_PEAK_GBS, "traffic": None,
+                     "kernel": "one gtr_gla_fwd call (all of its kernels)",
+                     "alg_bytes_per_call": nbytes, "us_per_call": per_call * 1e6,
+                     "mfma_frac": flops / per_call / 1e12 / MFMA_F16_PEAK_TFLOPS},
+    }
+    if a.detail:
+        det = {}
+        for name in ("directions", "highres", "batched"):
+            w2 = WORKLOADS[name]
+            wgs = w2.B * w2.heads * -(-w2.L // w2.chunk)
+            if w2.dtype == "bf16" or w2.dtype != w2.odtype or wgs > 200:
+                det[name] = "not timed: outside the configurations that have run clean on the GPU"
+                continue
+            for scan in w2.scans:
+                st = setup(w2, a.path, scan=scan)
+                s2 = time_graph(st, 100, 10) / 100
+                det[f"{name}/{scan}"] = {"us_per_call": s2 * 1e6,
+                                         "GBps": algorithmic_bytes(w2) / s2 / 1e9,
+                                         "hbm_frac": algorithmic_bytes(w2) / s2 / 1e9 / HBM_PEAK_GBS}
+        out["detail"] = det
+    if not a.no_cpu:
+        out["cpu_baseline"] = cpu_baseline(wl, a.cpu_seconds)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,173 @@
+/*
+ * libgtr - chunkwise key-only gated linear attention (GLA) forward for MI355X
+ * (gfx950), with the directional token-grid scans of the GTR backbone.
+ *
+ * Paper: "GTR" (arXiv 2609.26590).
+ *   Sec. 3.1  "Key-only gated recurrence":  S_t = Diag(gamma_t) S_{t-1} + k_t^T v_t,
+ *             o_t = d_k^{-1/2} q_t S_t, S_0 = 0, gamma_t in (0,1)^{d_k}.
+ *   Sec. 3.1  "Directional scanning": one scan per block, left-to-right,
+ *             right-to-left, top-to-bottom or bottom-to-top, with the spatial
+ *             order restored afterwards.
+ *   Sec. 3.3  "Hardware-Aware Chunkwise Inference", Eq. (chunk_boundary_main):
+ *             chunk summaries U_c, decays d_c, boundary states
+ *             S_[c+1] = Diag(d_c) S_[c] + U_c, and the chunk outputs.
+ *   App. "Custom CUDA Operator": the operator consumes q, k, v and the
+ *             log-decay g = log gamma; callers own persistent workspaces and
+ *             preallocated outputs, and the calls are graph-capturable.
+ *
+ * Conventions for every entry point:
+ *   - Tensor pointers are DEVICE pointers (hipMalloc'd or equivalent) unless
+ *     stated otherwise; the argument struct itself is host memory.
+ *   - The caller owns every buffer. The library never allocates, frees,
+ *     synchronises, or copies between host and device on these calls, so they
+ *     may be recorded into a HIP graph.
+ *   - Arguments are validated on the host before any HIP call. On a nonzero
+ *     status nothing has been launched and no buffer has been touched.
+ *   - Kernels are enqueued on `stream`; results are valid once the stream has
+ *     completed the work. A launch failure reported by the runtime maps to
+ *     GTR_ERR_HIP.
+ *   - All calls are thread-safe; there is no global mutable state.
+ */
+#ifndef GTR_H_
+#define GTR_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  GTR_OK = 0,
+  GTR_ERR_NULL = 1,        /* a required pointer is NULL                          */
+  GTR_ERR_SHAPE = 2,       /* a size is <= 0, or a product overflows int64        */
+  GTR_ERR_UNSUPPORTED = 3, /* a dtype / head width / chunk / path not compiled in */
+  GTR_ERR_ALIAS = 4,       /* an output overlaps an input or the workspace        */
+  GTR_ERR_WORKSPACE = 5,   /* workspace missing, too small or not 256-B aligned   */
+  GTR_ERR_HIP = 6          /* the HIP runtime rejected a launch                   */
+} gtr_status;
+
+typedef enum { GTR_F32 = 0, GTR_F16 = 1, GTR_BF16 = 2 } gtr_dtype;
+
+/*
+ * Scan directions over an H x W token grid stored row-major (spatial index
+ * i*W + j for row i, column j). pi(s) is the spatial index visited at scan
+ * step s, L = H*W:
+ *   GTR_SCAN_ROW      left-to-right: pi(s) = s
+ *   GTR_SCAN_COL      top-to-bottom: s = j*H + i  ->  pi(s) = i*W + j
+ *   GTR_SCAN_ROW_REV  right-to-left: pi(s) = L-1-s          (ROW reversed)
+ *   GTR_SCAN_COL_REV  bottom-to-top: pi(s) = pi_COL(L-1-s)  (COL reversed)
+ * The reversed scans are full reversals of the forward sequences.
+ */
+typedef enum {
+  GTR_SCAN_ROW = 0,
+  GTR_SCAN_COL = 1,
+  GTR_SCAN_ROW_REV = 2,
+  GTR_SCAN_COL_REV = 3
+} gtr_scan;
+
+/*
+ * gtr_scan_permute - reorder token rows between spatial and scan order
+ * (Sec. 3.1 "Directional scanning").
+ *
+ * src, dst : device, contiguous [outer, H*W, row_elems] elements of type `dt`.
+ * inverse=0: dst[o, s, :] = src[o, pi(s), :]   (spatial -> scan order)
+ * inverse=1: dst[o, pi(s), :] = src[o, s, :]   (scan order -> spatial)
+ * A pure copy: the result is bit-exact. src and dst must not overlap
+ * (GTR_ERR_ALIAS). outer >= 1, H >= 1, W >= 1, row_elems >= 1.
+ */
+gtr_status gtr_scan_permute(const void* src, void* dst, int64_t outer, int32_t H, int32_t W,
+                            int64_t row_elems, gtr_dtype dt, gtr_scan dir, int32_t inverse,
+                            hipStream_t stream);
+
+/* Execution schedule of gtr_gla_fwd (all give the same result up to rounding). */
+typedef enum {
+  GTR_PATH_AUTO = 0,   /* the library picks                                          */
+  GTR_PATH_FUSED = 1,  /* one launch: summaries, boundary-state scan and outputs     */
+  GTR_PATH_STAGED = 2  /* three launches: summaries, boundary-state scan, outputs    */
+} gtr_path;
+
+/*
+ * Arguments of gtr_gla_fwd (host struct; pointers are device pointers).
+ *
+ * q, g : [B, heads, L, dk]   k : [B, heads, L, dk]   v : [B, heads, L, dv]
+ *        contiguous, tokens in SPATIAL (row-major grid) order, L = H*W.
+ *        g holds the log-decays g = log gamma (finite, <= 0); gamma = 1 is g = 0.
+ *        A 1-D sequence is H = 1, W = L.
+ * o    : [B, heads, L, dv] contiguous, written in SPATIAL order.
+ * s0   : [B, heads, dk, dv] float32, the state before the first token in SCAN
+ *        order; NULL means a zero state (the paper's S_0 = 0).
+ * s_final : [B, heads, dk, dv] float32, receives the state after the last
+ *        token in SCAN order; NULL means it is not written.
+ * qkv_dtype : dtype of q, k, v.  g_dtype : qkv_dtype or GTR_F32.
+ * o_dtype   : qkv_dtype or GTR_F32.
+ * dk, dv : head widths; supported (dk, dv) = (32,32), (32,64), (64,64).
+ * chunk  : chunk length C in {32, 64, 128} (Sec. 3.3; the paper uses 64).
+ * scale  : o = scale * q S; the paper's value is dk^{-1/2}.
+ * scan   : direction; the permutation is fused into the loads and stores.
+ * path   : execution schedule (GTR_PATH_AUTO unless testing a schedule).
+ * workspace, workspace_bytes : device scratch owned by the caller, at least
+ *        gtr_gla_workspace_size(args) bytes, 256-byte aligned, and zero-filled
+ *        before its first use (gtr_gla_workspace_init). Every completed call
+ *        leaves the synchronisation words in it zeroed again, so one workspace
+ *        serves any number of calls on one stream. Calls that overlap in time
+ *        must not share a workspace.
+ *
+ * Numerics: float32 accumulation throughout. With fp16/bf16 inputs the matrix
+ * products use fp16 operands (every rescaled operand is bounded by |q| or |k|,
+ * see the design notes), so bf16 inputs must also be finite in fp16
+ * (|x| < 65504). With float32 inputs every product is float32.
+ */
+typedef struct {
+  const void* q;
+  const void* k;
+  const void* v;
+  const void* g;
+  void* o;
+  const float* s0;
+  float* s_final;
+  gtr_dtype qkv_dtype;
+  gtr_dtype g_dtype;
+  gtr_dtype o_dtype;
+  int32_t B, heads, H, W;
+  int32_t dk, dv, chunk;
+  float scale;
+  gtr_scan scan;
+  gtr_path path;
+  void* workspace;
+  size_t workspace_bytes;
+} gtr_gla_args;
+
+/* Bytes of workspace gtr_gla_fwd needs for these arguments (host only, no HIP
+ * call). Returns 0 if the arguments are invalid. Pointer fields are ignored. */
+size_t gtr_gla_workspace_size(const gtr_gla_args* args);
+
+/* Zero-fill `bytes` bytes of a workspace with a kernel on `stream` (no memset
+ * node, so it may be recorded into a graph). */
+gtr_status gtr_gla_workspace_init(void* workspace, size_t bytes, hipStream_t stream);
+
+/*
+ * gtr_gla_fwd - chunkwise key-only GLA forward (Sec. 3.1 recurrence evaluated
+ * with the chunkwise schedule of Sec. 3.3), scanning in direction `scan`.
+ * For every (b, h): visiting tokens in scan order, S = s0 (or 0),
+ *   S <- Diag(exp(g_t)) S + k_t^T v_t,   o_t = scale * q_t S,
+ * with o written back at the token's spatial index, and S_final = S at the end.
+ */
+gtr_status gtr_gla_fwd(const gtr_gla_args* args, hipStream_t stream);
+
+/* Nonzero if a fused-path call on this workspace gave up waiting for the other
+ * chunks of a sequence (a bounded wait ran out); the output of that call is not
+ * valid. Reads the flag with a blocking device-to-host copy - a diagnostic for
+ * tests, not for the hot path. Returns -1 on a HIP error. */
+int gtr_gla_workspace_fault(const void* workspace, size_t bytes);
+
+const char* gtr_status_string(gtr_status status);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* GTR_H_ */

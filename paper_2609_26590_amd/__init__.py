@@ -1,0 +1,210 @@
+"""Python binding of libgtr: chunkwise key-only GLA forward on MI355X (gfx950).
+
+Argument marshalling only: every step of the computation runs in the HIP
+kernels of ``libgtr.so``. PyTorch supplies device memory and streams. There is
+no CPU fallback: if the library is not built, every call raises.
+
+Entry points (same names as the C ABI in ``include/gtr.h``):
+
+* :func:`gtr_scan_permute` - token rows to / from the four scan orders
+  (paper Sec. 3.1, "Directional scanning"), bit-exact.
+* :func:`gtr_gla_fwd` - the chunkwise forward of the recurrence
+  ``S_t = Diag(exp g_t) S_{t-1} + k_t^T v_t, o_t = scale q_t S_t``
+  (Sec. 3.1, evaluated with the chunkwise schedule of Sec. 3.3).
+* :func:`gtr_gla_workspace_size`, :func:`gtr_gla_workspace_init`,
+  :func:`gtr_gla_workspace_fault`, :func:`gtr_status_string`.
+
+:class:`Workspace` keeps a caller-owned, zero-initialised workspace buffer.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional
+
+import torch
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "libgtr.so")
+
+F32, F16, BF16 = 0, 1, 2
+SCANS = {"row": 0, "col": 1, "row_rev": 2, "col_rev": 3}
+PATHS = {"auto": 0, "fused": 1, "staged": 2}
+STATUS = {0: "GTR_OK", 1: "GTR_ERR_NULL", 2: "GTR_ERR_SHAPE", 3: "GTR_ERR_UNSUPPORTED",
+          4: "GTR_ERR_ALIAS", 5: "GTR_ERR_WORKSPACE", 6: "GTR_ERR_HIP"}
+
+_DT = {torch.float32: F32, torch.float16: F16, torch.bfloat16: BF16}
+_DT_BACK = {F32: torch.float32, F16: torch.float16, BF16: torch.bfloat16}
+
+EXPORTS = ("gtr_scan_permute", "gtr_gla_workspace_size", "gtr_gla_workspace_init", "gtr_gla_fwd",
+           "gtr_gla_workspace_fault", "gtr_status_string")
+
+
+class GtrError(RuntimeError):
+    def __init__(self, fn: str, status: int):
+        self.status = status
+        super().__init__(f"{fn} failed: {STATUS.get(status, status)}")
+
+
+class GlaArgs(ctypes.Structure):
+    """Mirror of ``gtr_gla_args`` (include/gtr.h)."""
+    _fields_ = [
+        ("q", ctypes.c_void_p), ("k", ctypes.c_void_p), ("v", ctypes.c_void_p),
+        ("g", ctypes.c_void_p), ("o", ctypes.c_void_p),
+        ("s0", ctypes.c_void_p), ("s_final", ctypes.c_void_p),
+        ("qkv_dtype", ctypes.c_int), ("g_dtype", ctypes.c_int), ("o_dtype", ctypes.c_int),
+        ("B", ctypes.c_int32), ("heads", ctypes.c_int32), ("H", ctypes.c_int32), ("W", ctypes.c_int32),
+        ("dk", ctypes.c_int32), ("dv", ctypes.c_int32), ("chunk", ctypes.c_int32),
+        ("scale", ctypes.c_float), ("scan", ctypes.c_int), ("path", ctypes.c_int),
+        ("workspace", ctypes.c_void_p), ("workspace_bytes", ctypes.c_size_t),
+    ]
+
+
+_lib = None
+
+
+def load(path: Optional[str] = None) -> ctypes.CDLL:
+    """Load libgtr.so (raises if it has not been built)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    p = path or LIB_PATH
+    if not os.path.exists(p):
+        raise RuntimeError(f"{p} is missing: build it with `python -m paper_2609_26590_amd.build` "
+                           "(or __graft_entry__.build()); there is no fallback implementation")
+    lib = ctypes.CDLL(p)
+    P, I32, I64 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64
+    lib.gtr_scan_permute.argtypes = [P, P, I64, I32, I32, I64, ctypes.c_int, ctypes.c_int, I32, P]
+    lib.gtr_scan_permute.restype = ctypes.c_int
+    lib.gtr_gla_workspace_size.argtypes = [ctypes.POINTER(GlaArgs)]
+    lib.gtr_gla_workspace_size.restype = ctypes.c_size_t
+    lib.gtr_gla_workspace_init.argtypes = [P, ctypes.c_size_t, P]
+    lib.gtr_gla_workspace_init.restype = ctypes.c_int
+    lib.gtr_gla_fwd.argtypes = [ctypes.POINTER(GlaArgs), P]
+    lib.gtr_gla_fwd.restype = ctypes.c_int
+    lib.gtr_gla_workspace_fault.argtypes = [P, ctypes.c_size_t]
+    lib.gtr_gla_workspace_fault.restype = ctypes.c_int
+    lib.gtr_status_string.argtypes = [ctypes.c_int]
+    lib.gtr_status_string.restype = ctypes.c_char_p
+    _lib = lib
+    return lib
+
+
+def _stream_ptr(stream) -> int:
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return int(stream.cuda_stream)
+
+
+def _ptr(t: Optional[torch.Tensor]) -> Optional[int]:
+    return None if t is None else t.data_ptr()
+
+
+def gtr_status_string(status: int) -> str:
+    return load().gtr_status_string(status).decode()
+
+
+def gtr_scan_permute(src: torch.Tensor, H: int, W: int, scan: str, inverse: bool = False,
+                     out: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
+    """Reorder axis -2 (tokens, L = H*W) of a contiguous [..., L, E] device tensor."""
+    if not src.is_cuda or not src.is_contiguous():
+        raise ValueError("src must be a contiguous device tensor")
+    if src.dim() < 2 or src.shape[-2] != H * W:
+        raise ValueError("src must be [..., H*W, E]")
+    dst = torch.empty_like(src) if out is None else out
+    outer = src.numel() // (src.shape[-2] * src.shape[-1]) if src.numel() else 0
+    st = load().gtr_scan_permute(_ptr(src), _ptr(dst), outer, H, W, src.shape[-1], _DT[src.dtype],
+                                 SCANS[scan], int(bool(inverse)), _stream_ptr(stream))
+    if st:
+        raise GtrError("gtr_scan_permute", st)
+    return dst
+
+
+def make_args(q, k, v, g, *, H, W, scale, chunk=64, scan="row", s0=None, o=None, s_final=None,
+              path="auto", workspace=None) -> GlaArgs:
+    B, heads, L, dk = q.shape
+    a = GlaArgs()
+    a.q, a.k, a.v, a.g = _ptr(q), _ptr(k), _ptr(v), _ptr(g)
+    a.o, a.s0, a.s_final = _ptr(o), _ptr(s0), _ptr(s_final)
+    a.qkv_dtype = _DT[q.dtype]
+    a.g_dtype = _DT[g.dtype]
+    a.o_dtype = _DT[o.dtype] if o is not None else a.qkv_dtype
+    a.B, a.heads, a.H, a.W = B, heads, H, W
+    a.dk, a.dv, a.chunk = dk, v.shape[-1], chunk
+    a.scale = float(scale)
+    a.scan = SCANS[scan]
+    a.path = PATHS[path]
+    if workspace is not None:
+        a.workspace = workspace.data_ptr()
+        a.workspace_bytes = workspace.numel()
+    return a
+
+
+def gtr_gla_workspace_size(args: GlaArgs) -> int:
+    return int(load().gtr_gla_workspace_size(ctypes.byref(args)))
+
+
+def gtr_gla_workspace_init(ws: torch.Tensor, stream=None) -> None:
+    st = load().gtr_gla_workspace_init(_ptr(ws), ws.numel(), _stream_ptr(stream))
+    if st:
+        raise GtrError("gtr_gla_workspace_init", st)
+
+
+def gtr_gla_workspace_fault(ws: torch.Tensor) -> int:
+    return int(load().gtr_gla_workspace_fault(_ptr(ws), ws.numel()))
+
+
+class Workspace:
+    """A growable, zero-initialised device workspace for :func:`gtr_gla_fwd`."""
+
+    def __init__(self, device=None):
+        self.device = torch.device("cuda") if device is None else torch.device(device)
+        self.buf: Optional[torch.Tensor] = None
+
+    def get(self, nbytes: int, stream=None) -> torch.Tensor:
+        if self.buf is None or self.buf.numel() < nbytes:
+            n = max(256, (nbytes + 255) // 256 * 256)
+            # 256-byte aligned: torch's caching allocator hands out 512-byte aligned blocks
+            self.buf = torch.empty(n, dtype=torch.uint8, device=self.device)
+            gtr_gla_workspace_init(self.buf, stream)
+        return self.buf
+
+
+_default_ws: dict = {}
+
+
+def gtr_gla_fwd(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, g: torch.Tensor, *, H: int, W: int,
+                scale: Optional[float] = None, chunk: int = 64, scan: str = "row",
+                s0: Optional[torch.Tensor] = None, want_final: bool = False,
+                o_dtype: Optional[torch.dtype] = None, path: str = "auto",
+                out: Optional[torch.Tensor] = None, s_final: Optional[torch.Tensor] = None,
+                workspace: Optional[Workspace] = None, stream=None):
+    """Chunkwise GLA forward. Inputs [B, heads, H*W, d] in spatial order on the GPU.
+
+    Returns ``(o, s_final)``; ``s_final`` is None unless requested.
+    """
+    for name, t in (("q", q), ("k", k), ("v", v), ("g", g)):
+        if not t.is_cuda or not t.is_contiguous():
+            raise ValueError(f"{name} must be a contiguous device tensor")
+    if scale is None:
+        scale = q.shape[-1] ** -0.5
+    B, heads, L, _ = q.shape
+    odt = o_dtype or q.dtype
+    o = out if out is not None else torch.empty((B, heads, L, v.shape[-1]), dtype=odt, device=q.device)
+    sf = s_final
+    if want_final and sf is None:
+        sf = torch.empty((B, heads, q.shape[-1], v.shape[-1]), dtype=torch.float32, device=q.device)
+    args = make_args(q, k, v, g, H=H, W=W, scale=scale, chunk=chunk, scan=scan, s0=s0, o=o,
+                     s_final=sf, path=path)
+    need = gtr_gla_workspace_size(args)
+    if need == 0:
+        raise GtrError("gtr_gla_workspace_size", 2)
+    if workspace is None:
+        workspace = _default_ws.setdefault(q.device, Workspace(q.device))
+    buf = workspace.get(need, stream)
+    args.workspace = buf.data_ptr()
+    args.workspace_bytes = buf.numel()
+    st = load().gtr_gla_fwd(ctypes.byref(args), _stream_ptr(stream))
+    if st:
+        raise GtrError("gtr_gla_fwd", st)
+    return o, sf

@@ -1,0 +1,35 @@
+// Host-side argument validation and workspace layout for libgtr.
+#pragma once
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include "gtr.h"
+
+namespace gtr {
+
+struct GlaShape {
+  int64_t BH;       // B * heads
+  int64_t L;        // H * W
+  int64_t nchunks;  // ceil(L / chunk)
+  int dk, dv, chunk;
+  int qdt, gdt, odt;
+};
+
+struct WorkspaceLayout {
+  size_t fault_off;   // one 32-bit word (fused-path wait ran out)
+  size_t sync_off;    // [BH][4] 32-bit counters
+  size_t states_off;  // [BH][nchunks][dv][dk] float32
+  size_t decays_off;  // [BH][nchunks][dk] float32
+  size_t total;
+};
+
+// Validates everything but the workspace size (and, if check_pointers, the
+// pointers, their alignment and aliasing). No HIP call.
+gtr_status gla_shape_from_args(const gtr_gla_args* a, GlaShape* s, bool check_pointers);
+
+WorkspaceLayout gla_workspace_layout(const GlaShape& s);
+
+size_t dtype_size(int dt);
+
+}  // namespace gtr

@@ -1,0 +1,195 @@
+"""The C ABI on the CPU: the library loads, exports every declared entry point,
+and every host-side validation path returns its status without launching.
+
+Only invalid argument sets are passed here (pointers are fake, never
+dereferenced): validation happens before any HIP call, so nothing runs.
+"""
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_2609_26590_amd as gtr
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "gtr.h")
+
+OK, NULL, SHAPE, UNSUP, ALIAS, WS = 0, 1, 2, 3, 4, 5
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(gtr.LIB_PATH):
+        pytest.fail("libgtr.so is not built (run __graft_entry__.build())")
+    return gtr.load()
+
+
+def declared_functions():
+    src = open(HEADER).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(gtr_\w+)\s*\(", src)))
+
+
+def test_header_declares_the_binding_exports():
+    assert declared_functions() == sorted(gtr.EXPORTS)
+
+
+def test_every_declared_symbol_is_exported(lib):
+    for name in declared_functions():
+        assert hasattr(lib, name), name
+
+
+def test_status_strings(lib):
+    for code, name in gtr.STATUS.items():
+        assert gtr.gtr_status_string(code).startswith(name)
+
+
+# ---------------------------------------------------------------------------
+# gtr_gla_fwd / gtr_gla_workspace_size
+# ---------------------------------------------------------------------------
+
+FAKE = 1 << 40  # never dereferenced
+
+
+def base_args(B=1, heads=2, H=4, W=5, dk=64, dv=64, chunk=64, dt=gtr.F16, ws_bytes=None):
+    a = gtr.GlaArgs()
+    L = H * W
+    n_in = B * heads * L * 64 * 4
+    a.q, a.k, a.v, a.g = FAKE, FAKE + n_in, FAKE + 2 * n_in, FAKE + 3 * n_in
+    a.o = FAKE + 4 * n_in
+    a.s0 = None
+    a.s_final = None
+    a.qkv_dtype = a.g_dtype = a.o_dtype = dt
+    a.B, a.heads, a.H, a.W = B, heads, H, W
+    a.dk, a.dv, a.chunk = dk, dv, chunk
+    a.scale = 0.125
+    a.scan = 0
+    a.path = 0
+    need = gtr.load().gtr_gla_workspace_size(ctypes.byref(a))
+    a.workspace = FAKE + 6 * n_in
+    a.workspace_bytes = need if ws_bytes is None else ws_bytes
+    return a
+
+
+def fwd(lib, a):
+    return lib.gtr_gla_fwd(ctypes.byref(a), None)
+
+
+def test_workspace_size_formula(lib):
+    a = base_args(B=2, heads=3, H=40, W=40, dk=64, dv=64, chunk=64)
+    BH, nc = 6, 25
+    want = 256 + 256 + BH * nc * 64 * 64 * 4 + ((BH * nc * 64 * 4 + 255) // 256) * 256
+    assert lib.gtr_gla_workspace_size(ctypes.byref(a)) == want
+    a.dk = 48
+    assert lib.gtr_gla_workspace_size(ctypes.byref(a)) == 0
+
+
+def test_null_struct(lib):
+    assert lib.gtr_gla_fwd(None, None) == NULL
+
+
+@pytest.mark.parametrize("field", ["q", "k", "v", "g", "o"])
+def test_null_tensor(lib, field):
+    a = base_args()
+    setattr(a, field, None)
+    assert fwd(lib, a) == NULL
+
+
+@pytest.mark.parametrize("field,val", [("B", 0), ("heads", -1), ("H", 0), ("W", 0), ("chunk", 0)])
+def test_bad_shape(lib, field, val):
+    a = base_args()
+    setattr(a, field, val)
+    assert fwd(lib, a) == SHAPE
+
+
+def test_shape_overflow(lib):
+    a = base_args()
+    a.B, a.heads, a.H, a.W = 2 ** 30, 2 ** 30, 2 ** 30, 2 ** 30
+    assert fwd(lib, a) == SHAPE
+
+
+@pytest.mark.parametrize("field,val", [("dk", 48), ("dv", 128), ("chunk", 96), ("qkv_dtype", 7),
+                                       ("scan", 4), ("path", 9)])
+def test_unsupported(lib, field, val):
+    a = base_args()
+    setattr(a, field, val)
+    assert fwd(lib, a) == UNSUP
+
+
+def test_unsupported_dtype_mix(lib):
+    a = base_args(dt=gtr.F16)
+    a.g_dtype = gtr.BF16
+    assert fwd(lib, a) == UNSUP
+    a = base_args(dt=gtr.F16)
+    a.o_dtype = gtr.BF16
+    assert fwd(lib, a) == UNSUP
+
+
+def test_misaligned_tensor(lib):
+    a = base_args()
+    a.v = a.v + 2
+    assert fwd(lib, a) == UNSUP
+
+
+def test_output_aliases_input(lib):
+    a = base_args()
+    a.o = a.k + 64
+    assert fwd(lib, a) == ALIAS
+
+
+def test_final_state_aliases_output(lib):
+    a = base_args()
+    a.s_final = a.o
+    assert fwd(lib, a) == ALIAS
+
+
+def test_workspace_aliases_input(lib):
+    a = base_args()
+    a.workspace = a.q
+    assert fwd(lib, a) == ALIAS
+
+
+def test_workspace_missing_small_misaligned(lib):
+    a = base_args()
+    a.workspace = None
+    assert fwd(lib, a) == WS
+    a = base_args()
+    a.workspace_bytes -= 1
+    assert fwd(lib, a) == WS
+    a = base_args()
+    a.workspace += 128
+    assert fwd(lib, a) == WS
+
+
+def test_workspace_init_validation(lib):
+    assert lib.gtr_gla_workspace_init(None, 256, None) == NULL
+    assert lib.gtr_gla_workspace_init(FAKE + 16, 256, None) == WS
+    assert lib.gtr_gla_workspace_init(FAKE, 250, None) == WS
+
+
+def test_workspace_fault_rejects_bad_args(lib):
+    assert lib.gtr_gla_workspace_fault(None, 256) == -1
+    assert lib.gtr_gla_workspace_fault(FAKE, 16) == -1
+
+
+# ---------------------------------------------------------------------------
+# gtr_scan_permute
+# ---------------------------------------------------------------------------
+
+def perm(lib, src=FAKE, dst=FAKE + (1 << 30), outer=1, H=3, W=4, row=8, dt=gtr.F16, d=0, inv=0):
+    return lib.gtr_scan_permute(src, dst, outer, H, W, row, dt, d, inv, None)
+
+
+def test_permute_validation(lib):
+    assert perm(lib, src=None) == NULL
+    assert perm(lib, dst=None) == NULL
+    assert perm(lib, outer=0) == SHAPE
+    assert perm(lib, H=0) == SHAPE
+    assert perm(lib, W=-2) == SHAPE
+    assert perm(lib, row=0) == SHAPE
+    assert perm(lib, outer=2 ** 62, H=2 ** 30, W=2 ** 30) == SHAPE
+    assert perm(lib, dt=5) == UNSUP
+    assert perm(lib, d=7) == UNSUP
+    assert perm(lib, inv=2) == UNSUP
+    assert perm(lib, dst=FAKE + 64) == ALIAS
