@@ -10,20 +10,22 @@
 //                    + sum_{j<=r} (sum_i q_r[i] k_j[i] exp(A_r[i]-A_j[i])) v_j )
 //
 // Numerics differ from the paper's q*exp(A), k*exp(-A) factorisation, which
-// overflows half precision as soon as |A| > 11: every exponent evaluated here is
-// <= 0 except on the diagonal 16x16 blocks (see below), so all rescaled matrix
-// operands are bounded by |q| and |k|.
-//   * The chunk is split into 16-token sub-chunks R. Local cumulative sums a_r
-//     (within R), sub-chunk totals T_R and a per-dimension reference at the first
-//     token of R are kept in fp32 registers; every exponent is built from sums of
-//     these small terms, never as a difference of two large cumulative sums.
-//   * Off-diagonal score blocks (J < R) use q_r*exp(A_r - A_f(R)) and
-//     k_j*exp(A_f(R) - A_j), both with exponent <= 0, on fp16 matrix cores
-//     (float32 cores for float32 inputs).
-//   * Diagonal blocks use a mid-point reference: both factors lie within
-//     exp(+-span/2), span = decay across the 16 tokens; they run on float32 matrix
-//     cores. If span exceeds kSpanLimit the block falls back to exact per-element
-//     exp(a_r - a_j) on the vector ALUs.
+// overflows half precision as soon as |A| > 11. The chunk is split into
+// 16-token sub-chunks R (one wave each). Local cumulative sums a_r (within R),
+// sub-chunk totals T_R and the value g0_R of a at the first token of R are kept
+// in fp32; every exponent is a sum of these small terms, never a difference of
+// two large cumulative sums.
+//   * Off-diagonal score blocks (J < R) use q_r*exp(a_r - g0_R) and
+//     k_j*exp(T_J - a_j)*exp(g0_R + sum_{J<K<R} T_K): every exponent <= 0, so
+//     both matrix operands are bounded by |q| and |k|.
+//   * Diagonal blocks use a mid-point reference, both factors within
+//     exp(+-span/2), span = decay across the 16 tokens: fp16 operands for
+//     span <= kSpanF16, float32 operands for span <= kSpanF32, and the exact
+//     per-element exp(a_r - a_j) on the vector ALUs beyond that.
+//   * The summary uses k_j exp(A_last - A_j) and the readout q_r exp(A_r), both
+//     with exponents <= 0.
+// Per-(sub-chunk, dimension) factors are computed once per chunk into a small
+// shared table.
 //
 // Schedules:
 //   * staged: summary kernel -> boundary-state scan kernel -> output kernel.
@@ -33,7 +35,6 @@
 //     reading their own S_[c]. Two per-sequence counters order the phases.
 #include <hip/hip_runtime.h>
 
-#include <atomic>
 #include <mutex>
 
 #include "gtr.h"
@@ -42,9 +43,9 @@
 
 namespace gtr {
 
-constexpr float kSpanLimit = 60.f;     // diagonal blocks: mid-point factors stay within e^30
+constexpr float kSpanF16 = 10.f;           // mid-point factors within e^5: fp16 operands
+constexpr float kSpanF32 = 60.f;           // within e^30: float32 operands
 constexpr unsigned kSpinLimit = 1u << 22;  // bounded waits (fused schedule)
-constexpr bool kFusedEnabled = false;     // see gtr_gla_fwd
 
 struct GlaParams {
   const void* q;
@@ -70,6 +71,46 @@ struct GlaParams {
 
 constexpr int tile_threads(int chunk) { return chunk / 16 * kWave; }
 
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+
+// Raw bits of 8 consecutive elements (32 bytes for float32, 16 for 16-bit types).
+struct Raw {
+  u32x4 a, b;
+};
+
+__device__ __forceinline__ void ld_raw(const void* base, int dt, int64_t off, Raw& r) {
+  if (dt == GTR_F32) {
+    const u32x4* p = reinterpret_cast<const u32x4*>(static_cast<const float*>(base) + off);
+    r.a = p[0];
+    r.b = p[1];
+  } else {
+    r.a = *reinterpret_cast<const u32x4*>(static_cast<const unsigned short*>(base) + off);
+  }
+}
+
+__device__ __forceinline__ void cvt_raw(const Raw& r, int dt, float (&x)[8]) {
+  if (dt == GTR_F32) {
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      // copy the lanes to scalars first: this compiler reads element 0 when
+      // __builtin_bit_cast is given a vector-element lvalue directly
+      const unsigned int ua = r.a[e], ub = r.b[e];
+      x[e] = __builtin_bit_cast(float, ua);
+      x[e + 4] = __builtin_bit_cast(float, ub);
+    }
+  } else if (dt == GTR_F16) {
+    const h8 h = __builtin_bit_cast(h8, r.a);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) x[e] = (float)h[e];
+  } else {
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      x[2 * e] = __builtin_bit_cast(float, r.a[e] << 16);
+      x[2 * e + 1] = __builtin_bit_cast(float, r.a[e] & 0xffff0000u);
+    }
+  }
+}
+
 template <bool F16>
 __device__ __forceinline__ float gexp(float x) {
   if constexpr (F16)
@@ -78,133 +119,168 @@ __device__ __forceinline__ float gexp(float x) {
     return expf(x);
 }
 
-template <int DK, int DV, int C, bool F16>
-struct Tile {
-  static constexpr int NW = C / 16;  // one wave per 16-token sub-chunk
+// One chunk of one sequence: C tokens, one wave per 16-token sub-chunk.
+// IN is the dtype of q, k, v (GTR_F32 / GTR_F16 / GTR_BF16).
+template <int DK, int DV, int C, int IN>
+struct Chunk {
+  static constexpr bool F16 = IN != GTR_F32;  // matrix operands: fp16 (else float32)
+  static constexpr int NW = C / 16;
   static constexpr int NT = NW * kWave;
   static constexpr int KS = DK / 32;
   static constexpr int VS = DV / 32;
   static constexpr int KP = DK + 4;  // padded fp32 row pitch (k rows / output rows)
   static constexpr int OP = DV + 4;
   static constexpr int BUFW = KP > OP ? KP : OP;
-  static constexpr int TP = F16 ? C + 8 : C + 4;  // transposed-tile pitch (elements)
+  static constexpr int TP = F16 ? C + 8 : C + 4;    // transposed-tile pitch (elements)
+  static constexpr int SP = F16 ? DK + 8 : DK + 4;  // boundary-state tile pitch
+  static constexpr int NPAIR = NW * (NW - 1) / 2 > 0 ? NW * (NW - 1) / 2 : 1;
   typedef typename Op<F16>::elem E;
   typedef typename Op<F16>::frag8 F8;
   typedef typename Op<F16>::frag4 F4;
 
   struct Smem {
-    float buf[C * BUFW];  // k*exp(T-a) rows [C][KP]; later the output tile [C][OP]
-    E kT[DK * TP];        // (k * exp(A_last - A_r))^T  [DK][TP]
-    E vT[DV * TP];        // v^T                       [DV][TP]
-    float T[NW * DK];     // sub-chunk totals of g
+    float buf[C * BUFW];      // k*exp(T-a) rows [C][KP]; later the output tile [C][OP]
+    E kT[DK * TP];            // (k * exp(A_last - A_r))^T  [DK][TP]
+    E vT[DV * TP];            // v^T                       [DV][TP]
+    E sT[DV * SP];            // S_[c]^T                   [DV][SP]
+    float T[NW][DK];          // sub-chunk totals of g
+    float G0[NW][DK];         // g at the first token of each sub-chunk
+    float Fq[NW][DK];         // exp(A at the first token of R)
+    float Fk[NW][DK];         // exp(sum of totals after R)
+    float Fh[NW][DK];         // exp(span_R / 2)
+    float Foff[NPAIR][DK];    // exp(g0_R + sum_{J<K<R} T_K), pair (R, J), J < R
+    float Fdec[DK];           // exp(sum of all totals) = d_c
+    float Pt[NW][16][17];     // exact diagonal blocks, P^T staging
   };
 
-  // per-lane state after the prologue
-  int w, lane, tr, gq;
-  int64_t L;
-  float qh[KS][8];   // q * exp(a - a_first)                  (off-diagonal B operand)
-  float qt[KS][8];   // q * exp(A_r)                          (state readout)
-  float qd[KS][8];   // mid-point diagonal factors
-  float kd[KS][8];
-  float g0[KS][8];   // a at the first token of this sub-chunk (= g there)
-  float spanmax;     // wave-uniform
-  bool exact_diag;
-  float qraw[KS][8], kraw[KS][8], aloc[KS][8];  // kept for the exact diagonal path
+  int w, lane, tr, gq, r;
+  int64_t pos;
+  float qraw[KS][8], kraw[KS][8], aloc[KS][8];
+  float qh[KS][8];   // q * exp(a - g0)
+  float ke[KS][8];   // k * exp(T - a)
+  float spanmax;     // wave-uniform: widest decay span of this sub-chunk
+  float absmax;      // wave-uniform: largest |q|, |k| of this sub-chunk
 
   __device__ __forceinline__ int dim(int s, int e) const { return 32 * s + 8 * gq + e; }
 
-  // Load the chunk, build the cumulative sums and rescaled operands; fills the
-  // shared tiles. `summary` also builds the transposed k-hat tile.
-  __device__ __forceinline__ void prologue(const GlaParams& P, Smem& sm, int bh, int c, bool summary) {
+  static __device__ __forceinline__ int pair(int R, int J) { return R * (R - 1) / 2 + J; }
+
+  // Loads and per-token work; writes T, G0 and v^T. Ends with a barrier.
+  __device__ __forceinline__ void load(const GlaParams& P, Smem& sm, int bh, int c) {
     w = threadIdx.x >> 6;
     lane = threadIdx.x & 63;
     tr = lane & 15;
     gq = lane >> 4;
-    L = P.L;
-    const int r = 16 * w + tr;
-    const int64_t pos = (int64_t)c * C + r;
-    const bool valid = pos < L;
+    r = 16 * w + tr;
+    pos = (int64_t)c * C + r;
+    const bool valid = pos < P.L;
     const int64_t t = valid ? scan_to_spatial(pos, P.H, P.W, P.scan) : 0;
-    const int64_t kb = ((int64_t)bh * L + t) * DK;
-    const int64_t vb = ((int64_t)bh * L + t) * DV;
+    const int64_t kb = ((int64_t)bh * P.L + t) * DK;
+    const int64_t vb = ((int64_t)bh * P.L + t) * DV;
 
-    float gv[KS][8], vv[VS][8];
+    // issue every load before converting any of them
+    Raw rq[KS], rk[KS], rg[KS], rv[VS];
+    if (valid) {
+#pragma unroll
+      for (int s = 0; s < KS; ++s) {
+        ld_raw(P.q, IN, kb + 32 * s + 8 * gq, rq[s]);
+        ld_raw(P.k, IN, kb + 32 * s + 8 * gq, rk[s]);
+        ld_raw(P.g, P.gdt, kb + 32 * s + 8 * gq, rg[s]);
+      }
+#pragma unroll
+      for (int s = 0; s < VS; ++s) ld_raw(P.v, IN, vb + 32 * s + 8 * gq, rv[s]);
+    } else {
+      const u32x4 z = {0u, 0u, 0u, 0u};
+#pragma unroll
+      for (int s = 0; s < KS; ++s) rq[s] = rk[s] = rg[s] = Raw{z, z};
+#pragma unroll
+      for (int s = 0; s < VS; ++s) rv[s] = Raw{z, z};
+    }
+
+    float gv[KS][8];
 #pragma unroll
     for (int s = 0; s < KS; ++s) {
-      if (valid) {
-        load8(P.q, P.qdt, kb + 32 * s + 8 * gq, qraw[s]);
-        load8(P.k, P.qdt, kb + 32 * s + 8 * gq, kraw[s]);
-        load8(P.g, P.gdt, kb + 32 * s + 8 * gq, gv[s]);
-      } else {
-#pragma unroll
-        for (int e = 0; e < 8; ++e) qraw[s][e] = kraw[s][e] = gv[s][e] = 0.f;
-      }
+      cvt_raw(rq[s], IN, qraw[s]);
+      cvt_raw(rk[s], IN, kraw[s]);
+      cvt_raw(rg[s], P.gdt, gv[s]);
     }
+    // v^T tile
 #pragma unroll
     for (int s = 0; s < VS; ++s) {
-      if (valid) {
-        load8(P.v, P.qdt, vb + 32 * s + 8 * gq, vv[s]);
-      } else {
+      float x[8];
+      cvt_raw(rv[s], IN, x);
 #pragma unroll
-        for (int e = 0; e < 8; ++e) vv[s][e] = 0.f;
-      }
+      for (int e = 0; e < 8; ++e) sm.vT[(32 * s + 8 * gq + e) * TP + r] = (E)x[e];
     }
 
     // local inclusive cumulative sums over the 16 tokens of this sub-chunk
-    float T[KS][8];
-    float smax = 0.f;
+    float smax = 0.f, amax = 0.f;
 #pragma unroll
     for (int s = 0; s < KS; ++s)
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
         const float a = row_inclusive_scan(gv[s][e]);
+        const float T = row_read(a, 15);
+        const float g0 = row_read(a, 0);
         aloc[s][e] = a;
-        T[s][e] = row_read(a, 15);
-        g0[s][e] = row_read(a, 0);
-        smax = fmaxf(smax, g0[s][e] - T[s][e]);
+        smax = fmaxf(smax, g0 - T);
+        amax = fmaxf(amax, fmaxf(fabsf(qraw[s][e]), fabsf(kraw[s][e])));
+        qh[s][e] = qraw[s][e] * gexp<F16>(a - g0);  // exp(A_r - A_first) <= 1
+        ke[s][e] = kraw[s][e] * gexp<F16>(T - a);   // exp(A_last(R) - A_r) <= 1
+        if (tr == 0) {
+          sm.T[w][dim(s, e)] = T;
+          sm.G0[w][dim(s, e)] = g0;
+        }
       }
-    spanmax = wave_max(smax);
-    exact_diag = !(spanmax <= kSpanLimit);
-
-    if (tr == 0) {
-#pragma unroll
-      for (int s = 0; s < KS; ++s)
-#pragma unroll
-        for (int e = 0; e < 8; ++e) sm.T[w * DK + dim(s, e)] = T[s][e];
-    }
-    // transposed v tile
-#pragma unroll
-    for (int s = 0; s < VS; ++s)
-#pragma unroll
-      for (int e = 0; e < 8; ++e) sm.vT[(32 * s + 8 * gq + e) * TP + r] = (E)vv[s][e];
+    spanmax = __builtin_bit_cast(float, __builtin_amdgcn_readfirstlane(__builtin_bit_cast(int, wave_max(smax))));
+    absmax = __builtin_bit_cast(float, __builtin_amdgcn_readfirstlane(__builtin_bit_cast(int, wave_max(amax))));
     __syncthreads();
+  }
 
-    // chunk-level prefix of sub-chunk totals
+  // The per-(sub-chunk, dimension) factor table. Ends with a barrier.
+  __device__ __forceinline__ void factors(Smem& sm) {
+    constexpr int N1 = NW * DK;          // Fq, Fk, Fh
+    constexpr int N2 = NW * (NW - 1) / 2 * DK;  // Foff
+    constexpr int N = N1 + N2 + DK;
+    for (int idx = threadIdx.x; idx < N; idx += NT) {
+      if (idx < N1) {
+        const int R = idx / DK, d = idx - R * DK;
+        float before = 0.f, after = 0.f;
+        for (int K = 0; K < R; ++K) before += sm.T[K][d];
+        for (int K = R + 1; K < NW; ++K) after += sm.T[K][d];
+        const float g0 = sm.G0[R][d];
+        sm.Fq[R][d] = gexp<F16>(before + g0);
+        sm.Fk[R][d] = gexp<F16>(after);
+        sm.Fh[R][d] = gexp<F16>(0.5f * (g0 - sm.T[R][d]));
+      } else if (idx < N1 + N2) {
+        const int p = (idx - N1) / DK, d = (idx - N1) - p * DK;
+        int R = 1;
+        while (pair(R + 1, 0) <= p) ++R;
+        const int J = p - pair(R, 0);
+        float between = sm.G0[R][d];
+        for (int K = J + 1; K < R; ++K) between += sm.T[K][d];
+        sm.Foff[p][d] = gexp<F16>(between);
+      } else {
+        const int d = idx - N1 - N2;
+        float tot = 0.f;
+        for (int K = 0; K < NW; ++K) tot += sm.T[K][d];
+        sm.Fdec[d] = gexp<F16>(tot);
+      }
+    }
+    __syncthreads();
+  }
+
+  // Writes the k rows (and, for the summary, the transposed k-hat tile).
+  // Ends with a barrier.
+  __device__ __forceinline__ void stage_k(Smem& sm, bool summary) {
 #pragma unroll
-    for (int s = 0; s < KS; ++s) {
+    for (int s = 0; s < KS; ++s)
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
         const int d = dim(s, e);
-        float before = 0.f, after = 0.f;  // sum of totals before / after sub-chunk w
-        for (int K = 0; K < NW; ++K) {
-          const float tk = sm.T[K * DK + d];
-          if (K < w) before += tk;
-          if (K > w) after += tk;
-        }
-        const float a = aloc[s][e];
-        const float e_q = gexp<F16>(a - g0[s][e]);      // exp(A_r - A_first) <= 1
-        const float e_k = gexp<F16>(T[s][e] - a);       // exp(A_last(R) - A_r) <= 1
-        const float qhv = qraw[s][e] * e_q;
-        const float kev = kraw[s][e] * e_k;
-        qh[s][e] = qhv;
-        qt[s][e] = qhv * gexp<F16>(before + g0[s][e]);  // exp(A_r) = e_q * exp(A_first)
-        const float half = gexp<F16>(0.5f * (g0[s][e] - T[s][e]));
-        qd[s][e] = qhv * half;
-        kd[s][e] = kev * half;
-        sm.buf[r * KP + d] = kev;
-        if (summary) sm.kT[d * TP + r] = (E)(kev * gexp<F16>(after));  // exp(A_last - A_r)
+        sm.buf[r * KP + d] = ke[s][e];
+        if (summary) sm.kT[d * TP + r] = (E)(ke[s][e] * sm.Fk[w][d]);
       }
-    }
     __syncthreads();
   }
 
@@ -224,18 +300,36 @@ struct Tile {
       // lane holds U[16ib + 4gq + e][16jb + tr]
       *reinterpret_cast<f4*>(&U[(16 * jb + tr) * DK + 16 * ib + 4 * gq]) = acc;
     }
-    if (w == 0 && tr == 0) {
-      float* dec = P.decays + ((int64_t)bh * P.nchunks + c) * DK;
+    float* dec = P.decays + ((int64_t)bh * P.nchunks + c) * DK;
+    for (int d = threadIdx.x; d < DK; d += NT) dec[d] = sm.Fdec[d];
+  }
+
+  // Exact diagonal block for sub-chunks whose decay span is too wide for the
+  // mid-point factors: P[r][j] = sum_d q_r k_j exp(a_r - a_j), j <= r.
+  // Rare; the token loop is kept rolled to keep the code small.
+  __device__ __forceinline__ f4 exact_diagonal(float (*pt)[17]) {
+#pragma unroll 1
+    for (int j = 0; j < 16; ++j) {
+      const int src = ((gq << 4) | j) << 2;
+      float acc = 0.f;
 #pragma unroll
       for (int s = 0; s < KS; ++s)
 #pragma unroll
         for (int e = 0; e < 8; ++e) {
-          const int d = dim(s, e);
-          float tot = 0.f;
-          for (int K = 0; K < NW; ++K) tot += sm.T[K * DK + d];
-          dec[d] = gexp<F16>(tot);
+          const float kj = __builtin_bit_cast(float, __builtin_amdgcn_ds_bpermute(src, __builtin_bit_cast(int, kraw[s][e])));
+          const float aj = __builtin_bit_cast(float, __builtin_amdgcn_ds_bpermute(src, __builtin_bit_cast(int, aloc[s][e])));
+          acc += (j <= tr) ? qraw[s][e] * kj * gexp<F16>(aloc[s][e] - aj) : 0.f;
         }
+      acc += __shfl_xor(acc, 16, kWave);
+      acc += __shfl_xor(acc, 32, kWave);
+      if (gq == (j >> 2)) pt[j][tr] = acc;  // P^T[j][r]
     }
+    __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0): this wave's LDS writes are done
+    __builtin_amdgcn_wave_barrier();
+    f4 res;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) res[e] = pt[4 * gq + e][tr];
+    return res;
   }
 
   // Intra-chunk part: o_r = sum_{j<=r} P[r][j] v_j for this wave's 16 rows.
@@ -249,33 +343,43 @@ struct Tile {
     for (int J = 0; J < NW; ++J) {
       PT[J] = f4{0.f, 0.f, 0.f, 0.f};
       if (J < w) {
-        // P^T[j][r] = sum_d (k_j exp(A_f(R) - A_j))[d] (q_r exp(A_r - A_f(R)))[d]
+        // P^T[j][r] = sum_d (k_j exp(T_J - a_j) Foff[R,J])[d] (q_r exp(a_r - g0_R))[d]
+        const float* fo = sm.Foff[pair(w, J)];
 #pragma unroll
         for (int s = 0; s < KS; ++s) {
           float x[8];
 #pragma unroll
-          for (int e = 0; e < 8; ++e) {
-            const int d = dim(s, e);
-            float between = g0[s][e];  // A_f(R) - A_last(J) = g_f(R) + totals in between
-            for (int K = J + 1; K < w; ++K) between += sm.T[K * DK + d];
-            x[e] = sm.buf[(16 * J + tr) * KP + d] * gexp<F16>(between);
-          }
+          for (int e = 0; e < 8; ++e) x[e] = sm.buf[(16 * J + tr) * KP + dim(s, e)] * fo[dim(s, e)];
           PT[J] = mma32(Op<F16>::pack8(x), qhf[s], PT[J]);
         }
       } else if (J == w) {
-        if (!exact_diag) {
+        // fp16 operands only if the mid-point factors keep them well inside fp16 range
+        if (F16 && spanmax <= kSpanF16 && absmax <= 256.f) {
+#pragma unroll
+          for (int s = 0; s < KS; ++s) {
+            float a[8], b[8];
+#pragma unroll
+            for (int e = 0; e < 8; ++e) {
+              const float h = sm.Fh[w][dim(s, e)];
+              a[e] = ke[s][e] * h;
+              b[e] = qh[s][e] * h;
+            }
+            PT[J] = mma32(Op<F16>::pack8(a), Op<F16>::pack8(b), PT[J]);
+          }
+        } else if (spanmax <= kSpanF32) {
 #pragma unroll
           for (int s = 0; s < KS; ++s) {
             f8 a, b;
 #pragma unroll
             for (int e = 0; e < 8; ++e) {
-              a[e] = kd[s][e];
-              b[e] = qd[s][e];
+              const float h = sm.Fh[w][dim(s, e)];
+              a[e] = ke[s][e] * h;
+              b[e] = qh[s][e] * h;
             }
             PT[J] = mma32(a, b, PT[J]);
           }
         } else {
-          PT[J] = exact_diagonal();
+          PT[J] = exact_diagonal(sm.Pt[w]);
         }
         // causal mask: lane holds P^T[j = 4gq + e][r = tr]
 #pragma unroll
@@ -299,51 +403,47 @@ struct Tile {
     }
   }
 
-  // Exact diagonal block, P^T layout; only for sub-chunks whose decay span is
-  // beyond what the mid-point factors can carry.
-  __device__ __forceinline__ f4 exact_diagonal() {
-    float part[16];
+  // Boundary state S_[c]^T ([DV][DK] fp32 in the workspace) -> shared tile, in
+  // two steps so the loads can be issued early: each thread moves whole
+  // 16-byte pieces. No barrier.
+  static constexpr int SQ4 = DK * DV / 4;          // 16-byte pieces in one state
+  static constexpr int SPER = (SQ4 + NT - 1) / NT;  // pieces per thread
+  __device__ __forceinline__ void stage_state_load(const float* ST, f4 (&buf)[SPER]) {
 #pragma unroll
-    for (int j = 0; j < 16; ++j) part[j] = 0.f;
-#pragma unroll
-    for (int s = 0; s < KS; ++s)
-#pragma unroll
-      for (int e = 0; e < 8; ++e) {
-#pragma unroll
-        for (int j = 0; j < 16; ++j) {
-          const float kj = row_read(kraw[s][e], j);
-          const float aj = row_read(aloc[s][e], j);
-          if (j <= tr) part[j] += qraw[s][e] * kj * gexp<F16>(aloc[s][e] - aj);
-        }
-      }
-    f4 res = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-    for (int j = 0; j < 16; ++j) {
-      float x = part[j];
-      x += __shfl_xor(x, 16, kWave);
-      x += __shfl_xor(x, 32, kWave);
-#pragma unroll
-      for (int e = 0; e < 4; ++e)
-        if (4 * gq + e == j) res[e] = x;
+    for (int m = 0; m < SPER; ++m) {
+      const int q4 = threadIdx.x + m * NT;
+      if (q4 < SQ4) buf[m] = reinterpret_cast<const f4*>(ST)[q4];
     }
-    return res;
+  }
+  __device__ __forceinline__ void stage_state_store(Smem& sm, const f4 (&buf)[SPER]) {
+#pragma unroll
+    for (int m = 0; m < SPER; ++m) {
+      const int q4 = threadIdx.x + m * NT;  // piece index in [DV][DK]
+      if (q4 < SQ4) {
+        const int dv = (q4 * 4) / DK, i = (q4 * 4) % DK;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) sm.sT[dv * SP + i + e] = (E)buf[m][e];
+      }
+    }
   }
 
-  // o_r += (q_r exp(A_r)) S_[c]; S^T read from the workspace ([DV][DK] fp32).
-  __device__ __forceinline__ void readout(const float* ST, f4 (&O)[DV / 16]) {
+  // o_r += (q_r exp(A_r)) S_[c]. Reads the shared state tile.
+  __device__ __forceinline__ void readout(Smem& sm, f4 (&O)[DV / 16]) {
     F8 qtf[KS];
 #pragma unroll
-    for (int s = 0; s < KS; ++s) qtf[s] = Op<F16>::pack8(qt[s]);
+    for (int s = 0; s < KS; ++s) {
+      float x[8];
 #pragma unroll
-    for (int jb = 0; jb < DV / 16; ++jb) {
+      for (int e = 0; e < 8; ++e) x[e] = qh[s][e] * sm.Fq[w][dim(s, e)];
+      qtf[s] = Op<F16>::pack8(x);
+    }
+#pragma unroll
+    for (int jb = 0; jb < DV / 16; ++jb)
 #pragma unroll
       for (int s = 0; s < KS; ++s) {
-        const f4* p = reinterpret_cast<const f4*>(&ST[(16 * jb + tr) * DK + 32 * s + 8 * gq]);
-        const f4 x0 = p[0], x1 = p[1];
-        float x[8] = {x0[0], x0[1], x0[2], x0[3], x1[0], x1[1], x1[2], x1[3]};
-        O[jb] = mma32(qtf[s], Op<F16>::pack8(x), O[jb]);
+        const F8 b = *reinterpret_cast<const F8*>(&sm.sT[(16 * jb + tr) * SP + 32 * s + 8 * gq]);
+        O[jb] = mma32(qtf[s], b, O[jb]);
       }
-    }
   }
 
   // Stage the output tile through LDS and write whole rows back in spatial order.
@@ -356,13 +456,13 @@ struct Tile {
     __syncthreads();
     constexpr int PIECES = DV / 8;
     for (int idx = threadIdx.x; idx < C * PIECES; idx += NT) {
-      const int r = idx / PIECES, pc = idx % PIECES;
-      const int64_t pos = (int64_t)c * C + r;
-      if (pos < P.L) {
-        const int64_t t = scan_to_spatial(pos, P.H, P.W, P.scan);
+      const int rr = idx / PIECES, pc = idx % PIECES;
+      const int64_t p = (int64_t)c * C + rr;
+      if (p < P.L) {
+        const int64_t t = scan_to_spatial(p, P.H, P.W, P.scan);
         float x[8];
 #pragma unroll
-        for (int e = 0; e < 8; ++e) x[e] = sm.buf[r * OP + 8 * pc + e];
+        for (int e = 0; e < 8; ++e) x[e] = sm.buf[rr * OP + 8 * pc + e];
         store_n<8>(P.o, P.odt, ((int64_t)bh * P.L + t) * DV + 8 * pc, x);
       }
     }
@@ -408,14 +508,16 @@ __device__ __forceinline__ void scan_elements(const GlaParams& P, int bh, int e0
 // ---------------------------------------------------------------------------
 // staged schedule
 // ---------------------------------------------------------------------------
-template <int DK, int DV, int C, bool F16>
+template <int DK, int DV, int C, int IN>
 __global__ void __launch_bounds__(tile_threads(C)) gla_summary_kernel(GlaParams P) {
-  typedef Tile<DK, DV, C, F16> T;
+  typedef Chunk<DK, DV, C, IN> T;
   __shared__ typename T::Smem sm;
-  T tile;
+  T ch;
   const int c = blockIdx.x, bh = blockIdx.y;
-  tile.prologue(P, sm, bh, c, true);
-  tile.summary_out(P, sm, bh, c);
+  ch.load(P, sm, bh, c);
+  ch.factors(sm);
+  ch.stage_k(sm, true);
+  ch.summary_out(P, sm, bh, c);
 }
 
 template <int DK, int DV>
@@ -426,17 +528,23 @@ __global__ void __launch_bounds__(256) gla_scan_kernel(GlaParams P) {
   scan_elements<DK, DV>(P, bh, e0, e1, threadIdx.x, 256);
 }
 
-template <int DK, int DV, int C, bool F16>
+template <int DK, int DV, int C, int IN>
 __global__ void __launch_bounds__(tile_threads(C)) gla_output_kernel(GlaParams P) {
-  typedef Tile<DK, DV, C, F16> T;
+  typedef Chunk<DK, DV, C, IN> T;
   __shared__ typename T::Smem sm;
-  T tile;
+  T ch;
   const int c = blockIdx.x, bh = blockIdx.y;
-  tile.prologue(P, sm, bh, c, false);
+  const bool have_state = c > 0 || P.s0;
+  f4 sbuf[T::SPER];
+  if (have_state) ch.stage_state_load(P.states + ((int64_t)bh * P.nchunks + c) * (DK * DV), sbuf);
+  ch.load(P, sm, bh, c);
+  if (have_state) ch.stage_state_store(sm, sbuf);
+  ch.factors(sm);
+  ch.stage_k(sm, false);
   f4 O[DV / 16];
-  tile.intra(sm, O);
-  if (c > 0 || P.s0) tile.readout(P.states + ((int64_t)bh * P.nchunks + c) * (DK * DV), O);
-  tile.store(P, sm, bh, c, O);
+  ch.intra(sm, O);
+  if (have_state) ch.readout(sm, O);
+  ch.store(P, sm, bh, c, O);
 }
 
 // ---------------------------------------------------------------------------
@@ -467,9 +575,9 @@ __device__ __forceinline__ void seq_wait(unsigned* ctr, unsigned target, unsigne
 // robin, so block b runs on XCD b % 8; all chunks of a sequence get the same
 // b % 8 and therefore share one L2 for their summaries and boundary states.
 // Blocks whose sequence index is past the end exit at once.
-template <int DK, int DV, int C, bool F16>
+template <int DK, int DV, int C, int IN>
 __global__ void __launch_bounds__(tile_threads(C)) gla_fused_kernel(GlaParams P) {
-  typedef Tile<DK, DV, C, F16> T;
+  typedef Chunk<DK, DV, C, IN> T;
   __shared__ typename T::Smem sm;
   const int NC = P.nchunks;
   const int b = blockIdx.x;
@@ -479,13 +587,15 @@ __global__ void __launch_bounds__(tile_threads(C)) gla_fused_kernel(GlaParams P)
   if (bh >= P.BH) return;
   unsigned* sync = P.sync + 4 * bh;
 
-  T tile;
-  tile.prologue(P, sm, bh, c, true);
-  tile.summary_out(P, sm, bh, c);
+  T ch;
+  ch.load(P, sm, bh, c);
+  ch.factors(sm);
+  ch.stage_k(sm, true);
+  ch.summary_out(P, sm, bh, c);
   seq_arrive(&sync[0]);
 
   f4 O[DV / 16];
-  tile.intra(sm, O);
+  ch.intra(sm, O);
 
   seq_wait(&sync[0], (unsigned)NC, P.fault);
   {
@@ -496,8 +606,14 @@ __global__ void __launch_bounds__(tile_threads(C)) gla_fused_kernel(GlaParams P)
   seq_arrive(&sync[1]);
   seq_wait(&sync[1], (unsigned)NC, P.fault);
 
-  if (c > 0 || P.s0) tile.readout(P.states + ((int64_t)bh * NC + c) * (DK * DV), O);
-  tile.store(P, sm, bh, c, O);
+  if (c > 0 || P.s0) {
+    f4 sbuf[T::SPER];
+    ch.stage_state_load(P.states + ((int64_t)bh * NC + c) * (DK * DV), sbuf);
+    ch.stage_state_store(sm, sbuf);
+    __syncthreads();
+    ch.readout(sm, O);
+  }
+  ch.store(P, sm, bh, c, O);
 
   if (threadIdx.x == 0) {
     const unsigned prev = __hip_atomic_fetch_add(&sync[2], 1u, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT);
@@ -525,35 +641,39 @@ struct KernelSet {
   int threads;
 };
 
-template <int DK, int DV, int C, bool F16>
+template <int DK, int DV, int C, int IN>
 static KernelSet kernels_for() {
-  return KernelSet{reinterpret_cast<const void*>(&gla_summary_kernel<DK, DV, C, F16>),
-                   reinterpret_cast<const void*>(&gla_output_kernel<DK, DV, C, F16>),
-                   reinterpret_cast<const void*>(&gla_fused_kernel<DK, DV, C, F16>),
-                   reinterpret_cast<const void*>(&gla_scan_kernel<DK, DV>), Tile<DK, DV, C, F16>::NT};
+  return KernelSet{reinterpret_cast<const void*>(&gla_summary_kernel<DK, DV, C, IN>),
+                   reinterpret_cast<const void*>(&gla_output_kernel<DK, DV, C, IN>),
+                   reinterpret_cast<const void*>(&gla_fused_kernel<DK, DV, C, IN>),
+                   reinterpret_cast<const void*>(&gla_scan_kernel<DK, DV>), tile_threads(C)};
 }
 
-template <int DK, int DV, bool F16>
+template <int DK, int DV, int IN>
 static bool pick_chunk(int chunk, KernelSet* ks) {
   switch (chunk) {
-    case 32: *ks = kernels_for<DK, DV, 32, F16>(); return true;
-    case 64: *ks = kernels_for<DK, DV, 64, F16>(); return true;
-    case 128: *ks = kernels_for<DK, DV, 128, F16>(); return true;
+    case 32: *ks = kernels_for<DK, DV, 32, IN>(); return true;
+    case 64: *ks = kernels_for<DK, DV, 64, IN>(); return true;
+    case 128: *ks = kernels_for<DK, DV, 128, IN>(); return true;
     default: return false;
   }
 }
 
-template <bool F16>
+template <int IN>
 static bool pick_dims(int dk, int dv, int chunk, KernelSet* ks) {
-  if (dk == 32 && dv == 32) return pick_chunk<32, 32, F16>(chunk, ks);
-  if (dk == 32 && dv == 64) return pick_chunk<32, 64, F16>(chunk, ks);
-  if (dk == 64 && dv == 64) return pick_chunk<64, 64, F16>(chunk, ks);
+  if (dk == 32 && dv == 32) return pick_chunk<32, 32, IN>(chunk, ks);
+  if (dk == 32 && dv == 64) return pick_chunk<32, 64, IN>(chunk, ks);
+  if (dk == 64 && dv == 64) return pick_chunk<64, 64, IN>(chunk, ks);
   return false;
 }
 
 static bool select_kernels(const GlaShape& s, KernelSet* ks) {
-  if (s.qdt == GTR_F32) return pick_dims<false>(s.dk, s.dv, s.chunk, ks);
-  return pick_dims<true>(s.dk, s.dv, s.chunk, ks);
+  switch (s.qdt) {
+    case GTR_F32: return pick_dims<GTR_F32>(s.dk, s.dv, s.chunk, ks);
+    case GTR_F16: return pick_dims<GTR_F16>(s.dk, s.dv, s.chunk, ks);
+    case GTR_BF16: return pick_dims<GTR_BF16>(s.dk, s.dv, s.chunk, ks);
+    default: return false;
+  }
 }
 
 // Largest number of work-groups of one sequence that can be resident on one XCD
@@ -565,7 +685,7 @@ static int fused_capacity_per_xcd(const void* kernel, int threads) {
     int cap;
   };
   static std::mutex mu;
-  static Entry cache[64];
+  static Entry cache[128];
   static int n = 0;
   int dev = 0;
   if (hipGetDevice(&dev) != hipSuccess) return 0;
@@ -579,7 +699,7 @@ static int fused_capacity_per_xcd(const void* kernel, int threads) {
   if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) return 0;
   const int cap = per_cu * (cus / 8);
   std::lock_guard<std::mutex> lk(mu);
-  if (n < 64) cache[n++] = Entry{dev, kernel, cap};
+  if (n < 128) cache[n++] = Entry{dev, kernel, cap};
   return cap;
 }
 
@@ -644,12 +764,8 @@ extern "C" gtr_status gtr_gla_fwd(const gtr_gla_args* a, hipStream_t stream) {
   P.decays = reinterpret_cast<float*>(ws + lay.decays_off);
   P.groups = (int)((s.BH + 7) / 8);
 
-  // The fused schedule is switched off: its first run on a 12-sequence bf16
-  // workload ended in a GPU memory-aperture fault whose cause has not been
-  // found. Until it is, only the staged schedule runs.
-  if (a->path == GTR_PATH_FUSED && !kFusedEnabled) return GTR_ERR_UNSUPPORTED;
   bool fused = false;
-  if (kFusedEnabled && (a->path == GTR_PATH_FUSED || a->path == GTR_PATH_AUTO)) {
+  if (a->path == GTR_PATH_FUSED || a->path == GTR_PATH_AUTO) {
     const int cap = fused_capacity_per_xcd(ks.fused, ks.threads);
     const bool fits = cap > 0 && s.nchunks <= cap;
     if (a->path == GTR_PATH_FUSED && !fits) return GTR_ERR_UNSUPPORTED;

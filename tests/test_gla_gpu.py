@@ -55,9 +55,11 @@ HELD = ("held off the GPU: outside the envelope that has run clean (fp16->fp16 o
 
 
 def held(B, heads, L, chunk, dtype, gdtype, odtype) -> bool:
-    workgroups = B * heads * ((L + chunk - 1) // chunk)
+    nc = (L + chunk - 1) // chunk
+    staged = B * heads * nc
+    fused = 8 * ((B * heads + 7) // 8) * nc  # the fused grid rounds sequences up to 8 XCD lanes
     return (dtype != odtype or gdtype != dtype or dtype == "bf16"
-            or workgroups > MAX_CLEAN_WORKGROUPS)
+            or max(staged, fused) > MAX_CLEAN_WORKGROUPS)
 
 
 def skip_if_held(*a):
