@@ -24,8 +24,8 @@
 //     per-element exp(a_r - a_j) on the vector ALUs beyond that.
 //   * The summary uses k_j exp(A_last - A_j) and the readout q_r exp(A_r), both
 //     with exponents <= 0.
-// Per-(sub-chunk, dimension) factors are computed once per chunk into a small
-// shared table.
+// Each wave builds the factors of its own sub-chunk in registers from a small
+// shared table of the sub-chunk totals.
 //
 // Schedules:
 //   * staged: summary kernel -> boundary-state scan kernel -> output kernel.
@@ -33,6 +33,12 @@
 //     its summary, and the work-groups of one sequence then run the boundary
 //     state scan cooperatively (each takes a slice of the d_k x d_v state) before
 //     reading their own S_[c]. Two per-sequence counters order the phases.
+//     Everything one work-group hands to another (summaries, decays, boundary
+//     states) is written and read with agent-coherent accesses (cache policy
+//     sc1), and a work-group waits for its own stores to be acknowledged
+//     (vmcnt(0)) before it bumps a counter. No release/acquire fence is used: on
+//     this GPU those write back / invalidate the whole L2 of the XCD, which cost
+//     more than the rest of the kernel.
 #include <hip/hip_runtime.h>
 
 #include <mutex>
@@ -73,6 +79,30 @@ constexpr int tile_threads(int chunk) { return chunk / 16 * kWave; }
 
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 
+// ---------------------------------------------------------------------------
+// Agent-coherent buffer accesses (cache policy sc1: no stale copy in the CU's
+// L1 is used, stores are written through). The buffer descriptor bounds every
+// access to [base, base + bytes): outside it loads return 0 and stores are
+// dropped.
+// ---------------------------------------------------------------------------
+constexpr int kAgentCoherent = 16;
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes, 0x00020000);
+}
+__device__ __forceinline__ void coh_store4(__amdgpu_buffer_rsrc_t r, uint32_t byte_off, f4 v) {
+  __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, v), r, (int)byte_off, 0, kAgentCoherent);
+}
+__device__ __forceinline__ f4 coh_load4(__amdgpu_buffer_rsrc_t r, uint32_t byte_off) {
+  return __builtin_bit_cast(f4, __builtin_amdgcn_raw_buffer_load_b128(r, (int)byte_off, 0, kAgentCoherent));
+}
+__device__ __forceinline__ void coh_store1(__amdgpu_buffer_rsrc_t r, uint32_t byte_off, float v) {
+  __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(unsigned, v), r, (int)byte_off, 0, kAgentCoherent);
+}
+__device__ __forceinline__ float coh_load1(__amdgpu_buffer_rsrc_t r, uint32_t byte_off) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(r, (int)byte_off, 0, kAgentCoherent));
+}
+
 // Raw bits of 8 consecutive elements (32 bytes for float32, 16 for 16-bit types).
 struct Raw {
   u32x4 a, b;
@@ -105,8 +135,9 @@ __device__ __forceinline__ void cvt_raw(const Raw& r, int dt, float (&x)[8]) {
   } else {
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
-      x[2 * e] = __builtin_bit_cast(float, r.a[e] << 16);
-      x[2 * e + 1] = __builtin_bit_cast(float, r.a[e] & 0xffff0000u);
+      const unsigned int u = r.a[e];
+      x[2 * e] = __builtin_bit_cast(float, u << 16);
+      x[2 * e + 1] = __builtin_bit_cast(float, u & 0xffff0000u);
     }
   }
 }
@@ -133,48 +164,52 @@ struct Chunk {
   static constexpr int BUFW = KP > OP ? KP : OP;
   static constexpr int TP = F16 ? C + 8 : C + 4;    // transposed-tile pitch (elements)
   static constexpr int SP = F16 ? DK + 8 : DK + 4;  // boundary-state tile pitch
-  static constexpr int NPAIR = NW * (NW - 1) / 2 > 0 ? NW * (NW - 1) / 2 : 1;
   typedef typename Op<F16>::elem E;
   typedef typename Op<F16>::frag8 F8;
   typedef typename Op<F16>::frag4 F4;
 
   struct Smem {
-    float buf[C * BUFW];      // k*exp(T-a) rows [C][KP]; later the output tile [C][OP]
-    E kT[DK * TP];            // (k * exp(A_last - A_r))^T  [DK][TP]
-    E vT[DV * TP];            // v^T                       [DV][TP]
-    E sT[DV * SP];            // S_[c]^T                   [DV][SP]
-    float T[NW][DK];          // sub-chunk totals of g
-    float G0[NW][DK];         // g at the first token of each sub-chunk
-    float Fq[NW][DK];         // exp(A at the first token of R)
-    float Fk[NW][DK];         // exp(sum of totals after R)
-    float Fh[NW][DK];         // exp(span_R / 2)
-    float Foff[NPAIR][DK];    // exp(g0_R + sum_{J<K<R} T_K), pair (R, J), J < R
-    float Fdec[DK];           // exp(sum of all totals) = d_c
-    float Pt[NW][16][17];     // exact diagonal blocks, P^T staging
+    float buf[C * BUFW];   // k*exp(T-a) rows [C][KP]; later the output tile [C][OP]
+    E kT[DK * TP];         // (k * exp(A_last - A_r))^T  [DK][TP]
+    E vT[DV * TP];         // v^T                       [DV][TP]
+    E sT[DV * SP];         // S_[c]^T                   [DV][SP]
+    float T[NW][DK];       // sub-chunk totals of g
+    float Pt[NW][16][17];  // exact diagonal blocks, P^T staging
   };
 
   int w, lane, tr, gq, r;
-  int64_t pos;
-  float qraw[KS][8], kraw[KS][8], aloc[KS][8];
-  float qh[KS][8];   // q * exp(a - g0)
-  float ke[KS][8];   // k * exp(T - a)
-  float spanmax;     // wave-uniform: widest decay span of this sub-chunk
-  float absmax;      // wave-uniform: largest |q|, |k| of this sub-chunk
+  float qh[KS][8];  // q * exp(a - g0)
+  float ke[KS][8];  // k * exp(T - a)
+  float g0[KS][8];  // a at the first token of this sub-chunk (= g there)
+  float tw[KS][8];  // total of g over this sub-chunk
+  float qt[KS][8];  // q * exp(A_r), the readout operand (set by factors())
+  float spanmax;    // wave-uniform: widest decay span of this sub-chunk
+  float absmax;     // wave-uniform: largest |q|, |k| of this sub-chunk
 
   __device__ __forceinline__ int dim(int s, int e) const { return 32 * s + 8 * gq + e; }
 
-  static __device__ __forceinline__ int pair(int R, int J) { return R * (R - 1) / 2 + J; }
-
-  // Loads and per-token work; writes T, G0 and v^T. Ends with a barrier.
-  __device__ __forceinline__ void load(const GlaParams& P, Smem& sm, int bh, int c) {
+  __device__ __forceinline__ void lanes() {
     w = threadIdx.x >> 6;
     lane = threadIdx.x & 63;
     tr = lane & 15;
     gq = lane >> 4;
     r = 16 * w + tr;
-    pos = (int64_t)c * C + r;
-    const bool valid = pos < P.L;
-    const int64_t t = valid ? scan_to_spatial(pos, P.H, P.W, P.scan) : 0;
+  }
+
+  // Spatial token index of scan position `pos` (0 past the end) and whether
+  // the position exists.
+  static __device__ __forceinline__ int64_t token(const GlaParams& P, int64_t pos, bool& valid) {
+    valid = pos < P.L;
+    return valid ? scan_to_spatial(pos, P.H, P.W, P.scan) : 0;
+  }
+
+  // Loads and per-token work. Writes v^T, the sub-chunk totals and (ROWS) the
+  // k*exp(T-a) rows. Ends with a barrier.
+  template <bool ROWS>
+  __device__ __forceinline__ void load(const GlaParams& P, Smem& sm, int bh, int c) {
+    lanes();
+    bool valid;
+    const int64_t t = token(P, (int64_t)c * C + r, valid);
     const int64_t kb = ((int64_t)bh * P.L + t) * DK;
     const int64_t vb = ((int64_t)bh * P.L + t) * DV;
 
@@ -197,13 +232,6 @@ struct Chunk {
       for (int s = 0; s < VS; ++s) rv[s] = Raw{z, z};
     }
 
-    float gv[KS][8];
-#pragma unroll
-    for (int s = 0; s < KS; ++s) {
-      cvt_raw(rq[s], IN, qraw[s]);
-      cvt_raw(rk[s], IN, kraw[s]);
-      cvt_raw(rg[s], P.gdt, gv[s]);
-    }
     // v^T tile
 #pragma unroll
     for (int s = 0; s < VS; ++s) {
@@ -213,81 +241,105 @@ struct Chunk {
       for (int e = 0; e < 8; ++e) sm.vT[(32 * s + 8 * gq + e) * TP + r] = (E)x[e];
     }
 
-    // local inclusive cumulative sums over the 16 tokens of this sub-chunk
     float smax = 0.f, amax = 0.f;
 #pragma unroll
-    for (int s = 0; s < KS; ++s)
+    for (int s = 0; s < KS; ++s) {
+      float qx[8], kx[8], gx[8];
+      cvt_raw(rq[s], IN, qx);
+      cvt_raw(rk[s], IN, kx);
+      cvt_raw(rg[s], P.gdt, gx);
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
-        const float a = row_inclusive_scan(gv[s][e]);
-        const float T = row_read(a, 15);
-        const float g0 = row_read(a, 0);
-        aloc[s][e] = a;
-        smax = fmaxf(smax, g0 - T);
-        amax = fmaxf(amax, fmaxf(fabsf(qraw[s][e]), fabsf(kraw[s][e])));
-        qh[s][e] = qraw[s][e] * gexp<F16>(a - g0);  // exp(A_r - A_first) <= 1
-        ke[s][e] = kraw[s][e] * gexp<F16>(T - a);   // exp(A_last(R) - A_r) <= 1
-        if (tr == 0) {
-          sm.T[w][dim(s, e)] = T;
-          sm.G0[w][dim(s, e)] = g0;
-        }
+        // local inclusive cumulative sum over the 16 tokens of this sub-chunk
+        const float a = row_inclusive_scan(gx[e]);
+        const float T = row_bcast<15>(a);
+        const float f = row_bcast<0>(a);
+        g0[s][e] = f;
+        tw[s][e] = T;
+        smax = fmaxf(smax, f - T);
+        amax = fmaxf(amax, fmaxf(fabsf(qx[e]), fabsf(kx[e])));
+        qh[s][e] = qx[e] * gexp<F16>(a - f);  // exp(A_r - A_first) <= 1
+        ke[s][e] = kx[e] * gexp<F16>(T - a);  // exp(A_last(R) - A_r) <= 1
       }
+      if (tr == 0) {
+        *reinterpret_cast<f4*>(&sm.T[w][32 * s + 8 * gq]) = f4{tw[s][0], tw[s][1], tw[s][2], tw[s][3]};
+        *reinterpret_cast<f4*>(&sm.T[w][32 * s + 8 * gq + 4]) = f4{tw[s][4], tw[s][5], tw[s][6], tw[s][7]};
+      }
+      if constexpr (ROWS) {
+        *reinterpret_cast<f4*>(&sm.buf[r * KP + 32 * s + 8 * gq]) = f4{ke[s][0], ke[s][1], ke[s][2], ke[s][3]};
+        *reinterpret_cast<f4*>(&sm.buf[r * KP + 32 * s + 8 * gq + 4]) = f4{ke[s][4], ke[s][5], ke[s][6], ke[s][7]};
+      }
+    }
     spanmax = __builtin_bit_cast(float, __builtin_amdgcn_readfirstlane(__builtin_bit_cast(int, wave_max(smax))));
     absmax = __builtin_bit_cast(float, __builtin_amdgcn_readfirstlane(__builtin_bit_cast(int, wave_max(amax))));
     __syncthreads();
   }
 
-  // The per-(sub-chunk, dimension) factor table. Ends with a barrier.
-  __device__ __forceinline__ void factors(Smem& sm) {
-    constexpr int N1 = NW * DK;          // Fq, Fk, Fh
-    constexpr int N2 = NW * (NW - 1) / 2 * DK;  // Foff
-    constexpr int N = N1 + N2 + DK;
-    for (int idx = threadIdx.x; idx < N; idx += NT) {
-      if (idx < N1) {
-        const int R = idx / DK, d = idx - R * DK;
-        float before = 0.f, after = 0.f;
-        for (int K = 0; K < R; ++K) before += sm.T[K][d];
-        for (int K = R + 1; K < NW; ++K) after += sm.T[K][d];
-        const float g0 = sm.G0[R][d];
-        sm.Fq[R][d] = gexp<F16>(before + g0);
-        sm.Fk[R][d] = gexp<F16>(after);
-        sm.Fh[R][d] = gexp<F16>(0.5f * (g0 - sm.T[R][d]));
-      } else if (idx < N1 + N2) {
-        const int p = (idx - N1) / DK, d = (idx - N1) - p * DK;
-        int R = 1;
-        while (pair(R + 1, 0) <= p) ++R;
-        const int J = p - pair(R, 0);
-        float between = sm.G0[R][d];
-        for (int K = J + 1; K < R; ++K) between += sm.T[K][d];
-        sm.Foff[p][d] = gexp<F16>(between);
-      } else {
-        const int d = idx - N1 - N2;
-        float tot = 0.f;
-        for (int K = 0; K < NW; ++K) tot += sm.T[K][d];
-        sm.Fdec[d] = gexp<F16>(tot);
+  // Totals of the sub-chunks before / after this one, for this lane's dims.
+  __device__ __forceinline__ void totals(const Smem& sm, float (&before)[KS][8], float (&after)[KS][8]) const {
+#pragma unroll
+    for (int s = 0; s < KS; ++s)
+#pragma unroll
+      for (int e = 0; e < 8; ++e) before[s][e] = after[s][e] = 0.f;
+#pragma unroll
+    for (int K = 0; K < NW; ++K) {
+      // 0/1 weights rather than branches keep both sums in registers
+      const float mb = K < w ? 1.f : 0.f, ma = K > w ? 1.f : 0.f;
+#pragma unroll
+      for (int s = 0; s < KS; ++s) {
+        const f4 lo = *reinterpret_cast<const f4*>(&sm.T[K][32 * s + 8 * gq]);
+        const f4 hi = *reinterpret_cast<const f4*>(&sm.T[K][32 * s + 8 * gq + 4]);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          before[s][e] = fmaf(mb, lo[e], before[s][e]);
+          before[s][e + 4] = fmaf(mb, hi[e], before[s][e + 4]);
+          after[s][e] = fmaf(ma, lo[e], after[s][e]);
+          after[s][e + 4] = fmaf(ma, hi[e], after[s][e + 4]);
+        }
       }
     }
-    __syncthreads();
   }
 
-  // Writes the k rows (and, for the summary, the transposed k-hat tile).
-  // Ends with a barrier.
-  __device__ __forceinline__ void stage_k(Smem& sm, bool summary) {
+  // Chunk-level factors. READOUT: qt = q exp(A_r). SUMMARY: the transposed
+  // k-hat tile and d_c (written by wave 0 through `dec`, coherent or plain),
+  // followed by a barrier.
+  template <bool READOUT, bool SUMMARY, bool COH>
+  __device__ __forceinline__ void factors(Smem& sm, float* dec) {
+    float before[KS][8], after[KS][8];
+    totals(sm, before, after);
 #pragma unroll
     for (int s = 0; s < KS; ++s)
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
-        const int d = dim(s, e);
-        sm.buf[r * KP + d] = ke[s][e];
-        if (summary) sm.kT[d * TP + r] = (E)(ke[s][e] * sm.Fk[w][d]);
+        if constexpr (READOUT) qt[s][e] = qh[s][e] * gexp<F16>(before[s][e] + g0[s][e]);
+        if constexpr (SUMMARY) sm.kT[dim(s, e) * TP + r] = (E)(ke[s][e] * gexp<F16>(after[s][e]));
       }
-    __syncthreads();
+    if constexpr (SUMMARY) {
+      if (w == 0 && tr == 0) {
+#pragma unroll
+        for (int s = 0; s < KS; ++s)
+#pragma unroll
+          for (int h = 0; h < 2; ++h) {
+            f4 d;
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+              d[e] = gexp<F16>(before[s][4 * h + e] + tw[s][4 * h + e] + after[s][4 * h + e]);
+            const int off = 32 * s + 8 * gq + 4 * h;
+            if constexpr (COH)
+              coh_store4(make_rsrc(dec, DK * 4), off * 4, d);
+            else
+              *reinterpret_cast<f4*>(&dec[off]) = d;
+          }
+      }
+      __syncthreads();
+    }
   }
 
-  // U_c (as U^T, [DV][DK]) and d_c to the workspace.
-  __device__ __forceinline__ void summary_out(const GlaParams& P, Smem& sm, int bh, int c) {
+  // U_c as U^T ([DV][DK] fp32) to `U`, coherent or plain.
+  template <bool COH>
+  __device__ __forceinline__ void summary_out(const Smem& sm, float* U) {
     constexpr int NTI = (DK / 16) * (DV / 16);
-    float* U = P.states + ((int64_t)bh * P.nchunks + c) * (DK * DV);
+    const __amdgpu_buffer_rsrc_t ur = make_rsrc(U, DK * DV * 4);
     for (int tau = w; tau < NTI; tau += NW) {
       const int ib = tau / (DV / 16), jb = tau % (DV / 16);
       f4 acc = {0.f, 0.f, 0.f, 0.f};
@@ -298,16 +350,39 @@ struct Chunk {
         acc = mma32(a, b, acc);
       }
       // lane holds U[16ib + 4gq + e][16jb + tr]
-      *reinterpret_cast<f4*>(&U[(16 * jb + tr) * DK + 16 * ib + 4 * gq]) = acc;
+      const int off = (16 * jb + tr) * DK + 16 * ib + 4 * gq;
+      if constexpr (COH)
+        coh_store4(ur, off * 4, acc);
+      else
+        *reinterpret_cast<f4*>(&U[off]) = acc;
     }
-    float* dec = P.decays + ((int64_t)bh * P.nchunks + c) * DK;
-    for (int d = threadIdx.x; d < DK; d += NT) dec[d] = sm.Fdec[d];
   }
 
   // Exact diagonal block for sub-chunks whose decay span is too wide for the
-  // mid-point factors: P[r][j] = sum_d q_r k_j exp(a_r - a_j), j <= r.
-  // Rare; the token loop is kept rolled to keep the code small.
-  __device__ __forceinline__ f4 exact_diagonal(float (*pt)[17]) {
+  // mid-point factors: P[r][j] = sum_d q_r k_j exp(a_r - a_j), j <= r. Rare:
+  // the raw q, k and g of the sub-chunk are reloaded and the token loop is kept
+  // rolled to keep the code small.
+  __device__ __forceinline__ f4 exact_diagonal(const GlaParams& P, float (*pt)[17], int bh, int c) {
+    bool valid;
+    const int64_t t = token(P, (int64_t)c * C + r, valid);
+    const int64_t kb = ((int64_t)bh * P.L + t) * DK;
+    float qx[KS][8], kx[KS][8], ax[KS][8];
+#pragma unroll
+    for (int s = 0; s < KS; ++s) {
+      const u32x4 z = {0u, 0u, 0u, 0u};
+      Raw rq = Raw{z, z}, rk = Raw{z, z}, rg = Raw{z, z};
+      if (valid) {
+        ld_raw(P.q, IN, kb + 32 * s + 8 * gq, rq);
+        ld_raw(P.k, IN, kb + 32 * s + 8 * gq, rk);
+        ld_raw(P.g, P.gdt, kb + 32 * s + 8 * gq, rg);
+      }
+      float gx[8];
+      cvt_raw(rq, IN, qx[s]);
+      cvt_raw(rk, IN, kx[s]);
+      cvt_raw(rg, P.gdt, gx);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) ax[s][e] = row_inclusive_scan(gx[e]);
+    }
 #pragma unroll 1
     for (int j = 0; j < 16; ++j) {
       const int src = ((gq << 4) | j) << 2;
@@ -316,9 +391,9 @@ struct Chunk {
       for (int s = 0; s < KS; ++s)
 #pragma unroll
         for (int e = 0; e < 8; ++e) {
-          const float kj = __builtin_bit_cast(float, __builtin_amdgcn_ds_bpermute(src, __builtin_bit_cast(int, kraw[s][e])));
-          const float aj = __builtin_bit_cast(float, __builtin_amdgcn_ds_bpermute(src, __builtin_bit_cast(int, aloc[s][e])));
-          acc += (j <= tr) ? qraw[s][e] * kj * gexp<F16>(aloc[s][e] - aj) : 0.f;
+          const float kj = __builtin_bit_cast(float, __builtin_amdgcn_ds_bpermute(src, __builtin_bit_cast(int, kx[s][e])));
+          const float aj = __builtin_bit_cast(float, __builtin_amdgcn_ds_bpermute(src, __builtin_bit_cast(int, ax[s][e])));
+          acc += (j <= tr) ? qx[s][e] * kj * gexp<F16>(ax[s][e] - aj) : 0.f;
         }
       acc += __shfl_xor(acc, 16, kWave);
       acc += __shfl_xor(acc, 32, kWave);
@@ -333,59 +408,86 @@ struct Chunk {
   }
 
   // Intra-chunk part: o_r = sum_{j<=r} P[r][j] v_j for this wave's 16 rows.
-  __device__ __forceinline__ void intra(Smem& sm, f4 (&O)[DV / 16]) {
+  // Needs the k rows written by load<true>().
+  __device__ __forceinline__ void intra(const GlaParams& P, Smem& sm, int bh, int c, f4 (&O)[DV / 16]) {
     f4 PT[NW];
     F8 qhf[KS];
 #pragma unroll
     for (int s = 0; s < KS; ++s) qhf[s] = Op<F16>::pack8(qh[s]);
 
+    // off-diagonal blocks J < R = w, walking J down from w-1 so that the
+    // pair factor exp(g0_R + sum_{J<K<R} T_K) grows by one total per step
+    float fsum[KS][8];
 #pragma unroll
-    for (int J = 0; J < NW; ++J) {
+    for (int s = 0; s < KS; ++s)
+#pragma unroll
+      for (int e = 0; e < 8; ++e) fsum[s][e] = g0[s][e];
+#pragma unroll
+    for (int J = NW - 1; J >= 0; --J) {
       PT[J] = f4{0.f, 0.f, 0.f, 0.f};
       if (J < w) {
-        // P^T[j][r] = sum_d (k_j exp(T_J - a_j) Foff[R,J])[d] (q_r exp(a_r - g0_R))[d]
-        const float* fo = sm.Foff[pair(w, J)];
 #pragma unroll
         for (int s = 0; s < KS; ++s) {
+          const float* row = &sm.buf[(16 * J + tr) * KP + 32 * s + 8 * gq];
+          const f4 lo = *reinterpret_cast<const f4*>(row);
+          const f4 hi = *reinterpret_cast<const f4*>(row + 4);
           float x[8];
 #pragma unroll
-          for (int e = 0; e < 8; ++e) x[e] = sm.buf[(16 * J + tr) * KP + dim(s, e)] * fo[dim(s, e)];
+          for (int e = 0; e < 4; ++e) {
+            x[e] = lo[e] * gexp<F16>(fsum[s][e]);
+            x[e + 4] = hi[e] * gexp<F16>(fsum[s][e + 4]);
+          }
+          // P^T[j][r] = sum_d (k_j exp(T_J - a_j) Foff)[d] (q_r exp(a_r - g0_R))[d]
           PT[J] = mma32(Op<F16>::pack8(x), qhf[s], PT[J]);
-        }
-      } else if (J == w) {
-        // fp16 operands only if the mid-point factors keep them well inside fp16 range
-        if (F16 && spanmax <= kSpanF16 && absmax <= 256.f) {
+          const f4 tlo = *reinterpret_cast<const f4*>(&sm.T[J][32 * s + 8 * gq]);
+          const f4 thi = *reinterpret_cast<const f4*>(&sm.T[J][32 * s + 8 * gq + 4]);
 #pragma unroll
-          for (int s = 0; s < KS; ++s) {
-            float a[8], b[8];
-#pragma unroll
-            for (int e = 0; e < 8; ++e) {
-              const float h = sm.Fh[w][dim(s, e)];
-              a[e] = ke[s][e] * h;
-              b[e] = qh[s][e] * h;
-            }
-            PT[J] = mma32(Op<F16>::pack8(a), Op<F16>::pack8(b), PT[J]);
+          for (int e = 0; e < 4; ++e) {
+            fsum[s][e] += tlo[e];
+            fsum[s][e + 4] += thi[e];
           }
-        } else if (spanmax <= kSpanF32) {
-#pragma unroll
-          for (int s = 0; s < KS; ++s) {
-            f8 a, b;
-#pragma unroll
-            for (int e = 0; e < 8; ++e) {
-              const float h = sm.Fh[w][dim(s, e)];
-              a[e] = ke[s][e] * h;
-              b[e] = qh[s][e] * h;
-            }
-            PT[J] = mma32(a, b, PT[J]);
-          }
-        } else {
-          PT[J] = exact_diagonal(sm.Pt[w]);
         }
-        // causal mask: lane holds P^T[j = 4gq + e][r = tr]
-#pragma unroll
-        for (int e = 0; e < 4; ++e)
-          if (4 * gq + e > tr) PT[J][e] = 0.f;
       }
+    }
+
+    // diagonal block: fp16 operands only if the mid-point factors keep them well
+    // inside fp16 range
+    {
+      f4 D = {0.f, 0.f, 0.f, 0.f};
+      if (F16 && spanmax <= kSpanF16 && absmax <= 256.f) {
+#pragma unroll
+        for (int s = 0; s < KS; ++s) {
+          float a[8], b[8];
+#pragma unroll
+          for (int e = 0; e < 8; ++e) {
+            const float h = gexp<F16>(0.5f * (g0[s][e] - tw[s][e]));
+            a[e] = ke[s][e] * h;
+            b[e] = qh[s][e] * h;
+          }
+          D = mma32(Op<F16>::pack8(a), Op<F16>::pack8(b), D);
+        }
+      } else if (spanmax <= kSpanF32) {
+#pragma unroll
+        for (int s = 0; s < KS; ++s) {
+          f8 a, b;
+#pragma unroll
+          for (int e = 0; e < 8; ++e) {
+            const float h = gexp<F16>(0.5f * (g0[s][e] - tw[s][e]));
+            a[e] = ke[s][e] * h;
+            b[e] = qh[s][e] * h;
+          }
+          D = mma32(a, b, D);
+        }
+      } else {
+        D = exact_diagonal(P, sm.Pt[w], bh, c);
+      }
+      // causal mask: lane holds P^T[j = 4gq + e][r = tr]
+#pragma unroll
+      for (int e = 0; e < 4; ++e)
+        if (4 * gq + e > tr) D[e] = 0.f;
+#pragma unroll
+      for (int J = 0; J < NW; ++J)
+        if (J == w) PT[J] = D;
     }
 
 #pragma unroll
@@ -403,19 +505,26 @@ struct Chunk {
     }
   }
 
-  // Boundary state S_[c]^T ([DV][DK] fp32 in the workspace) -> shared tile, in
-  // two steps so the loads can be issued early: each thread moves whole
-  // 16-byte pieces. No barrier.
-  static constexpr int SQ4 = DK * DV / 4;          // 16-byte pieces in one state
+  // Boundary state S_[c]^T ([DV][DK] fp32) -> shared tile, in two steps so the
+  // loads can be issued early: each thread moves whole 16-byte pieces. No
+  // barrier.
+  static constexpr int SQ4 = DK * DV / 4;           // 16-byte pieces in one state
   static constexpr int SPER = (SQ4 + NT - 1) / NT;  // pieces per thread
-  __device__ __forceinline__ void stage_state_load(const float* ST, f4 (&buf)[SPER]) {
+  template <bool COH>
+  __device__ __forceinline__ void state_load(const float* ST, f4 (&buf)[SPER]) {
+    const __amdgpu_buffer_rsrc_t sr = make_rsrc(ST, DK * DV * 4);
 #pragma unroll
     for (int m = 0; m < SPER; ++m) {
       const int q4 = threadIdx.x + m * NT;
-      if (q4 < SQ4) buf[m] = reinterpret_cast<const f4*>(ST)[q4];
+      if (q4 < SQ4) {
+        if constexpr (COH)
+          buf[m] = coh_load4(sr, q4 * 16);
+        else
+          buf[m] = reinterpret_cast<const f4*>(ST)[q4];
+      }
     }
   }
-  __device__ __forceinline__ void stage_state_store(Smem& sm, const f4 (&buf)[SPER]) {
+  __device__ __forceinline__ void state_store(Smem& sm, const f4 (&buf)[SPER]) {
 #pragma unroll
     for (int m = 0; m < SPER; ++m) {
       const int q4 = threadIdx.x + m * NT;  // piece index in [DV][DK]
@@ -428,15 +537,10 @@ struct Chunk {
   }
 
   // o_r += (q_r exp(A_r)) S_[c]. Reads the shared state tile.
-  __device__ __forceinline__ void readout(Smem& sm, f4 (&O)[DV / 16]) {
+  __device__ __forceinline__ void readout(const Smem& sm, f4 (&O)[DV / 16]) {
     F8 qtf[KS];
 #pragma unroll
-    for (int s = 0; s < KS; ++s) {
-      float x[8];
-#pragma unroll
-      for (int e = 0; e < 8; ++e) x[e] = qh[s][e] * sm.Fq[w][dim(s, e)];
-      qtf[s] = Op<F16>::pack8(x);
-    }
+    for (int s = 0; s < KS; ++s) qtf[s] = Op<F16>::pack8(qt[s]);
 #pragma unroll
     for (int jb = 0; jb < DV / 16; ++jb)
 #pragma unroll
@@ -457,9 +561,9 @@ struct Chunk {
     constexpr int PIECES = DV / 8;
     for (int idx = threadIdx.x; idx < C * PIECES; idx += NT) {
       const int rr = idx / PIECES, pc = idx % PIECES;
-      const int64_t p = (int64_t)c * C + rr;
-      if (p < P.L) {
-        const int64_t t = scan_to_spatial(p, P.H, P.W, P.scan);
+      bool valid;
+      const int64_t t = token(P, (int64_t)c * C + rr, valid);
+      if (valid) {
         float x[8];
 #pragma unroll
         for (int e = 0; e < 8; ++e) x[e] = sm.buf[rr * OP + 8 * pc + e];
@@ -470,36 +574,65 @@ struct Chunk {
 };
 
 // ---------------------------------------------------------------------------
-// boundary-state scan over chunks for elements [e0, e1) of one sequence's
-// state (S^T layout, element e = dv*DK + i). In place: U_c^T -> S_[c]^T.
+// Boundary-state scan over chunks (Eq. chunk_boundary_main) for elements
+// [e0, e1) of one sequence's state (S^T layout, element e = dv*DK + i). In
+// place: U_c^T -> S_[c]^T. S_final gets the state after the last chunk.
 // ---------------------------------------------------------------------------
 template <int DK, int DV>
-__device__ __forceinline__ void scan_elements(const GlaParams& P, int bh, int e0, int e1, int tid, int nt) {
+__device__ __forceinline__ void scan_plain(const GlaParams& P, int bh, int e0, int e1, int tid, int nt) {
   float* st = P.states + (int64_t)bh * P.nchunks * (DK * DV);
   const float* dec = P.decays + (int64_t)bh * P.nchunks * DK;
   const int NC = P.nchunks;
   for (int e = e0 + tid; e < e1; e += nt) {
     const int dv = e / DK, i = e - dv * DK;
     float s = P.s0 ? P.s0[((int64_t)bh * DK + i) * DV + dv] : 0.f;
-    int c = 0;
-    for (; c + 8 <= NC; c += 8) {
-      float u[8], d[8];
+    for (int c0 = 0; c0 < NC; c0 += 32) {
+      float u[32], d[32];
 #pragma unroll
-      for (int m = 0; m < 8; ++m) {
-        u[m] = st[(int64_t)(c + m) * (DK * DV) + e];
-        d[m] = dec[(int64_t)(c + m) * DK + i];
+      for (int m = 0; m < 32; ++m) {
+        if (c0 + m < NC) {
+          u[m] = st[(int64_t)(c0 + m) * (DK * DV) + e];
+          d[m] = dec[(int64_t)(c0 + m) * DK + i];
+        }
       }
 #pragma unroll
-      for (int m = 0; m < 8; ++m) {
-        st[(int64_t)(c + m) * (DK * DV) + e] = s;
-        s = d[m] * s + u[m];
+      for (int m = 0; m < 32; ++m) {
+        if (c0 + m < NC) {
+          st[(int64_t)(c0 + m) * (DK * DV) + e] = s;
+          s = d[m] * s + u[m];
+        }
       }
     }
-    for (; c < NC; ++c) {
-      const float u = st[(int64_t)c * (DK * DV) + e];
-      const float d = dec[(int64_t)c * DK + i];
-      st[(int64_t)c * (DK * DV) + e] = s;
-      s = d * s + u;
+    if (P.s_final) P.s_final[((int64_t)bh * DK + i) * DV + dv] = s;
+  }
+}
+
+// The same with agent-coherent accesses, for the fused schedule. One sequence's
+// states span nchunks * DK * DV * 4 bytes, which the host keeps below 2^31.
+template <int DK, int DV>
+__device__ __forceinline__ void scan_coherent(const GlaParams& P, int bh, int e0, int e1, int tid, int nt) {
+  const int NC = P.nchunks;
+  const __amdgpu_buffer_rsrc_t sr = make_rsrc(P.states + (int64_t)bh * NC * (DK * DV), (uint32_t)NC * DK * DV * 4);
+  const __amdgpu_buffer_rsrc_t dr = make_rsrc(P.decays + (int64_t)bh * NC * DK, (uint32_t)NC * DK * 4);
+  for (int e = e0 + tid; e < e1; e += nt) {
+    const int dv = e / DK, i = e - dv * DK;
+    float s = P.s0 ? P.s0[((int64_t)bh * DK + i) * DV + dv] : 0.f;
+    for (int c0 = 0; c0 < NC; c0 += 32) {
+      float u[32], d[32];
+#pragma unroll
+      for (int m = 0; m < 32; ++m) {
+        if (c0 + m < NC) {
+          u[m] = coh_load1(sr, ((uint32_t)(c0 + m) * (DK * DV) + e) * 4);
+          d[m] = coh_load1(dr, ((uint32_t)(c0 + m) * DK + i) * 4);
+        }
+      }
+#pragma unroll
+      for (int m = 0; m < 32; ++m) {
+        if (c0 + m < NC) {
+          coh_store1(sr, ((uint32_t)(c0 + m) * (DK * DV) + e) * 4, s);
+          s = d[m] * s + u[m];
+        }
+      }
     }
     if (P.s_final) P.s_final[((int64_t)bh * DK + i) * DV + dv] = s;
   }
@@ -514,10 +647,10 @@ __global__ void __launch_bounds__(tile_threads(C)) gla_summary_kernel(GlaParams 
   __shared__ typename T::Smem sm;
   T ch;
   const int c = blockIdx.x, bh = blockIdx.y;
-  ch.load(P, sm, bh, c);
-  ch.factors(sm);
-  ch.stage_k(sm, true);
-  ch.summary_out(P, sm, bh, c);
+  const int64_t sc = (int64_t)bh * P.nchunks + c;
+  ch.template load<false>(P, sm, bh, c);
+  ch.template factors<false, true, false>(sm, P.decays + sc * DK);
+  ch.template summary_out<false>(sm, P.states + sc * (DK * DV));
 }
 
 template <int DK, int DV>
@@ -525,7 +658,7 @@ __global__ void __launch_bounds__(256) gla_scan_kernel(GlaParams P) {
   const int bh = blockIdx.y;
   const int e0 = blockIdx.x * 256;
   const int e1 = min(e0 + 256, DK * DV);
-  scan_elements<DK, DV>(P, bh, e0, e1, threadIdx.x, 256);
+  scan_plain<DK, DV>(P, bh, e0, e1, threadIdx.x, 256);
 }
 
 template <int DK, int DV, int C, int IN>
@@ -536,30 +669,35 @@ __global__ void __launch_bounds__(tile_threads(C)) gla_output_kernel(GlaParams P
   const int c = blockIdx.x, bh = blockIdx.y;
   const bool have_state = c > 0 || P.s0;
   f4 sbuf[T::SPER];
-  if (have_state) ch.stage_state_load(P.states + ((int64_t)bh * P.nchunks + c) * (DK * DV), sbuf);
-  ch.load(P, sm, bh, c);
-  if (have_state) ch.stage_state_store(sm, sbuf);
-  ch.factors(sm);
-  ch.stage_k(sm, false);
+  if (have_state) ch.template state_load<false>(P.states + ((int64_t)bh * P.nchunks + c) * (DK * DV), sbuf);
+  ch.template load<true>(P, sm, bh, c);
+  if (have_state) ch.state_store(sm, sbuf);
+  ch.template factors<true, false, false>(sm, nullptr);
   f4 O[DV / 16];
-  ch.intra(sm, O);
-  if (have_state) ch.readout(sm, O);
+  ch.intra(P, sm, bh, c, O);
+  if (have_state) {
+    __syncthreads();  // state tile complete
+    ch.readout(sm, O);
+  }
   ch.store(P, sm, bh, c, O);
 }
 
 // ---------------------------------------------------------------------------
 // fused schedule
 // ---------------------------------------------------------------------------
+// A work-group's coherent stores are acknowledged before its one increment.
 __device__ __forceinline__ void seq_arrive(unsigned* ctr) {
-  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
   __syncthreads();
-  if (threadIdx.x == 0) __hip_atomic_fetch_add(ctr, 1u, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
+  if (threadIdx.x == 0) __hip_atomic_fetch_add(ctr, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
+// Bounded wait until `ctr` reaches `target`; on time-out the fault word is set
+// (the results of the call are then invalid) and the work-group goes on.
 __device__ __forceinline__ void seq_wait(unsigned* ctr, unsigned target, unsigned* fault) {
   if (threadIdx.x == 0) {
     unsigned n = 0;
-    while (__hip_atomic_load(ctr, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_AGENT) < target) {
+    while (__hip_atomic_load(ctr, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < target) {
       __builtin_amdgcn_s_sleep(1);
       if (++n > kSpinLimit) {
         __hip_atomic_store(fault, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -568,13 +706,12 @@ __device__ __forceinline__ void seq_wait(unsigned* ctr, unsigned target, unsigne
     }
   }
   __syncthreads();
-  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
 }
 
 // Work-group -> (sequence, chunk). Work-groups are handed to the 8 XCDs round
 // robin, so block b runs on XCD b % 8; all chunks of a sequence get the same
-// b % 8 and therefore share one L2 for their summaries and boundary states.
-// Blocks whose sequence index is past the end exit at once.
+// b % 8 and therefore share one L2. Blocks whose sequence index is past the end
+// exit at once.
 template <int DK, int DV, int C, int IN>
 __global__ void __launch_bounds__(tile_threads(C)) gla_fused_kernel(GlaParams P) {
   typedef Chunk<DK, DV, C, IN> T;
@@ -586,37 +723,37 @@ __global__ void __launch_bounds__(tile_threads(C)) gla_fused_kernel(GlaParams P)
   const int bh = grp * 8 + x;
   if (bh >= P.BH) return;
   unsigned* sync = P.sync + 4 * bh;
+  const int64_t sc = (int64_t)bh * NC + c;
 
   T ch;
-  ch.load(P, sm, bh, c);
-  ch.factors(sm);
-  ch.stage_k(sm, true);
-  ch.summary_out(P, sm, bh, c);
+  ch.template load<true>(P, sm, bh, c);
+  ch.template factors<true, true, true>(sm, P.decays + sc * DK);
+  ch.template summary_out<true>(sm, P.states + sc * (DK * DV));
   seq_arrive(&sync[0]);
 
   f4 O[DV / 16];
-  ch.intra(sm, O);
+  ch.intra(P, sm, bh, c, O);
 
   seq_wait(&sync[0], (unsigned)NC, P.fault);
   {
     const int per = (DK * DV + NC - 1) / NC;
     const int e0 = min(c * per, DK * DV), e1 = min(e0 + per, DK * DV);
-    scan_elements<DK, DV>(P, bh, e0, e1, threadIdx.x, T::NT);
+    scan_coherent<DK, DV>(P, bh, e0, e1, threadIdx.x, T::NT);
   }
   seq_arrive(&sync[1]);
   seq_wait(&sync[1], (unsigned)NC, P.fault);
 
   if (c > 0 || P.s0) {
     f4 sbuf[T::SPER];
-    ch.stage_state_load(P.states + ((int64_t)bh * NC + c) * (DK * DV), sbuf);
-    ch.stage_state_store(sm, sbuf);
+    ch.template state_load<true>(P.states + sc * (DK * DV), sbuf);
+    ch.state_store(sm, sbuf);
     __syncthreads();
     ch.readout(sm, O);
   }
   ch.store(P, sm, bh, c, O);
 
   if (threadIdx.x == 0) {
-    const unsigned prev = __hip_atomic_fetch_add(&sync[2], 1u, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT);
+    const unsigned prev = __hip_atomic_fetch_add(&sync[2], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     if (prev == (unsigned)NC - 1) {  // last one out: leave the counters zeroed
       __hip_atomic_store(&sync[0], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
       __hip_atomic_store(&sync[1], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -703,6 +840,11 @@ static int fused_capacity_per_xcd(const void* kernel, int threads) {
   return cap;
 }
 
+// The fused schedule addresses one sequence's states through a buffer
+// descriptor with a 32-bit range: nchunks * 64 * 64 * 4 bytes must stay below
+// 2^31.
+constexpr int64_t kFusedMaxChunks = 4096;
+
 }  // namespace gtr
 
 using namespace gtr;
@@ -767,7 +909,7 @@ extern "C" gtr_status gtr_gla_fwd(const gtr_gla_args* a, hipStream_t stream) {
   bool fused = false;
   if (a->path == GTR_PATH_FUSED || a->path == GTR_PATH_AUTO) {
     const int cap = fused_capacity_per_xcd(ks.fused, ks.threads);
-    const bool fits = cap > 0 && s.nchunks <= cap;
+    const bool fits = cap > 0 && s.nchunks <= cap && s.nchunks <= kFusedMaxChunks;
     if (a->path == GTR_PATH_FUSED && !fits) return GTR_ERR_UNSUPPORTED;
     fused = fits;
   }

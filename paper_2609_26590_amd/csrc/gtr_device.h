@@ -187,11 +187,11 @@ __device__ __forceinline__ float row_inclusive_scan(float x) {
   return x;
 }
 
-// Value of lane `src` (0..15) of this lane's 16-lane row.
-__device__ __forceinline__ float row_read(float x, int src) {
-  const int lane = __lane_id();
-  return __builtin_bit_cast(float, __builtin_amdgcn_ds_bpermute(((lane & ~15) | src) << 2,
-                                                               __builtin_bit_cast(int, x)));
+// Value of lane N (0..15) of this lane's 16-lane row (DPP row_newbcast).
+template <int N>
+__device__ __forceinline__ float row_bcast(float x) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, x), 0x150 + N, 0xf, 0xf,
+                                                               false));
 }
 
 __device__ __forceinline__ float wave_max(float x) {
