@@ -9,13 +9,21 @@ once inside the timed region.
 Prints ONE JSON line (see the keys below). ``roofline`` prices the call's
 kernels against HBM bandwidth with the algorithmic bytes of the call;
 ``cpu_baseline`` times the float64 oracle on the host on a bounded sample of
-the same workload.
+the same workload. ``roofline.traffic`` is the HBM traffic per call read by
+rocprofv3 counters (FETCH_SIZE + WRITE_SIZE, scaled by a plain copy of known
+size), taken from the profile summary under ``profiles/``; it is null when the
+kernel sources have changed since that summary was written.
+
+``--calibrate-copy MB`` only runs a device-to-device copy of that size (the
+reference kernel for the counter scaling) and prints its byte count.
 """
 from __future__ import annotations
 
 import argparse
+import hashlib
 import json
 import os
+import re
 import sys
 import time
 
@@ -30,6 +38,29 @@ from paper_2609_26590_amd.workloads import (WORKLOADS, algorithmic_bytes, algori
 
 HBM_PEAK_GBS = 8000.0        # MI355X HBM3E, published
 MFMA_F16_PEAK_TFLOPS = 2500.0  # MI355X dense fp16 matrix, published
+KERNEL_SOURCES = ("paper_2609_26590_amd/csrc/gla_fwd.hip", "paper_2609_26590_amd/csrc/gtr_device.h")
+TRAFFIC_PROFILE = "profiles/gla_fused_kbench_traffic.txt"
+
+
+def kernel_source_hash() -> str:
+    h = hashlib.sha256()
+    for rel in KERNEL_SOURCES:
+        with open(os.path.join(ROOT, rel), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def stored_traffic():
+    """HBM bytes per call from the committed counter summary, if it is current."""
+    path = os.path.join(ROOT, TRAFFIC_PROFILE)
+    if not os.path.exists(path):
+        return None
+    txt = open(path).read()
+    m_hash = re.search(r"kernel source hash:\s*([0-9a-f]+)", txt)
+    m_val = re.search(r"traffic bytes per call:\s*([0-9.eE+]+)", txt)
+    if not m_hash or not m_val or m_hash.group(1) != kernel_source_hash():
+        return None
+    return float(m_val.group(1))
 
 
 def parse():
@@ -42,7 +73,25 @@ def parse():
     p.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     p.add_argument("--cpu-seconds", type=float, default=10.0)
     p.add_argument("--detail", action="store_true", help="also time the other workloads")
+    p.add_argument("--calibrate-copy", type=float, default=0.0, metavar="MB",
+                   help="only run a device-to-device copy of MB megabytes --steps times")
     return p.parse_args()
+
+
+def calibrate_copy(mb, steps):
+    n = int(mb * 1e6) // 16 * 16
+    src = torch.randint(0, 255, (n,), dtype=torch.uint8, device="cuda")
+    dst = torch.empty_like(src)
+    for _ in range(3):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    el = time.perf_counter() - t0
+    print(json.dumps({"copy_bytes_read": n, "copy_bytes_written": n, "copies": steps,
+                      "GBps_read_plus_write": 2 * n * steps / el / 1e9}), flush=True)
 
 
 def setup(wl, path, scan=None):
@@ -112,6 +161,9 @@ def main():
     if not torch.cuda.is_available():
         print(json.dumps({"error": "no GPU visible"}))
         sys.exit(1)
+    if a.calibrate_copy > 0:
+        calibrate_copy(a.calibrate_copy, a.steps)
+        return
     gtr.load()
     wl = WORKLOADS[a.workload]
     step = setup(wl, a.path, scan=wl.scans[0])
@@ -141,9 +193,13 @@ def main():
         "token_heads_per_s": tok_s,
         "tflops": flops / per_call / 1e12,
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": achieved / HBM_PEAK_GBS, "traffic": None,
-                     "kernel": "one gtr_gla_fwd call (all of its kernels)",
+                     "frac": achieved / HBM_PEAK_GBS,
+                     "traffic": stored_traffic() if a.path in ("auto", "fused") else None,
+                     "kernel": "gla_fused_kernel (the whole call is this one launch)" if a.path != "staged"
+                               else "one gtr_gla_fwd call (summary + scan + output kernels)",
                      "alg_bytes_per_call": nbytes, "us_per_call": per_call * 1e6,
+                     "timing": "HIP events around a graph of K calls on the launch stream, divided by K",
+                     "kernel_source_hash": kernel_source_hash(),
                      "mfma_frac": flops / per_call / 1e12 / MFMA_F16_PEAK_TFLOPS},
     }
     if a.detail:
