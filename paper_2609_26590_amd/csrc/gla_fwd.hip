@@ -24,8 +24,10 @@
 //     per-element exp(a_r - a_j) on the vector ALUs beyond that.
 //   * The summary uses k_j exp(A_last - A_j) and the readout q_r exp(A_r), both
 //     with exponents <= 0.
-// Each wave builds the factors of its own sub-chunk in registers from a small
-// shared table of the sub-chunk totals.
+// The factors that depend only on (sub-chunk, dimension) are computed once per
+// dimension (lane d of the wave for dimension d) into a small per-wave table in
+// LDS, from the shared table of sub-chunk totals, and read back by the lanes
+// that use them.
 //
 // Schedules:
 //   * staged: summary kernel -> boundary-state scan kernel -> output kernel.
@@ -164,6 +166,7 @@ struct Chunk {
   static constexpr int BUFW = KP > OP ? KP : OP;
   static constexpr int TP = F16 ? C + 8 : C + 4;    // transposed-tile pitch (elements)
   static constexpr int SP = F16 ? DK + 8 : DK + 4;  // boundary-state tile pitch
+  static constexpr int NF = 3 + (NW > 1 ? NW - 1 : 1);  // factor-table rows per wave
   typedef typename Op<F16>::elem E;
   typedef typename Op<F16>::frag8 F8;
   typedef typename Op<F16>::frag4 F4;
@@ -174,8 +177,15 @@ struct Chunk {
     E vT[DV * TP];         // v^T                       [DV][TP]
     E sT[DV * SP];         // S_[c]^T                   [DV][SP]
     float T[NW][DK];       // sub-chunk totals of g
+    float G0[NW][DK];      // g at the first token of each sub-chunk
+    float F[NW][NF][DK];   // per-wave factor table (rows kFq, kFk, kFh, kFoff + J)
     float Pt[NW][16][17];  // exact diagonal blocks, P^T staging
   };
+  // rows of the factor table of sub-chunk R, per dimension d:
+  static constexpr int kFq = 0;    // exp(A before R + g0_R): q readout factor
+  static constexpr int kFk = 1;    // exp(sum of totals after R): k-hat factor
+  static constexpr int kFh = 2;    // exp((g0_R - T_R) / 2): diagonal mid-point factor
+  static constexpr int kFoff = 3;  // + J: exp(g0_R + sum_{J<K<R} T_K), J < R
 
   int w, lane, tr, gq, r;
   float qh[KS][8];  // q * exp(a - g0)
@@ -264,6 +274,8 @@ struct Chunk {
       if (tr == 0) {
         *reinterpret_cast<f4*>(&sm.T[w][32 * s + 8 * gq]) = f4{tw[s][0], tw[s][1], tw[s][2], tw[s][3]};
         *reinterpret_cast<f4*>(&sm.T[w][32 * s + 8 * gq + 4]) = f4{tw[s][4], tw[s][5], tw[s][6], tw[s][7]};
+        *reinterpret_cast<f4*>(&sm.G0[w][32 * s + 8 * gq]) = f4{g0[s][0], g0[s][1], g0[s][2], g0[s][3]};
+        *reinterpret_cast<f4*>(&sm.G0[w][32 * s + 8 * gq + 4]) = f4{g0[s][4], g0[s][5], g0[s][6], g0[s][7]};
       }
       if constexpr (ROWS) {
         *reinterpret_cast<f4*>(&sm.buf[r * KP + 32 * s + 8 * gq]) = f4{ke[s][0], ke[s][1], ke[s][2], ke[s][3]};
@@ -275,64 +287,71 @@ struct Chunk {
     __syncthreads();
   }
 
-  // Totals of the sub-chunks before / after this one, for this lane's dims.
-  __device__ __forceinline__ void totals(const Smem& sm, float (&before)[KS][8], float (&after)[KS][8]) const {
+  // This lane's 8 consecutive dims of factor-table row `row`, for K-step s.
+  __device__ __forceinline__ void frow(const Smem& sm, int row, int s, float (&x)[8]) const {
+    const f4 lo = *reinterpret_cast<const f4*>(&sm.F[w][row][32 * s + 8 * gq]);
+    const f4 hi = *reinterpret_cast<const f4*>(&sm.F[w][row][32 * s + 8 * gq + 4]);
 #pragma unroll
-    for (int s = 0; s < KS; ++s)
-#pragma unroll
-      for (int e = 0; e < 8; ++e) before[s][e] = after[s][e] = 0.f;
-#pragma unroll
-    for (int K = 0; K < NW; ++K) {
-      // 0/1 weights rather than branches keep both sums in registers
-      const float mb = K < w ? 1.f : 0.f, ma = K > w ? 1.f : 0.f;
-#pragma unroll
-      for (int s = 0; s < KS; ++s) {
-        const f4 lo = *reinterpret_cast<const f4*>(&sm.T[K][32 * s + 8 * gq]);
-        const f4 hi = *reinterpret_cast<const f4*>(&sm.T[K][32 * s + 8 * gq + 4]);
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          before[s][e] = fmaf(mb, lo[e], before[s][e]);
-          before[s][e + 4] = fmaf(mb, hi[e], before[s][e + 4]);
-          after[s][e] = fmaf(ma, lo[e], after[s][e]);
-          after[s][e + 4] = fmaf(ma, hi[e], after[s][e + 4]);
-        }
-      }
+    for (int e = 0; e < 4; ++e) {
+      x[e] = lo[e];
+      x[e + 4] = hi[e];
     }
   }
 
-  // Chunk-level factors. READOUT: qt = q exp(A_r). SUMMARY: the transposed
-  // k-hat tile and d_c (written by wave 0 through `dec`, coherent or plain),
-  // followed by a barrier.
+  // Chunk-level factors. Lane d of each wave fills dimension d of its
+  // sub-chunk's factor table (one exponential per factor and dimension); the
+  // wave then reads back what its lanes need. READOUT: qt = q exp(A_r).
+  // SUMMARY: the transposed k-hat tile and d_c (written by wave 0 through
+  // `dec`, coherent or plain), followed by a barrier.
   template <bool READOUT, bool SUMMARY, bool COH>
   __device__ __forceinline__ void factors(Smem& sm, float* dec) {
-    float before[KS][8], after[KS][8];
-    totals(sm, before, after);
+    if (lane < DK) {
+      const int d = lane;
+      float tK[NW];
+      float before = 0.f, after = 0.f;
 #pragma unroll
-    for (int s = 0; s < KS; ++s)
-#pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        if constexpr (READOUT) qt[s][e] = qh[s][e] * gexp<F16>(before[s][e] + g0[s][e]);
-        if constexpr (SUMMARY) sm.kT[dim(s, e) * TP + r] = (E)(ke[s][e] * gexp<F16>(after[s][e]));
+      for (int K = 0; K < NW; ++K) {
+        tK[K] = sm.T[K][d];
+        before += K < w ? tK[K] : 0.f;
+        after += K > w ? tK[K] : 0.f;
       }
-    if constexpr (SUMMARY) {
-      if (w == 0 && tr == 0) {
+      const float g0d = sm.G0[w][d];
+      sm.F[w][kFq][d] = gexp<F16>(before + g0d);
+      sm.F[w][kFk][d] = gexp<F16>(after);
+      sm.F[w][kFh][d] = gexp<F16>(0.5f * (g0d - sm.T[w][d]));
+      float acc = g0d;  // exp(g0_R + sum_{J<K<R} T_K) for J = R-1, R-2, ...
 #pragma unroll
-        for (int s = 0; s < KS; ++s)
-#pragma unroll
-          for (int h = 0; h < 2; ++h) {
-            f4 d;
-#pragma unroll
-            for (int e = 0; e < 4; ++e)
-              d[e] = gexp<F16>(before[s][4 * h + e] + tw[s][4 * h + e] + after[s][4 * h + e]);
-            const int off = 32 * s + 8 * gq + 4 * h;
-            if constexpr (COH)
-              coh_store4(make_rsrc(dec, DK * 4), off * 4, d);
-            else
-              *reinterpret_cast<f4*>(&dec[off]) = d;
-          }
+      for (int J = NW - 2; J >= 0; --J) {
+        if (J < w) {
+          sm.F[w][kFoff + J][d] = gexp<F16>(acc);
+          acc += tK[J];
+        }
       }
-      __syncthreads();
+      if (SUMMARY && w == 0) {
+        const float dc = gexp<F16>(before + sm.T[0][d] + after);
+        if constexpr (COH)
+          coh_store1(make_rsrc(dec, DK * 4), d * 4, dc);
+        else
+          dec[d] = dc;
+      }
     }
+    __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0): the table writes of this wave are done
+    __builtin_amdgcn_wave_barrier();
+#pragma unroll
+    for (int s = 0; s < KS; ++s) {
+      float f[8];
+      if constexpr (READOUT) {
+        frow(sm, kFq, s, f);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) qt[s][e] = qh[s][e] * f[e];
+      }
+      if constexpr (SUMMARY) {
+        frow(sm, kFk, s, f);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) sm.kT[dim(s, e) * TP + r] = (E)(ke[s][e] * f[e]);
+      }
+    }
+    if constexpr (SUMMARY) __syncthreads();
   }
 
   // U_c as U^T ([DV][DK] fp32) to `U`, coherent or plain.
@@ -415,15 +434,9 @@ struct Chunk {
 #pragma unroll
     for (int s = 0; s < KS; ++s) qhf[s] = Op<F16>::pack8(qh[s]);
 
-    // off-diagonal blocks J < R = w, walking J down from w-1 so that the
-    // pair factor exp(g0_R + sum_{J<K<R} T_K) grows by one total per step
-    float fsum[KS][8];
+    // off-diagonal blocks J < R = w, with the pair factors of the table
 #pragma unroll
-    for (int s = 0; s < KS; ++s)
-#pragma unroll
-      for (int e = 0; e < 8; ++e) fsum[s][e] = g0[s][e];
-#pragma unroll
-    for (int J = NW - 1; J >= 0; --J) {
+    for (int J = 0; J < NW; ++J) {
       PT[J] = f4{0.f, 0.f, 0.f, 0.f};
       if (J < w) {
 #pragma unroll
@@ -431,21 +444,15 @@ struct Chunk {
           const float* row = &sm.buf[(16 * J + tr) * KP + 32 * s + 8 * gq];
           const f4 lo = *reinterpret_cast<const f4*>(row);
           const f4 hi = *reinterpret_cast<const f4*>(row + 4);
-          float x[8];
+          float fo[8], x[8];
+          frow(sm, kFoff + J, s, fo);
 #pragma unroll
           for (int e = 0; e < 4; ++e) {
-            x[e] = lo[e] * gexp<F16>(fsum[s][e]);
-            x[e + 4] = hi[e] * gexp<F16>(fsum[s][e + 4]);
+            x[e] = lo[e] * fo[e];
+            x[e + 4] = hi[e] * fo[e + 4];
           }
           // P^T[j][r] = sum_d (k_j exp(T_J - a_j) Foff)[d] (q_r exp(a_r - g0_R))[d]
           PT[J] = mma32(Op<F16>::pack8(x), qhf[s], PT[J]);
-          const f4 tlo = *reinterpret_cast<const f4*>(&sm.T[J][32 * s + 8 * gq]);
-          const f4 thi = *reinterpret_cast<const f4*>(&sm.T[J][32 * s + 8 * gq + 4]);
-#pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            fsum[s][e] += tlo[e];
-            fsum[s][e + 4] += thi[e];
-          }
         }
       }
     }
@@ -457,12 +464,12 @@ struct Chunk {
       if (F16 && spanmax <= kSpanF16 && absmax <= 256.f) {
 #pragma unroll
         for (int s = 0; s < KS; ++s) {
-          float a[8], b[8];
+          float a[8], b[8], h[8];
+          frow(sm, kFh, s, h);
 #pragma unroll
           for (int e = 0; e < 8; ++e) {
-            const float h = gexp<F16>(0.5f * (g0[s][e] - tw[s][e]));
-            a[e] = ke[s][e] * h;
-            b[e] = qh[s][e] * h;
+            a[e] = ke[s][e] * h[e];
+            b[e] = qh[s][e] * h[e];
           }
           D = mma32(Op<F16>::pack8(a), Op<F16>::pack8(b), D);
         }
@@ -470,11 +477,12 @@ struct Chunk {
 #pragma unroll
         for (int s = 0; s < KS; ++s) {
           f8 a, b;
+          float h[8];
+          frow(sm, kFh, s, h);
 #pragma unroll
           for (int e = 0; e < 8; ++e) {
-            const float h = gexp<F16>(0.5f * (g0[s][e] - tw[s][e]));
-            a[e] = ke[s][e] * h;
-            b[e] = qh[s][e] * h;
+            a[e] = ke[s][e] * h[e];
+            b[e] = qh[s][e] * h[e];
           }
           D = mma32(a, b, D);
         }
