@@ -14,6 +14,11 @@ rocprofv3 counters (FETCH_SIZE + WRITE_SIZE, scaled by a plain copy of known
 size), taken from the profile summary under ``profiles/``; it is null when the
 kernel sources have changed since that summary was written.
 
+``cold`` repeats the timing with the calls rotating over ``--cold-sets``
+distinct copies of the inputs (128 copies of 4.9 MB exceed the 256 MB MALL),
+so that every call reads its inputs from HBM; the headline ``value`` is the
+warm number (the same input buffers every call).
+
 ``--calibrate-copy MB`` only runs a device-to-device copy of that size (the
 reference kernel for the counter scaling) and prints its byte count.
 """
@@ -73,6 +78,9 @@ def parse():
     p.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     p.add_argument("--cpu-seconds", type=float, default=10.0)
     p.add_argument("--detail", action="store_true", help="also time the other workloads")
+    p.add_argument("--cold-sets", type=int, default=128,
+                   help="also time the calls rotating over this many distinct input sets (more bytes than the "
+                        "256 MB MALL holds, so every call reads HBM); 0 skips it")
     p.add_argument("--calibrate-copy", type=float, default=0.0, metavar="MB",
                    help="only run a device-to-device copy of MB megabytes --steps times")
     return p.parse_args()
@@ -94,10 +102,11 @@ def calibrate_copy(mb, steps):
                       "GBps_read_plus_write": 2 * n * steps / el / 1e9}), flush=True)
 
 
-def setup(wl, path, scan=None):
+def setup(wl, path, scan=None, sets=1):
     inp = make_inputs(wl)
     dev = torch.device("cuda")
-    q, k, v, g = (inp[n].to(dev) for n in ("q", "k", "v", "g"))
+    # `sets` distinct device copies of the inputs; call i reads copy i % sets
+    copies = [tuple(inp[n].to(dev) for n in ("q", "k", "v", "g")) for _ in range(sets)]
     s0 = None if inp["s0"] is None else inp["s0"].to(dev)
     o = torch.empty((wl.B, wl.heads, wl.L, wl.dv), dtype=torch_dtype(wl.odtype), device=dev)
     sf = torch.empty((wl.B, wl.heads, wl.dk, wl.dv), dtype=torch.float32, device=dev) if wl.want_final else None
@@ -105,6 +114,7 @@ def setup(wl, path, scan=None):
     scans = [scan] if scan else list(wl.scans)
 
     def step(i=0):
+        q, k, v, g = copies[i % sets]
         gtr.gtr_gla_fwd(q, k, v, g, H=wl.H, W=wl.W, scale=wl.scale, chunk=wl.chunk, scan=scans[i % len(scans)],
                         s0=s0, out=o, s_final=sf, path=path, workspace=ws)
 
@@ -202,6 +212,13 @@ def main():
                      "kernel_source_hash": kernel_source_hash(),
                      "mfma_frac": flops / per_call / 1e12 / MFMA_F16_PEAK_TFLOPS},
     }
+    if a.cold_sets > 1:
+        st = setup(wl, a.path, scan=wl.scans[0], sets=a.cold_sets)
+        cs = time_graph(st, a.steps, a.warmup) / a.steps
+        out["cold"] = {"sets": a.cold_sets, "set_bytes": nbytes - wl.B * wl.heads * wl.L * wl.dv *
+                       torch.tensor([], dtype=torch_dtype(wl.odtype)).element_size(),
+                       "us_per_call": cs * 1e6, "tokens_per_s": wl.B * wl.L / cs,
+                       "achieved_GBps": nbytes / cs / 1e9, "frac": nbytes / cs / 1e9 / HBM_PEAK_GBS}
     if a.detail:
         det = {}
         for name in ("directions", "highres", "batched"):

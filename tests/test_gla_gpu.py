@@ -248,8 +248,10 @@ def test_workspace_reuse_and_no_fault(gtr):
         assert gtr.gtr_gla_workspace_fault(ws.buf) == 0
         results.append(o)
     assert torch.equal(results[0], results[2])
-    # the synchronisation words are back to zero after each call
-    assert int(ws.buf[256:256 + 4 * 96 * 4].view(torch.int32).abs().sum()) == 0
+    # the per-sequence counters (4 words per sequence after the 256-byte
+    # header) are back to zero after each call
+    n_seq = WORKLOADS["kbench"].B * WORKLOADS["kbench"].heads
+    assert int(ws.buf[256:256 + 16 * n_seq].view(torch.int32).abs().sum()) == 0
 
 
 def test_paths_agree(gtr):
