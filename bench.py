@@ -74,7 +74,7 @@ def parse():
     p.add_argument("--steps", type=int, default=500)
     p.add_argument("--warmup", type=int, default=50)
     p.add_argument("--workload", default="kbench", choices=sorted(WORKLOADS))
-    p.add_argument("--path", default="auto", choices=["auto", "fused", "staged"])
+    p.add_argument("--path", default="auto", choices=["auto", "fused", "staged", "inline"])
     p.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     p.add_argument("--cpu-seconds", type=float, default=10.0)
     p.add_argument("--detail", action="store_true", help="also time the other workloads")

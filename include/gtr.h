@@ -83,11 +83,16 @@ gtr_status gtr_scan_permute(const void* src, void* dst, int64_t outer, int32_t H
                             int64_t row_elems, gtr_dtype dt, gtr_scan dir, int32_t inverse,
                             hipStream_t stream);
 
-/* Execution schedule of gtr_gla_fwd (all give the same result up to rounding). */
+/* Execution schedule of gtr_gla_fwd (all give the same result up to rounding;
+ * the length-aware dispatch of the paper's operator appendix). */
 typedef enum {
-  GTR_PATH_AUTO = 0,   /* the library picks                                          */
-  GTR_PATH_FUSED = 1,  /* one launch: summaries, boundary-state scan and outputs     */
-  GTR_PATH_STAGED = 2  /* three launches: summaries, boundary-state scan, outputs    */
+  GTR_PATH_AUTO = 0,   /* the library picks by the number of chunks per sequence       */
+  GTR_PATH_FUSED = 1,  /* one launch: summaries, boundary-state scan split over the
+                          work-groups of a sequence, outputs                          */
+  GTR_PATH_STAGED = 2, /* three launches: summaries, boundary-state scan, outputs      */
+  GTR_PATH_INLINE = 3  /* one launch: summaries, then every chunk rebuilds its own
+                          boundary state from the summaries before it (short
+                          sequences)                                                  */
 } gtr_path;
 
 /*

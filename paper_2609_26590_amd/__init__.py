@@ -29,7 +29,7 @@ LIB_PATH = os.path.join(_PKG, "libgtr.so")
 
 F32, F16, BF16 = 0, 1, 2
 SCANS = {"row": 0, "col": 1, "row_rev": 2, "col_rev": 3}
-PATHS = {"auto": 0, "fused": 1, "staged": 2}
+PATHS = {"auto": 0, "fused": 1, "staged": 2, "inline": 3}
 STATUS = {0: "GTR_OK", 1: "GTR_ERR_NULL", 2: "GTR_ERR_SHAPE", 3: "GTR_ERR_UNSUPPORTED",
           4: "GTR_ERR_ALIAS", 5: "GTR_ERR_WORKSPACE", 6: "GTR_ERR_HIP"}
 

@@ -31,6 +31,11 @@
 //
 // Schedules:
 //   * staged: summary kernel -> boundary-state scan kernel -> output kernel.
+//   * inline: one launch; each work-group publishes its summary and, once all
+//     summaries of its sequence are in, rebuilds its own boundary state from
+//     the summaries of the chunks before it,
+//       S_[c] = (prod_{m<c} Diag(d_m)) S_0 + sum_{j<c} (prod_{j<m<c} Diag(d_m)) U_j,
+//     which costs c reads of a summary but only one hand-off (short sequences).
 //   * fused : one launch; each work-group owns one (sequence, chunk), publishes
 //     its summary, and the work-groups of one sequence then run the boundary
 //     state scan cooperatively (each takes a slice of the d_k x d_v state) before
@@ -716,11 +721,78 @@ __device__ __forceinline__ void seq_wait(unsigned* ctr, unsigned target, unsigne
   __syncthreads();
 }
 
+// S_[c]^T ([DV][DK]) rebuilt from the summaries and decays of chunks 0..c-1 of
+// one sequence (agent-coherent loads) straight into the shared state tile
+// (STATE), walking the chunks backwards so that the weight of each summary is
+// one more decay factor than the one after it; FINAL also writes
+// S_final = Diag(d_c) S_[c] + U_c for the last chunk. Thread t owns the
+// 16-byte pieces t, t + NT, ...; with NT a multiple of DK / 4 they all share
+// dims i..i+3, so one decay load per chunk serves all of them. No barrier.
+template <int DK, int DV, int NT, typename Sm, typename E, int SP>
+__device__ __forceinline__ void state_inline(const GlaParams& P, Sm& sm, int bh, int c, bool state, bool final) {
+  constexpr int SQ4 = DK * DV / 4;
+  constexpr int SPER = (SQ4 + NT - 1) / NT;
+  static_assert(NT % (DK / 4) == 0, "the pieces of one thread must share their dims");
+  const int NC = P.nchunks;
+  const __amdgpu_buffer_rsrc_t sr = make_rsrc(P.states + (int64_t)bh * NC * (DK * DV), (uint32_t)NC * DK * DV * 4);
+  const __amdgpu_buffer_rsrc_t dr = make_rsrc(P.decays + (int64_t)bh * NC * DK, (uint32_t)NC * DK * 4);
+  const int i0 = (4 * (int)threadIdx.x) % DK;
+  f4 acc[SPER], wgt = {1.f, 1.f, 1.f, 1.f};
+#pragma unroll
+  for (int m = 0; m < SPER; ++m) acc[m] = f4{0.f, 0.f, 0.f, 0.f};
+  constexpr int B = SPER >= 16 ? 1 : 16 / SPER;  // chunks per batch of loads
+  for (int j1 = c; j1 > 0; j1 -= B) {
+    f4 u[B][SPER], d[B];
+#pragma unroll
+    for (int b = 0; b < B; ++b) {
+      const int j = j1 - 1 - b;
+      if (j >= 0) {
+        d[b] = coh_load4(dr, ((uint32_t)j * DK + i0) * 4);
+#pragma unroll
+        for (int m = 0; m < SPER; ++m) {
+          const int q4 = threadIdx.x + m * NT;
+          if (q4 < SQ4) u[b][m] = coh_load4(sr, ((uint32_t)j * (DK * DV) + 4 * q4) * 4);
+        }
+      }
+    }
+#pragma unroll
+    for (int b = 0; b < B; ++b) {
+      const int j = j1 - 1 - b;
+      if (j >= 0) {
+#pragma unroll
+        for (int m = 0; m < SPER; ++m) acc[m] += wgt * u[b][m];
+        wgt *= d[b];
+      }
+    }
+  }
+  const f4 dc = final ? coh_load4(dr, ((uint32_t)c * DK + i0) * 4) : f4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int m = 0; m < SPER; ++m) {
+    const int q4 = threadIdx.x + m * NT;
+    if (q4 < SQ4) {
+      const int dv = (4 * q4) / DK;
+      if (P.s0) {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) acc[m][e] += wgt[e] * P.s0[((int64_t)bh * DK + i0 + e) * DV + dv];
+      }
+      if (state) {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) sm.sT[dv * SP + i0 + e] = (E)acc[m][e];
+      }
+      if (final) {
+        const f4 uc = coh_load4(sr, ((uint32_t)c * (DK * DV) + 4 * q4) * 4);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) P.s_final[((int64_t)bh * DK + i0 + e) * DV + dv] = dc[e] * acc[m][e] + uc[e];
+      }
+    }
+  }
+}
+
 // Work-group -> (sequence, chunk). Work-groups are handed to the 8 XCDs round
 // robin, so block b runs on XCD b % 8; all chunks of a sequence get the same
 // b % 8 and therefore share one L2. Blocks whose sequence index is past the end
 // exit at once.
-template <int DK, int DV, int C, int IN>
+template <int DK, int DV, int C, int IN, bool INLINE>
 __global__ void __launch_bounds__(tile_threads(C)) gla_fused_kernel(GlaParams P) {
   typedef Chunk<DK, DV, C, IN> T;
   __shared__ typename T::Smem sm;
@@ -743,20 +815,31 @@ __global__ void __launch_bounds__(tile_threads(C)) gla_fused_kernel(GlaParams P)
   ch.intra(P, sm, bh, c, O);
 
   seq_wait(&sync[0], (unsigned)NC, P.fault);
-  {
-    const int per = (DK * DV + NC - 1) / NC;
-    const int e0 = min(c * per, DK * DV), e1 = min(e0 + per, DK * DV);
-    scan_coherent<DK, DV>(P, bh, e0, e1, threadIdx.x, T::NT);
-  }
-  seq_arrive(&sync[1]);
-  seq_wait(&sync[1], (unsigned)NC, P.fault);
+  if constexpr (INLINE) {
+    const bool state = c > 0 || P.s0;
+    const bool final = P.s_final && c == NC - 1;
+    if (state || final)
+      state_inline<DK, DV, T::NT, typename T::Smem, typename T::E, T::SP>(P, sm, bh, c, state, final);
+    if (state) {
+      __syncthreads();
+      ch.readout(sm, O);
+    }
+  } else {
+    {
+      const int per = (DK * DV + NC - 1) / NC;
+      const int e0 = min(c * per, DK * DV), e1 = min(e0 + per, DK * DV);
+      scan_coherent<DK, DV>(P, bh, e0, e1, threadIdx.x, T::NT);
+    }
+    seq_arrive(&sync[1]);
+    seq_wait(&sync[1], (unsigned)NC, P.fault);
 
-  if (c > 0 || P.s0) {
-    f4 sbuf[T::SPER];
-    ch.template state_load<true>(P.states + sc * (DK * DV), sbuf);
-    ch.state_store(sm, sbuf);
-    __syncthreads();
-    ch.readout(sm, O);
+    if (c > 0 || P.s0) {
+      f4 sbuf[T::SPER];
+      ch.template state_load<true>(P.states + sc * (DK * DV), sbuf);
+      ch.state_store(sm, sbuf);
+      __syncthreads();
+      ch.readout(sm, O);
+    }
   }
   ch.store(P, sm, bh, c, O);
 
@@ -782,6 +865,7 @@ struct KernelSet {
   const void* summary;
   const void* output;
   const void* fused;
+  const void* inlined;
   const void* scan;
   int threads;
 };
@@ -790,7 +874,8 @@ template <int DK, int DV, int C, int IN>
 static KernelSet kernels_for() {
   return KernelSet{reinterpret_cast<const void*>(&gla_summary_kernel<DK, DV, C, IN>),
                    reinterpret_cast<const void*>(&gla_output_kernel<DK, DV, C, IN>),
-                   reinterpret_cast<const void*>(&gla_fused_kernel<DK, DV, C, IN>),
+                   reinterpret_cast<const void*>(&gla_fused_kernel<DK, DV, C, IN, false>),
+                   reinterpret_cast<const void*>(&gla_fused_kernel<DK, DV, C, IN, true>),
                    reinterpret_cast<const void*>(&gla_scan_kernel<DK, DV>), tile_threads(C)};
 }
 
@@ -820,6 +905,9 @@ static bool select_kernels(const GlaShape& s, KernelSet* ks) {
     default: return false;
   }
 }
+
+// AUTO takes the inline schedule up to this many chunks per sequence.
+constexpr int64_t kInlineMaxChunks = 8;
 
 // Largest number of work-groups of one sequence that can be resident on one XCD
 // at once (8 XCDs per device); cached per (device, kernel).
@@ -914,19 +1002,25 @@ extern "C" gtr_status gtr_gla_fwd(const gtr_gla_args* a, hipStream_t stream) {
   P.decays = reinterpret_cast<float*>(ws + lay.decays_off);
   P.groups = (int)((s.BH + 7) / 8);
 
-  bool fused = false;
-  if (a->path == GTR_PATH_FUSED || a->path == GTR_PATH_AUTO) {
-    const int cap = fused_capacity_per_xcd(ks.fused, ks.threads);
+  // Length-aware dispatch: short sequences rebuild each boundary state from the
+  // summaries (one hand-off), longer ones split the scan over their chunks'
+  // work-groups (two hand-offs), and sequences whose chunks cannot all be
+  // resident at once on one XCD take the three-launch schedule.
+  const void* one_launch = nullptr;
+  if (a->path != GTR_PATH_STAGED) {
+    const bool inl = a->path == GTR_PATH_INLINE || (a->path == GTR_PATH_AUTO && s.nchunks <= kInlineMaxChunks);
+    const void* k = inl ? ks.inlined : ks.fused;
+    const int cap = fused_capacity_per_xcd(k, ks.threads);
     const bool fits = cap > 0 && s.nchunks <= cap && s.nchunks <= kFusedMaxChunks;
-    if (a->path == GTR_PATH_FUSED && !fits) return GTR_ERR_UNSUPPORTED;
-    fused = fits;
+    if (a->path != GTR_PATH_AUTO && !fits) return GTR_ERR_UNSUPPORTED;
+    if (fits) one_launch = k;
   }
 
   void* kargs[] = {&P};
   hipError_t err;
-  if (fused) {
+  if (one_launch) {
     const int64_t blocks = (int64_t)8 * P.groups * s.nchunks;
-    err = hipLaunchKernel(ks.fused, dim3((unsigned)blocks), dim3(ks.threads), kargs, 0, stream);
+    err = hipLaunchKernel(one_launch, dim3((unsigned)blocks), dim3(ks.threads), kargs, 0, stream);
   } else {
     err = hipLaunchKernel(ks.summary, dim3((unsigned)s.nchunks, (unsigned)s.BH), dim3(ks.threads), kargs, 0, stream);
     if (err == hipSuccess) {

@@ -36,7 +36,7 @@ gtr_status gla_shape_from_args(const gtr_gla_args* a, GlaShape* s, bool check_po
   if (a->g_dtype != q && a->g_dtype != GTR_F32) return GTR_ERR_UNSUPPORTED;
   if (a->o_dtype != q && a->o_dtype != GTR_F32) return GTR_ERR_UNSUPPORTED;
   if (a->scan < GTR_SCAN_ROW || a->scan > GTR_SCAN_COL_REV) return GTR_ERR_UNSUPPORTED;
-  if (a->path < GTR_PATH_AUTO || a->path > GTR_PATH_STAGED) return GTR_ERR_UNSUPPORTED;
+  if (a->path < GTR_PATH_AUTO || a->path > GTR_PATH_INLINE) return GTR_ERR_UNSUPPORTED;
 
   int64_t BH, L, n;
   if (!mul_ok(a->B, a->heads, &BH) || !mul_ok(a->H, a->W, &L)) return GTR_ERR_SHAPE;
