@@ -39,11 +39,12 @@ __device__ __forceinline__ float bf16_bits_to_f32(unsigned short b) {
 }
 
 __device__ __forceinline__ unsigned short f32_to_bf16_bits(float f) {
-  // round to nearest even; NaN stays NaN
-  uint32_t u = __builtin_bit_cast(uint32_t, f);
-  if ((u & 0x7f800000u) == 0x7f800000u && (u & 0x7fffffu)) return (unsigned short)((u >> 16) | 0x40);
-  u += 0x7fffu + ((u >> 16) & 1u);
-  return (unsigned short)(u >> 16);
+  // round to nearest even; a NaN stays a (quiet) NaN. Branch-free: a select,
+  // not a divergent branch per element.
+  const uint32_t u = __builtin_bit_cast(uint32_t, f);
+  const uint32_t rne = (u + 0x7fffu + ((u >> 16) & 1u)) >> 16;
+  const uint32_t nan = (u >> 16) | 0x40u;
+  return (unsigned short)((u & 0x7fffffffu) > 0x7f800000u ? nan : rne);
 }
 
 // Load 8 consecutive elements starting at element offset `off` of a tensor of

@@ -1,0 +1,238 @@
+"""CPU check of the generated gfx950 code: every memory address that the GLA
+kernels form is defined for every active lane and lies inside its buffer.
+
+The kernels are compiled to gfx950 assembly with the library's own flags and
+executed wave by wave in ``gfx950_wave`` (an emulator of our own listing, run
+on the CPU). This guards against a class of defect that source-level review
+cannot see: the compiler once produced, for the bf16 instantiation only, a
+global address from a register pair that was written on the fp16 and float32
+paths but not on the bf16 one (for the lanes that used it). The first test pins
+that the emulator reports exactly that pattern.
+"""
+from __future__ import annotations
+
+import hashlib
+import os
+import shutil
+import struct
+import subprocess
+
+import pytest
+
+import gfx950_wave as emu
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+CSRC = os.path.join(ROOT, "paper_2609_26590_amd", "csrc")
+BUILD = os.path.join(ROOT, "paper_2609_26590_amd", "_build")
+
+# ---------------------------------------------------------------------------
+# the emulator catches the defect class (a hand-written kernel)
+# ---------------------------------------------------------------------------
+SNIPPET = """
+{name}:
+	s_load_dwordx2 s[4:5], s[0:1], 0x0
+	{pre}
+	v_cmp_gt_u32_e32 vcc, 32, v0
+	s_and_saveexec_b64 s[6:7], vcc
+	v_mov_b32_e32 v2, v0
+	v_mov_b32_e32 v3, 0
+	s_or_b64 exec, exec, s[6:7]
+	s_waitcnt lgkmcnt(0)
+	v_lshl_add_u64 v[2:3], v[2:3], 2, s[4:5]
+	global_load_dword v4, v[2:3], off
+	s_endpgm
+.Lfunc_end0:
+	.amdhsa_kernel {name}
+		.amdhsa_group_segment_fixed_size 0
+		.amdhsa_private_segment_fixed_size 0
+		.amdhsa_kernarg_size 8
+		.amdhsa_user_sgpr_count 2
+		.amdhsa_user_sgpr_kernarg_segment_ptr 1
+		.amdhsa_system_sgpr_workgroup_id_x 1
+	.end_amdhsa_kernel
+"""
+
+
+def run_snippet(pre: str) -> emu.Report:
+    name = "_Zsnippet"
+    text = "\n" + SNIPPET.format(name=name, pre=pre)
+    prog, labels, desc = emu.parse_kernel(text, name)
+    base = 0x1000_0000_0000
+    regions = [emu.Region("buf", base, 64 * 4, "r"), emu.Region("kernarg", emu.KERNARG_BASE, 8, "r")]
+    rep = emu.Report()
+    emu.run_wave(prog, labels, desc, struct.pack("<Q", base), regions, 0, (0, 0, 0), 0, rep)
+    return rep
+
+
+def test_emulator_flags_address_from_lanes_left_unwritten():
+    # v[2:3] is written under the mask of lanes 0..31 only, then all 64 lanes
+    # use it as an address: lanes 32..63 read whatever an earlier wave left
+    rep = run_snippet("s_nop 0")
+    assert rep.counts.get("ERR-UNDEF-ADDR", 0) == 1
+    (_, raw, detail), = rep.items["ERR-UNDEF-ADDR"]
+    assert raw.startswith("global_load_dword") and "32" in detail
+
+
+def test_emulator_passes_the_same_code_with_every_lane_written():
+    rep = run_snippet("v_mov_b32_e32 v2, v0\n\tv_mov_b32_e32 v3, 0")
+    assert not [k for k in rep.counts if k.startswith("ERR")], dict(rep.counts)
+
+
+def test_emulator_flags_out_of_bounds():
+    # every lane writes its address (word tid + 1), lane 63 lands one word past
+    # the 64-word buffer; v0 = 64 leaves the masked block with no lanes
+    rep = run_snippet("v_add_u32_e32 v2, 1, v0\n\tv_mov_b32_e32 v3, 0\n\tv_mov_b32_e32 v0, 64")
+    assert rep.counts.get("ERR-OOB", 0) >= 1
+
+
+# ---------------------------------------------------------------------------
+# the library's kernels
+# ---------------------------------------------------------------------------
+DT = {"f32": (0, 4), "f16": (1, 2), "bf16": (2, 2)}
+SCAN = {"row": 0, "col": 1, "row_rev": 2, "col_rev": 3}
+KERNARG_BYTES = 144  # sizeof(GlaParams)
+
+
+def a256(x):
+    return (x + 255) & ~255
+
+
+def device_asm() -> str:
+    """gfx950 assembly of gla_fwd.hip with the library's flags (cached by source hash)."""
+    from paper_2609_26590_amd import build as b
+    h = hashlib.sha256()
+    for f in sorted(os.listdir(CSRC)):
+        with open(os.path.join(CSRC, f), "rb") as fh:
+            h.update(f.encode() + fh.read())
+    with open(os.path.join(ROOT, "include", "gtr.h"), "rb") as fh:
+        h.update(fh.read())
+    h.update(" ".join(b.HIPCC_FLAGS).encode())
+    os.makedirs(BUILD, exist_ok=True)
+    path = os.path.join(BUILD, f"gla_fwd.gfx950.{h.hexdigest()[:16]}.s")
+    if not os.path.exists(path):
+        hipcc = b._hipcc() if shutil.which("hipcc") or os.path.exists("/opt/rocm/bin/hipcc") else None
+        if hipcc is None:
+            pytest.skip("hipcc is not available")
+        tmp = path + f".tmp{os.getpid()}"
+        r = subprocess.run([hipcc, *b.HIPCC_FLAGS, "-S", "--cuda-device-only", os.path.join(CSRC, "gla_fwd.hip"),
+                            "-o", tmp], capture_output=True, text=True)
+        assert r.returncode == 0, r.stderr[-2000:]
+        os.replace(tmp, path)
+    with open(path) as fh:
+        return fh.read()
+
+
+class Shape:
+    def __init__(self, B, heads, H, W, dk, dv, chunk, dt, gdt, odt, scan, s0, sfinal):
+        self.B, self.heads, self.H, self.W = B, heads, H, W
+        self.dk, self.dv, self.chunk = dk, dv, chunk
+        self.dt, self.gdt, self.odt, self.scan, self.s0, self.sfinal = dt, gdt, odt, scan, s0, sfinal
+        self.BH = B * heads
+        self.L = H * W
+        self.NC = (self.L + chunk - 1) // chunk
+
+
+def kernel_args(c: Shape):
+    """GlaParams for shape c with every buffer at its own base, and the buffers."""
+    regions = []
+    nxt = [0x1000_0000_0000]
+
+    def alloc(name, size, mode):
+        base = nxt[0]
+        nxt[0] += 0x10_0000_0000
+        if size:
+            regions.append(emu.Region(name, base, size, mode))
+        return base if size else 0
+
+    esz = DT[c.dt][1]
+    q = alloc("q", c.BH * c.L * c.dk * esz, "r")
+    k = alloc("k", c.BH * c.L * c.dk * esz, "r")
+    v = alloc("v", c.BH * c.L * c.dv * esz, "r")
+    g = alloc("g", c.BH * c.L * c.dk * DT[c.gdt][1], "r")
+    o = alloc("o", c.BH * c.L * c.dv * DT[c.odt][1], "w")
+    s0 = alloc("s0", c.BH * c.dk * c.dv * 4, "r") if c.s0 else 0
+    sf = alloc("s_final", c.BH * c.dk * c.dv * 4, "w") if c.sfinal else 0
+    # workspace layout of gla_workspace_layout(): fault word, counters, states, decays
+    sync = 256
+    states = a256(sync + c.BH * 16)
+    decays = a256(states + c.BH * c.NC * c.dk * c.dv * 4)
+    total = a256(decays + c.BH * c.NC * c.dk * 4)
+    ws = alloc("workspace", total, "rw")
+    # hand-off counters read as complete, so every bounded wait ends at once
+    regions.insert(0, emu.Region("sync", ws + sync, c.BH * 16, "rw", load_value=0x7FFFFFFF))
+    regions.insert(0, emu.Region("fault", ws, 256, "rw"))
+    regions.append(emu.Region("kernarg", emu.KERNARG_BASE, KERNARG_BYTES, "r"))
+    kern = struct.pack("<7Q6iqifi4xQQQQi4x", q, k, v, g, o, s0, sf, DT[c.dt][0], DT[c.gdt][0], DT[c.odt][0],
+                       c.BH, c.H, c.W, c.L, c.NC, c.dk ** -0.5, SCAN[c.scan], ws + states, ws + decays,
+                       ws + sync, ws, (c.BH + 7) // 8)
+    assert len(kern) == KERNARG_BYTES
+    return kern, regions
+
+
+def mangled(kind: str, c: Shape) -> str:
+    t = f"ILi{c.dk}ELi{c.dv}ELi{c.chunk}ELi{DT[c.dt][0]}E"
+    if kind == "summary":
+        return f"_ZN3gtr18gla_summary_kernel{t}EEvNS_9GlaParamsE"
+    if kind == "output":
+        return f"_ZN3gtr17gla_output_kernel{t}EEvNS_9GlaParamsE"
+    if kind == "scan":
+        return f"_ZN3gtr15gla_scan_kernelILi{c.dk}ELi{c.dv}EEEvNS_9GlaParamsE"
+    return f"_ZN3gtr16gla_fused_kernel{t}Lb{1 if kind == 'inline' else 0}EEEvNS_9GlaParamsE"
+
+
+def work_groups(kind: str, c: Shape):
+    """First, second and last chunk of the first and last sequence (+ one block
+    of the one-launch grid that has no sequence)."""
+    nw = c.chunk // 16
+    cs = sorted({0, 1 % c.NC, c.NC - 1})
+    bhs = sorted({0, c.BH - 1})
+    if kind in ("summary", "output"):
+        return [((cc, bh, 0), nw) for cc in cs for bh in bhs]
+    if kind == "scan":
+        eb = (c.dk * c.dv + 255) // 256
+        return [((x, bh, 0), 4) for x in sorted({0, eb - 1}) for bh in bhs]
+    picks = {((bh // 8 * c.NC + cc) << 3) | (bh % 8) for bh in bhs for cc in cs}
+    last = (c.BH + 7) // 8 - 1
+    spare = [x for x in range(8) if last * 8 + x >= c.BH]
+    if spare:
+        picks.add(((last * c.NC) << 3) | spare[0])
+    return [((b, 0, 0), nw) for b in sorted(picks)]
+
+
+# (shape, kernels): the bf16 instantiations, float32 gates with 16-bit inputs,
+# every chunk size, reversed and column scans, S0 / S_final, partial chunks
+CHECKS = [
+    (Shape(1, 12, 40, 40, 64, 64, 64, "bf16", "bf16", "f32", "row", False, False),
+     ("summary", "scan", "output", "fused", "inline")),
+    (Shape(8, 12, 40, 40, 64, 64, 64, "bf16", "bf16", "f32", "col_rev", True, True), ("output", "fused", "inline")),
+    (Shape(2, 9, 12, 20, 32, 32, 32, "bf16", "f32", "f32", "col", True, True), ("summary", "output", "fused")),
+    (Shape(1, 2, 20, 20, 32, 64, 128, "bf16", "bf16", "bf16", "row_rev", False, False), ("output", "fused")),
+    (Shape(1, 6, 40, 40, 64, 64, 64, "f16", "f16", "f16", "row", False, False), ("fused",)),
+    (Shape(1, 3, 7, 9, 64, 64, 128, "f16", "f32", "f32", "col", True, True), ("output", "inline")),
+    (Shape(1, 2, 13, 11, 32, 32, 32, "f32", "f32", "f32", "row", False, True), ("summary", "output", "fused")),
+]
+
+
+@pytest.fixture(scope="module")
+def asm_text():
+    return device_asm()
+
+
+@pytest.mark.parametrize("case", range(len(CHECKS)))
+def test_gla_kernel_addresses(asm_text, case):
+    c, kinds = CHECKS[case]
+    names = set(emu.kernel_names(asm_text))
+    kern, regions = kernel_args(c)
+    for kind in kinds:
+        name = mangled(kind, c)
+        assert name in names, f"no kernel {name} in the listing"
+        prog, labels, desc = emu.parse_kernel(asm_text, name)
+        assert desc["amdhsa_kernarg_size"] == KERNARG_BYTES
+        rep = emu.Report()
+        for wg, nw in work_groups(kind, c):
+            for wave in range(nw):
+                emu.run_wave(prog, labels, desc, kern, regions, desc["amdhsa_group_segment_fixed_size"], wg,
+                             wave, rep)
+        bad = {k: sorted(v)[:4] for k, v in rep.items.items() if k.startswith(("ERR", "WARN", "NOTIMPL"))}
+        assert not bad, f"{kind}: {bad}"
+        assert "INFO-PATHLIMIT" not in rep.counts, f"{kind}: not every branch outcome was explored"

@@ -43,30 +43,6 @@ def _reference(wl: Workload, scan: str):
     return o, sf
 
 
-# Cases held off the GPU. The first runs of the 12-sequence bf16 workload (bf16
-# in, float32 out, 300-400 work-groups per launch) ended in a GPU
-# memory-aperture fault whose cause has not been shown. Until it is, only cases
-# inside the envelope that has run clean are sent to the GPU: fp16 in and out,
-# or float32 in and out, with at most 200 work-groups per GLA launch.
-MAX_CLEAN_WORKGROUPS = 200
-HELD = ("held off the GPU: outside the envelope that has run clean (fp16->fp16 or f32->f32, "
-        "<= 200 work-groups per launch) while the memory fault seen on the 12-sequence bf16 "
-        "workload is unexplained")
-
-
-def held(B, heads, L, chunk, dtype, gdtype, odtype) -> bool:
-    nc = (L + chunk - 1) // chunk
-    staged = B * heads * nc
-    fused = 8 * ((B * heads + 7) // 8) * nc  # the fused grid rounds sequences up to 8 XCD lanes
-    return (dtype != odtype or gdtype != dtype or dtype == "bf16"
-            or max(staged, fused) > MAX_CLEAN_WORKGROUPS)
-
-
-def skip_if_held(*a):
-    if held(*a):
-        pytest.skip(HELD)
-
-
 ONE_LAUNCH_UNFIT = ("a single-launch schedule needs every chunk of a sequence resident on one XCD at "
                     "once; the library reports GTR_ERR_UNSUPPORTED for this shape")
 
@@ -107,7 +83,6 @@ for name, wl in WORKLOADS.items():
 @pytest.mark.parametrize("name,scan,chunk", CASES)
 def test_workload_parity(gtr, name, scan, chunk, path):
     wl = WORKLOADS[name]
-    skip_if_held(wl.B, wl.heads, wl.L, chunk, wl.dtype, wl.dtype, wl.odtype)
     o_ref, sf_ref = _reference(wl, scan)
     o, sf = run_gpu(gtr, wl, scan, chunk, path)
     tol = tol_for(wl.dtype, wl.odtype)
@@ -148,7 +123,6 @@ def edge_workload(B, heads, H, W, dk, dv, chunk, dtype, gdtype, odtype, scan, s0
 @pytest.mark.parametrize("case", range(len(EDGE)))
 def test_edge_parity(gtr, case, path):
     B, heads, H, W, dk, dv, chunk, dtype, gdtype, odtype, scan, s0, final = EDGE[case]
-    skip_if_held(B, heads, H * W, chunk, dtype, gdtype, odtype)
     wl = edge_workload(B, heads, H, W, dk, dv, chunk, dtype, gdtype, odtype, scan, s0, final, 1000 + case)
     inp = make_inputs(wl)
     if gdtype != dtype:  # g in float32, drawn from the same values
@@ -204,7 +178,6 @@ def test_gate_extremes(gtr, mode, dtype, path):
 
 def test_canaries_and_inputs_untouched(gtr):
     wl = WORKLOADS["batched"].with_(B=2, H=17, W=9, dtype="f16", odtype="f16")
-    skip_if_held(wl.B, wl.heads, wl.L, wl.chunk, wl.dtype, wl.dtype, wl.odtype)
     inp = make_inputs(wl)
     dev = torch.device("cuda")
     q, k, v, g = (inp[n].to(dev) for n in ("q", "k", "v", "g"))
@@ -256,7 +229,6 @@ def test_workspace_reuse_and_no_fault(gtr):
 
 def test_paths_agree(gtr):
     wl = WORKLOADS["directions"]
-    skip_if_held(wl.B, wl.heads, wl.L, wl.chunk, wl.dtype, wl.dtype, wl.odtype)
     for scan in wl.scans:
         a, _ = run_gpu(gtr, wl, scan, 64, "fused")
         b, _ = run_gpu(gtr, wl, scan, 64, "staged")
@@ -267,7 +239,6 @@ def test_paths_agree(gtr):
 def test_graph_replays_match_eager(gtr):
     """Captured calls replay correctly, several times, with eager work in between."""
     wl = WORKLOADS["batched"].with_(B=1, heads=6, dtype="f16", odtype="f16")
-    skip_if_held(wl.B, wl.heads, wl.L, wl.chunk, wl.dtype, wl.dtype, wl.odtype)
     inp = make_inputs(wl)
     dev = torch.device("cuda")
     q, k, v, g = (inp[n].to(dev) for n in ("q", "k", "v", "g"))
