@@ -176,6 +176,10 @@ struct Chunk {
   typedef typename Op<F16>::frag8 F8;
   typedef typename Op<F16>::frag4 F4;
 
+  // Shared memory of the one-launch schedules (every part). The staged
+  // kernels use the subsets below, so that more of their work-groups fit on a
+  // CU at once: the summary kernel has no k rows, state or diagonal staging,
+  // the output kernel no k-hat tile.
   struct Smem {
     float buf[C * BUFW];   // k*exp(T-a) rows [C][KP]; later the output tile [C][OP]
     E kT[DK * TP];         // (k * exp(A_last - A_r))^T  [DK][TP]
@@ -185,6 +189,22 @@ struct Chunk {
     float G0[NW][DK];      // g at the first token of each sub-chunk
     float F[NW][NF][DK];   // per-wave factor table (rows kFq, kFk, kFh, kFoff + J)
     float Pt[NW][16][17];  // exact diagonal blocks, P^T staging
+  };
+  struct SmemSummary {
+    E kT[DK * TP];
+    E vT[DV * TP];
+    float T[NW][DK];
+    float G0[NW][DK];
+    float F[NW][NF][DK];
+  };
+  struct SmemOutput {
+    float buf[C * BUFW];
+    E vT[DV * TP];
+    E sT[DV * SP];
+    float T[NW][DK];
+    float G0[NW][DK];
+    float F[NW][NF][DK];
+    float Pt[NW][16][17];
   };
   // rows of the factor table of sub-chunk R, per dimension d:
   static constexpr int kFq = 0;    // exp(A before R + g0_R): q readout factor
@@ -220,8 +240,8 @@ struct Chunk {
 
   // Loads and per-token work. Writes v^T, the sub-chunk totals and (ROWS) the
   // k*exp(T-a) rows. Ends with a barrier.
-  template <bool ROWS>
-  __device__ __forceinline__ void load(const GlaParams& P, Smem& sm, int bh, int c) {
+  template <bool ROWS, class S>
+  __device__ __forceinline__ void load(const GlaParams& P, S& sm, int bh, int c) {
     lanes();
     bool valid;
     const int64_t t = token(P, (int64_t)c * C + r, valid);
@@ -293,7 +313,8 @@ struct Chunk {
   }
 
   // This lane's 8 consecutive dims of factor-table row `row`, for K-step s.
-  __device__ __forceinline__ void frow(const Smem& sm, int row, int s, float (&x)[8]) const {
+  template <class S>
+  __device__ __forceinline__ void frow(const S& sm, int row, int s, float (&x)[8]) const {
     const f4 lo = *reinterpret_cast<const f4*>(&sm.F[w][row][32 * s + 8 * gq]);
     const f4 hi = *reinterpret_cast<const f4*>(&sm.F[w][row][32 * s + 8 * gq + 4]);
 #pragma unroll
@@ -308,8 +329,8 @@ struct Chunk {
   // wave then reads back what its lanes need. READOUT: qt = q exp(A_r).
   // SUMMARY: the transposed k-hat tile and d_c (written by wave 0 through
   // `dec`, coherent or plain), followed by a barrier.
-  template <bool READOUT, bool SUMMARY, bool COH>
-  __device__ __forceinline__ void factors(Smem& sm, float* dec) {
+  template <bool READOUT, bool SUMMARY, bool COH, class S>
+  __device__ __forceinline__ void factors(S& sm, float* dec) {
     if (lane < DK) {
       const int d = lane;
       float tK[NW];
@@ -360,8 +381,8 @@ struct Chunk {
   }
 
   // U_c as U^T ([DV][DK] fp32) to `U`, coherent or plain.
-  template <bool COH>
-  __device__ __forceinline__ void summary_out(const Smem& sm, float* U) {
+  template <bool COH, class S>
+  __device__ __forceinline__ void summary_out(const S& sm, float* U) {
     constexpr int NTI = (DK / 16) * (DV / 16);
     const __amdgpu_buffer_rsrc_t ur = make_rsrc(U, DK * DV * 4);
     for (int tau = w; tau < NTI; tau += NW) {
@@ -433,7 +454,8 @@ struct Chunk {
 
   // Intra-chunk part: o_r = sum_{j<=r} P[r][j] v_j for this wave's 16 rows.
   // Needs the k rows written by load<true>().
-  __device__ __forceinline__ void intra(const GlaParams& P, Smem& sm, int bh, int c, f4 (&O)[DV / 16]) {
+  template <class S>
+  __device__ __forceinline__ void intra(const GlaParams& P, S& sm, int bh, int c, f4 (&O)[DV / 16]) {
     f4 PT[NW];
     F8 qhf[KS];
 #pragma unroll
@@ -537,7 +559,8 @@ struct Chunk {
       }
     }
   }
-  __device__ __forceinline__ void state_store(Smem& sm, const f4 (&buf)[SPER]) {
+  template <class S>
+  __device__ __forceinline__ void state_store(S& sm, const f4 (&buf)[SPER]) {
 #pragma unroll
     for (int m = 0; m < SPER; ++m) {
       const int q4 = threadIdx.x + m * NT;  // piece index in [DV][DK]
@@ -550,7 +573,8 @@ struct Chunk {
   }
 
   // o_r += (q_r exp(A_r)) S_[c]. Reads the shared state tile.
-  __device__ __forceinline__ void readout(const Smem& sm, f4 (&O)[DV / 16]) {
+  template <class S>
+  __device__ __forceinline__ void readout(const S& sm, f4 (&O)[DV / 16]) {
     F8 qtf[KS];
 #pragma unroll
     for (int s = 0; s < KS; ++s) qtf[s] = Op<F16>::pack8(qt[s]);
@@ -564,7 +588,8 @@ struct Chunk {
   }
 
   // Stage the output tile through LDS and write whole rows back in spatial order.
-  __device__ __forceinline__ void store(const GlaParams& P, Smem& sm, int bh, int c, const f4 (&O)[DV / 16]) {
+  template <class S>
+  __device__ __forceinline__ void store(const GlaParams& P, S& sm, int bh, int c, const f4 (&O)[DV / 16]) {
     __syncthreads();  // all waves are done with the k rows in buf
 #pragma unroll
     for (int jb = 0; jb < DV / 16; ++jb)
@@ -657,7 +682,7 @@ __device__ __forceinline__ void scan_coherent(const GlaParams& P, int bh, int e0
 template <int DK, int DV, int C, int IN>
 __global__ void __launch_bounds__(tile_threads(C)) gla_summary_kernel(GlaParams P) {
   typedef Chunk<DK, DV, C, IN> T;
-  __shared__ typename T::Smem sm;
+  __shared__ typename T::SmemSummary sm;
   T ch;
   const int c = blockIdx.x, bh = blockIdx.y;
   const int64_t sc = (int64_t)bh * P.nchunks + c;
@@ -677,7 +702,7 @@ __global__ void __launch_bounds__(256) gla_scan_kernel(GlaParams P) {
 template <int DK, int DV, int C, int IN>
 __global__ void __launch_bounds__(tile_threads(C)) gla_output_kernel(GlaParams P) {
   typedef Chunk<DK, DV, C, IN> T;
-  __shared__ typename T::Smem sm;
+  __shared__ typename T::SmemOutput sm;
   T ch;
   const int c = blockIdx.x, bh = blockIdx.y;
   const bool have_state = c > 0 || P.s0;
@@ -1004,10 +1029,14 @@ extern "C" gtr_status gtr_gla_fwd(const gtr_gla_args* a, hipStream_t stream) {
 
   // Length-aware dispatch: short sequences rebuild each boundary state from the
   // summaries (one hand-off), longer ones split the scan over their chunks'
-  // work-groups (two hand-offs), and sequences whose chunks cannot all be
-  // resident at once on one XCD take the three-launch schedule.
+  // work-groups (two hand-offs). Both need every chunk of a sequence resident
+  // at once on one XCD, and both lose to the three-launch schedule as soon as
+  // an XCD has to run more than one sequence (more than 8 sequences): then the
+  // sequences compete for the XCD's slots and partly resident ones spin while
+  // they wait for the rest, so AUTO takes the staged schedule there.
   const void* one_launch = nullptr;
-  if (a->path != GTR_PATH_STAGED) {
+  const bool auto_one_launch = a->path == GTR_PATH_AUTO && P.groups == 1;
+  if (a->path == GTR_PATH_FUSED || a->path == GTR_PATH_INLINE || auto_one_launch) {
     const bool inl = a->path == GTR_PATH_INLINE || (a->path == GTR_PATH_AUTO && s.nchunks <= kInlineMaxChunks);
     const void* k = inl ? ks.inlined : ks.fused;
     const int cap = fused_capacity_per_xcd(k, ks.threads);
