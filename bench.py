@@ -221,7 +221,7 @@ def main():
                        "achieved_GBps": nbytes / cs / 1e9, "frac": nbytes / cs / 1e9 / HBM_PEAK_GBS}
     if a.detail:
         det = {}
-        for name in ("directions", "highres", "batched"):
+        for name in ("directions", "highres", "batched", "op256", "op1600", "op16k"):
             w2 = WORKLOADS[name]
             for scan in w2.scans:
                 st = setup(w2, a.path, scan=scan)

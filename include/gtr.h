@@ -86,8 +86,9 @@ gtr_status gtr_scan_permute(const void* src, void* dst, int64_t outer, int32_t H
 /* Execution schedule of gtr_gla_fwd (all give the same result up to rounding;
  * the length-aware dispatch of the paper's operator appendix). */
 typedef enum {
-  GTR_PATH_AUTO = 0,   /* the library picks: up to 8 sequences, INLINE for at most 8
-                          chunks per sequence, else FUSED if every chunk of a sequence
+  GTR_PATH_AUTO = 0,   /* the library picks: up to 8 sequences, INLINE while the
+                          summaries of a sequence hold at most 64K elements
+                          (nchunks * dk * dv), else FUSED if every chunk of a sequence
                           can be resident on one XCD; otherwise (and for more than 8
                           sequences) STAGED                                           */
   GTR_PATH_FUSED = 1,  /* one launch: summaries, boundary-state scan split over the

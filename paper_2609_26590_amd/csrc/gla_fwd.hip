@@ -931,8 +931,12 @@ static bool select_kernels(const GlaShape& s, KernelSet* ks) {
   }
 }
 
-// AUTO takes the inline schedule up to this many chunks per sequence.
-constexpr int64_t kInlineMaxChunks = 8;
+// AUTO takes the inline schedule while the summaries of one sequence hold at
+// most this many elements (nchunks * dk * dv): rebuilding a boundary state reads
+// every summary before it, so the cost grows with their total size
+// (measured: d_k = d_v = 64 at 25 chunks is faster fused, d_k = 32, d_v = 64
+// at 25 chunks faster inline).
+constexpr int64_t kInlineMaxSummaryElems = 65536;
 
 // Largest number of work-groups of one sequence that can be resident on one XCD
 // at once (8 XCDs per device); cached per (device, kernel).
@@ -1037,7 +1041,8 @@ extern "C" gtr_status gtr_gla_fwd(const gtr_gla_args* a, hipStream_t stream) {
   const void* one_launch = nullptr;
   const bool auto_one_launch = a->path == GTR_PATH_AUTO && P.groups == 1;
   if (a->path == GTR_PATH_FUSED || a->path == GTR_PATH_INLINE || auto_one_launch) {
-    const bool inl = a->path == GTR_PATH_INLINE || (a->path == GTR_PATH_AUTO && s.nchunks <= kInlineMaxChunks);
+    const bool inl = a->path == GTR_PATH_INLINE ||
+                     (a->path == GTR_PATH_AUTO && s.nchunks * s.dk * s.dv <= kInlineMaxSummaryElems);
     const void* k = inl ? ks.inlined : ks.fused;
     const int cap = fused_capacity_per_xcd(k, ks.threads);
     const bool fits = cap > 0 && s.nchunks <= cap && s.nchunks <= kFusedMaxChunks;

@@ -74,9 +74,10 @@ class Workload:
         return replace(self, **kw)
 
 
-# The five workload shapes. ``tiny`` is small enough for the oracle to finish in
-# well under a second; ``kbench`` is the paper's operator-benchmark shape
-# (40x40 tokens, head width 64, fp16 inputs, chunk 64).
+# The workload shapes. ``tiny`` is small enough for the oracle to finish in
+# well under a second; ``kbench`` is the 40x40-token operator benchmark with head
+# width 64 (fp16 inputs, chunk 64); ``op*`` are the paper's own operator shape
+# (d_k = 32, d_v = 64) at its three benchmark lengths.
 WORKLOADS = {
     "tiny": Workload("tiny", B=1, heads=2, H=16, W=16, dk=32, dv=32, dtype="f32", odtype="f32",
                      gate_mu=2.0, gate_std=1.0, qk_std=32 ** -0.5, v_std=32 ** -0.5,
@@ -92,6 +93,14 @@ WORKLOADS = {
     "batched": Workload("batched", B=8, heads=12, H=40, W=40, dk=64, dv=64, dtype="bf16", odtype="f32",
                         gate_mu=2.0, gate_std=2.0, qk_std=1 / 8, v_std=1.0, s0_std=0.1,
                         want_final=True, chunk=64, seed=5),
+    # the paper's own operator shape (its operator appendix): d_k = 32, d_v = 64,
+    # 6 heads, fp16, C = 64, at 256, 1.6K and 16.4K tokens (16x16, 40x40, 128x128)
+    "op256": Workload("op256", B=1, heads=6, H=16, W=16, dk=32, dv=64, dtype="f16", odtype="f16",
+                      gate_mu=3.0, gate_std=1.0, qk_std=1 / 8, v_std=1.0, chunk=64, seed=6),
+    "op1600": Workload("op1600", B=1, heads=6, H=40, W=40, dk=32, dv=64, dtype="f16", odtype="f16",
+                       gate_mu=3.0, gate_std=1.0, qk_std=1 / 8, v_std=1.0, chunk=64, seed=7),
+    "op16k": Workload("op16k", B=1, heads=6, H=128, W=128, dk=32, dv=64, dtype="f16", odtype="f16",
+                      gate_mu=3.0, gate_std=1.0, qk_std=1 / 8, v_std=1.0, chunk=64, seed=8),
 }
 
 

@@ -210,6 +210,8 @@ CHECKS = [
     (Shape(1, 6, 40, 40, 64, 64, 64, "f16", "f16", "f16", "row", False, False), ("fused",)),
     (Shape(1, 3, 7, 9, 64, 64, 128, "f16", "f32", "f32", "col", True, True), ("output", "inline")),
     (Shape(1, 2, 13, 11, 32, 32, 32, "f32", "f32", "f32", "row", False, True), ("summary", "output", "fused")),
+    (Shape(1, 6, 128, 128, 32, 64, 64, "f16", "f16", "f16", "row", False, False),
+     ("summary", "scan", "output", "fused", "inline")),
 ]
 
 
