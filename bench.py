@@ -102,9 +102,20 @@ def calibrate_copy(mb, steps):
                       "GBps_read_plus_write": 2 * n * steps / el / 1e9}), flush=True)
 
 
-def setup(wl, path, scan=None, sets=1):
+def setup(wl, path, scan=None, sets=1, fusions=False):
+    """One call of the workload; ``fusions``: g holds gate logits (tau = 16) and
+    the output-gate epilogue (fp16/bf16 gate in the input dtype, RMSNorm weight)
+    is fused into the store."""
     inp = make_inputs(wl)
     dev = torch.device("cuda")
+    extra = {}
+    if fusions:
+        rng = torch.Generator().manual_seed(wl.seed)
+        inp["g"] = (torch.randn(inp["g"].shape, generator=rng) * 2.0).to(torch_dtype(wl.dtype))
+        extra = dict(gate_tau=16.0,
+                     out_gate=torch.randn((wl.B, wl.heads, wl.L, wl.dv), generator=rng).to(
+                         torch_dtype(wl.dtype)).to(dev),
+                     norm_weight=torch.rand(wl.dv, generator=rng).to(dev) + 0.5)
     # `sets` distinct device copies of the inputs; call i reads copy i % sets
     copies = [tuple(inp[n].to(dev) for n in ("q", "k", "v", "g")) for _ in range(sets)]
     s0 = None if inp["s0"] is None else inp["s0"].to(dev)
@@ -116,7 +127,7 @@ def setup(wl, path, scan=None, sets=1):
     def step(i=0):
         q, k, v, g = copies[i % sets]
         gtr.gtr_gla_fwd(q, k, v, g, H=wl.H, W=wl.W, scale=wl.scale, chunk=wl.chunk, scan=scans[i % len(scans)],
-                        s0=s0, out=o, s_final=sf, path=path, workspace=ws)
+                        s0=s0, out=o, s_final=sf, path=path, workspace=ws, **extra)
 
     step()  # sizes and zero-fills the workspace outside any capture
     torch.cuda.synchronize()
@@ -230,6 +241,15 @@ def main():
                                          "tokens_per_s": w2.B * w2.L / s2,
                                          "GBps": algorithmic_bytes(w2) / s2 / 1e9,
                                          "hbm_frac": algorithmic_bytes(w2) / s2 / 1e9 / HBM_PEAK_GBS}
+        # the same call with gate fusion and the output-gate epilogue (+ the gate input's bytes)
+        for name in ("kbench", "op1600", "batched"):
+            w2 = WORKLOADS[name]
+            st = setup(w2, a.path, scan=w2.scans[0], fusions=True)
+            s2 = time_graph(st, 100, 10) / 100
+            b2 = algorithmic_bytes(w2) + w2.B * w2.heads * w2.L * w2.dv * \
+                torch.tensor([], dtype=torch_dtype(w2.dtype)).element_size() + w2.dv * 4
+            det[f"{name}+fusions"] = {"us_per_call": s2 * 1e6, "tokens_per_s": w2.B * w2.L / s2,
+                                      "GBps": b2 / s2 / 1e9, "hbm_frac": b2 / s2 / 1e9 / HBM_PEAK_GBS}
         out["detail"] = det
     if not a.no_cpu:
         out["cpu_baseline"] = cpu_baseline(wl, a.cpu_seconds)

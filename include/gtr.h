@@ -83,6 +83,15 @@ gtr_status gtr_scan_permute(const void* src, void* dst, int64_t outer, int32_t H
                             int64_t row_elems, gtr_dtype dt, gtr_scan dir, int32_t inverse,
                             hipStream_t stream);
 
+/* What the g input of gtr_gla_fwd holds (Sec. 3.1, "Key-only gated recurrence":
+ * the retention gate is gamma = sigmoid(a)^(1/tau) of a per-token, per-key-dim
+ * logit a). */
+typedef enum {
+  GTR_GATE_LOG_DECAY = 0, /* g = log gamma, finite and <= 0 (the default)                */
+  GTR_GATE_LOGITS = 1     /* g = a, any finite value; the kernels use
+                             log gamma = logsigmoid(a) / gate_tau, in float32           */
+} gtr_gate_kind;
+
 /* Execution schedule of gtr_gla_fwd (all give the same result up to rounding;
  * the length-aware dispatch of the paper's operator appendix). */
 typedef enum {
@@ -118,12 +127,26 @@ typedef enum {
  * scale  : o = scale * q S; the paper's value is dk^{-1/2}.
  * scan   : direction; the permutation is fused into the loads and stores.
  * path   : execution schedule (GTR_PATH_AUTO unless testing a schedule).
+ * g_kind, gate_tau : gate fusion. With GTR_GATE_LOGITS, g holds the logits a
+ *        of the retention gate and log gamma = logsigmoid(a) / gate_tau is
+ *        formed in the kernels' loads (no separate pass over g).
+ * out_gate, out_gate_dtype, norm_eps, norm_weight : output-gate epilogue
+ *        (Sec. 3.1: u_t = SiLU(x_t W_r) * RMSNorm(o_t); the operator appendix
+ *        fuses it into the output kernel). When out_gate is not NULL it holds
+ *        x W_r in SPATIAL order like o, and o receives, per token and head,
+ *          u_j = SiLU(z_j) * o_j / sqrt(mean_i o_i^2 + norm_eps) * w_j,
+ *        mean over the dv channels of that head, o the scaled output above,
+ *        z = out_gate, w = norm_weight (ones if NULL); float32 arithmetic.
+ *        out_gate must not overlap o.
  * workspace, workspace_bytes : device scratch owned by the caller, at least
  *        gtr_gla_workspace_size(args) bytes, 256-byte aligned, and zero-filled
- *        before its first use (gtr_gla_workspace_init). Every completed call
- *        leaves the synchronisation words in it zeroed again, so one workspace
- *        serves any number of calls on one stream. Calls that overlap in time
- *        must not share a workspace.
+ *        before its first use (gtr_gla_workspace_init). The synchronisation
+ *        words of the one-launch schedules sit in a fixed region that no part
+ *        of any call's workspace overlaps, and every completed call leaves them
+ *        zeroed again, so one workspace (large enough for each) serves any
+ *        number of calls of any shapes on one stream. Calls that overlap in
+ *        time must not share a workspace. The one-launch schedules take at
+ *        most 1024 sequences (B * heads).
  *
  * Numerics: float32 accumulation throughout. With fp16/bf16 inputs the matrix
  * products use fp16 operands (every rescaled operand is bounded by |q| or |k|,
@@ -148,6 +171,14 @@ typedef struct {
   gtr_path path;
   void* workspace;
   size_t workspace_bytes;
+  /* Optional fusions; a zero-initialised struct leaves both off. */
+  gtr_gate_kind g_kind;     /* what g holds (gtr_gate_kind)                           */
+  float gate_tau;           /* GTR_GATE_LOGITS: the temperature tau (> 0; paper: 16)  */
+  const void* out_gate;     /* [B, heads, L, dv] output-gate pre-activation x W_r, or
+                               NULL for no epilogue                                   */
+  gtr_dtype out_gate_dtype; /* qkv_dtype or GTR_F32                                   */
+  float norm_eps;           /* RMSNorm epsilon (> 0) of the epilogue                  */
+  const float* norm_weight; /* [dv] RMSNorm weight, or NULL for ones                  */
 } gtr_gla_args;
 
 /* Bytes of workspace gtr_gla_fwd needs for these arguments (host only, no HIP

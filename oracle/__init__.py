@@ -11,6 +11,9 @@ input module, which holds no arithmetic of the method).
 * :func:`permute` - gather / scatter of token rows by that permutation.
 * :func:`gla` - the key-only GLA recurrence (Sec. 3.1), float64, token by token,
   in ``gla_oracle.c``.
+* :func:`log_decay_from_logits` - the retention gate of Sec. 3.1,
+  gamma = sigmoid(a)^(1/tau), as the log-decay g = log gamma the recurrence uses.
+* :func:`output_gate` - the output gate of Sec. 3.1, u = SiLU(x W_r) * RMSNorm(o).
 
 Readings taken where the paper is not explicit (each is listed with its reason
 in the design notes of the repository):
@@ -20,7 +23,10 @@ in the design notes of the repository):
 * column-major visits column 0 top to bottom, then column 1, ...;
 * S0 is applied before the first token in scan order and S_final is the state
   after the last token in scan order;
-* ``scale`` is explicit; the paper's value is d_k^{-1/2}.
+* ``scale`` is explicit; the paper's value is d_k^{-1/2};
+* RMSNorm of the output gate normalises each token of each head over its d_v
+  channels, with an explicit epsilon and an optional per-channel weight (the
+  paper names RMSNorm without its axis or epsilon).
 """
 from __future__ import annotations
 
@@ -140,3 +146,27 @@ def gla(q, k, v, g, s0=None, *, scale: float, H: int, W: int, scan: str = "row",
     if rc != 0:
         raise RuntimeError(f"oracle_gla_forward failed with {rc}")
     return o, sf
+
+
+def log_decay_from_logits(a, tau: float) -> np.ndarray:
+    """g = log gamma for gamma = sigmoid(a)^(1/tau) (Sec. 3.1, retention gate).
+
+    Written as -log(1 + exp(-a)) / tau, with log(1 + exp(-a)) evaluated as
+    logaddexp(0, -a) so that large |a| neither overflows nor loses the value.
+    """
+    a = _f64(a)
+    return -np.logaddexp(0.0, -a) / float(tau)
+
+
+def output_gate(o, z, weight=None, eps: float = 1e-5) -> np.ndarray:
+    """u = SiLU(z) * RMSNorm(o) per token (Sec. 3.1, output gate).
+
+    ``o`` and ``z`` are [..., d_v] (``z`` = x W_r, the gate before its SiLU);
+    RMSNorm(o)_j = o_j / sqrt(mean_i o_i^2 + eps) * w_j over the last axis, with
+    w = ``weight`` (ones if None). SiLU(z) = z * sigmoid(z) = z / (1 + exp(-z)).
+    """
+    o, z = _f64(o), _f64(z)
+    w = np.ones(o.shape[-1]) if weight is None else _f64(weight)
+    rms = np.sqrt(np.mean(o * o, axis=-1, keepdims=True) + float(eps))
+    silu = z / (1.0 + np.exp(-z))
+    return silu * (o / rms) * w

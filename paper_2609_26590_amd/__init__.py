@@ -57,6 +57,9 @@ class GlaArgs(ctypes.Structure):
         ("dk", ctypes.c_int32), ("dv", ctypes.c_int32), ("chunk", ctypes.c_int32),
         ("scale", ctypes.c_float), ("scan", ctypes.c_int), ("path", ctypes.c_int),
         ("workspace", ctypes.c_void_p), ("workspace_bytes", ctypes.c_size_t),
+        ("g_kind", ctypes.c_int), ("gate_tau", ctypes.c_float),
+        ("out_gate", ctypes.c_void_p), ("out_gate_dtype", ctypes.c_int),
+        ("norm_eps", ctypes.c_float), ("norm_weight", ctypes.c_void_p),
     ]
 
 
@@ -120,8 +123,12 @@ def gtr_scan_permute(src: torch.Tensor, H: int, W: int, scan: str, inverse: bool
     return dst
 
 
+GATE_LOG_DECAY, GATE_LOGITS = 0, 1
+
+
 def make_args(q, k, v, g, *, H, W, scale, chunk=64, scan="row", s0=None, o=None, s_final=None,
-              path="auto", workspace=None) -> GlaArgs:
+              path="auto", workspace=None, gate_tau=None, out_gate=None, norm_weight=None,
+              norm_eps=1e-5) -> GlaArgs:
     B, heads, L, dk = q.shape
     a = GlaArgs()
     a.q, a.k, a.v, a.g = _ptr(q), _ptr(k), _ptr(v), _ptr(g)
@@ -137,6 +144,14 @@ def make_args(q, k, v, g, *, H, W, scale, chunk=64, scan="row", s0=None, o=None,
     if workspace is not None:
         a.workspace = workspace.data_ptr()
         a.workspace_bytes = workspace.numel()
+    if gate_tau is not None:  # g holds gate logits: log gamma = logsigmoid(g) / gate_tau
+        a.g_kind = GATE_LOGITS
+        a.gate_tau = float(gate_tau)
+    if out_gate is not None:  # o receives SiLU(out_gate) * RMSNorm(o)
+        a.out_gate = _ptr(out_gate)
+        a.out_gate_dtype = _DT[out_gate.dtype]
+        a.norm_weight = _ptr(norm_weight)
+        a.norm_eps = float(norm_eps)
     return a
 
 
@@ -178,12 +193,20 @@ def gtr_gla_fwd(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, g: torch.Tens
                 s0: Optional[torch.Tensor] = None, want_final: bool = False,
                 o_dtype: Optional[torch.dtype] = None, path: str = "auto",
                 out: Optional[torch.Tensor] = None, s_final: Optional[torch.Tensor] = None,
-                workspace: Optional[Workspace] = None, stream=None):
+                workspace: Optional[Workspace] = None, stream=None, gate_tau: Optional[float] = None,
+                out_gate: Optional[torch.Tensor] = None, norm_weight: Optional[torch.Tensor] = None,
+                norm_eps: float = 1e-5):
     """Chunkwise GLA forward. Inputs [B, heads, H*W, d] in spatial order on the GPU.
 
+    ``gate_tau``: g holds gate logits a, log gamma = logsigmoid(a) / gate_tau.
+    ``out_gate`` ([B, heads, H*W, dv], x W_r) with optional ``norm_weight`` ([dv],
+    float32): the output is u = SiLU(out_gate) * RMSNorm(o) instead of o.
     Returns ``(o, s_final)``; ``s_final`` is None unless requested.
     """
-    for name, t in (("q", q), ("k", k), ("v", v), ("g", g)):
+    extra = [("out_gate", out_gate)] if out_gate is not None else []
+    if norm_weight is not None:
+        extra.append(("norm_weight", norm_weight))
+    for name, t in [("q", q), ("k", k), ("v", v), ("g", g)] + extra:
         if not t.is_cuda or not t.is_contiguous():
             raise ValueError(f"{name} must be a contiguous device tensor")
     if scale is None:
@@ -195,7 +218,8 @@ def gtr_gla_fwd(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, g: torch.Tens
     if want_final and sf is None:
         sf = torch.empty((B, heads, q.shape[-1], v.shape[-1]), dtype=torch.float32, device=q.device)
     args = make_args(q, k, v, g, H=H, W=W, scale=scale, chunk=chunk, scan=scan, s0=s0, o=o,
-                     s_final=sf, path=path)
+                     s_final=sf, path=path, gate_tau=gate_tau, out_gate=out_gate,
+                     norm_weight=norm_weight, norm_eps=norm_eps)
     need = gtr_gla_workspace_size(args)
     if need == 0:
         raise GtrError("gtr_gla_workspace_size", 2)

@@ -80,6 +80,12 @@ struct GlaParams {
   unsigned* sync;   // [BH][4]: arrive1, arrive2, leave, spare
   unsigned* fault;  // one word
   int groups;       // ceil(BH / 8), fused mapping
+  int gkind;        // GTR_GATE_LOG_DECAY or GTR_GATE_LOGITS (g holds the gate logits)
+  float inv_tau;    // 1 / tau of the gate fusion
+  const void* gate;  // output-gate pre-activation [BH][L][DV] (spatial), or null: no epilogue
+  const float* nw;   // RMSNorm weight [DV], or null (ones)
+  int gatedt;        // dtype of gate
+  float eps;         // RMSNorm epsilon
 };
 
 constexpr int tile_threads(int chunk) { return chunk / 16 * kWave; }
@@ -155,6 +161,25 @@ __device__ __forceinline__ float gexp(float x) {
     return __expf(x);
   else
     return expf(x);
+}
+
+// Log-decay of one key dimension from what g holds: log gamma itself, or (gate
+// fusion) the logit a of gamma = sigmoid(a)^(1/tau) (Sec. 3.1), giving
+// log gamma = logsigmoid(a) / tau = (min(a, 0) - log1p(exp(-|a|))) / tau.
+// log1p(e) for e in (0, 1] as log(u) * e / (u - 1), u = 1 + e rounded: the
+// factor e / (u - 1) undoes the rounding of u (u - 1 is exact), which keeps the
+// result within a few ulp with one log and one reciprocal.
+// Hardware log2 and reciprocal (about 1 ulp each); when u rounds to 1 the
+// quotient is not used (a select, not a branch).
+__device__ __forceinline__ float log_decay(const GlaParams& P, float x) {
+  if (P.gkind != GTR_GATE_LOGITS) return x;
+  constexpr float kLn2 = 0.693147180559945309f;
+  const float e = __expf(-fabsf(x));
+  const float u = 1.f + e;
+  const float d = u - 1.f;
+  const float r = __builtin_amdgcn_logf(u) * kLn2 * e * __builtin_amdgcn_rcpf(d);
+  const float l1p = d == 0.f ? e : r;
+  return (fminf(x, 0.f) - l1p) * P.inv_tau;
 }
 
 // One chunk of one sequence: C tokens, one wave per 16-token sub-chunk.
@@ -283,6 +308,8 @@ struct Chunk {
       cvt_raw(rq[s], IN, qx);
       cvt_raw(rk[s], IN, kx);
       cvt_raw(rg[s], P.gdt, gx);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) gx[e] = log_decay(P, gx[e]);
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
         // local inclusive cumulative sum over the 16 tokens of this sub-chunk
@@ -425,6 +452,8 @@ struct Chunk {
       cvt_raw(rq, IN, qx[s]);
       cvt_raw(rk, IN, kx[s]);
       cvt_raw(rg, P.gdt, gx);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) gx[e] = log_decay(P, gx[e]);
 #pragma unroll
       for (int e = 0; e < 8; ++e) ax[s][e] = row_inclusive_scan(gx[e]);
     }
@@ -588,26 +617,75 @@ struct Chunk {
   }
 
   // Stage the output tile through LDS and write whole rows back in spatial order.
+  // Gate values of the output-gate epilogue for the rows this thread stores,
+  // loaded early (with the other inputs) so that the epilogue does not wait
+  // for memory at the end of the kernel. Only when P.gate is set.
+  static constexpr int SITER = C * (DV / 8) / NT;  // store iterations per thread
+  __device__ __forceinline__ void prefetch_gate(const GlaParams& P, int bh, int c, Raw (&rz)[SITER]) const {
+#pragma unroll
+    for (int it = 0; it < SITER; ++it) {
+      const int idx = threadIdx.x + it * NT;
+      const int rr = idx / PIECES, pc = idx % PIECES;
+      bool valid;
+      const int64_t t = token(P, (int64_t)c * C + rr, valid);
+      ld_raw(P.gate, P.gatedt, ((int64_t)bh * P.L + t) * DV + 8 * pc, rz[it]);
+    }
+  }
+
   template <class S>
-  __device__ __forceinline__ void store(const GlaParams& P, S& sm, int bh, int c, const f4 (&O)[DV / 16]) {
+  __device__ __forceinline__ void store(const GlaParams& P, S& sm, int bh, int c, const f4 (&O)[DV / 16],
+                                        const Raw (&rz)[SITER]) {
     __syncthreads();  // all waves are done with the k rows in buf
 #pragma unroll
     for (int jb = 0; jb < DV / 16; ++jb)
 #pragma unroll
       for (int e = 0; e < 4; ++e) sm.buf[(16 * w + 4 * gq + e) * OP + 16 * jb + tr] = P.scale * O[jb][e];
     __syncthreads();
-    constexpr int PIECES = DV / 8;
-    for (int idx = threadIdx.x; idx < C * PIECES; idx += NT) {
+    // C * PIECES is a multiple of NT, so every lane runs the same number of
+    // iterations, and the PIECES lanes of a row are consecutive lanes of one wave
+    static_assert((C * PIECES) % NT == 0 && kWave % PIECES == 0, "row groups");
+#pragma unroll
+    for (int it = 0; it < SITER; ++it) {
+      const int idx = threadIdx.x + it * NT;
       const int rr = idx / PIECES, pc = idx % PIECES;
       bool valid;
       const int64_t t = token(P, (int64_t)c * C + rr, valid);
-      if (valid) {
-        float x[8];
+      const int64_t off = ((int64_t)bh * P.L + t) * DV + 8 * pc;  // token 0 past the end: in bounds
+      float x[8];
 #pragma unroll
-        for (int e = 0; e < 8; ++e) x[e] = sm.buf[rr * OP + 8 * pc + e];
-        store_n<8>(P.o, P.odt, ((int64_t)bh * P.L + t) * DV + 8 * pc, x);
-      }
+      for (int e = 0; e < 8; ++e) x[e] = sm.buf[rr * OP + 8 * pc + e];
+      if (P.gate) epilogue(P, rz[it], pc, x);
+      if (valid) store_n<8>(P.o, P.odt, off, x);
     }
+  }
+  static constexpr int PIECES = DV / 8;  // 8-element pieces of an output row
+
+  // Output-gate epilogue (Sec. 3.1): u = SiLU(z) * o / sqrt(mean(o^2) + eps) * w
+  // over the DV channels of one token; x holds this lane's 8 channels of o.
+  // Called by every lane (the row sum is a cross-lane reduction).
+  __device__ __forceinline__ void epilogue(const GlaParams& P, const Raw& rz, int pc, float (&x)[8]) const {
+    float ss = 0.f;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) ss = fmaf(x[e], x[e], ss);
+#pragma unroll
+    for (int m = 1; m < PIECES; m <<= 1) ss += __shfl_xor(ss, m, kWave);
+    const float rs = rsqrtf(ss * (1.f / DV) + P.eps);
+    float z[8], w[8];
+    cvt_raw(rz, P.gatedt, z);
+    if (P.nw) {
+      const f4 lo = *reinterpret_cast<const f4*>(P.nw + 8 * pc);
+      const f4 hi = *reinterpret_cast<const f4*>(P.nw + 8 * pc + 4);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        w[e] = lo[e];
+        w[e + 4] = hi[e];
+      }
+    } else {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) w[e] = 1.f;
+    }
+#pragma unroll
+    for (int e = 0; e < 8; ++e) x[e] = z[e] * __builtin_amdgcn_rcpf(1.f + __expf(-z[e])) * (x[e] * rs) * w[e];
   }
 };
 
@@ -709,6 +787,8 @@ __global__ void __launch_bounds__(tile_threads(C)) gla_output_kernel(GlaParams P
   f4 sbuf[T::SPER];
   if (have_state) ch.template state_load<false>(P.states + ((int64_t)bh * P.nchunks + c) * (DK * DV), sbuf);
   ch.template load<true>(P, sm, bh, c);
+  Raw rz[T::SITER];
+  if (P.gate) ch.prefetch_gate(P, bh, c, rz);
   if (have_state) ch.state_store(sm, sbuf);
   ch.template factors<true, false, false>(sm, nullptr);
   f4 O[DV / 16];
@@ -717,7 +797,7 @@ __global__ void __launch_bounds__(tile_threads(C)) gla_output_kernel(GlaParams P
     __syncthreads();  // state tile complete
     ch.readout(sm, O);
   }
-  ch.store(P, sm, bh, c, O);
+  ch.store(P, sm, bh, c, O, rz);
 }
 
 // ---------------------------------------------------------------------------
@@ -832,6 +912,8 @@ __global__ void __launch_bounds__(tile_threads(C)) gla_fused_kernel(GlaParams P)
 
   T ch;
   ch.template load<true>(P, sm, bh, c);
+  Raw rz[T::SITER];
+  if (P.gate) ch.prefetch_gate(P, bh, c, rz);
   ch.template factors<true, true, true>(sm, P.decays + sc * DK);
   ch.template summary_out<true>(sm, P.states + sc * (DK * DV));
   seq_arrive(&sync[0]);
@@ -866,7 +948,7 @@ __global__ void __launch_bounds__(tile_threads(C)) gla_fused_kernel(GlaParams P)
       ch.readout(sm, O);
     }
   }
-  ch.store(P, sm, bh, c, O);
+  ch.store(P, sm, bh, c, O, rz);
 
   if (threadIdx.x == 0) {
     const unsigned prev = __hip_atomic_fetch_add(&sync[2], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -1030,6 +1112,12 @@ extern "C" gtr_status gtr_gla_fwd(const gtr_gla_args* a, hipStream_t stream) {
   P.states = reinterpret_cast<float*>(ws + lay.states_off);
   P.decays = reinterpret_cast<float*>(ws + lay.decays_off);
   P.groups = (int)((s.BH + 7) / 8);
+  P.gkind = a->g_kind;
+  P.inv_tau = a->g_kind == GTR_GATE_LOGITS ? 1.f / a->gate_tau : 1.f;
+  P.gate = a->out_gate;
+  P.nw = a->out_gate ? a->norm_weight : nullptr;
+  P.gatedt = a->out_gate_dtype;
+  P.eps = a->norm_eps;
 
   // Length-aware dispatch: short sequences rebuild each boundary state from the
   // summaries (one hand-off), longer ones split the scan over their chunks'
@@ -1045,7 +1133,7 @@ extern "C" gtr_status gtr_gla_fwd(const gtr_gla_args* a, hipStream_t stream) {
                      (a->path == GTR_PATH_AUTO && s.nchunks * s.dk * s.dv <= kInlineMaxSummaryElems);
     const void* k = inl ? ks.inlined : ks.fused;
     const int cap = fused_capacity_per_xcd(k, ks.threads);
-    const bool fits = cap > 0 && s.nchunks <= cap && s.nchunks <= kFusedMaxChunks;
+    const bool fits = cap > 0 && s.nchunks <= cap && s.nchunks <= kFusedMaxChunks && s.BH <= kSyncSeqs;
     if (a->path != GTR_PATH_AUTO && !fits) return GTR_ERR_UNSUPPORTED;
     if (fits) one_launch = k;
   }

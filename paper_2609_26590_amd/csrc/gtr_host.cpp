@@ -37,6 +37,12 @@ gtr_status gla_shape_from_args(const gtr_gla_args* a, GlaShape* s, bool check_po
   if (a->o_dtype != q && a->o_dtype != GTR_F32) return GTR_ERR_UNSUPPORTED;
   if (a->scan < GTR_SCAN_ROW || a->scan > GTR_SCAN_COL_REV) return GTR_ERR_UNSUPPORTED;
   if (a->path < GTR_PATH_AUTO || a->path > GTR_PATH_INLINE) return GTR_ERR_UNSUPPORTED;
+  if (a->g_kind != GTR_GATE_LOG_DECAY && a->g_kind != GTR_GATE_LOGITS) return GTR_ERR_UNSUPPORTED;
+  if (a->g_kind == GTR_GATE_LOGITS && !(a->gate_tau > 0.f && a->gate_tau <= 3.0e38f)) return GTR_ERR_UNSUPPORTED;
+  if (a->out_gate) {
+    if (a->out_gate_dtype != q && a->out_gate_dtype != GTR_F32) return GTR_ERR_UNSUPPORTED;
+    if (!(a->norm_eps > 0.f && a->norm_eps <= 3.0e38f)) return GTR_ERR_UNSUPPORTED;
+  }
 
   int64_t BH, L, n;
   if (!mul_ok(a->B, a->heads, &BH) || !mul_ok(a->H, a->W, &L)) return GTR_ERR_SHAPE;
@@ -68,6 +74,9 @@ gtr_status gla_shape_from_args(const gtr_gla_args* a, GlaShape* s, bool check_po
                         reinterpret_cast<uintptr_t>(a->o);
   if (mis & 15u) return GTR_ERR_UNSUPPORTED;
   if ((reinterpret_cast<uintptr_t>(a->s0) | reinterpret_cast<uintptr_t>(a->s_final)) & 3u) return GTR_ERR_UNSUPPORTED;
+  // the epilogue reads 8 gate values and 8 weights of a row at a time
+  if ((reinterpret_cast<uintptr_t>(a->out_gate) | reinterpret_cast<uintptr_t>(a->norm_weight)) & 15u)
+    return GTR_ERR_UNSUPPORTED;
 
   const size_t qs = dtype_size(q), gs = dtype_size(a->g_dtype), os = dtype_size(a->o_dtype);
   const size_t ntok = (size_t)(BH * L);
@@ -88,7 +97,9 @@ gtr_status gla_shape_from_args(const gtr_gla_args* a, GlaShape* s, bool check_po
   if (a->workspace_bytes < lay.total) return GTR_ERR_WORKSPACE;
   const Range rw = rng(a->workspace, lay.total);
 
-  const Range ins[] = {rq, rk, rv, rg, rs0};
+  const Range rgate = a->out_gate ? rng(a->out_gate, ntok * a->dv * dtype_size(a->out_gate_dtype)) : Range{0, 0};
+  const Range rnw = a->out_gate && a->norm_weight ? rng(a->norm_weight, (size_t)a->dv * 4) : Range{0, 0};
+  const Range ins[] = {rq, rk, rv, rg, rs0, rgate, rnw};
   for (const Range& r : ins) {
     if (overlap(ro, r) || overlap(rsf, r) || overlap(rw, r)) return GTR_ERR_ALIAS;
   }
@@ -102,7 +113,7 @@ WorkspaceLayout gla_workspace_layout(const GlaShape& s) {
   w.fault_off = off;
   off += 256;
   w.sync_off = off;
-  off = align256(off + (size_t)s.BH * 4 * sizeof(uint32_t));
+  off = align256(off + (size_t)kSyncSeqs * 4 * sizeof(uint32_t));
   w.states_off = off;
   off = align256(off + (size_t)s.BH * s.nchunks * s.dk * s.dv * sizeof(float));
   w.decays_off = off;

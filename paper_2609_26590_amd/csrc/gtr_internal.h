@@ -16,9 +16,16 @@ struct GlaShape {
   int qdt, gdt, odt;
 };
 
+// The per-sequence hand-off counters of the one-launch schedules live in a
+// region of fixed size right after the 256-byte header, for this many
+// sequences, whatever the shape of a call. Everything else of a workspace
+// starts behind it, so no call of any shape ever writes where another call
+// expects zeroed counters (one workspace can serve calls of different shapes).
+constexpr int64_t kSyncSeqs = 1024;
+
 struct WorkspaceLayout {
   size_t fault_off;   // one 32-bit word (fused-path wait ran out)
-  size_t sync_off;    // [BH][4] 32-bit counters
+  size_t sync_off;    // [kSyncSeqs][4] 32-bit counters
   size_t states_off;  // [BH][nchunks][dv][dk] float32
   size_t decays_off;  // [BH][nchunks][dk] float32
   size_t total;

@@ -348,6 +348,26 @@ class Wave:
             raise NotImplementedError(f"v64 operand {tok}: {inst.raw}")
         return np.full(NL, lit & M64, np.uint64), np.ones(NL, bool), np.zeros(NL, bool)
 
+    def v64w(self, tok, inst):
+        """64-bit per-lane source with per-word flags: (value, d_lo, d_hi, o_lo, o_hi)."""
+        r = self.vidx(tok)
+        if r is not None:
+            i = r[0]
+            v = self.V[i].astype(np.uint64) | (self.V[i + 1].astype(np.uint64) << np.uint64(32))
+            return v, self.VD[i], self.VD[i + 1], self.VO[i], self.VO[i + 1]
+        v, d, o = self.v64(tok, inst)
+        return v, d, d, o, o
+
+    def vwrite64w(self, tok, v, d_lo, d_hi, o_lo, o_hi, lanes=None):
+        r = self.vidx(tok)
+        m = self.active() if lanes is None else lanes
+        i = r[0]
+        v = np.asarray(v, np.uint64)
+        self.V[i][m] = (v & np.uint64(M32)).astype(np.uint32)[m]
+        self.V[i + 1][m] = (v >> np.uint64(32)).astype(np.uint32)[m]
+        self.VD[i][m], self.VO[i][m] = d_lo[m], o_lo[m]
+        self.VD[i + 1][m], self.VO[i + 1][m] = d_hi[m], o_hi[m]
+
     def active(self):
         return ((np.uint64(self.exec) >> LANES.astype(np.uint64)) & np.uint64(1)).astype(bool)
 
@@ -1081,21 +1101,25 @@ def _vmov64(w, i):
     w.vwrite64(i.ops[0], v, d, o)
 
 
+# 64-bit results: the low word depends only on the low words of the 64-bit
+# sources (and on the 32-bit ones), the high word on everything.
 @handler('v_lshl_add_u64')
 def _lshladd64(w, i):
-    a, ad, ao = w.v64(i.ops[1], i)
+    a, adl, adh, aol, aoh = w.v64w(i.ops[1], i)
     s = w.v32(i.ops[2], i)
-    b, bd, bo = w.v64(i.ops[3], i)
+    b, bdl, bdh, bol, boh = w.v64w(i.ops[3], i)
     v = (a << (u64(s.v) & np.uint64(63))) + b
-    w.vwrite64(i.ops[0], v, ad & bd & s.d, ao | bo | s.o)
+    dl, ol = adl & bdl & s.d, aol | bol | s.o
+    w.vwrite64w(i.ops[0], v, dl, dl & adh & bdh, ol, ol | aoh | boh)
 
 
 @handler('v_lshlrev_b64')
 def _lshlrev64(w, i):
     s = w.v32(i.ops[1], i)
-    a, ad, ao = w.v64(i.ops[2], i)
+    a, adl, adh, aol, aoh = w.v64w(i.ops[2], i)
     v = a << (u64(s.v) & np.uint64(63))
-    w.vwrite64(i.ops[0], v, ad & s.d, ao | s.o)
+    dl, ol = adl & s.d, aol | s.o
+    w.vwrite64w(i.ops[0], v, dl, dl & adh, ol, ol | aoh)
 
 
 @handler('v_lshrrev_b64')
@@ -1130,7 +1154,7 @@ def carry_out(w, tok, bits, d, o):
 @handler('v_mad_u64_u32', 'v_mad_i64_i32')
 def _mad64(w, i):
     a, b = w.v32(i.ops[2], i), w.v32(i.ops[3], i)
-    c, cd, co = w.v64(i.ops[4], i)
+    c, cdl, cdh, col, coh = w.v64w(i.ops[4], i)
     if i.op == 'v_mad_u64_u32':
         p = a.v.astype(object) * b.v.astype(object)
     else:
@@ -1138,9 +1162,9 @@ def _mad64(w, i):
     full = p + (c.astype(object) if i.op == 'v_mad_u64_u32' else c.view(np.int64).astype(object))
     v = np.array([int(x) & M64 for x in full], dtype=np.uint64)
     carry = np.array([(int(x) >> 64) & 1 if i.op == 'v_mad_u64_u32' else 0 for x in full], bool)
-    d = a.d & b.d & cd
-    o = a.o | b.o | co
-    w.vwrite64(i.ops[0], v, d, o)
+    dl, ol = a.d & b.d & cdl, a.o | b.o | col
+    d, o = dl & cdh, ol | coh
+    w.vwrite64w(i.ops[0], v, dl, d, ol, o)
     carry_out(w, i.ops[1], carry, d, o)
 
 
@@ -1599,3 +1623,57 @@ def _cnd_sdwa(w, i):
     r = w.vidx(i.ops[0])
     m = w.active()
     w.VO[r[0]][m] = True
+
+
+def dataop_wide(nsrc, first=1):
+    """Data ops with register-pair operands (float64 helpers of the math library):
+    every destination register is opaque, defined iff every source register is."""
+    def h(w, i):
+        lanes = w.active()
+        d = np.ones(NL, bool)
+        for t in i.ops[first:first + nsrc]:
+            r = w.vidx(t)
+            if r is None:
+                sv, so, sd = w.s32(t, i) if not t.startswith('s[') else (0, 0, w.s64(t, i)[2])
+                d &= sd
+                continue
+            for j in range(r[0], r[1] + 1):
+                d &= w.VD[j]
+        w.vwrite_multi(i.ops[0], d, np.ones(NL, bool), lanes)
+    return h
+
+
+for _n, _k in [('v_frexp_mant_f32_e32', 1), ('v_frexp_exp_i32_f32_e32', 1), ('v_cvt_f64_f32_e32', 1),
+               ('v_frexp_exp_i32_f64_e32', 1), ('v_div_fixup_f32', 3), ('v_rsq_f32_e32', 1)]:
+    HANDLERS[_n] = dataop_wide(_k)
+
+
+@handler('v_div_scale_f32')
+def _divscale(w, i):
+    # v_div_scale_f32 vdst, sdst, s0, s1, s2: data result plus a per-lane flag mask
+    lanes = w.active()
+    srcs = [w.v32(t, i) for t in i.ops[2:5]]
+    d = np.ones(NL, bool)
+    for x in srcs:
+        d &= x.d
+    w.vwrite_multi(i.ops[0], d, np.ones(NL, bool), lanes)
+    ob = 0
+    for l in range(NL):
+        if lanes[l]:
+            ob |= 1 << l
+    w.s64set(i.ops[1], 0, ob, bool((d | ~lanes).all()))
+
+
+@handler('v_div_fmas_f32')
+def _divfmas(w, i):
+    # reads VCC (the flag mask of v_div_scale) besides its three sources
+    vv, vo, vd = w.s64('vcc', i)
+    if not vd:
+        w.rep.add('WARN-UNDEF-CMP', i, 'vcc')
+    dataop_wide(3)(w, i)
+
+
+for _t in ('f32',):
+    for _e in ('_e32', '_e64'):
+        HANDLERS[f'v_cmp_neq_{_t}{_e}'] = vcmp(lambda a, b: ~(a == b), _t)
+        HANDLERS[f'v_cmp_class_{_t}{_e}'] = vcmp(lambda a, b: np.zeros(a.shape, bool), 'u32')

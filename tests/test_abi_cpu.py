@@ -79,7 +79,7 @@ def fwd(lib, a):
 def test_workspace_size_formula(lib):
     a = base_args(B=2, heads=3, H=40, W=40, dk=64, dv=64, chunk=64)
     BH, nc = 6, 25
-    want = 256 + 256 + BH * nc * 64 * 64 * 4 + ((BH * nc * 64 * 4 + 255) // 256) * 256
+    want = 256 + 1024 * 16 + BH * nc * 64 * 64 * 4 + ((BH * nc * 64 * 4 + 255) // 256) * 256
     assert lib.gtr_gla_workspace_size(ctypes.byref(a)) == want
     a.dk = 48
     assert lib.gtr_gla_workspace_size(ctypes.byref(a)) == 0
@@ -193,3 +193,53 @@ def test_permute_validation(lib):
     assert perm(lib, d=7) == UNSUP
     assert perm(lib, inv=2) == UNSUP
     assert perm(lib, dst=FAKE + 64) == ALIAS
+
+
+# ---------------------------------------------------------------------------
+# gate fusion and output-gate epilogue arguments
+# ---------------------------------------------------------------------------
+
+def test_gate_kind_and_tau_checked(lib):
+    a = base_args()
+    a.g_kind = 2
+    assert fwd(lib, a) == UNSUP
+    for tau in (0.0, -1.0, float("nan"), float("inf")):
+        a = base_args()
+        a.g_kind = gtr.GATE_LOGITS
+        a.gate_tau = tau
+        assert fwd(lib, a) == UNSUP, tau
+        assert lib.gtr_gla_workspace_size(ctypes.byref(a)) == 0
+
+
+def epilogue_args(**kw):
+    a = base_args(**kw)
+    n_in = a.B * a.heads * a.H * a.W * 64 * 4
+    a.out_gate = FAKE + 5 * n_in
+    a.out_gate_dtype = a.qkv_dtype
+    a.norm_eps = 1e-5
+    return a
+
+
+def test_epilogue_arguments_checked(lib):
+    a = epilogue_args()
+    a.out_gate_dtype = gtr.BF16  # neither the input dtype (fp16) nor float32
+    assert fwd(lib, a) == UNSUP
+    for eps in (0.0, -1e-5, float("nan"), float("inf")):
+        a = epilogue_args()
+        a.norm_eps = eps
+        assert fwd(lib, a) == UNSUP, eps
+    a = epilogue_args()
+    a.out_gate += 8  # the epilogue reads 16-byte pieces
+    assert fwd(lib, a) == UNSUP
+    a = epilogue_args()
+    a.norm_weight = FAKE + 4  # misaligned weight
+    assert fwd(lib, a) == UNSUP
+
+
+def test_epilogue_gate_must_not_overlap_output(lib):
+    a = epilogue_args()
+    a.out_gate = a.o + 64
+    assert fwd(lib, a) == ALIAS
+    a = epilogue_args()
+    a.norm_weight = a.o
+    assert fwd(lib, a) == ALIAS

@@ -90,7 +90,7 @@ def test_emulator_flags_out_of_bounds():
 # ---------------------------------------------------------------------------
 DT = {"f32": (0, 4), "f16": (1, 2), "bf16": (2, 2)}
 SCAN = {"row": 0, "col": 1, "row_rev": 2, "col_rev": 3}
-KERNARG_BYTES = 144  # sizeof(GlaParams)
+KERNARG_BYTES = 176  # sizeof(GlaParams)
 
 
 def a256(x):
@@ -123,7 +123,9 @@ def device_asm() -> str:
 
 
 class Shape:
-    def __init__(self, B, heads, H, W, dk, dv, chunk, dt, gdt, odt, scan, s0, sfinal):
+    def __init__(self, B, heads, H, W, dk, dv, chunk, dt, gdt, odt, scan, s0, sfinal, logits=False, zdt=None,
+                 weighted=False):
+        self.logits, self.zdt, self.weighted = logits, zdt, weighted
         self.B, self.heads, self.H, self.W = B, heads, H, W
         self.dk, self.dv, self.chunk = dk, dv, chunk
         self.dt, self.gdt, self.odt, self.scan, self.s0, self.sfinal = dt, gdt, odt, scan, s0, sfinal
@@ -152,9 +154,11 @@ def kernel_args(c: Shape):
     o = alloc("o", c.BH * c.L * c.dv * DT[c.odt][1], "w")
     s0 = alloc("s0", c.BH * c.dk * c.dv * 4, "r") if c.s0 else 0
     sf = alloc("s_final", c.BH * c.dk * c.dv * 4, "w") if c.sfinal else 0
+    z = alloc("out_gate", c.BH * c.L * c.dv * DT[c.zdt][1], "r") if c.zdt else 0
+    nw = alloc("norm_weight", c.dv * 4, "r") if c.zdt and c.weighted else 0
     # workspace layout of gla_workspace_layout(): fault word, counters, states, decays
     sync = 256
-    states = a256(sync + c.BH * 16)
+    states = a256(sync + 1024 * 16)  # counters of up to 1024 sequences, a fixed region
     decays = a256(states + c.BH * c.NC * c.dk * c.dv * 4)
     total = a256(decays + c.BH * c.NC * c.dk * 4)
     ws = alloc("workspace", total, "rw")
@@ -162,9 +166,10 @@ def kernel_args(c: Shape):
     regions.insert(0, emu.Region("sync", ws + sync, c.BH * 16, "rw", load_value=0x7FFFFFFF))
     regions.insert(0, emu.Region("fault", ws, 256, "rw"))
     regions.append(emu.Region("kernarg", emu.KERNARG_BASE, KERNARG_BYTES, "r"))
-    kern = struct.pack("<7Q6iqifi4xQQQQi4x", q, k, v, g, o, s0, sf, DT[c.dt][0], DT[c.gdt][0], DT[c.odt][0],
-                       c.BH, c.H, c.W, c.L, c.NC, c.dk ** -0.5, SCAN[c.scan], ws + states, ws + decays,
-                       ws + sync, ws, (c.BH + 7) // 8)
+    kern = struct.pack("<7Q6iqifi4xQQQQiif4xQQif", q, k, v, g, o, s0, sf, DT[c.dt][0], DT[c.gdt][0],
+                       DT[c.odt][0], c.BH, c.H, c.W, c.L, c.NC, c.dk ** -0.5, SCAN[c.scan], ws + states,
+                       ws + decays, ws + sync, ws, (c.BH + 7) // 8, 1 if c.logits else 0, 1.0 / 16,
+                       z, nw, DT[c.zdt][0] if c.zdt else 0, 1e-5)
     assert len(kern) == KERNARG_BYTES
     return kern, regions
 
@@ -212,6 +217,11 @@ CHECKS = [
     (Shape(1, 2, 13, 11, 32, 32, 32, "f32", "f32", "f32", "row", False, True), ("summary", "output", "fused")),
     (Shape(1, 6, 128, 128, 32, 64, 64, "f16", "f16", "f16", "row", False, False),
      ("summary", "scan", "output", "fused", "inline")),
+    # gate fusion and the output-gate epilogue
+    (Shape(1, 12, 40, 40, 64, 64, 64, "bf16", "bf16", "f32", "col", True, True, True, "bf16", True),
+     ("summary", "output", "fused", "inline")),
+    (Shape(1, 3, 7, 9, 32, 64, 32, "f16", "f32", "f16", "row_rev", False, False, True, "f32", False),
+     ("summary", "output", "fused")),
 ]
 
 

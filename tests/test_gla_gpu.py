@@ -269,3 +269,100 @@ def test_graph_replays_match_eager(gtr):
             assert torch.equal(a, b), f"replay {rep} differs"
         calls()  # eager work between replays
         torch.cuda.synchronize()
+
+
+# ---------------------------------------------------------------------------
+# scope rows f1 / f3: gate fusion (g holds the gate logits, log gamma =
+# logsigmoid(a) / tau in the kernels) and the output-gate epilogue
+# u = SiLU(x W_r) * RMSNorm(o), both against the oracle's definitions
+# ---------------------------------------------------------------------------
+FUSIONS = [
+    # workload, gate logits, epilogue gate dtype (None: no epilogue), RMSNorm weight
+    ("kbench", True, None, False),
+    ("kbench", False, "f16", True),
+    ("kbench", True, "f32", False),
+    ("directions", True, "bf16", True),
+    ("op1600", True, "f16", True),
+    ("tiny", True, "f32", True),
+    ("batched", True, "f32", True),
+]
+
+
+@pytest.mark.parametrize("path", PATHS)
+@pytest.mark.parametrize("case", range(len(FUSIONS)))
+def test_fusions_parity(gtr, case, path):
+    name, logits, zdt, weighted = FUSIONS[case]
+    wl = WORKLOADS[name]
+    inp = make_inputs(wl)
+    rng = np.random.default_rng(500 + case)
+    tau, eps = 16.0, 1e-5
+    g_ref = inp["g"]
+    if logits:  # gate logits a ~ N(0, 2), rounded to the input dtype; the oracle gets log gamma of those
+        a = torch.from_numpy(rng.normal(0.0, 2.0, size=tuple(inp["g"].shape))).float().to(torch_dtype(wl.dtype))
+        inp["g"] = a
+        g_ref = oracle.log_decay_from_logits(a, tau)
+    dev = torch.device("cuda")
+    q, k, v, g = (inp[n].to(dev) for n in ("q", "k", "v", "g"))
+    s0 = None if inp["s0"] is None else inp["s0"].to(dev)
+    z = w = None
+    if zdt:
+        z = torch.from_numpy(rng.normal(0.0, 1.5, size=(wl.B, wl.heads, wl.L, wl.dv))).float().to(torch_dtype(zdt))
+        if weighted:
+            w = torch.from_numpy(rng.uniform(0.5, 1.5, size=wl.dv)).float()
+    o, sf = call(gtr, q, k, v, g, H=wl.H, W=wl.W, scale=wl.scale, chunk=wl.chunk, s0=s0, want_final=wl.want_final,
+                 o_dtype=torch_dtype(wl.odtype), path=path, gate_tau=tau if logits else None,
+                 out_gate=None if z is None else z.to(dev), norm_weight=None if w is None else w.to(dev),
+                 norm_eps=eps)
+    torch.cuda.synchronize()
+    o_ref, sf_ref = oracle.gla(inp["q"], inp["k"], inp["v"], g_ref, inp["s0"], scale=wl.scale, H=wl.H, W=wl.W)
+    if z is not None:
+        o_ref = oracle.output_gate(o_ref, z, w, eps)
+    tol = tol_for(wl.dtype, wl.odtype)
+    err = rel_err(o, o_ref)
+    assert err <= tol, f"{name} logits={logits} epilogue={zdt} {path}: {err:.3e} > {tol:.1e}"
+    if wl.want_final:
+        assert rel_err(sf, sf_ref) <= tol_for(wl.dtype, "f32")
+
+
+def test_epilogue_leaves_the_state_alone(gtr):
+    """The epilogue changes what is written to o, never the recurrence: S_final
+    is the same with and without it."""
+    wl = WORKLOADS["batched"].with_(B=1)
+    inp = make_inputs(wl)
+    dev = torch.device("cuda")
+    q, k, v, g = (inp[n].to(dev) for n in ("q", "k", "v", "g"))
+    s0 = inp["s0"].to(dev)
+    z = torch.randn((1, wl.heads, wl.L, wl.dv), device=dev)
+    _, sf1 = call(gtr, q, k, v, g, H=wl.H, W=wl.W, scale=wl.scale, s0=s0, want_final=True,
+                  o_dtype=torch.float32, path="staged")
+    _, sf2 = call(gtr, q, k, v, g, H=wl.H, W=wl.W, scale=wl.scale, s0=s0, want_final=True,
+                  o_dtype=torch.float32, path="staged", out_gate=z)
+    torch.cuda.synchronize()
+    assert torch.equal(sf1, sf2)
+
+
+def test_workspace_shared_across_shapes(gtr):
+    """One workspace serves calls of different shapes in any order: what a call
+    with few sequences writes must never land where a later one-launch call
+    with more sequences expects zeroed hand-off counters (regression: the
+    counters used to end where the chunk states of the smaller call began)."""
+    ws = gtr.Workspace()
+    dev = torch.device("cuda")
+    big, small = WORKLOADS["batched"], WORKLOADS["kbench"]
+
+    def run(wl, path):
+        inp = make_inputs(wl)
+        q, k, v, g = (inp[n].to(dev) for n in ("q", "k", "v", "g"))
+        s0 = None if inp["s0"] is None else inp["s0"].to(dev)
+        o, _ = call(gtr, q, k, v, g, H=wl.H, W=wl.W, scale=wl.scale, s0=s0, o_dtype=torch_dtype(wl.odtype),
+                    path=path, workspace=ws)
+        torch.cuda.synchronize()
+        assert gtr.gtr_gla_workspace_fault(ws.buf) == 0
+        return o
+
+    ref_big, _ = _reference(big, "row")
+    for first_path, big_path in (("staged", "fused"), ("fused", "inline"), ("inline", "fused")):
+        run(big, "staged")      # sizes the workspace for the large call
+        run(small, first_path)  # a smaller call writes its chunk states
+        o = run(big, big_path)
+        assert rel_err(o, ref_big) <= tol_for(big.dtype, big.odtype), (first_path, big_path)

@@ -349,3 +349,76 @@ def test_py_recurrence_without_mistake_passes_pins():
     # guards the mutation test itself: the unmutated copy passes every pin
     fn = lambda *a, **kw: py_recurrence(*a, **kw)
     assert all(pin(fn) for pin in ALL_PINS.values())
+
+
+# ---------------------------------------------------------------------------
+# gate fusion: g = log gamma for gamma = sigmoid(a)^(1/tau) (Sec. 3.1)
+# ---------------------------------------------------------------------------
+
+def test_log_decay_from_logits_matches_the_power_form():
+    from scipy.special import expit
+    a = np.random.default_rng(11).normal(0.0, 4.0, size=1000)
+    for tau in (1.0, 16.0):
+        g = oracle.log_decay_from_logits(a, tau)
+        # gamma written as the paper's power of a sigmoid, evaluated independently
+        np.testing.assert_allclose(np.exp(g), expit(a) ** (1.0 / tau), rtol=1e-13)
+        assert np.all(g < 0)
+
+
+def test_log_decay_from_logits_special_values():
+    g = oracle.log_decay_from_logits(np.array([0.0, -60.0, 60.0]), 16.0)
+    assert g[0] == pytest.approx(-np.log(2.0) / 16.0, rel=1e-15)
+    assert g[1] == pytest.approx(-60.0 / 16.0, rel=1e-15)           # log sigmoid(a) -> a for a -> -inf
+    assert g[2] == pytest.approx(-np.exp(-60.0) / 16.0, rel=1e-12)  # -> -e^-a for a -> +inf, not 0
+
+
+# ---------------------------------------------------------------------------
+# output gate: u = SiLU(x W_r) * RMSNorm(o) (Sec. 3.1)
+# ---------------------------------------------------------------------------
+
+def epilogue_pins(fn):
+    """Each returns True when ``fn(o, z, weight, eps)`` behaves as the definition."""
+    from scipy.special import expit
+    rng = np.random.default_rng(12)
+    o = rng.normal(size=(3, 5, 64)) * rng.uniform(0.1, 10.0, size=(3, 5, 1))
+    z = rng.normal(size=(3, 5, 64)) * 3.0
+    w = rng.uniform(0.5, 2.0, size=64)
+    u = fn(o, z, None, 0.0)
+    pins = []
+    # SiLU of the gate: u / (o / rms) is z * sigmoid(z), checked against scipy
+    rms = np.sqrt(np.mean(o * o, axis=-1, keepdims=True))
+    pins.append(np.allclose(u / (o / rms), z * expit(z), rtol=1e-12))
+    # RMSNorm is over the channels of one token: u / SiLU(z) has unit RMS per token
+    pins.append(np.allclose(np.sqrt(np.mean((u / (z * expit(z))) ** 2, axis=-1)), 1.0, rtol=1e-12))
+    # the weight scales channel j by w_j
+    pins.append(np.allclose(fn(o, z, w, 0.0), u * w, rtol=1e-12))
+    # epsilon enters under the root: a constant row c gives c / sqrt(c^2 + eps)
+    c = np.full((1, 64), 0.5)
+    zz = np.full((1, 64), 50.0)  # SiLU(50) = 50 (1 - 2e-22)
+    pins.append(np.allclose(fn(c, zz, None, 0.75), 50.0 * 0.5 / np.sqrt(0.25 + 0.75), rtol=1e-12))
+    # a zero output stays zero
+    pins.append(np.all(fn(np.zeros((1, 64)), zz, None, 1e-5) == 0.0))
+    return all(pins)
+
+
+def py_output_gate(o, z, weight, eps, mistake=None):
+    w = np.ones(o.shape[-1]) if weight is None else weight
+    axis = -2 if mistake == "token_axis" else -1
+    e = 0.0 if mistake == "drop_eps" else eps
+    ms = np.mean(o * o, axis=axis, keepdims=True)
+    rms = np.sqrt(ms) + e if mistake == "eps_outside" else np.sqrt(ms + e)
+    gate = 1.0 / (1.0 + np.exp(-z)) if mistake == "sigmoid_only" else z / (1.0 + np.exp(z) if mistake == "sign" else 1.0 + np.exp(-z))
+    return gate * (o / rms) * w
+
+
+def test_output_gate_oracle_passes_its_pins():
+    assert epilogue_pins(lambda o, z, w, eps: oracle.output_gate(o, z, w, eps))
+
+
+@pytest.mark.parametrize("mistake", ["token_axis", "drop_eps", "eps_outside", "sigmoid_only", "sign"])
+def test_output_gate_pins_reject_planted_mistakes(mistake):
+    assert not epilogue_pins(lambda o, z, w, eps: py_output_gate(o, z, w, eps, mistake))
+
+
+def test_output_gate_python_copy_passes_pins():
+    assert epilogue_pins(lambda o, z, w, eps: py_output_gate(o, z, w, eps))
