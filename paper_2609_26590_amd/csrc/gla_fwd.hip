@@ -86,6 +86,7 @@ struct GlaParams {
   const float* nw;   // RMSNorm weight [DV], or null (ones)
   int gatedt;        // dtype of gate
   float eps;         // RMSNorm epsilon
+  unsigned short* states16;  // [BH][nchunks][DV][DK] fp16 S_[c]^T (staged schedule, 16-bit inputs)
 };
 
 constexpr int tile_threads(int chunk) { return chunk / 16 * kWave; }
@@ -588,6 +589,30 @@ struct Chunk {
       }
     }
   }
+  // Staged schedule with 16-bit inputs: the scan kernel has already rounded
+  // S_[c]^T to the fp16 MFMA operand type (what state_store would do), so the
+  // output kernel moves 16-byte pieces of 8 elements straight to the tile.
+  static constexpr int SQ8 = DK * DV / 8;
+  static constexpr int SPER8 = (SQ8 + NT - 1) / NT;
+  __device__ __forceinline__ void state_load16(const unsigned short* ST, u32x4 (&buf)[SPER8]) const {
+#pragma unroll
+    for (int m = 0; m < SPER8; ++m) {
+      const int q8 = threadIdx.x + m * NT;
+      if (q8 < SQ8) buf[m] = reinterpret_cast<const u32x4*>(ST)[q8];
+    }
+  }
+  template <class S>
+  __device__ __forceinline__ void state_store16(S& sm, const u32x4 (&buf)[SPER8]) {
+    static_assert(F16 && (SP * 2) % 16 == 0, "16-byte rows of fp16 elements");
+#pragma unroll
+    for (int m = 0; m < SPER8; ++m) {
+      const int q8 = threadIdx.x + m * NT;
+      if (q8 < SQ8) {
+        const int dv = (q8 * 8) / DK, i = (q8 * 8) % DK;
+        *reinterpret_cast<u32x4*>(&sm.sT[dv * SP + i]) = buf[m];
+      }
+    }
+  }
   template <class S>
   __device__ __forceinline__ void state_store(S& sm, const f4 (&buf)[SPER]) {
 #pragma unroll
@@ -691,12 +716,15 @@ struct Chunk {
 
 // ---------------------------------------------------------------------------
 // Boundary-state scan over chunks (Eq. chunk_boundary_main) for elements
-// [e0, e1) of one sequence's state (S^T layout, element e = dv*DK + i). In
-// place: U_c^T -> S_[c]^T. S_final gets the state after the last chunk.
+// [e0, e1) of one sequence's state (S^T layout, element e = dv*DK + i). Reads
+// U_c^T and writes S_[c]^T in place (float32), or, for 16-bit inputs (H16), to
+// the fp16 states the output kernel feeds to its readout. S_final gets the
+// float32 state after the last chunk.
 // ---------------------------------------------------------------------------
-template <int DK, int DV>
+template <int DK, int DV, bool H16>
 __device__ __forceinline__ void scan_plain(const GlaParams& P, int bh, int e0, int e1, int tid, int nt) {
   float* st = P.states + (int64_t)bh * P.nchunks * (DK * DV);
+  _Float16* st16 = reinterpret_cast<_Float16*>(P.states16) + (int64_t)bh * P.nchunks * (DK * DV);
   const float* dec = P.decays + (int64_t)bh * P.nchunks * DK;
   const int NC = P.nchunks;
   for (int e = e0 + tid; e < e1; e += nt) {
@@ -714,7 +742,10 @@ __device__ __forceinline__ void scan_plain(const GlaParams& P, int bh, int e0, i
 #pragma unroll
       for (int m = 0; m < 32; ++m) {
         if (c0 + m < NC) {
-          st[(int64_t)(c0 + m) * (DK * DV) + e] = s;
+          if constexpr (H16)
+            st16[(int64_t)(c0 + m) * (DK * DV) + e] = (_Float16)s;
+          else
+            st[(int64_t)(c0 + m) * (DK * DV) + e] = s;
           s = d[m] * s + u[m];
         }
       }
@@ -769,12 +800,12 @@ __global__ void __launch_bounds__(tile_threads(C)) gla_summary_kernel(GlaParams 
   ch.template summary_out<false>(sm, P.states + sc * (DK * DV));
 }
 
-template <int DK, int DV>
+template <int DK, int DV, bool H16>
 __global__ void __launch_bounds__(256) gla_scan_kernel(GlaParams P) {
   const int bh = blockIdx.y;
   const int e0 = blockIdx.x * 256;
   const int e1 = min(e0 + 256, DK * DV);
-  scan_plain<DK, DV>(P, bh, e0, e1, threadIdx.x, 256);
+  scan_plain<DK, DV, H16>(P, bh, e0, e1, threadIdx.x, 256);
 }
 
 template <int DK, int DV, int C, int IN>
@@ -784,12 +815,24 @@ __global__ void __launch_bounds__(tile_threads(C)) gla_output_kernel(GlaParams P
   T ch;
   const int c = blockIdx.x, bh = blockIdx.y;
   const bool have_state = c > 0 || P.s0;
-  f4 sbuf[T::SPER];
-  if (have_state) ch.template state_load<false>(P.states + ((int64_t)bh * P.nchunks + c) * (DK * DV), sbuf);
+  const int64_t sc = (int64_t)bh * P.nchunks + c;
+  f4 sbuf[T::F16 ? 1 : T::SPER];
+  u32x4 hbuf[T::F16 ? T::SPER8 : 1];
+  if (have_state) {
+    if constexpr (T::F16)
+      ch.state_load16(P.states16 + sc * (DK * DV), hbuf);
+    else
+      ch.template state_load<false>(P.states + sc * (DK * DV), sbuf);
+  }
   ch.template load<true>(P, sm, bh, c);
   Raw rz[T::SITER];
   if (P.gate) ch.prefetch_gate(P, bh, c, rz);
-  if (have_state) ch.state_store(sm, sbuf);
+  if (have_state) {
+    if constexpr (T::F16)
+      ch.state_store16(sm, hbuf);
+    else
+      ch.state_store(sm, sbuf);
+  }
   ch.template factors<true, false, false>(sm, nullptr);
   f4 O[DV / 16];
   ch.intra(P, sm, bh, c, O);
@@ -983,7 +1026,7 @@ static KernelSet kernels_for() {
                    reinterpret_cast<const void*>(&gla_output_kernel<DK, DV, C, IN>),
                    reinterpret_cast<const void*>(&gla_fused_kernel<DK, DV, C, IN, false>),
                    reinterpret_cast<const void*>(&gla_fused_kernel<DK, DV, C, IN, true>),
-                   reinterpret_cast<const void*>(&gla_scan_kernel<DK, DV>), tile_threads(C)};
+                   reinterpret_cast<const void*>(&gla_scan_kernel<DK, DV, IN != GTR_F32>), tile_threads(C)};
 }
 
 template <int DK, int DV, int IN>
@@ -1111,6 +1154,7 @@ extern "C" gtr_status gtr_gla_fwd(const gtr_gla_args* a, hipStream_t stream) {
   P.sync = reinterpret_cast<unsigned*>(ws + lay.sync_off);
   P.states = reinterpret_cast<float*>(ws + lay.states_off);
   P.decays = reinterpret_cast<float*>(ws + lay.decays_off);
+  P.states16 = lay.states16_off ? reinterpret_cast<unsigned short*>(ws + lay.states16_off) : nullptr;
   P.groups = (int)((s.BH + 7) / 8);
   P.gkind = a->g_kind;
   P.inv_tau = a->g_kind == GTR_GATE_LOGITS ? 1.f / a->gate_tau : 1.f;

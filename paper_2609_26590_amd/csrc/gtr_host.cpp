@@ -118,6 +118,11 @@ WorkspaceLayout gla_workspace_layout(const GlaShape& s) {
   off = align256(off + (size_t)s.BH * s.nchunks * s.dk * s.dv * sizeof(float));
   w.decays_off = off;
   off = align256(off + (size_t)s.BH * s.nchunks * s.dk * sizeof(float));
+  w.states16_off = 0;
+  if (s.qdt != GTR_F32) {
+    w.states16_off = off;
+    off = align256(off + (size_t)s.BH * s.nchunks * s.dk * s.dv * 2);
+  }
   w.total = off;
   return w;
 }

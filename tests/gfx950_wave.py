@@ -1485,13 +1485,13 @@ def gaddr(w, i, vaddr_tok, saddr_tok):
     return a, v.d & sd, v.o | bool(so)
 
 
-def gload(nregs):
+def gload(nregs, nbytes=None):
     def h(w, i):
         dst, vaddr = i.ops[0], i.ops[1]
         saddr = i.ops[2] if len(i.ops) > 2 else 'off'
         lanes = w.active()
         a, d, o = gaddr(w, i, vaddr, saddr)
-        rg = w.check_addr(i, a, d, o, 4 * nregs, 'r', lanes)
+        rg = w.check_addr(i, a, d, o, nbytes or 4 * nregs, 'r', lanes)
         if rg is not None and rg.load_value is not None:
             r = w.vidx(dst)
             for j in range(r[0], r[1] + 1):
@@ -1503,13 +1503,13 @@ def gload(nregs):
     return h
 
 
-def gstore(nregs):
+def gstore(nregs, nbytes=None):
     def h(w, i):
         vaddr, data = i.ops[0], i.ops[1]
         saddr = i.ops[2] if len(i.ops) > 2 else 'off'
         lanes = w.active()
         a, d, o = gaddr(w, i, vaddr, saddr)
-        w.check_addr(i, a, d, o, 4 * nregs, 'w', lanes)
+        w.check_addr(i, a, d, o, nbytes or 4 * nregs, 'w', lanes)
         w.check_data(i, data, lanes, nregs)
     return h
 
@@ -1533,10 +1533,12 @@ def gatomic(w, i):
 
 
 HANDLERS.update({'global_load_dword': gload(1), 'global_load_dwordx2': gload(2), 'global_load_dwordx3': gload(3),
-                 'global_load_dwordx4': gload(4), 'global_load_ushort': gload(1),
+                 'global_load_dwordx4': gload(4), 'global_load_ushort': gload(1, 2),
+                 'global_load_short_d16': gload(1, 2), 'global_load_short_d16_hi': gload(1, 2),
                  'global_store_dword': gstore(1), 'global_store_dwordx2': gstore(2),
                  'global_store_dwordx3': gstore(3), 'global_store_dwordx4': gstore(4),
-                 'global_store_short': gstore(1), 'global_store_short_d16_hi': gstore(1)})
+                 'global_store_short': gstore(1, 2), 'global_store_short_d16_hi': gstore(1, 2),
+                 'global_store_byte': gstore(1, 1)})
 PREFIX_HANDLERS.append(('global_atomic_', gatomic))
 
 

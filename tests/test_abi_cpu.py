@@ -79,7 +79,8 @@ def fwd(lib, a):
 def test_workspace_size_formula(lib):
     a = base_args(B=2, heads=3, H=40, W=40, dk=64, dv=64, chunk=64)
     BH, nc = 6, 25
-    want = 256 + 1024 * 16 + BH * nc * 64 * 64 * 4 + ((BH * nc * 64 * 4 + 255) // 256) * 256
+    # header, counters of 1024 sequences, float32 states, decays, fp16 states (16-bit inputs)
+    want = 256 + 1024 * 16 + BH * nc * 64 * 64 * 4 + ((BH * nc * 64 * 4 + 255) // 256) * 256 + BH * nc * 64 * 64 * 2
     assert lib.gtr_gla_workspace_size(ctypes.byref(a)) == want
     a.dk = 48
     assert lib.gtr_gla_workspace_size(ctypes.byref(a)) == 0

@@ -90,7 +90,7 @@ def test_emulator_flags_out_of_bounds():
 # ---------------------------------------------------------------------------
 DT = {"f32": (0, 4), "f16": (1, 2), "bf16": (2, 2)}
 SCAN = {"row": 0, "col": 1, "row_rev": 2, "col_rev": 3}
-KERNARG_BYTES = 176  # sizeof(GlaParams)
+KERNARG_BYTES = 184  # sizeof(GlaParams)
 
 
 def a256(x):
@@ -160,16 +160,17 @@ def kernel_args(c: Shape):
     sync = 256
     states = a256(sync + 1024 * 16)  # counters of up to 1024 sequences, a fixed region
     decays = a256(states + c.BH * c.NC * c.dk * c.dv * 4)
-    total = a256(decays + c.BH * c.NC * c.dk * 4)
+    states16 = a256(decays + c.BH * c.NC * c.dk * 4)
+    total = a256(states16 + (c.BH * c.NC * c.dk * c.dv * 2 if c.dt != "f32" else 0))
     ws = alloc("workspace", total, "rw")
     # hand-off counters read as complete, so every bounded wait ends at once
     regions.insert(0, emu.Region("sync", ws + sync, c.BH * 16, "rw", load_value=0x7FFFFFFF))
     regions.insert(0, emu.Region("fault", ws, 256, "rw"))
     regions.append(emu.Region("kernarg", emu.KERNARG_BASE, KERNARG_BYTES, "r"))
-    kern = struct.pack("<7Q6iqifi4xQQQQiif4xQQif", q, k, v, g, o, s0, sf, DT[c.dt][0], DT[c.gdt][0],
+    kern = struct.pack("<7Q6iqifi4xQQQQiif4xQQifQ", q, k, v, g, o, s0, sf, DT[c.dt][0], DT[c.gdt][0],
                        DT[c.odt][0], c.BH, c.H, c.W, c.L, c.NC, c.dk ** -0.5, SCAN[c.scan], ws + states,
                        ws + decays, ws + sync, ws, (c.BH + 7) // 8, 1 if c.logits else 0, 1.0 / 16,
-                       z, nw, DT[c.zdt][0] if c.zdt else 0, 1e-5)
+                       z, nw, DT[c.zdt][0] if c.zdt else 0, 1e-5, ws + states16 if c.dt != "f32" else 0)
     assert len(kern) == KERNARG_BYTES
     return kern, regions
 
@@ -181,7 +182,7 @@ def mangled(kind: str, c: Shape) -> str:
     if kind == "output":
         return f"_ZN3gtr17gla_output_kernel{t}EEvNS_9GlaParamsE"
     if kind == "scan":
-        return f"_ZN3gtr15gla_scan_kernelILi{c.dk}ELi{c.dv}EEEvNS_9GlaParamsE"
+        return f"_ZN3gtr15gla_scan_kernelILi{c.dk}ELi{c.dv}ELb{int(c.dt != 'f32')}EEEvNS_9GlaParamsE"
     return f"_ZN3gtr16gla_fused_kernel{t}Lb{1 if kind == 'inline' else 0}EEEvNS_9GlaParamsE"
 
 
