@@ -134,6 +134,35 @@ def setup(wl, path, scan=None, sets=1, fusions=False):
     return step
 
 
+def swiglu_detail():
+    """Spatial SwiGLU (Sec. 3.1) at the GTR-L and GTR-X widths on the 40x40 grid, fp16."""
+    res = {}
+    dev = torch.device("cuda")
+    for name, d, h in (("swiglu GTR-L d384 h1536", 384, 1536), ("swiglu GTR-X d384 h2304", 384, 2304)):
+        gen = torch.Generator().manual_seed(d + h)
+        M = 1600
+        x = torch.randn((1, M, d), generator=gen).half().to(dev)
+        wg = (torch.randn((h, d), generator=gen) * d ** -0.5).half().to(dev)
+        wv = (torch.randn((h, d), generator=gen) * d ** -0.5).half().to(dev)
+        wo = (torch.randn((d, h), generator=gen) * h ** -0.5).half().to(dev)
+        cw = (torch.randn((h, 3, 3), generator=gen) / 3).to(dev)
+        cb = (torch.randn(h, generator=gen) * 0.1).to(dev)
+        y = torch.empty((1, M, d), dtype=torch.float16, device=dev)
+        ws = gtr.Workspace(dev)
+
+        def step(i=0):
+            gtr.gtr_spatial_swiglu(x, wg, wv, wo, cw, cb, H=40, W=40, out=y, workspace=ws)
+
+        step()
+        torch.cuda.synchronize()
+        t = time_graph(step, 100, 10) / 100
+        flops = 2.0 * M * d * 2 * h + 2.0 * M * h * d + 18.0 * M * h
+        nbytes = M * d * 2 * 2 + 3 * h * d * 2 + h * 40
+        res[name] = {"us_per_call": t * 1e6, "tflops": flops / t / 1e12,
+                     "mfma_frac": flops / t / 1e12 / MFMA_F16_PEAK_TFLOPS, "alg_GBps": nbytes / t / 1e9}
+    return res
+
+
 def time_graph(step, steps, warmup):
     for i in range(warmup):
         step(i)
@@ -251,6 +280,8 @@ def main():
             det[f"{name}+fusions"] = {"us_per_call": s2 * 1e6, "tokens_per_s": w2.B * w2.L / s2,
                                       "GBps": b2 / s2 / 1e9, "hbm_frac": b2 / s2 / 1e9 / HBM_PEAK_GBS}
         out["detail"] = det
+    if a.detail:
+        out["detail"].update(swiglu_detail())
     if not a.no_cpu:
         out["cpu_baseline"] = cpu_baseline(wl, a.cpu_seconds)
     print(json.dumps(out), flush=True)

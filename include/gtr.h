@@ -198,6 +198,49 @@ gtr_status gtr_gla_workspace_init(void* workspace, size_t bytes, hipStream_t str
  */
 gtr_status gtr_gla_fwd(const gtr_gla_args* args, hipStream_t stream);
 
+/*
+ * Spatial SwiGLU (Sec. 3.1, "Spatial SwiGLU"; the scope table's row f4):
+ *   Y = [SiLU(X W_g) * DWConv3x3(X W_v)] W_o
+ * for every image b: X = x[b] is [H*W, d] in SPATIAL (row-major grid) order, the
+ * value branch X W_v is convolved depthwise over the H x W grid (3 x 3,
+ * cross-correlation, zero padding, optional bias), the gate is tokenwise.
+ *
+ * x       : [B, H*W, d]           dtype
+ * w_gate  : [hidden, d]           dtype (linear-layer layout, output features first)
+ * w_value : [hidden, d]           dtype
+ * w_out   : [d, hidden]           dtype
+ * conv_w  : [hidden, 3, 3]        float32, conv_w[c][u][v] weighs the token at
+ *                                 grid offset (u - 1, v - 1)
+ * conv_b  : [hidden] float32 or NULL
+ * y       : [B, H*W, d]           y_dtype (dtype or GTR_F32); must not overlap
+ *                                 the inputs or the workspace
+ * dtype   : GTR_F16 or GTR_BF16; d and hidden multiples of 64; every pointer
+ *           16-byte aligned.
+ * The products accumulate in float32; X W_g and X W_v are kept in float32, the
+ * gated hidden activations are rounded to fp16 for the output product (so they
+ * must stay finite in fp16).
+ * workspace : caller-owned, 256-byte aligned, gtr_spatial_swiglu_workspace_size
+ *           bytes (B*H*W*hidden*10 rounded up); no initialisation needed.
+ * Errors as for gtr_gla_fwd; every check runs before any launch.
+ */
+typedef struct {
+  const void* x;
+  const void* w_gate;
+  const void* w_value;
+  const void* w_out;
+  const float* conv_w;
+  const float* conv_b;
+  void* y;
+  gtr_dtype dtype;
+  gtr_dtype y_dtype;
+  int32_t B, H, W, d, hidden;
+  void* workspace;
+  size_t workspace_bytes;
+} gtr_swiglu_args;
+
+size_t gtr_spatial_swiglu_workspace_size(const gtr_swiglu_args* args);
+gtr_status gtr_spatial_swiglu(const gtr_swiglu_args* args, hipStream_t stream);
+
 /* Nonzero if a fused-path call on this workspace gave up waiting for the other
  * chunks of a sequence (a bounded wait ran out); the output of that call is not
  * valid. Reads the flag with a blocking device-to-host copy - a diagnostic for

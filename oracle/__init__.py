@@ -14,6 +14,8 @@ input module, which holds no arithmetic of the method).
 * :func:`log_decay_from_logits` - the retention gate of Sec. 3.1,
   gamma = sigmoid(a)^(1/tau), as the log-decay g = log gamma the recurrence uses.
 * :func:`output_gate` - the output gate of Sec. 3.1, u = SiLU(x W_r) * RMSNorm(o).
+* :func:`spatial_swiglu` (with :func:`dwconv3x3`) - the Spatial SwiGLU of Sec. 3.1,
+  Y = [SiLU(X W_g) * DWConv3x3(X W_v)] W_o on the patch grid.
 
 Readings taken where the paper is not explicit (each is listed with its reason
 in the design notes of the repository):
@@ -26,7 +28,9 @@ in the design notes of the repository):
 * ``scale`` is explicit; the paper's value is d_k^{-1/2};
 * RMSNorm of the output gate normalises each token of each head over its d_v
   channels, with an explicit epsilon and an optional per-channel weight (the
-  paper names RMSNorm without its axis or epsilon).
+  paper names RMSNorm without its axis or epsilon);
+* the depthwise convolution of Spatial SwiGLU is a cross-correlation (as in
+  common deep-learning libraries) with zero padding and an optional bias.
 """
 from __future__ import annotations
 
@@ -170,3 +174,38 @@ def output_gate(o, z, weight=None, eps: float = 1e-5) -> np.ndarray:
     rms = np.sqrt(np.mean(o * o, axis=-1, keepdims=True) + float(eps))
     silu = z / (1.0 + np.exp(-z))
     return silu * (o / rms) * w
+
+
+def dwconv3x3(v, conv_w, conv_b=None, *, H: int, W: int) -> np.ndarray:
+    """Depthwise 3x3 convolution of token features on the H x W patch grid (Sec. 3.1,
+    Spatial SwiGLU): v [B, H*W, C] in row-major grid order, conv_w [C, 3, 3],
+    zero padding, out[b, i, j, c] = sum_{u, w in 0..2} v[b, i+u-1, j+w-1, c] conv_w[c, u, w]
+    (+ conv_b[c]); written as the nine shifted copies of the grid, one term each."""
+    v = _f64(v)
+    B, L, C = v.shape
+    if L != H * W:
+        raise ValueError("L must equal H*W")
+    grid = v.reshape(B, H, W, C)
+    pad = np.zeros((B, H + 2, W + 2, C))
+    pad[:, 1:H + 1, 1:W + 1] = grid
+    cw = _f64(conv_w)
+    out = np.zeros((B, H, W, C))
+    for u in range(3):
+        for w_ in range(3):
+            out += pad[:, u:u + H, w_:w_ + W, :] * cw[:, u, w_]
+    if conv_b is not None:
+        out += _f64(conv_b)
+    return out.reshape(B, L, C)
+
+
+def spatial_swiglu(x, w_gate, w_value, w_out, conv_w, conv_b=None, *, H: int, W: int) -> np.ndarray:
+    """Y = [SiLU(X W_g) * DWConv3x3(X W_v)] W_o (Sec. 3.1, Spatial SwiGLU), float64.
+
+    x [B, H*W, d] in row-major grid order; weights in the layout of a linear
+    layer (output features first): w_gate, w_value [h, d], w_out [d, h];
+    conv_w [h, 3, 3], conv_b [h] or None. Returns y [B, H*W, d]."""
+    x = _f64(x)
+    g = x @ _f64(w_gate).T
+    v = x @ _f64(w_value).T
+    hidden = (g / (1.0 + np.exp(-g))) * dwconv3x3(v, conv_w, conv_b, H=H, W=W)
+    return hidden @ _f64(w_out).T

@@ -13,6 +13,8 @@ Entry points (same names as the C ABI in ``include/gtr.h``):
   (Sec. 3.1, evaluated with the chunkwise schedule of Sec. 3.3).
 * :func:`gtr_gla_workspace_size`, :func:`gtr_gla_workspace_init`,
   :func:`gtr_gla_workspace_fault`, :func:`gtr_status_string`.
+* :func:`gtr_spatial_swiglu` - the Spatial SwiGLU channel mixer (Sec. 3.1),
+  with :func:`gtr_spatial_swiglu_workspace_size` in the C ABI.
 
 :class:`Workspace` keeps a caller-owned, zero-initialised workspace buffer.
 """
@@ -37,7 +39,8 @@ _DT = {torch.float32: F32, torch.float16: F16, torch.bfloat16: BF16}
 _DT_BACK = {F32: torch.float32, F16: torch.float16, BF16: torch.bfloat16}
 
 EXPORTS = ("gtr_scan_permute", "gtr_gla_workspace_size", "gtr_gla_workspace_init", "gtr_gla_fwd",
-           "gtr_gla_workspace_fault", "gtr_status_string")
+           "gtr_gla_workspace_fault", "gtr_status_string", "gtr_spatial_swiglu_workspace_size",
+           "gtr_spatial_swiglu")
 
 
 class GtrError(RuntimeError):
@@ -60,6 +63,17 @@ class GlaArgs(ctypes.Structure):
         ("g_kind", ctypes.c_int), ("gate_tau", ctypes.c_float),
         ("out_gate", ctypes.c_void_p), ("out_gate_dtype", ctypes.c_int),
         ("norm_eps", ctypes.c_float), ("norm_weight", ctypes.c_void_p),
+    ]
+
+
+class SwigluArgs(ctypes.Structure):
+    """Mirror of ``gtr_swiglu_args`` (include/gtr.h)."""
+    _fields_ = [
+        ("x", ctypes.c_void_p), ("w_gate", ctypes.c_void_p), ("w_value", ctypes.c_void_p),
+        ("w_out", ctypes.c_void_p), ("conv_w", ctypes.c_void_p), ("conv_b", ctypes.c_void_p),
+        ("y", ctypes.c_void_p), ("dtype", ctypes.c_int), ("y_dtype", ctypes.c_int),
+        ("B", ctypes.c_int32), ("H", ctypes.c_int32), ("W", ctypes.c_int32), ("d", ctypes.c_int32),
+        ("hidden", ctypes.c_int32), ("workspace", ctypes.c_void_p), ("workspace_bytes", ctypes.c_size_t),
     ]
 
 
@@ -89,6 +103,10 @@ def load(path: Optional[str] = None) -> ctypes.CDLL:
     lib.gtr_gla_workspace_fault.restype = ctypes.c_int
     lib.gtr_status_string.argtypes = [ctypes.c_int]
     lib.gtr_status_string.restype = ctypes.c_char_p
+    lib.gtr_spatial_swiglu_workspace_size.argtypes = [ctypes.POINTER(SwigluArgs)]
+    lib.gtr_spatial_swiglu_workspace_size.restype = ctypes.c_size_t
+    lib.gtr_spatial_swiglu.argtypes = [ctypes.POINTER(SwigluArgs), P]
+    lib.gtr_spatial_swiglu.restype = ctypes.c_int
     _lib = lib
     return lib
 
@@ -232,3 +250,38 @@ def gtr_gla_fwd(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, g: torch.Tens
     if st:
         raise GtrError("gtr_gla_fwd", st)
     return o, sf
+
+
+def gtr_spatial_swiglu(x: torch.Tensor, w_gate: torch.Tensor, w_value: torch.Tensor, w_out: torch.Tensor,
+                       conv_w: torch.Tensor, conv_b: Optional[torch.Tensor] = None, *, H: int, W: int,
+                       y_dtype: Optional[torch.dtype] = None, out: Optional[torch.Tensor] = None,
+                       workspace: Optional["Workspace"] = None, stream=None) -> torch.Tensor:
+    """Spatial SwiGLU (Sec. 3.1): y = [SiLU(x W_g^T) * DWConv3x3(x W_v^T)] W_o^T.
+
+    x [B, H*W, d] (fp16/bf16, spatial order), w_gate/w_value [hidden, d],
+    w_out [d, hidden] (same dtype), conv_w [hidden, 3, 3] and conv_b [hidden]
+    float32. Returns y [B, H*W, d] in ``y_dtype`` (default: x's dtype).
+    """
+    for name, t in (("x", x), ("w_gate", w_gate), ("w_value", w_value), ("w_out", w_out), ("conv_w", conv_w)) + \
+            ((("conv_b", conv_b),) if conv_b is not None else ()):
+        if not t.is_cuda or not t.is_contiguous():
+            raise ValueError(f"{name} must be a contiguous device tensor")
+    B, L, d = x.shape
+    y = out if out is not None else torch.empty((B, L, d), dtype=y_dtype or x.dtype, device=x.device)
+    a = SwigluArgs()
+    a.x, a.w_gate, a.w_value, a.w_out = _ptr(x), _ptr(w_gate), _ptr(w_value), _ptr(w_out)
+    a.conv_w, a.conv_b, a.y = _ptr(conv_w), _ptr(conv_b), _ptr(y)
+    a.dtype, a.y_dtype = _DT[x.dtype], _DT[y.dtype]
+    a.B, a.H, a.W, a.d, a.hidden = B, H, W, d, w_gate.shape[0]
+    lib = load()
+    need = int(lib.gtr_spatial_swiglu_workspace_size(ctypes.byref(a)))
+    if need == 0:
+        raise GtrError("gtr_spatial_swiglu_workspace_size", 2)
+    if workspace is None:
+        workspace = _default_ws.setdefault(("swiglu", x.device), Workspace(x.device))
+    buf = workspace.get(need, stream)
+    a.workspace, a.workspace_bytes = buf.data_ptr(), buf.numel()
+    st = lib.gtr_spatial_swiglu(ctypes.byref(a), _stream_ptr(stream))
+    if st:
+        raise GtrError("gtr_spatial_swiglu", st)
+    return y

@@ -761,6 +761,14 @@ def logic64(kind):
         elif kind == 'orn2':
             nb = bit_not(b[0], b[1])
             v, o = bit_or(a[0], a[1], nb[0], nb[1])
+        elif kind == 'nor':
+            v, o = bit_or(a[0], a[1], b[0], b[1])
+            v, o = bit_not(v, o)
+        elif kind == 'nand':
+            v, o = bit_and(a[0], a[1], b[0], b[1])
+            v, o = bit_not(v, o)
+        elif kind == 'xnor':
+            v, o = (~(a[0] ^ b[0])) & M64, a[1] | b[1]
         d = a[2] and b[2]
         if dst == 'exec':
             set_exec(w, i, v, o, d)
@@ -776,7 +784,8 @@ def logic64(kind):
 
 
 HANDLERS.update({'s_and_b64': logic64('and'), 's_or_b64': logic64('or'), 's_xor_b64': logic64('xor'),
-                 's_andn2_b64': logic64('andn2'), 's_orn2_b64': logic64('orn2')})
+                 's_andn2_b64': logic64('andn2'), 's_orn2_b64': logic64('orn2'), 's_nor_b64': logic64('nor'),
+                 's_nand_b64': logic64('nand'), 's_xnor_b64': logic64('xnor')})
 
 
 def saveexec(kind):

@@ -244,3 +244,58 @@ def test_epilogue_gate_must_not_overlap_output(lib):
     a = epilogue_args()
     a.norm_weight = a.o
     assert fwd(lib, a) == ALIAS
+
+
+# ---------------------------------------------------------------------------
+# gtr_spatial_swiglu
+# ---------------------------------------------------------------------------
+
+def swiglu_args(B=1, H=4, W=5, d=64, hidden=128, dt=gtr.F16):
+    a = gtr.SwigluArgs()
+    M = B * H * W
+    step = 1 << 30
+    a.x, a.w_gate, a.w_value, a.w_out = FAKE, FAKE + step, FAKE + 2 * step, FAKE + 3 * step
+    a.conv_w, a.conv_b, a.y = FAKE + 4 * step, None, FAKE + 5 * step
+    a.dtype, a.y_dtype = dt, dt
+    a.B, a.H, a.W, a.d, a.hidden = B, H, W, d, hidden
+    need = gtr.load().gtr_spatial_swiglu_workspace_size(ctypes.byref(a))
+    a.workspace, a.workspace_bytes = FAKE + 6 * step, need
+    return a
+
+
+def sw(lib, a):
+    return lib.gtr_spatial_swiglu(ctypes.byref(a), None)
+
+
+def test_swiglu_workspace_size(lib):
+    a = swiglu_args(B=2, H=40, W=40, d=384, hidden=1536)
+    M = 2 * 1600
+    a256 = lambda x: (x + 255) // 256 * 256
+    assert lib.gtr_spatial_swiglu_workspace_size(ctypes.byref(a)) == a256(a256(a256(M * 1536 * 4) + M * 1536 * 4)
+                                                                             + M * 1536 * 2)
+
+
+@pytest.mark.parametrize("field,val,want", [("B", 0, SHAPE), ("H", -1, SHAPE), ("d", 48, UNSUP),
+                                            ("hidden", 100, UNSUP), ("dtype", gtr.F32, UNSUP)])
+def test_swiglu_bad_arguments(lib, field, val, want):
+    a = swiglu_args()
+    setattr(a, field, val)
+    assert sw(lib, a) == want
+
+
+def test_swiglu_nulls_alignment_alias_workspace(lib):
+    a = swiglu_args()
+    a.w_out = None
+    assert sw(lib, a) == NULL
+    a = swiglu_args()
+    a.conv_b = FAKE + 8
+    assert sw(lib, a) == UNSUP
+    a = swiglu_args()
+    a.y = a.x  # output over the input
+    assert sw(lib, a) == ALIAS
+    a = swiglu_args()
+    a.workspace_bytes -= 256
+    assert sw(lib, a) == WS
+    a = swiglu_args()
+    a.y_dtype = gtr.BF16  # neither fp16 (the input dtype) nor float32
+    assert sw(lib, a) == UNSUP

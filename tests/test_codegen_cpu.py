@@ -249,3 +249,74 @@ def test_gla_kernel_addresses(asm_text, case):
         bad = {k: sorted(v)[:4] for k, v in rep.items.items() if k.startswith(("ERR", "WARN", "NOTIMPL"))}
         assert not bad, f"{kind}: {bad}"
         assert "INFO-PATHLIMIT" not in rep.counts, f"{kind}: not every branch outcome was explored"
+
+
+# ---------------------------------------------------------------------------
+# Spatial SwiGLU kernels (swiglu.hip)
+# ---------------------------------------------------------------------------
+def swiglu_asm() -> str:
+    from paper_2609_26590_amd import build as b
+    src = os.path.join(CSRC, "swiglu.hip")
+    h = hashlib.sha256()
+    for f in ("swiglu.hip", "gtr_device.h", "gtr_internal.h"):
+        with open(os.path.join(CSRC, f), "rb") as fh:
+            h.update(fh.read())
+    with open(os.path.join(ROOT, "include", "gtr.h"), "rb") as fh:
+        h.update(fh.read())
+    h.update(" ".join(b.HIPCC_FLAGS).encode())
+    os.makedirs(BUILD, exist_ok=True)
+    path = os.path.join(BUILD, f"swiglu.gfx950.{h.hexdigest()[:16]}.s")
+    if not os.path.exists(path):
+        tmp = path + f".tmp{os.getpid()}"
+        r = subprocess.run([b._hipcc(), *b.HIPCC_FLAGS, "-S", "--cuda-device-only", src, "-o", tmp],
+                           capture_output=True, text=True)
+        assert r.returncode == 0, r.stderr[-2000:]
+        os.replace(tmp, path)
+    with open(path) as fh:
+        return fh.read()
+
+
+def check_kernel(text, name, kern, regions, wgs, waves=4):
+    prog, labels, desc = emu.parse_kernel(text, name)
+    rep = emu.Report()
+    for wg in wgs:
+        for wave in range(waves):
+            emu.run_wave(prog, labels, desc, kern, regions, desc["amdhsa_group_segment_fixed_size"], wg, wave, rep)
+    bad = {k: sorted(v)[:4] for k, v in rep.items.items() if k.startswith(("ERR", "WARN", "NOTIMPL"))}
+    assert not bad, f"{name}: {bad}"
+    assert "INFO-PATHLIMIT" not in rep.counts
+
+
+@pytest.mark.parametrize("adt,bdt,mt,M,N,K,cdt", [(2, 2, 2, 126, 128, 64, 0), (1, 1, 1, 1600, 384, 1536, 1),
+                                                  (1, 2, 1, 63, 64, 128, 2)])
+def test_swiglu_gemm_addresses(adt, bdt, mt, M, N, K, cdt):
+    text = swiglu_asm()
+    base = 0x1000_0000_0000
+    es = {0: 4, 1: 2, 2: 2}
+    A, B0, B1, C0, C1 = (base + i * 0x10_0000_0000 for i in range(5))
+    regions = [emu.Region("A", A, M * K * 2, "r"), emu.Region("B0", B0, N * K * 2, "r"),
+               emu.Region("B1", B1, N * K * 2, "r"), emu.Region("C0", C0, M * N * es[cdt], "w"),
+               emu.Region("C1", C1, M * N * es[cdt], "w"), emu.Region("kernarg", emu.KERNARG_BASE, 56, "r")]
+    kern = struct.pack("<QQQQQiiii", A, B0, B1, C0, C1, M, N, K, cdt)
+    name = f"_ZN3gtr14gemm_nt_kernelILi{adt}ELi{bdt}ELi{mt}EEEvNS_8GemmArgsE"
+    assert name in emu.kernel_names(text)
+    gx, gy = (M + 63) // 64, N // 64
+    wgs = [(x, y, z) for x in sorted({0, gx - 1}) for y in sorted({0, gy - 1}) for z in (0, 1)]
+    check_kernel(text, name, kern, regions, wgs)
+
+
+def test_swiglu_conv_gate_addresses():
+    text = swiglu_asm()
+    B, H, W, hidden = 2, 7, 9, 128
+    M = B * H * W
+    base = 0x1000_0000_0000
+    G, V, CW, CB, HO = (base + i * 0x10_0000_0000 for i in range(5))
+    regions = [emu.Region("G", G, M * hidden * 4, "r"), emu.Region("V", V, M * hidden * 4, "r"),
+               emu.Region("cw", CW, hidden * 9 * 4, "r"), emu.Region("cb", CB, hidden * 4, "r"),
+               emu.Region("H", HO, M * hidden * 2, "w"), emu.Region("kernarg", emu.KERNARG_BASE, 56, "r")]
+    kern = struct.pack("<QQQQQiiii", G, V, CW, CB, HO, B, H, W, hidden)
+    name = "_ZN3gtr16conv_gate_kernelEPKfS1_S1_S1_PDF16_iiii"
+    names = emu.kernel_names(text)
+    name = [n for n in names if "conv_gate_kernel" in n][0]
+    nblk = (M * hidden // 8 + 255) // 256
+    check_kernel(text, name, kern, regions, [(0, 0, 0), (nblk // 2, 0, 0), (nblk - 1, 0, 0)])

@@ -366,3 +366,37 @@ def test_workspace_shared_across_shapes(gtr):
         run(small, first_path)  # a smaller call writes its chunk states
         o = run(big, big_path)
         assert rel_err(o, ref_big) <= tol_for(big.dtype, big.odtype), (first_path, big_path)
+
+
+# ---------------------------------------------------------------------------
+# scope row f4: Spatial SwiGLU, against the oracle's definition
+# ---------------------------------------------------------------------------
+SWIGLU = [
+    # B, H, W, d, hidden, dtype, y dtype, bias
+    (1, 40, 40, 384, 1536, "f16", "f16", True),     # GTR-L block at 640 x 640
+    (1, 40, 40, 384, 1536, "bf16", "f32", True),
+    (2, 7, 9, 64, 128, "f16", "f32", False),        # odd grid, partial 64-row tile, B = 2
+    (1, 1, 1, 64, 64, "bf16", "bf16", True),        # a single token: every neighbour is padding
+    (1, 16, 16, 192, 768, "f16", "f16", True),      # GTR-S width
+]
+
+
+@pytest.mark.parametrize("case", range(len(SWIGLU)))
+def test_spatial_swiglu_parity(gtr, case):
+    B, H, W, d, h, dt, ydt, bias = SWIGLU[case]
+    rng = np.random.default_rng(700 + case)
+    td = torch_dtype(dt)
+    x = torch.from_numpy(rng.normal(0.0, 1.0, size=(B, H * W, d))).float().to(td)
+    wg = torch.from_numpy(rng.normal(0.0, d ** -0.5, size=(h, d))).float().to(td)
+    wv = torch.from_numpy(rng.normal(0.0, d ** -0.5, size=(h, d))).float().to(td)
+    wo = torch.from_numpy(rng.normal(0.0, h ** -0.5, size=(d, h))).float().to(td)
+    cw = torch.from_numpy(rng.normal(0.0, 1.0 / 3.0, size=(h, 3, 3))).float()
+    cb = torch.from_numpy(rng.normal(0.0, 0.1, size=h)).float() if bias else None
+    dev = torch.device("cuda")
+    y = gtr.gtr_spatial_swiglu(x.to(dev), wg.to(dev), wv.to(dev), wo.to(dev), cw.to(dev),
+                               None if cb is None else cb.to(dev), H=H, W=W, y_dtype=torch_dtype(ydt))
+    torch.cuda.synchronize()
+    ref = oracle.spatial_swiglu(x, wg, wv, wo, cw, cb, H=H, W=W)
+    tol = 2e-3 + (2.0 ** -8 if ydt == "bf16" else 0.0)
+    assert y.dtype == torch_dtype(ydt)
+    assert rel_err(y, ref) <= tol, rel_err(y, ref)

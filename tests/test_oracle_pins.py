@@ -422,3 +422,84 @@ def test_output_gate_pins_reject_planted_mistakes(mistake):
 
 def test_output_gate_python_copy_passes_pins():
     assert epilogue_pins(lambda o, z, w, eps: py_output_gate(o, z, w, eps))
+
+
+# ---------------------------------------------------------------------------
+# Spatial SwiGLU (Sec. 3.1): Y = [SiLU(X W_g) * DWConv3x3(X W_v)] W_o
+# ---------------------------------------------------------------------------
+
+def test_dwconv_matches_scipy_per_channel():
+    from scipy.signal import correlate2d
+    rng = np.random.default_rng(21)
+    B, H, W, C = 2, 5, 7, 3
+    v = rng.normal(size=(B, H * W, C))
+    cw = rng.normal(size=(C, 3, 3))
+    cb = rng.normal(size=C)
+    out = oracle.dwconv3x3(v, cw, cb, H=H, W=W)
+    for b in range(B):
+        for c in range(C):
+            want = correlate2d(v[b, :, c].reshape(H, W), cw[c], mode="same", boundary="fill", fillvalue=0) + cb[c]
+            np.testing.assert_allclose(out[b, :, c].reshape(H, W), want, rtol=1e-13, atol=1e-13)
+
+
+def test_dwconv_is_not_its_flip():
+    # a kernel with one off-centre tap moves features in a known direction:
+    # out[i, j] = v[i - 1, j + 1] for the tap at (u, w) = (0, 2)
+    H, W = 4, 5
+    v = np.arange(H * W, dtype=float).reshape(1, H * W, 1) + 1
+    cw = np.zeros((1, 3, 3))
+    cw[0, 0, 2] = 1.0
+    out = oracle.dwconv3x3(v, cw, H=H, W=W).reshape(H, W)
+    g = v.reshape(H, W)
+    assert out[2, 1] == g[1, 2] and out[0, 1] == 0.0 and out[1, W - 1] == 0.0
+
+
+def swiglu_weights(rng, d, h):
+    return (rng.normal(size=(h, d)) / np.sqrt(d), rng.normal(size=(h, d)) / np.sqrt(d),
+            rng.normal(size=(d, h)) / np.sqrt(h), rng.normal(size=(h, 3, 3)) / 3.0, rng.normal(size=h) * 0.1)
+
+
+def test_spatial_swiglu_with_identity_conv_is_plain_swiglu():
+    from scipy.special import expit
+    rng = np.random.default_rng(22)
+    B, H, W, d, h = 1, 3, 4, 8, 16
+    x = rng.normal(size=(B, H * W, d))
+    wg, wv, wo, _, _ = swiglu_weights(rng, d, h)
+    ident = np.zeros((h, 3, 3))
+    ident[:, 1, 1] = 1.0
+    y = oracle.spatial_swiglu(x, wg, wv, wo, ident, None, H=H, W=W)
+    # the textbook SwiGLU, token by token with explicit sums
+    want = np.zeros_like(y)
+    for t in range(H * W):
+        gt = np.array([sum(x[0, t, k] * wg[j, k] for k in range(d)) for j in range(h)])
+        vt = np.array([sum(x[0, t, k] * wv[j, k] for k in range(d)) for j in range(h)])
+        ht = gt * expit(gt) * vt
+        want[0, t] = [sum(ht[j] * wo[i, j] for j in range(h)) for i in range(d)]
+    np.testing.assert_allclose(y, want, rtol=1e-12, atol=1e-12)
+
+
+def test_spatial_swiglu_transposes_with_the_grid():
+    # transposing the grid (and each 3x3 kernel) transposes the output tokens
+    rng = np.random.default_rng(23)
+    B, H, W, d, h = 2, 3, 5, 8, 8
+    x = rng.normal(size=(B, H * W, d))
+    wg, wv, wo, cw, cb = swiglu_weights(rng, d, h)
+    y = oracle.spatial_swiglu(x, wg, wv, wo, cw, cb, H=H, W=W)
+    xt = x.reshape(B, H, W, d).transpose(0, 2, 1, 3).reshape(B, H * W, d)
+    yt = oracle.spatial_swiglu(xt, wg, wv, wo, cw.transpose(0, 2, 1), cb, H=W, W=H)
+    np.testing.assert_allclose(yt, y.reshape(B, H, W, d).transpose(0, 2, 1, 3).reshape(B, H * W, d), rtol=1e-12,
+                               atol=1e-12)
+
+
+def test_spatial_swiglu_is_local():
+    # changing one token changes outputs only within its 3x3 neighbourhood
+    rng = np.random.default_rng(24)
+    B, H, W, d, h = 1, 6, 6, 8, 8
+    x = rng.normal(size=(B, H * W, d))
+    wg, wv, wo, cw, cb = swiglu_weights(rng, d, h)
+    y0 = oracle.spatial_swiglu(x, wg, wv, wo, cw, cb, H=H, W=W)
+    x2 = x.copy()
+    x2[0, 2 * W + 3] += 1.0
+    diff = np.abs(oracle.spatial_swiglu(x2, wg, wv, wo, cw, cb, H=H, W=W) - y0).max(axis=-1).reshape(H, W)
+    changed = np.argwhere(diff > 0)
+    assert changed.min(axis=0).tolist() == [1, 2] and changed.max(axis=0).tolist() == [3, 4]
