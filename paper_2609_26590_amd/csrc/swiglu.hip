@@ -59,71 +59,134 @@ __device__ __forceinline__ f4 mfma(const bf8& a, const bf8& b, f4 c) {
 }
 
 // C[M][N] = A[M][K] * B[N][K]^T, row-major, K a multiple of 32, N a multiple
-// of 64. Work-group tile 64 x 64 (4 waves of 32 x 32, 2 x 2 MFMA tiles each);
-// rows past M are read from row M-1 and not stored. blockIdx.z selects one of
-// two (B, C) pairs, so G and V come out of one launch.
+// of BN. Work-group tile BM x BN, 4 waves in a 2 x 2 grid, each wave a
+// (BM/2) x (BN/2) block of 16 x 16 MFMA tiles. Every K-step of 32 stages the
+// A and B tiles in LDS once (each element is read from memory by one thread
+// and from LDS by every wave that needs it); the loads of the next step are in
+// flight while the current one multiplies (two LDS buffers). Rows past M are
+// read from row M-1 and not stored. blockIdx.z selects one of two (B, C) pairs
+// (G and V come out of one launch) or, with ksplit > 1, a slice of K whose
+// partial product goes to C[1] + slice * M * N (float32) for a reduction.
 struct GemmArgs {
   const void* A;
   const void* B[2];
   void* C[2];
   int M, N, K;
-  int cdt;  // dtype of C (GTR_F32 / GTR_F16 / GTR_BF16)
+  int cdt;     // dtype of C (GTR_F32 / GTR_F16 / GTR_BF16)
+  int ksplit;  // number of K slices (1: none)
 };
 
-template <int ADT, int BDT, int MT>
+constexpr int KB = 4;     // minimum K-steps per slice when splitting K
+constexpr int kPitch = 40;  // LDS row pitch in 16-bit elements (32 + 8: 80-byte rows, 16-byte aligned)
+
+template <int ADT, int BDT, int MT, int BM, int BN>
 __global__ void __launch_bounds__(256) gemm_nt_kernel(GemmArgs g) {
   typedef Operand<ADT, MT> OA;
   typedef Operand<BDT, MT> OB;
+  constexpr int TI = BM / 32, TJ = BN / 32;   // MFMA tiles per wave
+  constexpr int PA = BM * 4 / 256, PB = BN * 4 / 256;  // 16-byte pieces per thread per step
+  __shared__ __attribute__((aligned(16))) unsigned short As[2][BM * kPitch];
+  __shared__ __attribute__((aligned(16))) unsigned short Bs[2][BN * kPitch];
+
   const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int r16 = lane & 15, kq = lane >> 4;
-  const int m0 = blockIdx.x * 64 + 32 * (w >> 1), n0 = blockIdx.y * 64 + 32 * (w & 1);
+  const int mb = blockIdx.x * BM, nb = blockIdx.y * BN;
+  const int wm = (w >> 1) * (BM / 2), wn = (w & 1) * (BN / 2);
+  const int pair = g.ksplit > 1 ? 0 : blockIdx.z;
   const unsigned short* A = static_cast<const unsigned short*>(g.A);
-  const unsigned short* B = static_cast<const unsigned short*>(g.B[blockIdx.z]);
+  const unsigned short* B = static_cast<const unsigned short*>(g.B[pair]);
   const int64_t K = g.K;
-  const int64_t ra0 = min(m0 + r16, g.M - 1), ra1 = min(m0 + 16 + r16, g.M - 1);
-  const int64_t rb0 = n0 + r16, rb1 = n0 + 16 + r16;
-  const w4* pa0 = reinterpret_cast<const w4*>(A + ra0 * K + 8 * kq);
-  const w4* pa1 = reinterpret_cast<const w4*>(A + ra1 * K + 8 * kq);
-  const w4* pb0 = reinterpret_cast<const w4*>(B + rb0 * K + 8 * kq);
-  const w4* pb1 = reinterpret_cast<const w4*>(B + rb1 * K + 8 * kq);
-  f4 acc[2][2];
+  const int steps = g.K / 32;
+  const int s_per = (steps + g.ksplit - 1) / g.ksplit;
+  const int s0 = g.ksplit > 1 ? blockIdx.z * s_per : 0;
+  const int s1 = min(s0 + s_per, steps);
+
+  // global pieces of this thread: piece p -> row p / 4, 16-byte column p % 4
+  const w4* ga[PA];
+  const w4* gb[PB];
+  int la[PA], lb[PB];
 #pragma unroll
-  for (int i = 0; i < 2; ++i)
-#pragma unroll
-    for (int j = 0; j < 2; ++j) acc[i][j] = f4{0.f, 0.f, 0.f, 0.f};
-  // one K-step of 32 elements is 4 pieces of 16 bytes per row
-  w4 a0 = pa0[0], a1 = pa1[0], b0 = pb0[0], b1 = pb1[0];
-  for (int64_t k = 32; k <= K; k += 32) {
-    // prefetch the next step while this one multiplies (the last prefetch
-    // re-reads the final step and is not used)
-    const int64_t kn = (k < K ? k : k - 32) / 8;
-    const w4 na0 = pa0[kn], na1 = pa1[kn], nb0 = pb0[kn], nb1 = pb1[kn];
-    const typename OA::T fa0 = OA::get(a0), fa1 = OA::get(a1);
-    const typename OB::T fb0 = OB::get(b0), fb1 = OB::get(b1);
-    acc[0][0] = mfma(fa0, fb0, acc[0][0]);
-    acc[0][1] = mfma(fa0, fb1, acc[0][1]);
-    acc[1][0] = mfma(fa1, fb0, acc[1][0]);
-    acc[1][1] = mfma(fa1, fb1, acc[1][1]);
-    a0 = na0;
-    a1 = na1;
-    b0 = nb0;
-    b1 = nb1;
+  for (int q = 0; q < PA; ++q) {
+    const int p = threadIdx.x + 256 * q, row = p >> 2, col = p & 3;
+    ga[q] = reinterpret_cast<const w4*>(A + (int64_t)min(mb + row, g.M - 1) * K + 8 * col);
+    la[q] = row * kPitch + 8 * col;
   }
-  // lane holds C[row 16i + 4kq + e][column 16j + r16] of this wave's 32 x 32
-  void* C = g.C[blockIdx.z];
 #pragma unroll
-  for (int i = 0; i < 2; ++i)
+  for (int q = 0; q < PB; ++q) {
+    const int p = threadIdx.x + 256 * q, row = p >> 2, col = p & 3;
+    gb[q] = reinterpret_cast<const w4*>(B + (int64_t)(nb + row) * K + 8 * col);
+    lb[q] = row * kPitch + 8 * col;
+  }
+  f4 acc[TI][TJ];
+#pragma unroll
+  for (int i = 0; i < TI; ++i)
+#pragma unroll
+    for (int j = 0; j < TJ; ++j) acc[i][j] = f4{0.f, 0.f, 0.f, 0.f};
+
+  // D K-steps of global loads in flight: a ring of register slots, each staged
+  // to LDS the step before it is multiplied (the loop is unrolled by D so
+  // every slot index is a compile-time constant)
+  constexpr int D = 4;
+  w4 ra[D][PA], rb[D][PB];
+  auto fetch = [&](int st, w4 (&a)[PA], w4 (&b)[PB]) {
+#pragma unroll
+    for (int q = 0; q < PA; ++q) a[q] = ga[q][4 * st];
+#pragma unroll
+    for (int q = 0; q < PB; ++q) b[q] = gb[q][4 * st];
+  };
+  auto stage = [&](int buf, const w4 (&a)[PA], const w4 (&b)[PB]) {
+#pragma unroll
+    for (int q = 0; q < PA; ++q) *reinterpret_cast<w4*>(&As[buf][la[q]]) = a[q];
+#pragma unroll
+    for (int q = 0; q < PB; ++q) *reinterpret_cast<w4*>(&Bs[buf][lb[q]]) = b[q];
+  };
+#pragma unroll
+  for (int q = 0; q < D; ++q)
+    if (s0 + q < s1) fetch(s0 + q, ra[q], rb[q]);
+  if (s0 < s1) stage(0, ra[0], rb[0]);
+  __syncthreads();
+  for (int sb = s0; sb < s1; sb += D) {
+#pragma unroll
+    for (int q = 0; q < D; ++q) {
+      const int st = sb + q;
+      if (st < s1) {
+        const int buf = (st - s0) & 1;
+        if (st + D < s1) fetch(st + D, ra[q], rb[q]);  // slot q was staged before this step
+        typename OA::T fa[TI];
+        typename OB::T fb[TJ];
+#pragma unroll
+        for (int i = 0; i < TI; ++i)
+          fa[i] = OA::get(*reinterpret_cast<const w4*>(&As[buf][(wm + 16 * i + r16) * kPitch + 8 * kq]));
+#pragma unroll
+        for (int j = 0; j < TJ; ++j)
+          fb[j] = OB::get(*reinterpret_cast<const w4*>(&Bs[buf][(wn + 16 * j + r16) * kPitch + 8 * kq]));
+#pragma unroll
+        for (int i = 0; i < TI; ++i)
+#pragma unroll
+          for (int j = 0; j < TJ; ++j) acc[i][j] = mfma(fa[i], fb[j], acc[i][j]);
+        if (st + 1 < s1) stage(buf ^ 1, ra[(q + 1) % D], rb[(q + 1) % D]);  // nobody reads buf ^ 1 now
+        __syncthreads();
+      }
+    }
+  }
+
+  // lane holds C[row 16i + 4kq + e][column 16j + r16] of this wave's block
+  void* C = g.ksplit > 1 ? static_cast<void*>(static_cast<float*>(g.C[1]) + (int64_t)blockIdx.z * g.M * g.N)
+                         : g.C[blockIdx.z];
+  const int cdt = g.ksplit > 1 ? (int)GTR_F32 : g.cdt;
+#pragma unroll
+  for (int i = 0; i < TI; ++i)
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
-      const int m = m0 + 16 * i + 4 * kq + e;
+      const int m = mb + wm + 16 * i + 4 * kq + e;
       if (m >= g.M) continue;
 #pragma unroll
-      for (int j = 0; j < 2; ++j) {
-        const int64_t off = (int64_t)m * g.N + n0 + 16 * j + r16;
+      for (int j = 0; j < TJ; ++j) {
+        const int64_t off = (int64_t)m * g.N + nb + wn + 16 * j + r16;
         const float x = acc[i][j][e];
-        if (g.cdt == GTR_F32)
+        if (cdt == GTR_F32)
           static_cast<float*>(C)[off] = x;
-        else if (g.cdt == GTR_F16)
+        else if (cdt == GTR_F16)
           static_cast<_Float16*>(C)[off] = (_Float16)x;
         else
           static_cast<unsigned short*>(C)[off] = f32_to_bf16_bits(x);
@@ -131,34 +194,44 @@ __global__ void __launch_bounds__(256) gemm_nt_kernel(GemmArgs g) {
     }
 }
 
-// H[b][t][c] = SiLU(G[b][t][c]) * (sum_{u,v} V[b][t + (u-1, v-1)][c] * cw[c][u][v] + cb[c]),
-// one thread per token and 8 channels; neighbours outside the grid are zero.
+// C = sum over the ksplit float32 partial products, converted to C's dtype;
+// 4 elements per thread.
+__global__ void __launch_bounds__(256) ksplit_reduce_kernel(const float* part, void* C, int64_t n4, int ksplit,
+                                                            int cdt) {
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (i >= n4) return;
+  f4 s = reinterpret_cast<const f4*>(part)[i];
+  for (int z = 1; z < ksplit; ++z) s += reinterpret_cast<const f4*>(part)[(int64_t)z * n4 + i];
+  if (cdt == GTR_F32) {
+    reinterpret_cast<f4*>(C)[i] = s;
+  } else {
+    float x[4] = {s[0], s[1], s[2], s[3]};
+    store_n<4>(C, cdt, 4 * i, x);
+  }
+}
+
+// H[b][t][c] = SiLU(G[b][t][c]) * (sum_{u,v} V[b][t + (u-1, v-1)][c] * cw[c][u][v] + cb[c]).
+// One thread per 8 channels and a column of CR vertically adjacent tokens: its
+// 72 weights stay in registers, and the CR + 2 rows of 3 neighbours are read
+// once for the whole column. Neighbours outside the grid are zero.
+constexpr int CR = 8;
+
 __global__ void __launch_bounds__(256) conv_gate_kernel(const float* G, const float* V, const float* cw,
                                                         const float* cb, _Float16* Hout, int B, int Hh, int W,
                                                         int hidden) {
   const int groups = hidden / 8;
-  const int64_t n = (int64_t)B * Hh * W * groups;
+  const int rblocks = (Hh + CR - 1) / CR;
+  const int64_t n = (int64_t)B * rblocks * W * groups;
   const int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x;  // launched with 256 threads
   if (idx >= n) return;
   const int cg = (int)(idx % groups);
-  const int64_t tok = idx / groups;  // b * L + t
+  int64_t r = idx / groups;
+  const int j = (int)(r % W);
+  r /= W;
+  const int rb = (int)(r % rblocks);
+  const int64_t b = r / rblocks;
   const int64_t L = (int64_t)Hh * W;
-  const int64_t b = tok / L, t = tok - b * L;
-  const int i = (int)(t / W), j = (int)(t - (int64_t)(t / W) * W);
-  const int c = 8 * cg;
-  float acc[8];
-  if (cb) {
-    const f4 lo = *reinterpret_cast<const f4*>(cb + c), hi = *reinterpret_cast<const f4*>(cb + c + 4);
-#pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      acc[e] = lo[e];
-      acc[e + 4] = hi[e];
-    }
-  } else {
-#pragma unroll
-    for (int e = 0; e < 8; ++e) acc[e] = 0.f;
-  }
-  // the 72 weights of channels c .. c+7 are contiguous ([hidden][3][3])
+  const int c = 8 * cg, i0 = rb * CR;
   float wt[72];
 #pragma unroll
   for (int q = 0; q < 18; ++q) {
@@ -166,44 +239,84 @@ __global__ void __launch_bounds__(256) conv_gate_kernel(const float* G, const fl
 #pragma unroll
     for (int e = 0; e < 4; ++e) wt[4 * q + e] = x[e];
   }
+  float bias[8];
 #pragma unroll
-  for (int u = 0; u < 3; ++u) {
-    const int ii = i + u - 1;
+  for (int e = 0; e < 8; ++e) bias[e] = 0.f;
+  if (cb) {
+    const f4 lo = *reinterpret_cast<const f4*>(cb + c), hi = *reinterpret_cast<const f4*>(cb + c + 4);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      bias[e] = lo[e];
+      bias[e + 4] = hi[e];
+    }
+  }
+  float acc[CR][8];
+#pragma unroll
+  for (int rr = 0; rr < CR; ++rr)
+#pragma unroll
+    for (int e = 0; e < 8; ++e) acc[rr][e] = bias[e];
+  // input row ii = i0 - 1 + y contributes to output rows rr = y - u (u = 0..2)
+#pragma unroll
+  for (int y = 0; y < CR + 2; ++y) {
+    const int ii = i0 - 1 + y;
+    if (ii < 0 || ii >= Hh) continue;
 #pragma unroll
     for (int v = 0; v < 3; ++v) {
       const int jj = j + v - 1;
-      if (ii < 0 || ii >= Hh || jj < 0 || jj >= W) continue;
+      if (jj < 0 || jj >= W) continue;
       const float* p = V + ((b * L + (int64_t)ii * W + jj) * hidden + c);
       const f4 lo = *reinterpret_cast<const f4*>(p), hi = *reinterpret_cast<const f4*>(p + 4);
 #pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        acc[e] = fmaf(lo[e], wt[9 * e + 3 * u + v], acc[e]);
-        acc[e + 4] = fmaf(hi[e], wt[9 * (e + 4) + 3 * u + v], acc[e + 4]);
+      for (int u = 0; u < 3; ++u) {
+        const int rr = y - u;
+        if (rr < 0 || rr >= CR) continue;  // compile-time after unrolling
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          acc[rr][e] = fmaf(lo[e], wt[9 * e + 3 * u + v], acc[rr][e]);
+          acc[rr][e + 4] = fmaf(hi[e], wt[9 * (e + 4) + 3 * u + v], acc[rr][e + 4]);
+        }
       }
     }
   }
-  const float* pg = G + tok * hidden + c;
-  const f4 glo = *reinterpret_cast<const f4*>(pg), ghi = *reinterpret_cast<const f4*>(pg + 4);
-  h8 out;
 #pragma unroll
-  for (int e = 0; e < 8; ++e) {
-    const float z = e < 4 ? glo[e] : ghi[e - 4];
-    out[e] = (_Float16)(z * __builtin_amdgcn_rcpf(1.f + __expf(-z)) * acc[e]);
+  for (int rr = 0; rr < CR; ++rr) {
+    const int i = i0 + rr;
+    if (i >= Hh) break;
+    const int64_t tok = b * L + (int64_t)i * W + j;
+    const float* pg = G + tok * hidden + c;
+    const f4 glo = *reinterpret_cast<const f4*>(pg), ghi = *reinterpret_cast<const f4*>(pg + 4);
+    h8 out;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const float z = e < 4 ? glo[e] : ghi[e - 4];
+      out[e] = (_Float16)(z * __builtin_amdgcn_rcpf(1.f + __expf(-z)) * acc[rr][e]);
+    }
+    *reinterpret_cast<h8*>(Hout + tok * hidden + c) = out;
   }
-  *reinterpret_cast<h8*>(Hout + tok * hidden + c) = out;
+}
+
+// K slices of the output product: enough work-groups to give every SIMD a few
+// waves when M x d alone does not (d is small next to hidden).
+static int out_ksplit(int64_t M, int d, int hidden) {
+  const int64_t wgs = ((M + 127) / 128) * (d / (d % 128 == 0 ? 128 : 64));
+  int s = 1;
+  while (wgs * s < 1024 && s < 8 && hidden / 32 >= 2 * s * KB) s *= 2;
+  return s;
 }
 
 struct SwigluLayout {
-  size_t g_off, v_off, h_off, total;
+  size_t g_off, v_off, h_off, part_off, total;
 };
 
-static SwigluLayout swiglu_layout(int64_t M, int64_t hidden) {
+static SwigluLayout swiglu_layout(int64_t M, int d, int64_t hidden) {
   auto a256 = [](size_t x) { return (x + 255) & ~(size_t)255; };
   SwigluLayout l;
   l.g_off = 0;
   l.v_off = a256((size_t)M * hidden * 4);
   l.h_off = a256(l.v_off + (size_t)M * hidden * 4);
-  l.total = a256(l.h_off + (size_t)M * hidden * 2);
+  l.part_off = a256(l.h_off + (size_t)M * hidden * 2);
+  const int ks = out_ksplit(M, d, (int)hidden);
+  l.total = a256(l.part_off + (ks > 1 ? (size_t)ks * M * d * 4 : 0));
   return l;
 }
 
@@ -226,7 +339,7 @@ static gtr_status swiglu_check(const gtr_swiglu_args* a, int64_t* M_out, bool ch
                         reinterpret_cast<uintptr_t>(a->conv_w) | reinterpret_cast<uintptr_t>(a->conv_b) |
                         reinterpret_cast<uintptr_t>(a->y);
   if (mis & 15u) return GTR_ERR_UNSUPPORTED;
-  const SwigluLayout lay = swiglu_layout(M, a->hidden);
+  const SwigluLayout lay = swiglu_layout(M, a->d, a->hidden);
   if (!a->workspace || (reinterpret_cast<uintptr_t>(a->workspace) & 255u)) return GTR_ERR_WORKSPACE;
   if (a->workspace_bytes < lay.total) return GTR_ERR_WORKSPACE;
   const size_t es = dtype_size(a->dtype);
@@ -257,7 +370,7 @@ using namespace gtr;
 extern "C" size_t gtr_spatial_swiglu_workspace_size(const gtr_swiglu_args* a) {
   int64_t M;
   if (!a || swiglu_check(a, &M, false) != GTR_OK) return 0;
-  return swiglu_layout(M, a->hidden).total;
+  return swiglu_layout(M, a->d, a->hidden).total;
 }
 
 extern "C" gtr_status gtr_spatial_swiglu(const gtr_swiglu_args* a, hipStream_t stream) {
@@ -265,31 +378,50 @@ extern "C" gtr_status gtr_spatial_swiglu(const gtr_swiglu_args* a, hipStream_t s
   int64_t M;
   gtr_status st = swiglu_check(a, &M, true);
   if (st != GTR_OK) return st;
-  const SwigluLayout lay = swiglu_layout(M, a->hidden);
+  const SwigluLayout lay = swiglu_layout(M, a->d, a->hidden);
   char* ws = static_cast<char*>(a->workspace);
   float* G = reinterpret_cast<float*>(ws + lay.g_off);
   float* V = reinterpret_cast<float*>(ws + lay.v_off);
   _Float16* Hb = reinterpret_cast<_Float16*>(ws + lay.h_off);
   const bool bf = a->dtype == GTR_BF16;
 
-  GemmArgs g1{a->x, {a->w_gate, a->w_value}, {G, V}, (int)M, a->hidden, a->d, GTR_F32};
-  const dim3 grid1((unsigned)((M + 63) / 64), (unsigned)(a->hidden / 64), 2);
-  if (bf)
-    hipLaunchKernelGGL((gemm_nt_kernel<GTR_BF16, GTR_BF16, GTR_BF16>), grid1, dim3(256), 0, stream, g1);
+  GemmArgs g1{a->x, {a->w_gate, a->w_value}, {G, V}, (int)M, a->hidden, a->d, GTR_F32, 1};
+  const bool n128 = a->hidden % 128 == 0;
+  const dim3 grid1((unsigned)((M + 127) / 128), (unsigned)(a->hidden / (n128 ? 128 : 64)), 2);
+  if (bf && n128)
+    hipLaunchKernelGGL((gemm_nt_kernel<GTR_BF16, GTR_BF16, GTR_BF16, 128, 128>), grid1, dim3(256), 0, stream, g1);
+  else if (bf)
+    hipLaunchKernelGGL((gemm_nt_kernel<GTR_BF16, GTR_BF16, GTR_BF16, 128, 64>), grid1, dim3(256), 0, stream, g1);
+  else if (n128)
+    hipLaunchKernelGGL((gemm_nt_kernel<GTR_F16, GTR_F16, GTR_F16, 128, 128>), grid1, dim3(256), 0, stream, g1);
   else
-    hipLaunchKernelGGL((gemm_nt_kernel<GTR_F16, GTR_F16, GTR_F16>), grid1, dim3(256), 0, stream, g1);
+    hipLaunchKernelGGL((gemm_nt_kernel<GTR_F16, GTR_F16, GTR_F16, 128, 64>), grid1, dim3(256), 0, stream, g1);
   if (hipGetLastError() != hipSuccess) return GTR_ERR_HIP;
 
-  const int64_t threads = M * (a->hidden / 8);
+  const int64_t threads = (int64_t)a->B * ((a->H + CR - 1) / CR) * a->W * (a->hidden / 8);
   hipLaunchKernelGGL(conv_gate_kernel, dim3((unsigned)((threads + 255) / 256)), dim3(256), 0, stream, G, V,
                      a->conv_w, a->conv_b, Hb, a->B, a->H, a->W, a->hidden);
   if (hipGetLastError() != hipSuccess) return GTR_ERR_HIP;
 
-  GemmArgs g3{Hb, {a->w_out, a->w_out}, {a->y, a->y}, (int)M, a->d, a->hidden, a->y_dtype};
-  const dim3 grid3((unsigned)((M + 63) / 64), (unsigned)(a->d / 64), 1);
-  if (bf)
-    hipLaunchKernelGGL((gemm_nt_kernel<GTR_F16, GTR_BF16, GTR_F16>), grid3, dim3(256), 0, stream, g3);
+  const int ks = out_ksplit(M, a->d, a->hidden);
+  float* part = reinterpret_cast<float*>(ws + lay.part_off);
+  GemmArgs g3{Hb, {a->w_out, a->w_out}, {a->y, ks > 1 ? static_cast<void*>(part) : a->y}, (int)M, a->d,
+              a->hidden, a->y_dtype, ks};
+  const bool d128 = a->d % 128 == 0;
+  const dim3 grid3((unsigned)((M + 127) / 128), (unsigned)(a->d / (d128 ? 128 : 64)), (unsigned)ks);
+  if (bf && d128)
+    hipLaunchKernelGGL((gemm_nt_kernel<GTR_F16, GTR_BF16, GTR_F16, 128, 128>), grid3, dim3(256), 0, stream, g3);
+  else if (bf)
+    hipLaunchKernelGGL((gemm_nt_kernel<GTR_F16, GTR_BF16, GTR_F16, 128, 64>), grid3, dim3(256), 0, stream, g3);
+  else if (d128)
+    hipLaunchKernelGGL((gemm_nt_kernel<GTR_F16, GTR_F16, GTR_F16, 128, 128>), grid3, dim3(256), 0, stream, g3);
   else
-    hipLaunchKernelGGL((gemm_nt_kernel<GTR_F16, GTR_F16, GTR_F16>), grid3, dim3(256), 0, stream, g3);
+    hipLaunchKernelGGL((gemm_nt_kernel<GTR_F16, GTR_F16, GTR_F16, 128, 64>), grid3, dim3(256), 0, stream, g3);
+  if (hipGetLastError() != hipSuccess) return GTR_ERR_HIP;
+  if (ks > 1) {
+    const int64_t n4 = M * a->d / 4;
+    hipLaunchKernelGGL(ksplit_reduce_kernel, dim3((unsigned)((n4 + 255) / 256)), dim3(256), 0, stream, part, a->y,
+                       n4, ks, (int)a->y_dtype);
+  }
   return hipGetLastError() == hipSuccess ? GTR_OK : GTR_ERR_HIP;
 }

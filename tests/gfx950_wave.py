@@ -666,6 +666,14 @@ def _smov(w, i):
     w.s32set(i.ops[0], v, o, d)
 
 
+@handler('s_mulk_i32')
+def _smulk(w, i):
+    v, o, d = w.s32(i.ops[0], i)
+    k = w.literal(i.ops[1])
+    k = k - 0x10000 if k >= 0x8000 else k
+    w.s32set(i.ops[0], (sx(v) * k) & M32, o, d)
+
+
 @handler('s_addk_i32')
 def _saddk(w, i):
     v, o, d = w.s32(i.ops[0], i)

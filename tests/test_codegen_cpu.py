@@ -287,21 +287,25 @@ def check_kernel(text, name, kern, regions, wgs, waves=4):
     assert "INFO-PATHLIMIT" not in rep.counts
 
 
-@pytest.mark.parametrize("adt,bdt,mt,M,N,K,cdt", [(2, 2, 2, 126, 128, 64, 0), (1, 1, 1, 1600, 384, 1536, 1),
-                                                  (1, 2, 1, 63, 64, 128, 2)])
-def test_swiglu_gemm_addresses(adt, bdt, mt, M, N, K, cdt):
+@pytest.mark.parametrize("adt,bdt,mt,bn,M,N,K,cdt,ks", [(2, 2, 2, 128, 126, 256, 64, 0, 1),
+                                                        (1, 1, 1, 128, 1600, 384, 1536, 1, 4),
+                                                        (1, 2, 1, 64, 63, 64, 128, 2, 1),
+                                                        (1, 1, 1, 64, 200, 192, 192, 1, 2)])
+def test_swiglu_gemm_addresses(adt, bdt, mt, bn, M, N, K, cdt, ks):
     text = swiglu_asm()
     base = 0x1000_0000_0000
     es = {0: 4, 1: 2, 2: 2}
     A, B0, B1, C0, C1 = (base + i * 0x10_0000_0000 for i in range(5))
+    c1_bytes = ks * M * N * 4 if ks > 1 else M * N * es[cdt]  # K-split partials are float32
     regions = [emu.Region("A", A, M * K * 2, "r"), emu.Region("B0", B0, N * K * 2, "r"),
                emu.Region("B1", B1, N * K * 2, "r"), emu.Region("C0", C0, M * N * es[cdt], "w"),
-               emu.Region("C1", C1, M * N * es[cdt], "w"), emu.Region("kernarg", emu.KERNARG_BASE, 56, "r")]
-    kern = struct.pack("<QQQQQiiii", A, B0, B1, C0, C1, M, N, K, cdt)
-    name = f"_ZN3gtr14gemm_nt_kernelILi{adt}ELi{bdt}ELi{mt}EEEvNS_8GemmArgsE"
+               emu.Region("C1", C1, c1_bytes, "w"), emu.Region("kernarg", emu.KERNARG_BASE, 64, "r")]
+    kern = struct.pack("<QQQQQiiiii4x", A, B0, B1, C0, C1, M, N, K, cdt, ks)
+    name = f"_ZN3gtr14gemm_nt_kernelILi{adt}ELi{bdt}ELi{mt}ELi128ELi{bn}EEEvNS_8GemmArgsE"
     assert name in emu.kernel_names(text)
-    gx, gy = (M + 63) // 64, N // 64
-    wgs = [(x, y, z) for x in sorted({0, gx - 1}) for y in sorted({0, gy - 1}) for z in (0, 1)]
+    gx, gy = (M + 127) // 128, N // bn
+    zs = range(ks) if ks > 1 else (0, 1)
+    wgs = [(x, y, z) for x in sorted({0, gx - 1}) for y in sorted({0, gy - 1}) for z in sorted({min(zs), max(zs)})]
     check_kernel(text, name, kern, regions, wgs)
 
 
@@ -318,5 +322,21 @@ def test_swiglu_conv_gate_addresses():
     name = "_ZN3gtr16conv_gate_kernelEPKfS1_S1_S1_PDF16_iiii"
     names = emu.kernel_names(text)
     name = [n for n in names if "conv_gate_kernel" in n][0]
-    nblk = (M * hidden // 8 + 255) // 256
+    nblk = (B * ((H + 7) // 8) * W * hidden // 8 + 255) // 256  # a column of 8 tokens per thread
     check_kernel(text, name, kern, regions, [(0, 0, 0), (nblk // 2, 0, 0), (nblk - 1, 0, 0)])
+
+
+@pytest.mark.parametrize("cdt", [0, 1, 2])
+def test_swiglu_ksplit_reduce_addresses(cdt):
+    text = swiglu_asm()
+    M, N, ks = 100, 64, 4
+    n4 = M * N // 4
+    es = {0: 4, 1: 2, 2: 2}
+    base = 0x1000_0000_0000
+    P, C = base, base + 0x10_0000_0000
+    regions = [emu.Region("part", P, ks * M * N * 4, "r"), emu.Region("C", C, M * N * es[cdt], "w"),
+               emu.Region("kernarg", emu.KERNARG_BASE, 32, "r")]
+    kern = struct.pack("<QQqii", P, C, n4, ks, cdt)
+    name = [n for n in emu.kernel_names(text) if "ksplit_reduce_kernel" in n][0]
+    nblk = (n4 + 255) // 256
+    check_kernel(text, name, kern, regions, [(0, 0, 0), (nblk - 1, 0, 0)])
