@@ -271,10 +271,10 @@ def test_swiglu_workspace_size(lib):
     a = swiglu_args(B=2, H=40, W=40, d=384, hidden=1536)
     M = 2 * 1600
     a256 = lambda x: (x + 255) // 256 * 256
-    # G and V (float32), H (fp16), then 4 float32 partial products of the output
-    # product split over K (300 work-groups of 64 x 64 alone would leave SIMDs idle)
+    # G and V (float32), H (fp16), then 8 float32 partial products of the output
+    # product split over K (75 work-groups of 128 x 128 alone would leave SIMDs idle)
     base = a256(a256(a256(M * 1536 * 4) + M * 1536 * 4) + M * 1536 * 2)
-    assert lib.gtr_spatial_swiglu_workspace_size(ctypes.byref(a)) == a256(base + 4 * M * 384 * 4)
+    assert lib.gtr_spatial_swiglu_workspace_size(ctypes.byref(a)) == a256(base + 8 * M * 384 * 4)
 
 
 @pytest.mark.parametrize("field,val,want", [("B", 0, SHAPE), ("H", -1, SHAPE), ("d", 48, UNSUP),
