@@ -3,12 +3,14 @@
 // X the patch tokens of one image in row-major grid order, the value branch
 // convolved depthwise over the H x W grid (zero padding), the gate tokenwise.
 //
-// Three launches:
-//   1. gemm_nt_kernel (z = 0, 1): G = X W_g^T and V = X W_v^T, float32 out,
-//      MFMA on the input dtype's operands (fp16 or bf16), float32 accumulation;
+// Three launches (four when the output product splits K):
+//   1. gemm_nt_kernel (z = 0, 1): G = X W_g^T and V = X W_v^T, MFMA on the
+//      input dtype's operands (fp16 or bf16), float32 accumulation, stored as
+//      fp16 (the type H is rounded to anyway);
 //   2. conv_gate_kernel: H = SiLU(G) * (DWConv3x3(V) + bias), rounded to fp16,
 //      the operand type of the next product;
-//   3. gemm_nt_kernel: Y = H W_o^T (fp16 operands; bf16 weights are widened).
+//   3. gemm_nt_kernel: Y = H W_o^T (fp16 operands; bf16 weights are widened),
+//      float32 partial products per K slice summed by ksplit_reduce_kernel.
 // Weights use the layout of a linear layer (output features first), so both
 // operands of every product are read along K in 16-byte pieces.
 #include <hip/hip_runtime.h>
@@ -77,7 +79,14 @@ struct GemmArgs {
 };
 
 constexpr int KB = 4;     // minimum K-steps per slice when splitting K
-constexpr int kPitch = 40;  // LDS row pitch in 16-bit elements (32 + 8: 80-byte rows, 16-byte aligned)
+// LDS tiles: rows of 32 K elements (64 bytes, no padding); the 16-byte piece
+// c of row r sits at piece c ^ kSwz(r). Measured on gfx950, ds_read_b128 serves
+// 32 lanes per cycle from 32 distinct 16-byte slots (address / 16 mod 32) and
+// ds_write_b128 16 lanes from 16 slots (mod 16): with this swizzle the operand
+// reads (lanes = 16 rows x 2 pieces) and the staging writes (lanes = 4 rows x
+// 4 pieces) both hit distinct slots.
+constexpr int kPitch = 32;
+__device__ __forceinline__ int kSwz(int r) { return (r >> 2) & 2; }
 
 template <int ADT, int BDT, int MT, int BM, int BN>
 __global__ void __launch_bounds__(256) gemm_nt_kernel(GemmArgs g) {
@@ -109,13 +118,13 @@ __global__ void __launch_bounds__(256) gemm_nt_kernel(GemmArgs g) {
   for (int q = 0; q < PA; ++q) {
     const int p = threadIdx.x + 256 * q, row = p >> 2, col = p & 3;
     ga[q] = reinterpret_cast<const w4*>(A + (int64_t)min(mb + row, g.M - 1) * K + 8 * col);
-    la[q] = row * kPitch + 8 * col;
+    la[q] = row * kPitch + 8 * (col ^ kSwz(row));
   }
 #pragma unroll
   for (int q = 0; q < PB; ++q) {
     const int p = threadIdx.x + 256 * q, row = p >> 2, col = p & 3;
     gb[q] = reinterpret_cast<const w4*>(B + (int64_t)(nb + row) * K + 8 * col);
-    lb[q] = row * kPitch + 8 * col;
+    lb[q] = row * kPitch + 8 * (col ^ kSwz(row));
   }
   f4 acc[TI][TJ];
 #pragma unroll
@@ -156,42 +165,36 @@ __global__ void __launch_bounds__(256) gemm_nt_kernel(GemmArgs g) {
         typename OB::T fb[TJ];
 #pragma unroll
         for (int i = 0; i < TI; ++i)
-          fa[i] = OA::get(*reinterpret_cast<const w4*>(&As[buf][(wm + 16 * i + r16) * kPitch + 8 * kq]));
+          fa[i] = OA::get(*reinterpret_cast<const w4*>(&As[buf][(wm + 16 * i + r16) * kPitch + 8 * (kq ^ kSwz(r16))]));
 #pragma unroll
         for (int j = 0; j < TJ; ++j)
-          fb[j] = OB::get(*reinterpret_cast<const w4*>(&Bs[buf][(wn + 16 * j + r16) * kPitch + 8 * kq]));
+          fb[j] = OB::get(*reinterpret_cast<const w4*>(&Bs[buf][(wn + 16 * j + r16) * kPitch + 8 * (kq ^ kSwz(r16))]));
 #pragma unroll
         for (int i = 0; i < TI; ++i)
 #pragma unroll
-          for (int j = 0; j < TJ; ++j) acc[i][j] = mfma(fa[i], fb[j], acc[i][j]);
+          for (int j = 0; j < TJ; ++j) acc[i][j] = mfma(fb[j], fa[i], acc[i][j]);  // C^T tiles
         if (st + 1 < s1) stage(buf ^ 1, ra[(q + 1) % D], rb[(q + 1) % D]);  // nobody reads buf ^ 1 now
         __syncthreads();
       }
     }
   }
 
-  // lane holds C[row 16i + 4kq + e][column 16j + r16] of this wave's block
+  // lane holds C[row 16i + r16][columns 16j + 4kq .. 16j + 4kq + 3] of this
+  // wave's block (the products above are C^T tiles): one 4-element store each
   void* C = g.ksplit > 1 ? static_cast<void*>(static_cast<float*>(g.C[1]) + (int64_t)blockIdx.z * g.M * g.N)
                          : g.C[blockIdx.z];
   const int cdt = g.ksplit > 1 ? (int)GTR_F32 : g.cdt;
 #pragma unroll
-  for (int i = 0; i < TI; ++i)
+  for (int i = 0; i < TI; ++i) {
+    const int m = mb + wm + 16 * i + r16;
+    if (m >= g.M) continue;
 #pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      const int m = mb + wm + 16 * i + 4 * kq + e;
-      if (m >= g.M) continue;
-#pragma unroll
-      for (int j = 0; j < TJ; ++j) {
-        const int64_t off = (int64_t)m * g.N + nb + wn + 16 * j + r16;
-        const float x = acc[i][j][e];
-        if (cdt == GTR_F32)
-          static_cast<float*>(C)[off] = x;
-        else if (cdt == GTR_F16)
-          static_cast<_Float16*>(C)[off] = (_Float16)x;
-        else
-          static_cast<unsigned short*>(C)[off] = f32_to_bf16_bits(x);
-      }
+    for (int j = 0; j < TJ; ++j) {
+      const int64_t off = (int64_t)m * g.N + nb + wn + 16 * j + 4 * kq;
+      const float x[4] = {acc[i][j][0], acc[i][j][1], acc[i][j][2], acc[i][j][3]};
+      store_n<4>(C, cdt, off, x);
     }
+  }
 }
 
 // C = sum over the ksplit float32 partial products, converted to C's dtype;
@@ -211,87 +214,103 @@ __global__ void __launch_bounds__(256) ksplit_reduce_kernel(const float* part, v
 }
 
 // H[b][t][c] = SiLU(G[b][t][c]) * (sum_{u,v} V[b][t + (u-1, v-1)][c] * cw[c][u][v] + cb[c]).
-// One thread per 8 channels and a column of CR vertically adjacent tokens: its
-// 72 weights stay in registers, and the CR + 2 rows of 3 neighbours are read
-// once for the whole column. Neighbours outside the grid are zero.
-constexpr int CR = 8;
+// One work-group per tile of kCT x kCT tokens and kCC channels. The
+// (kCT + 2)^2-token halo of V (zero outside the grid) is staged in LDS with
+// every global load of the work-group issued before any is used; each thread
+// then forms 8 channels of two tokens of the tile from LDS (a wave reads one
+// tile row of 8 tokens x 128 contiguous bytes per tap).
+constexpr int kCT = 8;            // tile edge in tokens
+constexpr int kCC = 64;           // channels per work-group (8 pieces of 8)
+constexpr int kHalo = kCT + 2;    // halo tile edge
+constexpr int kHaloPieces = kHalo * kHalo * (kCC / 8);
+constexpr int kHaloPer = (kHaloPieces + 255) / 256;
 
-__global__ void __launch_bounds__(256) conv_gate_kernel(const float* G, const float* V, const float* cw,
-                                                        const float* cb, _Float16* Hout, int B, int Hh, int W,
+__global__ void __launch_bounds__(256) conv_gate_kernel(const _Float16* G, const _Float16* V, const float* cw,
+                                                        const float* cb, _Float16* Hout, int Hh, int W,
                                                         int hidden) {
-  const int groups = hidden / 8;
-  const int rblocks = (Hh + CR - 1) / CR;
-  const int64_t n = (int64_t)B * rblocks * W * groups;
-  const int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x;  // launched with 256 threads
-  if (idx >= n) return;
-  const int cg = (int)(idx % groups);
-  int64_t r = idx / groups;
-  const int j = (int)(r % W);
-  r /= W;
-  const int rb = (int)(r % rblocks);
-  const int64_t b = r / rblocks;
+  __shared__ __attribute__((aligned(16))) _Float16 vs[kHalo * kHalo * kCC];
+  __shared__ __attribute__((aligned(16))) float wsm[kCC * 9];
+  __shared__ __attribute__((aligned(16))) float bsm[kCC];
+  const int tiles_x = (W + kCT - 1) / kCT, tiles_y = (Hh + kCT - 1) / kCT;
+  const int tx = (int)(blockIdx.x % tiles_x);
+  const int ty = (int)((blockIdx.x / tiles_x) % tiles_y);
+  const int64_t b = blockIdx.x / ((unsigned)tiles_x * tiles_y);
+  const int c0 = blockIdx.y * kCC;
   const int64_t L = (int64_t)Hh * W;
-  const int c = 8 * cg, i0 = rb * CR;
-  float wt[72];
+  const int tid = threadIdx.x;
+
+  // halo pieces (token of the halo tile, 16-byte piece of its kCC channels)
+  w4 hv[kHaloPer];
+#pragma unroll
+  for (int q = 0; q < kHaloPer; ++q) {
+    const int p = tid + 256 * q;
+    const int ht = p >> 3, pc = p & 7;
+    const int gy = ty * kCT - 1 + ht / kHalo, gx = tx * kCT - 1 + ht % kHalo;
+    const bool in = p < kHaloPieces && gy >= 0 && gy < Hh && gx >= 0 && gx < W;
+    hv[q] = w4{0u, 0u, 0u, 0u};
+    if (in) hv[q] = *reinterpret_cast<const w4*>(V + (b * L + (int64_t)gy * W + gx) * hidden + c0 + 8 * pc);
+  }
+  // this thread's outputs: channel piece pc, tile column rx, tile rows ry and ry + kCT / 2
+  const int pc = tid & 7, rx = (tid >> 3) % kCT, ry = (tid >> 3) / kCT;
+  w4 gv[2];
+  bool own[2];
+  int64_t tok[2];
+#pragma unroll
+  for (int k = 0; k < 2; ++k) {
+    const int gy = ty * kCT + ry + k * (kCT / 2), gx = tx * kCT + rx;
+    own[k] = gy < Hh && gx < W;
+    tok[k] = b * L + (int64_t)gy * W + gx;
+    gv[k] = w4{0u, 0u, 0u, 0u};
+    if (own[k]) gv[k] = *reinterpret_cast<const w4*>(G + tok[k] * hidden + c0 + 8 * pc);
+  }
+  // weights [kCC][9] and bias of the work-group's channels
+  f4 wv = {0.f, 0.f, 0.f, 0.f}, bv = {0.f, 0.f, 0.f, 0.f};
+  constexpr int WQ = kCC * 9 / 4, BQ = kCC / 4;
+  if (tid < WQ) wv = reinterpret_cast<const f4*>(cw + (int64_t)c0 * 9)[tid];
+  if (cb && tid >= WQ && tid < WQ + BQ) bv = reinterpret_cast<const f4*>(cb + c0)[tid - WQ];
+
+#pragma unroll
+  for (int q = 0; q < kHaloPer; ++q) {
+    const int p = tid + 256 * q;
+    if (p < kHaloPieces) *reinterpret_cast<w4*>(&vs[8 * p]) = hv[q];
+  }
+  if (tid < WQ) reinterpret_cast<f4*>(wsm)[tid] = wv;
+  if (tid >= WQ && tid < WQ + BQ) reinterpret_cast<f4*>(bsm)[tid - WQ] = bv;
+  __syncthreads();
+
+  float wt[72];  // wt[9 e + 3 u + v]: tap (u, v) of channel 8 pc + e
 #pragma unroll
   for (int q = 0; q < 18; ++q) {
-    const f4 x = *reinterpret_cast<const f4*>(cw + (int64_t)c * 9 + 4 * q);
+    const f4 x = reinterpret_cast<const f4*>(wsm + 72 * pc)[q];
 #pragma unroll
     for (int e = 0; e < 4; ++e) wt[4 * q + e] = x[e];
   }
-  float bias[8];
+  const f4 blo = reinterpret_cast<const f4*>(bsm + 8 * pc)[0], bhi = reinterpret_cast<const f4*>(bsm + 8 * pc)[1];
 #pragma unroll
-  for (int e = 0; e < 8; ++e) bias[e] = 0.f;
-  if (cb) {
-    const f4 lo = *reinterpret_cast<const f4*>(cb + c), hi = *reinterpret_cast<const f4*>(cb + c + 4);
+  for (int k = 0; k < 2; ++k) {
+    float acc[8];
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
-      bias[e] = lo[e];
-      bias[e + 4] = hi[e];
+      acc[e] = blo[e];
+      acc[e + 4] = bhi[e];
     }
-  }
-  float acc[CR][8];
+    const int hy = ry + k * (kCT / 2);
 #pragma unroll
-  for (int rr = 0; rr < CR; ++rr)
+    for (int u = 0; u < 3; ++u)
 #pragma unroll
-    for (int e = 0; e < 8; ++e) acc[rr][e] = bias[e];
-  // input row ii = i0 - 1 + y contributes to output rows rr = y - u (u = 0..2)
+      for (int v = 0; v < 3; ++v) {
+        const h8 x = *reinterpret_cast<const h8*>(&vs[((hy + u) * kHalo + rx + v) * kCC + 8 * pc]);
 #pragma unroll
-  for (int y = 0; y < CR + 2; ++y) {
-    const int ii = i0 - 1 + y;
-    if (ii < 0 || ii >= Hh) continue;
-#pragma unroll
-    for (int v = 0; v < 3; ++v) {
-      const int jj = j + v - 1;
-      if (jj < 0 || jj >= W) continue;
-      const float* p = V + ((b * L + (int64_t)ii * W + jj) * hidden + c);
-      const f4 lo = *reinterpret_cast<const f4*>(p), hi = *reinterpret_cast<const f4*>(p + 4);
-#pragma unroll
-      for (int u = 0; u < 3; ++u) {
-        const int rr = y - u;
-        if (rr < 0 || rr >= CR) continue;  // compile-time after unrolling
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          acc[rr][e] = fmaf(lo[e], wt[9 * e + 3 * u + v], acc[rr][e]);
-          acc[rr][e + 4] = fmaf(hi[e], wt[9 * (e + 4) + 3 * u + v], acc[rr][e + 4]);
-        }
+        for (int e = 0; e < 8; ++e) acc[e] = fmaf((float)x[e], wt[9 * e + 3 * u + v], acc[e]);
       }
-    }
-  }
-#pragma unroll
-  for (int rr = 0; rr < CR; ++rr) {
-    const int i = i0 + rr;
-    if (i >= Hh) break;
-    const int64_t tok = b * L + (int64_t)i * W + j;
-    const float* pg = G + tok * hidden + c;
-    const f4 glo = *reinterpret_cast<const f4*>(pg), ghi = *reinterpret_cast<const f4*>(pg + 4);
+    const h8 g8 = __builtin_bit_cast(h8, gv[k]);
     h8 out;
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
-      const float z = e < 4 ? glo[e] : ghi[e - 4];
-      out[e] = (_Float16)(z * __builtin_amdgcn_rcpf(1.f + __expf(-z)) * acc[rr][e]);
+      const float z = (float)g8[e];
+      out[e] = (_Float16)(z * __builtin_amdgcn_rcpf(1.f + __expf(-z)) * acc[e]);
     }
-    *reinterpret_cast<h8*>(Hout + tok * hidden + c) = out;
+    if (own[k]) *reinterpret_cast<h8*>(Hout + tok[k] * hidden + c0 + 8 * pc) = out;
   }
 }
 
@@ -312,8 +331,8 @@ static SwigluLayout swiglu_layout(int64_t M, int d, int64_t hidden) {
   auto a256 = [](size_t x) { return (x + 255) & ~(size_t)255; };
   SwigluLayout l;
   l.g_off = 0;
-  l.v_off = a256((size_t)M * hidden * 4);
-  l.h_off = a256(l.v_off + (size_t)M * hidden * 4);
+  l.v_off = a256((size_t)M * hidden * 2);
+  l.h_off = a256(l.v_off + (size_t)M * hidden * 2);
   l.part_off = a256(l.h_off + (size_t)M * hidden * 2);
   const int ks = out_ksplit(M, d, (int)hidden);
   l.total = a256(l.part_off + (ks > 1 ? (size_t)ks * M * d * 4 : 0));
@@ -380,12 +399,12 @@ extern "C" gtr_status gtr_spatial_swiglu(const gtr_swiglu_args* a, hipStream_t s
   if (st != GTR_OK) return st;
   const SwigluLayout lay = swiglu_layout(M, a->d, a->hidden);
   char* ws = static_cast<char*>(a->workspace);
-  float* G = reinterpret_cast<float*>(ws + lay.g_off);
-  float* V = reinterpret_cast<float*>(ws + lay.v_off);
+  _Float16* G = reinterpret_cast<_Float16*>(ws + lay.g_off);
+  _Float16* V = reinterpret_cast<_Float16*>(ws + lay.v_off);
   _Float16* Hb = reinterpret_cast<_Float16*>(ws + lay.h_off);
   const bool bf = a->dtype == GTR_BF16;
 
-  GemmArgs g1{a->x, {a->w_gate, a->w_value}, {G, V}, (int)M, a->hidden, a->d, GTR_F32, 1};
+  GemmArgs g1{a->x, {a->w_gate, a->w_value}, {G, V}, (int)M, a->hidden, a->d, GTR_F16, 1};
   const bool n128 = a->hidden % 128 == 0;
   const dim3 grid1((unsigned)((M + 127) / 128), (unsigned)(a->hidden / (n128 ? 128 : 64)), 2);
   if (bf && n128)
@@ -398,9 +417,9 @@ extern "C" gtr_status gtr_spatial_swiglu(const gtr_swiglu_args* a, hipStream_t s
     hipLaunchKernelGGL((gemm_nt_kernel<GTR_F16, GTR_F16, GTR_F16, 128, 64>), grid1, dim3(256), 0, stream, g1);
   if (hipGetLastError() != hipSuccess) return GTR_ERR_HIP;
 
-  const int64_t threads = (int64_t)a->B * ((a->H + CR - 1) / CR) * a->W * (a->hidden / 8);
-  hipLaunchKernelGGL(conv_gate_kernel, dim3((unsigned)((threads + 255) / 256)), dim3(256), 0, stream, G, V,
-                     a->conv_w, a->conv_b, Hb, a->B, a->H, a->W, a->hidden);
+  const int64_t tiles = (int64_t)a->B * ((a->H + kCT - 1) / kCT) * ((a->W + kCT - 1) / kCT);
+  hipLaunchKernelGGL(conv_gate_kernel, dim3((unsigned)tiles, (unsigned)(a->hidden / kCC)), dim3(256), 0, stream,
+                     G, V, a->conv_w, a->conv_b, Hb, a->H, a->W, a->hidden);
   if (hipGetLastError() != hipSuccess) return GTR_ERR_HIP;
 
   const int ks = out_ksplit(M, a->d, a->hidden);

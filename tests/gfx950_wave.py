@@ -1098,7 +1098,7 @@ def dataop(nsrc, first=1):
         srcs = [w.v32(t, i) for t in i.ops[first:first + nsrc] if t not in ('off',)]
         r = vres(np.zeros(NL, np.uint32), *srcs)
         r.o = np.ones(NL, bool)
-        preserve = i.mods.get('dst_unused') == 'UNUSED_PRESERVE' or i.op.startswith('v_fma_mix')
+        preserve = i.mods.get('dst_unused') == 'UNUSED_PRESERVE' or i.op.startswith(('v_fma_mixlo', 'v_fma_mixhi'))
         if preserve:
             old = w.v32(i.ops[0], i)
             r.d = r.d & old.d
@@ -1108,7 +1108,7 @@ def dataop(nsrc, first=1):
 
 for _n, _k in [('v_cvt_f32_f16_e32', 1), ('v_cvt_f32_f16_sdwa', 1), ('v_cvt_f16_f32_e32', 1),
                ('v_cvt_pk_f16_f32', 2), ('v_pack_b32_f16', 2), ('v_perm_b32', 3), ('v_or_b32_sdwa', 2),
-               ('v_fma_mixlo_f16', 3), ('v_fma_mixhi_f16', 3), ('v_cvt_f32_bf16', 1)]:
+               ('v_fma_mixlo_f16', 3), ('v_fma_mixhi_f16', 3), ('v_fma_mix_f32', 3), ('v_cvt_f32_bf16', 1)]:
     HANDLERS[_n] = dataop(_k)
 
 
@@ -1633,6 +1633,58 @@ def run_wave(prog, labels, desc, kernarg, regions, lds_size, wg, wave, report, m
             report.add('INFO-PATHLIMIT', prog[0], str(len(todo)))
             break
     return paths
+
+
+_SDWA_SEL = {'DWORD': (0, 32), 'WORD_0': (0, 16), 'WORD_1': (16, 16), 'BYTE_0': (0, 8), 'BYTE_1': (8, 8),
+             'BYTE_2': (16, 8), 'BYTE_3': (24, 8)}
+
+
+def sdwa_int(fn, nsrc):
+    """Integer SDWA ops: each source field is zero-extended from its src*_sel;
+    only a full-dword destination is supported."""
+    def h(w, i):
+        if i.mods.get('dst_sel', 'DWORD') != 'DWORD' or any('sext' in t for t in i.ops):
+            raise NotImplementedError(i.raw)
+        srcs = [w.v32(t, i) for t in i.ops[1:1 + nsrc]]
+        vals = []
+        for k, sv in enumerate(srcs):
+            sh, nb = _SDWA_SEL[i.mods.get(f'src{k}_sel', 'DWORD')]
+            vals.append((sv.v >> np.uint32(sh)) & np.uint32((1 << nb) - 1) if nb < 32 else sv.v)
+        with np.errstate(all='ignore'):
+            v = fn(*vals)
+        w.vwrite(i.ops[0], vres(np.asarray(v, np.uint32), *srcs))
+    return h
+
+
+def _bitop3(a, b, c, tt):
+    """Three-input bitwise function by truth table: result bit = bit
+    (4 a + 2 b + c) of tt (a <-> 0xF0, b <-> 0xCC, c <-> 0xAA)."""
+    r = np.zeros_like(a)
+    for idx in range(8):
+        if (tt >> idx) & 1:
+            r |= (a if idx & 4 else ~a) & (b if idx & 2 else ~b) & (c if idx & 1 else ~c)
+    return r
+
+
+@handler('v_bitop3_b32')
+def _vbitop3(w, i):
+    tt = int(i.mods['bitop3'], 0)
+    valu(lambda a, b, c: _bitop3(a, b, c, tt), 3)(w, i)
+
+
+HANDLERS.update({
+    'v_add_u32_sdwa': sdwa_int(lambda a, b: a + b, 2),
+    'v_sub_u32_sdwa': sdwa_int(lambda a, b: a - b, 2),
+    'v_mov_b32_sdwa': sdwa_int(lambda a: a, 1),
+    'v_and_b32_sdwa': sdwa_int(lambda a, b: a & b, 2),
+    'v_mul_lo_u16_sdwa': sdwa_int(lambda a, b: (u64(a & np.uint32(0xFFFF)) * u64(b & np.uint32(0xFFFF))
+                                                & np.uint64(0xFFFF)).astype(np.uint32), 2),
+    # 16-bit VOP2 ops of this generation write the low half and zero the high half
+    'v_mul_lo_u16_e32': valu(lambda a, b: (u64(a & np.uint32(0xFFFF)) * u64(b & np.uint32(0xFFFF))
+                                          & np.uint64(0xFFFF)).astype(np.uint32), 2),
+    'v_sub_u16_e32': valu(lambda a, b: (a - b) & np.uint32(0xFFFF), 2),
+    'v_lshrrev_b16_e32': valu(lambda a, b: (b & np.uint32(0xFFFF)) >> (a & np.uint32(15)), 2),
+})
 
 
 @handler('v_cndmask_b32_sdwa')

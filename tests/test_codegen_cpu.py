@@ -309,21 +309,21 @@ def test_swiglu_gemm_addresses(adt, bdt, mt, bn, M, N, K, cdt, ks):
     check_kernel(text, name, kern, regions, wgs)
 
 
-def test_swiglu_conv_gate_addresses():
+@pytest.mark.parametrize("B,H,W,hidden", [(2, 7, 9, 128), (1, 40, 40, 192), (1, 16, 3, 64)])
+def test_swiglu_conv_gate_addresses(B, H, W, hidden):
     text = swiglu_asm()
-    B, H, W, hidden = 2, 7, 9, 128
     M = B * H * W
     base = 0x1000_0000_0000
     G, V, CW, CB, HO = (base + i * 0x10_0000_0000 for i in range(5))
-    regions = [emu.Region("G", G, M * hidden * 4, "r"), emu.Region("V", V, M * hidden * 4, "r"),
+    regions = [emu.Region("G", G, M * hidden * 2, "r"), emu.Region("V", V, M * hidden * 2, "r"),
                emu.Region("cw", CW, hidden * 9 * 4, "r"), emu.Region("cb", CB, hidden * 4, "r"),
                emu.Region("H", HO, M * hidden * 2, "w"), emu.Region("kernarg", emu.KERNARG_BASE, 56, "r")]
-    kern = struct.pack("<QQQQQiiii", G, V, CW, CB, HO, B, H, W, hidden)
-    name = "_ZN3gtr16conv_gate_kernelEPKfS1_S1_S1_PDF16_iiii"
-    names = emu.kernel_names(text)
-    name = [n for n in names if "conv_gate_kernel" in n][0]
-    nblk = (B * ((H + 7) // 8) * W * hidden // 8 + 255) // 256  # a column of 8 tokens per thread
-    check_kernel(text, name, kern, regions, [(0, 0, 0), (nblk // 2, 0, 0), (nblk - 1, 0, 0)])
+    kern = struct.pack("<QQQQQiii4x", G, V, CW, CB, HO, H, W, hidden)
+    name = [n for n in emu.kernel_names(text) if "conv_gate_kernel" in n][0]
+    tx, ty = (W + 7) // 8, (H + 7) // 8  # one work-group per 8 x 8 tokens x 64 channels
+    nt, nc = B * tx * ty, hidden // 64
+    wgs = sorted({(x, y, 0) for x in (0, tx - 1, nt - 1, nt // 2) for y in (0, nc - 1)})
+    check_kernel(text, name, kern, regions, wgs)
 
 
 @pytest.mark.parametrize("cdt", [0, 1, 2])
