@@ -216,11 +216,14 @@ gtr_status gtr_gla_fwd(const gtr_gla_args* args, hipStream_t stream);
  *                                 the inputs or the workspace
  * dtype   : GTR_F16 or GTR_BF16; d and hidden multiples of 64; every pointer
  *           16-byte aligned.
- * The products accumulate in float32; X W_g and X W_v are kept in float32, the
- * gated hidden activations are rounded to fp16 for the output product (so they
- * must stay finite in fp16).
+ * The products accumulate in float32; X W_g and X W_v are rounded to fp16 on
+ * chip (one launch forms the gated convolution per tile of tokens, its halo
+ * recomputed), the gated hidden activations are stored in fp16 for the output
+ * product; all three must stay finite in fp16.
  * workspace : caller-owned, 256-byte aligned, gtr_spatial_swiglu_workspace_size
- *           bytes (B*H*W*hidden*10 rounded up); no initialisation needed.
+ *           bytes (B*H*W*hidden*2 for the activations plus the float32 partial
+ *           products of a K-split output product, rounded up); no
+ *           initialisation needed.
  * Errors as for gtr_gla_fwd; every check runs before any launch.
  */
 typedef struct {

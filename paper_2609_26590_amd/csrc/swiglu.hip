@@ -3,13 +3,13 @@
 // X the patch tokens of one image in row-major grid order, the value branch
 // convolved depthwise over the H x W grid (zero padding), the gate tokenwise.
 //
-// Three launches (four when the output product splits K):
-//   1. gemm_nt_kernel (z = 0, 1): G = X W_g^T and V = X W_v^T, MFMA on the
-//      input dtype's operands (fp16 or bf16), float32 accumulation, stored as
-//      fp16 (the type H is rounded to anyway);
-//   2. conv_gate_kernel: H = SiLU(G) * (DWConv3x3(V) + bias), rounded to fp16,
-//      the operand type of the next product;
-//   3. gemm_nt_kernel: Y = H W_o^T (fp16 operands; bf16 weights are widened),
+// Two launches (three when the output product splits K):
+//   1. gated_conv_kernel: H = SiLU(X W_g^T) * (DWConv3x3(X W_v^T) + bias) per
+//      tile of tokens, both products on MFMA with the input dtype's operands
+//      (fp16 or bf16) and float32 accumulation, rounded to fp16 on chip, the
+//      convolution's halo recomputed per tile; H is stored in fp16, the
+//      operand type of the next product;
+//   2. gemm_nt_kernel: Y = H W_o^T (fp16 operands; bf16 weights are widened),
 //      float32 partial products per K slice summed by ksplit_reduce_kernel.
 // Weights use the layout of a linear layer (output features first), so both
 // operands of every product are read along K in 16-byte pieces.
@@ -213,71 +213,170 @@ __global__ void __launch_bounds__(256) ksplit_reduce_kernel(const float* part, v
   }
 }
 
-// H[b][t][c] = SiLU(G[b][t][c]) * (sum_{u,v} V[b][t + (u-1, v-1)][c] * cw[c][u][v] + cb[c]).
-// One work-group per tile of kCT x kCT tokens and kCC channels. The
-// (kCT + 2)^2-token halo of V (zero outside the grid) is staged in LDS with
-// every global load of the work-group issued before any is used; each thread
-// then forms 8 channels of two tokens of the tile from LDS (a wave reads one
-// tile row of 8 tokens x 128 contiguous bytes per tap).
-constexpr int kCT = 8;            // tile edge in tokens
-constexpr int kCC = 64;           // channels per work-group (8 pieces of 8)
-constexpr int kHalo = kCT + 2;    // halo tile edge
-constexpr int kHaloPieces = kHalo * kHalo * (kCC / 8);
-constexpr int kHaloPer = (kHaloPieces + 255) / 256;
+// H[b][t][c] = SiLU(G[b][t][c]) * (sum_{u,v} V[b][t + (u-1, v-1)][c] * cw[c][u][v] + cb[c]),
+// G = X W_g^T and V = X W_v^T, in one launch. A work-group owns a tile of
+// kFH x kFW tokens of one image and kFN channels. Its K loop multiplies the
+// tile's (kFH + 2) x (kFW + 2)-token halo of X (rows outside the image are
+// zero) by the kFN rows of W_v, and the tile's own tokens (each tile row is a
+// run of 16 consecutive halo rows) by the kFN rows of W_g, with the load ring,
+// LDS swizzle and C^T accumulator layout of gemm_nt_kernel. The epilogue
+// rounds both products to fp16 into the LDS the K loop used and forms the
+// gated convolution there: G and V never leave the chip, and the halo's extra
+// V rows are the price (180 V rows per 128 tokens).
+constexpr int kFH = 8, kFW = 16;         // tile: 8 rows of 16 tokens
+constexpr int kFHW = kFW + 2;            // halo row length
+constexpr int kFV = (kFH + 2) * kFHW;    // halo tokens (180)
+constexpr int kFVT = (kFV + 15) / 16;    // MFMA row blocks of V (12; rows 180..191 are zero padding)
+constexpr int kFN = 64;                  // channels per work-group
+constexpr int kFA = kFVT * 16 * 4 / 256; // 16-byte A pieces per thread per K step (3)
+static_assert(kFVT % 4 == 0 && kFH % 4 == 0, "row blocks split evenly over 4 waves");
 
-__global__ void __launch_bounds__(256) conv_gate_kernel(const _Float16* G, const _Float16* V, const float* cw,
-                                                        const float* cb, _Float16* Hout, int Hh, int W,
-                                                        int hidden) {
-  __shared__ __attribute__((aligned(16))) _Float16 vs[kHalo * kHalo * kCC];
-  __shared__ __attribute__((aligned(16))) float wsm[kCC * 9];
-  __shared__ __attribute__((aligned(16))) float bsm[kCC];
-  const int tiles_x = (W + kCT - 1) / kCT, tiles_y = (Hh + kCT - 1) / kCT;
+struct GatedConvArgs {
+  const void* X;
+  const void* Wg;
+  const void* Wv;
+  const float* cw;  // [hidden][9]
+  const float* cb;  // [hidden] or null
+  _Float16* H;      // [B * Hh * W][hidden]
+  int Hh, W, d, hidden;
+};
+
+template <int DT>
+__global__ void __launch_bounds__(256) gated_conv_kernel(GatedConvArgs f) {
+  typedef Operand<DT, DT> OP;
+  constexpr int SA = kFVT * 16 * kPitch, SB = kFN * kPitch;  // 16-bit elements per stage
+  constexpr int VT = kFVT / 4, GT = kFH / 4;                 // row blocks of V and G per wave
+  constexpr int NJ = kFN / 16;                               // column blocks (all waves)
+  static_assert(2 * (SA + 2 * SB) >= (kFVT * 16 + kFH * kFW) * kFN, "epilogue tiles fit the stage buffers");
+  __shared__ __attribute__((aligned(16))) unsigned short stg[2][SA + 2 * SB];
+  __shared__ __attribute__((aligned(16))) float wsm[kFN * 9 + kFN];
+
+  const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63;
+  const int r16 = lane & 15, kq = lane >> 4;
+  const int tiles_x = (f.W + kFW - 1) / kFW, tiles_y = (f.Hh + kFH - 1) / kFH;
   const int tx = (int)(blockIdx.x % tiles_x);
   const int ty = (int)((blockIdx.x / tiles_x) % tiles_y);
   const int64_t b = blockIdx.x / ((unsigned)tiles_x * tiles_y);
-  const int c0 = blockIdx.y * kCC;
-  const int64_t L = (int64_t)Hh * W;
-  const int tid = threadIdx.x;
+  const int y0 = ty * kFH, x0 = tx * kFW;
+  const int c0 = blockIdx.y * kFN;
+  const int64_t L = (int64_t)f.Hh * f.W, K = f.d;
+  const unsigned short* X = static_cast<const unsigned short*>(f.X);
 
-  // halo pieces (token of the halo tile, 16-byte piece of its kCC channels)
-  w4 hv[kHaloPer];
-#pragma unroll
-  for (int q = 0; q < kHaloPer; ++q) {
-    const int p = tid + 256 * q;
-    const int ht = p >> 3, pc = p & 7;
-    const int gy = ty * kCT - 1 + ht / kHalo, gx = tx * kCT - 1 + ht % kHalo;
-    const bool in = p < kHaloPieces && gy >= 0 && gy < Hh && gx >= 0 && gx < W;
-    hv[q] = w4{0u, 0u, 0u, 0u};
-    if (in) hv[q] = *reinterpret_cast<const w4*>(V + (b * L + (int64_t)gy * W + gx) * hidden + c0 + 8 * pc);
+  // conv weights and bias of the work-group's channels (read in the epilogue)
+  if (tid < kFN * 9 / 4) reinterpret_cast<f4*>(wsm)[tid] = reinterpret_cast<const f4*>(f.cw + (int64_t)c0 * 9)[tid];
+  if (tid >= 160 && tid < 160 + kFN / 4) {
+    const int q = tid - 160;
+    reinterpret_cast<f4*>(wsm + kFN * 9)[q] =
+        f.cb ? reinterpret_cast<const f4*>(f.cb + c0)[q] : f4{0.f, 0.f, 0.f, 0.f};
   }
-  // this thread's outputs: channel piece pc, tile column rx, tile rows ry and ry + kCT / 2
-  const int pc = tid & 7, rx = (tid >> 3) % kCT, ry = (tid >> 3) / kCT;
-  w4 gv[2];
-  bool own[2];
-  int64_t tok[2];
-#pragma unroll
-  for (int k = 0; k < 2; ++k) {
-    const int gy = ty * kCT + ry + k * (kCT / 2), gx = tx * kCT + rx;
-    own[k] = gy < Hh && gx < W;
-    tok[k] = b * L + (int64_t)gy * W + gx;
-    gv[k] = w4{0u, 0u, 0u, 0u};
-    if (own[k]) gv[k] = *reinterpret_cast<const w4*>(G + tok[k] * hidden + c0 + 8 * pc);
-  }
-  // weights [kCC][9] and bias of the work-group's channels
-  f4 wv = {0.f, 0.f, 0.f, 0.f}, bv = {0.f, 0.f, 0.f, 0.f};
-  constexpr int WQ = kCC * 9 / 4, BQ = kCC / 4;
-  if (tid < WQ) wv = reinterpret_cast<const f4*>(cw + (int64_t)c0 * 9)[tid];
-  if (cb && tid >= WQ && tid < WQ + BQ) bv = reinterpret_cast<const f4*>(cb + c0)[tid - WQ];
 
+  // this thread's 16-byte pieces of the A (halo) and B (weight) tiles
+  const w4* ga[kFA];
+  unsigned am[kFA];  // all-ones for a token of the image, zero otherwise
+  int la[kFA];
 #pragma unroll
-  for (int q = 0; q < kHaloPer; ++q) {
-    const int p = tid + 256 * q;
-    if (p < kHaloPieces) *reinterpret_cast<w4*>(&vs[8 * p]) = hv[q];
+  for (int q = 0; q < kFA; ++q) {
+    const int p = tid + 256 * q, row = p >> 2, col = p & 3;
+    const int hy = row / kFHW, hx = row - hy * kFHW;
+    const int y = y0 - 1 + hy, x = x0 - 1 + hx;
+    const bool in = row < kFV && y >= 0 && y < f.Hh && x >= 0 && x < f.W;
+    ga[q] = reinterpret_cast<const w4*>(X + (in ? (b * L + (int64_t)y * f.W + x) * K : 0) + 8 * col);
+    am[q] = in ? 0xffffffffu : 0u;
+    la[q] = row * kPitch + 8 * (col ^ kSwz(row));
   }
-  if (tid < WQ) reinterpret_cast<f4*>(wsm)[tid] = wv;
-  if (tid >= WQ && tid < WQ + BQ) reinterpret_cast<f4*>(bsm)[tid - WQ] = bv;
+  const int brow = tid >> 2, bcol = tid & 3;
+  const w4* gbg = reinterpret_cast<const w4*>(static_cast<const unsigned short*>(f.Wg) + (int64_t)(c0 + brow) * K + 8 * bcol);
+  const w4* gbv = reinterpret_cast<const w4*>(static_cast<const unsigned short*>(f.Wv) + (int64_t)(c0 + brow) * K + 8 * bcol);
+  const int lb = brow * kPitch + 8 * (bcol ^ kSwz(brow));
+
+  f4 av[VT][NJ], ag[GT][NJ];
+#pragma unroll
+  for (int t = 0; t < VT; ++t)
+#pragma unroll
+    for (int j = 0; j < NJ; ++j) av[t][j] = f4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int t = 0; t < GT; ++t)
+#pragma unroll
+    for (int j = 0; j < NJ; ++j) ag[t][j] = f4{0.f, 0.f, 0.f, 0.f};
+
+  constexpr int D = 4;
+  w4 ra[D][kFA], rg[D], rv[D];
+  auto fetch = [&](int s, w4 (&a)[kFA], w4& g, w4& v) {
+#pragma unroll
+    for (int q = 0; q < kFA; ++q) a[q] = ga[q][4 * s];
+    g = gbg[4 * s];
+    v = gbv[4 * s];
+  };
+  auto stage = [&](int buf, const w4 (&a)[kFA], const w4& g, const w4& v) {
+    unsigned short* S = stg[buf];
+#pragma unroll
+    for (int q = 0; q < kFA; ++q) *reinterpret_cast<w4*>(&S[la[q]]) = a[q] & am[q];  // zero outside the image
+    *reinterpret_cast<w4*>(&S[SA + lb]) = g;
+    *reinterpret_cast<w4*>(&S[SA + SB + lb]) = v;
+  };
+  auto frag = [&](const unsigned short* S, int row) {
+    return OP::get(*reinterpret_cast<const w4*>(&S[row * kPitch + 8 * (kq ^ kSwz(row))]));
+  };
+  const int steps = f.d / 32;
+#pragma unroll
+  for (int q = 0; q < D; ++q)
+    if (q < steps) fetch(q, ra[q], rg[q], rv[q]);
+  stage(0, ra[0], rg[0], rv[0]);
+  __syncthreads();
+  for (int sb = 0; sb < steps; sb += D) {
+#pragma unroll
+    for (int q = 0; q < D; ++q) {
+      const int s = sb + q;
+      if (s < steps) {
+        const unsigned short* S = stg[s & 1];
+        if (s + D < steps) fetch(s + D, ra[q], rg[q], rv[q]);  // slot q was staged before this step
+        typename OP::T fg[NJ], fv[NJ];
+#pragma unroll
+        for (int j = 0; j < NJ; ++j) {
+          fg[j] = frag(S + SA, 16 * j + r16);
+          fv[j] = frag(S + SA + SB, 16 * j + r16);
+        }
+#pragma unroll
+        for (int t = 0; t < VT; ++t) {
+          const typename OP::T fa = frag(S, 16 * (VT * w + t) + r16);
+#pragma unroll
+          for (int j = 0; j < NJ; ++j) av[t][j] = mfma(fv[j], fa, av[t][j]);  // V^T tiles
+        }
+#pragma unroll
+        for (int t = 0; t < GT; ++t) {
+          const int ci = GT * w + t;  // tile row: halo rows (ci + 1) * kFHW + 1 .. + 16
+          const typename OP::T fa = frag(S, (ci + 1) * kFHW + 1 + r16);
+#pragma unroll
+          for (int j = 0; j < NJ; ++j) ag[t][j] = mfma(fg[j], fa, ag[t][j]);  // G^T tiles
+        }
+        if (s + 1 < steps) stage((s & 1) ^ 1, ra[(q + 1) % D], rg[(q + 1) % D], rv[(q + 1) % D]);
+        __syncthreads();
+      }
+    }
+  }
+
+  // epilogue: V [192 halo rows][kFN] and G [128 tile tokens][kFN] in fp16, in
+  // the stage buffers (every wave passed the K loop's last barrier)
+  _Float16* Vt = reinterpret_cast<_Float16*>(&stg[0][0]);
+  _Float16* Gt = Vt + kFVT * 16 * kFN;
+#pragma unroll
+  for (int t = 0; t < VT; ++t)
+#pragma unroll
+    for (int j = 0; j < NJ; ++j) {
+      const h4 hv = {(_Float16)av[t][j][0], (_Float16)av[t][j][1], (_Float16)av[t][j][2], (_Float16)av[t][j][3]};
+      *reinterpret_cast<h4*>(&Vt[(16 * (VT * w + t) + r16) * kFN + 16 * j + 4 * kq]) = hv;
+    }
+#pragma unroll
+  for (int t = 0; t < GT; ++t)
+#pragma unroll
+    for (int j = 0; j < NJ; ++j) {
+      const h4 hg = {(_Float16)ag[t][j][0], (_Float16)ag[t][j][1], (_Float16)ag[t][j][2], (_Float16)ag[t][j][3]};
+      *reinterpret_cast<h4*>(&Gt[(16 * (GT * w + t) + r16) * kFN + 16 * j + 4 * kq]) = hg;
+    }
   __syncthreads();
 
+  // gated convolution: 8 channels (piece pc) of 4 tile tokens per thread
+  const int pc = tid & 7, tg = tid >> 3;
   float wt[72];  // wt[9 e + 3 u + v]: tap (u, v) of channel 8 pc + e
 #pragma unroll
   for (int q = 0; q < 18; ++q) {
@@ -285,32 +384,34 @@ __global__ void __launch_bounds__(256) conv_gate_kernel(const _Float16* G, const
 #pragma unroll
     for (int e = 0; e < 4; ++e) wt[4 * q + e] = x[e];
   }
-  const f4 blo = reinterpret_cast<const f4*>(bsm + 8 * pc)[0], bhi = reinterpret_cast<const f4*>(bsm + 8 * pc)[1];
+  const f4 blo = reinterpret_cast<const f4*>(wsm + kFN * 9 + 8 * pc)[0];
+  const f4 bhi = reinterpret_cast<const f4*>(wsm + kFN * 9 + 8 * pc)[1];
 #pragma unroll
-  for (int k = 0; k < 2; ++k) {
+  for (int m = 0; m < kFH * kFW / 32; ++m) {
+    const int ct = tg + 32 * m, ci = ct / kFW, cj = ct % kFW;
     float acc[8];
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
       acc[e] = blo[e];
       acc[e + 4] = bhi[e];
     }
-    const int hy = ry + k * (kCT / 2);
 #pragma unroll
     for (int u = 0; u < 3; ++u)
 #pragma unroll
       for (int v = 0; v < 3; ++v) {
-        const h8 x = *reinterpret_cast<const h8*>(&vs[((hy + u) * kHalo + rx + v) * kCC + 8 * pc]);
+        const h8 x = *reinterpret_cast<const h8*>(&Vt[((ci + u) * kFHW + cj + v) * kFN + 8 * pc]);
 #pragma unroll
         for (int e = 0; e < 8; ++e) acc[e] = fmaf((float)x[e], wt[9 * e + 3 * u + v], acc[e]);
       }
-    const h8 g8 = __builtin_bit_cast(h8, gv[k]);
+    const h8 g8 = *reinterpret_cast<const h8*>(&Gt[ct * kFN + 8 * pc]);
     h8 out;
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
       const float z = (float)g8[e];
       out[e] = (_Float16)(z * __builtin_amdgcn_rcpf(1.f + __expf(-z)) * acc[e]);
     }
-    if (own[k]) *reinterpret_cast<h8*>(Hout + tok[k] * hidden + c0 + 8 * pc) = out;
+    const int y = y0 + ci, x = x0 + cj;
+    if (y < f.Hh && x < f.W) *reinterpret_cast<h8*>(f.H + (b * L + (int64_t)y * f.W + x) * f.hidden + c0 + 8 * pc) = out;
   }
 }
 
@@ -324,16 +425,14 @@ static int out_ksplit(int64_t M, int d, int hidden) {
 }
 
 struct SwigluLayout {
-  size_t g_off, v_off, h_off, part_off, total;
+  size_t h_off, part_off, total;
 };
 
 static SwigluLayout swiglu_layout(int64_t M, int d, int64_t hidden) {
   auto a256 = [](size_t x) { return (x + 255) & ~(size_t)255; };
   SwigluLayout l;
-  l.g_off = 0;
-  l.v_off = a256((size_t)M * hidden * 2);
-  l.h_off = a256(l.v_off + (size_t)M * hidden * 2);
-  l.part_off = a256(l.h_off + (size_t)M * hidden * 2);
+  l.h_off = 0;
+  l.part_off = a256((size_t)M * hidden * 2);
   const int ks = out_ksplit(M, d, (int)hidden);
   l.total = a256(l.part_off + (ks > 1 ? (size_t)ks * M * d * 4 : 0));
   return l;
@@ -399,27 +498,16 @@ extern "C" gtr_status gtr_spatial_swiglu(const gtr_swiglu_args* a, hipStream_t s
   if (st != GTR_OK) return st;
   const SwigluLayout lay = swiglu_layout(M, a->d, a->hidden);
   char* ws = static_cast<char*>(a->workspace);
-  _Float16* G = reinterpret_cast<_Float16*>(ws + lay.g_off);
-  _Float16* V = reinterpret_cast<_Float16*>(ws + lay.v_off);
   _Float16* Hb = reinterpret_cast<_Float16*>(ws + lay.h_off);
   const bool bf = a->dtype == GTR_BF16;
 
-  GemmArgs g1{a->x, {a->w_gate, a->w_value}, {G, V}, (int)M, a->hidden, a->d, GTR_F16, 1};
-  const bool n128 = a->hidden % 128 == 0;
-  const dim3 grid1((unsigned)((M + 127) / 128), (unsigned)(a->hidden / (n128 ? 128 : 64)), 2);
-  if (bf && n128)
-    hipLaunchKernelGGL((gemm_nt_kernel<GTR_BF16, GTR_BF16, GTR_BF16, 128, 128>), grid1, dim3(256), 0, stream, g1);
-  else if (bf)
-    hipLaunchKernelGGL((gemm_nt_kernel<GTR_BF16, GTR_BF16, GTR_BF16, 128, 64>), grid1, dim3(256), 0, stream, g1);
-  else if (n128)
-    hipLaunchKernelGGL((gemm_nt_kernel<GTR_F16, GTR_F16, GTR_F16, 128, 128>), grid1, dim3(256), 0, stream, g1);
+  const GatedConvArgs gc{a->x, a->w_gate, a->w_value, a->conv_w, a->conv_b, Hb, a->H, a->W, a->d, a->hidden};
+  const int64_t tiles = (int64_t)a->B * ((a->H + kFH - 1) / kFH) * ((a->W + kFW - 1) / kFW);
+  const dim3 grid1((unsigned)tiles, (unsigned)(a->hidden / kFN));
+  if (bf)
+    hipLaunchKernelGGL(gated_conv_kernel<GTR_BF16>, grid1, dim3(256), 0, stream, gc);
   else
-    hipLaunchKernelGGL((gemm_nt_kernel<GTR_F16, GTR_F16, GTR_F16, 128, 64>), grid1, dim3(256), 0, stream, g1);
-  if (hipGetLastError() != hipSuccess) return GTR_ERR_HIP;
-
-  const int64_t tiles = (int64_t)a->B * ((a->H + kCT - 1) / kCT) * ((a->W + kCT - 1) / kCT);
-  hipLaunchKernelGGL(conv_gate_kernel, dim3((unsigned)tiles, (unsigned)(a->hidden / kCC)), dim3(256), 0, stream,
-                     G, V, a->conv_w, a->conv_b, Hb, a->H, a->W, a->hidden);
+    hipLaunchKernelGGL(gated_conv_kernel<GTR_F16>, grid1, dim3(256), 0, stream, gc);
   if (hipGetLastError() != hipSuccess) return GTR_ERR_HIP;
 
   const int ks = out_ksplit(M, a->d, a->hidden);

@@ -841,6 +841,23 @@ HANDLERS.update({
 })
 
 
+def scmpk(fn, signed):
+    """s_cmpk_*: SGPR against a 16-bit immediate (sign-extended for the _i32 forms)."""
+    def h(w, i):
+        a = w.s32(i.ops[0], i)
+        k = int(i.ops[1], 0) & 0xFFFF
+        if signed and k & 0x8000:
+            k -= 0x10000
+        set_scc(w, fn(sx(a[0]) if signed else a[0], k) if not a[1] else 0, bool(a[1]), a[2])
+    return h
+
+
+for _n, _f in [('eq', lambda a, b: a == b), ('lg', lambda a, b: a != b), ('gt', lambda a, b: a > b),
+               ('ge', lambda a, b: a >= b), ('lt', lambda a, b: a < b), ('le', lambda a, b: a <= b)]:
+    HANDLERS[f's_cmpk_{_n}_i32'] = scmpk(_f, True)
+    HANDLERS[f's_cmpk_{_n}_u32'] = scmpk(_f, False)
+
+
 @handler('s_set_gpr_idx_on')
 def _gidx_on(w, i):
     v, o, d = w.s32(i.ops[0], i)
@@ -1677,6 +1694,10 @@ HANDLERS.update({
     'v_sub_u32_sdwa': sdwa_int(lambda a, b: a - b, 2),
     'v_mov_b32_sdwa': sdwa_int(lambda a: a, 1),
     'v_and_b32_sdwa': sdwa_int(lambda a, b: a & b, 2),
+    'v_mul_i32_i24_sdwa': sdwa_int(lambda a, b: ((s24(a) * s24(b)).astype(np.uint64) & np.uint64(M32))
+                                   .astype(np.uint32), 2),
+    'v_mul_u32_u24_sdwa': sdwa_int(lambda a, b: ((u64(a & np.uint32(0xFFFFFF)) * u64(b & np.uint32(0xFFFFFF)))
+                                                 & np.uint64(M32)).astype(np.uint32), 2),
     'v_mul_lo_u16_sdwa': sdwa_int(lambda a, b: (u64(a & np.uint32(0xFFFF)) * u64(b & np.uint32(0xFFFF))
                                                 & np.uint64(0xFFFF)).astype(np.uint32), 2),
     # 16-bit VOP2 ops of this generation write the low half and zero the high half

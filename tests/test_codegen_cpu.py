@@ -287,7 +287,7 @@ def check_kernel(text, name, kern, regions, wgs, waves=4):
     assert "INFO-PATHLIMIT" not in rep.counts
 
 
-@pytest.mark.parametrize("adt,bdt,mt,bn,M,N,K,cdt,ks", [(2, 2, 2, 128, 126, 256, 64, 0, 1),
+@pytest.mark.parametrize("adt,bdt,mt,bn,M,N,K,cdt,ks", [(1, 2, 1, 128, 126, 256, 64, 0, 1),
                                                         (1, 1, 1, 128, 1600, 384, 1536, 1, 4),
                                                         (1, 2, 1, 64, 63, 64, 128, 2, 1),
                                                         (1, 1, 1, 64, 200, 192, 192, 1, 2)])
@@ -309,18 +309,20 @@ def test_swiglu_gemm_addresses(adt, bdt, mt, bn, M, N, K, cdt, ks):
     check_kernel(text, name, kern, regions, wgs)
 
 
-@pytest.mark.parametrize("B,H,W,hidden", [(2, 7, 9, 128), (1, 40, 40, 192), (1, 16, 3, 64)])
-def test_swiglu_conv_gate_addresses(B, H, W, hidden):
+@pytest.mark.parametrize("dt,B,H,W,d,hidden", [(1, 2, 7, 9, 64, 128), (2, 1, 40, 40, 384, 192),
+                                                (1, 1, 16, 3, 128, 64), (2, 1, 9, 33, 64, 64)])
+def test_swiglu_gated_conv_addresses(dt, B, H, W, d, hidden):
     text = swiglu_asm()
     M = B * H * W
     base = 0x1000_0000_0000
-    G, V, CW, CB, HO = (base + i * 0x10_0000_0000 for i in range(5))
-    regions = [emu.Region("G", G, M * hidden * 2, "r"), emu.Region("V", V, M * hidden * 2, "r"),
-               emu.Region("cw", CW, hidden * 9 * 4, "r"), emu.Region("cb", CB, hidden * 4, "r"),
-               emu.Region("H", HO, M * hidden * 2, "w"), emu.Region("kernarg", emu.KERNARG_BASE, 56, "r")]
-    kern = struct.pack("<QQQQQiii4x", G, V, CW, CB, HO, H, W, hidden)
-    name = [n for n in emu.kernel_names(text) if "conv_gate_kernel" in n][0]
-    tx, ty = (W + 7) // 8, (H + 7) // 8  # one work-group per 8 x 8 tokens x 64 channels
+    X, WG, WV, CW, CB, HO = (base + i * 0x10_0000_0000 for i in range(6))
+    regions = [emu.Region("X", X, M * d * 2, "r"), emu.Region("Wg", WG, hidden * d * 2, "r"),
+               emu.Region("Wv", WV, hidden * d * 2, "r"), emu.Region("cw", CW, hidden * 9 * 4, "r"),
+               emu.Region("cb", CB, hidden * 4, "r"), emu.Region("H", HO, M * hidden * 2, "w"),
+               emu.Region("kernarg", emu.KERNARG_BASE, 64, "r")]
+    kern = struct.pack("<QQQQQQiiii", X, WG, WV, CW, CB, HO, H, W, d, hidden)
+    name = [n for n in emu.kernel_names(text) if "gated_conv_kernel" in n and f"ILi{dt}E" in n][0]
+    tx, ty = (W + 15) // 16, (H + 7) // 8  # one work-group per 8 x 16 tokens x 64 channels
     nt, nc = B * tx * ty, hidden // 64
     wgs = sorted({(x, y, 0) for x in (0, tx - 1, nt - 1, nt // 2) for y in (0, nc - 1)})
     check_kernel(text, name, kern, regions, wgs)
