@@ -81,6 +81,8 @@ def parse():
     p.add_argument("--cold-sets", type=int, default=128,
                    help="also time the calls rotating over this many distinct input sets (more bytes than the "
                         "256 MB MALL holds, so every call reads HBM); 0 skips it")
+    p.add_argument("--swiglu-only", action="store_true",
+                   help="only time the Spatial SwiGLU (GTR-L and GTR-X widths) and print its JSON line")
     p.add_argument("--calibrate-copy", type=float, default=0.0, metavar="MB",
                    help="only run a device-to-device copy of MB megabytes --steps times")
     return p.parse_args()
@@ -215,6 +217,9 @@ def main():
         calibrate_copy(a.calibrate_copy, a.steps)
         return
     gtr.load()
+    if a.swiglu_only:
+        print(json.dumps(swiglu_detail()), flush=True)
+        return
     wl = WORKLOADS[a.workload]
     step = setup(wl, a.path, scan=wl.scans[0])
     secs = time_graph(step, a.steps, a.warmup)
