@@ -401,3 +401,88 @@ def test_spatial_swiglu_parity(gtr, case):
     tol = 2e-3 + (2.0 ** -8 if ydt == "bf16" else 0.0)
     assert y.dtype == torch_dtype(ydt)
     assert rel_err(y, ref) <= tol, rel_err(y, ref)
+
+
+# ---------------------------------------------------------------------------
+# randomized shapes: a fixed-seed draw over every argument the kernels branch
+# on (sizes, head widths, chunk, dtypes, a float32 g with 16-bit inputs, scan,
+# S0, S_final, schedule, gate strength from slow to fast decay)
+# ---------------------------------------------------------------------------
+def _random_cases(n=32, seed=2609):
+    rng = np.random.default_rng(seed)
+    cases = []
+    for i in range(n):
+        dt = ("f32", "f16", "bf16")[rng.integers(3)]
+        odt = {"f32": "f32", "f16": ("f16", "f32")[rng.integers(2)], "bf16": ("f32", "bf16")[rng.integers(2)]}[dt]
+        dk, dv = ((32, 32), (32, 64), (64, 64))[rng.integers(3)]
+        wl = Workload(f"rand{i}", B=int(rng.integers(1, 4)), heads=int(rng.integers(1, 6)),
+                      H=int(rng.integers(1, 24)), W=int(rng.integers(1, 24)), dk=dk, dv=dv, dtype=dt, odtype=odt,
+                      gate_mu=float(rng.uniform(-1.0, 5.0)), gate_std=float(rng.uniform(0.5, 2.0)),
+                      qk_std=dk ** -0.5, v_std=1.0, s0_std=0.1 if rng.random() < 0.5 else None,
+                      want_final=bool(rng.random() < 0.5), chunk=int((32, 64, 128)[rng.integers(3)]), seed=1000 + i)
+        scan = ("row", "col", "row_rev", "col_rev")[rng.integers(4)]
+        path = ("auto", "staged", "fused", "inline")[rng.integers(4)]
+        g32 = dt != "f32" and bool(rng.random() < 0.3)
+        cases.append((wl, scan, path, g32))
+    return cases
+
+
+RANDOM = _random_cases()
+
+
+@pytest.mark.parametrize("case", range(len(RANDOM)))
+def test_random_shapes(gtr, case):
+    wl, scan, path, g32 = RANDOM[case]
+    inp = make_inputs(wl)
+    if g32:
+        inp = dict(inp, g=inp["g"].float())  # the rounded values, widened exactly
+    ref_o, ref_sf = oracle.gla(inp["q"], inp["k"], inp["v"], inp["g"], inp["s0"], scale=wl.scale, H=wl.H, W=wl.W,
+                               scan=scan)
+    o, sf = run_gpu(gtr, wl, scan, wl.chunk, path, inp=inp)
+    tol = tol_for(wl.dtype, wl.odtype)
+    assert rel_err(o, ref_o) <= tol, (wl, scan, path, g32)
+    if wl.want_final:
+        assert rel_err(sf, ref_sf) <= tol_for(wl.dtype, "f32"), (wl, scan, path, g32)
+
+
+# ---------------------------------------------------------------------------
+# Spatial SwiGLU: graph replays, guard regions, untouched inputs, determinism
+# ---------------------------------------------------------------------------
+def test_spatial_swiglu_graph_canaries_deterministic(gtr):
+    B, H, W, d, h = 2, 17, 35, 128, 192
+    rng = np.random.default_rng(7)
+    dev = torch.device("cuda")
+    mk = lambda shape, s, dt=torch.float16: torch.from_numpy(rng.normal(0.0, s, size=shape)).float().to(dt).to(dev)
+    x, wg, wv, wo = mk((B, H * W, d), 1.0), mk((h, d), d ** -0.5), mk((h, d), d ** -0.5), mk((d, h), h ** -0.5)
+    cw, cb = mk((h, 3, 3), 1 / 3, torch.float32), mk((h,), 0.1, torch.float32)
+    before = [t.clone() for t in (x, wg, wv, wo, cw, cb)]
+    n, guard = B * H * W * d, 4096
+    ybuf = [torch.full((n + 2 * guard,), 321.0, dtype=torch.float16, device=dev) for _ in range(2)]
+    ys = [yb[guard:guard + n].view(B, H * W, d) for yb in ybuf]
+    ws = gtr.Workspace(dev)
+
+    def calls():
+        for y in ys:
+            gtr.gtr_spatial_swiglu(x, wg, wv, wo, cw, cb, H=H, W=W, out=y, workspace=ws)
+
+    calls()
+    torch.cuda.synchronize()
+    eager = ys[0].clone()
+    assert torch.equal(ys[0], ys[1])  # same inputs, same bits
+    for yb in ybuf:
+        assert torch.all(yb[:guard] == 321.0) and torch.all(yb[guard + n:] == 321.0)
+    for a, b in zip(before, (x, wg, wv, wo, cw, cb)):
+        assert torch.equal(a, b)
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        calls()
+    for rep in range(3):
+        for y in ys:
+            y.fill_(float("nan"))
+        torch.cuda.synchronize()
+        graph.replay()
+        torch.cuda.synchronize()
+        for y in ys:
+            assert torch.equal(y, eager), f"replay {rep} differs"
+        calls()  # eager work between replays
+        torch.cuda.synchronize()
