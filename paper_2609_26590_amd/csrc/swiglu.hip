@@ -66,13 +66,14 @@ __device__ __forceinline__ f4 mfma(const bf8& a, const bf8& b, f4 c) {
 // A and B tiles in LDS once (each element is read from memory by one thread
 // and from LDS by every wave that needs it); the loads of the next step are in
 // flight while the current one multiplies (two LDS buffers). Rows past M are
-// read from row M-1 and not stored. blockIdx.z selects one of two (B, C) pairs
-// (G and V come out of one launch) or, with ksplit > 1, a slice of K whose
-// partial product goes to C[1] + slice * M * N (float32) for a reduction.
+// read from row M-1 and not stored. With ksplit > 1, blockIdx.z selects a
+// slice of K whose partial product goes to part + slice * M * N (float32) for
+// ksplit_reduce_kernel; with ksplit = 1 the product goes to C.
 struct GemmArgs {
   const void* A;
-  const void* B[2];
-  void* C[2];
+  const void* B;
+  void* C;
+  float* part;
   int M, N, K;
   int cdt;     // dtype of C (GTR_F32 / GTR_F16 / GTR_BF16)
   int ksplit;  // number of K slices (1: none)
@@ -101,9 +102,8 @@ __global__ void __launch_bounds__(256) gemm_nt_kernel(GemmArgs g) {
   const int r16 = lane & 15, kq = lane >> 4;
   const int mb = blockIdx.x * BM, nb = blockIdx.y * BN;
   const int wm = (w >> 1) * (BM / 2), wn = (w & 1) * (BN / 2);
-  const int pair = g.ksplit > 1 ? 0 : blockIdx.z;
   const unsigned short* A = static_cast<const unsigned short*>(g.A);
-  const unsigned short* B = static_cast<const unsigned short*>(g.B[pair]);
+  const unsigned short* B = static_cast<const unsigned short*>(g.B);
   const int64_t K = g.K;
   const int steps = g.K / 32;
   const int s_per = (steps + g.ksplit - 1) / g.ksplit;
@@ -181,8 +181,7 @@ __global__ void __launch_bounds__(256) gemm_nt_kernel(GemmArgs g) {
 
   // lane holds C[row 16i + r16][columns 16j + 4kq .. 16j + 4kq + 3] of this
   // wave's block (the products above are C^T tiles): one 4-element store each
-  void* C = g.ksplit > 1 ? static_cast<void*>(static_cast<float*>(g.C[1]) + (int64_t)blockIdx.z * g.M * g.N)
-                         : g.C[blockIdx.z];
+  void* C = g.ksplit > 1 ? static_cast<void*>(g.part + (int64_t)blockIdx.z * g.M * g.N) : g.C;
   const int cdt = g.ksplit > 1 ? (int)GTR_F32 : g.cdt;
 #pragma unroll
   for (int i = 0; i < TI; ++i) {
@@ -512,8 +511,7 @@ extern "C" gtr_status gtr_spatial_swiglu(const gtr_swiglu_args* a, hipStream_t s
 
   const int ks = out_ksplit(M, a->d, a->hidden);
   float* part = reinterpret_cast<float*>(ws + lay.part_off);
-  GemmArgs g3{Hb, {a->w_out, a->w_out}, {a->y, ks > 1 ? static_cast<void*>(part) : a->y}, (int)M, a->d,
-              a->hidden, a->y_dtype, ks};
+  GemmArgs g3{Hb, a->w_out, a->y, part, (int)M, a->d, a->hidden, a->y_dtype, ks};
   const bool d128 = a->d % 128 == 0;
   const dim3 grid3((unsigned)((M + 127) / 128), (unsigned)(a->d / (d128 ? 128 : 64)), (unsigned)ks);
   if (bf && d128)

@@ -295,16 +295,16 @@ def test_swiglu_gemm_addresses(adt, bdt, mt, bn, M, N, K, cdt, ks):
     text = swiglu_asm()
     base = 0x1000_0000_0000
     es = {0: 4, 1: 2, 2: 2}
-    A, B0, B1, C0, C1 = (base + i * 0x10_0000_0000 for i in range(5))
-    c1_bytes = ks * M * N * 4 if ks > 1 else M * N * es[cdt]  # K-split partials are float32
-    regions = [emu.Region("A", A, M * K * 2, "r"), emu.Region("B0", B0, N * K * 2, "r"),
-               emu.Region("B1", B1, N * K * 2, "r"), emu.Region("C0", C0, M * N * es[cdt], "w"),
-               emu.Region("C1", C1, c1_bytes, "w"), emu.Region("kernarg", emu.KERNARG_BASE, 64, "r")]
-    kern = struct.pack("<QQQQQiiiii4x", A, B0, B1, C0, C1, M, N, K, cdt, ks)
+    A, B, C, P = (base + i * 0x10_0000_0000 for i in range(4))
+    regions = [emu.Region("A", A, M * K * 2, "r"), emu.Region("B", B, N * K * 2, "r"),
+               emu.Region("C", C, M * N * es[cdt], "w"),
+               emu.Region("part", P, ks * M * N * 4, "w"),  # K-split partials are float32
+               emu.Region("kernarg", emu.KERNARG_BASE, 64, "r")]
+    kern = struct.pack("<QQQQiiiii4x", A, B, C, P, M, N, K, cdt, ks)
     name = f"_ZN3gtr14gemm_nt_kernelILi{adt}ELi{bdt}ELi{mt}ELi128ELi{bn}EEEvNS_8GemmArgsE"
     assert name in emu.kernel_names(text)
     gx, gy = (M + 127) // 128, N // bn
-    zs = range(ks) if ks > 1 else (0, 1)
+    zs = range(ks)
     wgs = [(x, y, z) for x in sorted({0, gx - 1}) for y in sorted({0, gy - 1}) for z in sorted({min(zs), max(zs)})]
     check_kernel(text, name, kern, regions, wgs)
 
