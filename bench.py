@@ -44,7 +44,7 @@ from paper_2609_26590_amd.workloads import (WORKLOADS, algorithmic_bytes, algori
 HBM_PEAK_GBS = 8000.0        # MI355X HBM3E, published
 MFMA_F16_PEAK_TFLOPS = 2500.0  # MI355X dense fp16 matrix, published
 KERNEL_SOURCES = ("paper_2609_26590_amd/csrc/gla_fwd.hip", "paper_2609_26590_amd/csrc/gtr_device.h")
-TRAFFIC_PROFILE = "profiles/gla_fused_kbench_traffic.txt"
+TRAFFIC_PROFILE = "profiles/gla_kbench_auto_traffic.txt"  # counters of the default (AUTO) run
 
 
 def kernel_source_hash() -> str:
@@ -55,17 +55,34 @@ def kernel_source_hash() -> str:
     return h.hexdigest()[:16]
 
 
-def stored_traffic():
-    """HBM bytes per call from the committed counter summary, if it is current."""
+def stored_traffic(schedule):
+    """HBM bytes per call from the committed counter profile, if it was taken on
+    these kernel sources and for this schedule (else None)."""
     path = os.path.join(ROOT, TRAFFIC_PROFILE)
     if not os.path.exists(path):
         return None
     txt = open(path).read()
     m_hash = re.search(r"kernel source hash:\s*([0-9a-f]+)", txt)
+    m_sched = re.search(r"schedule:\s*(\w+)", txt)
     m_val = re.search(r"traffic bytes per call:\s*([0-9.eE+]+)", txt)
-    if not m_hash or not m_val or m_hash.group(1) != kernel_source_hash():
+    if not m_hash or not m_val or not m_sched or m_hash.group(1) != kernel_source_hash() or \
+            m_sched.group(1) != schedule:
         return None
     return float(m_val.group(1))
+
+
+def schedule_of(wl, path):
+    """The schedule gtr_gla_fwd runs for the workload (empty tensors of its shapes)."""
+    dev = torch.device("cuda")
+    mk = lambda d: torch.empty((wl.B, wl.heads, wl.L, d), dtype=torch_dtype(wl.dtype), device=dev)
+    s0 = torch.empty((wl.B, wl.heads, wl.dk, wl.dv), device=dev) if wl.s0_std is not None else None
+    return gtr.gtr_gla_schedule(mk(wl.dk), mk(wl.dk), mk(wl.dv), mk(wl.dk), H=wl.H, W=wl.W, chunk=wl.chunk,
+                                s0=s0, want_final=wl.want_final, o_dtype=torch_dtype(wl.odtype), path=path)
+
+
+KERNEL_OF = {"inline": "gla_fused_kernel<..., true> (inline schedule; the whole call is this one launch)",
+             "fused": "gla_fused_kernel<..., false> (fused schedule; the whole call is this one launch)",
+             "staged": "one gtr_gla_fwd call (summary + scan + output kernels)"}
 
 
 def parse():
@@ -221,6 +238,7 @@ def main():
         print(json.dumps(swiglu_detail()), flush=True)
         return
     wl = WORKLOADS[a.workload]
+    sched = schedule_of(wl, a.path)
     step = setup(wl, a.path, scan=wl.scans[0])
     secs = time_graph(step, a.steps, a.warmup)
     per_call = secs / a.steps
@@ -249,9 +267,8 @@ def main():
         "tflops": flops / per_call / 1e12,
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": achieved / HBM_PEAK_GBS,
-                     "traffic": stored_traffic() if a.path in ("auto", "fused") else None,
-                     "kernel": "gla_fused_kernel (the whole call is this one launch)" if a.path != "staged"
-                               else "one gtr_gla_fwd call (summary + scan + output kernels)",
+                     "traffic": stored_traffic(sched) if a.workload == "kbench" else None,
+                     "kernel": KERNEL_OF[sched], "schedule": sched,
                      "alg_bytes_per_call": nbytes, "us_per_call": per_call * 1e6,
                      "timing": "HIP events around a graph of K calls on the launch stream, divided by K",
                      "kernel_source_hash": kernel_source_hash(),

@@ -96,10 +96,11 @@ typedef enum {
  * the length-aware dispatch of the paper's operator appendix). */
 typedef enum {
   GTR_PATH_AUTO = 0,   /* the library picks: up to 8 sequences, INLINE while the
-                          summaries of a sequence hold at most 64K elements
-                          (nchunks * dk * dv), else FUSED if every chunk of a sequence
-                          can be resident on one XCD; otherwise (and for more than 8
-                          sequences) STAGED                                           */
+                          summaries of a sequence take at most 256 KB (nchunks * dk *
+                          dv elements, fp16 for 16-bit inputs, float32 otherwise),
+                          else FUSED if every chunk of a sequence can be resident on
+                          one XCD; otherwise (and for more than 8 sequences) STAGED.
+                          gtr_gla_schedule reports the choice.                        */
   GTR_PATH_FUSED = 1,  /* one launch: summaries, boundary-state scan split over the
                           work-groups of a sequence, outputs                          */
   GTR_PATH_STAGED = 2, /* three launches: summaries, boundary-state scan, outputs      */
@@ -197,6 +198,17 @@ gtr_status gtr_gla_workspace_init(void* workspace, size_t bytes, hipStream_t str
  * with o written back at the token's spatial index, and S_final = S at the end.
  */
 gtr_status gtr_gla_fwd(const gtr_gla_args* args, hipStream_t stream);
+
+/*
+ * gtr_gla_schedule - the schedule gtr_gla_fwd would run for `args`
+ * (GTR_PATH_FUSED, GTR_PATH_STAGED or GTR_PATH_INLINE; for an explicit path,
+ * that path), or -1 if the arguments are invalid (pointers are not checked) or
+ * an explicit one-launch path does not fit. Host-only; reads the current
+ * device's occupancy for the one-launch schedules (without a usable device
+ * AUTO reports GTR_PATH_STAGED). The length-aware dispatch of the paper's
+ * operator appendix.
+ */
+int gtr_gla_schedule(const gtr_gla_args* args);
 
 /*
  * Spatial SwiGLU (Sec. 3.1, "Spatial SwiGLU"; the scope table's row f4):

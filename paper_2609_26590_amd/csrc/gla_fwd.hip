@@ -49,6 +49,7 @@
 #include <hip/hip_runtime.h>
 
 #include <mutex>
+#include <type_traits>
 
 #include "gtr.h"
 #include "gtr_device.h"
@@ -92,6 +93,7 @@ struct GlaParams {
 constexpr int tile_threads(int chunk) { return chunk / 16 * kWave; }
 
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));
 
 // ---------------------------------------------------------------------------
 // Agent-coherent buffer accesses (cache policy sc1: no stale copy in the CU's
@@ -408,9 +410,11 @@ struct Chunk {
     if constexpr (SUMMARY) __syncthreads();
   }
 
-  // U_c as U^T ([DV][DK] fp32) to `U`, coherent or plain.
-  template <bool COH, class S>
-  __device__ __forceinline__ void summary_out(const S& sm, float* U) {
+  // U_c as U^T ([DV][DK]) to `U` in float32 or, with U16 (16-bit inputs), to
+  // `U16p` rounded to fp16, the type the states are handed over in; coherent
+  // (agent scope) or plain.
+  template <bool COH, bool U16 = false, class S>
+  __device__ __forceinline__ void summary_out(const S& sm, float* U, unsigned short* U16p = nullptr) {
     constexpr int NTI = (DK / 16) * (DV / 16);
     const __amdgpu_buffer_rsrc_t ur = make_rsrc(U, DK * DV * 4);
     for (int tau = w; tau < NTI; tau += NW) {
@@ -424,7 +428,14 @@ struct Chunk {
       }
       // lane holds U[16ib + 4gq + e][16jb + tr]
       const int off = (16 * jb + tr) * DK + 16 * ib + 4 * gq;
-      if constexpr (COH)
+      if constexpr (U16) {
+        const h4 hv = {(_Float16)acc[0], (_Float16)acc[1], (_Float16)acc[2], (_Float16)acc[3]};
+        if constexpr (COH)
+          __builtin_amdgcn_raw_buffer_store_b64(__builtin_bit_cast(u32x2, hv), make_rsrc(U16p, DK * DV * 2), off * 2, 0,
+                                                kAgentCoherent);
+        else
+          *reinterpret_cast<h4*>(reinterpret_cast<_Float16*>(U16p) + off) = hv;
+      } else if constexpr (COH)
         coh_store4(ur, off * 4, acc);
       else
         *reinterpret_cast<f4*>(&U[off]) = acc;
@@ -589,16 +600,23 @@ struct Chunk {
       }
     }
   }
-  // Staged schedule with 16-bit inputs: the scan kernel has already rounded
-  // S_[c]^T to the fp16 MFMA operand type (what state_store would do), so the
-  // output kernel moves 16-byte pieces of 8 elements straight to the tile.
+  // 16-bit inputs: the states are handed over already rounded to the fp16 MFMA
+  // operand type (what state_store would do), so 16-byte pieces of 8 elements
+  // move straight to the tile.
   static constexpr int SQ8 = DK * DV / 8;
   static constexpr int SPER8 = (SQ8 + NT - 1) / NT;
+  template <bool COH = false>
   __device__ __forceinline__ void state_load16(const unsigned short* ST, u32x4 (&buf)[SPER8]) const {
+    const __amdgpu_buffer_rsrc_t sr = make_rsrc(ST, DK * DV * 2);
 #pragma unroll
     for (int m = 0; m < SPER8; ++m) {
       const int q8 = threadIdx.x + m * NT;
-      if (q8 < SQ8) buf[m] = reinterpret_cast<const u32x4*>(ST)[q8];
+      if (q8 < SQ8) {
+        if constexpr (COH)
+          buf[m] = __builtin_amdgcn_raw_buffer_load_b128(sr, q8 * 16, 0, kAgentCoherent);
+        else
+          buf[m] = reinterpret_cast<const u32x4*>(ST)[q8];
+      }
     }
   }
   template <class S>
@@ -717,40 +735,61 @@ struct Chunk {
 // ---------------------------------------------------------------------------
 // Boundary-state scan over chunks (Eq. chunk_boundary_main) for elements
 // [e0, e1) of one sequence's state (S^T layout, element e = dv*DK + i). Reads
-// U_c^T and writes S_[c]^T in place (float32), or, for 16-bit inputs (H16), to
-// the fp16 states the output kernel feeds to its readout. S_final gets the
-// float32 state after the last chunk.
+// U_c^T and writes S_[c]^T in place, float32, or, for 16-bit inputs (H16),
+// fp16 in and out (the summaries as the summary kernel rounded them, the states
+// as the output kernel's readout consumes them), accumulating in float32.
+// S_final gets the float32 state after the last chunk.
 // ---------------------------------------------------------------------------
 template <int DK, int DV, bool H16>
 __device__ __forceinline__ void scan_plain(const GlaParams& P, int bh, int e0, int e1, int tid, int nt) {
+  // two adjacent elements (dims i, i + 1 of one d_v row) per thread: 8-byte
+  // loads of U and of the decays, 4-byte fp16 (or 8-byte float32) stores
+  typedef float f2 __attribute__((ext_vector_type(2)));
+  typedef _Float16 h2 __attribute__((ext_vector_type(2)));
+  static_assert(DK % 2 == 0, "element pairs share a d_v row");
   float* st = P.states + (int64_t)bh * P.nchunks * (DK * DV);
   _Float16* st16 = reinterpret_cast<_Float16*>(P.states16) + (int64_t)bh * P.nchunks * (DK * DV);
   const float* dec = P.decays + (int64_t)bh * P.nchunks * DK;
   const int NC = P.nchunks;
-  for (int e = e0 + tid; e < e1; e += nt) {
+  for (int e = e0 + 2 * tid; e < e1; e += 2 * nt) {
     const int dv = e / DK, i = e - dv * DK;
-    float s = P.s0 ? P.s0[((int64_t)bh * DK + i) * DV + dv] : 0.f;
+    f2 s = {0.f, 0.f};
+    if (P.s0) {
+      s[0] = P.s0[((int64_t)bh * DK + i) * DV + dv];
+      s[1] = P.s0[((int64_t)bh * DK + i + 1) * DV + dv];
+    }
     for (int c0 = 0; c0 < NC; c0 += 32) {
-      float u[32], d[32];
+      // raw loads first (all 32 in flight), conversions only where the values
+      // are used: a conversion next to its load would wait for that load
+      typedef typename std::conditional<H16, h2, f2>::type U2;
+      U2 u[32];
+      f2 d[32];
 #pragma unroll
       for (int m = 0; m < 32; ++m) {
         if (c0 + m < NC) {
-          u[m] = st[(int64_t)(c0 + m) * (DK * DV) + e];
-          d[m] = dec[(int64_t)(c0 + m) * DK + i];
+          if constexpr (H16)
+            u[m] = *reinterpret_cast<const h2*>(&st16[(int64_t)(c0 + m) * (DK * DV) + e]);
+          else
+            u[m] = *reinterpret_cast<const f2*>(&st[(int64_t)(c0 + m) * (DK * DV) + e]);
+          d[m] = *reinterpret_cast<const f2*>(&dec[(int64_t)(c0 + m) * DK + i]);
         }
       }
 #pragma unroll
       for (int m = 0; m < 32; ++m) {
         if (c0 + m < NC) {
           if constexpr (H16)
-            st16[(int64_t)(c0 + m) * (DK * DV) + e] = (_Float16)s;
+            *reinterpret_cast<h2*>(&st16[(int64_t)(c0 + m) * (DK * DV) + e]) = h2{(_Float16)s[0], (_Float16)s[1]};
           else
-            st[(int64_t)(c0 + m) * (DK * DV) + e] = s;
-          s = d[m] * s + u[m];
+            *reinterpret_cast<f2*>(&st[(int64_t)(c0 + m) * (DK * DV) + e]) = s;
+          s[0] = d[m][0] * s[0] + (float)u[m][0];
+          s[1] = d[m][1] * s[1] + (float)u[m][1];
         }
       }
     }
-    if (P.s_final) P.s_final[((int64_t)bh * DK + i) * DV + dv] = s;
+    if (P.s_final) {
+      P.s_final[((int64_t)bh * DK + i) * DV + dv] = s[0];
+      P.s_final[((int64_t)bh * DK + i + 1) * DV + dv] = s[1];
+    }
   }
 }
 
@@ -785,6 +824,53 @@ __device__ __forceinline__ void scan_coherent(const GlaParams& P, int bh, int e0
   }
 }
 
+// The same over fp16 summaries and states (16-bit inputs), two adjacent
+// elements per thread, accumulating in float32.
+template <int DK, int DV>
+__device__ __forceinline__ void scan_coherent16(const GlaParams& P, int bh, int e0, int e1, int tid, int nt) {
+  typedef float f2 __attribute__((ext_vector_type(2)));
+  typedef _Float16 h2 __attribute__((ext_vector_type(2)));
+  const int NC = P.nchunks;
+  const __amdgpu_buffer_rsrc_t sr = make_rsrc(P.states16 + (int64_t)bh * NC * (DK * DV), (uint32_t)NC * DK * DV * 2);
+  const __amdgpu_buffer_rsrc_t dr = make_rsrc(P.decays + (int64_t)bh * NC * DK, (uint32_t)NC * DK * 4);
+  for (int e = e0 + 2 * tid; e < e1; e += 2 * nt) {
+    const int dv = e / DK, i = e - dv * DK;
+    f2 s = {0.f, 0.f};
+    if (P.s0) {
+      s[0] = P.s0[((int64_t)bh * DK + i) * DV + dv];
+      s[1] = P.s0[((int64_t)bh * DK + i + 1) * DV + dv];
+    }
+    for (int c0 = 0; c0 < NC; c0 += 32) {
+      unsigned u[32];
+      u32x2 d[32];
+#pragma unroll
+      for (int m = 0; m < 32; ++m) {
+        if (c0 + m < NC) {
+          u[m] = __builtin_amdgcn_raw_buffer_load_b32(sr, (int)(((uint32_t)(c0 + m) * (DK * DV) + e) * 2), 0,
+                                                      kAgentCoherent);
+          d[m] = __builtin_amdgcn_raw_buffer_load_b64(dr, (int)(((uint32_t)(c0 + m) * DK + i) * 4), 0, kAgentCoherent);
+        }
+      }
+#pragma unroll
+      for (int m = 0; m < 32; ++m) {
+        if (c0 + m < NC) {
+          const h2 hs = {(_Float16)s[0], (_Float16)s[1]};
+          __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(unsigned, hs), sr,
+                                                (int)(((uint32_t)(c0 + m) * (DK * DV) + e) * 2), 0, kAgentCoherent);
+          const h2 hu = __builtin_bit_cast(h2, u[m]);
+          const f2 dd = __builtin_bit_cast(f2, d[m]);
+          s[0] = dd[0] * s[0] + (float)hu[0];
+          s[1] = dd[1] * s[1] + (float)hu[1];
+        }
+      }
+    }
+    if (P.s_final) {
+      P.s_final[((int64_t)bh * DK + i) * DV + dv] = s[0];
+      P.s_final[((int64_t)bh * DK + i + 1) * DV + dv] = s[1];
+    }
+  }
+}
+
 // ---------------------------------------------------------------------------
 // staged schedule
 // ---------------------------------------------------------------------------
@@ -797,15 +883,19 @@ __global__ void __launch_bounds__(tile_threads(C)) gla_summary_kernel(GlaParams 
   const int64_t sc = (int64_t)bh * P.nchunks + c;
   ch.template load<false>(P, sm, bh, c);
   ch.template factors<false, true, false>(sm, P.decays + sc * DK);
-  ch.template summary_out<false>(sm, P.states + sc * (DK * DV));
+  if constexpr (T::F16)
+    ch.template summary_out<false, true>(sm, nullptr, P.states16 + sc * (DK * DV));
+  else
+    ch.template summary_out<false>(sm, P.states + sc * (DK * DV));
 }
 
+// 128 threads per work-group, two elements each: 256 elements per work-group.
 template <int DK, int DV, bool H16>
-__global__ void __launch_bounds__(256) gla_scan_kernel(GlaParams P) {
+__global__ void __launch_bounds__(128) gla_scan_kernel(GlaParams P) {
   const int bh = blockIdx.y;
   const int e0 = blockIdx.x * 256;
   const int e1 = min(e0 + 256, DK * DV);
-  scan_plain<DK, DV, H16>(P, bh, e0, e1, threadIdx.x, 256);
+  scan_plain<DK, DV, H16>(P, bh, e0, e1, threadIdx.x, 128);
 }
 
 template <int DK, int DV, int C, int IN>
@@ -936,6 +1026,91 @@ __device__ __forceinline__ void state_inline(const GlaParams& P, Sm& sm, int bh,
   }
 }
 
+// The same from fp16 summaries (16-bit inputs): 16-byte pieces of 8 elements,
+// which share dims i..i+7 when NT is a multiple of DK / 8; float32 sums.
+template <int DK, int DV, int NT, typename Sm, typename E, int SP>
+__device__ __forceinline__ void state_inline16(const GlaParams& P, Sm& sm, int bh, int c, bool state, bool final) {
+  constexpr int SQ8 = DK * DV / 8;
+  constexpr int SPER = (SQ8 + NT - 1) / NT;
+  static_assert(NT % (DK / 8) == 0, "the pieces of one thread must share their dims");
+  const int NC = P.nchunks;
+  const __amdgpu_buffer_rsrc_t sr = make_rsrc(P.states16 + (int64_t)bh * NC * (DK * DV), (uint32_t)NC * DK * DV * 2);
+  const __amdgpu_buffer_rsrc_t dr = make_rsrc(P.decays + (int64_t)bh * NC * DK, (uint32_t)NC * DK * 4);
+  const int i0 = (8 * (int)threadIdx.x) % DK;
+  float acc[SPER][8], wgt[8];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) wgt[e] = 1.f;
+#pragma unroll
+  for (int m = 0; m < SPER; ++m)
+#pragma unroll
+    for (int e = 0; e < 8; ++e) acc[m][e] = 0.f;
+  constexpr int B = SPER >= 16 ? 1 : 16 / SPER;  // chunks per batch of loads
+  for (int j1 = c; j1 > 0; j1 -= B) {
+    u32x4 u[B][SPER];
+    f4 d[B][2];
+#pragma unroll
+    for (int b = 0; b < B; ++b) {
+      const int j = j1 - 1 - b;
+      if (j >= 0) {
+        d[b][0] = coh_load4(dr, ((uint32_t)j * DK + i0) * 4);
+        d[b][1] = coh_load4(dr, ((uint32_t)j * DK + i0 + 4) * 4);
+#pragma unroll
+        for (int m = 0; m < SPER; ++m) {
+          const int q8 = threadIdx.x + m * NT;
+          if (q8 < SQ8)
+            u[b][m] = __builtin_amdgcn_raw_buffer_load_b128(sr, (int)(((uint32_t)j * (DK * DV) + 8 * q8) * 2), 0,
+                                                            kAgentCoherent);
+        }
+      }
+    }
+#pragma unroll
+    for (int b = 0; b < B; ++b) {
+      const int j = j1 - 1 - b;
+      if (j >= 0) {
+#pragma unroll
+        for (int m = 0; m < SPER; ++m) {
+          const h8 hv = __builtin_bit_cast(h8, u[b][m]);
+#pragma unroll
+          for (int e = 0; e < 8; ++e) acc[m][e] += wgt[e] * (float)hv[e];
+        }
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          wgt[e] *= d[b][0][e];
+          wgt[e + 4] *= d[b][1][e];
+        }
+      }
+    }
+  }
+  f4 dc[2] = {{0.f, 0.f, 0.f, 0.f}, {0.f, 0.f, 0.f, 0.f}};
+  if (final) {
+    dc[0] = coh_load4(dr, ((uint32_t)c * DK + i0) * 4);
+    dc[1] = coh_load4(dr, ((uint32_t)c * DK + i0 + 4) * 4);
+  }
+#pragma unroll
+  for (int m = 0; m < SPER; ++m) {
+    const int q8 = threadIdx.x + m * NT;
+    if (q8 < SQ8) {
+      const int dv = (8 * q8) / DK;
+      if (P.s0) {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) acc[m][e] += wgt[e] * P.s0[((int64_t)bh * DK + i0 + e) * DV + dv];
+      }
+      if (state) {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) sm.sT[dv * SP + i0 + e] = (E)acc[m][e];
+      }
+      if (final) {
+        const h8 uc = __builtin_bit_cast(
+            h8, __builtin_amdgcn_raw_buffer_load_b128(sr, (int)(((uint32_t)c * (DK * DV) + 8 * q8) * 2), 0,
+                                                      kAgentCoherent));
+#pragma unroll
+        for (int e = 0; e < 8; ++e)
+          P.s_final[((int64_t)bh * DK + i0 + e) * DV + dv] = dc[e >> 2][e & 3] * acc[m][e] + (float)uc[e];
+      }
+    }
+  }
+}
+
 // Work-group -> (sequence, chunk). Work-groups are handed to the 8 XCDs round
 // robin, so block b runs on XCD b % 8; all chunks of a sequence get the same
 // b % 8 and therefore share one L2. Blocks whose sequence index is past the end
@@ -958,7 +1133,10 @@ __global__ void __launch_bounds__(tile_threads(C)) gla_fused_kernel(GlaParams P)
   Raw rz[T::SITER];
   if (P.gate) ch.prefetch_gate(P, bh, c, rz);
   ch.template factors<true, true, true>(sm, P.decays + sc * DK);
-  ch.template summary_out<true>(sm, P.states + sc * (DK * DV));
+  if constexpr (T::F16)
+    ch.template summary_out<true, true>(sm, nullptr, P.states16 + sc * (DK * DV));
+  else
+    ch.template summary_out<true>(sm, P.states + sc * (DK * DV));
   seq_arrive(&sync[0]);
 
   f4 O[DV / 16];
@@ -968,14 +1146,22 @@ __global__ void __launch_bounds__(tile_threads(C)) gla_fused_kernel(GlaParams P)
   if constexpr (INLINE) {
     const bool state = c > 0 || P.s0;
     const bool final = P.s_final && c == NC - 1;
-    if (state || final)
-      state_inline<DK, DV, T::NT, typename T::Smem, typename T::E, T::SP>(P, sm, bh, c, state, final);
+    if (state || final) {
+      if constexpr (T::F16)
+        state_inline16<DK, DV, T::NT, typename T::Smem, typename T::E, T::SP>(P, sm, bh, c, state, final);
+      else
+        state_inline<DK, DV, T::NT, typename T::Smem, typename T::E, T::SP>(P, sm, bh, c, state, final);
+    }
     if (state) {
       __syncthreads();
       ch.readout(sm, O);
     }
   } else {
-    {
+    if constexpr (T::F16) {
+      const int per = 2 * ((DK * DV / 2 + NC - 1) / NC);  // element pairs
+      const int e0 = min(c * per, DK * DV), e1 = min(e0 + per, DK * DV);
+      scan_coherent16<DK, DV>(P, bh, e0, e1, threadIdx.x, T::NT);
+    } else {
       const int per = (DK * DV + NC - 1) / NC;
       const int e0 = min(c * per, DK * DV), e1 = min(e0 + per, DK * DV);
       scan_coherent<DK, DV>(P, bh, e0, e1, threadIdx.x, T::NT);
@@ -984,9 +1170,15 @@ __global__ void __launch_bounds__(tile_threads(C)) gla_fused_kernel(GlaParams P)
     seq_wait(&sync[1], (unsigned)NC, P.fault);
 
     if (c > 0 || P.s0) {
-      f4 sbuf[T::SPER];
-      ch.template state_load<true>(P.states + sc * (DK * DV), sbuf);
-      ch.state_store(sm, sbuf);
+      if constexpr (T::F16) {
+        u32x4 hbuf[T::SPER8];
+        ch.template state_load16<true>(P.states16 + sc * (DK * DV), hbuf);
+        ch.state_store16(sm, hbuf);
+      } else {
+        f4 sbuf[T::SPER];
+        ch.template state_load<true>(P.states + sc * (DK * DV), sbuf);
+        ch.state_store(sm, sbuf);
+      }
       __syncthreads();
       ch.readout(sm, O);
     }
@@ -1056,12 +1248,13 @@ static bool select_kernels(const GlaShape& s, KernelSet* ks) {
   }
 }
 
-// AUTO takes the inline schedule while the summaries of one sequence hold at
-// most this many elements (nchunks * dk * dv): rebuilding a boundary state reads
-// every summary before it, so the cost grows with their total size
-// (measured: d_k = d_v = 64 at 25 chunks is faster fused, d_k = 32, d_v = 64
-// at 25 chunks faster inline).
-constexpr int64_t kInlineMaxSummaryElems = 65536;
+// AUTO takes the inline schedule while the summaries of one sequence take at
+// most this many bytes (nchunks * dk * dv elements, float32 for float32 inputs,
+// fp16 otherwise): rebuilding a boundary state reads every summary before it,
+// so the cost grows with their total size (measured with float32 summaries:
+// d_k = d_v = 64 at 25 chunks, 400 KB, faster fused; d_k = 32, d_v = 64 at 25
+// chunks, 200 KB, faster inline).
+constexpr int64_t kInlineMaxSummaryBytes = 262144;
 
 // Largest number of work-groups of one sequence that can be resident on one XCD
 // at once (8 XCDs per device); cached per (device, kernel).
@@ -1095,6 +1288,29 @@ static int fused_capacity_per_xcd(const void* kernel, int threads) {
 // 2^31.
 constexpr int64_t kFusedMaxChunks = 4096;
 
+// Length-aware dispatch: short sequences rebuild each boundary state from the
+// summaries (one hand-off), longer ones split the scan over their chunks'
+// work-groups (two hand-offs). Both need every chunk of a sequence resident at
+// once on one XCD, and both lose to the three-launch schedule as soon as an XCD
+// has to run more than one sequence (more than 8 sequences): then the sequences
+// compete for the XCD's slots and partly resident ones spin while they wait for
+// the rest, so AUTO takes the staged schedule there. An explicit one-launch
+// path that does not fit is GTR_ERR_UNSUPPORTED.
+static gtr_status choose_schedule(const GlaShape& s, int path, const KernelSet& ks, int* sched) {
+  *sched = GTR_PATH_STAGED;
+  const bool auto_one_launch = path == GTR_PATH_AUTO && s.BH <= 8;
+  if (path == GTR_PATH_FUSED || path == GTR_PATH_INLINE || auto_one_launch) {
+    const bool inl = path == GTR_PATH_INLINE ||
+                     (path == GTR_PATH_AUTO &&
+                      s.nchunks * s.dk * s.dv * (s.qdt == GTR_F32 ? 4 : 2) <= kInlineMaxSummaryBytes);
+    const int cap = fused_capacity_per_xcd(inl ? ks.inlined : ks.fused, ks.threads);
+    const bool fits = cap > 0 && s.nchunks <= cap && s.nchunks <= kFusedMaxChunks && s.BH <= kSyncSeqs;
+    if (path != GTR_PATH_AUTO && !fits) return GTR_ERR_UNSUPPORTED;
+    if (fits) *sched = inl ? GTR_PATH_INLINE : GTR_PATH_FUSED;
+  }
+  return GTR_OK;
+}
+
 }  // namespace gtr
 
 using namespace gtr;
@@ -1120,6 +1336,15 @@ extern "C" int gtr_gla_workspace_fault(const void* workspace, size_t bytes) {
   unsigned v = 0;
   if (hipMemcpy(&v, workspace, sizeof(v), hipMemcpyDeviceToHost) != hipSuccess) return -1;
   return v != 0;
+}
+
+extern "C" int gtr_gla_schedule(const gtr_gla_args* a) {
+  GlaShape s;
+  KernelSet ks;
+  int sched = -1;
+  if (!a || gla_shape_from_args(a, &s, /*check_pointers=*/false) != GTR_OK || !select_kernels(s, &ks)) return -1;
+  if (choose_schedule(s, a->path, ks, &sched) != GTR_OK) return -1;
+  return sched;
 }
 
 extern "C" gtr_status gtr_gla_fwd(const gtr_gla_args* a, hipStream_t stream) {
@@ -1163,24 +1388,10 @@ extern "C" gtr_status gtr_gla_fwd(const gtr_gla_args* a, hipStream_t stream) {
   P.gatedt = a->out_gate_dtype;
   P.eps = a->norm_eps;
 
-  // Length-aware dispatch: short sequences rebuild each boundary state from the
-  // summaries (one hand-off), longer ones split the scan over their chunks'
-  // work-groups (two hand-offs). Both need every chunk of a sequence resident
-  // at once on one XCD, and both lose to the three-launch schedule as soon as
-  // an XCD has to run more than one sequence (more than 8 sequences): then the
-  // sequences compete for the XCD's slots and partly resident ones spin while
-  // they wait for the rest, so AUTO takes the staged schedule there.
-  const void* one_launch = nullptr;
-  const bool auto_one_launch = a->path == GTR_PATH_AUTO && P.groups == 1;
-  if (a->path == GTR_PATH_FUSED || a->path == GTR_PATH_INLINE || auto_one_launch) {
-    const bool inl = a->path == GTR_PATH_INLINE ||
-                     (a->path == GTR_PATH_AUTO && s.nchunks * s.dk * s.dv <= kInlineMaxSummaryElems);
-    const void* k = inl ? ks.inlined : ks.fused;
-    const int cap = fused_capacity_per_xcd(k, ks.threads);
-    const bool fits = cap > 0 && s.nchunks <= cap && s.nchunks <= kFusedMaxChunks && s.BH <= kSyncSeqs;
-    if (a->path != GTR_PATH_AUTO && !fits) return GTR_ERR_UNSUPPORTED;
-    if (fits) one_launch = k;
-  }
+  int sched = GTR_PATH_STAGED;
+  const gtr_status cs = choose_schedule(s, a->path, ks, &sched);
+  if (cs != GTR_OK) return cs;
+  const void* one_launch = sched == GTR_PATH_INLINE ? ks.inlined : sched == GTR_PATH_FUSED ? ks.fused : nullptr;
 
   void* kargs[] = {&P};
   hipError_t err;
@@ -1191,7 +1402,7 @@ extern "C" gtr_status gtr_gla_fwd(const gtr_gla_args* a, hipStream_t stream) {
     err = hipLaunchKernel(ks.summary, dim3((unsigned)s.nchunks, (unsigned)s.BH), dim3(ks.threads), kargs, 0, stream);
     if (err == hipSuccess) {
       const unsigned eb = (unsigned)((s.dk * s.dv + 255) / 256);
-      err = hipLaunchKernel(ks.scan, dim3(eb, (unsigned)s.BH), dim3(256), kargs, 0, stream);
+      err = hipLaunchKernel(ks.scan, dim3(eb, (unsigned)s.BH), dim3(128), kargs, 0, stream);
     }
     if (err == hipSuccess)
       err = hipLaunchKernel(ks.output, dim3((unsigned)s.nchunks, (unsigned)s.BH), dim3(ks.threads), kargs, 0, stream);

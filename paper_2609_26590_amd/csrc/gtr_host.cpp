@@ -114,8 +114,10 @@ WorkspaceLayout gla_workspace_layout(const GlaShape& s) {
   off += 256;
   w.sync_off = off;
   off = align256(off + (size_t)kSyncSeqs * 4 * sizeof(uint32_t));
+  // chunk summaries and boundary states travel in float32 for float32 inputs,
+  // in fp16 (states16) for 16-bit inputs; the other region has size 0
   w.states_off = off;
-  off = align256(off + (size_t)s.BH * s.nchunks * s.dk * s.dv * sizeof(float));
+  if (s.qdt == GTR_F32) off = align256(off + (size_t)s.BH * s.nchunks * s.dk * s.dv * sizeof(float));
   w.decays_off = off;
   off = align256(off + (size_t)s.BH * s.nchunks * s.dk * sizeof(float));
   w.states16_off = 0;

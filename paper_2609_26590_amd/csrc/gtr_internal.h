@@ -26,7 +26,7 @@ constexpr int64_t kSyncSeqs = 1024;
 struct WorkspaceLayout {
   size_t fault_off;   // one 32-bit word (fused-path wait ran out)
   size_t sync_off;    // [kSyncSeqs][4] 32-bit counters
-  size_t states_off;  // [BH][nchunks][dv][dk] float32
+  size_t states_off;  // [BH][nchunks][dv][dk] float32 (float32 inputs only, else size 0)
   size_t decays_off;  // [BH][nchunks][dk] float32
   size_t states16_off;  // [BH][nchunks][dv][dk] fp16 (16-bit inputs only, else 0)
   size_t total;

@@ -79,11 +79,30 @@ def fwd(lib, a):
 def test_workspace_size_formula(lib):
     a = base_args(B=2, heads=3, H=40, W=40, dk=64, dv=64, chunk=64)
     BH, nc = 6, 25
-    # header, counters of 1024 sequences, float32 states, decays, fp16 states (16-bit inputs)
-    want = 256 + 1024 * 16 + BH * nc * 64 * 64 * 4 + ((BH * nc * 64 * 4 + 255) // 256) * 256 + BH * nc * 64 * 64 * 2
-    assert lib.gtr_gla_workspace_size(ctypes.byref(a)) == want
+    # header, counters of 1024 sequences, decays, then the summaries / states:
+    # fp16 for 16-bit inputs, float32 (ahead of the decays) for float32 inputs
+    dec = ((BH * nc * 64 * 4 + 255) // 256) * 256
+    want = 256 + 1024 * 16 + dec + BH * nc * 64 * 64 * 2
+    assert a.qkv_dtype != gtr.F32 and lib.gtr_gla_workspace_size(ctypes.byref(a)) == want
+    a.qkv_dtype = a.g_dtype = a.o_dtype = gtr.F32
+    assert lib.gtr_gla_workspace_size(ctypes.byref(a)) == 256 + 1024 * 16 + BH * nc * 64 * 64 * 4 + dec
     a.dk = 48
     assert lib.gtr_gla_workspace_size(ctypes.byref(a)) == 0
+
+
+def test_schedule_query_without_device(lib):
+    """gtr_gla_schedule: -1 for invalid arguments; without a usable device the
+    one-launch schedules cannot be sized, so AUTO reports STAGED and an explicit
+    one-launch path reports -1 (gtr_gla_fwd would return GTR_ERR_UNSUPPORTED)."""
+    assert lib.gtr_gla_schedule(None) == -1
+    a = base_args(B=1, heads=6, H=40, W=40)
+    assert lib.gtr_gla_schedule(ctypes.byref(a)) == 2
+    a.path = 2
+    assert lib.gtr_gla_schedule(ctypes.byref(a)) == 2
+    a.path = 1
+    assert lib.gtr_gla_schedule(ctypes.byref(a)) == -1
+    a.path, a.dk = 0, 48
+    assert lib.gtr_gla_schedule(ctypes.byref(a)) == -1
 
 
 def test_null_struct(lib):

@@ -134,6 +134,9 @@ class Shape:
         self.NC = (self.L + chunk - 1) // chunk
 
 
+UNMAPPED = 0x7000_0000_0000  # an address inside no registered buffer: any access is reported
+
+
 def kernel_args(c: Shape):
     """GlaParams for shape c with every buffer at its own base, and the buffers."""
     regions = []
@@ -156,10 +159,11 @@ def kernel_args(c: Shape):
     sf = alloc("s_final", c.BH * c.dk * c.dv * 4, "w") if c.sfinal else 0
     z = alloc("out_gate", c.BH * c.L * c.dv * DT[c.zdt][1], "r") if c.zdt else 0
     nw = alloc("norm_weight", c.dv * 4, "r") if c.zdt and c.weighted else 0
-    # workspace layout of gla_workspace_layout(): fault word, counters, states, decays
+    # workspace layout of gla_workspace_layout(): fault word, counters, float32
+    # states (float32 inputs), decays, fp16 states (16-bit inputs)
     sync = 256
     states = a256(sync + 1024 * 16)  # counters of up to 1024 sequences, a fixed region
-    decays = a256(states + c.BH * c.NC * c.dk * c.dv * 4)
+    decays = a256(states + (c.BH * c.NC * c.dk * c.dv * 4 if c.dt == "f32" else 0))
     states16 = a256(decays + c.BH * c.NC * c.dk * 4)
     total = a256(states16 + (c.BH * c.NC * c.dk * c.dv * 2 if c.dt != "f32" else 0))
     ws = alloc("workspace", total, "rw")
@@ -168,7 +172,8 @@ def kernel_args(c: Shape):
     regions.insert(0, emu.Region("fault", ws, 256, "rw"))
     regions.append(emu.Region("kernarg", emu.KERNARG_BASE, KERNARG_BYTES, "r"))
     kern = struct.pack("<7Q6iqifi4xQQQQiif4xQQifQ", q, k, v, g, o, s0, sf, DT[c.dt][0], DT[c.gdt][0],
-                       DT[c.odt][0], c.BH, c.H, c.W, c.L, c.NC, c.dk ** -0.5, SCAN[c.scan], ws + states,
+                       DT[c.odt][0], c.BH, c.H, c.W, c.L, c.NC, c.dk ** -0.5, SCAN[c.scan],
+                       ws + states if c.dt == "f32" else UNMAPPED,  # 16-bit inputs never touch float32 states
                        ws + decays, ws + sync, ws, (c.BH + 7) // 8, 1 if c.logits else 0, 1.0 / 16,
                        z, nw, DT[c.zdt][0] if c.zdt else 0, 1e-5, ws + states16 if c.dt != "f32" else 0)
     assert len(kern) == KERNARG_BYTES
@@ -196,7 +201,7 @@ def work_groups(kind: str, c: Shape):
         return [((cc, bh, 0), nw) for cc in cs for bh in bhs]
     if kind == "scan":
         eb = (c.dk * c.dv + 255) // 256
-        return [((x, bh, 0), 4) for x in sorted({0, eb - 1}) for bh in bhs]
+        return [((x, bh, 0), 2) for x in sorted({0, eb - 1}) for bh in bhs]  # 128 threads
     picks = {((bh // 8 * c.NC + cc) << 3) | (bh % 8) for bh in bhs for cc in cs}
     last = (c.BH + 7) // 8 - 1
     spare = [x for x in range(8) if last * 8 + x >= c.BH]

@@ -227,6 +227,22 @@ def test_workspace_reuse_and_no_fault(gtr):
     assert int(ws.buf[256:256 + 16 * n_seq].view(torch.int32).abs().sum()) == 0
 
 
+@pytest.mark.parametrize("name,want", [("kbench", "inline"), ("tiny", "inline"), ("op1600", "inline"),
+                                       ("directions", "staged"), ("batched", "staged"), ("highres", "staged"),
+                                       ("op16k", "staged")])
+def test_auto_schedule(gtr, name, want):
+    """AUTO's choice (the length-aware dispatch) as gtr_gla_schedule reports it."""
+    wl = WORKLOADS[name]
+    dev = torch.device("cuda")
+    mk = lambda d: torch.empty((wl.B, wl.heads, wl.L, d), dtype=torch_dtype(wl.dtype), device=dev)
+    s0 = torch.empty((wl.B, wl.heads, wl.dk, wl.dv), device=dev) if wl.s0_std is not None else None
+    got = gtr.gtr_gla_schedule(mk(wl.dk), mk(wl.dk), mk(wl.dv), mk(wl.dk), H=wl.H, W=wl.W, chunk=wl.chunk, s0=s0,
+                               want_final=wl.want_final, o_dtype=torch_dtype(wl.odtype))
+    assert got == want
+    assert gtr.gtr_gla_schedule(mk(wl.dk), mk(wl.dk), mk(wl.dv), mk(wl.dk), H=wl.H, W=wl.W, chunk=wl.chunk,
+                                path="staged") == "staged"
+
+
 def test_paths_agree(gtr):
     wl = WORKLOADS["directions"]
     for scan in wl.scans:
