@@ -337,8 +337,8 @@ struct Chunk {
         *reinterpret_cast<f4*>(&sm.buf[r * KP + 32 * s + 8 * gq + 4]) = f4{ke[s][4], ke[s][5], ke[s][6], ke[s][7]};
       }
     }
-    spanmax = __builtin_bit_cast(float, __builtin_amdgcn_readfirstlane(__builtin_bit_cast(int, wave_max(smax))));
-    absmax = __builtin_bit_cast(float, __builtin_amdgcn_readfirstlane(__builtin_bit_cast(int, wave_max(amax))));
+    spanmax = __builtin_bit_cast(float, __builtin_amdgcn_readfirstlane(__builtin_bit_cast(int, wave_max_uniform(smax))));
+    absmax = __builtin_bit_cast(float, __builtin_amdgcn_readfirstlane(__builtin_bit_cast(int, wave_max_uniform(amax))));
     __syncthreads();
   }
 

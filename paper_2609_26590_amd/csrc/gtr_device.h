@@ -195,10 +195,26 @@ __device__ __forceinline__ float row_bcast(float x) {
                                                                false));
 }
 
-__device__ __forceinline__ float wave_max(float x) {
-#pragma unroll
-  for (int m = 32; m >= 1; m >>= 1) x = fmaxf(x, __shfl_xor(x, m, kWave));
-  return x;
+// Maximum over the 64 lanes, as a wave-uniform value: a running maximum along
+// each 16-lane row with DPP row shifts (a lane whose source is outside its row
+// keeps its own value), then the four row maxima (lanes 15, 31, 47, 63) read
+// into scalar registers. No LDS round trips.
+template <int SHIFT>
+__device__ __forceinline__ float row_shr_keep(float x) {
+  const int b = __builtin_bit_cast(int, x);
+  return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(b, b, 0x110 + SHIFT, 0xf, 0xf, false));
+}
+__device__ __forceinline__ float wave_max_uniform(float x) {
+  x = fmaxf(x, row_shr_keep<1>(x));
+  x = fmaxf(x, row_shr_keep<2>(x));
+  x = fmaxf(x, row_shr_keep<4>(x));
+  x = fmaxf(x, row_shr_keep<8>(x));
+  const int b = __builtin_bit_cast(int, x);
+  const float r0 = __builtin_bit_cast(float, __builtin_amdgcn_readlane(b, 15));
+  const float r1 = __builtin_bit_cast(float, __builtin_amdgcn_readlane(b, 31));
+  const float r2 = __builtin_bit_cast(float, __builtin_amdgcn_readlane(b, 47));
+  const float r3 = __builtin_bit_cast(float, __builtin_amdgcn_readlane(b, 63));
+  return fmaxf(fmaxf(r0, r1), fmaxf(r2, r3));
 }
 
 }  // namespace gtr
