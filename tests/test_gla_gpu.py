@@ -79,7 +79,7 @@ for name, wl in WORKLOADS.items():
             CASES.append((name, scan, chunk))
 
 
-@pytest.mark.parametrize("path", PATHS)
+@pytest.mark.parametrize("path", PATHS + ("auto",))  # auto: the configuration bench.py times
 @pytest.mark.parametrize("name,scan,chunk", CASES)
 def test_workload_parity(gtr, name, scan, chunk, path):
     wl = WORKLOADS[name]
