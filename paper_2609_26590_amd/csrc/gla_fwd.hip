@@ -134,6 +134,15 @@ __device__ __forceinline__ void ld_raw(const void* base, int dt, int64_t off, Ra
   }
 }
 
+// The same through a buffer descriptor over one sequence's rows: a byte offset
+// at or beyond the descriptor's range (kOutOfRange) reads zeros, which is what
+// the positions past the end of a sequence must hold.
+constexpr uint32_t kOutOfRange = 0x7fffff00u;  // the host keeps every sequence's rows below this many bytes
+__device__ __forceinline__ void ld_raw_buf(__amdgpu_buffer_rsrc_t rs, int dt, uint32_t byte_off, Raw& r) {
+  r.a = __builtin_amdgcn_raw_buffer_load_b128(rs, (int)byte_off, 0, 0);
+  if (dt == GTR_F32) r.b = __builtin_amdgcn_raw_buffer_load_b128(rs, (int)(byte_off + 16u), 0, 0);
+}
+
 __device__ __forceinline__ void cvt_raw(const Raw& r, int dt, float (&x)[8]) {
   if (dt == GTR_F32) {
 #pragma unroll
@@ -273,27 +282,31 @@ struct Chunk {
     lanes();
     bool valid;
     const int64_t t = token(P, (int64_t)c * C + r, valid);
-    const int64_t kb = ((int64_t)bh * P.L + t) * DK;
-    const int64_t vb = ((int64_t)bh * P.L + t) * DV;
 
-    // issue every load before converting any of them
+    // issue every load before converting any of them; a position past the end
+    // of the sequence reads zeros through the descriptors' range check
+    constexpr uint32_t ES = F16 ? 2 : 4;
+    const uint32_t gs = P.gdt == GTR_F32 ? 4 : 2;
+    const int64_t L = P.L;
+    const char* qb = static_cast<const char*>(P.q) + (int64_t)bh * L * DK * ES;
+    const char* kb = static_cast<const char*>(P.k) + (int64_t)bh * L * DK * ES;
+    const char* vb = static_cast<const char*>(P.v) + (int64_t)bh * L * DV * ES;
+    const char* gb = static_cast<const char*>(P.g) + (int64_t)bh * L * DK * gs;
+    const __amdgpu_buffer_rsrc_t qr = make_rsrc(qb, (uint32_t)(L * DK * ES));
+    const __amdgpu_buffer_rsrc_t kr = make_rsrc(kb, (uint32_t)(L * DK * ES));
+    const __amdgpu_buffer_rsrc_t vr = make_rsrc(vb, (uint32_t)(L * DV * ES));
+    const __amdgpu_buffer_rsrc_t gr = make_rsrc(gb, (uint32_t)(L * DK * gs));
     Raw rq[KS], rk[KS], rg[KS], rv[VS];
-    if (valid) {
 #pragma unroll
-      for (int s = 0; s < KS; ++s) {
-        ld_raw(P.q, IN, kb + 32 * s + 8 * gq, rq[s]);
-        ld_raw(P.k, IN, kb + 32 * s + 8 * gq, rk[s]);
-        ld_raw(P.g, P.gdt, kb + 32 * s + 8 * gq, rg[s]);
-      }
-#pragma unroll
-      for (int s = 0; s < VS; ++s) ld_raw(P.v, IN, vb + 32 * s + 8 * gq, rv[s]);
-    } else {
-      const u32x4 z = {0u, 0u, 0u, 0u};
-#pragma unroll
-      for (int s = 0; s < KS; ++s) rq[s] = rk[s] = rg[s] = Raw{z, z};
-#pragma unroll
-      for (int s = 0; s < VS; ++s) rv[s] = Raw{z, z};
+    for (int s = 0; s < KS; ++s) {
+      const uint32_t e = (uint32_t)t * DK + 32 * s + 8 * gq;
+      ld_raw_buf(qr, IN, valid ? e * ES : kOutOfRange, rq[s]);
+      ld_raw_buf(kr, IN, valid ? e * ES : kOutOfRange, rk[s]);
+      ld_raw_buf(gr, P.gdt, valid ? e * gs : kOutOfRange, rg[s]);
     }
+#pragma unroll
+    for (int s = 0; s < VS; ++s)
+      ld_raw_buf(vr, IN, valid ? ((uint32_t)t * DV + 32 * s + 8 * gq) * ES : kOutOfRange, rv[s]);
 
     // v^T tile
 #pragma unroll

@@ -188,11 +188,11 @@ __device__ __forceinline__ float row_inclusive_scan(float x) {
   return x;
 }
 
-// Value of lane N (0..15) of this lane's 16-lane row (DPP row_newbcast).
+// Value of lane N (0..15) of this lane's 16-lane row (DPP row_newbcast). Every
+// lane receives a value, so the move needs no initialised destination.
 template <int N>
 __device__ __forceinline__ float row_bcast(float x) {
-  return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, x), 0x150 + N, 0xf, 0xf,
-                                                               false));
+  return __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, x), 0x150 + N, 0xf, 0xf, false));
 }
 
 // Maximum over the 64 lanes, as a wave-uniform value: a running maximum along

@@ -48,6 +48,9 @@ gtr_status gla_shape_from_args(const gtr_gla_args* a, GlaShape* s, bool check_po
   if (!mul_ok(a->B, a->heads, &BH) || !mul_ok(a->H, a->W, &L)) return GTR_ERR_SHAPE;
   const int dmax = a->dk > a->dv ? a->dk : a->dv;
   if (!mul_ok(BH, L, &n) || !mul_ok(n, dmax, &n) || !mul_ok(n, 4, &n)) return GTR_ERR_SHAPE;
+  // the kernels address one sequence's rows through a buffer descriptor with
+  // a 32-bit range (and use 0x7fffff00 as their out-of-range offset)
+  if (L * dmax * 4 >= 0x7fffff00LL) return GTR_ERR_SHAPE;
   const int64_t nchunks = (L + a->chunk - 1) / a->chunk;
   // launch-grid limits: staged grids are (nchunks, BH); the fused grid is 1-D
   int64_t fused_blocks;

@@ -631,6 +631,19 @@ def salu64(fn):
     return h
 
 
+def salu64_shift(fn):
+    """64-bit shifts: the shift amount is a 32-bit operand."""
+    def h(w, i):
+        a = w.s64(i.ops[1], i)
+        b = w.s32(i.ops[2], i)
+        ob = bool(a[1]) or bool(b[1])
+        d = bool(a[2]) and bool(b[2])
+        res, scc = fn(a[0], b[0])
+        w.s64set(i.ops[0], res & M64, M64 if ob else 0, d)
+        set_scc(w, scc, ob, d)
+    return h
+
+
 HANDLERS.update({
     's_add_u32': salu32(lambda a, b: (a + b, (a + b) >> 32)),
     's_addc_u32': salu32(lambda a, b, c: (a + b + c, (a + b + c) >> 32), 'carry_in'),
@@ -652,8 +665,8 @@ HANDLERS.update({
     's_min_u32': salu32(lambda a, b: (min(a, b), a < b)),
     's_max_u32': salu32(lambda a, b: (max(a, b), a > b)),
     's_abs_i32': salu32(lambda a: (abs(sx(a)), abs(sx(a)) != 0)),
-    's_lshl_b64': salu64(lambda a, b: ((a << (b & 63)) & M64, ((a << (b & 63)) & M64) != 0)),
-    's_lshr_b64': salu64(lambda a, b: (a >> (b & 63), (a >> (b & 63)) != 0)),
+    's_lshl_b64': salu64_shift(lambda a, b: ((a << (b & 63)) & M64, ((a << (b & 63)) & M64) != 0)),
+    's_lshr_b64': salu64_shift(lambda a, b: (a >> (b & 63), (a >> (b & 63)) != 0)),
 })
 
 

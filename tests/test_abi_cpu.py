@@ -105,6 +105,16 @@ def test_schedule_query_without_device(lib):
     assert lib.gtr_gla_schedule(ctypes.byref(a)) == -1
 
 
+def test_sequence_rows_beyond_descriptor_range(lib):
+    """One sequence's rows are addressed through a 32-bit buffer descriptor:
+    L * max(dk, dv) * 4 bytes must stay below 0x7fffff00."""
+    a = base_args(B=1, heads=1, H=4096, W=2048, dk=64, dv=64)  # 8.4M tokens: 2.1 GB of float32 rows
+    assert lib.gtr_gla_workspace_size(ctypes.byref(a)) == 0
+    assert lib.gtr_gla_fwd(ctypes.byref(a), None) == SHAPE
+    a.W = 2047
+    assert lib.gtr_gla_workspace_size(ctypes.byref(a)) > 0
+
+
 def test_null_struct(lib):
     assert lib.gtr_gla_fwd(None, None) == NULL
 
