@@ -46,6 +46,10 @@
 //     (vmcnt(0)) before it bumps a counter. No release/acquire fence is used: on
 //     this GPU those write back / invalidate the whole L2 of the XCD, which cost
 //     more than the rest of the kernel.
+// Hand-off precision: with fp16/bf16 inputs the summaries U_c and the boundary
+// states S_[c] travel in fp16 (the readout's MFMA operand type); every scan and
+// rebuild accumulates in float32, and S_final is the float32 accumulator. With
+// float32 inputs everything stays float32.
 #include <hip/hip_runtime.h>
 
 #include <mutex>
@@ -76,7 +80,7 @@ struct GlaParams {
   int nchunks;
   float scale;
   int scan;
-  float* states;    // [BH][nchunks][DV][DK]: U_c^T, then S_[c]^T in place
+  float* states;    // [BH][nchunks][DV][DK] float32 U_c^T, then S_[c]^T (float32 inputs only)
   float* decays;    // [BH][nchunks][DK]
   unsigned* sync;   // [BH][4]: arrive1, arrive2, leave, spare
   unsigned* fault;  // one word
@@ -87,7 +91,7 @@ struct GlaParams {
   const float* nw;   // RMSNorm weight [DV], or null (ones)
   int gatedt;        // dtype of gate
   float eps;         // RMSNorm epsilon
-  unsigned short* states16;  // [BH][nchunks][DV][DK] fp16 S_[c]^T (staged schedule, 16-bit inputs)
+  unsigned short* states16;  // [BH][nchunks][DV][DK] fp16 U_c^T, then S_[c]^T (16-bit inputs only)
 };
 
 constexpr int tile_threads(int chunk) { return chunk / 16 * kWave; }
