@@ -414,12 +414,17 @@ __global__ void __launch_bounds__(256) gated_conv_kernel(GatedConvArgs f) {
   }
 }
 
-// K slices of the output product: enough work-groups to give every SIMD a few
-// waves when M x d alone does not (d is small next to hidden).
+// The output product uses 128 x 64 work-group tiles (d is small next to
+// hidden) and splits K into the fewest slices that give one work-group per CU
+// (256) when M x d alone does not: every slice costs a float32 partial product
+// and its share of the reduction. Measured at GTR-L width, one image (product +
+// reduction, microseconds): 128 x 64 tiles with 1 / 2 / 4 / 8 slices 21.5 /
+// 16.5 / 15.8 / 17.1, 128 x 128 tiles 20.7 / 19.0 / 16.5 / 18.7.
+constexpr int kOutBN = 64;
 static int out_ksplit(int64_t M, int d, int hidden) {
-  const int64_t wgs = ((M + 127) / 128) * (d / (d % 128 == 0 ? 128 : 64));
+  const int64_t wgs = ((M + 127) / 128) * (d / kOutBN);
   int s = 1;
-  while (wgs * s < 1024 && s < 8 && hidden / 32 >= 2 * s * KB) s *= 2;
+  while (wgs * s < 256 && s < 8 && hidden / 32 >= 2 * s * KB) s *= 2;
   return s;
 }
 
@@ -512,16 +517,11 @@ extern "C" gtr_status gtr_spatial_swiglu(const gtr_swiglu_args* a, hipStream_t s
   const int ks = out_ksplit(M, a->d, a->hidden);
   float* part = reinterpret_cast<float*>(ws + lay.part_off);
   GemmArgs g3{Hb, a->w_out, a->y, part, (int)M, a->d, a->hidden, a->y_dtype, ks};
-  const bool d128 = a->d % 128 == 0;
-  const dim3 grid3((unsigned)((M + 127) / 128), (unsigned)(a->d / (d128 ? 128 : 64)), (unsigned)ks);
-  if (bf && d128)
-    hipLaunchKernelGGL((gemm_nt_kernel<GTR_F16, GTR_BF16, GTR_F16, 128, 128>), grid3, dim3(256), 0, stream, g3);
-  else if (bf)
-    hipLaunchKernelGGL((gemm_nt_kernel<GTR_F16, GTR_BF16, GTR_F16, 128, 64>), grid3, dim3(256), 0, stream, g3);
-  else if (d128)
-    hipLaunchKernelGGL((gemm_nt_kernel<GTR_F16, GTR_F16, GTR_F16, 128, 128>), grid3, dim3(256), 0, stream, g3);
+  const dim3 grid3((unsigned)((M + 127) / 128), (unsigned)(a->d / kOutBN), (unsigned)ks);
+  if (bf)
+    hipLaunchKernelGGL((gemm_nt_kernel<GTR_F16, GTR_BF16, GTR_F16, 128, kOutBN>), grid3, dim3(256), 0, stream, g3);
   else
-    hipLaunchKernelGGL((gemm_nt_kernel<GTR_F16, GTR_F16, GTR_F16, 128, 64>), grid3, dim3(256), 0, stream, g3);
+    hipLaunchKernelGGL((gemm_nt_kernel<GTR_F16, GTR_F16, GTR_F16, 128, kOutBN>), grid3, dim3(256), 0, stream, g3);
   if (hipGetLastError() != hipSuccess) return GTR_ERR_HIP;
   if (ks > 1) {
     const int64_t n4 = M * a->d / 4;

@@ -300,10 +300,16 @@ def test_swiglu_workspace_size(lib):
     a = swiglu_args(B=2, H=40, W=40, d=384, hidden=1536)
     M = 2 * 1600
     a256 = lambda x: (x + 255) // 256 * 256
-    # G and V (float32), H (fp16), then 8 float32 partial products of the output
-    # product split over K (75 work-groups of 128 x 128 alone would leave SIMDs idle)
-    base = a256(M * 1536 * 2)  # H in fp16 (G and V stay on chip)
-    assert lib.gtr_spatial_swiglu_workspace_size(ctypes.byref(a)) == a256(base + 8 * M * 384 * 4)
+    # H in fp16 (G and V stay on chip), then 2 float32 partial products of the
+    # output product split over K: 25 x 6 work-groups of 128 x 64 alone would
+    # leave CUs idle, two slices give 300 >= 256.
+    base = a256(M * 1536 * 2)
+    assert lib.gtr_spatial_swiglu_workspace_size(ctypes.byref(a)) == a256(base + 2 * M * 384 * 4)
+    one = swiglu_args(B=1, H=40, W=40, d=384, hidden=1536)  # 13 x 6 work-groups: 4 slices
+    assert lib.gtr_spatial_swiglu_workspace_size(ctypes.byref(one)) == \
+        a256(a256(1600 * 1536 * 2) + 4 * 1600 * 384 * 4)
+    big = swiglu_args(B=8, H=40, W=40, d=384, hidden=1536)  # 100 x 6 work-groups: no split
+    assert lib.gtr_spatial_swiglu_workspace_size(ctypes.byref(big)) == a256(12800 * 1536 * 2)
 
 
 @pytest.mark.parametrize("field,val,want", [("B", 0, SHAPE), ("H", -1, SHAPE), ("d", 48, UNSUP),

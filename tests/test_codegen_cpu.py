@@ -292,8 +292,8 @@ def check_kernel(text, name, kern, regions, wgs, waves=4):
     assert "INFO-PATHLIMIT" not in rep.counts
 
 
-@pytest.mark.parametrize("adt,bdt,mt,bn,M,N,K,cdt,ks", [(1, 2, 1, 128, 126, 256, 64, 0, 1),
-                                                        (1, 1, 1, 128, 1600, 384, 1536, 1, 4),
+@pytest.mark.parametrize("adt,bdt,mt,bn,M,N,K,cdt,ks", [(1, 2, 1, 64, 126, 256, 64, 0, 1),
+                                                        (1, 1, 1, 64, 1600, 384, 1536, 1, 4),
                                                         (1, 2, 1, 64, 63, 64, 128, 2, 1),
                                                         (1, 1, 1, 64, 200, 192, 192, 1, 2)])
 def test_swiglu_gemm_addresses(adt, bdt, mt, bn, M, N, K, cdt, ks):
