@@ -107,7 +107,9 @@ typedef enum {
   GTR_PATH_STAGED = 2, /* three launches: summaries, boundary-state scan, outputs      */
   GTR_PATH_INLINE = 3  /* one launch: summaries, then every chunk rebuilds its own
                           boundary state from the summaries before it (short
-                          sequences)                                                  */
+                          sequences). With d_v = 64, no output gate and at most
+                          one work-group per CU after doubling, each chunk's value
+                          columns are split over two work-groups.                     */
 } gtr_path;
 
 /*
@@ -212,7 +214,17 @@ gtr_status gtr_gla_fwd(const gtr_gla_args* args, hipStream_t stream);
 int gtr_gla_schedule(const gtr_gla_args* args);
 
 /*
- * Spatial SwiGLU (Sec. 3.1, "Spatial SwiGLU"; the scope table's row f4):
+ * gtr_gla_value_parts - how many work-groups share each chunk's d_v value
+ * columns in the schedule gtr_gla_schedule reports: 2 where the inline
+ * schedule splits them (d_v = 64, no output gate, and at most one work-group
+ * per CU after doubling), else 1; -1 where gtr_gla_schedule gives -1.
+ * Host-only, like gtr_gla_schedule. The split changes which work-group
+ * computes what, not the arithmetic of any output element.
+ */
+int gtr_gla_value_parts(const gtr_gla_args* args);
+
+/*
+ * Spatial SwiGLU (Sec. 3.1, "Spatial SwiGLU"):
  *   Y = [SiLU(X W_g) * DWConv3x3(X W_v)] W_o
  * for every image b: X = x[b] is [H*W, d] in SPATIAL (row-major grid) order, the
  * value branch X W_v is convolved depthwise over the H x W grid (3 x 3,

@@ -39,7 +39,7 @@ _DT = {torch.float32: F32, torch.float16: F16, torch.bfloat16: BF16}
 _DT_BACK = {F32: torch.float32, F16: torch.float16, BF16: torch.bfloat16}
 
 EXPORTS = ("gtr_scan_permute", "gtr_gla_workspace_size", "gtr_gla_workspace_init", "gtr_gla_fwd",
-           "gtr_gla_schedule", "gtr_gla_workspace_fault", "gtr_status_string", "gtr_spatial_swiglu_workspace_size",
+           "gtr_gla_schedule", "gtr_gla_value_parts", "gtr_gla_workspace_fault", "gtr_status_string", "gtr_spatial_swiglu_workspace_size",
            "gtr_spatial_swiglu")
 
 
@@ -101,6 +101,8 @@ def load(path: Optional[str] = None) -> ctypes.CDLL:
     lib.gtr_gla_fwd.restype = ctypes.c_int
     lib.gtr_gla_schedule.argtypes = [ctypes.POINTER(GlaArgs)]
     lib.gtr_gla_schedule.restype = ctypes.c_int
+    lib.gtr_gla_value_parts.argtypes = [ctypes.POINTER(GlaArgs)]
+    lib.gtr_gla_value_parts.restype = ctypes.c_int
     lib.gtr_gla_workspace_fault.argtypes = [P, ctypes.c_size_t]
     lib.gtr_gla_workspace_fault.restype = ctypes.c_int
     lib.gtr_status_string.argtypes = [ctypes.c_int]
@@ -257,18 +259,32 @@ def gtr_gla_fwd(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, g: torch.Tens
 SCHEDULES = {1: "fused", 2: "staged", 3: "inline"}
 
 
+def _schedule_args(q, k, v, g, H, W, chunk, scan, s0, want_final, o_dtype, path):
+    o = torch.empty((0,), dtype=o_dtype or q.dtype, device=q.device)
+    sf = torch.empty((0,), dtype=torch.float32, device=q.device) if want_final else None
+    return make_args(q, k, v, g, H=H, W=W, scale=1.0, chunk=chunk, scan=scan, s0=s0, o=o, s_final=sf, path=path)
+
+
 def gtr_gla_schedule(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, g: torch.Tensor, *, H: int, W: int,
                      chunk: int = 64, scan: str = "row", s0: Optional[torch.Tensor] = None,
                      want_final: bool = False, o_dtype: Optional[torch.dtype] = None, path: str = "auto") -> str:
     """The schedule gtr_gla_fwd runs for these arguments: "fused", "staged" or "inline"."""
-    B, heads, L, _ = q.shape
-    o = torch.empty((0,), dtype=o_dtype or q.dtype, device=q.device)
-    sf = torch.empty((0,), dtype=torch.float32, device=q.device) if want_final else None
-    args = make_args(q, k, v, g, H=H, W=W, scale=1.0, chunk=chunk, scan=scan, s0=s0, o=o, s_final=sf, path=path)
+    args = _schedule_args(q, k, v, g, H, W, chunk, scan, s0, want_final, o_dtype, path)
     r = int(load().gtr_gla_schedule(ctypes.byref(args)))
     if r not in SCHEDULES:
         raise GtrError("gtr_gla_schedule", 3)
     return SCHEDULES[r]
+
+
+def gtr_gla_value_parts(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, g: torch.Tensor, *, H: int, W: int,
+                        chunk: int = 64, scan: str = "row", s0: Optional[torch.Tensor] = None,
+                        want_final: bool = False, o_dtype: Optional[torch.dtype] = None, path: str = "auto") -> int:
+    """Work-groups per chunk's value columns in that schedule: 2 under the inline value split, else 1."""
+    args = _schedule_args(q, k, v, g, H, W, chunk, scan, s0, want_final, o_dtype, path)
+    r = int(load().gtr_gla_value_parts(ctypes.byref(args)))
+    if r not in (1, 2):
+        raise GtrError("gtr_gla_value_parts", 3)
+    return r
 
 
 def gtr_spatial_swiglu(x: torch.Tensor, w_gate: torch.Tensor, w_value: torch.Tensor, w_out: torch.Tensor,

@@ -92,6 +92,8 @@ struct GlaParams {
   int gatedt;        // dtype of gate
   float eps;         // RMSNorm epsilon
   unsigned short* states16;  // [BH][nchunks][DV][DK] fp16 U_c^T, then S_[c]^T (16-bit inputs only)
+  int dvp;     // row pitch (elements) of v, o, the gate, S0 and S_final: the full d_v
+  int vparts;  // value split of the inline schedule: work-groups per chunk, each d_v / vparts columns
 };
 
 constexpr int tile_threads(int chunk) { return chunk / 16 * kWave; }
@@ -294,11 +296,11 @@ struct Chunk {
     const int64_t L = P.L;
     const char* qb = static_cast<const char*>(P.q) + (int64_t)bh * L * DK * ES;
     const char* kb = static_cast<const char*>(P.k) + (int64_t)bh * L * DK * ES;
-    const char* vb = static_cast<const char*>(P.v) + (int64_t)bh * L * DV * ES;
+    const char* vb = static_cast<const char*>(P.v) + (int64_t)bh * L * P.dvp * ES;
     const char* gb = static_cast<const char*>(P.g) + (int64_t)bh * L * DK * gs;
     const __amdgpu_buffer_rsrc_t qr = make_rsrc(qb, (uint32_t)(L * DK * ES));
     const __amdgpu_buffer_rsrc_t kr = make_rsrc(kb, (uint32_t)(L * DK * ES));
-    const __amdgpu_buffer_rsrc_t vr = make_rsrc(vb, (uint32_t)(L * DV * ES));
+    const __amdgpu_buffer_rsrc_t vr = make_rsrc(vb, (uint32_t)(L * P.dvp * ES));
     const __amdgpu_buffer_rsrc_t gr = make_rsrc(gb, (uint32_t)(L * DK * gs));
     Raw rq[KS], rk[KS], rg[KS], rv[VS];
 #pragma unroll
@@ -310,7 +312,7 @@ struct Chunk {
     }
 #pragma unroll
     for (int s = 0; s < VS; ++s)
-      ld_raw_buf(vr, IN, valid ? ((uint32_t)t * DV + 32 * s + 8 * gq) * ES : kOutOfRange, rv[s]);
+      ld_raw_buf(vr, IN, valid ? ((uint32_t)t * P.dvp + 32 * s + 8 * gq) * ES : kOutOfRange, rv[s]);
 
     // v^T tile
 #pragma unroll
@@ -688,7 +690,7 @@ struct Chunk {
       const int rr = idx / PIECES, pc = idx % PIECES;
       bool valid;
       const int64_t t = token(P, (int64_t)c * C + rr, valid);
-      ld_raw(P.gate, P.gatedt, ((int64_t)bh * P.L + t) * DV + 8 * pc, rz[it]);
+      ld_raw(P.gate, P.gatedt, ((int64_t)bh * P.L + t) * P.dvp + 8 * pc, rz[it]);
     }
   }
 
@@ -710,7 +712,7 @@ struct Chunk {
       const int rr = idx / PIECES, pc = idx % PIECES;
       bool valid;
       const int64_t t = token(P, (int64_t)c * C + rr, valid);
-      const int64_t off = ((int64_t)bh * P.L + t) * DV + 8 * pc;  // token 0 past the end: in bounds
+      const int64_t off = ((int64_t)bh * P.L + t) * P.dvp + 8 * pc;  // token 0 past the end: in bounds
       float x[8];
 #pragma unroll
       for (int e = 0; e < 8; ++e) x[e] = sm.buf[rr * OP + 8 * pc + e];
@@ -983,13 +985,17 @@ __device__ __forceinline__ void seq_wait(unsigned* ctr, unsigned target, unsigne
 // S_final = Diag(d_c) S_[c] + U_c for the last chunk. Thread t owns the
 // 16-byte pieces t, t + NT, ...; with NT a multiple of DK / 4 they all share
 // dims i..i+3, so one decay load per chunk serves all of them. No barrier.
+// `seq` indexes the summaries (a head's value part under the value split),
+// `bh` the decays, S0 and S_final (the head; P's S0 and S_final pointers
+// already start at the part's first column).
 template <int DK, int DV, int NT, typename Sm, typename E, int SP>
-__device__ __forceinline__ void state_inline(const GlaParams& P, Sm& sm, int bh, int c, bool state, bool final) {
+__device__ __forceinline__ void state_inline(const GlaParams& P, Sm& sm, int seq, int bh, int c, bool state,
+                                             bool final) {
   constexpr int SQ4 = DK * DV / 4;
   constexpr int SPER = (SQ4 + NT - 1) / NT;
   static_assert(NT % (DK / 4) == 0, "the pieces of one thread must share their dims");
   const int NC = P.nchunks;
-  const __amdgpu_buffer_rsrc_t sr = make_rsrc(P.states + (int64_t)bh * NC * (DK * DV), (uint32_t)NC * DK * DV * 4);
+  const __amdgpu_buffer_rsrc_t sr = make_rsrc(P.states + (int64_t)seq * NC * (DK * DV), (uint32_t)NC * DK * DV * 4);
   const __amdgpu_buffer_rsrc_t dr = make_rsrc(P.decays + (int64_t)bh * NC * DK, (uint32_t)NC * DK * 4);
   const int i0 = (4 * (int)threadIdx.x) % DK;
   f4 acc[SPER], wgt = {1.f, 1.f, 1.f, 1.f};
@@ -1028,7 +1034,7 @@ __device__ __forceinline__ void state_inline(const GlaParams& P, Sm& sm, int bh,
       const int dv = (4 * q4) / DK;
       if (P.s0) {
 #pragma unroll
-        for (int e = 0; e < 4; ++e) acc[m][e] += wgt[e] * P.s0[((int64_t)bh * DK + i0 + e) * DV + dv];
+        for (int e = 0; e < 4; ++e) acc[m][e] += wgt[e] * P.s0[((int64_t)bh * DK + i0 + e) * P.dvp + dv];
       }
       if (state) {
 #pragma unroll
@@ -1037,7 +1043,7 @@ __device__ __forceinline__ void state_inline(const GlaParams& P, Sm& sm, int bh,
       if (final) {
         const f4 uc = coh_load4(sr, ((uint32_t)c * (DK * DV) + 4 * q4) * 4);
 #pragma unroll
-        for (int e = 0; e < 4; ++e) P.s_final[((int64_t)bh * DK + i0 + e) * DV + dv] = dc[e] * acc[m][e] + uc[e];
+        for (int e = 0; e < 4; ++e) P.s_final[((int64_t)bh * DK + i0 + e) * P.dvp + dv] = dc[e] * acc[m][e] + uc[e];
       }
     }
   }
@@ -1046,12 +1052,13 @@ __device__ __forceinline__ void state_inline(const GlaParams& P, Sm& sm, int bh,
 // The same from fp16 summaries (16-bit inputs): 16-byte pieces of 8 elements,
 // which share dims i..i+7 when NT is a multiple of DK / 8; float32 sums.
 template <int DK, int DV, int NT, typename Sm, typename E, int SP>
-__device__ __forceinline__ void state_inline16(const GlaParams& P, Sm& sm, int bh, int c, bool state, bool final) {
+__device__ __forceinline__ void state_inline16(const GlaParams& P, Sm& sm, int seq, int bh, int c, bool state,
+                                               bool final) {
   constexpr int SQ8 = DK * DV / 8;
   constexpr int SPER = (SQ8 + NT - 1) / NT;
   static_assert(NT % (DK / 8) == 0, "the pieces of one thread must share their dims");
   const int NC = P.nchunks;
-  const __amdgpu_buffer_rsrc_t sr = make_rsrc(P.states16 + (int64_t)bh * NC * (DK * DV), (uint32_t)NC * DK * DV * 2);
+  const __amdgpu_buffer_rsrc_t sr = make_rsrc(P.states16 + (int64_t)seq * NC * (DK * DV), (uint32_t)NC * DK * DV * 2);
   const __amdgpu_buffer_rsrc_t dr = make_rsrc(P.decays + (int64_t)bh * NC * DK, (uint32_t)NC * DK * 4);
   const int i0 = (8 * (int)threadIdx.x) % DK;
   float acc[SPER][8], wgt[8];
@@ -1110,7 +1117,7 @@ __device__ __forceinline__ void state_inline16(const GlaParams& P, Sm& sm, int b
       const int dv = (8 * q8) / DK;
       if (P.s0) {
 #pragma unroll
-        for (int e = 0; e < 8; ++e) acc[m][e] += wgt[e] * P.s0[((int64_t)bh * DK + i0 + e) * DV + dv];
+        for (int e = 0; e < 8; ++e) acc[m][e] += wgt[e] * P.s0[((int64_t)bh * DK + i0 + e) * P.dvp + dv];
       }
       if (state) {
 #pragma unroll
@@ -1122,7 +1129,7 @@ __device__ __forceinline__ void state_inline16(const GlaParams& P, Sm& sm, int b
                                                       kAgentCoherent));
 #pragma unroll
         for (int e = 0; e < 8; ++e)
-          P.s_final[((int64_t)bh * DK + i0 + e) * DV + dv] = dc[e >> 2][e & 3] * acc[m][e] + (float)uc[e];
+          P.s_final[((int64_t)bh * DK + i0 + e) * P.dvp + dv] = dc[e >> 2][e & 3] * acc[m][e] + (float)uc[e];
       }
     }
   }
@@ -1132,24 +1139,46 @@ __device__ __forceinline__ void state_inline16(const GlaParams& P, Sm& sm, int b
 // robin, so block b runs on XCD b % 8; all chunks of a sequence get the same
 // b % 8 and therefore share one L2. Blocks whose sequence index is past the end
 // exit at once.
+// Value split (inline schedule, P.vparts = 2): the work-groups of a chunk each
+// take DV of the head's 2 DV value columns, so a head runs as two sequences
+// with their own summaries, counters and boundary states (columns of S) over
+// the same q, k, g; both write the chunk decays, with identical values. The
+// grid is then exactly (sequences x chunks), chunks in descending order: the
+// chunks with the longest rebuilds start first, and the work-groups that
+// share a CU once every CU has one are the first chunks of their sequences.
 template <int DK, int DV, int C, int IN, bool INLINE>
 __global__ void __launch_bounds__(tile_threads(C)) gla_fused_kernel(GlaParams P) {
   typedef Chunk<DK, DV, C, IN> T;
   __shared__ typename T::Smem sm;
   const int NC = P.nchunks;
   const int b = blockIdx.x;
-  const int x = b & 7, slot = b >> 3;
-  const int grp = slot / NC, c = slot - grp * NC;
-  const int bh = grp * 8 + x;
-  if (bh >= P.BH) return;
-  unsigned* sync = P.sync + 4 * bh;
-  const int64_t sc = (int64_t)bh * NC + c;
+  int seq, c, bh;
+  if (INLINE && P.vparts > 1) {
+    const int ns = P.BH * P.vparts;
+    const int row = b / ns;
+    seq = b - row * ns;
+    c = NC - 1 - row;
+    bh = seq / P.vparts;
+    const int vp = seq - bh * P.vparts;
+    P.v = static_cast<const char*>(P.v) + (int64_t)vp * DV * (T::F16 ? 2 : 4);
+    P.o = static_cast<char*>(P.o) + (int64_t)vp * DV * (P.odt == GTR_F32 ? 4 : 2);
+    if (P.s0) P.s0 += vp * DV;
+    if (P.s_final) P.s_final += vp * DV;
+  } else {
+    const int x = b & 7, slot = b >> 3;
+    const int grp = slot / NC;
+    c = slot - grp * NC;
+    seq = bh = grp * 8 + x;
+    if (bh >= P.BH) return;
+  }
+  unsigned* sync = P.sync + 4 * seq;
+  const int64_t sc = (int64_t)seq * NC + c;
 
   T ch;
   ch.template load<true>(P, sm, bh, c);
   Raw rz[T::SITER];
   if (P.gate) ch.prefetch_gate(P, bh, c, rz);
-  ch.template factors<true, true, true>(sm, P.decays + sc * DK);
+  ch.template factors<true, true, true>(sm, P.decays + ((int64_t)bh * NC + c) * DK);
   if constexpr (T::F16)
     ch.template summary_out<true, true>(sm, nullptr, P.states16 + sc * (DK * DV));
   else
@@ -1165,9 +1194,9 @@ __global__ void __launch_bounds__(tile_threads(C)) gla_fused_kernel(GlaParams P)
     const bool final = P.s_final && c == NC - 1;
     if (state || final) {
       if constexpr (T::F16)
-        state_inline16<DK, DV, T::NT, typename T::Smem, typename T::E, T::SP>(P, sm, bh, c, state, final);
+        state_inline16<DK, DV, T::NT, typename T::Smem, typename T::E, T::SP>(P, sm, seq, bh, c, state, final);
       else
-        state_inline<DK, DV, T::NT, typename T::Smem, typename T::E, T::SP>(P, sm, bh, c, state, final);
+        state_inline<DK, DV, T::NT, typename T::Smem, typename T::E, T::SP>(P, sm, seq, bh, c, state, final);
     }
     if (state) {
       __syncthreads();
@@ -1225,16 +1254,20 @@ struct KernelSet {
   const void* output;
   const void* fused;
   const void* inlined;
+  const void* inlined_split;  // inline schedule with d_v split in two (d_v = 64 only), else null
   const void* scan;
   int threads;
 };
 
 template <int DK, int DV, int C, int IN>
 static KernelSet kernels_for() {
+  const void* split = nullptr;
+  if constexpr (DV == 64) split = reinterpret_cast<const void*>(&gla_fused_kernel<DK, DV / 2, C, IN, true>);
   return KernelSet{reinterpret_cast<const void*>(&gla_summary_kernel<DK, DV, C, IN>),
                    reinterpret_cast<const void*>(&gla_output_kernel<DK, DV, C, IN>),
                    reinterpret_cast<const void*>(&gla_fused_kernel<DK, DV, C, IN, false>),
                    reinterpret_cast<const void*>(&gla_fused_kernel<DK, DV, C, IN, true>),
+                   split,
                    reinterpret_cast<const void*>(&gla_scan_kernel<DK, DV, IN != GTR_F32>), tile_threads(C)};
 }
 
@@ -1273,30 +1306,36 @@ static bool select_kernels(const GlaShape& s, KernelSet* ks) {
 // chunks, 200 KB, faster inline).
 constexpr int64_t kInlineMaxSummaryBytes = 262144;
 
-// Largest number of work-groups of one sequence that can be resident on one XCD
-// at once (8 XCDs per device); cached per (device, kernel).
-static int fused_capacity_per_xcd(const void* kernel, int threads) {
+// Largest number of work-groups of one kernel that can be resident on one XCD
+// at once (8 XCDs per device), and the XCD's CU count (0 for both if a query
+// fails); cached per (device, kernel).
+static int fused_capacity_per_xcd(const void* kernel, int threads, int* cus_per_xcd = nullptr) {
   struct Entry {
     int dev;
     const void* k;
-    int cap;
+    int cap, cus;
   };
   static std::mutex mu;
   static Entry cache[128];
   static int n = 0;
   int dev = 0;
+  if (cus_per_xcd) *cus_per_xcd = 0;
   if (hipGetDevice(&dev) != hipSuccess) return 0;
   {
     std::lock_guard<std::mutex> lk(mu);
     for (int i = 0; i < n; ++i)
-      if (cache[i].dev == dev && cache[i].k == kernel) return cache[i].cap;
+      if (cache[i].dev == dev && cache[i].k == kernel) {
+        if (cus_per_xcd) *cus_per_xcd = cache[i].cus;
+        return cache[i].cap;
+      }
   }
   int per_cu = 0, cus = 0;
   if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kernel, threads, 0) != hipSuccess) return 0;
   if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) return 0;
   const int cap = per_cu * (cus / 8);
+  if (cus_per_xcd) *cus_per_xcd = cus / 8;
   std::lock_guard<std::mutex> lk(mu);
-  if (n < 128) cache[n++] = Entry{dev, kernel, cap};
+  if (n < 128) cache[n++] = Entry{dev, kernel, cap, cus / 8};
   return cap;
 }
 
@@ -1313,8 +1352,18 @@ constexpr int64_t kFusedMaxChunks = 4096;
 // compete for the XCD's slots and partly resident ones spin while they wait for
 // the rest, so AUTO takes the staged schedule there. An explicit one-launch
 // path that does not fit is GTR_ERR_UNSUPPORTED.
-static gtr_status choose_schedule(const GlaShape& s, int path, const KernelSet& ks, int* sched) {
+// The inline schedule splits d_v = 64 over two work-groups per chunk (half the
+// value work and half the summary bytes that each chunk's rebuild reads) when
+// there is no output-gate epilogue (its RMSNorm needs whole rows) and the
+// doubled grid still gives every work-group a CU of its own (the split grid is
+// spread over all XCDs: work-group b runs on XCD b % 8). Measured at 40x40
+// tokens, fp16, d_k = d_v = 64: 4 heads 11.5 against 13.2 us, 2 heads 11.4
+// against 12.9; at 6 heads (300 work-groups, some CUs running two) no gain, and
+// for d_k = 32 at 6 heads 13.3 against 10.7 us. *vparts is 1 or 2.
+static gtr_status choose_schedule(const GlaShape& s, int path, bool gate, const KernelSet& ks, int* sched,
+                                  int* vparts) {
   *sched = GTR_PATH_STAGED;
+  *vparts = 1;
   const bool auto_one_launch = path == GTR_PATH_AUTO && s.BH <= 8;
   if (path == GTR_PATH_FUSED || path == GTR_PATH_INLINE || auto_one_launch) {
     const bool inl = path == GTR_PATH_INLINE ||
@@ -1324,6 +1373,12 @@ static gtr_status choose_schedule(const GlaShape& s, int path, const KernelSet& 
     const bool fits = cap > 0 && s.nchunks <= cap && s.nchunks <= kFusedMaxChunks && s.BH <= kSyncSeqs;
     if (path != GTR_PATH_AUTO && !fits) return GTR_ERR_UNSUPPORTED;
     if (fits) *sched = inl ? GTR_PATH_INLINE : GTR_PATH_FUSED;
+    if (fits && inl && !gate && ks.inlined_split && 2 * s.BH <= kSyncSeqs) {
+      int cus = 0;
+      const int scap = fused_capacity_per_xcd(ks.inlined_split, ks.threads, &cus);
+      const int64_t per_xcd = (2 * s.BH * s.nchunks + 7) / 8;
+      if (per_xcd <= scap && per_xcd <= cus) *vparts = 2;
+    }
   }
   return GTR_OK;
 }
@@ -1358,10 +1413,19 @@ extern "C" int gtr_gla_workspace_fault(const void* workspace, size_t bytes) {
 extern "C" int gtr_gla_schedule(const gtr_gla_args* a) {
   GlaShape s;
   KernelSet ks;
-  int sched = -1;
+  int sched = -1, vparts = 1;
   if (!a || gla_shape_from_args(a, &s, /*check_pointers=*/false) != GTR_OK || !select_kernels(s, &ks)) return -1;
-  if (choose_schedule(s, a->path, ks, &sched) != GTR_OK) return -1;
+  if (choose_schedule(s, a->path, a->out_gate != nullptr, ks, &sched, &vparts) != GTR_OK) return -1;
   return sched;
+}
+
+extern "C" int gtr_gla_value_parts(const gtr_gla_args* a) {
+  GlaShape s;
+  KernelSet ks;
+  int sched = -1, vparts = 1;
+  if (!a || gla_shape_from_args(a, &s, /*check_pointers=*/false) != GTR_OK || !select_kernels(s, &ks)) return -1;
+  if (choose_schedule(s, a->path, a->out_gate != nullptr, ks, &sched, &vparts) != GTR_OK) return -1;
+  return vparts;
 }
 
 extern "C" gtr_status gtr_gla_fwd(const gtr_gla_args* a, hipStream_t stream) {
@@ -1404,16 +1468,19 @@ extern "C" gtr_status gtr_gla_fwd(const gtr_gla_args* a, hipStream_t stream) {
   P.nw = a->out_gate ? a->norm_weight : nullptr;
   P.gatedt = a->out_gate_dtype;
   P.eps = a->norm_eps;
+  P.dvp = s.dv;
 
   int sched = GTR_PATH_STAGED;
-  const gtr_status cs = choose_schedule(s, a->path, ks, &sched);
+  const gtr_status cs = choose_schedule(s, a->path, a->out_gate != nullptr, ks, &sched, &P.vparts);
   if (cs != GTR_OK) return cs;
-  const void* one_launch = sched == GTR_PATH_INLINE ? ks.inlined : sched == GTR_PATH_FUSED ? ks.fused : nullptr;
+  const void* one_launch = sched == GTR_PATH_INLINE ? (P.vparts > 1 ? ks.inlined_split : ks.inlined)
+                           : sched == GTR_PATH_FUSED ? ks.fused
+                                                     : nullptr;
 
   void* kargs[] = {&P};
   hipError_t err;
   if (one_launch) {
-    const int64_t blocks = (int64_t)8 * P.groups * s.nchunks;
+    const int64_t blocks = P.vparts > 1 ? (int64_t)P.vparts * s.BH * s.nchunks : (int64_t)8 * P.groups * s.nchunks;
     err = hipLaunchKernel(one_launch, dim3((unsigned)blocks), dim3(ks.threads), kargs, 0, stream);
   } else {
     err = hipLaunchKernel(ks.summary, dim3((unsigned)s.nchunks, (unsigned)s.BH), dim3(ks.threads), kargs, 0, stream);

@@ -665,6 +665,9 @@ HANDLERS.update({
     's_min_u32': salu32(lambda a, b: (min(a, b), a < b)),
     's_max_u32': salu32(lambda a, b: (max(a, b), a > b)),
     's_abs_i32': salu32(lambda a: (abs(sx(a)), abs(sx(a)) != 0)),
+    's_not_b32': salu32(lambda a: (~a & M32, (~a & M32) != 0)),
+    's_andn2_b32': salu32(lambda a, b: (a & ~b & M32, (a & ~b & M32) != 0)),
+    's_orn2_b32': salu32(lambda a, b: ((a | ~b) & M32, ((a | ~b) & M32) != 0)),
     's_lshl_b64': salu64_shift(lambda a, b: ((a << (b & 63)) & M64, ((a << (b & 63)) & M64) != 0)),
     's_lshr_b64': salu64_shift(lambda a, b: (a >> (b & 63), (a >> (b & 63)) != 0)),
 })

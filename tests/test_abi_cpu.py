@@ -103,6 +103,11 @@ def test_schedule_query_without_device(lib):
     assert lib.gtr_gla_schedule(ctypes.byref(a)) == -1
     a.path, a.dk = 0, 48
     assert lib.gtr_gla_schedule(ctypes.byref(a)) == -1
+    # the value split is a variant of the inline schedule only
+    assert lib.gtr_gla_value_parts(None) == -1
+    assert lib.gtr_gla_value_parts(ctypes.byref(a)) == -1
+    a.dk = 64
+    assert lib.gtr_gla_value_parts(ctypes.byref(a)) == 1
 
 
 def test_sequence_rows_beyond_descriptor_range(lib):

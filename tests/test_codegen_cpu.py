@@ -90,7 +90,7 @@ def test_emulator_flags_out_of_bounds():
 # ---------------------------------------------------------------------------
 DT = {"f32": (0, 4), "f16": (1, 2), "bf16": (2, 2)}
 SCAN = {"row": 0, "col": 1, "row_rev": 2, "col_rev": 3}
-KERNARG_BYTES = 184  # sizeof(GlaParams)
+KERNARG_BYTES = 192  # sizeof(GlaParams)
 
 
 def a256(x):
@@ -137,8 +137,9 @@ class Shape:
 UNMAPPED = 0x7000_0000_0000  # an address inside no registered buffer: any access is reported
 
 
-def kernel_args(c: Shape):
-    """GlaParams for shape c with every buffer at its own base, and the buffers."""
+def kernel_args(c: Shape, vparts: int = 1):
+    """GlaParams for shape c with every buffer at its own base, and the buffers
+    (vparts = 2: the inline schedule's value split)."""
     regions = []
     nxt = [0x1000_0000_0000]
 
@@ -168,14 +169,15 @@ def kernel_args(c: Shape):
     total = a256(states16 + (c.BH * c.NC * c.dk * c.dv * 2 if c.dt != "f32" else 0))
     ws = alloc("workspace", total, "rw")
     # hand-off counters read as complete, so every bounded wait ends at once
-    regions.insert(0, emu.Region("sync", ws + sync, c.BH * 16, "rw", load_value=0x7FFFFFFF))
+    regions.insert(0, emu.Region("sync", ws + sync, vparts * c.BH * 16, "rw", load_value=0x7FFFFFFF))
     regions.insert(0, emu.Region("fault", ws, 256, "rw"))
     regions.append(emu.Region("kernarg", emu.KERNARG_BASE, KERNARG_BYTES, "r"))
-    kern = struct.pack("<7Q6iqifi4xQQQQiif4xQQifQ", q, k, v, g, o, s0, sf, DT[c.dt][0], DT[c.gdt][0],
+    kern = struct.pack("<7Q6iqifi4xQQQQiif4xQQifQii", q, k, v, g, o, s0, sf, DT[c.dt][0], DT[c.gdt][0],
                        DT[c.odt][0], c.BH, c.H, c.W, c.L, c.NC, c.dk ** -0.5, SCAN[c.scan],
                        ws + states if c.dt == "f32" else UNMAPPED,  # 16-bit inputs never touch float32 states
                        ws + decays, ws + sync, ws, (c.BH + 7) // 8, 1 if c.logits else 0, 1.0 / 16,
-                       z, nw, DT[c.zdt][0] if c.zdt else 0, 1e-5, ws + states16 if c.dt != "f32" else 0)
+                       z, nw, DT[c.zdt][0] if c.zdt else 0, 1e-5, ws + states16 if c.dt != "f32" else 0,
+                       c.dv, vparts)
     assert len(kern) == KERNARG_BYTES
     return kern, regions
 
@@ -188,6 +190,8 @@ def mangled(kind: str, c: Shape) -> str:
         return f"_ZN3gtr17gla_output_kernel{t}EEvNS_9GlaParamsE"
     if kind == "scan":
         return f"_ZN3gtr15gla_scan_kernelILi{c.dk}ELi{c.dv}ELb{int(c.dt != 'f32')}EEEvNS_9GlaParamsE"
+    if kind == "inline_split":  # d_v / 2 columns per work-group
+        return f"_ZN3gtr16gla_fused_kernelILi{c.dk}ELi{c.dv // 2}ELi{c.chunk}ELi{DT[c.dt][0]}ELb1EEEvNS_9GlaParamsE"
     return f"_ZN3gtr16gla_fused_kernel{t}Lb{1 if kind == 'inline' else 0}EEEvNS_9GlaParamsE"
 
 
@@ -202,6 +206,9 @@ def work_groups(kind: str, c: Shape):
     if kind == "scan":
         eb = (c.dk * c.dv + 255) // 256
         return [((x, bh, 0), 2) for x in sorted({0, eb - 1}) for bh in bhs]  # 128 threads
+    if kind == "inline_split":  # block b: sequence b % ns (head, part), chunk NC - 1 - b // ns
+        ns = 2 * c.BH
+        return [(((c.NC - 1 - cc) * ns + sq, 0, 0), nw) for cc in cs for sq in sorted({0, 1, ns - 1})]
     picks = {((bh // 8 * c.NC + cc) << 3) | (bh % 8) for bh in bhs for cc in cs}
     last = (c.BH + 7) // 8 - 1
     spare = [x for x in range(8) if last * 8 + x >= c.BH]
@@ -214,15 +221,16 @@ def work_groups(kind: str, c: Shape):
 # every chunk size, reversed and column scans, S0 / S_final, partial chunks
 CHECKS = [
     (Shape(1, 12, 40, 40, 64, 64, 64, "bf16", "bf16", "f32", "row", False, False),
-     ("summary", "scan", "output", "fused", "inline")),
+     ("summary", "scan", "output", "fused", "inline", "inline_split")),
     (Shape(8, 12, 40, 40, 64, 64, 64, "bf16", "bf16", "f32", "col_rev", True, True), ("output", "fused", "inline")),
     (Shape(2, 9, 12, 20, 32, 32, 32, "bf16", "f32", "f32", "col", True, True), ("summary", "output", "fused")),
     (Shape(1, 2, 20, 20, 32, 64, 128, "bf16", "bf16", "bf16", "row_rev", False, False), ("output", "fused")),
     (Shape(1, 6, 40, 40, 64, 64, 64, "f16", "f16", "f16", "row", False, False), ("fused",)),
-    (Shape(1, 3, 7, 9, 64, 64, 128, "f16", "f32", "f32", "col", True, True), ("output", "inline")),
+    (Shape(1, 3, 7, 9, 64, 64, 128, "f16", "f32", "f32", "col", True, True), ("output", "inline", "inline_split")),
+    (Shape(1, 2, 13, 11, 64, 64, 32, "f32", "f32", "f32", "row_rev", True, True), ("inline", "inline_split")),
     (Shape(1, 2, 13, 11, 32, 32, 32, "f32", "f32", "f32", "row", False, True), ("summary", "output", "fused")),
     (Shape(1, 6, 128, 128, 32, 64, 64, "f16", "f16", "f16", "row", False, False),
-     ("summary", "scan", "output", "fused", "inline")),
+     ("summary", "scan", "output", "fused", "inline", "inline_split")),
     # gate fusion and the output-gate epilogue
     (Shape(1, 12, 40, 40, 64, 64, 64, "bf16", "bf16", "f32", "col", True, True, True, "bf16", True),
      ("summary", "output", "fused", "inline")),
@@ -240,8 +248,8 @@ def asm_text():
 def test_gla_kernel_addresses(asm_text, case):
     c, kinds = CHECKS[case]
     names = set(emu.kernel_names(asm_text))
-    kern, regions = kernel_args(c)
     for kind in kinds:
+        kern, regions = kernel_args(c, 2 if kind == "inline_split" else 1)
         name = mangled(kind, c)
         assert name in names, f"no kernel {name} in the listing"
         prog, labels, desc = emu.parse_kernel(asm_text, name)

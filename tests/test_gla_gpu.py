@@ -119,6 +119,42 @@ def edge_workload(B, heads, H, W, dk, dv, chunk, dtype, gdtype, odtype, scan, s0
                     want_final=final, chunk=chunk, scans=(scan,), seed=seed)
 
 
+# inline schedule with the value split (two work-groups per chunk, d_v / 2
+# columns each): S0 and S_final column halves, ragged chunks, every dtype mix
+SPLIT = [
+    (1, 4, 40, 40, 64, 64, 64, "f16", "f16", "f16", "row", False, False),  # 40x40 operator shape, 4 heads
+    (1, 2, 13, 11, 64, 64, 32, "bf16", "bf16", "f32", "col_rev", True, True),
+    (2, 1, 7, 9, 64, 64, 128, "f16", "f32", "f32", "col", True, True),
+    (1, 2, 13, 11, 32, 64, 64, "f32", "f32", "f32", "row_rev", True, True),
+    (1, 6, 16, 16, 32, 64, 64, "bf16", "bf16", "bf16", "row", True, True),
+]
+
+
+@pytest.mark.parametrize("case", range(len(SPLIT)))
+def test_value_split_parity(gtr, case):
+    B, heads, H, W, dk, dv, chunk, dtype, gdtype, odtype, scan, s0, final = SPLIT[case]
+    wl = edge_workload(B, heads, H, W, dk, dv, chunk, dtype, gdtype, odtype, scan, s0, final, 3000 + case)
+    inp = make_inputs(wl)
+    if gdtype != dtype:
+        inp["g"] = inp["g"].float()
+    dev = torch.device("cuda")
+    q, k, v, g = (inp[n].to(dev) for n in ("q", "k", "v", "g"))
+    s0t = None if inp["s0"] is None else inp["s0"].to(dev)
+    kw = dict(H=H, W=W, chunk=chunk, scan=scan, s0=s0t, want_final=final, o_dtype=torch_dtype(odtype))
+    for path in ("inline", "auto"):
+        assert gtr.gtr_gla_schedule(q, k, v, g, path=path, **kw) == "inline"
+        assert gtr.gtr_gla_value_parts(q, k, v, g, path=path, **kw) == 2
+    o_ref, sf_ref = oracle.gla(inp["q"], inp["k"], inp["v"], inp["g"], inp["s0"], scale=wl.scale, H=H, W=W,
+                               scan=scan)
+    o, sf = run_gpu(gtr, wl, scan, chunk, "inline", inp)
+    tol = tol_for(dtype, odtype)
+    assert rel_err(o, o_ref) <= tol, rel_err(o, o_ref)
+    if final:
+        assert rel_err(sf, sf_ref) <= tol_for(dtype, "f32"), rel_err(sf, sf_ref)
+    o2, _ = run_gpu(gtr, wl, scan, chunk, "inline", inp)
+    assert torch.equal(o, o2)  # run to run: same work-group for each output element
+
+
 @pytest.mark.parametrize("path", PATHS)
 @pytest.mark.parametrize("case", range(len(EDGE)))
 def test_edge_parity(gtr, case, path):
@@ -227,18 +263,23 @@ def test_workspace_reuse_and_no_fault(gtr):
     assert int(ws.buf[256:256 + 16 * n_seq].view(torch.int32).abs().sum()) == 0
 
 
-@pytest.mark.parametrize("name,want", [("kbench", "inline"), ("tiny", "inline"), ("op1600", "inline"),
-                                       ("directions", "staged"), ("batched", "staged"), ("highres", "staged"),
-                                       ("op16k", "staged")])
-def test_auto_schedule(gtr, name, want):
-    """AUTO's choice (the length-aware dispatch) as gtr_gla_schedule reports it."""
-    wl = WORKLOADS[name]
+@pytest.mark.parametrize("name,heads,want,parts", [
+    ("kbench", None, "inline", 1), ("tiny", None, "inline", 1), ("op1600", None, "inline", 1),
+    ("op256", None, "inline", 2), ("kbench", 4, "inline", 2), ("op1600", 2, "inline", 2),
+    ("directions", None, "staged", 1), ("batched", None, "staged", 1), ("highres", None, "staged", 1),
+    ("op16k", None, "staged", 1)])
+def test_auto_schedule(gtr, name, heads, want, parts):
+    """AUTO's choice (the length-aware dispatch) as gtr_gla_schedule reports it,
+    and the inline value split (one work-group per CU after doubling: 4 x 25
+    chunks x 2 = 200 work-groups split, 6 x 25 x 2 = 300 do not)."""
+    wl = WORKLOADS[name] if heads is None else WORKLOADS[name].with_(heads=heads)
     dev = torch.device("cuda")
     mk = lambda d: torch.empty((wl.B, wl.heads, wl.L, d), dtype=torch_dtype(wl.dtype), device=dev)
     s0 = torch.empty((wl.B, wl.heads, wl.dk, wl.dv), device=dev) if wl.s0_std is not None else None
-    got = gtr.gtr_gla_schedule(mk(wl.dk), mk(wl.dk), mk(wl.dv), mk(wl.dk), H=wl.H, W=wl.W, chunk=wl.chunk, s0=s0,
-                               want_final=wl.want_final, o_dtype=torch_dtype(wl.odtype))
+    kw = dict(H=wl.H, W=wl.W, chunk=wl.chunk, s0=s0, want_final=wl.want_final, o_dtype=torch_dtype(wl.odtype))
+    got = gtr.gtr_gla_schedule(mk(wl.dk), mk(wl.dk), mk(wl.dv), mk(wl.dk), **kw)
     assert got == want
+    assert gtr.gtr_gla_value_parts(mk(wl.dk), mk(wl.dk), mk(wl.dv), mk(wl.dk), **kw) == parts
     assert gtr.gtr_gla_schedule(mk(wl.dk), mk(wl.dk), mk(wl.dv), mk(wl.dk), H=wl.H, W=wl.W, chunk=wl.chunk,
                                 path="staged") == "staged"
 
@@ -288,7 +329,7 @@ def test_graph_replays_match_eager(gtr):
 
 
 # ---------------------------------------------------------------------------
-# scope rows f1 / f3: gate fusion (g holds the gate logits, log gamma =
+# Gate fusion (g holds the gate logits, log gamma =
 # logsigmoid(a) / tau in the kernels) and the output-gate epilogue
 # u = SiLU(x W_r) * RMSNorm(o), both against the oracle's definitions
 # ---------------------------------------------------------------------------
@@ -385,7 +426,7 @@ def test_workspace_shared_across_shapes(gtr):
 
 
 # ---------------------------------------------------------------------------
-# scope row f4: Spatial SwiGLU, against the oracle's definition
+# Spatial SwiGLU (Sec. 3.1), against the oracle's definition
 # ---------------------------------------------------------------------------
 SWIGLU = [
     # B, H, W, d, hidden, dtype, y dtype, bias
