@@ -43,8 +43,9 @@ extern "C" {
 typedef enum {
   GTR_OK = 0,
   GTR_ERR_NULL = 1,        /* a required pointer is NULL                          */
-  GTR_ERR_SHAPE = 2,       /* a size is <= 0, a product overflows int64, or (GLA)
-                              one sequence's rows take 2 GB or more               */
+  GTR_ERR_SHAPE = 2,       /* a size is <= 0, a product overflows int64, (GLA)
+                              one sequence's rows take 2 GB or more, or (SwiGLU)
+                              a launch would need 2^31 work-groups or more        */
   GTR_ERR_UNSUPPORTED = 3, /* a dtype / head width / chunk / path not compiled in */
   GTR_ERR_ALIAS = 4,       /* an output overlaps an input or the workspace        */
   GTR_ERR_WORKSPACE = 5,   /* workspace missing, too small or not 256-B aligned   */

@@ -60,15 +60,22 @@ __device__ __forceinline__ f4 mfma(const bf8& a, const bf8& b, f4 c) {
   return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
 }
 
-// C[M][N] = A[M][K] * B[N][K]^T, row-major, K a multiple of 32, N a multiple
+// C[M][N] = A[M][K] * B[N][K]^T, row-major, K a multiple of 64, N a multiple
 // of BN. Work-group tile BM x BN, 4 waves in a 2 x 2 grid, each wave a
-// (BM/2) x (BN/2) block of 16 x 16 MFMA tiles. Every K-step of 32 stages the
+// (BM/2) x (BN/2) block of 16 x 16 MFMA tiles. Every K-step of 64 stages the
 // A and B tiles in LDS once (each element is read from memory by one thread
-// and from LDS by every wave that needs it); the loads of the next step are in
-// flight while the current one multiplies (two LDS buffers). Rows past M are
-// read from row M-1 and not stored. With ksplit > 1, blockIdx.z selects a
-// slice of K whose partial product goes to part + slice * M * N (float32) for
-// ksplit_reduce_kernel; with ksplit = 1 the product goes to C.
+// and from LDS by every wave that needs it) and runs two 32-deep MFMA passes
+// over them; the loads of the next steps are in flight while the current one
+// multiplies (two LDS buffers). Rows past M are read from row M-1 and not
+// stored. With ksplit > 1, K is cut into ksplit slices whose partial products
+// go to part + slice * M * N (float32) for ksplit_reduce_kernel; with
+// ksplit = 1 the product goes to C.
+// The grid is one-dimensional, gx * gy * ksplit work-groups (gx = ceil(M / BM),
+// gy = N / BN). Work-group b runs on XCD b % 8 (round-robin dispatch), and each
+// XCD takes a contiguous range of the tile order (slice, row block, column
+// block), column blocks fastest: the work-groups that read the same rows of A
+// (all column blocks of a row block and slice) share one XCD's L2 instead of
+// fetching those rows once per XCD.
 struct GemmArgs {
   const void* A;
   const void* B;
@@ -79,7 +86,7 @@ struct GemmArgs {
   int ksplit;  // number of K slices (1: none)
 };
 
-constexpr int KB = 4;     // minimum K-steps per slice when splitting K
+constexpr int KB = 4;     // minimum 64-wide K-steps per slice when splitting K
 // LDS tiles: rows of 32 K elements (64 bytes, no padding); the 16-byte piece
 // c of row r sits at piece c ^ kSwz(r). Measured on gfx950, ds_read_b128 serves
 // 32 lanes per cycle from 32 distinct 16-byte slots (address / 16 mod 32) and
@@ -88,43 +95,56 @@ constexpr int KB = 4;     // minimum K-steps per slice when splitting K
 // 4 pieces) both hit distinct slots.
 constexpr int kPitch = 32;
 __device__ __forceinline__ int kSwz(int r) { return (r >> 2) & 2; }
+// The output product's 64-wide rows (128 bytes, 8 pieces): piece c of row r at
+// c ^ kSwz64(r). Operand reads (16 rows x 2 pieces per 32 lanes) then hit 32
+// distinct slots (rows r, r + 4, r + 8, r + 12 share address / 16 mod 32 up to
+// the piece, and the swizzle gives them 4 disjoint piece pairs); staging writes
+// (2 rows x 8 pieces per 16 lanes) hit 16.
+constexpr int kPitch64 = 64;
+__device__ __forceinline__ int kSwz64(int r) { return ((r >> 2) & 3) << 1; }
 
 template <int ADT, int BDT, int MT, int BM, int BN>
 __global__ void __launch_bounds__(256) gemm_nt_kernel(GemmArgs g) {
   typedef Operand<ADT, MT> OA;
   typedef Operand<BDT, MT> OB;
   constexpr int TI = BM / 32, TJ = BN / 32;   // MFMA tiles per wave
-  constexpr int PA = BM * 4 / 256, PB = BN * 4 / 256;  // 16-byte pieces per thread per step
-  __shared__ __attribute__((aligned(16))) unsigned short As[2][BM * kPitch];
-  __shared__ __attribute__((aligned(16))) unsigned short Bs[2][BN * kPitch];
+  constexpr int PA = BM * 8 / 256, PB = BN * 8 / 256;  // 16-byte pieces per thread per step
+  __shared__ __attribute__((aligned(16))) unsigned short As[2][BM * kPitch64];
+  __shared__ __attribute__((aligned(16))) unsigned short Bs[2][BN * kPitch64];
 
   const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int r16 = lane & 15, kq = lane >> 4;
-  const int mb = blockIdx.x * BM, nb = blockIdx.y * BN;
+  // tile of this work-group: XCD k = b % 8 takes positions [start_k, start_k +
+  // count_k) of the tile order, count_k = ceil((T - k) / 8)
+  const int gx = (g.M + BM - 1) / BM, gy = g.N / BN;
+  const int T = gx * gy * g.ksplit, xcd = blockIdx.x & 7, slot = blockIdx.x >> 3;
+  const int j = xcd * (T >> 3) + min(xcd, T & 7) + slot;
+  const int by = j % gy, bxz = j / gy, bx = bxz % gx, bz = bxz / gx;
+  const int mb = bx * BM, nb = by * BN;
   const int wm = (w >> 1) * (BM / 2), wn = (w & 1) * (BN / 2);
   const unsigned short* A = static_cast<const unsigned short*>(g.A);
   const unsigned short* B = static_cast<const unsigned short*>(g.B);
   const int64_t K = g.K;
-  const int steps = g.K / 32;
+  const int steps = g.K / 64;
   const int s_per = (steps + g.ksplit - 1) / g.ksplit;
-  const int s0 = g.ksplit > 1 ? blockIdx.z * s_per : 0;
+  const int s0 = g.ksplit > 1 ? bz * s_per : 0;
   const int s1 = min(s0 + s_per, steps);
 
-  // global pieces of this thread: piece p -> row p / 4, 16-byte column p % 4
+  // global pieces of this thread: piece p -> row p / 8, 16-byte column p % 8
   const w4* ga[PA];
   const w4* gb[PB];
   int la[PA], lb[PB];
 #pragma unroll
   for (int q = 0; q < PA; ++q) {
-    const int p = threadIdx.x + 256 * q, row = p >> 2, col = p & 3;
+    const int p = threadIdx.x + 256 * q, row = p >> 3, col = p & 7;
     ga[q] = reinterpret_cast<const w4*>(A + (int64_t)min(mb + row, g.M - 1) * K + 8 * col);
-    la[q] = row * kPitch + 8 * (col ^ kSwz(row));
+    la[q] = row * kPitch64 + 8 * (col ^ kSwz64(row));
   }
 #pragma unroll
   for (int q = 0; q < PB; ++q) {
-    const int p = threadIdx.x + 256 * q, row = p >> 2, col = p & 3;
+    const int p = threadIdx.x + 256 * q, row = p >> 3, col = p & 7;
     gb[q] = reinterpret_cast<const w4*>(B + (int64_t)(nb + row) * K + 8 * col);
-    lb[q] = row * kPitch + 8 * (col ^ kSwz(row));
+    lb[q] = row * kPitch64 + 8 * (col ^ kSwz64(row));
   }
   f4 acc[TI][TJ];
 #pragma unroll
@@ -139,9 +159,9 @@ __global__ void __launch_bounds__(256) gemm_nt_kernel(GemmArgs g) {
   w4 ra[D][PA], rb[D][PB];
   auto fetch = [&](int st, w4 (&a)[PA], w4 (&b)[PB]) {
 #pragma unroll
-    for (int q = 0; q < PA; ++q) a[q] = ga[q][4 * st];
+    for (int q = 0; q < PA; ++q) a[q] = ga[q][8 * st];
 #pragma unroll
-    for (int q = 0; q < PB; ++q) b[q] = gb[q][4 * st];
+    for (int q = 0; q < PB; ++q) b[q] = gb[q][8 * st];
   };
   auto stage = [&](int buf, const w4 (&a)[PA], const w4 (&b)[PB]) {
 #pragma unroll
@@ -161,18 +181,22 @@ __global__ void __launch_bounds__(256) gemm_nt_kernel(GemmArgs g) {
       if (st < s1) {
         const int buf = (st - s0) & 1;
         if (st + D < s1) fetch(st + D, ra[q], rb[q]);  // slot q was staged before this step
-        typename OA::T fa[TI];
-        typename OB::T fb[TJ];
 #pragma unroll
-        for (int i = 0; i < TI; ++i)
-          fa[i] = OA::get(*reinterpret_cast<const w4*>(&As[buf][(wm + 16 * i + r16) * kPitch + 8 * (kq ^ kSwz(r16))]));
+        for (int h = 0; h < 2; ++h) {  // the two 32-deep halves of the step
+          const int pc = (4 * h + kq) ^ kSwz64(r16);
+          typename OA::T fa[TI];
+          typename OB::T fb[TJ];
 #pragma unroll
-        for (int j = 0; j < TJ; ++j)
-          fb[j] = OB::get(*reinterpret_cast<const w4*>(&Bs[buf][(wn + 16 * j + r16) * kPitch + 8 * (kq ^ kSwz(r16))]));
+          for (int i = 0; i < TI; ++i)
+            fa[i] = OA::get(*reinterpret_cast<const w4*>(&As[buf][(wm + 16 * i + r16) * kPitch64 + 8 * pc]));
 #pragma unroll
-        for (int i = 0; i < TI; ++i)
+          for (int j = 0; j < TJ; ++j)
+            fb[j] = OB::get(*reinterpret_cast<const w4*>(&Bs[buf][(wn + 16 * j + r16) * kPitch64 + 8 * pc]));
 #pragma unroll
-          for (int j = 0; j < TJ; ++j) acc[i][j] = mfma(fb[j], fa[i], acc[i][j]);  // C^T tiles
+          for (int i = 0; i < TI; ++i)
+#pragma unroll
+            for (int j = 0; j < TJ; ++j) acc[i][j] = mfma(fb[j], fa[i], acc[i][j]);  // C^T tiles
+        }
         if (st + 1 < s1) stage(buf ^ 1, ra[(q + 1) % D], rb[(q + 1) % D]);  // nobody reads buf ^ 1 now
         __syncthreads();
       }
@@ -181,7 +205,7 @@ __global__ void __launch_bounds__(256) gemm_nt_kernel(GemmArgs g) {
 
   // lane holds C[row 16i + r16][columns 16j + 4kq .. 16j + 4kq + 3] of this
   // wave's block (the products above are C^T tiles): one 4-element store each
-  void* C = g.ksplit > 1 ? static_cast<void*>(g.part + (int64_t)blockIdx.z * g.M * g.N) : g.C;
+  void* C = g.ksplit > 1 ? static_cast<void*>(g.part + (int64_t)bz * g.M * g.N) : g.C;
   const int cdt = g.ksplit > 1 ? (int)GTR_F32 : g.cdt;
 #pragma unroll
   for (int i = 0; i < TI; ++i) {
@@ -221,7 +245,13 @@ __global__ void __launch_bounds__(256) ksplit_reduce_kernel(const float* part, v
 // LDS swizzle and C^T accumulator layout of gemm_nt_kernel. The epilogue
 // rounds both products to fp16 into the LDS the K loop used and forms the
 // gated convolution there: G and V never leave the chip, and the halo's extra
-// V rows are the price (180 V rows per 128 tokens).
+// V rows are the price (180 V rows per 128 tokens). One-dimensional grid of
+// tiles * (hidden / kFN) work-groups; as in gemm_nt_kernel each XCD takes a
+// contiguous range of the order (tile, channel block), channel blocks
+// fastest, so the work-groups that read the same X halo share one XCD's L2.
+// (Measured at 40x40 tokens, one image, us per SwiGLU call: GTR-L 34.4, GTR-X
+// 45.9 with this order; 35.1 / 46.9 with channel blocks slowest; 34.2 / 46.6
+// with the plain two-dimensional grid.)
 constexpr int kFH = 8, kFW = 16;         // tile: 8 rows of 16 tokens
 constexpr int kFHW = kFW + 2;            // halo row length
 constexpr int kFV = (kFH + 2) * kFHW;    // halo tokens (180)
@@ -238,6 +268,7 @@ struct GatedConvArgs {
   const float* cb;  // [hidden] or null
   _Float16* H;      // [B * Hh * W][hidden]
   int Hh, W, d, hidden;
+  int B;            // images
 };
 
 template <int DT>
@@ -253,11 +284,16 @@ __global__ void __launch_bounds__(256) gated_conv_kernel(GatedConvArgs f) {
   const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63;
   const int r16 = lane & 15, kq = lane >> 4;
   const int tiles_x = (f.W + kFW - 1) / kFW, tiles_y = (f.Hh + kFH - 1) / kFH;
-  const int tx = (int)(blockIdx.x % tiles_x);
-  const int ty = (int)((blockIdx.x / tiles_x) % tiles_y);
-  const int64_t b = blockIdx.x / ((unsigned)tiles_x * tiles_y);
+  const int tiles = f.B * tiles_x * tiles_y;
+  const int T = tiles * (f.hidden / kFN), xcd = blockIdx.x & 7, slot = blockIdx.x >> 3;
+  const int ncb = f.hidden / kFN;
+  const int j = xcd * (T >> 3) + min(xcd, T & 7) + slot;  // position in the (tile, channel block) order
+  const int tile = j / ncb;
+  const int tx = tile % tiles_x;
+  const int ty = (tile / tiles_x) % tiles_y;
+  const int64_t b = tile / (tiles_x * tiles_y);
   const int y0 = ty * kFH, x0 = tx * kFW;
-  const int c0 = blockIdx.y * kFN;
+  const int c0 = (j % ncb) * kFN;
   const int64_t L = (int64_t)f.Hh * f.W, K = f.d;
   const unsigned short* X = static_cast<const unsigned short*>(f.X);
 
@@ -424,7 +460,7 @@ constexpr int kOutBN = 64;
 static int out_ksplit(int64_t M, int d, int hidden) {
   const int64_t wgs = ((M + 127) / 128) * (d / kOutBN);
   int s = 1;
-  while (wgs * s < 256 && s < 8 && hidden / 32 >= 2 * s * KB) s *= 2;
+  while (wgs * s < 256 && s < 8 && hidden / 64 >= 2 * s * KB) s *= 2;
   return s;
 }
 
@@ -452,6 +488,10 @@ static gtr_status swiglu_check(const gtr_swiglu_args* a, int64_t* M_out, bool ch
   if (__builtin_mul_overflow((int64_t)a->H, (int64_t)a->W, &L) || __builtin_mul_overflow(L, (int64_t)a->B, &M))
     return GTR_ERR_SHAPE;
   if (M > 0x7fffffff - 64 || __builtin_mul_overflow(M, (int64_t)a->hidden, &n) || n > ((int64_t)1 << 40))
+    return GTR_ERR_SHAPE;
+  // both launches number their work-groups with 32-bit ints
+  const int64_t tiles = (int64_t)a->B * ((a->H + kFH - 1) / kFH) * ((a->W + kFW - 1) / kFW);
+  if (tiles * (a->hidden / kFN) > 0x7fffffff || ((M + 127) / 128) * (a->d / kOutBN) * 8 > 0x7fffffff)
     return GTR_ERR_SHAPE;
   *M_out = M;
   if (!check_pointers) return GTR_OK;
@@ -505,9 +545,9 @@ extern "C" gtr_status gtr_spatial_swiglu(const gtr_swiglu_args* a, hipStream_t s
   _Float16* Hb = reinterpret_cast<_Float16*>(ws + lay.h_off);
   const bool bf = a->dtype == GTR_BF16;
 
-  const GatedConvArgs gc{a->x, a->w_gate, a->w_value, a->conv_w, a->conv_b, Hb, a->H, a->W, a->d, a->hidden};
+  const GatedConvArgs gc{a->x, a->w_gate, a->w_value, a->conv_w, a->conv_b, Hb, a->H, a->W, a->d, a->hidden, a->B};
   const int64_t tiles = (int64_t)a->B * ((a->H + kFH - 1) / kFH) * ((a->W + kFW - 1) / kFW);
-  const dim3 grid1((unsigned)tiles, (unsigned)(a->hidden / kFN));
+  const dim3 grid1((unsigned)(tiles * (a->hidden / kFN)));
   if (bf)
     hipLaunchKernelGGL(gated_conv_kernel<GTR_BF16>, grid1, dim3(256), 0, stream, gc);
   else
@@ -517,7 +557,7 @@ extern "C" gtr_status gtr_spatial_swiglu(const gtr_swiglu_args* a, hipStream_t s
   const int ks = out_ksplit(M, a->d, a->hidden);
   float* part = reinterpret_cast<float*>(ws + lay.part_off);
   GemmArgs g3{Hb, a->w_out, a->y, part, (int)M, a->d, a->hidden, a->y_dtype, ks};
-  const dim3 grid3((unsigned)((M + 127) / 128), (unsigned)(a->d / kOutBN), (unsigned)ks);
+  const dim3 grid3((unsigned)(((M + 127) / 128) * (a->d / kOutBN) * ks));
   if (bf)
     hipLaunchKernelGGL((gemm_nt_kernel<GTR_F16, GTR_BF16, GTR_F16, 128, kOutBN>), grid3, dim3(256), 0, stream, g3);
   else

@@ -317,9 +317,22 @@ def test_swiglu_gemm_addresses(adt, bdt, mt, bn, M, N, K, cdt, ks):
     name = f"_ZN3gtr14gemm_nt_kernelILi{adt}ELi{bdt}ELi{mt}ELi128ELi{bn}EEEvNS_8GemmArgsE"
     assert name in emu.kernel_names(text)
     gx, gy = (M + 127) // 128, N // bn
-    zs = range(ks)
-    wgs = [(x, y, z) for x in sorted({0, gx - 1}) for y in sorted({0, gy - 1}) for z in sorted({min(zs), max(zs)})]
-    check_kernel(text, name, kern, regions, wgs)
+    T = gx * gy * ks
+
+    def block_of(x, y, z):
+        """The 1-D block id whose tile is (x, y, z): XCD k = b % 8 runs tile
+        positions k (T // 8) + min(k, T % 8) + b // 8, column blocks fastest."""
+        j = (z * gx + x) * gy + y
+        for k in range(8):
+            start, count = k * (T // 8) + min(k, T % 8), (T - k + 7) // 8
+            if start <= j < start + count:
+                return (j - start) * 8 + k
+        raise AssertionError(j)
+
+    ids = sorted({block_of(x, y, z) for x in sorted({0, gx - 1}) for y in sorted({0, gy - 1})
+                  for z in sorted({0, ks - 1})})
+    assert all(0 <= b < T for b in ids)
+    check_kernel(text, name, kern, regions, [(b, 0, 0) for b in ids])
 
 
 @pytest.mark.parametrize("dt,B,H,W,d,hidden", [(1, 2, 7, 9, 64, 128), (2, 1, 40, 40, 384, 192),
@@ -333,12 +346,25 @@ def test_swiglu_gated_conv_addresses(dt, B, H, W, d, hidden):
                emu.Region("Wv", WV, hidden * d * 2, "r"), emu.Region("cw", CW, hidden * 9 * 4, "r"),
                emu.Region("cb", CB, hidden * 4, "r"), emu.Region("H", HO, M * hidden * 2, "w"),
                emu.Region("kernarg", emu.KERNARG_BASE, 64, "r")]
-    kern = struct.pack("<QQQQQQiiii", X, WG, WV, CW, CB, HO, H, W, d, hidden)
+    kern = struct.pack("<QQQQQQiiiii4x", X, WG, WV, CW, CB, HO, H, W, d, hidden, B)
     name = [n for n in emu.kernel_names(text) if "gated_conv_kernel" in n and f"ILi{dt}E" in n][0]
     tx, ty = (W + 15) // 16, (H + 7) // 8  # one work-group per 8 x 16 tokens x 64 channels
     nt, nc = B * tx * ty, hidden // 64
-    wgs = sorted({(x, y, 0) for x in (0, tx - 1, nt - 1, nt // 2) for y in (0, nc - 1)})
-    check_kernel(text, name, kern, regions, wgs)
+    T = nt * nc
+
+    def block_of(tile, cb):
+        """1-D block id of (tile, channel block): XCD k = b % 8 runs positions
+        k (T // 8) + min(k, T % 8) + b // 8 of the order, channel blocks fastest."""
+        j = tile * nc + cb
+        for k in range(8):
+            start, count = k * (T // 8) + min(k, T % 8), (T - k + 7) // 8
+            if start <= j < start + count:
+                return (j - start) * 8 + k
+        raise AssertionError(j)
+
+    ids = sorted({block_of(t, c) for t in (0, tx - 1, nt - 1, nt // 2) for c in (0, nc - 1)})
+    assert all(0 <= b < T for b in ids)
+    check_kernel(text, name, kern, regions, [(b, 0, 0) for b in ids])
 
 
 @pytest.mark.parametrize("cdt", [0, 1, 2])
