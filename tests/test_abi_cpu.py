@@ -325,6 +325,18 @@ def test_swiglu_bad_arguments(lib, field, val, want):
     assert sw(lib, a) == want
 
 
+def test_swiglu_grid_bounds(lib):
+    """Launch sizes are checked on the host: 2^30 one-token images at hidden
+    192 would need 3 * 2^30 gated-convolution work-groups (more than 2^31 - 1):
+    GTR_ERR_SHAPE, with no launch; at hidden 64 (2^30 work-groups) the shape
+    is accepted."""
+    a = swiglu_args(B=1 << 30, H=1, W=1, d=64, hidden=192)
+    assert lib.gtr_spatial_swiglu_workspace_size(ctypes.byref(a)) == 0
+    assert sw(lib, a) == SHAPE
+    a = swiglu_args(B=1 << 30, H=1, W=1, d=64, hidden=64)
+    assert lib.gtr_spatial_swiglu_workspace_size(ctypes.byref(a)) > 0
+
+
 def test_swiglu_nulls_alignment_alias_workspace(lib):
     a = swiglu_args()
     a.w_out = None
