@@ -391,22 +391,29 @@ __global__ void __launch_bounds__(256) gated_conv_kernel(GatedConvArgs f) {
   }
 
   // epilogue: V [192 halo rows][kFN] and G [128 tile tokens][kFN] in fp16, in
-  // the stage buffers (every wave passed the K loop's last barrier)
+  // the stage buffers (every wave passed the K loop's last barrier). The
+  // 16-byte piece p of row r sits at piece p ^ eswz(r): the C^T writes (16
+  // rows x 2 half-pieces per 32 lanes) and the convolution's reads (4
+  // consecutive rows x 8 pieces per 32 lanes) then both spread over all banks;
+  // unswizzled, the writes of rows r, r + 2, r + 4, ... hit the same banks.
   _Float16* Vt = reinterpret_cast<_Float16*>(&stg[0][0]);
   _Float16* Gt = Vt + kFVT * 16 * kFN;
+  auto eswz = [](int row) { return (row >> 1) & 7; };
 #pragma unroll
   for (int t = 0; t < VT; ++t)
 #pragma unroll
     for (int j = 0; j < NJ; ++j) {
+      const int row = 16 * (VT * w + t) + r16;
       const h4 hv = {(_Float16)av[t][j][0], (_Float16)av[t][j][1], (_Float16)av[t][j][2], (_Float16)av[t][j][3]};
-      *reinterpret_cast<h4*>(&Vt[(16 * (VT * w + t) + r16) * kFN + 16 * j + 4 * kq]) = hv;
+      *reinterpret_cast<h4*>(&Vt[row * kFN + 8 * ((2 * j + (kq >> 1)) ^ eswz(row)) + 4 * (kq & 1)]) = hv;
     }
 #pragma unroll
   for (int t = 0; t < GT; ++t)
 #pragma unroll
     for (int j = 0; j < NJ; ++j) {
+      const int row = 16 * (GT * w + t) + r16;
       const h4 hg = {(_Float16)ag[t][j][0], (_Float16)ag[t][j][1], (_Float16)ag[t][j][2], (_Float16)ag[t][j][3]};
-      *reinterpret_cast<h4*>(&Gt[(16 * (GT * w + t) + r16) * kFN + 16 * j + 4 * kq]) = hg;
+      *reinterpret_cast<h4*>(&Gt[row * kFN + 8 * ((2 * j + (kq >> 1)) ^ eswz(row)) + 4 * (kq & 1)]) = hg;
     }
   __syncthreads();
 
@@ -434,11 +441,12 @@ __global__ void __launch_bounds__(256) gated_conv_kernel(GatedConvArgs f) {
     for (int u = 0; u < 3; ++u)
 #pragma unroll
       for (int v = 0; v < 3; ++v) {
-        const h8 x = *reinterpret_cast<const h8*>(&Vt[((ci + u) * kFHW + cj + v) * kFN + 8 * pc]);
+        const int row = (ci + u) * kFHW + cj + v;
+        const h8 x = *reinterpret_cast<const h8*>(&Vt[row * kFN + 8 * (pc ^ eswz(row))]);
 #pragma unroll
         for (int e = 0; e < 8; ++e) acc[e] = fmaf((float)x[e], wt[9 * e + 3 * u + v], acc[e]);
       }
-    const h8 g8 = *reinterpret_cast<const h8*>(&Gt[ct * kFN + 8 * pc]);
+    const h8 g8 = *reinterpret_cast<const h8*>(&Gt[ct * kFN + 8 * (pc ^ eswz(ct))]);
     h8 out;
 #pragma unroll
     for (int e = 0; e < 8; ++e) {

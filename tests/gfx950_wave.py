@@ -1502,6 +1502,7 @@ HANDLERS.update({
     'ds_write_b16': ds_write(2), 'ds_write_b16_d16_hi': ds_write(2), 'ds_write_b8': ds_write(1),
     'ds_write2_b32': ds_write(4, True), 'ds_write2st64_b32': ds_write(4, True, True),
     'ds_write2_b64': ds_write(8, True), 'ds_write_b96': ds_write(12),
+    'ds_write2st64_b64': ds_write(8, True, True), 'ds_read2st64_b64': ds_read(4, 8, True, True),
 })
 
 
