@@ -503,3 +503,75 @@ def test_spatial_swiglu_is_local():
     diff = np.abs(oracle.spatial_swiglu(x2, wg, wv, wo, cw, cb, H=H, W=W) - y0).max(axis=-1).reshape(H, W)
     changed = np.argwhere(diff > 0)
     assert changed.min(axis=0).tolist() == [1, 2] and changed.max(axis=0).tolist() == [3, 4]
+
+
+def swiglu_by_loops(x, wg, wv, wo, cw, cb, H, W):
+    """Eq. spatial_swiglu written out token by token with scalar loops: the value
+    branch X W_v is convolved over the 3 x 3 neighbourhood (zero outside the grid),
+    then gated by SiLU of the token's own X W_g, then mapped by W_o."""
+    import math
+    B, L, d = x.shape
+    h = wg.shape[0]
+    y = np.zeros((B, L, d))
+    for b in range(B):
+        val = [[sum(x[b, t, k] * wv[c, k] for k in range(d)) for c in range(h)] for t in range(L)]
+        for i in range(H):
+            for j in range(W):
+                t = i * W + j
+                hid = []
+                for c in range(h):
+                    conv = cb[c] if cb is not None else 0.0
+                    for u in range(3):
+                        for w_ in range(3):
+                            ii, jj = i + u - 1, j + w_ - 1
+                            if 0 <= ii < H and 0 <= jj < W:
+                                conv += val[ii * W + jj][c] * cw[c, u, w_]
+                    gate = sum(x[b, t, k] * wg[c, k] for k in range(d))
+                    hid.append(gate / (1.0 + math.exp(-gate)) * conv)
+                for o_ in range(d):
+                    y[b, t, o_] = sum(hid[c] * wo[o_, c] for c in range(h))
+    return y
+
+
+def swiglu_composition_pin(fn):
+    """True when ``fn`` (the oracle's signature) agrees with the scalar loops on a
+    3 x 4 grid with a non-identity 3 x 3 kernel per channel."""
+    rng = np.random.default_rng(25)
+    B, H, W, d, h = 1, 3, 4, 2, 3
+    x = rng.normal(size=(B, H * W, d))
+    wg, wv, wo = rng.normal(size=(h, d)), rng.normal(size=(h, d)), rng.normal(size=(d, h))
+    cw = rng.normal(size=(h, 3, 3))  # every tap nonzero, no symmetry
+    cb = rng.normal(size=h)
+    want = swiglu_by_loops(x, wg, wv, wo, cw, cb, H, W)
+    got = fn(x, wg, wv, wo, cw, cb, H=H, W=W)
+    return np.allclose(got, want, rtol=1e-12, atol=1e-12)
+
+
+def py_spatial_swiglu(x, wg, wv, wo, cw, cb, *, H, W, mistake=None):
+    """A copy of the composition in which one mistake can be planted (the
+    depthwise convolution itself is the pinned oracle routine)."""
+    g = x @ wg.T
+    v = x @ wv.T
+    silu = lambda a: a / (1.0 + np.exp(-a))
+    if mistake == "conv_on_gate":
+        hid = silu(oracle.dwconv3x3(g, cw, cb, H=H, W=W)) * v
+    elif mistake == "conv_after_gating":
+        hid = oracle.dwconv3x3(silu(g) * v, cw, cb, H=H, W=W)
+    elif mistake == "no_bias":
+        hid = silu(g) * oracle.dwconv3x3(v, cw, None, H=H, W=W)
+    else:
+        hid = silu(g) * oracle.dwconv3x3(v, cw, cb, H=H, W=W)
+    return hid @ wo.T
+
+
+def test_spatial_swiglu_composition_matches_scalar_loops():
+    assert swiglu_composition_pin(oracle.spatial_swiglu)
+
+
+def test_spatial_swiglu_python_copy_passes_the_composition_pin():
+    assert swiglu_composition_pin(lambda *a, **kw: py_spatial_swiglu(*a, **kw))
+
+
+@pytest.mark.parametrize("mistake", ["conv_on_gate", "conv_after_gating", "no_bias"])
+def test_spatial_swiglu_composition_pin_rejects_planted_mistakes(mistake):
+    assert not swiglu_composition_pin(lambda *a, **kw: py_spatial_swiglu(*a, mistake=mistake, **kw))
