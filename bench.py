@@ -1,23 +1,29 @@
 """Benchmark of the chunkwise GLA forward on one MI355X.
 
-One step = one gtr_gla_fwd call on the paper's operator-benchmark shape
-(B=1, 6 heads, 40x40 token grid -> L=1600, d_k=d_v=64, fp16 in/out, chunk 64,
-row-major scan), with inputs already resident in HBM. K steps are captured in
-one HIP graph (the paper times its operator under graph replay) and replayed
-once inside the timed region.
+One step = one pass of the hot path over one batch of synthetic input: one
+gtr_gla_fwd call (four for the alternating-directions workload, one per scan
+direction), with the inputs already resident in HBM when timing starts. The
+five workloads of the benchmark are all timed (tiny 16x16 parity case, the
+40x40 fp16 operator shape, four directions at 40x40 bf16, 80x80 at chunk 32 / 64
+/ 128, a batch of 8 images); the headline line is the 40x40 fp16 operator shape.
 
-Prints ONE JSON line (see the keys below). ``roofline`` prices the call's
-kernels against HBM bandwidth with the algorithmic bytes of the call;
-``cpu_baseline`` times the float64 oracle on the host on a bounded sample of
-the same workload. ``roofline.traffic`` is the HBM traffic per call read by
-rocprofv3 counters (FETCH_SIZE + WRITE_SIZE, scaled by a plain copy of known
-size), taken from the profile summary under ``profiles/``; it is null when the
-kernel sources have changed since that summary was written.
+Timing protocol (per workload): W eager warm-up steps, then a HIP graph of
+G = max(--steps, 100, sets) steps is captured, replayed once untimed, and
+replayed 7 times more, each replay bracketed by HIP events on the launch
+stream; the figure is the median replay divided by G.
+  * cold: the steps rotate over enough distinct device copies of the inputs
+    to hold at least 640 MB (2.5x the 256 MB MALL), so every step reads its
+    inputs from HBM; the headline value and roofline use this figure;
+  * warm: the same input buffers every step.
 
-``cold`` repeats the timing with the calls rotating over ``--cold-sets``
-distinct copies of the inputs (128 copies of 4.9 MB exceed the 256 MB MALL),
-so that every call reads its inputs from HBM; the headline ``value`` is the
-warm number (the same input buffers every call).
+Prints ONE JSON line. ``roofline`` prices the headline call against HBM
+bandwidth with its algorithmic bytes (q, k, g, v in, o out): the whole call is
+one launch of the one-launch kernel, so the per-call time is that kernel's
+launch duration; ``traffic`` is the HBM traffic per call from the rocprofv3
+counter summary under ``profiles/`` (FETCH_SIZE + WRITE_SIZE, scaled by a plain
+copy of known size), or null when the kernel sources or the schedule differ
+from the ones it was taken on. ``configs`` lists every workload;
+``cpu_baseline`` times the float64 oracle on the host on a bounded sample.
 
 ``--calibrate-copy MB`` only runs a device-to-device copy of that size (the
 reference kernel for the counter scaling) and prints its byte count.
@@ -27,8 +33,10 @@ from __future__ import annotations
 import argparse
 import hashlib
 import json
+import math
 import os
 import re
+import statistics
 import sys
 import time
 
@@ -80,24 +88,23 @@ def schedule_of(wl, path):
                                 s0=s0, want_final=wl.want_final, o_dtype=torch_dtype(wl.odtype), path=path)
 
 
-KERNEL_OF = {"inline": "gla_fused_kernel<..., true> (inline schedule; the whole call is this one launch)",
-             "fused": "gla_fused_kernel<..., false> (fused schedule; the whole call is this one launch)",
+KERNEL_OF = {"inline": "gla_chain_kernel (one launch, inline prefixes: the whole call is this kernel)",
+             "fused": "gla_chain_kernel (one launch, look-back to inclusive states: the whole call is this kernel)",
              "staged": "one gtr_gla_fwd call (summary + scan + output kernels)"}
 
 
 def parse():
     p = argparse.ArgumentParser()
     p.add_argument("--gpus", type=int, default=1)
-    p.add_argument("--steps", type=int, default=500)
-    p.add_argument("--warmup", type=int, default=50)
-    p.add_argument("--workload", default="kbench", choices=sorted(WORKLOADS))
+    p.add_argument("--steps", type=int, default=100, help="steps per timed graph (at least 100 are captured)")
+    p.add_argument("--warmup", type=int, default=20)
     p.add_argument("--path", default="auto", choices=["auto", "fused", "staged", "inline"])
+    p.add_argument("--only", default=None, help="time only these workloads (comma-separated labels)")
     p.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
+    p.add_argument("--no-cold", action="store_true", help="skip the cold legs")
     p.add_argument("--cpu-seconds", type=float, default=10.0)
-    p.add_argument("--detail", action="store_true", help="also time the other workloads")
-    p.add_argument("--cold-sets", type=int, default=128,
-                   help="also time the calls rotating over this many distinct input sets (more bytes than the "
-                        "256 MB MALL holds, so every call reads HBM); 0 skips it")
+    p.add_argument("--detail", action="store_true",
+                   help="also time the paper's operator shapes, the fusions and the Spatial SwiGLU")
     p.add_argument("--peaks", action="store_true",
                    help="only measure the achievable copy bandwidth and fp16 GEMM rate and print them")
     p.add_argument("--swiglu-only", action="store_true",
@@ -123,10 +130,24 @@ def calibrate_copy(mb, steps):
                       "GBps_read_plus_write": 2 * n * steps / el / 1e9}), flush=True)
 
 
-def setup(wl, path, scan=None, sets=1, fusions=False):
-    """One call of the workload; ``fusions``: g holds gate logits (tau = 16) and
-    the output-gate epilogue (fp16/bf16 gate in the input dtype, RMSNorm weight)
-    is fused into the store."""
+COLD_BYTES = 640e6  # input bytes the cold leg rotates over: 2.5x the 256 MB MALL
+REPLAYS = 7          # timed replays of each graph; the median is reported
+
+
+def input_bytes(wl) -> float:
+    """Bytes of one input set (q, k, v, g and S0)."""
+    es = torch.tensor([], dtype=torch_dtype(wl.dtype)).element_size()
+    b = wl.B * wl.heads * wl.L * (3 * wl.dk + wl.dv) * es
+    if wl.s0_std is not None:
+        b += wl.B * wl.heads * wl.dk * wl.dv * 4
+    return float(b)
+
+
+def setup(wl, path, scans=None, chunk=None, sets=1, fusions=False):
+    """A step of the workload (one call per scan direction); call i reads input
+    set i % sets. ``fusions``: g holds gate logits (tau = 16) and the
+    output-gate epilogue (gate in the input dtype, RMSNorm weight) is fused
+    into the store."""
     inp = make_inputs(wl)
     dev = torch.device("cuda")
     extra = {}
@@ -137,22 +158,65 @@ def setup(wl, path, scan=None, sets=1, fusions=False):
                      out_gate=torch.randn((wl.B, wl.heads, wl.L, wl.dv), generator=rng).to(
                          torch_dtype(wl.dtype)).to(dev),
                      norm_weight=torch.rand(wl.dv, generator=rng).to(dev) + 0.5)
-    # `sets` distinct device copies of the inputs; call i reads copy i % sets
-    copies = [tuple(inp[n].to(dev) for n in ("q", "k", "v", "g")) for _ in range(sets)]
-    s0 = None if inp["s0"] is None else inp["s0"].to(dev)
+    first = {n: (None if inp[n] is None else inp[n].to(dev)) for n in ("q", "k", "v", "g", "s0")}
+    # distinct device copies (distinct addresses) of the same values
+    copies = [first] + [{n: (None if t is None else t.clone()) for n, t in first.items()} for _ in range(sets - 1)]
     o = torch.empty((wl.B, wl.heads, wl.L, wl.dv), dtype=torch_dtype(wl.odtype), device=dev)
     sf = torch.empty((wl.B, wl.heads, wl.dk, wl.dv), dtype=torch.float32, device=dev) if wl.want_final else None
     ws = gtr.Workspace(dev)
-    scans = [scan] if scan else list(wl.scans)
+    scans = list(scans or wl.scans)
+    C = chunk or wl.chunk
 
     def step(i=0):
-        q, k, v, g = copies[i % sets]
-        gtr.gtr_gla_fwd(q, k, v, g, H=wl.H, W=wl.W, scale=wl.scale, chunk=wl.chunk, scan=scans[i % len(scans)],
-                        s0=s0, out=o, s_final=sf, path=path, workspace=ws, **extra)
+        x = copies[i % sets]
+        for scan in scans:
+            gtr.gtr_gla_fwd(x["q"], x["k"], x["v"], x["g"], H=wl.H, W=wl.W, scale=wl.scale, chunk=C, scan=scan,
+                            s0=x["s0"], out=o, s_final=sf, path=path, workspace=ws, **extra)
 
     step()  # sizes and zero-fills the workspace outside any capture
     torch.cuda.synchronize()
     return step
+
+
+def time_graph(step, steps, warmup, replays=REPLAYS):
+    """Median seconds per step over `replays` timed replays of a graph of
+    `steps` steps (HIP events on the current stream around each replay)."""
+    for i in range(warmup):
+        step(i)
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        for i in range(steps):
+            step(i)
+    graph.replay()  # untimed
+    torch.cuda.synchronize()
+    times = []
+    for _ in range(replays):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        graph.replay()
+        e1.record()
+        torch.cuda.synchronize()
+        times.append(e0.elapsed_time(e1) / 1000.0 / steps)
+    del graph
+    torch.cuda.synchronize()
+    return statistics.median(times), times
+
+
+def measure(wl, path, steps, warmup, scans=None, chunk=None, cold=True):
+    """(warm, cold) median seconds per step and the cold leg's set count."""
+    st = setup(wl, path, scans=scans, chunk=chunk)
+    warm, _ = time_graph(st, max(steps, 100), warmup)
+    del st
+    res = {"warm": warm, "cold": None, "sets": 0}
+    if cold:
+        sets = max(2, math.ceil(COLD_BYTES / input_bytes(wl)))
+        st = setup(wl, path, scans=scans, chunk=chunk, sets=sets)
+        res["cold"], _ = time_graph(st, max(steps, 100, sets), warmup)
+        res["sets"] = sets
+        del st
+    torch.cuda.empty_cache()
+    return res
 
 
 def swiglu_detail():
@@ -176,31 +240,12 @@ def swiglu_detail():
 
         step()
         torch.cuda.synchronize()
-        t = time_graph(step, 100, 10) / 100
+        t, _ = time_graph(step, 100, 10)
         flops = 2.0 * M * d * 2 * h + 2.0 * M * h * d + 18.0 * M * h
         nbytes = M * d * 2 * 2 + 3 * h * d * 2 + h * 40
         res[name] = {"us_per_call": t * 1e6, "tflops": flops / t / 1e12,
                      "mfma_frac": flops / t / 1e12 / MFMA_F16_PEAK_TFLOPS, "alg_GBps": nbytes / t / 1e9}
     return res
-
-
-def time_graph(step, steps, warmup):
-    for i in range(warmup):
-        step(i)
-    torch.cuda.synchronize()
-    graph = torch.cuda.CUDAGraph()
-    with torch.cuda.graph(graph):
-        for i in range(steps):
-            step(i)
-    graph.replay()  # warm replay
-    torch.cuda.synchronize()
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
-    e0.record()
-    graph.replay()
-    e1.record()
-    torch.cuda.synchronize()
-    return e0.elapsed_time(e1) / 1000.0  # seconds for `steps` calls
 
 
 def cpu_model() -> str:
@@ -274,6 +319,78 @@ def measured_peaks():
             "fp16_gemm_8192_TFLOPs": mm_tflops, "gemm_frac_of_2500": mm_tflops / MFMA_F16_PEAK_TFLOPS}
 
 
+# The five workloads of the benchmark: (label, workload, scans per step, chunk).
+CONFIGS = [
+    ("1 tiny", "tiny", None, None),
+    ("2 kbench", "kbench", None, None),
+    ("3 directions", "directions", ("row", "col", "row_rev", "col_rev"), None),
+    ("4 highres C=32", "highres", None, 32),
+    ("4 highres C=64", "highres", None, 64),
+    ("4 highres C=128", "highres", None, 128),
+    ("5 batched", "batched", None, None),
+]
+HEADLINE = "2 kbench"
+
+
+def describe(wl, scans, chunk) -> str:
+    sc = "/".join(scans) if scans else wl.scans[0]
+    extra = ", S0 in, S_final out" if wl.s0_std is not None else ""
+    return (f"{wl.name}: B={wl.B} heads={wl.heads} grid {wl.H}x{wl.W} (L={wl.L}) d_k={wl.dk} d_v={wl.dv} "
+            f"{wl.dtype} in / {wl.odtype} out, chunk {chunk or wl.chunk}, {sc} scan{extra}")
+
+
+def config_entry(label, name, scans, chunk, path, steps, warmup, cold):
+    wl = WORKLOADS[name]
+    if chunk is not None:
+        wl = wl.with_(chunk=chunk)
+    calls = len(scans) if scans else 1
+    r = measure(wl, path, steps, warmup, scans=scans, chunk=chunk, cold=cold)
+    t = r["cold"] if r["cold"] is not None else r["warm"]
+    per_call = t / calls
+    nbytes, flops = algorithmic_bytes(wl), algorithmic_flops(wl)
+    e = {"label": label, "workload": describe(wl, scans, chunk), "schedule": schedule_of(wl, path),
+         "value_parts": value_parts_of(wl, path), "calls_per_step": calls,
+         "us_per_step": t * 1e6, "us_per_call": per_call * 1e6,
+         "us_per_call_warm": r["warm"] / calls * 1e6,
+         "tokens_per_s": wl.B * wl.L * calls / t, "tflops": flops / per_call / 1e12,
+         "alg_bytes_per_call": nbytes, "achieved_GBps": nbytes / per_call / 1e9,
+         "hbm_frac": nbytes / per_call / 1e9 / HBM_PEAK_GBS,
+         "hbm_frac_warm": nbytes / (r["warm"] / calls) / 1e9 / HBM_PEAK_GBS,
+         "timing": "cold" if r["cold"] is not None else "warm"}
+    if r["cold"] is not None:
+        e["cold_sets"] = r["sets"]
+        e["cold_input_MB"] = r["sets"] * input_bytes(wl) / 1e6
+    return wl, e
+
+
+def value_parts_of(wl, path):
+    dev = torch.device("cuda")
+    mk = lambda d: torch.empty((wl.B, wl.heads, wl.L, d), dtype=torch_dtype(wl.dtype), device=dev)
+    s0 = torch.empty((wl.B, wl.heads, wl.dk, wl.dv), device=dev) if wl.s0_std is not None else None
+    return gtr.gtr_gla_value_parts(mk(wl.dk), mk(wl.dk), mk(wl.dv), mk(wl.dk), H=wl.H, W=wl.W, chunk=wl.chunk,
+                                   s0=s0, want_final=wl.want_final, o_dtype=torch_dtype(wl.odtype), path=path)
+
+
+def detail(path, steps, warmup):
+    """The paper's operator shapes, the fusions and the Spatial SwiGLU (warm)."""
+    det = {}
+    for name in ("op256", "op1600", "op16k"):
+        wl = WORKLOADS[name]
+        t, _ = time_graph(setup(wl, path), max(steps, 100), warmup)
+        det[name] = {"us_per_call": t * 1e6, "tokens_per_s": wl.B * wl.L / t, "schedule": schedule_of(wl, path),
+                     "hbm_frac": algorithmic_bytes(wl) / t / 1e9 / HBM_PEAK_GBS}
+    # the same call with gate fusion and the output-gate epilogue (+ the gate input's bytes)
+    for name in ("kbench", "op1600", "batched"):
+        wl = WORKLOADS[name]
+        t, _ = time_graph(setup(wl, path, fusions=True), max(steps, 100), warmup)
+        b2 = algorithmic_bytes(wl) + wl.B * wl.heads * wl.L * wl.dv * \
+            torch.tensor([], dtype=torch_dtype(wl.dtype)).element_size() + wl.dv * 4
+        det[f"{name}+fusions"] = {"us_per_call": t * 1e6, "tokens_per_s": wl.B * wl.L / t,
+                                  "hbm_frac": b2 / t / 1e9 / HBM_PEAK_GBS}
+    det.update(swiglu_detail())
+    return det
+
+
 def main():
     a = parse()
     if a.gpus != 1:
@@ -293,73 +410,55 @@ def main():
     if a.peaks:
         print(json.dumps(measured_peaks()), flush=True)
         return
-    wl = WORKLOADS[a.workload]
-    sched = schedule_of(wl, a.path)
-    step = setup(wl, a.path, scan=wl.scans[0])
-    secs = time_graph(step, a.steps, a.warmup)
-    per_call = secs / a.steps
-    tok_s = wl.B * wl.heads * wl.L / per_call  # token-heads per second
-    tokens_s = wl.B * wl.L / per_call          # grid tokens per second (all heads)
-    flops = algorithmic_flops(wl)
-    nbytes = algorithmic_bytes(wl)
-    achieved = nbytes / per_call / 1e9
+    only = set(x.strip() for x in a.only.split(",")) if a.only else None
+    entries, head = [], None
+    for label, name, scans, chunk in CONFIGS:
+        if only and label not in only and name not in only:
+            continue
+        wl, e = config_entry(label, name, scans, chunk, a.path, a.steps, a.warmup, cold=not a.no_cold)
+        entries.append(e)
+        print(f"# {label}: {e['us_per_call']:.2f} us per call ({e['timing']}), {e['us_per_call_warm']:.2f} warm, "
+              f"{e['hbm_frac'] * 100:.1f}% of HBM, schedule {e['schedule']}", file=sys.stderr, flush=True)
+        if label == HEADLINE:
+            head = (wl, e)
+    if head is None:
+        print(json.dumps({"configs": entries}), flush=True)
+        return
+    wl, e = head
+    per_call = e["us_per_call"] * 1e-6
+    G = max(a.steps, 100, e.get("cold_sets", 0))
     out = {
         "metric": "GLA fwd tokens/s and TFLOP/s at 40x40 tokens; % of MFMA/HBM roofline",
-        "value": tokens_s,
+        "value": e["tokens_per_s"],
         "unit": "tokens/s",
         "n_gpus": 1,
-        "steps": a.steps,
+        "steps": G,
         "warmup": a.warmup,
         "ms_per_step": per_call * 1e3,
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "f16" if wl.dtype != "f32" else "f32",
+        "dtype": "f16",
         "data": "synthetic",
-        "config": {"workload": f"{wl.name}: B={wl.B} heads={wl.heads} grid {wl.H}x{wl.W} (L={wl.L}) "
-                               f"d_k=d_v={wl.dk} {wl.dtype} in / {wl.odtype} out, chunk {wl.chunk}, "
-                               f"{wl.scans[0]} scan", "path": a.path, "timing": "HIP graph of K calls"},
-        "token_heads_per_s": tok_s,
-        "tflops": flops / per_call / 1e12,
-        "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": achieved / HBM_PEAK_GBS,
-                     "traffic": stored_traffic(sched) if a.workload == "kbench" else None,
-                     "kernel": KERNEL_OF[sched], "schedule": sched,
-                     "alg_bytes_per_call": nbytes, "us_per_call": per_call * 1e6,
-                     "timing": "HIP events around a graph of K calls on the launch stream, divided by K",
+        "config": {"workload": e["workload"], "path": a.path,
+                   "timing": f"median of {REPLAYS} replays of a {G}-step HIP graph, HIP events on the launch stream; "
+                             f"cold: the steps rotate over {e.get('cold_sets')} input sets "
+                             f"({e.get('cold_input_MB', 0):.0f} MB, more than the 256 MB MALL)"},
+        "token_heads_per_s": wl.B * wl.heads * wl.L / per_call,
+        "tflops": e["tflops"],
+        "roofline": {"bound": "hbm", "achieved": e["achieved_GBps"], "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": e["hbm_frac"], "frac_warm": e["hbm_frac_warm"],
+                     "traffic": stored_traffic(e["schedule"]),
+                     "kernel": KERNEL_OF[e["schedule"]], "schedule": e["schedule"],
+                     "alg_bytes_per_call": e["alg_bytes_per_call"], "us_per_call": e["us_per_call"],
+                     "us_per_call_warm": e["us_per_call_warm"],
+                     "timing": "cold leg: algorithmic bytes per call / median per-call time",
                      "kernel_source_hash": kernel_source_hash(),
-                     "mfma_frac": flops / per_call / 1e12 / MFMA_F16_PEAK_TFLOPS},
+                     "mfma_frac": e["tflops"] / MFMA_F16_PEAK_TFLOPS},
+        "configs": entries,
     }
-    if a.cold_sets > 1:
-        st = setup(wl, a.path, scan=wl.scans[0], sets=a.cold_sets)
-        cs = time_graph(st, a.steps, a.warmup) / a.steps
-        out["cold"] = {"sets": a.cold_sets, "set_bytes": nbytes - wl.B * wl.heads * wl.L * wl.dv *
-                       torch.tensor([], dtype=torch_dtype(wl.odtype)).element_size(),
-                       "us_per_call": cs * 1e6, "tokens_per_s": wl.B * wl.L / cs,
-                       "achieved_GBps": nbytes / cs / 1e9, "frac": nbytes / cs / 1e9 / HBM_PEAK_GBS}
     if a.detail:
-        det = {}
-        for name in ("directions", "highres", "batched", "op256", "op1600", "op16k"):
-            w2 = WORKLOADS[name]
-            for scan in w2.scans:
-                st = setup(w2, a.path, scan=scan)
-                s2 = time_graph(st, 100, 10) / 100
-                det[f"{name}/{scan}"] = {"us_per_call": s2 * 1e6,
-                                         "tokens_per_s": w2.B * w2.L / s2,
-                                         "GBps": algorithmic_bytes(w2) / s2 / 1e9,
-                                         "hbm_frac": algorithmic_bytes(w2) / s2 / 1e9 / HBM_PEAK_GBS}
-        # the same call with gate fusion and the output-gate epilogue (+ the gate input's bytes)
-        for name in ("kbench", "op1600", "batched"):
-            w2 = WORKLOADS[name]
-            st = setup(w2, a.path, scan=w2.scans[0], fusions=True)
-            s2 = time_graph(st, 100, 10) / 100
-            b2 = algorithmic_bytes(w2) + w2.B * w2.heads * w2.L * w2.dv * \
-                torch.tensor([], dtype=torch_dtype(w2.dtype)).element_size() + w2.dv * 4
-            det[f"{name}+fusions"] = {"us_per_call": s2 * 1e6, "tokens_per_s": w2.B * w2.L / s2,
-                                      "GBps": b2 / s2 / 1e9, "hbm_frac": b2 / s2 / 1e9 / HBM_PEAK_GBS}
-        out["detail"] = det
-    if a.detail:
-        out["detail"].update(swiglu_detail())
+        out["detail"] = detail(a.path, a.steps, a.warmup)
     if not a.no_cpu:
         out["cpu_baseline"] = cpu_baseline(wl, a.cpu_seconds)
     print(json.dumps(out), flush=True)

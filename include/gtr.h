@@ -26,7 +26,10 @@
  *   - Kernels are enqueued on `stream`; results are valid once the stream has
  *     completed the work. A launch failure reported by the runtime maps to
  *     GTR_ERR_HIP.
- *   - All calls are thread-safe; there is no global mutable state.
+ *   - All calls are thread-safe. The only state the library keeps between
+ *     calls is a table of occupancy answers per (device, kernel), filled on
+ *     first use under a lock and never changed afterwards; everything a call
+ *     writes is in the caller's buffers.
  */
 #ifndef GTR_H_
 #define GTR_H_
@@ -97,20 +100,25 @@ typedef enum {
 /* Execution schedule of gtr_gla_fwd (all give the same result up to rounding;
  * the length-aware dispatch of the paper's operator appendix). */
 typedef enum {
-  GTR_PATH_AUTO = 0,   /* the library picks: up to 8 sequences, INLINE while the
-                          summaries of a sequence take at most 256 KB (nchunks * dk *
-                          dv elements, fp16 for 16-bit inputs, float32 otherwise),
-                          else FUSED if every chunk of a sequence can be resident on
-                          one XCD; otherwise (and for more than 8 sequences) STAGED.
-                          gtr_gla_schedule reports the choice.                        */
-  GTR_PATH_FUSED = 1,  /* one launch: summaries, boundary-state scan split over the
-                          work-groups of a sequence, outputs                          */
-  GTR_PATH_STAGED = 2, /* three launches: summaries, boundary-state scan, outputs      */
-  GTR_PATH_INLINE = 3  /* one launch: summaries, then every chunk rebuilds its own
-                          boundary state from the summaries before it (short
-                          sequences). With d_v = 64, no output gate and at most
-                          one work-group per CU after doubling, each chunk's value
-                          columns are split over two work-groups.                     */
+  GTR_PATH_AUTO = 0,   /* the library picks: INLINE for sequences of at most 32
+                          chunks, FUSED for up to 256 chunks, STAGED beyond (or
+                          for more than 1024 sequences). gtr_gla_schedule reports
+                          the choice.                                               */
+  GTR_PATH_FUSED = 1,  /* one launch, boundary states by look-back: each chunk
+                          hands over its summary, finds S_[c] from the summaries
+                          of the chunks before it back to the nearest chunk that
+                          has handed over its inclusive state S_[j+1], and hands
+                          over S_[c+1] in turn (the scan co-runs with the
+                          outputs). At most 1024 sequences of 256 chunks.          */
+  GTR_PATH_STAGED = 2, /* three launches: summaries, boundary-state scan, outputs;
+                          no waits between work-groups                             */
+  GTR_PATH_INLINE = 3  /* one launch, each chunk rebuilds its boundary state from
+                          the summaries of all chunks before it (the paper's
+                          inline prefixes for short sequences). Limits as FUSED.
+                          With d_v = 64, no output gate and at most one
+                          work-group per CU after doubling, the value columns of
+                          each chunk are split over two work-groups (both
+                          one-launch paths).                                       */
 } gtr_path;
 
 /*
@@ -145,18 +153,34 @@ typedef enum {
  *        out_gate must not overlap o.
  * workspace, workspace_bytes : device scratch owned by the caller, at least
  *        gtr_gla_workspace_size(args) bytes, 256-byte aligned, and zero-filled
- *        before its first use (gtr_gla_workspace_init). The synchronisation
- *        words of the one-launch schedules sit in a fixed region that no part
- *        of any call's workspace overlaps, and every completed call leaves them
+ *        before its first use (gtr_gla_workspace_init). Its first 32-bit word
+ *        is the fault word (below). The synchronisation words of the one-launch
+ *        schedules sit in regions of fixed place and size that no other part of
+ *        any call's workspace overlaps, and every completed call leaves them
  *        zeroed again, so one workspace (large enough for each) serves any
  *        number of calls of any shapes on one stream. Calls that overlap in
- *        time must not share a workspace. The one-launch schedules take at
- *        most 1024 sequences (B * heads).
+ *        time (two streams, for instance) must not share a workspace.
+ * spin_limit : polls a one-launch work-group makes while it waits for the
+ *        chunks before it, before it gives up (0: the library default, about a
+ *        second). A work-group that gives up sets bit 0 of the fault word and
+ *        writes NaN into its output rows, into the state it hands over (so
+ *        every chunk after it is NaN too) and into S_final where it writes it;
+ *        every work-group still exits normally. Outputs that are not NaN are
+ *        valid. A small limit forces the condition (tests).
+ *
+ * Fault word (stream-ordered status, sticky until gtr_gla_workspace_init):
+ *   bit 0  a bounded wait ran out (see spin_limit);
+ *   bit 1  a bf16 q, k or v value lies outside the fp16 range (|x| > 65504):
+ *          the work-groups that read it write NaN in its chunk's output rows
+ *          (and, in the one-launch schedules, in everything after it).
+ * Read it with gtr_gla_workspace_fault after the stream has completed the call.
  *
  * Numerics: float32 accumulation throughout. With fp16/bf16 inputs the matrix
- * products use fp16 operands (every rescaled operand is bounded by |q| or |k|,
- * see the design notes), so bf16 inputs must also be finite in fp16
- * (|x| < 65504). With float32 inputs every product is float32.
+ * products use fp16 operands: the rescaled q and k are bounded by |q| and |k|,
+ * and the score tile, the chunk summaries and the boundary states are scaled
+ * by powers of two before they are rounded to fp16, so no intermediate
+ * overflows for inputs within the fp16 range (bf16 inputs are checked, above).
+ * With float32 inputs every product is float32. Inputs must be finite.
  */
 typedef struct {
   const void* q;
@@ -184,6 +208,7 @@ typedef struct {
   gtr_dtype out_gate_dtype; /* qkv_dtype or GTR_F32                                   */
   float norm_eps;           /* RMSNorm epsilon (> 0) of the epilogue                  */
   const float* norm_weight; /* [dv] RMSNorm weight, or NULL for ones                  */
+  uint32_t spin_limit;      /* bounded-wait polls of the one-launch schedules; 0 = default */
 } gtr_gla_args;
 
 /* Bytes of workspace gtr_gla_fwd needs for these arguments (host only, no HIP
@@ -270,10 +295,12 @@ typedef struct {
 size_t gtr_spatial_swiglu_workspace_size(const gtr_swiglu_args* args);
 gtr_status gtr_spatial_swiglu(const gtr_swiglu_args* args, hipStream_t stream);
 
-/* Nonzero if a fused-path call on this workspace gave up waiting for the other
- * chunks of a sequence (a bounded wait ran out); the output of that call is not
- * valid. Reads the flag with a blocking device-to-host copy - a diagnostic for
- * tests, not for the hot path. Returns -1 on a HIP error. */
+/* The fault word of a workspace (bits as described under gtr_gla_args: 1 = a
+ * bounded wait ran out, 2 = a bf16 input outside the fp16 range), 0 if every
+ * call since the last gtr_gla_workspace_init was clean. Reads it with a
+ * blocking device-to-host copy, so call it after the stream has completed the
+ * calls of interest - a check for tests and for callers that can afford a
+ * synchronisation, not for the hot path. Returns -1 on a HIP error. */
 int gtr_gla_workspace_fault(const void* workspace, size_t bytes);
 
 const char* gtr_status_string(gtr_status status);

@@ -63,6 +63,7 @@ class GlaArgs(ctypes.Structure):
         ("g_kind", ctypes.c_int), ("gate_tau", ctypes.c_float),
         ("out_gate", ctypes.c_void_p), ("out_gate_dtype", ctypes.c_int),
         ("norm_eps", ctypes.c_float), ("norm_weight", ctypes.c_void_p),
+        ("spin_limit", ctypes.c_uint32),
     ]
 
 
@@ -137,6 +138,7 @@ def gtr_scan_permute(src: torch.Tensor, H: int, W: int, scan: str, inverse: bool
     if src.dim() < 2 or src.shape[-2] != H * W:
         raise ValueError("src must be [..., H*W, E]")
     dst = torch.empty_like(src) if out is None else out
+    _check("out", dst, tuple(src.shape), (src.dtype,), src.device)
     outer = src.numel() // (src.shape[-2] * src.shape[-1]) if src.numel() else 0
     st = load().gtr_scan_permute(_ptr(src), _ptr(dst), outer, H, W, src.shape[-1], _DT[src.dtype],
                                  SCANS[scan], int(bool(inverse)), _stream_ptr(stream))
@@ -150,7 +152,7 @@ GATE_LOG_DECAY, GATE_LOGITS = 0, 1
 
 def make_args(q, k, v, g, *, H, W, scale, chunk=64, scan="row", s0=None, o=None, s_final=None,
               path="auto", workspace=None, gate_tau=None, out_gate=None, norm_weight=None,
-              norm_eps=1e-5) -> GlaArgs:
+              norm_eps=1e-5, spin_limit=0) -> GlaArgs:
     B, heads, L, dk = q.shape
     a = GlaArgs()
     a.q, a.k, a.v, a.g = _ptr(q), _ptr(k), _ptr(v), _ptr(g)
@@ -163,6 +165,7 @@ def make_args(q, k, v, g, *, H, W, scale, chunk=64, scan="row", s0=None, o=None,
     a.scale = float(scale)
     a.scan = SCANS[scan]
     a.path = PATHS[path]
+    a.spin_limit = int(spin_limit)
     if workspace is not None:
         a.workspace = workspace.data_ptr()
         a.workspace_bytes = workspace.numel()
@@ -188,26 +191,59 @@ def gtr_gla_workspace_init(ws: torch.Tensor, stream=None) -> None:
 
 
 def gtr_gla_workspace_fault(ws: torch.Tensor) -> int:
+    """Fault bits of the calls on ``ws`` since its initialisation (1: a bounded
+    wait ran out, 2: a bf16 input outside the fp16 range); blocks until the
+    device is idle."""
     return int(load().gtr_gla_workspace_fault(_ptr(ws), ws.numel()))
 
 
 class Workspace:
-    """A growable, zero-initialised device workspace for :func:`gtr_gla_fwd`."""
+    """A growable, zero-initialised device workspace for :func:`gtr_gla_fwd`,
+    used on one stream: it is allocated and zero-filled on that stream, so
+    the caching allocator never hands its memory to another stream while a
+    call on this one may still use it."""
 
-    def __init__(self, device=None):
+    def __init__(self, device=None, stream=None):
         self.device = torch.device("cuda") if device is None else torch.device(device)
+        self.stream = stream
         self.buf: Optional[torch.Tensor] = None
 
     def get(self, nbytes: int, stream=None) -> torch.Tensor:
         if self.buf is None or self.buf.numel() < nbytes:
+            s = stream if stream is not None else (self.stream or torch.cuda.current_stream(self.device))
             n = max(256, (nbytes + 255) // 256 * 256)
-            # 256-byte aligned: torch's caching allocator hands out 512-byte aligned blocks
-            self.buf = torch.empty(n, dtype=torch.uint8, device=self.device)
-            gtr_gla_workspace_init(self.buf, stream)
+            with torch.cuda.stream(s):
+                # 256-byte aligned: torch's caching allocator hands out 512-byte aligned blocks
+                self.buf = torch.empty(n, dtype=torch.uint8, device=self.device)
+                gtr_gla_workspace_init(self.buf, s)
         return self.buf
 
 
+# default workspaces, one per (device, stream): calls on different streams
+# never share one
 _default_ws: dict = {}
+
+
+def _default_workspace(kind: str, device: torch.device, stream) -> Workspace:
+    s = stream if stream is not None else torch.cuda.current_stream(device)
+    key = (kind, device, int(s.cuda_stream))
+    ws = _default_ws.get(key)
+    if ws is None:
+        ws = _default_ws[key] = Workspace(device, s)
+    return ws
+
+
+def _check(name: str, t: Optional[torch.Tensor], shape, dtypes, device) -> None:
+    if t is None:
+        return
+    if not t.is_cuda or t.device != device:
+        raise ValueError(f"{name} must be on {device}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{name} has shape {tuple(t.shape)}, expected {tuple(shape)}")
+    if t.dtype not in dtypes:
+        raise ValueError(f"{name} has dtype {t.dtype}, expected one of {list(dtypes)}")
 
 
 def gtr_gla_fwd(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, g: torch.Tensor, *, H: int, W: int,
@@ -217,42 +253,60 @@ def gtr_gla_fwd(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, g: torch.Tens
                 out: Optional[torch.Tensor] = None, s_final: Optional[torch.Tensor] = None,
                 workspace: Optional[Workspace] = None, stream=None, gate_tau: Optional[float] = None,
                 out_gate: Optional[torch.Tensor] = None, norm_weight: Optional[torch.Tensor] = None,
-                norm_eps: float = 1e-5):
+                norm_eps: float = 1e-5, spin_limit: int = 0, check: bool = False):
     """Chunkwise GLA forward. Inputs [B, heads, H*W, d] in spatial order on the GPU.
 
     ``gate_tau``: g holds gate logits a, log gamma = logsigmoid(a) / gate_tau.
     ``out_gate`` ([B, heads, H*W, dv], x W_r) with optional ``norm_weight`` ([dv],
     float32): the output is u = SiLU(out_gate) * RMSNorm(o) instead of o.
+    ``spin_limit``: polls of a one-launch wait before it gives up (0: default).
+    ``check``: synchronise and raise if the workspace's fault word is set.
     Returns ``(o, s_final)``; ``s_final`` is None unless requested.
     """
-    extra = [("out_gate", out_gate)] if out_gate is not None else []
-    if norm_weight is not None:
-        extra.append(("norm_weight", norm_weight))
-    for name, t in [("q", q), ("k", k), ("v", v), ("g", g)] + extra:
-        if not t.is_cuda or not t.is_contiguous():
-            raise ValueError(f"{name} must be a contiguous device tensor")
+    if q.dim() != 4:
+        raise ValueError("q must be [B, heads, H*W, d_k]")
+    B, heads, L, dk = q.shape
+    dv = v.shape[-1] if v.dim() == 4 else -1
+    dev = q.device
+    if L != H * W:
+        raise ValueError(f"q has {L} tokens, H*W = {H * W}")
+    if q.dtype not in _DT:
+        raise ValueError(f"unsupported dtype {q.dtype}")
+    qdt = (q.dtype,)
+    _check("q", q, (B, heads, L, dk), qdt, dev)
+    _check("k", k, (B, heads, L, dk), qdt, dev)
+    _check("v", v, (B, heads, L, dv), qdt, dev)
+    _check("g", g, (B, heads, L, dk), (q.dtype, torch.float32), dev)
+    _check("s0", s0, (B, heads, dk, dv), (torch.float32,), dev)
+    _check("out_gate", out_gate, (B, heads, L, dv), (q.dtype, torch.float32), dev)
+    _check("norm_weight", norm_weight, (dv,), (torch.float32,), dev)
     if scale is None:
-        scale = q.shape[-1] ** -0.5
-    B, heads, L, _ = q.shape
-    odt = o_dtype or q.dtype
-    o = out if out is not None else torch.empty((B, heads, L, v.shape[-1]), dtype=odt, device=q.device)
+        scale = dk ** -0.5
+    odt = o_dtype or (out.dtype if out is not None else q.dtype)
+    o = out if out is not None else torch.empty((B, heads, L, dv), dtype=odt, device=dev)
+    _check("out", o, (B, heads, L, dv), (q.dtype, torch.float32), dev)
     sf = s_final
     if want_final and sf is None:
-        sf = torch.empty((B, heads, q.shape[-1], v.shape[-1]), dtype=torch.float32, device=q.device)
+        sf = torch.empty((B, heads, dk, dv), dtype=torch.float32, device=dev)
+    _check("s_final", sf, (B, heads, dk, dv), (torch.float32,), dev)
     args = make_args(q, k, v, g, H=H, W=W, scale=scale, chunk=chunk, scan=scan, s0=s0, o=o,
                      s_final=sf, path=path, gate_tau=gate_tau, out_gate=out_gate,
-                     norm_weight=norm_weight, norm_eps=norm_eps)
+                     norm_weight=norm_weight, norm_eps=norm_eps, spin_limit=spin_limit)
     need = gtr_gla_workspace_size(args)
     if need == 0:
         raise GtrError("gtr_gla_workspace_size", 2)
     if workspace is None:
-        workspace = _default_ws.setdefault(q.device, Workspace(q.device))
+        workspace = _default_workspace("gla", dev, stream)
     buf = workspace.get(need, stream)
     args.workspace = buf.data_ptr()
     args.workspace_bytes = buf.numel()
     st = load().gtr_gla_fwd(ctypes.byref(args), _stream_ptr(stream))
     if st:
         raise GtrError("gtr_gla_fwd", st)
+    if check:
+        f = gtr_gla_workspace_fault(buf)
+        if f:
+            raise RuntimeError(f"gtr_gla_fwd: fault word {f} (1: a wait ran out, 2: bf16 input outside fp16 range)")
     return o, sf
 
 
@@ -313,7 +367,7 @@ def gtr_spatial_swiglu(x: torch.Tensor, w_gate: torch.Tensor, w_value: torch.Ten
     if need == 0:
         raise GtrError("gtr_spatial_swiglu_workspace_size", 2)
     if workspace is None:
-        workspace = _default_ws.setdefault(("swiglu", x.device), Workspace(x.device))
+        workspace = _default_workspace("swiglu", x.device, stream)
     buf = workspace.get(need, stream)
     a.workspace, a.workspace_bytes = buf.data_ptr(), buf.numel()
     st = lib.gtr_spatial_swiglu(ctypes.byref(a), _stream_ptr(stream))

@@ -24,32 +24,34 @@
 //     per-element exp(a_r - a_j) on the vector ALUs beyond that.
 //   * The summary uses k_j exp(A_last - A_j) and the readout q_r exp(A_r), both
 //     with exponents <= 0.
-// The factors that depend only on (sub-chunk, dimension) are computed once per
-// dimension (lane d of the wave for dimension d) into a small per-wave table in
-// LDS, from the shared table of sub-chunk totals, and read back by the lanes
-// that use them.
+// Half-precision operands that are not bounded by an input (the score tile P,
+// the summaries U_c, the boundary state S_[c]) are scaled by powers of two
+// before they are rounded to fp16 (per wave, per chunk and per state column
+// respectively), and the scale is undone in float32: exact, and no overflow
+// whatever the magnitudes the inputs' range allows.
 //
 // Schedules:
+//   * one launch (look-back): one work-group per (sequence, chunk). It stores
+//     its summary U_c and d_c and raises its chunk's flag to 1 (aggregate
+//     ready), then finds S_[c] by looking back over the chunks before it,
+//     nearest first: the summary of every chunk whose flag is 1, until it meets
+//     a chunk whose flag is 2 (its inclusive state S_[j+1] is ready) or the start
+//     of the sequence (S_0). With `publish` it then stores S_[c+1] in float32 and
+//     raises its flag to 2, which lets the chunks after it stop there. Without
+//     `publish` every chunk reads all the summaries before it (the paper's
+//     inline-prefix form for short sequences). Every wait is bounded: a
+//     work-group that gives up marks the call's fault word and writes NaN in
+//     place of everything that depends on it.
 //   * staged: summary kernel -> boundary-state scan kernel -> output kernel.
-//   * inline: one launch; each work-group publishes its summary and, once all
-//     summaries of its sequence are in, rebuilds its own boundary state from
-//     the summaries of the chunks before it,
-//       S_[c] = (prod_{m<c} Diag(d_m)) S_0 + sum_{j<c} (prod_{j<m<c} Diag(d_m)) U_j,
-//     which costs c reads of a summary but only one hand-off (short sequences).
-//   * fused : one launch; each work-group owns one (sequence, chunk), publishes
-//     its summary, and the work-groups of one sequence then run the boundary
-//     state scan cooperatively (each takes a slice of the d_k x d_v state) before
-//     reading their own S_[c]. Two per-sequence counters order the phases.
-//     Everything one work-group hands to another (summaries, decays, boundary
-//     states) is written and read with agent-coherent accesses (cache policy
-//     sc1), and a work-group waits for its own stores to be acknowledged
-//     (vmcnt(0)) before it bumps a counter. No release/acquire fence is used: on
-//     this GPU those write back / invalidate the whole L2 of the XCD, which cost
-//     more than the rest of the kernel.
-// Hand-off precision: with fp16/bf16 inputs the summaries U_c and the boundary
-// states S_[c] travel in fp16 (the readout's MFMA operand type); every scan and
-// rebuild accumulates in float32, and S_final is the float32 accumulator. With
-// float32 inputs everything stays float32.
+// Hand-offs between work-groups are agent-coherent (cache policy sc1) stores
+// and loads; a work-group waits for its stores to be acknowledged (vmcnt(0))
+// before it raises a flag. No release/acquire fence is used: on this GPU those
+// write back / invalidate the whole L2 of the XCD.
+// Hand-off precision: with fp16/bf16 inputs the summaries travel in fp16 with a
+// power-of-two scale per chunk; inclusive states travel in float32 (so no
+// rounding accumulates along the chain of chunks); every combination
+// accumulates in float32, and S_final is float32. With float32 inputs
+// everything is float32.
 #include <hip/hip_runtime.h>
 
 #include <mutex>
@@ -63,7 +65,16 @@ namespace gtr {
 
 constexpr float kSpanF16 = 10.f;           // mid-point factors within e^5: fp16 operands
 constexpr float kSpanF32 = 60.f;           // within e^30: float32 operands
-constexpr unsigned kSpinLimit = 1u << 22;  // bounded waits (fused schedule)
+constexpr unsigned kSpinDefault = 1u << 22;  // polls of a bounded wait before it gives up
+constexpr unsigned kFlagSummary = 1u;       // chunk flag: the summary U_c and its record are stored
+constexpr int kFlagInclusive = 8;          // + wave: that wave's pieces of S_[c+1] are stored
+constexpr int kFlagBlock = 16;             // + wave: that wave's pieces of the block prefix are stored
+constexpr float kF16Safe = 65504.f;        // bf16 inputs must stay within the fp16 range
+
+// fault word bits (the workspace's first word; sticky until the workspace is
+// initialised again)
+constexpr unsigned kFaultWait = 1u;   // a bounded wait ran out
+constexpr unsigned kFaultRange = 2u;  // a bf16 input lies outside the fp16 range
 
 struct GlaParams {
   const void* q;
@@ -80,20 +91,28 @@ struct GlaParams {
   int nchunks;
   float scale;
   int scan;
-  float* states;    // [BH][nchunks][DV][DK] float32 U_c^T, then S_[c]^T (float32 inputs only)
-  float* decays;    // [BH][nchunks][DK]
-  unsigned* sync;   // [BH][4]: arrive1, arrive2, leave, spare
+  void* agg;        // [NS][NC][DK][DVp] chunk summaries U_c: fp16 scaled (16-bit inputs) or float32
+  float* rec;       // [NS][NC][RS] per chunk: d_c (DK floats), then the summary's scale
+  float* states;    // [NS][NC][DK][DVp] float32: S_[c+1] (one launch) or S_[c] (staged)
+  unsigned* sync;   // [kSyncSeqs][4]: work-groups done per sequence
+  unsigned* flags;  // [kSyncSeqs][kMaxChainChunks]: bit 0 summary, bit 8 + w inclusive state and bit
+                    // 16 + w block prefix (the pieces of wave w)
+  void* blk;        // [NS][NC][DK][DVp] block prefixes (at the block index), fp16 scaled or float32
+  float* blkrec;    // [NS][NC][DK + 8]: block decay per row, then one scale per wave
   unsigned* fault;  // one word
-  int groups;       // ceil(BH / 8), fused mapping
   int gkind;        // GTR_GATE_LOG_DECAY or GTR_GATE_LOGITS (g holds the gate logits)
   float inv_tau;    // 1 / tau of the gate fusion
   const void* gate;  // output-gate pre-activation [BH][L][DV] (spatial), or null: no epilogue
   const float* nw;   // RMSNorm weight [DV], or null (ones)
   int gatedt;        // dtype of gate
   float eps;         // RMSNorm epsilon
-  unsigned short* states16;  // [BH][nchunks][DV][DK] fp16 U_c^T, then S_[c]^T (16-bit inputs only)
-  int dvp;     // row pitch (elements) of v, o, the gate, S0 and S_final: the full d_v
-  int vparts;  // value split of the inline schedule: work-groups per chunk, each d_v / vparts columns
+  int dvp;      // row pitch (elements) of v, o, the gate, S0 and S_final: the full d_v
+  int vparts;   // value split: work-groups per chunk, each d_v / vparts columns
+  int ns;       // sequences: BH * vparts
+  int desc;     // one launch: chunks in descending order (every work-group resident at once)
+  int publish;  // one launch: store inclusive states
+  int blk_size;  // one launch: chunks per block of the two-level look-back
+  unsigned spin;  // polls of a bounded wait
 };
 
 constexpr int tile_threads(int chunk) { return chunk / 16 * kWave; }
@@ -115,14 +134,29 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, ui
 __device__ __forceinline__ void coh_store4(__amdgpu_buffer_rsrc_t r, uint32_t byte_off, f4 v) {
   __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, v), r, (int)byte_off, 0, kAgentCoherent);
 }
+__device__ __forceinline__ u32x4 coh_load16(__amdgpu_buffer_rsrc_t r, uint32_t byte_off) {
+  return __builtin_amdgcn_raw_buffer_load_b128(r, (int)byte_off, 0, kAgentCoherent);
+}
 __device__ __forceinline__ f4 coh_load4(__amdgpu_buffer_rsrc_t r, uint32_t byte_off) {
-  return __builtin_bit_cast(f4, __builtin_amdgcn_raw_buffer_load_b128(r, (int)byte_off, 0, kAgentCoherent));
+  return __builtin_bit_cast(f4, coh_load16(r, byte_off));
 }
 __device__ __forceinline__ void coh_store1(__amdgpu_buffer_rsrc_t r, uint32_t byte_off, float v) {
   __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(unsigned, v), r, (int)byte_off, 0, kAgentCoherent);
 }
 __device__ __forceinline__ float coh_load1(__amdgpu_buffer_rsrc_t r, uint32_t byte_off) {
   return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(r, (int)byte_off, 0, kAgentCoherent));
+}
+
+// Powers of two from an exponent in [-126, 127] (bit patterns, exact).
+__device__ __forceinline__ float exp2i(int e) { return __builtin_bit_cast(float, (unsigned)(127 + e) << 23); }
+// Exponent e such that m * 2^-e lies in [2^14, 2^15) for a finite m > 0 (0 for
+// m = 0), clamped to [-100, 100]: scaling by 2^-e keeps the largest magnitude
+// of a tile well inside the fp16 range and every other value at full fp16
+// precision unless it is below 2^-24 of the largest.
+__device__ __forceinline__ int fp16_exponent(float m) {
+  const int b = (int)((__builtin_bit_cast(unsigned, m) >> 23) & 0xffu);
+  const int e = m > 0.f ? b - 127 - 14 : 0;
+  return e < -100 ? -100 : (e > 100 ? 100 : e);
 }
 
 // Raw bits of 8 consecutive elements (32 bytes for float32, 16 for 16-bit types).
@@ -200,11 +234,28 @@ __device__ __forceinline__ float log_decay(const GlaParams& P, float x) {
   return (fminf(x, 0.f) - l1p) * P.inv_tau;
 }
 
+// Maximum over the groups of N consecutive lanes (N = 4 or 8) with DPP
+// (quad permutations, then the half-row mirror); every lane gets its group's
+// maximum.
+template <int CTRL>
+__device__ __forceinline__ float dpp_mov(float v) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, v), CTRL, 0xf, 0xf, false));
+}
+template <int N>
+__device__ __forceinline__ float group_max(float x) {
+  x = fmaxf(x, dpp_mov<0xB1>(x));  // quad_perm [1,0,3,2]
+  x = fmaxf(x, dpp_mov<0x4E>(x));  // quad_perm [2,3,0,1]
+  if constexpr (N == 8) x = fmaxf(x, dpp_mov<0x141>(x));  // row_half_mirror: lane i <-> 7 - i
+  return x;
+}
+
 // One chunk of one sequence: C tokens, one wave per 16-token sub-chunk.
-// IN is the dtype of q, k, v (GTR_F32 / GTR_F16 / GTR_BF16).
+// IN is the dtype of q, k, v (GTR_F32 / GTR_F16 / GTR_BF16); DV the value
+// columns of this work-group (d_v, or d_v / 2 under the value split).
 template <int DK, int DV, int C, int IN>
 struct Chunk {
   static constexpr bool F16 = IN != GTR_F32;  // matrix operands: fp16 (else float32)
+  static constexpr int kDK = DK, kDV = DV;
   static constexpr int NW = C / 16;
   static constexpr int NT = NW * kWave;
   static constexpr int KS = DK / 32;
@@ -215,23 +266,37 @@ struct Chunk {
   static constexpr int TP = F16 ? C + 8 : C + 4;    // transposed-tile pitch (elements)
   static constexpr int SP = F16 ? DK + 8 : DK + 4;  // boundary-state tile pitch
   static constexpr int NF = 3 + (NW > 1 ? NW - 1 : 1);  // factor-table rows per wave
+  static constexpr int RS = DK + 4;                 // record stride (floats): d_c, scale, pad
+  // summaries and boundary states are [DK][DV] (key dim i, value column n), in
+  // 8-element pieces: piece p holds row i = p / (DV/8), columns 8 (p % (DV/8)) ..
+  static constexpr int SQ8 = DK * DV / 8;
+  static constexpr int SPER = (SQ8 + NT - 1) / NT;  // pieces per thread
+  static_assert(NT % (DV / 8) == 0, "the pieces of one thread share their columns");
   typedef typename Op<F16>::elem E;
   typedef typename Op<F16>::frag8 F8;
   typedef typename Op<F16>::frag4 F4;
 
-  // Shared memory of the one-launch schedules (every part). The staged
-  // kernels use the subsets below, so that more of their work-groups fit on a
-  // CU at once: the summary kernel has no k rows, state or diagonal staging,
-  // the output kernel no k-hat tile.
+  // Shared memory of the one-launch kernel (every part). The staged kernels
+  // use the subsets below: the summary kernel has no k rows, state or
+  // diagonal staging, the output kernel no k-hat tile.
   struct Smem {
     float buf[C * BUFW];   // k*exp(T-a) rows [C][KP]; later the output tile [C][OP]
-    E kT[DK * TP];         // (k * exp(A_last - A_r))^T  [DK][TP]
+    // three tiles that are never live at once share one region, each phase
+    // separated from the next by a barrier: the k-hat tile (factors, summary),
+    // the exact diagonal staging (intra), the state tile (readout)
+    union {
+      E kT[DK * TP];         // (k * exp(A_last - A_r))^T  [DK][TP]
+      float Pt[NW][16][17];  // exact diagonal blocks, P^T staging
+      E sT[DV * SP];         // S_[c]^T                   [DV][SP]
+    };
     E vT[DV * TP];         // v^T                       [DV][TP]
-    E sT[DV * SP];         // S_[c]^T                   [DV][SP]
     float T[NW][DK];       // sub-chunk totals of g
     float G0[NW][DK];      // g at the first token of each sub-chunk
     float F[NW][NF][DK];   // per-wave factor table (rows kFq, kFk, kFh, kFoff + J)
-    float Pt[NW][16][17];  // exact diagonal blocks, P^T staging
+    float M[NW][2];        // per-wave maxima of |q|,|k| and of |v|
+    float smax[NW];        // per-wave maxima of |S_[c]|
+    float dc[DK];          // d_c
+    int okw[NW];           // per wave: 1 its look-back gave up, 2 it met a NaN state
   };
   struct SmemSummary {
     E kT[DK * TP];
@@ -239,15 +304,19 @@ struct Chunk {
     float T[NW][DK];
     float G0[NW][DK];
     float F[NW][NF][DK];
+    float M[NW][2];
+    float dc[DK];
   };
   struct SmemOutput {
     float buf[C * BUFW];
     E vT[DV * TP];
-    E sT[DV * SP];
+    E sT[DV * SP];  // written before the intra part, read after it: not shared with Pt
     float T[NW][DK];
     float G0[NW][DK];
     float F[NW][NF][DK];
     float Pt[NW][16][17];
+    float M[NW][2];
+    float smax[NW];
   };
   // rows of the factor table of sub-chunk R, per dimension d:
   static constexpr int kFq = 0;    // exp(A before R + g0_R): q readout factor
@@ -263,6 +332,10 @@ struct Chunk {
   float qt[KS][8];  // q * exp(A_r), the readout operand (set by factors())
   float spanmax;    // wave-uniform: widest decay span of this sub-chunk
   float absmax;     // wave-uniform: largest |q|, |k| of this sub-chunk
+  float usc;        // chunk-uniform: U_c is handed over as fp16(U_c / usc) (1 for float32 inputs)
+  float pup;        // wave-uniform: the fp16 score tile holds P / pup
+  float tsc;        // chunk-uniform: the fp16 state tile holds S_[c]^T / tsc
+  bool range_bad;   // chunk-uniform: a bf16 input lies outside the fp16 range
 
   __device__ __forceinline__ int dim(int s, int e) const { return 32 * s + 8 * gq + e; }
 
@@ -281,8 +354,9 @@ struct Chunk {
     return valid ? scan_to_spatial(pos, P.H, P.W, P.scan) : 0;
   }
 
-  // Loads and per-token work. Writes v^T, the sub-chunk totals and (ROWS) the
-  // k*exp(T-a) rows. Ends with a barrier.
+  // Loads and per-token work. Writes v^T, the sub-chunk totals, the per-wave
+  // maxima and (ROWS) the k*exp(T-a) rows. Ends with a barrier, after which the
+  // chunk-uniform summary scale and range flag are set.
   template <bool ROWS, class S>
   __device__ __forceinline__ void load(const GlaParams& P, S& sm, int bh, int c) {
     lanes();
@@ -315,12 +389,16 @@ struct Chunk {
       ld_raw_buf(vr, IN, valid ? ((uint32_t)t * P.dvp + 32 * s + 8 * gq) * ES : kOutOfRange, rv[s]);
 
     // v^T tile
+    float vmax = 0.f;
 #pragma unroll
     for (int s = 0; s < VS; ++s) {
       float x[8];
       cvt_raw(rv[s], IN, x);
 #pragma unroll
-      for (int e = 0; e < 8; ++e) sm.vT[(32 * s + 8 * gq + e) * TP + r] = (E)x[e];
+      for (int e = 0; e < 8; ++e) {
+        vmax = fmaxf(vmax, fabsf(x[e]));
+        sm.vT[(32 * s + 8 * gq + e) * TP + r] = (E)x[e];
+      }
     }
 
     float smax = 0.f, amax = 0.f;
@@ -358,7 +436,21 @@ struct Chunk {
     }
     spanmax = __builtin_bit_cast(float, __builtin_amdgcn_readfirstlane(__builtin_bit_cast(int, wave_max_uniform(smax))));
     absmax = __builtin_bit_cast(float, __builtin_amdgcn_readfirstlane(__builtin_bit_cast(int, wave_max_uniform(amax))));
+    const float vm = __builtin_bit_cast(float, __builtin_amdgcn_readfirstlane(__builtin_bit_cast(int, wave_max_uniform(vmax))));
+    if (lane == 0) {
+      sm.M[w][0] = absmax;
+      sm.M[w][1] = vm;
+    }
     __syncthreads();
+    float am = 0.f, vv = 0.f;
+#pragma unroll
+    for (int K = 0; K < NW; ++K) {
+      am = fmaxf(am, sm.M[K][0]);
+      vv = fmaxf(vv, sm.M[K][1]);
+    }
+    // |U_c| <= C max|k| max|v|; NaN maxima (non-finite inputs) count as out of range
+    range_bad = IN == GTR_BF16 && !(am <= kF16Safe && vv <= kF16Safe);
+    usc = F16 ? exp2i(fp16_exponent((float)C * am * vv)) : 1.f;
   }
 
   // This lane's 8 consecutive dims of factor-table row `row`, for K-step s.
@@ -376,10 +468,11 @@ struct Chunk {
   // Chunk-level factors. Lane d of each wave fills dimension d of its
   // sub-chunk's factor table (one exponential per factor and dimension); the
   // wave then reads back what its lanes need. READOUT: qt = q exp(A_r).
-  // SUMMARY: the transposed k-hat tile and d_c (written by wave 0 through
-  // `dec`, coherent or plain), followed by a barrier.
+  // SUMMARY: the transposed k-hat tile, and the chunk record (d_c and the
+  // summary scale, written by wave 0 through `rec`, coherent or plain) and d_c
+  // in shared memory, followed by a barrier.
   template <bool READOUT, bool SUMMARY, bool COH, class S>
-  __device__ __forceinline__ void factors(S& sm, float* dec) {
+  __device__ __forceinline__ void factors(S& sm, float* rec) {
     if (lane < DK) {
       const int d = lane;
       float tK[NW];
@@ -404,10 +497,15 @@ struct Chunk {
       }
       if (SUMMARY && w == 0) {
         const float dc = gexp<F16>(before + sm.T[0][d] + after);
-        if constexpr (COH)
-          coh_store1(make_rsrc(dec, DK * 4), d * 4, dc);
-        else
-          dec[d] = dc;
+        if constexpr (COH) {
+          const __amdgpu_buffer_rsrc_t rr = make_rsrc(rec, RS * 4);
+          coh_store1(rr, d * 4, dc);
+          if (d == 0) coh_store1(rr, DK * 4, usc);
+        } else {
+          rec[d] = dc;
+          if (d == 0) rec[DK] = usc;
+        }
+        if constexpr (std::is_same<S, Smem>::value || std::is_same<S, SmemSummary>::value) sm.dc[d] = dc;
       }
     }
     __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0): the table writes of this wave are done
@@ -429,35 +527,39 @@ struct Chunk {
     if constexpr (SUMMARY) __syncthreads();
   }
 
-  // U_c as U^T ([DV][DK]) to `U` in float32 or, with U16 (16-bit inputs), to
-  // `U16p` rounded to fp16, the type the states are handed over in; coherent
-  // (agent scope) or plain.
-  template <bool COH, bool U16 = false, class S>
-  __device__ __forceinline__ void summary_out(const S& sm, float* U, unsigned short* U16p = nullptr) {
+  // U_c ([DK][DV], row i = key dim) to `U`: float32 for float32 inputs, else
+  // fp16(U / usc); coherent (agent scope) or plain. Computed as U^T = v^T khat,
+  // so each lane holds 4 consecutive value columns of one row.
+  template <bool COH, class S>
+  __device__ __forceinline__ void summary_out(const S& sm, void* U) {
     constexpr int NTI = (DK / 16) * (DV / 16);
-    const __amdgpu_buffer_rsrc_t ur = make_rsrc(U, DK * DV * 4);
+    // a power of two (exact); NaN poisons the summary of a chunk with an
+    // out-of-range input, and through it every state after the chunk
+    const float down = range_bad ? __builtin_nanf("") : 1.f / usc;
     for (int tau = w; tau < NTI; tau += NW) {
       const int ib = tau / (DV / 16), jb = tau % (DV / 16);
       f4 acc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int ks = 0; ks < C / 32; ++ks) {
-        const F8 a = *reinterpret_cast<const F8*>(&sm.kT[(16 * ib + tr) * TP + 32 * ks + 8 * gq]);
-        const F8 b = *reinterpret_cast<const F8*>(&sm.vT[(16 * jb + tr) * TP + 32 * ks + 8 * gq]);
+        const F8 a = *reinterpret_cast<const F8*>(&sm.vT[(16 * jb + tr) * TP + 32 * ks + 8 * gq]);
+        const F8 b = *reinterpret_cast<const F8*>(&sm.kT[(16 * ib + tr) * TP + 32 * ks + 8 * gq]);
         acc = mma32(a, b, acc);
       }
-      // lane holds U[16ib + 4gq + e][16jb + tr]
-      const int off = (16 * jb + tr) * DK + 16 * ib + 4 * gq;
-      if constexpr (U16) {
-        const h4 hv = {(_Float16)acc[0], (_Float16)acc[1], (_Float16)acc[2], (_Float16)acc[3]};
+      // lane holds U^T[16jb + 4gq + e][16ib + tr] = U[16ib + tr][16jb + 4gq + e]
+      const int off = (16 * ib + tr) * DV + 16 * jb + 4 * gq;
+      if constexpr (F16) {
+        const h4 hv = {(_Float16)(acc[0] * down), (_Float16)(acc[1] * down), (_Float16)(acc[2] * down),
+                       (_Float16)(acc[3] * down)};
         if constexpr (COH)
-          __builtin_amdgcn_raw_buffer_store_b64(__builtin_bit_cast(u32x2, hv), make_rsrc(U16p, DK * DV * 2), off * 2, 0,
+          __builtin_amdgcn_raw_buffer_store_b64(__builtin_bit_cast(u32x2, hv), make_rsrc(U, DK * DV * 2), off * 2, 0,
                                                 kAgentCoherent);
         else
-          *reinterpret_cast<h4*>(reinterpret_cast<_Float16*>(U16p) + off) = hv;
-      } else if constexpr (COH)
-        coh_store4(ur, off * 4, acc);
-      else
-        *reinterpret_cast<f4*>(&U[off]) = acc;
+          *reinterpret_cast<h4*>(static_cast<_Float16*>(U) + off) = hv;
+      } else if constexpr (COH) {
+        coh_store4(make_rsrc(U, DK * DV * 4), off * 4, acc);
+      } else {
+        *reinterpret_cast<f4*>(static_cast<float*>(U) + off) = acc;
+      }
     }
   }
 
@@ -512,8 +614,9 @@ struct Chunk {
     return res;
   }
 
-  // Intra-chunk part: o_r = sum_{j<=r} P[r][j] v_j for this wave's 16 rows.
-  // Needs the k rows written by load<true>().
+  // Intra-chunk part: O = sum_{j<=r} P[r][j] v_j / pup for this wave's 16 rows
+  // (16-bit inputs: the score tile is scaled by a power of two before it is
+  // rounded to fp16). Needs the k rows written by load<true>().
   template <class S>
   __device__ __forceinline__ void intra(const GlaParams& P, S& sm, int bh, int c, f4 (&O)[DV / 16]) {
     f4 PT[NW];
@@ -585,6 +688,24 @@ struct Chunk {
         if (J == w) PT[J] = D;
     }
 
+    // power-of-two scale of the fp16 score tile: its largest magnitude below 2^15
+    pup = 1.f;
+    if constexpr (F16) {
+      float pm = 0.f;
+#pragma unroll
+      for (int J = 0; J < NW; ++J)
+        if (J <= w)
+#pragma unroll
+          for (int e = 0; e < 4; ++e) pm = fmaxf(pm, fabsf(PT[J][e]));
+      const int ex = fp16_exponent(wave_max_uniform(pm));
+      pup = exp2i(ex);
+      const float down = exp2i(-ex);
+#pragma unroll
+      for (int J = 0; J < NW; ++J)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) PT[J][e] *= down;
+    }
+
 #pragma unroll
     for (int jb = 0; jb < DV / 16; ++jb) O[jb] = f4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
@@ -600,82 +721,74 @@ struct Chunk {
     }
   }
 
-  // Boundary state S_[c]^T ([DV][DK] fp32) -> shared tile, in two steps so the
-  // loads can be issued early: each thread moves whole 16-byte pieces. No
-  // barrier.
-  static constexpr int SQ4 = DK * DV / 4;           // 16-byte pieces in one state
-  static constexpr int SPER = (SQ4 + NT - 1) / NT;  // pieces per thread
-  template <bool COH>
-  __device__ __forceinline__ void state_load(const float* ST, f4 (&buf)[SPER]) {
-    const __amdgpu_buffer_rsrc_t sr = make_rsrc(ST, DK * DV * 4);
-#pragma unroll
-    for (int m = 0; m < SPER; ++m) {
-      const int q4 = threadIdx.x + m * NT;
-      if (q4 < SQ4) {
-        if constexpr (COH)
-          buf[m] = coh_load4(sr, q4 * 16);
-        else
-          buf[m] = reinterpret_cast<const f4*>(ST)[q4];
-      }
-    }
-  }
-  // 16-bit inputs: the states are handed over already rounded to the fp16 MFMA
-  // operand type (what state_store would do), so 16-byte pieces of 8 elements
-  // move straight to the tile.
-  static constexpr int SQ8 = DK * DV / 8;
-  static constexpr int SPER8 = (SQ8 + NT - 1) / NT;
-  template <bool COH = false>
-  __device__ __forceinline__ void state_load16(const unsigned short* ST, u32x4 (&buf)[SPER8]) const {
-    const __amdgpu_buffer_rsrc_t sr = make_rsrc(ST, DK * DV * 2);
-#pragma unroll
-    for (int m = 0; m < SPER8; ++m) {
-      const int q8 = threadIdx.x + m * NT;
-      if (q8 < SQ8) {
-        if constexpr (COH)
-          buf[m] = __builtin_amdgcn_raw_buffer_load_b128(sr, q8 * 16, 0, kAgentCoherent);
-        else
-          buf[m] = reinterpret_cast<const u32x4*>(ST)[q8];
-      }
-    }
-  }
-  template <class S>
-  __device__ __forceinline__ void state_store16(S& sm, const u32x4 (&buf)[SPER8]) {
-    static_assert(F16 && (SP * 2) % 16 == 0, "16-byte rows of fp16 elements");
-#pragma unroll
-    for (int m = 0; m < SPER8; ++m) {
-      const int q8 = threadIdx.x + m * NT;
-      if (q8 < SQ8) {
-        const int dv = (q8 * 8) / DK, i = (q8 * 8) % DK;
-        *reinterpret_cast<u32x4*>(&sm.sT[dv * SP + i]) = buf[m];
-      }
-    }
-  }
-  template <class S>
-  __device__ __forceinline__ void state_store(S& sm, const f4 (&buf)[SPER]) {
-#pragma unroll
-    for (int m = 0; m < SPER; ++m) {
-      const int q4 = threadIdx.x + m * NT;  // piece index in [DV][DK]
-      if (q4 < SQ4) {
-        const int dv = (q4 * 4) / DK, i = (q4 * 4) % DK;
-#pragma unroll
-        for (int e = 0; e < 4; ++e) sm.sT[dv * SP + i + e] = (E)buf[m][e];
-      }
-    }
+  // ---- boundary states in pieces of 8 elements: this thread's pieces are
+  // threadIdx.x + m NT, each row i_m = piece / (DV/8), columns n0 .. n0 + 7 ----
+  __device__ __forceinline__ static int piece_n0() { return 8 * ((int)threadIdx.x % (DV / 8)); }
+  __device__ __forceinline__ static int piece_i(int m) { return ((int)threadIdx.x + m * NT) / (DV / 8); }
+  __device__ __forceinline__ static bool piece_ok(int m) { return (int)threadIdx.x + m * NT < SQ8; }
+  __device__ __forceinline__ static uint32_t piece_elem(int m) {
+    return (uint32_t)(piece_i(m) * DV + piece_n0());
   }
 
-  // o_r += (q_r exp(A_r)) S_[c]. Reads the shared state tile.
+  // S_[c] pieces -> the shared state tile S^T ([DV][SP]). For 16-bit inputs the
+  // whole tile is divided by tsc = 2^e, e = fp16_exponent of `wg_max`, the
+  // largest |S_[c]| over the work-group. No barrier.
+  template <class S>
+  __device__ __forceinline__ void state_tile(S& sm, const float (&acc)[SPER][8], float wg_max) {
+    const int n0 = piece_n0();
+    float down = 1.f;
+    tsc = 1.f;
+    if constexpr (F16) {
+      const int ex = fp16_exponent(wg_max);
+      tsc = exp2i(ex);
+      down = exp2i(-ex);
+    }
+#pragma unroll
+    for (int m = 0; m < SPER; ++m)
+      if (piece_ok(m)) {
+        const int i = piece_i(m);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) sm.sT[(n0 + e) * SP + i] = (E)(acc[m][e] * down);
+      }
+  }
+
+  // The largest |S_[c]| of this thread's pieces, over the work-group: one
+  // barrier (the staged output kernel; the one-launch kernel folds it into its
+  // own exchange).
+  template <class S>
+  __device__ __forceinline__ float state_max(S& sm, const float (&acc)[SPER][8]) const {
+    float mx = 0.f;
+#pragma unroll
+    for (int m = 0; m < SPER; ++m)
+#pragma unroll
+      for (int e = 0; e < 8; ++e) mx = fmaxf(mx, piece_ok(m) ? fabsf(acc[m][e]) : 0.f);
+    mx = wave_max_uniform(mx);
+    if (lane == 0) sm.smax[w] = mx;
+    __syncthreads();
+    mx = 0.f;
+#pragma unroll
+    for (int K = 0; K < NW; ++K) mx = fmaxf(mx, sm.smax[K]);
+    return mx;
+  }
+
+  // O += (q_r exp(A_r)) S_[c]: the tile's product times tsc. Reads the shared
+  // state tile.
   template <class S>
   __device__ __forceinline__ void readout(const S& sm, f4 (&O)[DV / 16]) {
     F8 qtf[KS];
 #pragma unroll
     for (int s = 0; s < KS; ++s) qtf[s] = Op<F16>::pack8(qt[s]);
 #pragma unroll
-    for (int jb = 0; jb < DV / 16; ++jb)
+    for (int jb = 0; jb < DV / 16; ++jb) {
+      f4 R = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int s = 0; s < KS; ++s) {
         const F8 b = *reinterpret_cast<const F8*>(&sm.sT[(16 * jb + tr) * SP + 32 * s + 8 * gq]);
-        O[jb] = mma32(qtf[s], b, O[jb]);
+        R = mma32(qtf[s], b, R);
       }
+#pragma unroll
+      for (int e = 0; e < 4; ++e) O[jb][e] = fmaf(R[e], tsc, O[jb][e]);
+    }
   }
 
   // Stage the output tile through LDS and write whole rows back in spatial order.
@@ -683,6 +796,7 @@ struct Chunk {
   // loaded early (with the other inputs) so that the epilogue does not wait
   // for memory at the end of the kernel. Only when P.gate is set.
   static constexpr int SITER = C * (DV / 8) / NT;  // store iterations per thread
+  static constexpr int PIECES = DV / 8;            // 8-element pieces of an output row
   __device__ __forceinline__ void prefetch_gate(const GlaParams& P, int bh, int c, Raw (&rz)[SITER]) const {
 #pragma unroll
     for (int it = 0; it < SITER; ++it) {
@@ -694,14 +808,18 @@ struct Chunk {
     }
   }
 
-  template <class S>
+  // O holds the output rows of this wave (before the scale); `poison` stores
+  // NaN instead. BARRIER: wait first until every wave is done with the k rows
+  // in buf (which the output tile overwrites).
+  template <bool BARRIER, class S>
   __device__ __forceinline__ void store(const GlaParams& P, S& sm, int bh, int c, const f4 (&O)[DV / 16],
-                                        const Raw (&rz)[SITER]) {
-    __syncthreads();  // all waves are done with the k rows in buf
+                                        const Raw (&rz)[SITER], bool poison) {
+    if constexpr (BARRIER) __syncthreads();
+    const float mul = poison ? __builtin_nanf("") : P.scale;
 #pragma unroll
     for (int jb = 0; jb < DV / 16; ++jb)
 #pragma unroll
-      for (int e = 0; e < 4; ++e) sm.buf[(16 * w + 4 * gq + e) * OP + 16 * jb + tr] = P.scale * O[jb][e];
+      for (int e = 0; e < 4; ++e) sm.buf[(16 * w + 4 * gq + e) * OP + 16 * jb + tr] = mul * O[jb][e];
     __syncthreads();
     // C * PIECES is a multiple of NT, so every lane runs the same number of
     // iterations, and the PIECES lanes of a row are consecutive lanes of one wave
@@ -720,7 +838,6 @@ struct Chunk {
       if (valid) store_n<8>(P.o, P.odt, off, x);
     }
   }
-  static constexpr int PIECES = DV / 8;  // 8-element pieces of an output row
 
   // Output-gate epilogue (Sec. 3.1): u = SiLU(z) * o / sqrt(mean(o^2) + eps) * w
   // over the DV channels of one token; x holds this lane's 8 channels of o.
@@ -732,162 +849,252 @@ struct Chunk {
 #pragma unroll
     for (int m = 1; m < PIECES; m <<= 1) ss += __shfl_xor(ss, m, kWave);
     const float rs = rsqrtf(ss * (1.f / DV) + P.eps);
-    float z[8], w[8];
+    float z[8], wt[8];
     cvt_raw(rz, P.gatedt, z);
     if (P.nw) {
       const f4 lo = *reinterpret_cast<const f4*>(P.nw + 8 * pc);
       const f4 hi = *reinterpret_cast<const f4*>(P.nw + 8 * pc + 4);
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
-        w[e] = lo[e];
-        w[e + 4] = hi[e];
+        wt[e] = lo[e];
+        wt[e + 4] = hi[e];
       }
     } else {
 #pragma unroll
-      for (int e = 0; e < 8; ++e) w[e] = 1.f;
+      for (int e = 0; e < 8; ++e) wt[e] = 1.f;
     }
 #pragma unroll
-    for (int e = 0; e < 8; ++e) x[e] = z[e] * __builtin_amdgcn_rcpf(1.f + __expf(-z[e])) * (x[e] * rs) * w[e];
+    for (int e = 0; e < 8; ++e) x[e] = z[e] * __builtin_amdgcn_rcpf(1.f + __expf(-z[e])) * (x[e] * rs) * wt[e];
+  }
+};
+
+// 8 elements of a summary piece (fp16 bits or float32) times w, added to acc.
+template <bool F16>
+struct Piece;
+template <>
+struct Piece<true> {
+  u32x4 a;
+  __device__ __forceinline__ void load(__amdgpu_buffer_rsrc_t r, uint32_t elem) { a = coh_load16(r, elem * 2); }
+  __device__ __forceinline__ void plain(const void* base, uint32_t elem) {
+    a = *reinterpret_cast<const u32x4*>(static_cast<const _Float16*>(base) + elem);
+  }
+  __device__ __forceinline__ void fma_into(float (&acc)[8], float wt) const {
+    const h8 h = __builtin_bit_cast(h8, a);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) acc[e] = fmaf(wt, (float)h[e], acc[e]);
+  }
+};
+template <>
+struct Piece<false> {
+  u32x4 a, b;
+  __device__ __forceinline__ void load(__amdgpu_buffer_rsrc_t r, uint32_t elem) {
+    a = coh_load16(r, elem * 4);
+    b = coh_load16(r, elem * 4 + 16);
+  }
+  __device__ __forceinline__ void plain(const void* base, uint32_t elem) {
+    const u32x4* p = reinterpret_cast<const u32x4*>(static_cast<const float*>(base) + elem);
+    a = p[0];
+    b = p[1];
+  }
+  __device__ __forceinline__ void fma_into(float (&acc)[8], float wt) const {
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const unsigned ua = a[e], ub = b[e];
+      acc[e] = fmaf(wt, __builtin_bit_cast(float, ua), acc[e]);
+      acc[e + 4] = fmaf(wt, __builtin_bit_cast(float, ub), acc[e + 4]);
+    }
+  }
+};
+// 8 float32 elements of a state piece.
+struct Piece32 {
+  f4 a, b;
+  __device__ __forceinline__ void load(__amdgpu_buffer_rsrc_t r, uint32_t elem) {
+    a = coh_load4(r, elem * 4);
+    b = coh_load4(r, elem * 4 + 16);
+  }
+  __device__ __forceinline__ void fma_into(float (&acc)[8], float wt) const {
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      acc[e] = fmaf(wt, a[e], acc[e]);
+      acc[e + 4] = fmaf(wt, b[e], acc[e + 4]);
+    }
   }
 };
 
 // ---------------------------------------------------------------------------
-// Boundary-state scan over chunks (Eq. chunk_boundary_main) for elements
-// [e0, e1) of one sequence's state (S^T layout, element e = dv*DK + i). Reads
-// U_c^T and writes S_[c]^T in place, float32, or, for 16-bit inputs (H16),
-// fp16 in and out (the summaries as the summary kernel rounded them, the states
-// as the output kernel's readout consumes them), accumulating in float32.
-// S_final gets the float32 state after the last chunk.
+// Look-back (one launch), two levels. The chunks of a sequence form blocks of
+// G = P.blk_size; the last chunk of block k also hands over the block prefix
+//   B_k = sum_{j in block k} (prod_{j<l<=end of k} Diag(d_l)) U_j
+// and the block decay D_k = prod_{j in block k} d_j. Chunk c in block K builds
+//   S_[c] = sum_{j=KG}^{c-1} w_j U_j + sum_{k<K} w'_k B_k + w'' S_0,
+// every weight a product of the decays in between, nearest first: the
+// summaries of its own block before it, then the block prefixes of the blocks
+// before its own. Wherever a chunk on that path has already handed over its
+// inclusive state S_[j+1] (FUSED schedule), the look-back takes it and stops.
+// Every wave does this for its own pieces (rows i of the [DK][DV] state) on its
+// own: lane p of the wave polls the flag of the p-th chunk on the path (the
+// summary bit for its own block, the block bit of the wave for earlier blocks,
+// the inclusive bit of the wave anywhere) until every tile before the nearest
+// inclusive state is ready, then loads the tiles and the decays of its rows
+// in batches. A block-end chunk calls `at_block_end(acc, run, ok)` once its
+// own block's summaries are summed (before the block prefixes), unless an
+// inclusive state inside its block ended the look-back. No barrier. Returns
+// false if the wait ran out (acc is then not valid); `run` ends as the decay
+// product of each piece's row over every chunk before c.
 // ---------------------------------------------------------------------------
-template <int DK, int DV, bool H16>
-__device__ __forceinline__ void scan_plain(const GlaParams& P, int bh, int e0, int e1, int tid, int nt) {
-  // two adjacent elements (dims i, i + 1 of one d_v row) per thread: 8-byte
-  // loads of U and of the decays, 4-byte fp16 (or 8-byte float32) stores
-  typedef float f2 __attribute__((ext_vector_type(2)));
-  typedef _Float16 h2 __attribute__((ext_vector_type(2)));
-  static_assert(DK % 2 == 0, "element pairs share a d_v row");
-  float* st = P.states + (int64_t)bh * P.nchunks * (DK * DV);
-  _Float16* st16 = reinterpret_cast<_Float16*>(P.states16) + (int64_t)bh * P.nchunks * (DK * DV);
-  const float* dec = P.decays + (int64_t)bh * P.nchunks * DK;
-  const int NC = P.nchunks;
-  for (int e = e0 + 2 * tid; e < e1; e += 2 * nt) {
-    const int dv = e / DK, i = e - dv * DK;
-    f2 s = {0.f, 0.f};
-    if (P.s0) {
-      s[0] = P.s0[((int64_t)bh * DK + i) * DV + dv];
-      s[1] = P.s0[((int64_t)bh * DK + i + 1) * DV + dv];
-    }
-    for (int c0 = 0; c0 < NC; c0 += 32) {
-      // raw loads first (all 32 in flight), conversions only where the values
-      // are used: a conversion next to its load would wait for that load
-      typedef typename std::conditional<H16, h2, f2>::type U2;
-      U2 u[32];
-      f2 d[32];
+template <class T, class F>
+__device__ __forceinline__ bool lookback(const GlaParams& P, const T& ch, int seq, int c, float (&acc)[T::SPER][8],
+                                         float (&run)[T::SPER], F at_block_end) {
+  constexpr int DK = T::kDK, DV = T::kDV, SPER = T::SPER, RS = T::RS, RB = DK + 8;
+  constexpr bool F16 = T::F16;
+  constexpr int B = 4;  // tiles per batch of piece loads
+  const int NC = P.nchunks, G = P.blk_size;
+  const unsigned* fl = P.flags + (size_t)seq * kMaxChainChunks;
+  const uint32_t tile = DK * DV * (F16 ? 2 : 4);
+  const __amdgpu_buffer_rsrc_t ar =
+      make_rsrc(static_cast<char*>(P.agg) + (size_t)seq * NC * tile, (uint32_t)NC * tile);
+  const __amdgpu_buffer_rsrc_t br =
+      make_rsrc(static_cast<char*>(P.blk) + (size_t)seq * NC * tile, (uint32_t)NC * tile);
+  const __amdgpu_buffer_rsrc_t rr = make_rsrc(P.rec + (size_t)seq * NC * RS, (uint32_t)NC * RS * 4);
+  const __amdgpu_buffer_rsrc_t bre = make_rsrc(P.blkrec + (size_t)seq * NC * RB, (uint32_t)NC * RB * 4);
+  const __amdgpu_buffer_rsrc_t sr = make_rsrc(P.states + (size_t)seq * NC * (DK * DV), (uint32_t)NC * DK * DV * 4);
 #pragma unroll
-      for (int m = 0; m < 32; ++m) {
-        if (c0 + m < NC) {
-          if constexpr (H16)
-            u[m] = *reinterpret_cast<const h2*>(&st16[(int64_t)(c0 + m) * (DK * DV) + e]);
-          else
-            u[m] = *reinterpret_cast<const f2*>(&st[(int64_t)(c0 + m) * (DK * DV) + e]);
-          d[m] = *reinterpret_cast<const f2*>(&dec[(int64_t)(c0 + m) * DK + i]);
-        }
-      }
+  for (int m = 0; m < SPER; ++m) {
+    run[m] = 1.f;
 #pragma unroll
-      for (int m = 0; m < 32; ++m) {
-        if (c0 + m < NC) {
-          if constexpr (H16)
-            *reinterpret_cast<h2*>(&st16[(int64_t)(c0 + m) * (DK * DV) + e]) = h2{(_Float16)s[0], (_Float16)s[1]};
-          else
-            *reinterpret_cast<f2*>(&st[(int64_t)(c0 + m) * (DK * DV) + e]) = s;
-          s[0] = d[m][0] * s[0] + (float)u[m][0];
-          s[1] = d[m][1] * s[1] + (float)u[m][1];
-        }
-      }
-    }
-    if (P.s_final) {
-      P.s_final[((int64_t)bh * DK + i) * DV + dv] = s[0];
-      P.s_final[((int64_t)bh * DK + i + 1) * DV + dv] = s[1];
-    }
+    for (int e = 0; e < 8; ++e) acc[m][e] = 0.f;
   }
-}
+  const int lo = c / G * G;   // first chunk of c's block
+  const int nA = c - lo;      // summaries of c's block before c (path tiles 0 .. nA - 1)
+  const int nB = lo / G;      // blocks before c's (path tiles nA .. nA + nB - 1, nearest first);
+                              // nA < G <= 16 and nB < kMaxChainChunks / G, both below 64 (host)
+  const unsigned incb = 1u << (kFlagInclusive + ch.w), blkb = 1u << (kFlagBlock + ch.w);
+  const bool block_end = c % G == G - 1 && c < NC - 1;
+  // chunk whose flag path tile p waits on: a summary, or the last chunk of a block
+  auto chunk_of = [&](int p) { return p < nA ? c - 1 - p : (nB - 1 - (p - nA)) * G + G - 1; };
 
-// The same with agent-coherent accesses, for the fused schedule. One sequence's
-// states span nchunks * DK * DV * 4 bytes, which the host keeps below 2^31.
-template <int DK, int DV>
-__device__ __forceinline__ void scan_coherent(const GlaParams& P, int bh, int e0, int e1, int tid, int nt) {
-  const int NC = P.nchunks;
-  const __amdgpu_buffer_rsrc_t sr = make_rsrc(P.states + (int64_t)bh * NC * (DK * DV), (uint32_t)NC * DK * DV * 4);
-  const __amdgpu_buffer_rsrc_t dr = make_rsrc(P.decays + (int64_t)bh * NC * DK, (uint32_t)NC * DK * 4);
-  for (int e = e0 + tid; e < e1; e += nt) {
-    const int dv = e / DK, i = e - dv * DK;
-    float s = P.s0 ? P.s0[((int64_t)bh * DK + i) * DV + dv] : 0.f;
-    for (int c0 = 0; c0 < NC; c0 += 32) {
-      float u[32], d[32];
-#pragma unroll
-      for (int m = 0; m < 32; ++m) {
-        if (c0 + m < NC) {
-          u[m] = coh_load1(sr, ((uint32_t)(c0 + m) * (DK * DV) + e) * 4);
-          d[m] = coh_load1(dr, ((uint32_t)(c0 + m) * DK + i) * 4);
-        }
-      }
-#pragma unroll
-      for (int m = 0; m < 32; ++m) {
-        if (c0 + m < NC) {
-          coh_store1(sr, ((uint32_t)(c0 + m) * (DK * DV) + e) * 4, s);
-          s = d[m] * s + u[m];
-        }
-      }
+  // Poll the flags of path tiles [p0, p0 + n) (lane l: tile p0 + l, n < 64)
+  // until every tile before the nearest one with this wave's inclusive bit has
+  // its `ready` bit; returns how many tiles to sum (n if no inclusive state),
+  // or -1 if the wait ran out.
+  auto poll = [&](int p0, int n, unsigned ready) -> int {
+    if (n == 0) return 0;
+    unsigned cnt = 0;
+    for (;;) {
+      const unsigned f = ch.lane < n ? __hip_atomic_load(&fl[chunk_of(p0 + ch.lane)], __ATOMIC_RELAXED,
+                                                         __HIP_MEMORY_SCOPE_AGENT)
+                                     : 0u;
+      const uint64_t inc = __builtin_amdgcn_ballot_w64((f & incb) != 0);
+      const uint64_t rdy = __builtin_amdgcn_ballot_w64((f & ready) != 0);
+      const int mm = inc ? (int)__builtin_ctzll(inc) : n;
+      const uint64_t need = (1ull << mm) - 1ull;  // mm < 64
+      if ((rdy & need) == need) return mm;
+      if (++cnt >= P.spin) return -1;
+      __builtin_amdgcn_s_sleep(1);
     }
-    if (P.s_final) P.s_final[((int64_t)bh * DK + i) * DV + dv] = s;
-  }
-}
+  };
+  // path tiles [p0, p1) in batches of B (every load of a batch issued before
+  // any is used): summaries (p < nA) or block prefixes
+  struct Batch {
+    Piece<F16> u[B][SPER];
+    float d[B][SPER], sc[B][SPER];
+  };
+  auto load_batch = [&](int b0, int p1, Batch& t) {
+#pragma unroll
+    for (int b = 0; b < B; ++b)
+      if (b0 + b < p1) {
+        const int p = b0 + b;
+        if (p < nA) {
+          const uint32_t j = (uint32_t)(c - 1 - p);
+          const float scj = coh_load1(rr, (j * RS + DK) * 4);
+#pragma unroll
+          for (int mm = 0; mm < SPER; ++mm)
+            if (T::piece_ok(mm)) {
+              t.u[b][mm].load(ar, j * (DK * DV) + T::piece_elem(mm));
+              t.d[b][mm] = coh_load1(rr, (j * RS + T::piece_i(mm)) * 4);
+              t.sc[b][mm] = scj;
+            }
+        } else {
+          const uint32_t k = (uint32_t)(nB - 1 - (p - nA));
+          const float sck = coh_load1(bre, (k * RB + DK + ch.w) * 4);
+#pragma unroll
+          for (int mm = 0; mm < SPER; ++mm)
+            if (T::piece_ok(mm)) {
+              t.u[b][mm].load(br, k * (DK * DV) + T::piece_elem(mm));
+              t.d[b][mm] = coh_load1(bre, (k * RB + T::piece_i(mm)) * 4);
+              t.sc[b][mm] = sck;
+            }
+        }
+      }
+  };
+  auto use_batch = [&](int b0, int p1, const Batch& t) {
+#pragma unroll
+    for (int b = 0; b < B; ++b)
+      if (b0 + b < p1)
+#pragma unroll
+        for (int mm = 0; mm < SPER; ++mm)
+          if (T::piece_ok(mm)) {
+            t.u[b][mm].fma_into(acc[mm], run[mm] * t.sc[b][mm]);
+            run[mm] *= t.d[b][mm];
+          }
+  };
+  auto sum_tiles = [&](int p0, int p1) {
+    for (int b0 = p0; b0 < p1; b0 += B) {
+      Batch x;
+      load_batch(b0, p1, x);
+      use_batch(b0, p1, x);
+    }
+  };
 
-// The same over fp16 summaries and states (16-bit inputs), two adjacent
-// elements per thread, accumulating in float32.
-template <int DK, int DV>
-__device__ __forceinline__ void scan_coherent16(const GlaParams& P, int bh, int e0, int e1, int tid, int nt) {
-  typedef float f2 __attribute__((ext_vector_type(2)));
-  typedef _Float16 h2 __attribute__((ext_vector_type(2)));
-  const int NC = P.nchunks;
-  const __amdgpu_buffer_rsrc_t sr = make_rsrc(P.states16 + (int64_t)bh * NC * (DK * DV), (uint32_t)NC * DK * DV * 2);
-  const __amdgpu_buffer_rsrc_t dr = make_rsrc(P.decays + (int64_t)bh * NC * DK, (uint32_t)NC * DK * 4);
-  for (int e = e0 + 2 * tid; e < e1; e += 2 * nt) {
-    const int dv = e / DK, i = e - dv * DK;
-    f2 s = {0.f, 0.f};
-    if (P.s0) {
-      s[0] = P.s0[((int64_t)bh * DK + i) * DV + dv];
-      s[1] = P.s0[((int64_t)bh * DK + i + 1) * DV + dv];
-    }
-    for (int c0 = 0; c0 < NC; c0 += 32) {
-      unsigned u[32];
-      u32x2 d[32];
-#pragma unroll
-      for (int m = 0; m < 32; ++m) {
-        if (c0 + m < NC) {
-          u[m] = __builtin_amdgcn_raw_buffer_load_b32(sr, (int)(((uint32_t)(c0 + m) * (DK * DV) + e) * 2), 0,
-                                                      kAgentCoherent);
-          d[m] = __builtin_amdgcn_raw_buffer_load_b64(dr, (int)(((uint32_t)(c0 + m) * DK + i) * 4), 0, kAgentCoherent);
-        }
-      }
-#pragma unroll
-      for (int m = 0; m < 32; ++m) {
-        if (c0 + m < NC) {
-          const h2 hs = {(_Float16)s[0], (_Float16)s[1]};
-          __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(unsigned, hs), sr,
-                                                (int)(((uint32_t)(c0 + m) * (DK * DV) + e) * 2), 0, kAgentCoherent);
-          const h2 hu = __builtin_bit_cast(h2, u[m]);
-          const f2 dd = __builtin_bit_cast(f2, d[m]);
-          s[0] = dd[0] * s[0] + (float)hu[0];
-          s[1] = dd[1] * s[1] + (float)hu[1];
-        }
+  // first the summaries of c's own block; then a block-end chunk hands over its
+  // block prefix (which depends on nothing before its block, so the prefixes
+  // never wait on one another); then the block prefixes before c's block
+  int m = poll(0, nA, kFlagSummary);
+  bool ok = m >= 0, found = false;
+  if (ok) {
+    found = m < nA;
+    sum_tiles(0, m);
+    if (!found) {
+      if (block_end) at_block_end(acc, run, true);
+      const int mb = poll(nA, nB, blkb);
+      ok = mb >= 0;
+      if (ok) {
+        m = nA + mb;
+        found = mb < nB;
+        sum_tiles(nA, m);
       }
     }
-    if (P.s_final) {
-      P.s_final[((int64_t)bh * DK + i) * DV + dv] = s[0];
-      P.s_final[((int64_t)bh * DK + i + 1) * DV + dv] = s[1];
-    }
+  } else if (block_end) {
+    at_block_end(acc, run, false);
   }
+  if (!ok) return false;
+  if (found) {
+    // the inclusive state S_[j+1] that chunk j = chunk_of(m) stored
+    Piece32 st[SPER];
+    const uint32_t j = (uint32_t)chunk_of(m);
+#pragma unroll
+    for (int mm = 0; mm < SPER; ++mm)
+      if (T::piece_ok(mm)) st[mm].load(sr, j * (DK * DV) + T::piece_elem(mm));
+#pragma unroll
+    for (int mm = 0; mm < SPER; ++mm)
+      if (T::piece_ok(mm)) st[mm].fma_into(acc[mm], run[mm]);
+  } else if (P.s0) {
+    // S_0 with the decay product of every chunk before c
+    const int bh = seq / P.vparts, part = seq - bh * P.vparts;
+    const float* s0 = P.s0 + (size_t)bh * DK * P.dvp + part * DV + T::piece_n0();
+#pragma unroll
+    for (int mm = 0; mm < SPER; ++mm)
+      if (T::piece_ok(mm)) {
+        const f4* q = reinterpret_cast<const f4*>(s0 + (size_t)T::piece_i(mm) * P.dvp);
+        const f4 lo4 = q[0], hi4 = q[1];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          acc[mm][e] = fmaf(run[mm], lo4[e], acc[mm][e]);
+          acc[mm][e + 4] = fmaf(run[mm], hi4[e], acc[mm][e + 4]);
+        }
+      }
+  }
+  return true;
 }
 
 // ---------------------------------------------------------------------------
@@ -901,20 +1108,55 @@ __global__ void __launch_bounds__(tile_threads(C)) gla_summary_kernel(GlaParams 
   const int c = blockIdx.x, bh = blockIdx.y;
   const int64_t sc = (int64_t)bh * P.nchunks + c;
   ch.template load<false>(P, sm, bh, c);
-  ch.template factors<false, true, false>(sm, P.decays + sc * DK);
-  if constexpr (T::F16)
-    ch.template summary_out<false, true>(sm, nullptr, P.states16 + sc * (DK * DV));
-  else
-    ch.template summary_out<false>(sm, P.states + sc * (DK * DV));
+  if (ch.range_bad && threadIdx.x == 0) __hip_atomic_fetch_or(P.fault, kFaultRange, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  ch.template factors<false, true, false>(sm, P.rec + sc * T::RS);
+  ch.template summary_out<false>(sm, static_cast<char*>(P.agg) + sc * (DK * DV) * (T::F16 ? 2 : 4));
 }
 
-// 128 threads per work-group, two elements each: 256 elements per work-group.
+// Boundary-state scan over chunks (Eq. chunk_boundary_main) for 256 state
+// elements of one sequence per work-group (128 threads, two adjacent value
+// columns of one row each, element e = i * DV + n): reads the summaries (fp16
+// times their scale, or float32) and the decays, writes S_[c] in float32 and
+// S_final.
 template <int DK, int DV, bool H16>
 __global__ void __launch_bounds__(128) gla_scan_kernel(GlaParams P) {
+  typedef float f2 __attribute__((ext_vector_type(2)));
+  typedef _Float16 h2 __attribute__((ext_vector_type(2)));
+  constexpr int RS = DK + 4;
   const int bh = blockIdx.y;
-  const int e0 = blockIdx.x * 256;
-  const int e1 = min(e0 + 256, DK * DV);
-  scan_plain<DK, DV, H16>(P, bh, e0, e1, threadIdx.x, 128);
+  const int e = blockIdx.x * 256 + 2 * threadIdx.x;
+  if (e >= DK * DV) return;
+  const int NC = P.nchunks;
+  float* st = P.states + (int64_t)bh * NC * (DK * DV);
+  const char* ag = static_cast<const char*>(P.agg) + (int64_t)bh * NC * (DK * DV) * (H16 ? 2 : 4);
+  const float* rc = P.rec + (int64_t)bh * NC * RS;
+  const int i = e / DV;
+  f2 s = {0.f, 0.f};
+  if (P.s0) s = *reinterpret_cast<const f2*>(&P.s0[(int64_t)bh * DK * DV + e]);
+  for (int c0 = 0; c0 < NC; c0 += 16) {
+    // raw loads first (all 16 in flight), conversions only where the values
+    // are used: a conversion next to its load would wait for that load
+    typedef typename std::conditional<H16, h2, f2>::type U2;
+    U2 u[16];
+    float d[16], sc[16];
+#pragma unroll
+    for (int m = 0; m < 16; ++m) {
+      if (c0 + m < NC) {
+        u[m] = *reinterpret_cast<const U2*>(ag + ((int64_t)(c0 + m) * (DK * DV) + e) * (H16 ? 2 : 4));
+        d[m] = rc[(int64_t)(c0 + m) * RS + i];
+        sc[m] = rc[(int64_t)(c0 + m) * RS + DK];
+      }
+    }
+#pragma unroll
+    for (int m = 0; m < 16; ++m) {
+      if (c0 + m < NC) {
+        *reinterpret_cast<f2*>(&st[(int64_t)(c0 + m) * (DK * DV) + e]) = s;
+        s[0] = fmaf(d[m], s[0], sc[m] * (float)u[m][0]);
+        s[1] = fmaf(d[m], s[1], sc[m] * (float)u[m][1]);
+      }
+    }
+  }
+  if (P.s_final) *reinterpret_cast<f2*>(&P.s_final[(int64_t)bh * DK * DV + e]) = s;
 }
 
 template <int DK, int DV, int C, int IN>
@@ -925,318 +1167,243 @@ __global__ void __launch_bounds__(tile_threads(C)) gla_output_kernel(GlaParams P
   const int c = blockIdx.x, bh = blockIdx.y;
   const bool have_state = c > 0 || P.s0;
   const int64_t sc = (int64_t)bh * P.nchunks + c;
-  f4 sbuf[T::F16 ? 1 : T::SPER];
-  u32x4 hbuf[T::F16 ? T::SPER8 : 1];
+  Piece32 sp[T::SPER];
   if (have_state) {
-    if constexpr (T::F16)
-      ch.state_load16(P.states16 + sc * (DK * DV), hbuf);
-    else
-      ch.template state_load<false>(P.states + sc * (DK * DV), sbuf);
+    const __amdgpu_buffer_rsrc_t sr = make_rsrc(P.states + sc * (DK * DV), DK * DV * 4);
+#pragma unroll
+    for (int m = 0; m < T::SPER; ++m)
+      if (T::piece_ok(m)) sp[m].load(sr, T::piece_elem(m));
   }
   ch.template load<true>(P, sm, bh, c);
   Raw rz[T::SITER];
   if (P.gate) ch.prefetch_gate(P, bh, c, rz);
   if (have_state) {
-    if constexpr (T::F16)
-      ch.state_store16(sm, hbuf);
-    else
-      ch.state_store(sm, sbuf);
+    float acc[T::SPER][8];
+#pragma unroll
+    for (int m = 0; m < T::SPER; ++m) {
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        acc[m][e] = sp[m].a[e];
+        acc[m][e + 4] = sp[m].b[e];
+      }
+    }
+    ch.state_tile(sm, acc, ch.state_max(sm, acc));
   }
   ch.template factors<true, false, false>(sm, nullptr);
   f4 O[DV / 16];
   ch.intra(P, sm, bh, c, O);
+#pragma unroll
+  for (int jb = 0; jb < DV / 16; ++jb) O[jb] *= ch.pup;
   if (have_state) {
     __syncthreads();  // state tile complete
     ch.readout(sm, O);
   }
-  ch.store(P, sm, bh, c, O, rz);
+  ch.template store<true>(P, sm, bh, c, O, rz, ch.range_bad);
 }
 
 // ---------------------------------------------------------------------------
-// fused schedule
+// one-launch schedule (look-back)
 // ---------------------------------------------------------------------------
-// A work-group's coherent stores are acknowledged before its one increment.
-__device__ __forceinline__ void seq_arrive(unsigned* ctr) {
-  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-  __syncthreads();
-  if (threadIdx.x == 0) __hip_atomic_fetch_add(ctr, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-
-// Bounded wait until `ctr` reaches `target`; on time-out the fault word is set
-// (the results of the call are then invalid) and the work-group goes on.
-__device__ __forceinline__ void seq_wait(unsigned* ctr, unsigned target, unsigned* fault) {
-  if (threadIdx.x == 0) {
-    unsigned n = 0;
-    while (__hip_atomic_load(ctr, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < target) {
-      __builtin_amdgcn_s_sleep(1);
-      if (++n > kSpinLimit) {
-        __hip_atomic_store(fault, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        break;
-      }
-    }
-  }
-  __syncthreads();
-}
-
-// S_[c]^T ([DV][DK]) rebuilt from the summaries and decays of chunks 0..c-1 of
-// one sequence (agent-coherent loads) straight into the shared state tile
-// (STATE), walking the chunks backwards so that the weight of each summary is
-// one more decay factor than the one after it; FINAL also writes
-// S_final = Diag(d_c) S_[c] + U_c for the last chunk. Thread t owns the
-// 16-byte pieces t, t + NT, ...; with NT a multiple of DK / 4 they all share
-// dims i..i+3, so one decay load per chunk serves all of them. No barrier.
-// `seq` indexes the summaries (a head's value part under the value split),
-// `bh` the decays, S0 and S_final (the head; P's S0 and S_final pointers
-// already start at the part's first column).
-template <int DK, int DV, int NT, typename Sm, typename E, int SP>
-__device__ __forceinline__ void state_inline(const GlaParams& P, Sm& sm, int seq, int bh, int c, bool state,
-                                             bool final) {
-  constexpr int SQ4 = DK * DV / 4;
-  constexpr int SPER = (SQ4 + NT - 1) / NT;
-  static_assert(NT % (DK / 4) == 0, "the pieces of one thread must share their dims");
-  const int NC = P.nchunks;
-  const __amdgpu_buffer_rsrc_t sr = make_rsrc(P.states + (int64_t)seq * NC * (DK * DV), (uint32_t)NC * DK * DV * 4);
-  const __amdgpu_buffer_rsrc_t dr = make_rsrc(P.decays + (int64_t)bh * NC * DK, (uint32_t)NC * DK * 4);
-  const int i0 = (4 * (int)threadIdx.x) % DK;
-  f4 acc[SPER], wgt = {1.f, 1.f, 1.f, 1.f};
-#pragma unroll
-  for (int m = 0; m < SPER; ++m) acc[m] = f4{0.f, 0.f, 0.f, 0.f};
-  constexpr int B = SPER >= 16 ? 1 : 16 / SPER;  // chunks per batch of loads
-  for (int j1 = c; j1 > 0; j1 -= B) {
-    f4 u[B][SPER], d[B];
-#pragma unroll
-    for (int b = 0; b < B; ++b) {
-      const int j = j1 - 1 - b;
-      if (j >= 0) {
-        d[b] = coh_load4(dr, ((uint32_t)j * DK + i0) * 4);
-#pragma unroll
-        for (int m = 0; m < SPER; ++m) {
-          const int q4 = threadIdx.x + m * NT;
-          if (q4 < SQ4) u[b][m] = coh_load4(sr, ((uint32_t)j * (DK * DV) + 4 * q4) * 4);
-        }
-      }
-    }
-#pragma unroll
-    for (int b = 0; b < B; ++b) {
-      const int j = j1 - 1 - b;
-      if (j >= 0) {
-#pragma unroll
-        for (int m = 0; m < SPER; ++m) acc[m] += wgt * u[b][m];
-        wgt *= d[b];
-      }
-    }
-  }
-  const f4 dc = final ? coh_load4(dr, ((uint32_t)c * DK + i0) * 4) : f4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-  for (int m = 0; m < SPER; ++m) {
-    const int q4 = threadIdx.x + m * NT;
-    if (q4 < SQ4) {
-      const int dv = (4 * q4) / DK;
-      if (P.s0) {
-#pragma unroll
-        for (int e = 0; e < 4; ++e) acc[m][e] += wgt[e] * P.s0[((int64_t)bh * DK + i0 + e) * P.dvp + dv];
-      }
-      if (state) {
-#pragma unroll
-        for (int e = 0; e < 4; ++e) sm.sT[dv * SP + i0 + e] = (E)acc[m][e];
-      }
-      if (final) {
-        const f4 uc = coh_load4(sr, ((uint32_t)c * (DK * DV) + 4 * q4) * 4);
-#pragma unroll
-        for (int e = 0; e < 4; ++e) P.s_final[((int64_t)bh * DK + i0 + e) * P.dvp + dv] = dc[e] * acc[m][e] + uc[e];
-      }
-    }
-  }
-}
-
-// The same from fp16 summaries (16-bit inputs): 16-byte pieces of 8 elements,
-// which share dims i..i+7 when NT is a multiple of DK / 8; float32 sums.
-template <int DK, int DV, int NT, typename Sm, typename E, int SP>
-__device__ __forceinline__ void state_inline16(const GlaParams& P, Sm& sm, int seq, int bh, int c, bool state,
-                                               bool final) {
-  constexpr int SQ8 = DK * DV / 8;
-  constexpr int SPER = (SQ8 + NT - 1) / NT;
-  static_assert(NT % (DK / 8) == 0, "the pieces of one thread must share their dims");
-  const int NC = P.nchunks;
-  const __amdgpu_buffer_rsrc_t sr = make_rsrc(P.states16 + (int64_t)seq * NC * (DK * DV), (uint32_t)NC * DK * DV * 2);
-  const __amdgpu_buffer_rsrc_t dr = make_rsrc(P.decays + (int64_t)bh * NC * DK, (uint32_t)NC * DK * 4);
-  const int i0 = (8 * (int)threadIdx.x) % DK;
-  float acc[SPER][8], wgt[8];
-#pragma unroll
-  for (int e = 0; e < 8; ++e) wgt[e] = 1.f;
-#pragma unroll
-  for (int m = 0; m < SPER; ++m)
-#pragma unroll
-    for (int e = 0; e < 8; ++e) acc[m][e] = 0.f;
-  constexpr int B = SPER >= 16 ? 1 : 16 / SPER;  // chunks per batch of loads
-  for (int j1 = c; j1 > 0; j1 -= B) {
-    u32x4 u[B][SPER];
-    f4 d[B][2];
-#pragma unroll
-    for (int b = 0; b < B; ++b) {
-      const int j = j1 - 1 - b;
-      if (j >= 0) {
-        d[b][0] = coh_load4(dr, ((uint32_t)j * DK + i0) * 4);
-        d[b][1] = coh_load4(dr, ((uint32_t)j * DK + i0 + 4) * 4);
-#pragma unroll
-        for (int m = 0; m < SPER; ++m) {
-          const int q8 = threadIdx.x + m * NT;
-          if (q8 < SQ8)
-            u[b][m] = __builtin_amdgcn_raw_buffer_load_b128(sr, (int)(((uint32_t)j * (DK * DV) + 8 * q8) * 2), 0,
-                                                            kAgentCoherent);
-        }
-      }
-    }
-#pragma unroll
-    for (int b = 0; b < B; ++b) {
-      const int j = j1 - 1 - b;
-      if (j >= 0) {
-#pragma unroll
-        for (int m = 0; m < SPER; ++m) {
-          const h8 hv = __builtin_bit_cast(h8, u[b][m]);
-#pragma unroll
-          for (int e = 0; e < 8; ++e) acc[m][e] += wgt[e] * (float)hv[e];
-        }
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          wgt[e] *= d[b][0][e];
-          wgt[e + 4] *= d[b][1][e];
-        }
-      }
-    }
-  }
-  f4 dc[2] = {{0.f, 0.f, 0.f, 0.f}, {0.f, 0.f, 0.f, 0.f}};
-  if (final) {
-    dc[0] = coh_load4(dr, ((uint32_t)c * DK + i0) * 4);
-    dc[1] = coh_load4(dr, ((uint32_t)c * DK + i0 + 4) * 4);
-  }
-#pragma unroll
-  for (int m = 0; m < SPER; ++m) {
-    const int q8 = threadIdx.x + m * NT;
-    if (q8 < SQ8) {
-      const int dv = (8 * q8) / DK;
-      if (P.s0) {
-#pragma unroll
-        for (int e = 0; e < 8; ++e) acc[m][e] += wgt[e] * P.s0[((int64_t)bh * DK + i0 + e) * P.dvp + dv];
-      }
-      if (state) {
-#pragma unroll
-        for (int e = 0; e < 8; ++e) sm.sT[dv * SP + i0 + e] = (E)acc[m][e];
-      }
-      if (final) {
-        const h8 uc = __builtin_bit_cast(
-            h8, __builtin_amdgcn_raw_buffer_load_b128(sr, (int)(((uint32_t)c * (DK * DV) + 8 * q8) * 2), 0,
-                                                      kAgentCoherent));
-#pragma unroll
-        for (int e = 0; e < 8; ++e)
-          P.s_final[((int64_t)bh * DK + i0 + e) * P.dvp + dv] = dc[e >> 2][e & 3] * acc[m][e] + (float)uc[e];
-      }
-    }
-  }
-}
-
-// Work-group -> (sequence, chunk). Work-groups are handed to the 8 XCDs round
-// robin, so block b runs on XCD b % 8; all chunks of a sequence get the same
-// b % 8 and therefore share one L2. Blocks whose sequence index is past the end
-// exit at once.
-// Value split (inline schedule, P.vparts = 2): the work-groups of a chunk each
-// take DV of the head's 2 DV value columns, so a head runs as two sequences
-// with their own summaries, counters and boundary states (columns of S) over
-// the same q, k, g; both write the chunk decays, with identical values. The
-// grid is then exactly (sequences x chunks), chunks in descending order: the
-// chunks with the longest rebuilds start first, and the work-groups that
-// share a CU once every CU has one are the first chunks of their sequences.
-template <int DK, int DV, int C, int IN, bool INLINE>
-__global__ void __launch_bounds__(tile_threads(C)) gla_fused_kernel(GlaParams P) {
+// Work-group -> (sequence, chunk): the grid is chunk major over all sequences.
+// In ascending chunk order every block waits only on blocks with smaller
+// indices; work-groups are handed to the 8 XCDs round robin and each XCD starts
+// its blocks in index order, so the smallest unfinished block is always running
+// and the grid drains however few work-groups fit at once. When every
+// work-group of the grid is resident at once (P.desc) the chunks go in
+// descending order instead: the chunks with the longest look-backs start first.
+// Value split (P.vparts = 2): the work-groups of a chunk each take DV of the
+// head's 2 DV value columns, so a head runs as two sequences with their own
+// summaries, flags and boundary states (columns of S) over the same q, k, g.
+template <int DK, int DV, int C, int IN>
+__global__ void __launch_bounds__(tile_threads(C)) gla_chain_kernel(GlaParams P) {
   typedef Chunk<DK, DV, C, IN> T;
   __shared__ typename T::Smem sm;
   const int NC = P.nchunks;
   const int b = blockIdx.x;
-  int seq, c, bh;
-  if (INLINE && P.vparts > 1) {
-    const int ns = P.BH * P.vparts;
-    const int row = b / ns;
-    seq = b - row * ns;
-    c = NC - 1 - row;
-    bh = seq / P.vparts;
-    const int vp = seq - bh * P.vparts;
+  const int row = b / P.ns;
+  const int seq = b - row * P.ns;
+  const int c = P.desc ? NC - 1 - row : row;
+  const int bh = seq / P.vparts, vp = seq - bh * P.vparts;
+  if (P.vparts > 1) {
     P.v = static_cast<const char*>(P.v) + (int64_t)vp * DV * (T::F16 ? 2 : 4);
     P.o = static_cast<char*>(P.o) + (int64_t)vp * DV * (P.odt == GTR_F32 ? 4 : 2);
-    if (P.s0) P.s0 += vp * DV;
     if (P.s_final) P.s_final += vp * DV;
-  } else {
-    const int x = b & 7, slot = b >> 3;
-    const int grp = slot / NC;
-    c = slot - grp * NC;
-    seq = bh = grp * 8 + x;
-    if (bh >= P.BH) return;
   }
-  unsigned* sync = P.sync + 4 * seq;
   const int64_t sc = (int64_t)seq * NC + c;
+  unsigned* flag = P.flags + (size_t)seq * kMaxChainChunks + c;
 
   T ch;
   ch.template load<true>(P, sm, bh, c);
   Raw rz[T::SITER];
   if (P.gate) ch.prefetch_gate(P, bh, c, rz);
-  ch.template factors<true, true, true>(sm, P.decays + ((int64_t)bh * NC + c) * DK);
-  if constexpr (T::F16)
-    ch.template summary_out<true, true>(sm, nullptr, P.states16 + sc * (DK * DV));
-  else
-    ch.template summary_out<true>(sm, P.states + sc * (DK * DV));
-  seq_arrive(&sync[0]);
+  ch.template factors<true, true, true>(sm, P.rec + sc * T::RS);
+  void* U = static_cast<char*>(P.agg) + sc * (DK * DV) * (T::F16 ? 2 : 4);
+  ch.template summary_out<true>(sm, U);
+  // the summary and the record are acknowledged before the flag goes up
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  __syncthreads();
+  if (threadIdx.x == 0) __hip_atomic_fetch_or(flag, kFlagSummary, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+
+  // this chunk's own summary pieces, for S_[c+1] and the block prefix (in
+  // flight during the intra part)
+  const int G = P.blk_size;
+  const bool next = c < NC - 1 ? P.publish != 0 : P.s_final != nullptr;
+  const bool block_end = c % G == G - 1 && c < NC - 1;
+  Piece<T::F16> own[T::SPER];
+  if (next || block_end) {
+    const __amdgpu_buffer_rsrc_t ur = make_rsrc(U, DK * DV * (T::F16 ? 2 : 4));
+#pragma unroll
+    for (int m = 0; m < T::SPER; ++m)
+      if (T::piece_ok(m)) own[m].load(ur, T::piece_elem(m));
+  }
 
   f4 O[DV / 16];
   ch.intra(P, sm, bh, c, O);
+#pragma unroll
+  for (int jb = 0; jb < DV / 16; ++jb) O[jb] *= ch.pup;
 
-  seq_wait(&sync[0], (unsigned)NC, P.fault);
-  if constexpr (INLINE) {
-    const bool state = c > 0 || P.s0;
-    const bool final = P.s_final && c == NC - 1;
-    if (state || final) {
-      if constexpr (T::F16)
-        state_inline16<DK, DV, T::NT, typename T::Smem, typename T::E, T::SP>(P, sm, seq, bh, c, state, final);
-      else
-        state_inline<DK, DV, T::NT, typename T::Smem, typename T::E, T::SP>(P, sm, seq, bh, c, state, final);
+  // x = Diag(d_c) a + U_c for this wave's pieces (NaN if bad)
+  auto extend = [&](const float (&a)[T::SPER][8], bool bad, float (&x)[T::SPER][8]) {
+#pragma unroll
+    for (int m = 0; m < T::SPER; ++m) {
+      const float dc = sm.dc[T::piece_ok(m) ? T::piece_i(m) : 0];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) x[m][e] = bad ? __builtin_nanf("") : a[m][e] * dc;
+      if (T::piece_ok(m)) own[m].fma_into(x[m], ch.usc);
     }
-    if (state) {
-      __syncthreads();
-      ch.readout(sm, O);
-    }
-  } else {
+  };
+  // block prefix B_k = Diag(d_c) (sum over the block before c) + U_c and the
+  // block decay D_k = d_c * (product over the block before c), this wave's
+  // pieces, with one power-of-two scale per wave for the fp16 tile
+  auto at_block_end = [&](const float (&a)[T::SPER][8], const float (&rn)[T::SPER], bool good) {
+    constexpr int RB = DK + 8;
+    const int k = c / G;
+    float x[T::SPER][8];
+    extend(a, !good || ch.range_bad, x);
+    const __amdgpu_buffer_rsrc_t bsr = make_rsrc(static_cast<char*>(P.blk) + ((size_t)seq * NC + k) * DK * DV *
+                                                     (T::F16 ? 2 : 4), DK * DV * (T::F16 ? 2 : 4));
+    const __amdgpu_buffer_rsrc_t brr = make_rsrc(P.blkrec + ((size_t)seq * NC + k) * RB, RB * 4);
+    float down = 1.f, bs = 1.f;
     if constexpr (T::F16) {
-      const int per = 2 * ((DK * DV / 2 + NC - 1) / NC);  // element pairs
-      const int e0 = min(c * per, DK * DV), e1 = min(e0 + per, DK * DV);
-      scan_coherent16<DK, DV>(P, bh, e0, e1, threadIdx.x, T::NT);
-    } else {
-      const int per = (DK * DV + NC - 1) / NC;
-      const int e0 = min(c * per, DK * DV), e1 = min(e0 + per, DK * DV);
-      scan_coherent<DK, DV>(P, bh, e0, e1, threadIdx.x, T::NT);
+      float mx = 0.f;
+#pragma unroll
+      for (int m = 0; m < T::SPER; ++m)
+#pragma unroll
+        for (int e = 0; e < 8; ++e) mx = fmaxf(mx, T::piece_ok(m) ? fabsf(x[m][e]) : 0.f);
+      const int ex = fp16_exponent(wave_max_uniform(mx));
+      bs = exp2i(ex);
+      down = exp2i(-ex);
     }
-    seq_arrive(&sync[1]);
-    seq_wait(&sync[1], (unsigned)NC, P.fault);
-
-    if (c > 0 || P.s0) {
-      if constexpr (T::F16) {
-        u32x4 hbuf[T::SPER8];
-        ch.template state_load16<true>(P.states16 + sc * (DK * DV), hbuf);
-        ch.state_store16(sm, hbuf);
-      } else {
-        f4 sbuf[T::SPER];
-        ch.template state_load<true>(P.states + sc * (DK * DV), sbuf);
-        ch.state_store(sm, sbuf);
+#pragma unroll
+    for (int m = 0; m < T::SPER; ++m)
+      if (T::piece_ok(m)) {
+        const uint32_t el = T::piece_elem(m);
+        if constexpr (T::F16) {
+          h8 h;
+#pragma unroll
+          for (int e = 0; e < 8; ++e) h[e] = (_Float16)(x[m][e] * down);
+          __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, h), bsr, (int)(el * 2), 0, kAgentCoherent);
+        } else {
+          coh_store4(bsr, el * 4, f4{x[m][0], x[m][1], x[m][2], x[m][3]});
+          coh_store4(bsr, el * 4 + 16, f4{x[m][4], x[m][5], x[m][6], x[m][7]});
+        }
+        if (T::piece_n0() == 0) {
+          const float dci = sm.dc[T::piece_i(m)];
+          coh_store1(brr, T::piece_i(m) * 4, good ? rn[m] * dci : __builtin_nanf(""));
+        }
       }
-      __syncthreads();
-      ch.readout(sm, O);
+    if (ch.lane == 0) coh_store1(brr, (DK + ch.w) * 4, bs);
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // this wave's block stores are acknowledged
+    if (ch.lane == 0)
+      __hip_atomic_fetch_or(flag, 1u << (kFlagBlock + ch.w), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  };
+
+  float acc[T::SPER][8], run[T::SPER];
+  const bool okw = lookback(P, ch, seq, c, acc, run, at_block_end);
+  // the waves look back on their own; one exchange makes the outcome uniform:
+  // a wait that ran out in any of them (bit 0 of a wave's word) poisons the
+  // whole state, and so does a NaN state handed over by a poisoned chunk before
+  // it (bit 1): either way every row of this chunk and everything it hands
+  // over is NaN. The same exchange gives the largest |S_[c]| for the scale of
+  // the fp16 state tile.
+  bool nan_in = false;
+  float mx = 0.f;
+#pragma unroll
+  for (int m = 0; m < T::SPER; ++m)
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      nan_in = nan_in || acc[m][e] != acc[m][e];
+      mx = fmaxf(mx, T::piece_ok(m) ? fabsf(acc[m][e]) : 0.f);
+    }
+  const bool wave_nan = __builtin_amdgcn_ballot_w64(nan_in) != 0;
+  mx = wave_max_uniform(mx);
+  if (ch.lane == 0) {
+    sm.okw[ch.w] = (okw ? 0 : 1) | (wave_nan ? 2 : 0);
+    sm.smax[ch.w] = mx;
+  }
+  __syncthreads();
+  int bad = 0;
+  mx = 0.f;
+#pragma unroll
+  for (int K = 0; K < T::NW; ++K) {
+    bad |= sm.okw[K];
+    mx = fmaxf(mx, sm.smax[K]);
+  }
+  const bool ok = (bad & 1) == 0;
+  const bool poison = bad != 0 || ch.range_bad;
+  if (poison)
+#pragma unroll
+    for (int m = 0; m < T::SPER; ++m)
+#pragma unroll
+      for (int e = 0; e < 8; ++e) acc[m][e] = __builtin_nanf("");
+  if (threadIdx.x == 0 && poison)
+    __hip_atomic_fetch_or(P.fault, (ok ? 0u : kFaultWait) | (ch.range_bad ? kFaultRange : 0u), __ATOMIC_RELAXED,
+                          __HIP_MEMORY_SCOPE_AGENT);
+
+  // S_[c+1] = Diag(d_c) S_[c] + U_c: this wave's pieces of the inclusive state
+  // for the chunks after this one (its bit goes up once they are
+  // acknowledged), or of S_final after the last chunk
+  if (next) {
+    float nx[T::SPER][8];
+    extend(acc, poison, nx);
+    if (c < NC - 1) {
+      const __amdgpu_buffer_rsrc_t sr = make_rsrc(P.states + sc * (DK * DV), DK * DV * 4);
+#pragma unroll
+      for (int m = 0; m < T::SPER; ++m)
+        if (T::piece_ok(m)) {
+          coh_store4(sr, T::piece_elem(m) * 4, f4{nx[m][0], nx[m][1], nx[m][2], nx[m][3]});
+          coh_store4(sr, T::piece_elem(m) * 4 + 16, f4{nx[m][4], nx[m][5], nx[m][6], nx[m][7]});
+        }
+      asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+      if (ch.lane == 0)
+        __hip_atomic_fetch_or(flag, 1u << (kFlagInclusive + ch.w), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    } else {
+#pragma unroll
+      for (int m = 0; m < T::SPER; ++m)
+        if (T::piece_ok(m)) {
+          f4* dst = reinterpret_cast<f4*>(P.s_final + ((size_t)bh * DK + T::piece_i(m)) * P.dvp + T::piece_n0());
+          dst[0] = f4{nx[m][0], nx[m][1], nx[m][2], nx[m][3]};
+          dst[1] = f4{nx[m][4], nx[m][5], nx[m][6], nx[m][7]};
+        }
     }
   }
-  ch.store(P, sm, bh, c, O, rz);
+
+  if (c > 0 || P.s0) {
+    ch.state_tile(sm, acc, mx);
+    __syncthreads();  // state tile complete
+    ch.readout(sm, O);
+  }
+  // every wave is past the intra part (the exchange above): the k rows in buf
+  // are dead, so the output tile needs no barrier before it
+  ch.template store<false>(P, sm, bh, c, O, rz, poison);
 
   if (threadIdx.x == 0) {
-    const unsigned prev = __hip_atomic_fetch_add(&sync[2], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    if (prev == (unsigned)NC - 1) {  // last one out: leave the counters zeroed
-      __hip_atomic_store(&sync[0], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      __hip_atomic_store(&sync[1], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      __hip_atomic_store(&sync[2], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    unsigned* done = P.sync + 4 * seq;
+    const unsigned prev = __hip_atomic_fetch_add(done, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (prev == (unsigned)NC - 1) {  // last one out: leave the flags and the count zeroed
+      unsigned* fl = P.flags + (size_t)seq * kMaxChainChunks;
+      for (int j = 0; j < NC; ++j) __hip_atomic_store(&fl[j], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      __hip_atomic_store(done, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }
   }
 }
@@ -1252,23 +1419,20 @@ __global__ void zero_fill_kernel(uint4* p, size_t n16) {
 struct KernelSet {
   const void* summary;
   const void* output;
-  const void* fused;
-  const void* inlined;
-  const void* inlined_split;  // inline schedule with d_v split in two (d_v = 64 only), else null
   const void* scan;
+  const void* chain;
+  const void* chain_split;  // one launch with d_v split in two (d_v = 64 only), else null
   int threads;
 };
 
 template <int DK, int DV, int C, int IN>
 static KernelSet kernels_for() {
   const void* split = nullptr;
-  if constexpr (DV == 64) split = reinterpret_cast<const void*>(&gla_fused_kernel<DK, DV / 2, C, IN, true>);
+  if constexpr (DV == 64) split = reinterpret_cast<const void*>(&gla_chain_kernel<DK, DV / 2, C, IN>);
   return KernelSet{reinterpret_cast<const void*>(&gla_summary_kernel<DK, DV, C, IN>),
                    reinterpret_cast<const void*>(&gla_output_kernel<DK, DV, C, IN>),
-                   reinterpret_cast<const void*>(&gla_fused_kernel<DK, DV, C, IN, false>),
-                   reinterpret_cast<const void*>(&gla_fused_kernel<DK, DV, C, IN, true>),
-                   split,
-                   reinterpret_cast<const void*>(&gla_scan_kernel<DK, DV, IN != GTR_F32>), tile_threads(C)};
+                   reinterpret_cast<const void*>(&gla_scan_kernel<DK, DV, IN != GTR_F32>),
+                   reinterpret_cast<const void*>(&gla_chain_kernel<DK, DV, C, IN>), split, tile_threads(C)};
 }
 
 template <int DK, int DV, int IN>
@@ -1298,88 +1462,93 @@ static bool select_kernels(const GlaShape& s, KernelSet* ks) {
   }
 }
 
-// AUTO takes the inline schedule while the summaries of one sequence take at
-// most this many bytes (nchunks * dk * dv elements, float32 for float32 inputs,
-// fp16 otherwise): rebuilding a boundary state reads every summary before it,
-// so the cost grows with their total size (measured with float32 summaries:
-// d_k = d_v = 64 at 25 chunks, 400 KB, faster fused; d_k = 32, d_v = 64 at 25
-// chunks, 200 KB, faster inline).
-constexpr int64_t kInlineMaxSummaryBytes = 262144;
-
-// Largest number of work-groups of one kernel that can be resident on one XCD
-// at once (8 XCDs per device), and the XCD's CU count (0 for both if a query
-// fails); cached per (device, kernel).
-static int fused_capacity_per_xcd(const void* kernel, int threads, int* cus_per_xcd = nullptr) {
+// Work-groups of `kernel` resident per CU and the device's CU count (0 if a
+// query fails). The occupancy answer depends only on the kernel and the
+// device, so it is kept in a small table that is filled once per (device,
+// kernel) pair and never changes afterwards.
+static int resident_per_cu(const void* kernel, int threads, int* cus) {
   struct Entry {
     int dev;
     const void* k;
-    int cap, cus;
+    int per_cu, cus;
   };
   static std::mutex mu;
-  static Entry cache[128];
+  static Entry cache[256];
   static int n = 0;
   int dev = 0;
-  if (cus_per_xcd) *cus_per_xcd = 0;
+  *cus = 0;
   if (hipGetDevice(&dev) != hipSuccess) return 0;
   {
     std::lock_guard<std::mutex> lk(mu);
     for (int i = 0; i < n; ++i)
       if (cache[i].dev == dev && cache[i].k == kernel) {
-        if (cus_per_xcd) *cus_per_xcd = cache[i].cus;
-        return cache[i].cap;
+        *cus = cache[i].cus;
+        return cache[i].per_cu;
       }
   }
-  int per_cu = 0, cus = 0;
+  int per_cu = 0, ncu = 0;
   if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kernel, threads, 0) != hipSuccess) return 0;
-  if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) return 0;
-  const int cap = per_cu * (cus / 8);
-  if (cus_per_xcd) *cus_per_xcd = cus / 8;
+  if (hipDeviceGetAttribute(&ncu, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) return 0;
+  *cus = ncu;
   std::lock_guard<std::mutex> lk(mu);
-  if (n < 128) cache[n++] = Entry{dev, kernel, cap, cus / 8};
-  return cap;
+  if (n < 256) cache[n++] = Entry{dev, kernel, per_cu, ncu};
+  return per_cu;
 }
 
-// The fused schedule addresses one sequence's states through a buffer
-// descriptor with a 32-bit range: nchunks * 64 * 64 * 4 bytes must stay below
-// 2^31.
-constexpr int64_t kFusedMaxChunks = 4096;
+struct Plan {
+  int sched;    // GTR_PATH_FUSED (one launch, look-back), GTR_PATH_INLINE (one launch, no inclusive states)
+                // or GTR_PATH_STAGED
+  int vparts;   // value split of the one-launch schedules
+  int desc;     // chunks in descending order (every work-group resident at once)
+  int blk_size;  // chunks per block of the two-level look-back
+  int64_t blocks;
+};
 
-// Length-aware dispatch: short sequences rebuild each boundary state from the
-// summaries (one hand-off), longer ones split the scan over their chunks'
-// work-groups (two hand-offs). Both need every chunk of a sequence resident at
-// once on one XCD, and both lose to the three-launch schedule as soon as an XCD
-// has to run more than one sequence (more than 8 sequences): then the sequences
-// compete for the XCD's slots and partly resident ones spin while they wait for
-// the rest, so AUTO takes the staged schedule there. An explicit one-launch
-// path that does not fit is GTR_ERR_UNSUPPORTED.
-// The inline schedule splits d_v = 64 over two work-groups per chunk (half the
-// value work and half the summary bytes that each chunk's rebuild reads) when
-// there is no output-gate epilogue (its RMSNorm needs whole rows) and the
-// doubled grid still gives every work-group a CU of its own (the split grid is
-// spread over all XCDs: work-group b runs on XCD b % 8). Measured at 40x40
-// tokens, fp16, d_k = d_v = 64: 4 heads 11.5 against 13.2 us, 2 heads 11.4
-// against 12.9; at 6 heads (300 work-groups, some CUs running two) no gain, and
-// for d_k = 32 at 6 heads 13.3 against 10.7 us. *vparts is 1 or 2.
-static gtr_status choose_schedule(const GlaShape& s, int path, bool gate, const KernelSet& ks, int* sched,
-                                  int* vparts) {
-  *sched = GTR_PATH_STAGED;
-  *vparts = 1;
-  const bool auto_one_launch = path == GTR_PATH_AUTO && s.BH <= 8;
-  if (path == GTR_PATH_FUSED || path == GTR_PATH_INLINE || auto_one_launch) {
-    const bool inl = path == GTR_PATH_INLINE ||
-                     (path == GTR_PATH_AUTO &&
-                      s.nchunks * s.dk * s.dv * (s.qdt == GTR_F32 ? 4 : 2) <= kInlineMaxSummaryBytes);
-    const int cap = fused_capacity_per_xcd(inl ? ks.inlined : ks.fused, ks.threads);
-    const bool fits = cap > 0 && s.nchunks <= cap && s.nchunks <= kFusedMaxChunks && s.BH <= kSyncSeqs;
-    if (path != GTR_PATH_AUTO && !fits) return GTR_ERR_UNSUPPORTED;
-    if (fits) *sched = inl ? GTR_PATH_INLINE : GTR_PATH_FUSED;
-    if (fits && inl && !gate && ks.inlined_split && 2 * s.BH <= kSyncSeqs) {
-      int cus = 0;
-      const int scap = fused_capacity_per_xcd(ks.inlined_split, ks.threads, &cus);
-      const int64_t per_xcd = (2 * s.BH * s.nchunks + 7) / 8;
-      if (per_xcd <= scap && per_xcd <= cus) *vparts = 2;
-    }
+// Length-aware dispatch (the paper's operator appendix switches to inline
+// prefixes for short sequences and co-runs the scan with the outputs
+// otherwise):
+//   * one launch whenever the flags fit (at most kSyncSeqs sequences of at
+//     most kMaxChainChunks chunks); INLINE (every chunk reads all summaries
+//     before it, no inclusive states) while a sequence has at most
+//     kInlineMaxChunks chunks and the whole grid is resident at once, FUSED
+//     (look-back to the nearest inclusive state) otherwise;
+//   * the value split (d_v = 64 in two halves, no output gate: its RMSNorm needs
+//     whole rows) when the doubled grid still gives every work-group a CU of
+//     its own;
+//   * the chunk-major grid, in descending chunk order when every work-group is
+//     resident at once.
+// An explicit path that does not fit is GTR_ERR_UNSUPPORTED; STAGED always fits.
+constexpr int64_t kInlineMaxChunks = 32;
+constexpr int kBlockChunks = 32;  // chunks per block of the one-launch look-back
+
+static gtr_status plan_call(const GlaShape& s, int path, bool gate, const KernelSet& ks, Plan* pl) {
+  pl->sched = GTR_PATH_STAGED;
+  pl->vparts = 1;
+  pl->desc = 0;
+  pl->blk_size = 2;
+  pl->blocks = 0;
+  if (path == GTR_PATH_STAGED) return GTR_OK;
+  const bool fits = s.nchunks <= kMaxChainChunks && s.BH <= kSyncSeqs;
+  if (!fits) return path == GTR_PATH_AUTO ? GTR_OK : GTR_ERR_UNSUPPORTED;
+  int cus = 0;
+  const int per_cu = resident_per_cu(ks.chain, ks.threads, &cus);
+  const int64_t resident = (int64_t)per_cu * cus;  // 0 without a usable device
+  if (!gate && ks.chain_split && 2 * s.BH <= kSyncSeqs && cus > 0 && 2 * s.BH * s.nchunks <= cus) {
+    int c2 = 0;
+    if (resident_per_cu(ks.chain_split, ks.threads, &c2) > 0) pl->vparts = 2;
   }
+  const int64_t ns = s.BH * pl->vparts;
+  const bool all_resident = resident > 0 && ns * s.nchunks <= resident;
+  if (path == GTR_PATH_AUTO)
+    pl->sched = all_resident && s.nchunks <= kInlineMaxChunks ? GTR_PATH_INLINE : GTR_PATH_FUSED;
+  else
+    pl->sched = path;
+  pl->desc = all_resident ? 1 : 0;
+  // blocks of 32 chunks: a sequence of at most 32 chunks has one block and a
+  // single-level look-back; longer ones read at most 31 summaries and 7 block
+  // prefixes (kMaxChainChunks / 32 - 1), which bounds what one wave polls at once
+  pl->blk_size = kBlockChunks;
+  pl->blocks = ns * s.nchunks;
   return GTR_OK;
 }
 
@@ -1407,25 +1576,25 @@ extern "C" int gtr_gla_workspace_fault(const void* workspace, size_t bytes) {
   if (!workspace || bytes < 256) return -1;
   unsigned v = 0;
   if (hipMemcpy(&v, workspace, sizeof(v), hipMemcpyDeviceToHost) != hipSuccess) return -1;
-  return v != 0;
+  return (int)(v & 0xffu);
+}
+
+static int plan_query(const gtr_gla_args* a, Plan* pl) {
+  GlaShape s;
+  KernelSet ks;
+  if (!a || gla_shape_from_args(a, &s, /*check_pointers=*/false) != GTR_OK || !select_kernels(s, &ks)) return -1;
+  if (plan_call(s, a->path, a->out_gate != nullptr, ks, pl) != GTR_OK) return -1;
+  return 0;
 }
 
 extern "C" int gtr_gla_schedule(const gtr_gla_args* a) {
-  GlaShape s;
-  KernelSet ks;
-  int sched = -1, vparts = 1;
-  if (!a || gla_shape_from_args(a, &s, /*check_pointers=*/false) != GTR_OK || !select_kernels(s, &ks)) return -1;
-  if (choose_schedule(s, a->path, a->out_gate != nullptr, ks, &sched, &vparts) != GTR_OK) return -1;
-  return sched;
+  Plan pl;
+  return plan_query(a, &pl) ? -1 : pl.sched;
 }
 
 extern "C" int gtr_gla_value_parts(const gtr_gla_args* a) {
-  GlaShape s;
-  KernelSet ks;
-  int sched = -1, vparts = 1;
-  if (!a || gla_shape_from_args(a, &s, /*check_pointers=*/false) != GTR_OK || !select_kernels(s, &ks)) return -1;
-  if (choose_schedule(s, a->path, a->out_gate != nullptr, ks, &sched, &vparts) != GTR_OK) return -1;
-  return vparts;
+  Plan pl;
+  return plan_query(a, &pl) ? -1 : pl.vparts;
 }
 
 extern "C" gtr_status gtr_gla_fwd(const gtr_gla_args* a, hipStream_t stream) {
@@ -1435,6 +1604,9 @@ extern "C" gtr_status gtr_gla_fwd(const gtr_gla_args* a, hipStream_t stream) {
   if (st != GTR_OK) return st;
   KernelSet ks;
   if (!select_kernels(s, &ks)) return GTR_ERR_UNSUPPORTED;
+  Plan pl;
+  st = plan_call(s, a->path, a->out_gate != nullptr, ks, &pl);
+  if (st != GTR_OK) return st;
 
   const WorkspaceLayout lay = gla_workspace_layout(s);
   char* ws = static_cast<char*>(a->workspace);
@@ -1458,10 +1630,12 @@ extern "C" gtr_status gtr_gla_fwd(const gtr_gla_args* a, hipStream_t stream) {
   P.scan = a->scan;
   P.fault = reinterpret_cast<unsigned*>(ws + lay.fault_off);
   P.sync = reinterpret_cast<unsigned*>(ws + lay.sync_off);
+  P.flags = reinterpret_cast<unsigned*>(ws + lay.flags_off);
+  P.agg = ws + lay.agg_off;
+  P.blk = ws + lay.blk_off;
+  P.blkrec = reinterpret_cast<float*>(ws + lay.blkrec_off);
+  P.rec = reinterpret_cast<float*>(ws + lay.rec_off);
   P.states = reinterpret_cast<float*>(ws + lay.states_off);
-  P.decays = reinterpret_cast<float*>(ws + lay.decays_off);
-  P.states16 = lay.states16_off ? reinterpret_cast<unsigned short*>(ws + lay.states16_off) : nullptr;
-  P.groups = (int)((s.BH + 7) / 8);
   P.gkind = a->g_kind;
   P.inv_tau = a->g_kind == GTR_GATE_LOGITS ? 1.f / a->gate_tau : 1.f;
   P.gate = a->out_gate;
@@ -1469,19 +1643,18 @@ extern "C" gtr_status gtr_gla_fwd(const gtr_gla_args* a, hipStream_t stream) {
   P.gatedt = a->out_gate_dtype;
   P.eps = a->norm_eps;
   P.dvp = s.dv;
-
-  int sched = GTR_PATH_STAGED;
-  const gtr_status cs = choose_schedule(s, a->path, a->out_gate != nullptr, ks, &sched, &P.vparts);
-  if (cs != GTR_OK) return cs;
-  const void* one_launch = sched == GTR_PATH_INLINE ? (P.vparts > 1 ? ks.inlined_split : ks.inlined)
-                           : sched == GTR_PATH_FUSED ? ks.fused
-                                                     : nullptr;
+  P.vparts = pl.vparts;
+  P.ns = (int)(s.BH * pl.vparts);
+  P.desc = pl.desc;
+  P.publish = pl.sched == GTR_PATH_FUSED;
+  P.blk_size = pl.blk_size;
+  P.spin = a->spin_limit ? a->spin_limit : kSpinDefault;
 
   void* kargs[] = {&P};
   hipError_t err;
-  if (one_launch) {
-    const int64_t blocks = P.vparts > 1 ? (int64_t)P.vparts * s.BH * s.nchunks : (int64_t)8 * P.groups * s.nchunks;
-    err = hipLaunchKernel(one_launch, dim3((unsigned)blocks), dim3(ks.threads), kargs, 0, stream);
+  if (pl.sched != GTR_PATH_STAGED) {
+    const void* k = pl.vparts > 1 ? ks.chain_split : ks.chain;
+    err = hipLaunchKernel(k, dim3((unsigned)pl.blocks), dim3(ks.threads), kargs, 0, stream);
   } else {
     err = hipLaunchKernel(ks.summary, dim3((unsigned)s.nchunks, (unsigned)s.BH), dim3(ks.threads), kargs, 0, stream);
     if (err == hipSuccess) {

@@ -52,10 +52,11 @@ gtr_status gla_shape_from_args(const gtr_gla_args* a, GlaShape* s, bool check_po
   // a 32-bit range (and use 0x7fffff00 as their out-of-range offset)
   if (L * dmax * 4 >= 0x7fffff00LL) return GTR_ERR_SHAPE;
   const int64_t nchunks = (L + a->chunk - 1) / a->chunk;
-  // launch-grid limits: staged grids are (nchunks, BH); the fused grid is 1-D
-  int64_t fused_blocks;
+  // launch-grid limits: staged grids are (nchunks, BH); the one-launch grid is
+  // 1-D, at most (2 BH rounded up to 8) * nchunks work-groups
+  int64_t chain_blocks;
   if (BH > 65535 || nchunks > 0x7fffffff) return GTR_ERR_SHAPE;
-  if (!mul_ok((BH + 7) / 8 * 8, nchunks, &fused_blocks) || fused_blocks > 0x7fffffff) return GTR_ERR_SHAPE;
+  if (!mul_ok((2 * BH + 7) / 8 * 8, nchunks, &chain_blocks) || chain_blocks > 0x7fffffff) return GTR_ERR_SHAPE;
   int64_t st;
   if (!mul_ok(BH * nchunks, (int64_t)a->dk * a->dv * 4, &st)) return GTR_ERR_SHAPE;
 
@@ -117,17 +118,19 @@ WorkspaceLayout gla_workspace_layout(const GlaShape& s) {
   off += 256;
   w.sync_off = off;
   off = align256(off + (size_t)kSyncSeqs * 4 * sizeof(uint32_t));
-  // chunk summaries and boundary states travel in float32 for float32 inputs,
-  // in fp16 (states16) for 16-bit inputs; the other region has size 0
+  w.flags_off = off;
+  off = align256(off + (size_t)kSyncSeqs * kMaxChainChunks * sizeof(uint32_t));
+  const size_t tiles = (size_t)s.BH * s.nchunks;  // (sequence, chunk) pairs; the value split keeps the total
+  w.agg_off = off;
+  off = align256(off + tiles * s.dk * s.dv * (s.qdt == GTR_F32 ? 4 : 2));
+  w.rec_off = off;
+  off = align256(off + 2 * tiles * (s.dk + 4) * sizeof(float));  // two records per chunk under the value split
   w.states_off = off;
-  if (s.qdt == GTR_F32) off = align256(off + (size_t)s.BH * s.nchunks * s.dk * s.dv * sizeof(float));
-  w.decays_off = off;
-  off = align256(off + (size_t)s.BH * s.nchunks * s.dk * sizeof(float));
-  w.states16_off = 0;
-  if (s.qdt != GTR_F32) {
-    w.states16_off = off;
-    off = align256(off + (size_t)s.BH * s.nchunks * s.dk * s.dv * 2);
-  }
+  off = align256(off + tiles * s.dk * s.dv * sizeof(float));
+  w.blk_off = off;
+  off = align256(off + tiles * s.dk * s.dv * (s.qdt == GTR_F32 ? 4 : 2));
+  w.blkrec_off = off;
+  off = align256(off + 2 * tiles * (s.dk + 8) * sizeof(float));
   w.total = off;
   return w;
 }

@@ -16,19 +16,24 @@ struct GlaShape {
   int qdt, gdt, odt;
 };
 
-// The per-sequence hand-off counters of the one-launch schedules live in a
-// region of fixed size right after the 256-byte header, for this many
-// sequences, whatever the shape of a call. Everything else of a workspace
-// starts behind it, so no call of any shape ever writes where another call
-// expects zeroed counters (one workspace can serve calls of different shapes).
+// The synchronisation words of the one-launch schedule (a done count per
+// sequence, one flag per chunk) live in regions of fixed size right after the
+// 256-byte header, for kSyncSeqs sequences of up to kMaxChainChunks chunks,
+// whatever the shape of a call: the word of (sequence s, chunk c) is always at
+// the same place, and every completed call leaves them zeroed, so one workspace
+// serves calls of different shapes. Everything else starts behind them.
 constexpr int64_t kSyncSeqs = 1024;
+constexpr int64_t kMaxChainChunks = 256;
 
 struct WorkspaceLayout {
-  size_t fault_off;   // one 32-bit word (fused-path wait ran out)
+  size_t fault_off;   // one 32-bit word: fault bits of the calls since the last init
   size_t sync_off;    // [kSyncSeqs][4] 32-bit counters
-  size_t states_off;  // [BH][nchunks][dv][dk] float32 (float32 inputs only, else size 0)
-  size_t decays_off;  // [BH][nchunks][dk] float32
-  size_t states16_off;  // [BH][nchunks][dv][dk] fp16 (16-bit inputs only, else 0)
+  size_t flags_off;   // [kSyncSeqs][kMaxChainChunks] 32-bit chunk flags
+  size_t agg_off;     // [BH][nchunks][dk][dv] summaries: fp16 (16-bit inputs) or float32
+  size_t rec_off;     // [2 BH][nchunks][dk + 4] float32 chunk records (decays, summary scale)
+  size_t states_off;  // [BH][nchunks][dk][dv] float32 boundary states
+  size_t blk_off;     // [BH][nchunks][dk][dv] block prefixes of the one-launch look-back (as the summaries)
+  size_t blkrec_off;  // [2 BH][nchunks][dk + 8] float32 block records (decays, per-wave scales)
   size_t total;
 };
 

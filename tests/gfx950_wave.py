@@ -56,6 +56,8 @@ class Inst:
 
 
 def parse_inst(t, idx):
+    # DPP quad permutations print as quad_perm:[a,b,c,d]: keep them one modifier
+    t = re.sub(r'quad_perm:\[(\d),(\d),(\d),(\d)\]', r'quad_perm:\1\2\3\4', t)
     parts = t.split(None, 1)
     op = parts[0]
     ops, mods = [], {}
@@ -732,6 +734,24 @@ def _sbcnt(w, i):
     set_scc(w, r != 0, o, d)
 
 
+@handler('s_bitcmp1_b32', 's_bitcmp0_b32')
+def _sbitcmp(w, i):
+    v, o, d = w.s32(i.ops[0], i)
+    b, bo, bd = w.s32(i.ops[1], i)
+    bit = (v >> (b & 31)) & 1
+    set_scc(w, bit == (1 if i.op == 's_bitcmp1_b32' else 0), bool(o) or bool(bo), bool(d) and bool(bd))
+
+
+@handler('s_ff1_i32_b64', 's_ff1_i32_b32')
+def _sff1(w, i):
+    if i.op.endswith('b64'):
+        v, o, d = w.s64(i.ops[1], i)
+    else:
+        v, o, d = w.s32(i.ops[1], i)
+    r = (v & -v).bit_length() - 1 if v else M32  # index of the lowest set bit, -1 if none
+    w.s32set(i.ops[0], r & M32, M32 if o else 0, d)
+
+
 @handler('s_mov_b64')
 def _smov64(w, i):
     v, o, d = w.s64(i.ops[1], i)
@@ -1039,6 +1059,11 @@ HANDLERS.update({
     'v_max_u32_e32': valu(lambda a, b: np.maximum(a, b), 2),
     'v_min_i32_e32': valu(lambda a, b: np.minimum(a.view(np.int32), b.view(np.int32)).view(np.uint32), 2),
     'v_max_i32_e32': valu(lambda a, b: np.maximum(a.view(np.int32), b.view(np.int32)).view(np.uint32), 2),
+    'v_xad_u32': valu(lambda a, b, c: (u64(a ^ b) + u64(c)) & np.uint64(M32), 3),
+    'v_med3_u32': valu(lambda a, b, c: np.maximum(np.minimum(a, b), np.minimum(np.maximum(a, b), c)), 3),
+    'v_med3_i32': valu(lambda a, b, c: np.maximum(np.minimum(a.view(np.int32), b.view(np.int32)),
+                                                  np.minimum(np.maximum(a.view(np.int32), b.view(np.int32)),
+                                                             c.view(np.int32))).view(np.uint32), 3),
     # float
     'v_add_f32_e32': fop(lambda a, b: a + b, 2), 'v_add_f32_e64': fop(lambda a, b: a + b, 2),
     'v_sub_f32_e32': fop(lambda a, b: a - b, 2), 'v_sub_f32_e64': fop(lambda a, b: a - b, 2),
@@ -1139,7 +1164,7 @@ def dataop(nsrc, first=1):
     return h
 
 
-for _n, _k in [('v_cvt_f32_f16_e32', 1), ('v_cvt_f32_f16_sdwa', 1), ('v_cvt_f16_f32_e32', 1),
+for _n, _k in [('v_cvt_f32_f16_e32', 1), ('v_cvt_f32_f16_e64', 1), ('v_cvt_f32_f16_sdwa', 1), ('v_cvt_f16_f32_e32', 1),
                ('v_cvt_pk_f16_f32', 2), ('v_pack_b32_f16', 2), ('v_perm_b32', 3), ('v_or_b32_sdwa', 2),
                ('v_fma_mixlo_f16', 3), ('v_fma_mixhi_f16', 3), ('v_fma_mix_f32', 3), ('v_cvt_f32_bf16', 1)]:
     HANDLERS[_n] = dataop(_k)
@@ -1382,7 +1407,14 @@ def dpp_src(w, i, tok):
     elif 'row_newbcast' in i.mods:
         n = int(i.mods['row_newbcast'], 0)
         idx = (LANES // 16) * 16 + n
-    elif 'row_bcast' in i.mods or 'wave_shr' in i.mods or 'quad_perm' in i.mods or 'row_ror' in i.mods:
+    elif 'quad_perm' in i.mods:
+        perm = np.array([int(ch) for ch in i.mods['quad_perm']])
+        idx = (LANES // 4) * 4 + perm[LANES % 4]
+    elif 'row_half_mirror' in i.mods:
+        idx = (LANES // 8) * 8 + 7 - LANES % 8
+    elif 'row_mirror' in i.mods:
+        idx = (LANES // 16) * 16 + 15 - LANES % 16
+    elif 'row_bcast' in i.mods or 'wave_shr' in i.mods or 'row_ror' in i.mods:
         raise NotImplementedError(f"dpp {i.mods}")
     valid = valid & act[idx]
     v = src.v[idx].copy()

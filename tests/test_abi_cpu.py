@@ -79,31 +79,46 @@ def fwd(lib, a):
 def test_workspace_size_formula(lib):
     a = base_args(B=2, heads=3, H=40, W=40, dk=64, dv=64, chunk=64)
     BH, nc = 6, 25
-    # header, counters of 1024 sequences, decays, then the summaries / states:
-    # fp16 for 16-bit inputs, float32 (ahead of the decays) for float32 inputs
-    dec = ((BH * nc * 64 * 4 + 255) // 256) * 256
-    want = 256 + 1024 * 16 + dec + BH * nc * 64 * 64 * 2
+    a256 = lambda x: (x + 255) // 256 * 256
+    # header, done counters of 1024 sequences, chunk flags of 1024 x 256, then
+    # the summaries (fp16 for 16-bit inputs, float32 for float32 inputs), the
+    # chunk records (two per chunk for the value split) and the float32 states
+    # and (one-launch look-back) the block prefixes and the block records
+    fixed = 256 + 1024 * 16 + 1024 * 256 * 4
+    rec = a256(2 * BH * nc * (64 + 4) * 4)
+    brec = a256(2 * BH * nc * (64 + 8) * 4)
+    states = BH * nc * 64 * 64 * 4
+    want = fixed + BH * nc * 64 * 64 * 2 + rec + states + BH * nc * 64 * 64 * 2 + brec
     assert a.qkv_dtype != gtr.F32 and lib.gtr_gla_workspace_size(ctypes.byref(a)) == want
     a.qkv_dtype = a.g_dtype = a.o_dtype = gtr.F32
-    assert lib.gtr_gla_workspace_size(ctypes.byref(a)) == 256 + 1024 * 16 + BH * nc * 64 * 64 * 4 + dec
+    want = fixed + BH * nc * 64 * 64 * 4 + rec + states + BH * nc * 64 * 64 * 4 + brec
+    assert lib.gtr_gla_workspace_size(ctypes.byref(a)) == want
     a.dk = 48
     assert lib.gtr_gla_workspace_size(ctypes.byref(a)) == 0
 
 
 def test_schedule_query_without_device(lib):
-    """gtr_gla_schedule: -1 for invalid arguments; without a usable device the
-    one-launch schedules cannot be sized, so AUTO reports STAGED and an explicit
-    one-launch path reports -1 (gtr_gla_fwd would return GTR_ERR_UNSUPPORTED)."""
+    """gtr_gla_schedule: -1 for invalid arguments. AUTO is length-aware: INLINE
+    up to 32 chunks per sequence when the whole grid is resident at once, FUSED
+    up to 256 chunks, STAGED beyond; an explicit one-launch path that does not
+    fit (more than 256 chunks) reports -1. Without a usable device residency is
+    unknown (so AUTO takes FUSED) and the value split is off."""
     assert lib.gtr_gla_schedule(None) == -1
-    a = base_args(B=1, heads=6, H=40, W=40)
-    assert lib.gtr_gla_schedule(ctypes.byref(a)) == 2
-    a.path = 2
+    a = base_args(B=1, heads=6, H=40, W=40)  # 25 chunks
+    assert lib.gtr_gla_schedule(ctypes.byref(a)) == 1
+    a.path = 3
+    assert lib.gtr_gla_schedule(ctypes.byref(a)) == 3
+    a.path = 0
+    a.H = a.W = 80  # 100 chunks
+    assert lib.gtr_gla_schedule(ctypes.byref(a)) == 1
+    a.H = a.W = 200  # 625 chunks
     assert lib.gtr_gla_schedule(ctypes.byref(a)) == 2
     a.path = 1
     assert lib.gtr_gla_schedule(ctypes.byref(a)) == -1
+    a.path, a.H, a.W = 2, 40, 40
+    assert lib.gtr_gla_schedule(ctypes.byref(a)) == 2
     a.path, a.dk = 0, 48
     assert lib.gtr_gla_schedule(ctypes.byref(a)) == -1
-    # the value split is a variant of the inline schedule only
     assert lib.gtr_gla_value_parts(None) == -1
     assert lib.gtr_gla_value_parts(ctypes.byref(a)) == -1
     a.dk = 64

@@ -90,7 +90,7 @@ def test_emulator_flags_out_of_bounds():
 # ---------------------------------------------------------------------------
 DT = {"f32": (0, 4), "f16": (1, 2), "bf16": (2, 2)}
 SCAN = {"row": 0, "col": 1, "row_rev": 2, "col_rev": 3}
-KERNARG_BYTES = 192  # sizeof(GlaParams)
+KERNARG_BYTES = 232  # sizeof(GlaParams)
 
 
 def a256(x):
@@ -134,12 +134,20 @@ class Shape:
         self.NC = (self.L + chunk - 1) // chunk
 
 
-UNMAPPED = 0x7000_0000_0000  # an address inside no registered buffer: any access is reported
+class Launch:
+    """How the one-launch kernel is run: value parts, descending chunk order
+    (every work-group resident), inclusive states published, and the value
+    every chunk flag reads as (FLAG_BLOCKS: summaries and block prefixes, the
+    look-back walks back to the start; FLAG_ALL: inclusive states everywhere as
+    well, it stops at the nearest; FLAG_NONE: nothing is ever ready, every wait
+    runs out after the spin limit)."""
+
+    def __init__(self, vparts=1, desc=0, publish=1, flag=0x00FF0001):
+        self.vparts, self.desc, self.publish, self.flag = vparts, desc, publish, flag
 
 
-def kernel_args(c: Shape, vparts: int = 1):
-    """GlaParams for shape c with every buffer at its own base, and the buffers
-    (vparts = 2: the inline schedule's value split)."""
+def kernel_args(c: Shape, ln: Launch = Launch()):
+    """GlaParams for shape c with every buffer at its own base, and the buffers."""
     regions = []
     nxt = [0x1000_0000_0000]
 
@@ -160,24 +168,31 @@ def kernel_args(c: Shape, vparts: int = 1):
     sf = alloc("s_final", c.BH * c.dk * c.dv * 4, "w") if c.sfinal else 0
     z = alloc("out_gate", c.BH * c.L * c.dv * DT[c.zdt][1], "r") if c.zdt else 0
     nw = alloc("norm_weight", c.dv * 4, "r") if c.zdt and c.weighted else 0
-    # workspace layout of gla_workspace_layout(): fault word, counters, float32
-    # states (float32 inputs), decays, fp16 states (16-bit inputs)
+    # workspace layout of gla_workspace_layout(): header (fault word), done
+    # counters, chunk flags, summaries, chunk records, states
     sync = 256
-    states = a256(sync + 1024 * 16)  # counters of up to 1024 sequences, a fixed region
-    decays = a256(states + (c.BH * c.NC * c.dk * c.dv * 4 if c.dt == "f32" else 0))
-    states16 = a256(decays + c.BH * c.NC * c.dk * 4)
-    total = a256(states16 + (c.BH * c.NC * c.dk * c.dv * 2 if c.dt != "f32" else 0))
+    flags = a256(sync + 1024 * 16)
+    agg = a256(flags + 1024 * 256 * 4)
+    tiles = c.BH * c.NC
+    rec = a256(agg + tiles * c.dk * c.dv * (4 if c.dt == "f32" else 2))
+    states = a256(rec + 2 * tiles * (c.dk + 4) * 4)
+    blk = a256(states + tiles * c.dk * c.dv * 4)
+    blkrec = a256(blk + tiles * c.dk * c.dv * (4 if c.dt == "f32" else 2))
+    total = a256(blkrec + 2 * tiles * (c.dk + 8) * 4)
     ws = alloc("workspace", total, "rw")
-    # hand-off counters read as complete, so every bounded wait ends at once
-    regions.insert(0, emu.Region("sync", ws + sync, vparts * c.BH * 16, "rw", load_value=0x7FFFFFFF))
+    ns = c.BH * ln.vparts
+    regions.insert(0, emu.Region("flags", ws + flags, 1024 * 256 * 4, "rw", load_value=ln.flag))
+    regions.insert(0, emu.Region("sync", ws + sync, ns * 16, "rw"))
     regions.insert(0, emu.Region("fault", ws, 256, "rw"))
     regions.append(emu.Region("kernarg", emu.KERNARG_BASE, KERNARG_BYTES, "r"))
-    kern = struct.pack("<7Q6iqifi4xQQQQiif4xQQifQii", q, k, v, g, o, s0, sf, DT[c.dt][0], DT[c.gdt][0],
+    G = 2
+    while G < 16 and G * G < c.NC:
+        G += 1
+    kern = struct.pack("<7Q6iqifi4x8Qif2Qif6iI4x", q, k, v, g, o, s0, sf, DT[c.dt][0], DT[c.gdt][0],
                        DT[c.odt][0], c.BH, c.H, c.W, c.L, c.NC, c.dk ** -0.5, SCAN[c.scan],
-                       ws + states if c.dt == "f32" else UNMAPPED,  # 16-bit inputs never touch float32 states
-                       ws + decays, ws + sync, ws, (c.BH + 7) // 8, 1 if c.logits else 0, 1.0 / 16,
-                       z, nw, DT[c.zdt][0] if c.zdt else 0, 1e-5, ws + states16 if c.dt != "f32" else 0,
-                       c.dv, vparts)
+                       ws + agg, ws + rec, ws + states, ws + sync, ws + flags, ws + blk, ws + blkrec, ws,
+                       1 if c.logits else 0, 1.0 / 16, z, nw, DT[c.zdt][0] if c.zdt else 0, 1e-5,
+                       c.dv, ln.vparts, ns, ln.desc, ln.publish, G, 8)
     assert len(kern) == KERNARG_BYTES
     return kern, regions
 
@@ -190,14 +205,14 @@ def mangled(kind: str, c: Shape) -> str:
         return f"_ZN3gtr17gla_output_kernel{t}EEvNS_9GlaParamsE"
     if kind == "scan":
         return f"_ZN3gtr15gla_scan_kernelILi{c.dk}ELi{c.dv}ELb{int(c.dt != 'f32')}EEEvNS_9GlaParamsE"
-    if kind == "inline_split":  # d_v / 2 columns per work-group
-        return f"_ZN3gtr16gla_fused_kernelILi{c.dk}ELi{c.dv // 2}ELi{c.chunk}ELi{DT[c.dt][0]}ELb1EEEvNS_9GlaParamsE"
-    return f"_ZN3gtr16gla_fused_kernel{t}Lb{1 if kind == 'inline' else 0}EEEvNS_9GlaParamsE"
+    if kind == "chain_split":  # d_v / 2 columns per work-group
+        return f"_ZN3gtr16gla_chain_kernelILi{c.dk}ELi{c.dv // 2}ELi{c.chunk}ELi{DT[c.dt][0]}EEEvNS_9GlaParamsE"
+    return f"_ZN3gtr16gla_chain_kernel{t}EEvNS_9GlaParamsE"
 
 
-def work_groups(kind: str, c: Shape):
+def work_groups(kind: str, c: Shape, ln: Launch):
     """First, second and last chunk of the first and last sequence (+ one block
-    of the one-launch grid that has no sequence)."""
+    of the XCD-ordered grid that has no sequence)."""
     nw = c.chunk // 16
     cs = sorted({0, 1 % c.NC, c.NC - 1})
     bhs = sorted({0, c.BH - 1})
@@ -206,37 +221,50 @@ def work_groups(kind: str, c: Shape):
     if kind == "scan":
         eb = (c.dk * c.dv + 255) // 256
         return [((x, bh, 0), 2) for x in sorted({0, eb - 1}) for bh in bhs]  # 128 threads
-    if kind == "inline_split":  # block b: sequence b % ns (head, part), chunk NC - 1 - b // ns
-        ns = 2 * c.BH
-        return [(((c.NC - 1 - cc) * ns + sq, 0, 0), nw) for cc in cs for sq in sorted({0, 1, ns - 1})]
-    picks = {((bh // 8 * c.NC + cc) << 3) | (bh % 8) for bh in bhs for cc in cs}
-    last = (c.BH + 7) // 8 - 1
-    spare = [x for x in range(8) if last * 8 + x >= c.BH]
-    if spare:
-        picks.add(((last * c.NC) << 3) | spare[0])
-    return [((b, 0, 0), nw) for b in sorted(picks)]
+    ns = c.BH * ln.vparts
+    seqs = sorted({0, ns - 1})
+    # chunk-major grid: block row * ns + seq, row = chunk (or NC - 1 - chunk)
+    rows = sorted({(c.NC - 1 - cc) if ln.desc else cc for cc in cs})
+    return [((r * ns + sq, 0, 0), nw) for r in rows for sq in seqs]
 
 
 # (shape, kernels): the bf16 instantiations, float32 gates with 16-bit inputs,
-# every chunk size, reversed and column scans, S0 / S_final, partial chunks
+# every chunk size, reversed and column scans, S0 / S_final, partial chunks;
+# the one-launch kernel in both chunk orders, both flag states and the value split
+CHAIN = ("chain", "chain_x", "chain_i")
 CHECKS = [
     (Shape(1, 12, 40, 40, 64, 64, 64, "bf16", "bf16", "f32", "row", False, False),
-     ("summary", "scan", "output", "fused", "inline", "inline_split")),
-    (Shape(8, 12, 40, 40, 64, 64, 64, "bf16", "bf16", "f32", "col_rev", True, True), ("output", "fused", "inline")),
-    (Shape(2, 9, 12, 20, 32, 32, 32, "bf16", "f32", "f32", "col", True, True), ("summary", "output", "fused")),
-    (Shape(1, 2, 20, 20, 32, 64, 128, "bf16", "bf16", "bf16", "row_rev", False, False), ("output", "fused")),
-    (Shape(1, 6, 40, 40, 64, 64, 64, "f16", "f16", "f16", "row", False, False), ("fused",)),
-    (Shape(1, 3, 7, 9, 64, 64, 128, "f16", "f32", "f32", "col", True, True), ("output", "inline", "inline_split")),
-    (Shape(1, 2, 13, 11, 64, 64, 32, "f32", "f32", "f32", "row_rev", True, True), ("inline", "inline_split")),
-    (Shape(1, 2, 13, 11, 32, 32, 32, "f32", "f32", "f32", "row", False, True), ("summary", "output", "fused")),
-    (Shape(1, 6, 128, 128, 32, 64, 64, "f16", "f16", "f16", "row", False, False),
-     ("summary", "scan", "output", "fused", "inline", "inline_split")),
+     ("summary", "scan", "output") + CHAIN + ("chain_split",)),
+    (Shape(8, 12, 40, 40, 64, 64, 64, "bf16", "bf16", "f32", "col_rev", True, True), ("output",) + CHAIN),
+    (Shape(2, 9, 12, 20, 32, 32, 32, "bf16", "f32", "f32", "col", True, True), ("summary", "output") + CHAIN),
+    (Shape(1, 2, 20, 20, 32, 64, 128, "bf16", "bf16", "bf16", "row_rev", False, False), ("output",) + CHAIN),
+    (Shape(1, 6, 40, 40, 64, 64, 64, "f16", "f16", "f16", "row", False, False), CHAIN + ("chain_split",)),
+    (Shape(1, 3, 7, 9, 64, 64, 128, "f16", "f32", "f32", "col", True, True), ("output",) + CHAIN + ("chain_split",)),
+    (Shape(1, 2, 13, 11, 64, 64, 32, "f32", "f32", "f32", "row_rev", True, True), CHAIN + ("chain_split",)),
+    (Shape(1, 2, 13, 11, 32, 32, 32, "f32", "f32", "f32", "row", False, True), ("summary", "output") + CHAIN),
+    (Shape(1, 6, 80, 80, 64, 64, 64, "f16", "f16", "f16", "row", False, False), ("scan",) + CHAIN),
     # gate fusion and the output-gate epilogue
     (Shape(1, 12, 40, 40, 64, 64, 64, "bf16", "bf16", "f32", "col", True, True, True, "bf16", True),
-     ("summary", "output", "fused", "inline")),
+     ("summary", "output") + CHAIN),
     (Shape(1, 3, 7, 9, 32, 64, 32, "f16", "f32", "f16", "row_rev", False, False, True, "f32", False),
-     ("summary", "output", "fused")),
+     ("summary", "output", "chain")),
 ]
+
+
+FLAG_BLOCKS, FLAG_ALL, FLAG_NONE = 0x00FF0001, 0x00FFFF01, 0
+
+
+def launches(kind: str, c: Shape):
+    """The launch variants a kind stands for."""
+    if kind == "chain":  # ascending chunks, summaries and block prefixes: the look-back reads back to the start
+        return [Launch(flag=FLAG_BLOCKS), Launch(flag=FLAG_NONE)]
+    if kind == "chain_x":  # descending chunks, inclusive states everywhere
+        return [Launch(desc=1, flag=FLAG_ALL)]
+    if kind == "chain_i":  # no inclusive states published (the inline form)
+        return [Launch(desc=1, publish=0, flag=FLAG_BLOCKS)]
+    if kind == "chain_split":
+        return [Launch(vparts=2, flag=FLAG_BLOCKS), Launch(vparts=2, desc=1, flag=FLAG_ALL)]
+    return [Launch()]
 
 
 @pytest.fixture(scope="module")
@@ -249,19 +277,20 @@ def test_gla_kernel_addresses(asm_text, case):
     c, kinds = CHECKS[case]
     names = set(emu.kernel_names(asm_text))
     for kind in kinds:
-        kern, regions = kernel_args(c, 2 if kind == "inline_split" else 1)
-        name = mangled(kind, c)
+        name = mangled(kind if kind == "chain_split" else kind.split("_")[0], c)
         assert name in names, f"no kernel {name} in the listing"
         prog, labels, desc = emu.parse_kernel(asm_text, name)
         assert desc["amdhsa_kernarg_size"] == KERNARG_BYTES
-        rep = emu.Report()
-        for wg, nw in work_groups(kind, c):
-            for wave in range(nw):
-                emu.run_wave(prog, labels, desc, kern, regions, desc["amdhsa_group_segment_fixed_size"], wg,
-                             wave, rep)
-        bad = {k: sorted(v)[:4] for k, v in rep.items.items() if k.startswith(("ERR", "WARN", "NOTIMPL"))}
-        assert not bad, f"{kind}: {bad}"
-        assert "INFO-PATHLIMIT" not in rep.counts, f"{kind}: not every branch outcome was explored"
+        for ln in launches(kind, c):
+            kern, regions = kernel_args(c, ln)
+            rep = emu.Report()
+            for wg, nw in work_groups(kind.split("_")[0] if kind != "chain_split" else kind, c, ln):
+                for wave in range(nw):
+                    emu.run_wave(prog, labels, desc, kern, regions, desc["amdhsa_group_segment_fixed_size"], wg,
+                                 wave, rep)
+            bad = {k: sorted(v)[:4] for k, v in rep.items.items() if k.startswith(("ERR", "WARN", "NOTIMPL"))}
+            assert not bad, f"{kind}: {bad}"
+            assert "INFO-PATHLIMIT" not in rep.counts, f"{kind}: not every branch outcome was explored"
 
 
 # ---------------------------------------------------------------------------

@@ -43,8 +43,8 @@ def _reference(wl: Workload, scan: str):
     return o, sf
 
 
-ONE_LAUNCH_UNFIT = ("a single-launch schedule needs every chunk of a sequence resident on one XCD at "
-                    "once; the library reports GTR_ERR_UNSUPPORTED for this shape")
+ONE_LAUNCH_UNFIT = ("the single-launch schedules take at most 1024 sequences of 256 chunks; the library "
+                    "reports GTR_ERR_UNSUPPORTED for this shape")
 
 
 def call(gtr, *args, path, **kw):
@@ -143,16 +143,16 @@ def test_value_split_parity(gtr, case):
     kw = dict(H=H, W=W, chunk=chunk, scan=scan, s0=s0t, want_final=final, o_dtype=torch_dtype(odtype))
     for path in ("inline", "auto"):
         assert gtr.gtr_gla_schedule(q, k, v, g, path=path, **kw) == "inline"
+    for path in ("inline", "fused", "auto"):
         assert gtr.gtr_gla_value_parts(q, k, v, g, path=path, **kw) == 2
     o_ref, sf_ref = oracle.gla(inp["q"], inp["k"], inp["v"], inp["g"], inp["s0"], scale=wl.scale, H=H, W=W,
                                scan=scan)
-    o, sf = run_gpu(gtr, wl, scan, chunk, "inline", inp)
     tol = tol_for(dtype, odtype)
-    assert rel_err(o, o_ref) <= tol, rel_err(o, o_ref)
-    if final:
-        assert rel_err(sf, sf_ref) <= tol_for(dtype, "f32"), rel_err(sf, sf_ref)
-    o2, _ = run_gpu(gtr, wl, scan, chunk, "inline", inp)
-    assert torch.equal(o, o2)  # run to run: same work-group for each output element
+    for path in ("inline", "fused"):
+        o, sf = run_gpu(gtr, wl, scan, chunk, path, inp)
+        assert rel_err(o, o_ref) <= tol, (path, rel_err(o, o_ref))
+        if final:
+            assert rel_err(sf, sf_ref) <= tol_for(dtype, "f32"), (path, rel_err(sf, sf_ref))
 
 
 @pytest.mark.parametrize("path", PATHS)
@@ -234,7 +234,7 @@ def test_canaries_and_inputs_untouched(gtr):
             assert torch.equal(a, b)
 
 
-@pytest.mark.parametrize("path", PATHS)
+@pytest.mark.parametrize("path", ("staged", "inline", "auto"))
 def test_deterministic(gtr, path):
     wl = WORKLOADS["kbench"]
     o1, _ = run_gpu(gtr, wl, "col", 64, path)
@@ -242,35 +242,55 @@ def test_deterministic(gtr, path):
     assert torch.equal(o1, o2)
 
 
+def test_fused_repeats_to_rounding(gtr):
+    """The FUSED look-back stops at whichever inclusive state is ready when a
+    chunk looks back, so the order of the state's sum (and with it the last
+    bits) can change from call to call; the results agree to rounding (here one
+    ulp of the fp16 output, 2^-10 of the largest output), and each is within the
+    parity bar of the oracle."""
+    wl = WORKLOADS["highres"]
+    o_ref, _ = _reference(wl, "row")
+    o1, _ = run_gpu(gtr, wl, "row", 64, "fused")
+    for _ in range(3):
+        o2, _ = run_gpu(gtr, wl, "row", 64, "fused")
+        assert rel_err(o1, o2.double().cpu().numpy()) <= 2.0 ** -10
+        assert rel_err(o2, o_ref) <= 2e-3
+
+
 def test_workspace_reuse_and_no_fault(gtr):
     ws = gtr.Workspace()
     dev = torch.device("cuda")
     results = []
-    for name in ("kbench", "tiny", "kbench"):
+    for name, path in (("kbench", "auto"), ("tiny", "fused"), ("kbench", "fused"), ("kbench", "auto")):
         wl = WORKLOADS[name]
         inp = make_inputs(wl)
         q, k, v, g = (inp[n].to(dev) for n in ("q", "k", "v", "g"))
         s0 = None if inp["s0"] is None else inp["s0"].to(dev)
         o, _ = call(gtr, q, k, v, g, H=wl.H, W=wl.W, scale=wl.scale, s0=s0,
-                    o_dtype=torch_dtype(wl.odtype), path="auto", workspace=ws)
+                    o_dtype=torch_dtype(wl.odtype), path=path, workspace=ws)
         torch.cuda.synchronize()
         assert gtr.gtr_gla_workspace_fault(ws.buf) == 0
         results.append(o)
-    assert torch.equal(results[0], results[2])
-    # the per-sequence counters (4 words per sequence after the 256-byte
-    # header) are back to zero after each call
-    n_seq = WORKLOADS["kbench"].B * WORKLOADS["kbench"].heads
-    assert int(ws.buf[256:256 + 16 * n_seq].view(torch.int32).abs().sum()) == 0
+        # the done counters (4 words per sequence after the 256-byte header) and
+        # the chunk flags (256 words per sequence after the counters of 1024
+        # sequences) are back to zero after each call
+        n_seq = 2 * wl.B * wl.heads  # value split: two sequences per head
+        assert int(ws.buf[256:256 + 16 * n_seq].view(torch.int32).abs().sum()) == 0
+        flags = 16640
+        assert int(ws.buf[flags:flags + 1024 * n_seq].view(torch.int32).abs().sum()) == 0
+    assert torch.equal(results[0], results[3])
 
 
 @pytest.mark.parametrize("name,heads,want,parts", [
     ("kbench", None, "inline", 1), ("tiny", None, "inline", 1), ("op1600", None, "inline", 1),
     ("op256", None, "inline", 2), ("kbench", 4, "inline", 2), ("op1600", 2, "inline", 2),
-    ("directions", None, "staged", 1), ("batched", None, "staged", 1), ("highres", None, "staged", 1),
-    ("op16k", None, "staged", 1)])
+    ("directions", None, ("inline", "fused"), 1), ("batched", None, "fused", 1), ("highres", None, "fused", 1),
+    ("op16k", None, "fused", 1), ("tiny", 1100, "staged", 1)])
 def test_auto_schedule(gtr, name, heads, want, parts):
-    """AUTO's choice (the length-aware dispatch) as gtr_gla_schedule reports it,
-    and the inline value split (one work-group per CU after doubling: 4 x 25
+    """AUTO's choice (the length-aware dispatch) as gtr_gla_schedule reports it:
+    INLINE up to 32 chunks while the whole grid is resident (two work-groups per
+    CU: 512), FUSED up to 256 chunks and 1024 sequences, STAGED beyond; the value
+    split where the doubled grid gives every work-group its own CU (4 x 25
     chunks x 2 = 200 work-groups split, 6 x 25 x 2 = 300 do not)."""
     wl = WORKLOADS[name] if heads is None else WORKLOADS[name].with_(heads=heads)
     dev = torch.device("cuda")
@@ -278,7 +298,8 @@ def test_auto_schedule(gtr, name, heads, want, parts):
     s0 = torch.empty((wl.B, wl.heads, wl.dk, wl.dv), device=dev) if wl.s0_std is not None else None
     kw = dict(H=wl.H, W=wl.W, chunk=wl.chunk, s0=s0, want_final=wl.want_final, o_dtype=torch_dtype(wl.odtype))
     got = gtr.gtr_gla_schedule(mk(wl.dk), mk(wl.dk), mk(wl.dv), mk(wl.dk), **kw)
-    assert got == want
+    # 12 x 25 = 300 work-groups are all resident (INLINE) only at two work-groups per CU
+    assert got in want if isinstance(want, tuple) else got == want
     assert gtr.gtr_gla_value_parts(mk(wl.dk), mk(wl.dk), mk(wl.dv), mk(wl.dk), **kw) == parts
     assert gtr.gtr_gla_schedule(mk(wl.dk), mk(wl.dk), mk(wl.dv), mk(wl.dk), H=wl.H, W=wl.W, chunk=wl.chunk,
                                 path="staged") == "staged"
@@ -289,8 +310,11 @@ def test_paths_agree(gtr):
     for scan in wl.scans:
         a, _ = run_gpu(gtr, wl, scan, 64, "fused")
         b, _ = run_gpu(gtr, wl, scan, 64, "staged")
-        # same arithmetic per element in both schedules except the state scan split
-        assert rel_err(a, b.double().cpu().numpy()) <= 1e-5
+        # the same arithmetic except the order in which the boundary state is
+        # summed (look-back nearest first against the scan's chunk order), so an
+        # fp16 rounding of S can flip: well below the 2e-3 parity bar that each
+        # schedule meets against the oracle on its own
+        assert rel_err(a, b.double().cpu().numpy()) <= 2e-4
 
 
 def test_graph_replays_match_eager(gtr):
@@ -423,6 +447,153 @@ def test_workspace_shared_across_shapes(gtr):
         run(small, first_path)  # a smaller call writes its chunk states
         o = run(big, big_path)
         assert rel_err(o, ref_big) <= tol_for(big.dtype, big.odtype), (first_path, big_path)
+
+
+# ---------------------------------------------------------------------------
+# failure handling of the one-launch schedules, forced from the host, and the
+# fp16 range of the intermediates
+# ---------------------------------------------------------------------------
+
+def _chunk_rows(o, wl, scan, chunk):
+    """o [B, heads, L, dv] in spatial order -> [B, heads, n_chunks, rows] scan-order views."""
+    order = oracle.scan_order(wl.H, wl.W, scan)
+    x = o.detach().double().cpu().numpy()[:, :, order, :]
+    nc = (wl.L + chunk - 1) // chunk
+    return [x[:, :, c * chunk:(c + 1) * chunk, :] for c in range(nc)]
+
+
+@pytest.mark.parametrize("path", ["fused", "inline"])
+def test_forced_give_up_poisons_and_reports(gtr, path):
+    """A one-launch work-group that gives up waiting (a spin limit of one poll,
+    set from the host) writes NaN into its rows and into the state it hands
+    over, sets bit 0 of the fault word and exits normally; every row that is
+    not NaN is still correct, and the next clean call on a re-initialised
+    workspace is clean."""
+    wl = WORKLOADS["highres"].with_(s0_std=0.1, want_final=True, odtype="f32")
+    inp = make_inputs(wl)
+    o_ref, sf_ref = _reference(wl, "row")
+    dev = torch.device("cuda")
+    q, k, v, g = (inp[n].to(dev) for n in ("q", "k", "v", "g"))
+    s0 = inp["s0"].to(dev)
+    ws = gtr.Workspace(dev)
+    faulted = False
+    for attempt in range(5):
+        if ws.buf is not None:
+            gtr.gtr_gla_workspace_init(ws.buf)
+        o, sf = gtr.gtr_gla_fwd(q, k, v, g, H=wl.H, W=wl.W, scale=wl.scale, s0=s0, want_final=True,
+                                o_dtype=torch.float32, path=path, workspace=ws, spin_limit=1)
+        torch.cuda.synchronize()
+        fault = gtr.gtr_gla_workspace_fault(ws.buf)
+        rows = _chunk_rows(o, wl, "row", wl.chunk)
+        refs = _chunk_rows(torch.from_numpy(o_ref), wl, "row", wl.chunk)
+        scale = np.max(np.abs(o_ref)) + 1e-6
+        nan_chunks = 0
+        for c, (x, r) in enumerate(zip(rows, refs)):
+            for b in range(wl.B):
+                for h in range(wl.heads):
+                    xc = x[b, h]
+                    if np.isnan(xc).any():
+                        assert np.isnan(xc).all(), f"chunk {c} of head {h} partly NaN"
+                        nan_chunks += 1
+                    else:
+                        assert np.max(np.abs(xc - r[b, h])) / scale <= 2e-3, f"chunk {c} head {h} wrong"
+        sfn = sf.detach().double().cpu().numpy()
+        for h in range(wl.heads):
+            if not np.isnan(sfn[0, h]).all():
+                assert not np.isnan(sfn[0, h]).any()
+                assert np.max(np.abs(sfn[0, h] - sf_ref[0, h])) / (np.max(np.abs(sf_ref)) + 1e-6) <= 2e-3
+        assert (fault & 1) == (1 if nan_chunks else 0), (fault, nan_chunks)
+        if nan_chunks:
+            faulted = True
+            break
+    assert faulted, "a spin limit of one poll never made a wait give up on a 100-chunk sequence"
+    gtr.gtr_gla_workspace_init(ws.buf)
+    o, sf = gtr.gtr_gla_fwd(q, k, v, g, H=wl.H, W=wl.W, scale=wl.scale, s0=s0, want_final=True,
+                            o_dtype=torch.float32, path=path, workspace=ws)
+    torch.cuda.synchronize()
+    assert gtr.gtr_gla_workspace_fault(ws.buf) == 0
+    assert rel_err(o, o_ref) <= 2e-3 and rel_err(sf, sf_ref) <= 2e-3
+
+
+@pytest.mark.parametrize("path", PATHS)
+def test_bf16_outside_fp16_range_is_reported(gtr, path):
+    """A bf16 value beyond the fp16 range cannot be an fp16 MFMA operand: bit 1
+    of the fault word is set and the work-groups that read it write NaN for
+    their chunk and hand NaN on to every chunk after it. Everything that does
+    not depend on the value stays correct: the chunks before it, the other
+    head, and (under the value split) the value columns the other half-head
+    computes."""
+    wl = WORKLOADS["kbench"].with_(dtype="bf16", odtype="f32", heads=2)
+    inp = make_inputs(wl)
+    bad_pos = 10 * 64 + 5  # scan position (row scan: spatial index) in chunk 10
+    inp["v"][0, 1, bad_pos, 3] = 1.0e6
+    o_ref, _ = oracle.gla(inp["q"], inp["k"], inp["v"], inp["g"], None, scale=wl.scale, H=wl.H, W=wl.W)
+    dev = torch.device("cuda")
+    q, k, v, g = (inp[n].to(dev) for n in ("q", "k", "v", "g"))
+    ws = gtr.Workspace(dev)
+    o, _ = call(gtr, q, k, v, g, H=wl.H, W=wl.W, scale=wl.scale, o_dtype=torch.float32, path=path, workspace=ws)
+    torch.cuda.synchronize()
+    assert gtr.gtr_gla_workspace_fault(ws.buf) & 2
+    x = o.double().cpu().numpy()
+    assert not np.isnan(x[0, 1, :640]).any()
+    assert rel_err(x[0, 1, :640], o_ref[0, 1, :640]) <= 2e-3
+    assert np.isnan(x[0, 1, 640:, 3]).all()  # every later token of the column that depends on the value
+    fin = ~np.isnan(x[0, 1, 640:])
+    err = np.max(np.abs(x[0, 1, 640:][fin] - o_ref[0, 1, 640:][fin]), initial=0.0)
+    assert err / np.max(np.abs(o_ref[0, 1])) <= 2e-3  # whatever is not NaN is correct
+    assert rel_err(x[0, 0], o_ref[0, 0]) <= 2e-3  # the other head is clean
+
+
+@pytest.mark.parametrize("path", PATHS)
+@pytest.mark.parametrize("dtype", ["f16", "bf16"])
+def test_large_magnitudes_stay_in_range(gtr, dtype, path):
+    """Correlated keys and values, gates of 1 and |v| in the hundreds: the
+    states grow past the fp16 range (|S| ~ L |k| |v|), the chunk summaries and
+    the scores come close to it. The power-of-two scaling of every fp16
+    intermediate keeps the result within the usual tolerance."""
+    H = W = 40
+    wl = Workload("large", B=1, heads=2, H=H, W=W, dk=64, dv=64, dtype=dtype, odtype="f32", gate_mu=2.0,
+                  gate_std=1.0, qk_std=0.125, v_std=1.0, seed=91)
+    rng = np.random.default_rng(91)
+    base_k = rng.normal(size=(1, 2, 1, 64))
+    base_v = rng.normal(size=(1, 2, 1, 64))
+    k = base_k + 0.1 * rng.normal(size=(1, 2, wl.L, 64))
+    v = 300.0 * (base_v + 0.1 * rng.normal(size=(1, 2, wl.L, 64)))
+    q = base_k + 0.3 * rng.normal(size=(1, 2, wl.L, 64))
+    td = torch_dtype(dtype)
+    inp = {"q": torch.from_numpy(q).float().to(td), "k": torch.from_numpy(k).float().to(td),
+           "v": torch.from_numpy(v).float().to(td), "g": torch.zeros((1, 2, wl.L, 64), dtype=td), "s0": None}
+    o_ref, _ = oracle.gla(inp["q"], inp["k"], inp["v"], inp["g"], None, scale=wl.scale, H=H, W=W)
+    assert np.max(np.abs(o_ref)) > 1e5  # the output, and with it the states, is far past 65504
+    o, _ = run_gpu(gtr, wl, "row", 64, path, inp)
+    assert np.isfinite(o.double().cpu().numpy()).all()
+    assert rel_err(o, o_ref) <= 2e-3, rel_err(o, o_ref)
+
+
+def test_default_workspaces_are_per_stream(gtr):
+    """Calls on two streams at once, each with the binding's default workspace,
+    give the same results as calls on one stream."""
+    wl = WORKLOADS["kbench"]
+    dev = torch.device("cuda")
+    inps = [make_inputs(wl, seed=s) for s in (31, 32)]
+    refs = []
+    ts = []
+    for inp in inps:
+        t = tuple(inp[n].to(dev) for n in ("q", "k", "v", "g"))
+        ts.append(t)
+        o, _ = gtr.gtr_gla_fwd(*t, H=wl.H, W=wl.W, path="auto")
+        refs.append(o.clone())
+    torch.cuda.synchronize()
+    streams = [torch.cuda.Stream(dev), torch.cuda.Stream(dev)]
+    outs = [[torch.empty_like(refs[i]) for _ in range(20)] for i in range(2)]
+    for n in range(20):
+        for i in range(2):
+            with torch.cuda.stream(streams[i]):
+                gtr.gtr_gla_fwd(*ts[i], H=wl.H, W=wl.W, path="auto", out=outs[i][n], stream=streams[i])
+    torch.cuda.synchronize()
+    for i in range(2):
+        for n in range(20):
+            assert torch.equal(outs[i][n], refs[i]), (i, n)
 
 
 # ---------------------------------------------------------------------------
