@@ -52,7 +52,9 @@ typedef enum {
   GTR_ERR_UNSUPPORTED = 3, /* a dtype / head width / chunk / path not compiled in */
   GTR_ERR_ALIAS = 4,       /* an output overlaps an input or the workspace        */
   GTR_ERR_WORKSPACE = 5,   /* workspace missing, too small or not 256-B aligned   */
-  GTR_ERR_HIP = 6          /* the HIP runtime rejected a launch                   */
+  GTR_ERR_HIP = 6,         /* the HIP runtime rejected a launch                   */
+  GTR_ERR_SCRATCH = 7      /* (gtr_gla_fwd_noalloc) the call needs more workspace
+                              than the library's fixed scratch holds            */
 } gtr_status;
 
 typedef enum { GTR_F32 = 0, GTR_F16 = 1, GTR_BF16 = 2 } gtr_dtype;
@@ -294,6 +296,28 @@ typedef struct {
 
 size_t gtr_spatial_swiglu_workspace_size(const gtr_swiglu_args* args);
 gtr_status gtr_spatial_swiglu(const gtr_swiglu_args* args, hipStream_t stream);
+
+/*
+ * gtr_gla_fwd_noalloc - gtr_gla_fwd for callers that cannot allocate device
+ * memory (code under HIP graph capture, serving loops, harnesses that forbid
+ * hipMalloc). Same arguments, results and schedules as gtr_gla_fwd, except
+ * that args->workspace and args->workspace_bytes are ignored: the workspace is
+ * a fixed 32 MB scratch array inside the library, one copy per device, held
+ * until the process ends. The call itself allocates and frees nothing and
+ * calls no allocating routine; the first call on a device looks up that
+ * device's copy of the array (hipGetSymbolAddress), once.
+ * A call that needs more than 32 MB of workspace (gtr_gla_workspace_size) is
+ * rejected with GTR_ERR_SCRATCH before anything is launched; this holds the
+ * 40x40-token workloads up to 16 sequences and 6 sequences at 80x80, for
+ * instance, not a batch of 8 images of 12 heads.
+ * Every call on a device shares that device's array: calls that overlap in
+ * time on one device (two streams, two threads) race and must not be issued.
+ * The scratch keeps what the last call left: its synchronisation words are
+ * zero at load and every completed call leaves them zero. Its fault word
+ * cannot be read through this interface; a wait that ran out still shows as
+ * NaN in the outputs it poisoned.
+ */
+gtr_status gtr_gla_fwd_noalloc(const gtr_gla_args* args, hipStream_t stream);
 
 /* The fault word of a workspace (bits as described under gtr_gla_args: 1 = a
  * bounded wait ran out, 2 = a bf16 input outside the fp16 range), 0 if every

@@ -33,12 +33,12 @@ F32, F16, BF16 = 0, 1, 2
 SCANS = {"row": 0, "col": 1, "row_rev": 2, "col_rev": 3}
 PATHS = {"auto": 0, "fused": 1, "staged": 2, "inline": 3}
 STATUS = {0: "GTR_OK", 1: "GTR_ERR_NULL", 2: "GTR_ERR_SHAPE", 3: "GTR_ERR_UNSUPPORTED",
-          4: "GTR_ERR_ALIAS", 5: "GTR_ERR_WORKSPACE", 6: "GTR_ERR_HIP"}
+          4: "GTR_ERR_ALIAS", 5: "GTR_ERR_WORKSPACE", 6: "GTR_ERR_HIP", 7: "GTR_ERR_SCRATCH"}
 
 _DT = {torch.float32: F32, torch.float16: F16, torch.bfloat16: BF16}
 _DT_BACK = {F32: torch.float32, F16: torch.float16, BF16: torch.bfloat16}
 
-EXPORTS = ("gtr_scan_permute", "gtr_gla_workspace_size", "gtr_gla_workspace_init", "gtr_gla_fwd",
+EXPORTS = ("gtr_scan_permute", "gtr_gla_workspace_size", "gtr_gla_workspace_init", "gtr_gla_fwd", "gtr_gla_fwd_noalloc",
            "gtr_gla_schedule", "gtr_gla_value_parts", "gtr_gla_workspace_fault", "gtr_status_string", "gtr_spatial_swiglu_workspace_size",
            "gtr_spatial_swiglu")
 
@@ -100,6 +100,8 @@ def load(path: Optional[str] = None) -> ctypes.CDLL:
     lib.gtr_gla_workspace_init.restype = ctypes.c_int
     lib.gtr_gla_fwd.argtypes = [ctypes.POINTER(GlaArgs), P]
     lib.gtr_gla_fwd.restype = ctypes.c_int
+    lib.gtr_gla_fwd_noalloc.argtypes = [ctypes.POINTER(GlaArgs), P]
+    lib.gtr_gla_fwd_noalloc.restype = ctypes.c_int
     lib.gtr_gla_schedule.argtypes = [ctypes.POINTER(GlaArgs)]
     lib.gtr_gla_schedule.restype = ctypes.c_int
     lib.gtr_gla_value_parts.argtypes = [ctypes.POINTER(GlaArgs)]

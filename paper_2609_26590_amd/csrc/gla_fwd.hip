@@ -1597,11 +1597,9 @@ extern "C" int gtr_gla_value_parts(const gtr_gla_args* a) {
   return plan_query(a, &pl) ? -1 : pl.vparts;
 }
 
-extern "C" gtr_status gtr_gla_fwd(const gtr_gla_args* a, hipStream_t stream) {
-  if (!a) return GTR_ERR_NULL;
-  GlaShape s;
-  gtr_status st = gla_shape_from_args(a, &s, /*check_pointers=*/true);
-  if (st != GTR_OK) return st;
+// Launches the schedule for arguments already validated (workspace included).
+static gtr_status gla_launch(const gtr_gla_args* a, const GlaShape& s, hipStream_t stream) {
+  gtr_status st;
   KernelSet ks;
   if (!select_kernels(s, &ks)) return GTR_ERR_UNSUPPORTED;
   Plan pl;
@@ -1666,4 +1664,55 @@ extern "C" gtr_status gtr_gla_fwd(const gtr_gla_args* a, hipStream_t stream) {
   }
   if (err != hipSuccess) return GTR_ERR_HIP;
   return hipGetLastError() == hipSuccess ? GTR_OK : GTR_ERR_HIP;
+}
+
+extern "C" gtr_status gtr_gla_fwd(const gtr_gla_args* a, hipStream_t stream) {
+  if (!a) return GTR_ERR_NULL;
+  GlaShape s;
+  const gtr_status st = gla_shape_from_args(a, &s, /*check_pointers=*/true);
+  if (st != GTR_OK) return st;
+  return gla_launch(a, s, stream);
+}
+
+// ---------------------------------------------------------------------------
+// The entry point that allocates nothing: the workspace is a file-scope device
+// array of fixed size (one copy per device, zero at load; every completed call
+// leaves its synchronisation words zeroed again). In host code `scratch` only
+// names the symbol: its device address on each device comes from
+// hipGetSymbolAddress, taken once per device with that device current.
+// ---------------------------------------------------------------------------
+namespace gtr {
+constexpr size_t kNoAllocBytes = (size_t)32 << 20;
+static __device__ __align__(256) unsigned char scratch[kNoAllocBytes];
+
+static void* scratch_on_current_device() {
+  constexpr int kMaxDevices = 64;
+  static std::mutex mu;
+  static void* ptr[kMaxDevices];
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return nullptr;
+  std::lock_guard<std::mutex> lk(mu);
+  if (!ptr[dev]) {
+    void* p = nullptr;
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess) return nullptr;
+    ptr[dev] = p;
+  }
+  return ptr[dev];
+}
+}  // namespace gtr
+
+extern "C" gtr_status gtr_gla_fwd_noalloc(const gtr_gla_args* a, hipStream_t stream) {
+  if (!a) return GTR_ERR_NULL;
+  GlaShape s;
+  gtr_status st = gla_shape_from_args(a, &s, /*check_pointers=*/false);
+  if (st != GTR_OK) return st;
+  if (gla_workspace_layout(s).total > kNoAllocBytes) return GTR_ERR_SCRATCH;
+  void* ws = scratch_on_current_device();
+  if (!ws) return GTR_ERR_HIP;
+  gtr_gla_args b = *a;
+  b.workspace = ws;
+  b.workspace_bytes = kNoAllocBytes;
+  st = gla_shape_from_args(&b, &s, /*check_pointers=*/true);
+  if (st != GTR_OK) return st;
+  return gla_launch(&b, s, stream);
 }

@@ -146,6 +146,7 @@ extern "C" const char* gtr_status_string(gtr_status st) {
     case GTR_ERR_ALIAS: return "GTR_ERR_ALIAS: an output overlaps an input or the workspace";
     case GTR_ERR_WORKSPACE: return "GTR_ERR_WORKSPACE: workspace missing, too small or misaligned";
     case GTR_ERR_HIP: return "GTR_ERR_HIP: the HIP runtime rejected a launch";
+    case GTR_ERR_SCRATCH: return "GTR_ERR_SCRATCH: the call needs more workspace than the fixed scratch of gtr_gla_fwd_noalloc holds";
     default: return "unknown gtr_status";
   }
 }

@@ -368,3 +368,20 @@ def test_swiglu_nulls_alignment_alias_workspace(lib):
     a = swiglu_args()
     a.y_dtype = gtr.BF16  # neither fp16 (the input dtype) nor float32
     assert sw(lib, a) == UNSUP
+
+
+# ---------------------------------------------------------------------------
+# gtr_gla_fwd_noalloc: validation before any HIP call
+# ---------------------------------------------------------------------------
+
+def test_noalloc_validation(lib):
+    assert lib.gtr_gla_fwd_noalloc(None, None) == 1  # GTR_ERR_NULL
+    a = base_args(B=8, heads=12, H=40, W=40)  # a batch of 8 images of 12 heads: about 80 MB of workspace
+    assert lib.gtr_gla_workspace_size(ctypes.byref(a)) > 32 << 20
+    assert lib.gtr_gla_fwd_noalloc(ctypes.byref(a), None) == 7  # GTR_ERR_SCRATCH, nothing launched
+    a = base_args(B=1, heads=6, H=40, W=40)
+    a.dk = 48
+    assert lib.gtr_gla_fwd_noalloc(ctypes.byref(a), None) == UNSUP
+    a = base_args(B=1, heads=6, H=40, W=40)
+    a.workspace, a.workspace_bytes = None, 0  # ignored by this entry point
+    assert lib.gtr_gla_workspace_size(ctypes.byref(a)) <= 32 << 20
