@@ -51,7 +51,8 @@ from paper_2609_26590_amd.workloads import (WORKLOADS, algorithmic_bytes, algori
 
 HBM_PEAK_GBS = 8000.0        # MI355X HBM3E, published
 MFMA_F16_PEAK_TFLOPS = 2500.0  # MI355X dense fp16 matrix, published
-KERNEL_SOURCES = ("paper_2609_26590_amd/csrc/gla_fwd.hip", "paper_2609_26590_amd/csrc/gtr_device.h")
+KERNEL_SOURCES = ("paper_2609_26590_amd/csrc/gla_fwd.hip", "paper_2609_26590_amd/csrc/gla_lean.hip",
+                  "paper_2609_26590_amd/csrc/gla_common.h", "paper_2609_26590_amd/csrc/gtr_device.h")
 TRAFFIC_PROFILE = "profiles/gla_kbench_auto_traffic.txt"  # counters of the default (AUTO) run
 
 
@@ -88,8 +89,10 @@ def schedule_of(wl, path):
                                 s0=s0, want_final=wl.want_final, o_dtype=torch_dtype(wl.odtype), path=path)
 
 
-KERNEL_OF = {"inline": "gla_chain_kernel (one launch, inline prefixes: the whole call is this kernel)",
-             "fused": "gla_chain_kernel (one launch, look-back to inclusive states: the whole call is this kernel)",
+KERNEL_OF = {"inline": "gla_lean_kernel for 16-bit inputs at chunk 64, else gla_chain_kernel (one launch, "
+                       "look-back over summaries: the whole call is this kernel)",
+             "fused": "gla_lean_kernel for 16-bit inputs at chunk 64, else gla_chain_kernel (one launch, "
+                      "look-back to inclusive states: the whole call is this kernel)",
              "staged": "one gtr_gla_fwd call (summary + scan + output kernels)"}
 
 

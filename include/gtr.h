@@ -102,10 +102,11 @@ typedef enum {
 /* Execution schedule of gtr_gla_fwd (all give the same result up to rounding;
  * the length-aware dispatch of the paper's operator appendix). */
 typedef enum {
-  GTR_PATH_AUTO = 0,   /* the library picks: INLINE for sequences of at most 32
-                          chunks, FUSED for up to 256 chunks, STAGED beyond (or
-                          for more than 1024 sequences). gtr_gla_schedule reports
-                          the choice.                                               */
+  GTR_PATH_AUTO = 0,   /* the library picks (gtr_gla_schedule reports the choice):
+                          INLINE for sequences of at most 32 chunks whose chunks
+                          are all resident at once, FUSED for sequences of at
+                          most 64 chunks, STAGED beyond (or for more than 1024
+                          sequences).                                               */
   GTR_PATH_FUSED = 1,  /* one launch, boundary states by look-back: each chunk
                           hands over its summary, finds S_[c] from the summaries
                           of the chunks before it back to the nearest chunk that

@@ -57,197 +57,12 @@
 #include <mutex>
 #include <type_traits>
 
+#include "gla_common.h"
 #include "gtr.h"
 #include "gtr_device.h"
 #include "gtr_internal.h"
 
 namespace gtr {
-
-constexpr float kSpanF16 = 10.f;           // mid-point factors within e^5: fp16 operands
-constexpr float kSpanF32 = 60.f;           // within e^30: float32 operands
-constexpr unsigned kSpinDefault = 1u << 22;  // polls of a bounded wait before it gives up
-constexpr unsigned kFlagSummary = 1u;       // chunk flag: the summary U_c and its record are stored
-constexpr int kFlagInclusive = 8;          // + wave: that wave's pieces of S_[c+1] are stored
-constexpr int kFlagBlock = 16;             // + wave: that wave's pieces of the block prefix are stored
-constexpr float kF16Safe = 65504.f;        // bf16 inputs must stay within the fp16 range
-
-// fault word bits (the workspace's first word; sticky until the workspace is
-// initialised again)
-constexpr unsigned kFaultWait = 1u;   // a bounded wait ran out
-constexpr unsigned kFaultRange = 2u;  // a bf16 input lies outside the fp16 range
-
-struct GlaParams {
-  const void* q;
-  const void* k;
-  const void* v;
-  const void* g;
-  void* o;
-  const float* s0;
-  float* s_final;
-  int qdt, gdt, odt;
-  int BH;
-  int H, W;
-  int64_t L;
-  int nchunks;
-  float scale;
-  int scan;
-  void* agg;        // [NS][NC][DK][DVp] chunk summaries U_c: fp16 scaled (16-bit inputs) or float32
-  float* rec;       // [NS][NC][RS] per chunk: d_c (DK floats), then the summary's scale
-  float* states;    // [NS][NC][DK][DVp] float32: S_[c+1] (one launch) or S_[c] (staged)
-  unsigned* sync;   // [kSyncSeqs][4]: work-groups done per sequence
-  unsigned* flags;  // [kSyncSeqs][kMaxChainChunks]: bit 0 summary, bit 8 + w inclusive state and bit
-                    // 16 + w block prefix (the pieces of wave w)
-  void* blk;        // [NS][NC][DK][DVp] block prefixes (at the block index), fp16 scaled or float32
-  float* blkrec;    // [NS][NC][DK + 8]: block decay per row, then one scale per wave
-  unsigned* fault;  // one word
-  int gkind;        // GTR_GATE_LOG_DECAY or GTR_GATE_LOGITS (g holds the gate logits)
-  float inv_tau;    // 1 / tau of the gate fusion
-  const void* gate;  // output-gate pre-activation [BH][L][DV] (spatial), or null: no epilogue
-  const float* nw;   // RMSNorm weight [DV], or null (ones)
-  int gatedt;        // dtype of gate
-  float eps;         // RMSNorm epsilon
-  int dvp;      // row pitch (elements) of v, o, the gate, S0 and S_final: the full d_v
-  int vparts;   // value split: work-groups per chunk, each d_v / vparts columns
-  int ns;       // sequences: BH * vparts
-  int desc;     // one launch: chunks in descending order (every work-group resident at once)
-  int publish;  // one launch: store inclusive states
-  int blk_size;  // one launch: chunks per block of the two-level look-back
-  unsigned spin;  // polls of a bounded wait
-};
-
-constexpr int tile_threads(int chunk) { return chunk / 16 * kWave; }
-
-typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
-typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));
-
-// ---------------------------------------------------------------------------
-// Agent-coherent buffer accesses (cache policy sc1: no stale copy in the CU's
-// L1 is used, stores are written through). The buffer descriptor bounds every
-// access to [base, base + bytes): outside it loads return 0 and stores are
-// dropped.
-// ---------------------------------------------------------------------------
-constexpr int kAgentCoherent = 16;
-
-__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, uint32_t bytes) {
-  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes, 0x00020000);
-}
-__device__ __forceinline__ void coh_store4(__amdgpu_buffer_rsrc_t r, uint32_t byte_off, f4 v) {
-  __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, v), r, (int)byte_off, 0, kAgentCoherent);
-}
-__device__ __forceinline__ u32x4 coh_load16(__amdgpu_buffer_rsrc_t r, uint32_t byte_off) {
-  return __builtin_amdgcn_raw_buffer_load_b128(r, (int)byte_off, 0, kAgentCoherent);
-}
-__device__ __forceinline__ f4 coh_load4(__amdgpu_buffer_rsrc_t r, uint32_t byte_off) {
-  return __builtin_bit_cast(f4, coh_load16(r, byte_off));
-}
-__device__ __forceinline__ void coh_store1(__amdgpu_buffer_rsrc_t r, uint32_t byte_off, float v) {
-  __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(unsigned, v), r, (int)byte_off, 0, kAgentCoherent);
-}
-__device__ __forceinline__ float coh_load1(__amdgpu_buffer_rsrc_t r, uint32_t byte_off) {
-  return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(r, (int)byte_off, 0, kAgentCoherent));
-}
-
-// Powers of two from an exponent in [-126, 127] (bit patterns, exact).
-__device__ __forceinline__ float exp2i(int e) { return __builtin_bit_cast(float, (unsigned)(127 + e) << 23); }
-// Exponent e such that m * 2^-e lies in [2^14, 2^15) for a finite m > 0 (0 for
-// m = 0), clamped to [-100, 100]: scaling by 2^-e keeps the largest magnitude
-// of a tile well inside the fp16 range and every other value at full fp16
-// precision unless it is below 2^-24 of the largest.
-__device__ __forceinline__ int fp16_exponent(float m) {
-  const int b = (int)((__builtin_bit_cast(unsigned, m) >> 23) & 0xffu);
-  const int e = m > 0.f ? b - 127 - 14 : 0;
-  return e < -100 ? -100 : (e > 100 ? 100 : e);
-}
-
-// Raw bits of 8 consecutive elements (32 bytes for float32, 16 for 16-bit types).
-struct Raw {
-  u32x4 a, b;
-};
-
-__device__ __forceinline__ void ld_raw(const void* base, int dt, int64_t off, Raw& r) {
-  if (dt == GTR_F32) {
-    const u32x4* p = reinterpret_cast<const u32x4*>(static_cast<const float*>(base) + off);
-    r.a = p[0];
-    r.b = p[1];
-  } else {
-    r.a = *reinterpret_cast<const u32x4*>(static_cast<const unsigned short*>(base) + off);
-  }
-}
-
-// The same through a buffer descriptor over one sequence's rows: a byte offset
-// at or beyond the descriptor's range (kOutOfRange) reads zeros, which is what
-// the positions past the end of a sequence must hold.
-constexpr uint32_t kOutOfRange = 0x7fffff00u;  // the host keeps every sequence's rows below this many bytes
-__device__ __forceinline__ void ld_raw_buf(__amdgpu_buffer_rsrc_t rs, int dt, uint32_t byte_off, Raw& r) {
-  r.a = __builtin_amdgcn_raw_buffer_load_b128(rs, (int)byte_off, 0, 0);
-  if (dt == GTR_F32) r.b = __builtin_amdgcn_raw_buffer_load_b128(rs, (int)(byte_off + 16u), 0, 0);
-}
-
-__device__ __forceinline__ void cvt_raw(const Raw& r, int dt, float (&x)[8]) {
-  if (dt == GTR_F32) {
-#pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      // copy the lanes to scalars first: this compiler reads element 0 when
-      // __builtin_bit_cast is given a vector-element lvalue directly
-      const unsigned int ua = r.a[e], ub = r.b[e];
-      x[e] = __builtin_bit_cast(float, ua);
-      x[e + 4] = __builtin_bit_cast(float, ub);
-    }
-  } else if (dt == GTR_F16) {
-    const h8 h = __builtin_bit_cast(h8, r.a);
-#pragma unroll
-    for (int e = 0; e < 8; ++e) x[e] = (float)h[e];
-  } else {
-#pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      const unsigned int u = r.a[e];
-      x[2 * e] = __builtin_bit_cast(float, u << 16);
-      x[2 * e + 1] = __builtin_bit_cast(float, u & 0xffff0000u);
-    }
-  }
-}
-
-template <bool F16>
-__device__ __forceinline__ float gexp(float x) {
-  if constexpr (F16)
-    return __expf(x);
-  else
-    return expf(x);
-}
-
-// Log-decay of one key dimension from what g holds: log gamma itself, or (gate
-// fusion) the logit a of gamma = sigmoid(a)^(1/tau) (Sec. 3.1), giving
-// log gamma = logsigmoid(a) / tau = (min(a, 0) - log1p(exp(-|a|))) / tau.
-// log1p(e) for e in (0, 1] as log(u) * e / (u - 1), u = 1 + e rounded: the
-// factor e / (u - 1) undoes the rounding of u (u - 1 is exact), which keeps the
-// result within a few ulp with one log and one reciprocal.
-// Hardware log2 and reciprocal (about 1 ulp each); when u rounds to 1 the
-// quotient is not used (a select, not a branch).
-__device__ __forceinline__ float log_decay(const GlaParams& P, float x) {
-  if (P.gkind != GTR_GATE_LOGITS) return x;
-  constexpr float kLn2 = 0.693147180559945309f;
-  const float e = __expf(-fabsf(x));
-  const float u = 1.f + e;
-  const float d = u - 1.f;
-  const float r = __builtin_amdgcn_logf(u) * kLn2 * e * __builtin_amdgcn_rcpf(d);
-  const float l1p = d == 0.f ? e : r;
-  return (fminf(x, 0.f) - l1p) * P.inv_tau;
-}
-
-// Maximum over the groups of N consecutive lanes (N = 4 or 8) with DPP
-// (quad permutations, then the half-row mirror); every lane gets its group's
-// maximum.
-template <int CTRL>
-__device__ __forceinline__ float dpp_mov(float v) {
-  return __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, v), CTRL, 0xf, 0xf, false));
-}
-template <int N>
-__device__ __forceinline__ float group_max(float x) {
-  x = fmaxf(x, dpp_mov<0xB1>(x));  // quad_perm [1,0,3,2]
-  x = fmaxf(x, dpp_mov<0x4E>(x));  // quad_perm [2,3,0,1]
-  if constexpr (N == 8) x = fmaxf(x, dpp_mov<0x141>(x));  // row_half_mirror: lane i <-> 7 - i
-  return x;
-}
 
 // One chunk of one sequence: C tokens, one wave per 16-token sub-chunk.
 // IN is the dtype of q, k, v (GTR_F32 / GTR_F16 / GTR_BF16); DV the value
@@ -266,12 +81,13 @@ struct Chunk {
   static constexpr int TP = F16 ? C + 8 : C + 4;    // transposed-tile pitch (elements)
   static constexpr int SP = F16 ? DK + 8 : DK + 4;  // boundary-state tile pitch
   static constexpr int NF = 3 + (NW > 1 ? NW - 1 : 1);  // factor-table rows per wave
-  static constexpr int RS = DK + 4;                 // record stride (floats): d_c, scale, pad
+  static constexpr int RS = 2 * DK;                 // record stride (floats): (d_c[i], scale) pairs
   // summaries and boundary states are [DK][DV] (key dim i, value column n), in
   // 8-element pieces: piece p holds row i = p / (DV/8), columns 8 (p % (DV/8)) ..
   static constexpr int SQ8 = DK * DV / 8;
   static constexpr int SPER = (SQ8 + NT - 1) / NT;  // pieces per thread
-  static_assert(NT % (DV / 8) == 0, "the pieces of one thread share their columns");
+  static constexpr int TPR = DV / (8 * SPER);       // threads per state row
+  static_assert(DV % (8 * SPER) == 0, "the pieces of one thread lie in one row");
   typedef typename Op<F16>::elem E;
   typedef typename Op<F16>::frag8 F8;
   typedef typename Op<F16>::frag4 F4;
@@ -469,9 +285,9 @@ struct Chunk {
   // sub-chunk's factor table (one exponential per factor and dimension); the
   // wave then reads back what its lanes need. READOUT: qt = q exp(A_r).
   // SUMMARY: the transposed k-hat tile, and the chunk record (d_c and the
-  // summary scale, written by wave 0 through `rec`, coherent or plain) and d_c
+  // summary scale, written by wave 0 through `rec` unless it is null) and d_c
   // in shared memory, followed by a barrier.
-  template <bool READOUT, bool SUMMARY, bool COH, class S>
+  template <bool READOUT, bool SUMMARY, class S>
   __device__ __forceinline__ void factors(S& sm, float* rec) {
     if (lane < DK) {
       const int d = lane;
@@ -497,14 +313,7 @@ struct Chunk {
       }
       if (SUMMARY && w == 0) {
         const float dc = gexp<F16>(before + sm.T[0][d] + after);
-        if constexpr (COH) {
-          const __amdgpu_buffer_rsrc_t rr = make_rsrc(rec, RS * 4);
-          coh_store1(rr, d * 4, dc);
-          if (d == 0) coh_store1(rr, DK * 4, usc);
-        } else {
-          rec[d] = dc;
-          if (d == 0) rec[DK] = usc;
-        }
+        if (rec) *reinterpret_cast<f2*>(rec + 2 * d) = f2{dc, usc};
         if constexpr (std::is_same<S, Smem>::value || std::is_same<S, SmemSummary>::value) sm.dc[d] = dc;
       }
     }
@@ -721,13 +530,14 @@ struct Chunk {
     }
   }
 
-  // ---- boundary states in pieces of 8 elements: this thread's pieces are
-  // threadIdx.x + m NT, each row i_m = piece / (DV/8), columns n0 .. n0 + 7 ----
-  __device__ __forceinline__ static int piece_n0() { return 8 * ((int)threadIdx.x % (DV / 8)); }
-  __device__ __forceinline__ static int piece_i(int m) { return ((int)threadIdx.x + m * NT) / (DV / 8); }
-  __device__ __forceinline__ static bool piece_ok(int m) { return (int)threadIdx.x + m * NT < SQ8; }
+  // ---- boundary states in pieces of 8 elements: the SPER pieces of a thread
+  // are consecutive columns n0(m) .. n0(m) + 7 of one row i of the [DK][DV]
+  // state (TPR threads per row), so one decay per tile serves them all ----
+  __device__ __forceinline__ static int piece_n0(int m) { return 8 * (SPER * ((int)threadIdx.x % TPR) + m); }
+  __device__ __forceinline__ static int piece_i(int m) { return (int)threadIdx.x / TPR; }
+  __device__ __forceinline__ static bool piece_ok(int m) { return (int)threadIdx.x < DK * TPR; }
   __device__ __forceinline__ static uint32_t piece_elem(int m) {
-    return (uint32_t)(piece_i(m) * DV + piece_n0());
+    return (uint32_t)(piece_i(m) * DV + piece_n0(m));
   }
 
   // S_[c] pieces -> the shared state tile S^T ([DV][SP]). For 16-bit inputs the
@@ -735,7 +545,6 @@ struct Chunk {
   // largest |S_[c]| over the work-group. No barrier.
   template <class S>
   __device__ __forceinline__ void state_tile(S& sm, const float (&acc)[SPER][8], float wg_max) {
-    const int n0 = piece_n0();
     float down = 1.f;
     tsc = 1.f;
     if constexpr (F16) {
@@ -746,7 +555,7 @@ struct Chunk {
 #pragma unroll
     for (int m = 0; m < SPER; ++m)
       if (piece_ok(m)) {
-        const int i = piece_i(m);
+        const int i = piece_i(m), n0 = piece_n0(m);
 #pragma unroll
         for (int e = 0; e < 8; ++e) sm.sT[(n0 + e) * SP + i] = (E)(acc[m][e] * down);
       }
@@ -868,235 +677,6 @@ struct Chunk {
   }
 };
 
-// 8 elements of a summary piece (fp16 bits or float32) times w, added to acc.
-template <bool F16>
-struct Piece;
-template <>
-struct Piece<true> {
-  u32x4 a;
-  __device__ __forceinline__ void load(__amdgpu_buffer_rsrc_t r, uint32_t elem) { a = coh_load16(r, elem * 2); }
-  __device__ __forceinline__ void plain(const void* base, uint32_t elem) {
-    a = *reinterpret_cast<const u32x4*>(static_cast<const _Float16*>(base) + elem);
-  }
-  __device__ __forceinline__ void fma_into(float (&acc)[8], float wt) const {
-    const h8 h = __builtin_bit_cast(h8, a);
-#pragma unroll
-    for (int e = 0; e < 8; ++e) acc[e] = fmaf(wt, (float)h[e], acc[e]);
-  }
-};
-template <>
-struct Piece<false> {
-  u32x4 a, b;
-  __device__ __forceinline__ void load(__amdgpu_buffer_rsrc_t r, uint32_t elem) {
-    a = coh_load16(r, elem * 4);
-    b = coh_load16(r, elem * 4 + 16);
-  }
-  __device__ __forceinline__ void plain(const void* base, uint32_t elem) {
-    const u32x4* p = reinterpret_cast<const u32x4*>(static_cast<const float*>(base) + elem);
-    a = p[0];
-    b = p[1];
-  }
-  __device__ __forceinline__ void fma_into(float (&acc)[8], float wt) const {
-#pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      const unsigned ua = a[e], ub = b[e];
-      acc[e] = fmaf(wt, __builtin_bit_cast(float, ua), acc[e]);
-      acc[e + 4] = fmaf(wt, __builtin_bit_cast(float, ub), acc[e + 4]);
-    }
-  }
-};
-// 8 float32 elements of a state piece.
-struct Piece32 {
-  f4 a, b;
-  __device__ __forceinline__ void load(__amdgpu_buffer_rsrc_t r, uint32_t elem) {
-    a = coh_load4(r, elem * 4);
-    b = coh_load4(r, elem * 4 + 16);
-  }
-  __device__ __forceinline__ void fma_into(float (&acc)[8], float wt) const {
-#pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      acc[e] = fmaf(wt, a[e], acc[e]);
-      acc[e + 4] = fmaf(wt, b[e], acc[e + 4]);
-    }
-  }
-};
-
-// ---------------------------------------------------------------------------
-// Look-back (one launch), two levels. The chunks of a sequence form blocks of
-// G = P.blk_size; the last chunk of block k also hands over the block prefix
-//   B_k = sum_{j in block k} (prod_{j<l<=end of k} Diag(d_l)) U_j
-// and the block decay D_k = prod_{j in block k} d_j. Chunk c in block K builds
-//   S_[c] = sum_{j=KG}^{c-1} w_j U_j + sum_{k<K} w'_k B_k + w'' S_0,
-// every weight a product of the decays in between, nearest first: the
-// summaries of its own block before it, then the block prefixes of the blocks
-// before its own. Wherever a chunk on that path has already handed over its
-// inclusive state S_[j+1] (FUSED schedule), the look-back takes it and stops.
-// Every wave does this for its own pieces (rows i of the [DK][DV] state) on its
-// own: lane p of the wave polls the flag of the p-th chunk on the path (the
-// summary bit for its own block, the block bit of the wave for earlier blocks,
-// the inclusive bit of the wave anywhere) until every tile before the nearest
-// inclusive state is ready, then loads the tiles and the decays of its rows
-// in batches. A block-end chunk calls `at_block_end(acc, run, ok)` once its
-// own block's summaries are summed (before the block prefixes), unless an
-// inclusive state inside its block ended the look-back. No barrier. Returns
-// false if the wait ran out (acc is then not valid); `run` ends as the decay
-// product of each piece's row over every chunk before c.
-// ---------------------------------------------------------------------------
-template <class T, class F>
-__device__ __forceinline__ bool lookback(const GlaParams& P, const T& ch, int seq, int c, float (&acc)[T::SPER][8],
-                                         float (&run)[T::SPER], F at_block_end) {
-  constexpr int DK = T::kDK, DV = T::kDV, SPER = T::SPER, RS = T::RS, RB = DK + 8;
-  constexpr bool F16 = T::F16;
-  constexpr int B = 4;  // tiles per batch of piece loads
-  const int NC = P.nchunks, G = P.blk_size;
-  const unsigned* fl = P.flags + (size_t)seq * kMaxChainChunks;
-  const uint32_t tile = DK * DV * (F16 ? 2 : 4);
-  const __amdgpu_buffer_rsrc_t ar =
-      make_rsrc(static_cast<char*>(P.agg) + (size_t)seq * NC * tile, (uint32_t)NC * tile);
-  const __amdgpu_buffer_rsrc_t br =
-      make_rsrc(static_cast<char*>(P.blk) + (size_t)seq * NC * tile, (uint32_t)NC * tile);
-  const __amdgpu_buffer_rsrc_t rr = make_rsrc(P.rec + (size_t)seq * NC * RS, (uint32_t)NC * RS * 4);
-  const __amdgpu_buffer_rsrc_t bre = make_rsrc(P.blkrec + (size_t)seq * NC * RB, (uint32_t)NC * RB * 4);
-  const __amdgpu_buffer_rsrc_t sr = make_rsrc(P.states + (size_t)seq * NC * (DK * DV), (uint32_t)NC * DK * DV * 4);
-#pragma unroll
-  for (int m = 0; m < SPER; ++m) {
-    run[m] = 1.f;
-#pragma unroll
-    for (int e = 0; e < 8; ++e) acc[m][e] = 0.f;
-  }
-  const int lo = c / G * G;   // first chunk of c's block
-  const int nA = c - lo;      // summaries of c's block before c (path tiles 0 .. nA - 1)
-  const int nB = lo / G;      // blocks before c's (path tiles nA .. nA + nB - 1, nearest first);
-                              // nA < G <= 16 and nB < kMaxChainChunks / G, both below 64 (host)
-  const unsigned incb = 1u << (kFlagInclusive + ch.w), blkb = 1u << (kFlagBlock + ch.w);
-  const bool block_end = c % G == G - 1 && c < NC - 1;
-  // chunk whose flag path tile p waits on: a summary, or the last chunk of a block
-  auto chunk_of = [&](int p) { return p < nA ? c - 1 - p : (nB - 1 - (p - nA)) * G + G - 1; };
-
-  // Poll the flags of path tiles [p0, p0 + n) (lane l: tile p0 + l, n < 64)
-  // until every tile before the nearest one with this wave's inclusive bit has
-  // its `ready` bit; returns how many tiles to sum (n if no inclusive state),
-  // or -1 if the wait ran out.
-  auto poll = [&](int p0, int n, unsigned ready) -> int {
-    if (n == 0) return 0;
-    unsigned cnt = 0;
-    for (;;) {
-      const unsigned f = ch.lane < n ? __hip_atomic_load(&fl[chunk_of(p0 + ch.lane)], __ATOMIC_RELAXED,
-                                                         __HIP_MEMORY_SCOPE_AGENT)
-                                     : 0u;
-      const uint64_t inc = __builtin_amdgcn_ballot_w64((f & incb) != 0);
-      const uint64_t rdy = __builtin_amdgcn_ballot_w64((f & ready) != 0);
-      const int mm = inc ? (int)__builtin_ctzll(inc) : n;
-      const uint64_t need = (1ull << mm) - 1ull;  // mm < 64
-      if ((rdy & need) == need) return mm;
-      if (++cnt >= P.spin) return -1;
-      __builtin_amdgcn_s_sleep(1);
-    }
-  };
-  // path tiles [p0, p1) in batches of B (every load of a batch issued before
-  // any is used): summaries (p < nA) or block prefixes
-  struct Batch {
-    Piece<F16> u[B][SPER];
-    float d[B][SPER], sc[B][SPER];
-  };
-  auto load_batch = [&](int b0, int p1, Batch& t) {
-#pragma unroll
-    for (int b = 0; b < B; ++b)
-      if (b0 + b < p1) {
-        const int p = b0 + b;
-        if (p < nA) {
-          const uint32_t j = (uint32_t)(c - 1 - p);
-          const float scj = coh_load1(rr, (j * RS + DK) * 4);
-#pragma unroll
-          for (int mm = 0; mm < SPER; ++mm)
-            if (T::piece_ok(mm)) {
-              t.u[b][mm].load(ar, j * (DK * DV) + T::piece_elem(mm));
-              t.d[b][mm] = coh_load1(rr, (j * RS + T::piece_i(mm)) * 4);
-              t.sc[b][mm] = scj;
-            }
-        } else {
-          const uint32_t k = (uint32_t)(nB - 1 - (p - nA));
-          const float sck = coh_load1(bre, (k * RB + DK + ch.w) * 4);
-#pragma unroll
-          for (int mm = 0; mm < SPER; ++mm)
-            if (T::piece_ok(mm)) {
-              t.u[b][mm].load(br, k * (DK * DV) + T::piece_elem(mm));
-              t.d[b][mm] = coh_load1(bre, (k * RB + T::piece_i(mm)) * 4);
-              t.sc[b][mm] = sck;
-            }
-        }
-      }
-  };
-  auto use_batch = [&](int b0, int p1, const Batch& t) {
-#pragma unroll
-    for (int b = 0; b < B; ++b)
-      if (b0 + b < p1)
-#pragma unroll
-        for (int mm = 0; mm < SPER; ++mm)
-          if (T::piece_ok(mm)) {
-            t.u[b][mm].fma_into(acc[mm], run[mm] * t.sc[b][mm]);
-            run[mm] *= t.d[b][mm];
-          }
-  };
-  auto sum_tiles = [&](int p0, int p1) {
-    for (int b0 = p0; b0 < p1; b0 += B) {
-      Batch x;
-      load_batch(b0, p1, x);
-      use_batch(b0, p1, x);
-    }
-  };
-
-  // first the summaries of c's own block; then a block-end chunk hands over its
-  // block prefix (which depends on nothing before its block, so the prefixes
-  // never wait on one another); then the block prefixes before c's block
-  int m = poll(0, nA, kFlagSummary);
-  bool ok = m >= 0, found = false;
-  if (ok) {
-    found = m < nA;
-    sum_tiles(0, m);
-    if (!found) {
-      if (block_end) at_block_end(acc, run, true);
-      const int mb = poll(nA, nB, blkb);
-      ok = mb >= 0;
-      if (ok) {
-        m = nA + mb;
-        found = mb < nB;
-        sum_tiles(nA, m);
-      }
-    }
-  } else if (block_end) {
-    at_block_end(acc, run, false);
-  }
-  if (!ok) return false;
-  if (found) {
-    // the inclusive state S_[j+1] that chunk j = chunk_of(m) stored
-    Piece32 st[SPER];
-    const uint32_t j = (uint32_t)chunk_of(m);
-#pragma unroll
-    for (int mm = 0; mm < SPER; ++mm)
-      if (T::piece_ok(mm)) st[mm].load(sr, j * (DK * DV) + T::piece_elem(mm));
-#pragma unroll
-    for (int mm = 0; mm < SPER; ++mm)
-      if (T::piece_ok(mm)) st[mm].fma_into(acc[mm], run[mm]);
-  } else if (P.s0) {
-    // S_0 with the decay product of every chunk before c
-    const int bh = seq / P.vparts, part = seq - bh * P.vparts;
-    const float* s0 = P.s0 + (size_t)bh * DK * P.dvp + part * DV + T::piece_n0();
-#pragma unroll
-    for (int mm = 0; mm < SPER; ++mm)
-      if (T::piece_ok(mm)) {
-        const f4* q = reinterpret_cast<const f4*>(s0 + (size_t)T::piece_i(mm) * P.dvp);
-        const f4 lo4 = q[0], hi4 = q[1];
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          acc[mm][e] = fmaf(run[mm], lo4[e], acc[mm][e]);
-          acc[mm][e + 4] = fmaf(run[mm], hi4[e], acc[mm][e + 4]);
-        }
-      }
-  }
-  return true;
-}
-
 // ---------------------------------------------------------------------------
 // staged schedule
 // ---------------------------------------------------------------------------
@@ -1109,7 +689,7 @@ __global__ void __launch_bounds__(tile_threads(C)) gla_summary_kernel(GlaParams 
   const int64_t sc = (int64_t)bh * P.nchunks + c;
   ch.template load<false>(P, sm, bh, c);
   if (ch.range_bad && threadIdx.x == 0) __hip_atomic_fetch_or(P.fault, kFaultRange, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-  ch.template factors<false, true, false>(sm, P.rec + sc * T::RS);
+  ch.template factors<false, true>(sm, P.rec + sc * T::RS);
   ch.template summary_out<false>(sm, static_cast<char*>(P.agg) + sc * (DK * DV) * (T::F16 ? 2 : 4));
 }
 
@@ -1120,9 +700,8 @@ __global__ void __launch_bounds__(tile_threads(C)) gla_summary_kernel(GlaParams 
 // S_final.
 template <int DK, int DV, bool H16>
 __global__ void __launch_bounds__(128) gla_scan_kernel(GlaParams P) {
-  typedef float f2 __attribute__((ext_vector_type(2)));
   typedef _Float16 h2 __attribute__((ext_vector_type(2)));
-  constexpr int RS = DK + 4;
+  constexpr int RS = 2 * DK;
   const int bh = blockIdx.y;
   const int e = blockIdx.x * 256 + 2 * threadIdx.x;
   if (e >= DK * DV) return;
@@ -1143,8 +722,9 @@ __global__ void __launch_bounds__(128) gla_scan_kernel(GlaParams P) {
     for (int m = 0; m < 16; ++m) {
       if (c0 + m < NC) {
         u[m] = *reinterpret_cast<const U2*>(ag + ((int64_t)(c0 + m) * (DK * DV) + e) * (H16 ? 2 : 4));
-        d[m] = rc[(int64_t)(c0 + m) * RS + i];
-        sc[m] = rc[(int64_t)(c0 + m) * RS + DK];
+        const f2 r = *reinterpret_cast<const f2*>(&rc[(int64_t)(c0 + m) * RS + 2 * i]);
+        d[m] = r[0];
+        sc[m] = r[1];
       }
     }
 #pragma unroll
@@ -1189,7 +769,7 @@ __global__ void __launch_bounds__(tile_threads(C)) gla_output_kernel(GlaParams P
     }
     ch.state_tile(sm, acc, ch.state_max(sm, acc));
   }
-  ch.template factors<true, false, false>(sm, nullptr);
+  ch.template factors<true, false>(sm, nullptr);
   f4 O[DV / 16];
   ch.intra(P, sm, bh, c, O);
 #pragma unroll
@@ -1236,102 +816,41 @@ __global__ void __launch_bounds__(tile_threads(C)) gla_chain_kernel(GlaParams P)
   ch.template load<true>(P, sm, bh, c);
   Raw rz[T::SITER];
   if (P.gate) ch.prefetch_gate(P, bh, c, rz);
-  ch.template factors<true, true, true>(sm, P.rec + sc * T::RS);
+  // the chunk record (d_c, the summary's scale) for the chunks after this one
+  ch.template factors<true, true>(sm, nullptr);
+  if (ch.w == 0 && ch.lane < DK)
+    __builtin_amdgcn_raw_buffer_store_b64(__builtin_bit_cast(u32x2, f2{sm.dc[ch.lane], ch.usc}),
+                                          make_rsrc(P.rec + sc * T::RS, T::RS * 4), ch.lane * 8, 0, kAgentCoherent);
   void* U = static_cast<char*>(P.agg) + sc * (DK * DV) * (T::F16 ? 2 : 4);
   ch.template summary_out<true>(sm, U);
-  // the summary and the record are acknowledged before the flag goes up
-  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-  __syncthreads();
-  if (threadIdx.x == 0) __hip_atomic_fetch_or(flag, kFlagSummary, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 
-  // this chunk's own summary pieces, for S_[c+1] and the block prefix (in
-  // flight during the intra part)
-  const int G = P.blk_size;
-  const bool next = c < NC - 1 ? P.publish != 0 : P.s_final != nullptr;
-  const bool block_end = c % G == G - 1 && c < NC - 1;
-  Piece<T::F16> own[T::SPER];
-  if (next || block_end) {
-    const __amdgpu_buffer_rsrc_t ur = make_rsrc(U, DK * DV * (T::F16 ? 2 : 4));
-#pragma unroll
-    for (int m = 0; m < T::SPER; ++m)
-      if (T::piece_ok(m)) own[m].load(ur, T::piece_elem(m));
-  }
-
+  // the intra part runs while the summary stores are acknowledged
   f4 O[DV / 16];
   ch.intra(P, sm, bh, c, O);
 #pragma unroll
   for (int jb = 0; jb < DV / 16; ++jb) O[jb] *= ch.pup;
+  // every wave's summary tiles (and the record) are acknowledged before the
+  // chunk's flag goes up
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  __syncthreads();
+  if (threadIdx.x == 0) __hip_atomic_fetch_or(flag, kFlagSummary, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 
-  // x = Diag(d_c) a + U_c for this wave's pieces (NaN if bad)
-  auto extend = [&](const float (&a)[T::SPER][8], bool bad, float (&x)[T::SPER][8]) {
-#pragma unroll
-    for (int m = 0; m < T::SPER; ++m) {
-      const float dc = sm.dc[T::piece_ok(m) ? T::piece_i(m) : 0];
-#pragma unroll
-      for (int e = 0; e < 8; ++e) x[m][e] = bad ? __builtin_nanf("") : a[m][e] * dc;
-      if (T::piece_ok(m)) own[m].fma_into(x[m], ch.usc);
-    }
-  };
-  // block prefix B_k = Diag(d_c) (sum over the block before c) + U_c and the
-  // block decay D_k = d_c * (product over the block before c), this wave's
-  // pieces, with one power-of-two scale per wave for the fp16 tile
-  auto at_block_end = [&](const float (&a)[T::SPER][8], const float (&rn)[T::SPER], bool good) {
-    constexpr int RB = DK + 8;
-    const int k = c / G;
-    float x[T::SPER][8];
-    extend(a, !good || ch.range_bad, x);
-    const __amdgpu_buffer_rsrc_t bsr = make_rsrc(static_cast<char*>(P.blk) + ((size_t)seq * NC + k) * DK * DV *
-                                                     (T::F16 ? 2 : 4), DK * DV * (T::F16 ? 2 : 4));
-    const __amdgpu_buffer_rsrc_t brr = make_rsrc(P.blkrec + ((size_t)seq * NC + k) * RB, RB * 4);
-    float down = 1.f, bs = 1.f;
-    if constexpr (T::F16) {
-      float mx = 0.f;
-#pragma unroll
-      for (int m = 0; m < T::SPER; ++m)
-#pragma unroll
-        for (int e = 0; e < 8; ++e) mx = fmaxf(mx, T::piece_ok(m) ? fabsf(x[m][e]) : 0.f);
-      const int ex = fp16_exponent(wave_max_uniform(mx));
-      bs = exp2i(ex);
-      down = exp2i(-ex);
-    }
-#pragma unroll
-    for (int m = 0; m < T::SPER; ++m)
-      if (T::piece_ok(m)) {
-        const uint32_t el = T::piece_elem(m);
-        if constexpr (T::F16) {
-          h8 h;
-#pragma unroll
-          for (int e = 0; e < 8; ++e) h[e] = (_Float16)(x[m][e] * down);
-          __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, h), bsr, (int)(el * 2), 0, kAgentCoherent);
-        } else {
-          coh_store4(bsr, el * 4, f4{x[m][0], x[m][1], x[m][2], x[m][3]});
-          coh_store4(bsr, el * 4 + 16, f4{x[m][4], x[m][5], x[m][6], x[m][7]});
-        }
-        if (T::piece_n0() == 0) {
-          const float dci = sm.dc[T::piece_i(m)];
-          coh_store1(brr, T::piece_i(m) * 4, good ? rn[m] * dci : __builtin_nanf(""));
-        }
-      }
-    if (ch.lane == 0) coh_store1(brr, (DK + ch.w) * 4, bs);
-    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // this wave's block stores are acknowledged
-    if (ch.lane == 0)
-      __hip_atomic_fetch_or(flag, 1u << (kFlagBlock + ch.w), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-  };
-
-  float acc[T::SPER][8], run[T::SPER];
-  const bool okw = lookback(P, ch, seq, c, acc, run, at_block_end);
-  // the waves look back on their own; one exchange makes the outcome uniform:
-  // a wait that ran out in any of them (bit 0 of a wave's word) poisons the
-  // whole state, and so does a NaN state handed over by a poisoned chunk before
-  // it (bit 1): either way every row of this chunk and everything it hands
-  // over is NaN. The same exchange gives the largest |S_[c]| for the scale of
-  // the fp16 state tile.
+  float acc[T::SPER][8];
+  const int base = lookback_base(P, ch, seq, c);
+  const bool okw = base >= -1;
+  if (okw) lookback_sum(P, ch, seq, c, base, acc);
+  // one exchange makes the outcome uniform: a wait that ran out (bit 0 of a
+  // wave's word) poisons the whole state, and so does a NaN state handed over
+  // by a poisoned chunk before it (bit 1): either way every row of this chunk
+  // and everything it hands over is NaN. The same exchange gives the largest
+  // |S_[c]| for the scale of the fp16 state tile.
   bool nan_in = false;
   float mx = 0.f;
 #pragma unroll
   for (int m = 0; m < T::SPER; ++m)
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
+      if (!okw) acc[m][e] = 0.f;
       nan_in = nan_in || acc[m][e] != acc[m][e];
       mx = fmaxf(mx, T::piece_ok(m) ? fabsf(acc[m][e]) : 0.f);
     }
@@ -1360,12 +879,25 @@ __global__ void __launch_bounds__(tile_threads(C)) gla_chain_kernel(GlaParams P)
     __hip_atomic_fetch_or(P.fault, (ok ? 0u : kFaultWait) | (ch.range_bad ? kFaultRange : 0u), __ATOMIC_RELAXED,
                           __HIP_MEMORY_SCOPE_AGENT);
 
-  // S_[c+1] = Diag(d_c) S_[c] + U_c: this wave's pieces of the inclusive state
-  // for the chunks after this one (its bit goes up once they are
-  // acknowledged), or of S_final after the last chunk
+  // S_[c+1] = Diag(d_c) S_[c] + U_c: the inclusive state for the chunks after
+  // this one (the flag goes up once every wave's pieces are acknowledged), or
+  // S_final after the last chunk. U_c is read back from the stores every wave
+  // had acknowledged before the flag went up.
+  const bool next = c < NC - 1 ? P.publish != 0 && c % kPublishEvery == kPublishEvery - 1 : P.s_final != nullptr;
   if (next) {
+    Piece<T::F16> own[T::SPER];
+    const __amdgpu_buffer_rsrc_t ur = make_rsrc(U, DK * DV * (T::F16 ? 2 : 4));
+#pragma unroll
+    for (int m = 0; m < T::SPER; ++m)
+      if (T::piece_ok(m)) own[m].load(ur, T::piece_elem(m));
     float nx[T::SPER][8];
-    extend(acc, poison, nx);
+#pragma unroll
+    for (int m = 0; m < T::SPER; ++m) {
+      const float dc = sm.dc[T::piece_ok(m) ? T::piece_i(m) : 0];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) nx[m][e] = acc[m][e] * dc;
+      if (T::piece_ok(m)) own[m].fma_into(nx[m], ch.usc);
+    }
     if (c < NC - 1) {
       const __amdgpu_buffer_rsrc_t sr = make_rsrc(P.states + sc * (DK * DV), DK * DV * 4);
 #pragma unroll
@@ -1375,13 +907,13 @@ __global__ void __launch_bounds__(tile_threads(C)) gla_chain_kernel(GlaParams P)
           coh_store4(sr, T::piece_elem(m) * 4 + 16, f4{nx[m][4], nx[m][5], nx[m][6], nx[m][7]});
         }
       asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-      if (ch.lane == 0)
-        __hip_atomic_fetch_or(flag, 1u << (kFlagInclusive + ch.w), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      __syncthreads();
+      if (threadIdx.x == 0) __hip_atomic_fetch_or(flag, kFlagInclusive, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     } else {
 #pragma unroll
       for (int m = 0; m < T::SPER; ++m)
         if (T::piece_ok(m)) {
-          f4* dst = reinterpret_cast<f4*>(P.s_final + ((size_t)bh * DK + T::piece_i(m)) * P.dvp + T::piece_n0());
+          f4* dst = reinterpret_cast<f4*>(P.s_final + ((size_t)bh * DK + T::piece_i(m)) * P.dvp + T::piece_n0(m));
           dst[0] = f4{nx[m][0], nx[m][1], nx[m][2], nx[m][3]};
           dst[1] = f4{nx[m][4], nx[m][5], nx[m][6], nx[m][7]};
         }
@@ -1423,6 +955,11 @@ struct KernelSet {
   const void* chain;
   const void* chain_split;  // one launch with d_v split in two (d_v = 64 only), else null
   int threads;
+  const void* lean;        // one launch for 16-bit inputs at chunk 64 (gla_lean.hip), else null
+  const void* lean_split;  // the same with d_v split in two, else null
+  // the one-launch kernels that run: the lean ones where they exist
+  const void* one() const { return lean ? lean : chain; }
+  const void* one_split() const { return lean_split ? lean_split : chain_split; }
 };
 
 template <int DK, int DV, int C, int IN>
@@ -1454,12 +991,15 @@ static bool pick_dims(int dk, int dv, int chunk, KernelSet* ks) {
 }
 
 static bool select_kernels(const GlaShape& s, KernelSet* ks) {
+  bool ok = false;
   switch (s.qdt) {
-    case GTR_F32: return pick_dims<GTR_F32>(s.dk, s.dv, s.chunk, ks);
-    case GTR_F16: return pick_dims<GTR_F16>(s.dk, s.dv, s.chunk, ks);
-    case GTR_BF16: return pick_dims<GTR_BF16>(s.dk, s.dv, s.chunk, ks);
+    case GTR_F32: ok = pick_dims<GTR_F32>(s.dk, s.dv, s.chunk, ks); break;
+    case GTR_F16: ok = pick_dims<GTR_F16>(s.dk, s.dv, s.chunk, ks); break;
+    case GTR_BF16: ok = pick_dims<GTR_BF16>(s.dk, s.dv, s.chunk, ks); break;
     default: return false;
   }
+  if (ok) lean_kernels(s.qdt, s.dk, s.dv, s.chunk, &ks->lean, &ks->lean_split);
+  return ok;
 }
 
 // Work-groups of `kernel` resident per CU and the device's CU count (0 if a
@@ -1495,12 +1035,29 @@ static int resident_per_cu(const void* kernel, int threads, int* cus) {
   return per_cu;
 }
 
+// XCDs of the current device (1 if the query fails): the one-launch kernel for
+// 16-bit inputs lays out its grid so that every chunk of a sequence runs on one
+// XCD. Kept per device like the occupancy answers.
+static int xcd_count() {
+  static std::mutex mu;
+  static int cache[64];
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 1;
+  std::lock_guard<std::mutex> lk(mu);
+  if (cache[dev] == 0) {
+    int n = 0;
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeNumberOfXccs, dev) != hipSuccess || n < 1 || n > 16) n = 1;
+    cache[dev] = n;
+  }
+  return cache[dev];
+}
+
 struct Plan {
   int sched;    // GTR_PATH_FUSED (one launch, look-back), GTR_PATH_INLINE (one launch, no inclusive states)
                 // or GTR_PATH_STAGED
   int vparts;   // value split of the one-launch schedules
   int desc;     // chunks in descending order (every work-group resident at once)
-  int blk_size;  // chunks per block of the two-level look-back
+  int nxcd;     // sequence-per-XCD grid of the 16-bit kernel (0: chunk-major grid)
   int64_t blocks;
 };
 
@@ -1519,36 +1076,54 @@ struct Plan {
 //     resident at once.
 // An explicit path that does not fit is GTR_ERR_UNSUPPORTED; STAGED always fits.
 constexpr int64_t kInlineMaxChunks = 32;
-constexpr int kBlockChunks = 32;  // chunks per block of the one-launch look-back
+constexpr int64_t kFusedMaxChunks = 64;  // longer sequences: the staged kernels are faster
 
 static gtr_status plan_call(const GlaShape& s, int path, bool gate, const KernelSet& ks, Plan* pl) {
   pl->sched = GTR_PATH_STAGED;
   pl->vparts = 1;
   pl->desc = 0;
-  pl->blk_size = 2;
+  pl->nxcd = 0;
   pl->blocks = 0;
   if (path == GTR_PATH_STAGED) return GTR_OK;
   const bool fits = s.nchunks <= kMaxChainChunks && s.BH <= kSyncSeqs;
   if (!fits) return path == GTR_PATH_AUTO ? GTR_OK : GTR_ERR_UNSUPPORTED;
   int cus = 0;
-  const int per_cu = resident_per_cu(ks.chain, ks.threads, &cus);
-  const int64_t resident = (int64_t)per_cu * cus;  // 0 without a usable device
-  if (!gate && ks.chain_split && 2 * s.BH <= kSyncSeqs && cus > 0 && 2 * s.BH * s.nchunks <= cus) {
+  const int per_cu = resident_per_cu(ks.one(), ks.threads, &cus);
+  int64_t resident = (int64_t)per_cu * cus;  // 0 without a usable device
+  if (!gate && ks.one_split() && 2 * s.BH <= kSyncSeqs && cus > 0 && 2 * s.BH * s.nchunks <= cus) {
     int c2 = 0;
-    if (resident_per_cu(ks.chain_split, ks.threads, &c2) > 0) pl->vparts = 2;
+    const int per_cu2 = resident_per_cu(ks.one_split(), ks.threads, &c2);
+    if (per_cu2 > 0) {
+      pl->vparts = 2;
+      resident = (int64_t)per_cu2 * c2;
+    }
   }
   const int64_t ns = s.BH * pl->vparts;
-  const bool all_resident = resident > 0 && ns * s.nchunks <= resident;
-  if (path == GTR_PATH_AUTO)
-    pl->sched = all_resident && s.nchunks <= kInlineMaxChunks ? GTR_PATH_INLINE : GTR_PATH_FUSED;
-  else
+  bool all_resident = resident > 0 && ns * s.nchunks <= resident;
+  const int nx = (pl->vparts > 1 ? ks.lean_split : ks.lean) ? xcd_count() : 1;
+  if (nx > 1 && cus >= nx && (ns + nx - 1) / nx * s.nchunks <= cus / nx) {
+    // every XCD runs ceil(ns / nx) sequences, one work-group per CU: the
+    // summaries stay in the XCD's L2. (Where the sequences do not spread
+    // evenly or need more than one round of an XCD's CUs, the chunk-major grid
+    // over all XCDs is faster.)
+    pl->nxcd = nx;
+    all_resident = true;
+  }
+  if (path == GTR_PATH_AUTO) {
+    if (all_resident && s.nchunks <= kInlineMaxChunks)
+      pl->sched = GTR_PATH_INLINE;
+    else
+      pl->sched = s.nchunks <= kFusedMaxChunks ? GTR_PATH_FUSED : GTR_PATH_STAGED;
+  } else {
     pl->sched = path;
+  }
+  if (pl->sched == GTR_PATH_STAGED) {
+    pl->vparts = 1;
+    pl->nxcd = 0;
+    return GTR_OK;
+  }
   pl->desc = all_resident ? 1 : 0;
-  // blocks of 32 chunks: a sequence of at most 32 chunks has one block and a
-  // single-level look-back; longer ones read at most 31 summaries and 7 block
-  // prefixes (kMaxChainChunks / 32 - 1), which bounds what one wave polls at once
-  pl->blk_size = kBlockChunks;
-  pl->blocks = ns * s.nchunks;
+  pl->blocks = pl->nxcd > 1 ? (int64_t)pl->nxcd * ((ns + pl->nxcd - 1) / pl->nxcd) * s.nchunks : ns * s.nchunks;
   return GTR_OK;
 }
 
@@ -1630,8 +1205,6 @@ static gtr_status gla_launch(const gtr_gla_args* a, const GlaShape& s, hipStream
   P.sync = reinterpret_cast<unsigned*>(ws + lay.sync_off);
   P.flags = reinterpret_cast<unsigned*>(ws + lay.flags_off);
   P.agg = ws + lay.agg_off;
-  P.blk = ws + lay.blk_off;
-  P.blkrec = reinterpret_cast<float*>(ws + lay.blkrec_off);
   P.rec = reinterpret_cast<float*>(ws + lay.rec_off);
   P.states = reinterpret_cast<float*>(ws + lay.states_off);
   P.gkind = a->g_kind;
@@ -1645,13 +1218,13 @@ static gtr_status gla_launch(const gtr_gla_args* a, const GlaShape& s, hipStream
   P.ns = (int)(s.BH * pl.vparts);
   P.desc = pl.desc;
   P.publish = pl.sched == GTR_PATH_FUSED;
-  P.blk_size = pl.blk_size;
+  P.nxcd = pl.nxcd;
   P.spin = a->spin_limit ? a->spin_limit : kSpinDefault;
 
   void* kargs[] = {&P};
   hipError_t err;
   if (pl.sched != GTR_PATH_STAGED) {
-    const void* k = pl.vparts > 1 ? ks.chain_split : ks.chain;
+    const void* k = pl.vparts > 1 ? ks.one_split() : ks.one();
     err = hipLaunchKernel(k, dim3((unsigned)pl.blocks), dim3(ks.threads), kargs, 0, stream);
   } else {
     err = hipLaunchKernel(ks.summary, dim3((unsigned)s.nchunks, (unsigned)s.BH), dim3(ks.threads), kargs, 0, stream);

@@ -124,13 +124,9 @@ WorkspaceLayout gla_workspace_layout(const GlaShape& s) {
   w.agg_off = off;
   off = align256(off + tiles * s.dk * s.dv * (s.qdt == GTR_F32 ? 4 : 2));
   w.rec_off = off;
-  off = align256(off + 2 * tiles * (s.dk + 4) * sizeof(float));  // two records per chunk under the value split
+  off = align256(off + 2 * tiles * (2 * s.dk) * sizeof(float));  // two records per chunk under the value split
   w.states_off = off;
   off = align256(off + tiles * s.dk * s.dv * sizeof(float));
-  w.blk_off = off;
-  off = align256(off + tiles * s.dk * s.dv * (s.qdt == GTR_F32 ? 4 : 2));
-  w.blkrec_off = off;
-  off = align256(off + 2 * tiles * (s.dk + 8) * sizeof(float));
   w.total = off;
   return w;
 }

@@ -30,10 +30,8 @@ struct WorkspaceLayout {
   size_t sync_off;    // [kSyncSeqs][4] 32-bit counters
   size_t flags_off;   // [kSyncSeqs][kMaxChainChunks] 32-bit chunk flags
   size_t agg_off;     // [BH][nchunks][dk][dv] summaries: fp16 (16-bit inputs) or float32
-  size_t rec_off;     // [2 BH][nchunks][dk + 4] float32 chunk records (decays, summary scale)
+  size_t rec_off;     // [2 BH][nchunks][dk][2] float32 chunk records (decay, summary scale)
   size_t states_off;  // [BH][nchunks][dk][dv] float32 boundary states
-  size_t blk_off;     // [BH][nchunks][dk][dv] block prefixes of the one-launch look-back (as the summaries)
-  size_t blkrec_off;  // [2 BH][nchunks][dk + 8] float32 block records (decays, per-wave scales)
   size_t total;
 };
 

@@ -25,6 +25,8 @@ Reported per instruction:
   WARN-DATA-ADDR  an address depends on loaded data
   WARN-UNDEF-DATA stored data (active lanes) is undefined
   INFO-BUFFER-OOR buffer accesses dropped by the descriptor's range check
+  INFO-DATA-OFFSET a buffer access whose offset depends on loaded data, with
+                  the descriptor's whole range inside one registered buffer
 Barriers, waits and cache maintenance are no-ops; atomics return opaque data
 unless the buffer they hit has a fixed load value.
 """
@@ -406,6 +408,18 @@ class Wave:
         self.s64set(tok, bits, obits, dbits)
 
     # ---- memory checks
+    def check_window(self, inst, base, size, mode):
+        """A buffer descriptor's whole range [base, base + size): inside one
+        registered buffer that allows `mode` (INFO-DATA-OFFSET), else ERR-OOB."""
+        for rg in self.regions:
+            if rg.base <= base and base + size <= rg.base + rg.size:
+                if mode == 'w' and 'w' not in rg.mode:
+                    self.rep.add('ERR-MODE', inst, rg.name)
+                else:
+                    self.rep.add('INFO-DATA-OFFSET', inst, rg.name)
+                return
+        self.rep.add('ERR-OOB', inst, f"descriptor window {base:#x}+{size:#x} {near(self.regions, base)}")
+
     def check_addr(self, inst, addr, d, o, size, mode, lanes):
         """addr uint64[64]; returns nothing; reports."""
         act = lanes
@@ -528,6 +542,15 @@ def _endpgm(w, i):
 @handler('s_nop', 's_waitcnt', 's_barrier', 's_sleep', 's_setprio', 's_waitcnt_vscnt', 's_sethalt', 'buffer_wbl2', 'buffer_inv', 'buffer_gl0_inv', 'buffer_gl1_inv')
 def _nop(w, i):
     return False
+
+
+HWREG_VALUE = 0  # what s_getreg_b32 reads: the emulated wave runs on XCC 0
+
+
+@handler('s_getreg_b32')
+def _getreg(w, i):
+    r = w.sreg_index(i.ops[0])
+    w.sset(r, HWREG_VALUE, 0, True)
 
 
 @handler('s_branch')
@@ -827,6 +850,15 @@ def logic64(kind):
     return h
 
 
+@handler('s_not_b64')
+def _s_not_b64(w, i):
+    a = w.s64(i.ops[1], i)
+    v, o = bit_not(a[0], a[1])
+    w.s64set(i.ops[0], v, o, a[2])
+    known1 = v & ~o
+    set_scc(w, 1 if known1 else 0, bool(o) and not known1, a[2])
+
+
 HANDLERS.update({'s_and_b64': logic64('and'), 's_or_b64': logic64('or'), 's_xor_b64': logic64('xor'),
                  's_andn2_b64': logic64('andn2'), 's_orn2_b64': logic64('orn2'), 's_nor_b64': logic64('nor'),
                  's_nand_b64': logic64('nand'), 's_xnor_b64': logic64('xnor')})
@@ -997,6 +1029,16 @@ def valu(fn, nsrc):
     return h
 
 
+def _bfe_i32(a, b, c):
+    """Signed bit-field extract: width c & 31 bits of a from offset b & 31, sign-extended."""
+    off = (b & np.uint32(31)).astype(np.int64)
+    wid = (c & np.uint32(31)).astype(np.int64)
+    x = (a.astype(np.int64) >> off) & ((np.int64(1) << wid) - 1)
+    sign = np.where(wid > 0, (x >> np.maximum(wid - 1, 0)) & 1, 0)
+    x = np.where(sign == 1, x - (np.int64(1) << wid), x)
+    return (x & M32).astype(np.uint32)
+
+
 def u64(x):
     return x.astype(np.uint64)
 
@@ -1046,6 +1088,7 @@ HANDLERS.update({
     'v_lshl_or_b32': valu(lambda a, b, c: (a << (b & np.uint32(31))) | c, 3),
     'v_add_lshl_u32': valu(lambda a, b, c: (a + b) << (c & np.uint32(31)), 3),
     'v_and_or_b32': valu(lambda a, b, c: (a & b) | c, 3),
+    'v_bfe_i32': valu(lambda a, b, c: _bfe_i32(a, b, c), 3),
     'v_bfe_u32': valu(lambda a, b, c: (a >> (b & np.uint32(31))) & ((np.uint64(1) << u64(c & np.uint32(31))) - np.uint64(1)).astype(np.uint32), 3),
     'v_mul_lo_u32': valu(lambda a, b: (u64(a) * u64(b)) & np.uint64(M32), 2),
     'v_mul_hi_u32': valu(lambda a, b: (u64(a) * u64(b)) >> np.uint64(32), 2),
@@ -1166,7 +1209,8 @@ def dataop(nsrc, first=1):
 
 for _n, _k in [('v_cvt_f32_f16_e32', 1), ('v_cvt_f32_f16_e64', 1), ('v_cvt_f32_f16_sdwa', 1), ('v_cvt_f16_f32_e32', 1),
                ('v_cvt_pk_f16_f32', 2), ('v_pack_b32_f16', 2), ('v_perm_b32', 3), ('v_or_b32_sdwa', 2),
-               ('v_fma_mixlo_f16', 3), ('v_fma_mixhi_f16', 3), ('v_fma_mix_f32', 3), ('v_cvt_f32_bf16', 1)]:
+               ('v_fma_mixlo_f16', 3), ('v_fma_mixhi_f16', 3), ('v_fma_mix_f32', 3), ('v_cvt_f32_bf16', 1),
+               ('v_pk_mul_f16', 2)]:
     HANDLERS[_n] = dataop(_k)
 
 
@@ -1527,6 +1571,8 @@ def ds_write(size, two=False, st64=False):
 HANDLERS.update({
     'ds_read_b32': ds_read(1, 4), 'ds_read_b64': ds_read(2, 8), 'ds_read_b128': ds_read(4, 16),
     'ds_read_b96': ds_read(3, 12),
+    # transposing read: each lane reads 8 bytes of the row block; same address rules as ds_read_b64
+    'ds_read_b64_tr_b16': ds_read(2, 8),
     'ds_read2_b32': ds_read(2, 4, True), 'ds_read2st64_b32': ds_read(2, 4, True, True),
     'ds_read2_b64': ds_read(4, 8, True),
     'ds_read_u16': ds_read(1, 2), 'ds_read_u16_d16': ds_read(1, 2), 'ds_read_u16_d16_hi': ds_read(1, 2),
@@ -1658,6 +1704,11 @@ def buffer_op(nregs, store):
         o = vo | bool(so_o) | ro
         if (~d & lanes).any():
             w.rep.add('ERR-UNDEF-ADDR', i, f"lanes {np.nonzero(~d & lanes)[0][:8].tolist()}")
+        elif (o & lanes).any() and not ro and not so_o and lanes.any():
+            # an offset that depends on loaded data: the descriptor still
+            # confines every access to [base, base + num_records), so the whole
+            # window must lie inside one buffer the access may touch
+            w.check_window(i, base + so_v, nrec, 'w' if store else 'r')
         elif (o & lanes).any():
             w.rep.add('WARN-DATA-ADDR', i)
         else:

@@ -82,16 +82,15 @@ def test_workspace_size_formula(lib):
     a256 = lambda x: (x + 255) // 256 * 256
     # header, done counters of 1024 sequences, chunk flags of 1024 x 256, then
     # the summaries (fp16 for 16-bit inputs, float32 for float32 inputs), the
-    # chunk records (two per chunk for the value split) and the float32 states
-    # and (one-launch look-back) the block prefixes and the block records
+    # chunk records ((decay, scale) pairs per key dim, two per chunk for the
+    # value split) and the float32 states
     fixed = 256 + 1024 * 16 + 1024 * 256 * 4
-    rec = a256(2 * BH * nc * (64 + 4) * 4)
-    brec = a256(2 * BH * nc * (64 + 8) * 4)
+    rec = a256(2 * BH * nc * (2 * 64) * 4)
     states = BH * nc * 64 * 64 * 4
-    want = fixed + BH * nc * 64 * 64 * 2 + rec + states + BH * nc * 64 * 64 * 2 + brec
+    want = fixed + a256(BH * nc * 64 * 64 * 2) + rec + states
     assert a.qkv_dtype != gtr.F32 and lib.gtr_gla_workspace_size(ctypes.byref(a)) == want
     a.qkv_dtype = a.g_dtype = a.o_dtype = gtr.F32
-    want = fixed + BH * nc * 64 * 64 * 4 + rec + states + BH * nc * 64 * 64 * 4 + brec
+    want = fixed + BH * nc * 64 * 64 * 4 + rec + states
     assert lib.gtr_gla_workspace_size(ctypes.byref(a)) == want
     a.dk = 48
     assert lib.gtr_gla_workspace_size(ctypes.byref(a)) == 0
@@ -100,7 +99,7 @@ def test_workspace_size_formula(lib):
 def test_schedule_query_without_device(lib):
     """gtr_gla_schedule: -1 for invalid arguments. AUTO is length-aware: INLINE
     up to 32 chunks per sequence when the whole grid is resident at once, FUSED
-    up to 256 chunks, STAGED beyond; an explicit one-launch path that does not
+    up to 64 chunks, STAGED beyond; an explicit one-launch path that does not
     fit (more than 256 chunks) reports -1. Without a usable device residency is
     unknown (so AUTO takes FUSED) and the value split is off."""
     assert lib.gtr_gla_schedule(None) == -1
@@ -109,8 +108,13 @@ def test_schedule_query_without_device(lib):
     a.path = 3
     assert lib.gtr_gla_schedule(ctypes.byref(a)) == 3
     a.path = 0
-    a.H = a.W = 80  # 100 chunks
+    a.H, a.W = 40, 80  # 50 chunks
     assert lib.gtr_gla_schedule(ctypes.byref(a)) == 1
+    a.H = a.W = 80  # 100 chunks
+    assert lib.gtr_gla_schedule(ctypes.byref(a)) == 2
+    a.path = 1  # an explicit one-launch path still fits
+    assert lib.gtr_gla_schedule(ctypes.byref(a)) == 1
+    a.path = 0
     a.H = a.W = 200  # 625 chunks
     assert lib.gtr_gla_schedule(ctypes.byref(a)) == 2
     a.path = 1

@@ -85,12 +85,53 @@ def test_emulator_flags_out_of_bounds():
     assert rep.counts.get("ERR-OOB", 0) >= 1
 
 
+WINDOW_SNIPPET = """
+{name}:
+	s_load_dwordx2 s[4:5], s[0:1], 0x0
+	s_waitcnt lgkmcnt(0)
+	v_mov_b32_e32 v2, s4
+	v_mov_b32_e32 v3, s5
+	global_load_dword v4, v[2:3], off
+	s_mov_b32 s8, s4
+	s_and_b32 s9, s5, 0xffff
+	s_mov_b32 s10, {nrec}
+	s_mov_b32 s11, 0x20000
+	s_waitcnt vmcnt(0)
+	buffer_load_dword v5, v4, s[8:11], 0 offen
+	s_endpgm
+.Lfunc_end0:
+	.amdhsa_kernel {name}
+		.amdhsa_group_segment_fixed_size 0
+		.amdhsa_private_segment_fixed_size 0
+		.amdhsa_kernarg_size 8
+		.amdhsa_user_sgpr_count 2
+		.amdhsa_user_sgpr_kernarg_segment_ptr 1
+		.amdhsa_system_sgpr_workgroup_id_x 1
+	.end_amdhsa_kernel
+"""
+
+
+def test_emulator_bounds_a_data_dependent_buffer_offset_by_its_descriptor():
+    # the offset of the buffer load is loaded data (unknown): safe exactly when
+    # the descriptor's whole window lies inside the 256-byte buffer
+    for nrec, bad in ((256, False), (260, True)):
+        name = "_Zwindow"
+        prog, labels, desc = emu.parse_kernel("\n" + WINDOW_SNIPPET.format(name=name, nrec=nrec), name)
+        base = 0x1000_0000_0000
+        regions = [emu.Region("buf", base, 64 * 4, "r"), emu.Region("kernarg", emu.KERNARG_BASE, 8, "r")]
+        rep = emu.Report()
+        emu.run_wave(prog, labels, desc, struct.pack("<Q", base), regions, 0, (0, 0, 0), 0, rep)
+        assert (rep.counts.get("ERR-OOB", 0) >= 1) == bad, (nrec, dict(rep.counts))
+        assert (rep.counts.get("INFO-DATA-OFFSET", 0) >= 1) == (not bad), (nrec, dict(rep.counts))
+        assert "WARN-DATA-ADDR" not in rep.counts
+
+
 # ---------------------------------------------------------------------------
 # the library's kernels
 # ---------------------------------------------------------------------------
 DT = {"f32": (0, 4), "f16": (1, 2), "bf16": (2, 2)}
 SCAN = {"row": 0, "col": 1, "row_rev": 2, "col_rev": 3}
-KERNARG_BYTES = 232  # sizeof(GlaParams)
+KERNARG_BYTES = 216  # sizeof(GlaParams)
 
 
 def a256(x):
@@ -98,7 +139,8 @@ def a256(x):
 
 
 def device_asm() -> str:
-    """gfx950 assembly of gla_fwd.hip with the library's flags (cached by source hash)."""
+    """gfx950 assembly of the GLA kernels (gla_fwd.hip, gla_lean.hip) with the
+    library's flags, cached by source hash."""
     from paper_2609_26590_amd import build as b
     h = hashlib.sha256()
     for f in sorted(os.listdir(CSRC)):
@@ -108,18 +150,21 @@ def device_asm() -> str:
         h.update(fh.read())
     h.update(" ".join(b.HIPCC_FLAGS).encode())
     os.makedirs(BUILD, exist_ok=True)
-    path = os.path.join(BUILD, f"gla_fwd.gfx950.{h.hexdigest()[:16]}.s")
-    if not os.path.exists(path):
-        hipcc = b._hipcc() if shutil.which("hipcc") or os.path.exists("/opt/rocm/bin/hipcc") else None
-        if hipcc is None:
-            pytest.skip("hipcc is not available")
-        tmp = path + f".tmp{os.getpid()}"
-        r = subprocess.run([hipcc, *b.HIPCC_FLAGS, "-S", "--cuda-device-only", os.path.join(CSRC, "gla_fwd.hip"),
-                            "-o", tmp], capture_output=True, text=True)
-        assert r.returncode == 0, r.stderr[-2000:]
-        os.replace(tmp, path)
-    with open(path) as fh:
-        return fh.read()
+    texts = []
+    for src in ("gla_fwd.hip", "gla_lean.hip"):
+        path = os.path.join(BUILD, f"{src[:-4]}.gfx950.{h.hexdigest()[:16]}.s")
+        if not os.path.exists(path):
+            hipcc = b._hipcc() if shutil.which("hipcc") or os.path.exists("/opt/rocm/bin/hipcc") else None
+            if hipcc is None:
+                pytest.skip("hipcc is not available")
+            tmp = path + f".tmp{os.getpid()}"
+            r = subprocess.run([hipcc, *b.HIPCC_FLAGS, "-S", "--cuda-device-only", os.path.join(CSRC, src),
+                                "-o", tmp], capture_output=True, text=True)
+            assert r.returncode == 0, r.stderr[-2000:]
+            os.replace(tmp, path)
+        with open(path) as fh:
+            texts.append(fh.read())
+    return "\n".join(texts)
 
 
 class Shape:
@@ -136,14 +181,14 @@ class Shape:
 
 class Launch:
     """How the one-launch kernel is run: value parts, descending chunk order
-    (every work-group resident), inclusive states published, and the value
-    every chunk flag reads as (FLAG_BLOCKS: summaries and block prefixes, the
-    look-back walks back to the start; FLAG_ALL: inclusive states everywhere as
-    well, it stops at the nearest; FLAG_NONE: nothing is ever ready, every wait
-    runs out after the spin limit)."""
+    (every work-group resident), inclusive states published, the value every
+    chunk flag reads as (FLAG_SUMMARY: summaries only, the look-back walks back
+    to the start; FLAG_ALL: inclusive states everywhere as well, it stops at the
+    nearest; FLAG_NONE: nothing is ever ready, every wait runs out after the
+    spin limit) and the XCDs of the sequence-per-XCD grid (0: chunk-major)."""
 
-    def __init__(self, vparts=1, desc=0, publish=1, flag=0x00FF0001):
-        self.vparts, self.desc, self.publish, self.flag = vparts, desc, publish, flag
+    def __init__(self, vparts=1, desc=0, publish=1, flag=1, nxcd=0):
+        self.vparts, self.desc, self.publish, self.flag, self.nxcd = vparts, desc, publish, flag, nxcd
 
 
 def kernel_args(c: Shape, ln: Launch = Launch()):
@@ -175,24 +220,19 @@ def kernel_args(c: Shape, ln: Launch = Launch()):
     agg = a256(flags + 1024 * 256 * 4)
     tiles = c.BH * c.NC
     rec = a256(agg + tiles * c.dk * c.dv * (4 if c.dt == "f32" else 2))
-    states = a256(rec + 2 * tiles * (c.dk + 4) * 4)
-    blk = a256(states + tiles * c.dk * c.dv * 4)
-    blkrec = a256(blk + tiles * c.dk * c.dv * (4 if c.dt == "f32" else 2))
-    total = a256(blkrec + 2 * tiles * (c.dk + 8) * 4)
+    states = a256(rec + 2 * tiles * (2 * c.dk) * 4)
+    total = a256(states + tiles * c.dk * c.dv * 4)
     ws = alloc("workspace", total, "rw")
     ns = c.BH * ln.vparts
     regions.insert(0, emu.Region("flags", ws + flags, 1024 * 256 * 4, "rw", load_value=ln.flag))
     regions.insert(0, emu.Region("sync", ws + sync, ns * 16, "rw"))
     regions.insert(0, emu.Region("fault", ws, 256, "rw"))
     regions.append(emu.Region("kernarg", emu.KERNARG_BASE, KERNARG_BYTES, "r"))
-    G = 2
-    while G < 16 and G * G < c.NC:
-        G += 1
-    kern = struct.pack("<7Q6iqifi4x8Qif2Qif6iI4x", q, k, v, g, o, s0, sf, DT[c.dt][0], DT[c.gdt][0],
+    kern = struct.pack("<7Q6iqifi4x6Qif2Qif6iI4x", q, k, v, g, o, s0, sf, DT[c.dt][0], DT[c.gdt][0],
                        DT[c.odt][0], c.BH, c.H, c.W, c.L, c.NC, c.dk ** -0.5, SCAN[c.scan],
-                       ws + agg, ws + rec, ws + states, ws + sync, ws + flags, ws + blk, ws + blkrec, ws,
+                       ws + agg, ws + rec, ws + states, ws + sync, ws + flags, ws,
                        1 if c.logits else 0, 1.0 / 16, z, nw, DT[c.zdt][0] if c.zdt else 0, 1e-5,
-                       c.dv, ln.vparts, ns, ln.desc, ln.publish, G, 8)
+                       c.dv, ln.vparts, ns, ln.desc, ln.publish, ln.nxcd, 8)
     assert len(kern) == KERNARG_BYTES
     return kern, regions
 
@@ -207,6 +247,10 @@ def mangled(kind: str, c: Shape) -> str:
         return f"_ZN3gtr15gla_scan_kernelILi{c.dk}ELi{c.dv}ELb{int(c.dt != 'f32')}EEEvNS_9GlaParamsE"
     if kind == "chain_split":  # d_v / 2 columns per work-group
         return f"_ZN3gtr16gla_chain_kernelILi{c.dk}ELi{c.dv // 2}ELi{c.chunk}ELi{DT[c.dt][0]}EEEvNS_9GlaParamsE"
+    if kind == "lean_split":
+        return f"_ZN3gtr15gla_lean_kernelILi{c.dk}ELi{c.dv // 2}ELi{c.chunk}ELi{DT[c.dt][0]}EEEvNS_9GlaParamsE"
+    if kind == "lean":
+        return f"_ZN3gtr15gla_lean_kernel{t}EEvNS_9GlaParamsE"
     return f"_ZN3gtr16gla_chain_kernel{t}EEvNS_9GlaParamsE"
 
 
@@ -223,47 +267,76 @@ def work_groups(kind: str, c: Shape, ln: Launch):
         return [((x, bh, 0), 2) for x in sorted({0, eb - 1}) for bh in bhs]  # 128 threads
     ns = c.BH * ln.vparts
     seqs = sorted({0, ns - 1})
-    # chunk-major grid: block row * ns + seq, row = chunk (or NC - 1 - chunk)
     rows = sorted({(c.NC - 1 - cc) if ln.desc else cc for cc in cs})
+    if ln.nxcd > 1:
+        # sequence-per-XCD grid: block (row * nx + j) * nxcd + x runs sequence
+        # x + nxcd * j, nx = the sequences of XCD x; blocks past an XCD's share return
+        nx = lambda x: (ns - x + ln.nxcd - 1) // ln.nxcd
+        blocks = ln.nxcd * ((ns + ln.nxcd - 1) // ln.nxcd) * c.NC
+        out = [(((r * nx(sq % ln.nxcd) + sq // ln.nxcd) * ln.nxcd + sq % ln.nxcd, 0, 0), nw)
+               for r in rows for sq in seqs]
+        pad = [(nx(x) * c.NC) * ln.nxcd + x for x in range(ln.nxcd)]
+        out += [((bb, 0, 0), nw) for bb in pad if bb < blocks][:1]
+        return out
+    # chunk-major grid: block row * ns + seq, row = chunk (or NC - 1 - chunk)
     return [((r * ns + sq, 0, 0), nw) for r in rows for sq in seqs]
 
 
 # (shape, kernels): the bf16 instantiations, float32 gates with 16-bit inputs,
 # every chunk size, reversed and column scans, S0 / S_final, partial chunks;
-# the one-launch kernel in both chunk orders, both flag states and the value split
+# the one-launch kernels in both chunk orders, every flag state, the value split
+# and (16-bit kernel) the sequence-per-XCD grid
 CHAIN = ("chain", "chain_x", "chain_i")
+# the 16-bit kernel at chunk 64: every launch variant on one shape, one variant on the others
+LEAN = ("lean", "lean_n", "lean_x", "lean_i", "lean_xcd", "lean_split")
 CHECKS = [
     (Shape(1, 12, 40, 40, 64, 64, 64, "bf16", "bf16", "f32", "row", False, False),
-     ("summary", "scan", "output") + CHAIN + ("chain_split",)),
-    (Shape(8, 12, 40, 40, 64, 64, 64, "bf16", "bf16", "f32", "col_rev", True, True), ("output",) + CHAIN),
+     ("summary", "scan", "output") + CHAIN + ("chain_split",) + LEAN),
+    (Shape(8, 12, 40, 40, 64, 64, 64, "bf16", "bf16", "f32", "col_rev", True, True), ("output",) + CHAIN + ("lean_x",)),
     (Shape(2, 9, 12, 20, 32, 32, 32, "bf16", "f32", "f32", "col", True, True), ("summary", "output") + CHAIN),
     (Shape(1, 2, 20, 20, 32, 64, 128, "bf16", "bf16", "bf16", "row_rev", False, False), ("output",) + CHAIN),
-    (Shape(1, 6, 40, 40, 64, 64, 64, "f16", "f16", "f16", "row", False, False), CHAIN + ("chain_split",)),
+    (Shape(1, 6, 40, 40, 64, 64, 64, "f16", "f16", "f16", "row", False, False),
+     CHAIN + ("chain_split", "lean_split")),
+    (Shape(1, 5, 9, 23, 32, 64, 64, "f16", "f32", "f32", "row_rev", True, True), ("lean", "lean_split")),
+    (Shape(3, 3, 16, 16, 32, 32, 64, "bf16", "f32", "bf16", "col", False, True), ("lean_xcd",)),
     (Shape(1, 3, 7, 9, 64, 64, 128, "f16", "f32", "f32", "col", True, True), ("output",) + CHAIN + ("chain_split",)),
     (Shape(1, 2, 13, 11, 64, 64, 32, "f32", "f32", "f32", "row_rev", True, True), CHAIN + ("chain_split",)),
     (Shape(1, 2, 13, 11, 32, 32, 32, "f32", "f32", "f32", "row", False, True), ("summary", "output") + CHAIN),
-    (Shape(1, 6, 80, 80, 64, 64, 64, "f16", "f16", "f16", "row", False, False), ("scan",) + CHAIN),
+    (Shape(1, 6, 80, 80, 64, 64, 64, "f16", "f16", "f16", "row", False, False), ("scan",) + CHAIN + ("lean",)),
     # gate fusion and the output-gate epilogue
     (Shape(1, 12, 40, 40, 64, 64, 64, "bf16", "bf16", "f32", "col", True, True, True, "bf16", True),
-     ("summary", "output") + CHAIN),
+     ("summary", "output") + CHAIN + ("lean_i",)),
+    (Shape(2, 3, 8, 8, 64, 64, 64, "f16", "f32", "f16", "row", False, False, True, "f32", False), ("lean",)),
     (Shape(1, 3, 7, 9, 32, 64, 32, "f16", "f32", "f16", "row_rev", False, False, True, "f32", False),
      ("summary", "output", "chain")),
 ]
 
 
-FLAG_BLOCKS, FLAG_ALL, FLAG_NONE = 0x00FF0001, 0x00FFFF01, 0
+FLAG_SUMMARY, FLAG_ALL, FLAG_NONE = 1, 3, 0  # summaries only; summaries and inclusive states; nothing
 
 
 def launches(kind: str, c: Shape):
     """The launch variants a kind stands for."""
-    if kind == "chain":  # ascending chunks, summaries and block prefixes: the look-back reads back to the start
-        return [Launch(flag=FLAG_BLOCKS), Launch(flag=FLAG_NONE)]
+    if kind == "chain":  # ascending chunks, summaries only: the look-back reads back to the start
+        return [Launch(flag=FLAG_SUMMARY), Launch(flag=FLAG_NONE)]
     if kind == "chain_x":  # descending chunks, inclusive states everywhere
         return [Launch(desc=1, flag=FLAG_ALL)]
     if kind == "chain_i":  # no inclusive states published (the inline form)
-        return [Launch(desc=1, publish=0, flag=FLAG_BLOCKS)]
+        return [Launch(desc=1, publish=0, flag=FLAG_SUMMARY)]
     if kind == "chain_split":
-        return [Launch(vparts=2, flag=FLAG_BLOCKS), Launch(vparts=2, desc=1, flag=FLAG_ALL)]
+        return [Launch(vparts=2, flag=FLAG_SUMMARY), Launch(vparts=2, desc=1, flag=FLAG_ALL)]
+    if kind == "lean":
+        return [Launch(flag=FLAG_SUMMARY)]
+    if kind == "lean_n":
+        return [Launch(flag=FLAG_NONE)]
+    if kind == "lean_x":
+        return [Launch(desc=1, flag=FLAG_ALL)]
+    if kind == "lean_i":
+        return [Launch(desc=1, publish=0, flag=FLAG_SUMMARY)]
+    if kind == "lean_xcd":  # eight XCDs, every sequence's chunks on one
+        return [Launch(desc=1, flag=FLAG_SUMMARY, nxcd=8)]
+    if kind == "lean_split":
+        return [Launch(vparts=2, desc=1, flag=FLAG_ALL, nxcd=8)]
     return [Launch()]
 
 
@@ -272,25 +345,56 @@ def asm_text():
     return device_asm()
 
 
+_JOBS = {}  # kernel listings shared with the forked workers
+
+
+def _wave_job(job):
+    name, kern, regions, wg, wave = job
+    prog, labels, desc = _JOBS[name]
+    rep = emu.Report()
+    emu.run_wave(prog, labels, desc, kern, regions, desc["amdhsa_group_segment_fixed_size"], wg, wave, rep)
+    return dict(rep.items), dict(rep.counts)
+
+
+def run_waves(jobs):
+    """Run independent waves (in forked worker processes where there are enough
+    CPUs); the findings per job, in order."""
+    workers = min(len(jobs), max(1, (os.cpu_count() or 1) // int(os.environ.get("PYTEST_XDIST_WORKER_COUNT", "1"))),
+                  8)
+    if workers <= 1:
+        return [_wave_job(j) for j in jobs]
+    import multiprocessing
+    with multiprocessing.get_context("fork").Pool(workers) as pool:
+        return pool.map(_wave_job, jobs, chunksize=1)
+
+
 @pytest.mark.parametrize("case", range(len(CHECKS)))
 def test_gla_kernel_addresses(asm_text, case):
     c, kinds = CHECKS[case]
     names = set(emu.kernel_names(asm_text))
+    jobs, keys = [], []
     for kind in kinds:
-        name = mangled(kind if kind == "chain_split" else kind.split("_")[0], c)
+        name = mangled(kind if kind in ("chain_split", "lean_split") else kind.split("_")[0], c)
         assert name in names, f"no kernel {name} in the listing"
-        prog, labels, desc = emu.parse_kernel(asm_text, name)
-        assert desc["amdhsa_kernarg_size"] == KERNARG_BYTES
-        for ln in launches(kind, c):
+        if name not in _JOBS:
+            _JOBS[name] = emu.parse_kernel(asm_text, name)
+        assert _JOBS[name][2]["amdhsa_kernarg_size"] == KERNARG_BYTES
+        for li, ln in enumerate(launches(kind, c)):
             kern, regions = kernel_args(c, ln)
-            rep = emu.Report()
-            for wg, nw in work_groups(kind.split("_")[0] if kind != "chain_split" else kind, c, ln):
+            for wg, nw in work_groups(kind.split("_")[0], c, ln):
                 for wave in range(nw):
-                    emu.run_wave(prog, labels, desc, kern, regions, desc["amdhsa_group_segment_fixed_size"], wg,
-                                 wave, rep)
-            bad = {k: sorted(v)[:4] for k, v in rep.items.items() if k.startswith(("ERR", "WARN", "NOTIMPL"))}
-            assert not bad, f"{kind}: {bad}"
-            assert "INFO-PATHLIMIT" not in rep.counts, f"{kind}: not every branch outcome was explored"
+                    jobs.append((name, kern, regions, wg, wave))
+                    keys.append((kind, li))
+    found = {}
+    for key, (items, counts) in zip(keys, run_waves(jobs)):
+        f = found.setdefault(key, ({}, set()))
+        for k, v in items.items():
+            if k.startswith(("ERR", "WARN", "NOTIMPL")):
+                f[0].setdefault(k, set()).update(v)
+        f[1].update(counts)
+    for (kind, li), (bad, counts) in found.items():
+        assert not bad, f"{kind} launch {li}: { {k: sorted(v)[:4] for k, v in bad.items()} }"
+        assert "INFO-PATHLIMIT" not in counts, f"{kind} launch {li}: not every branch outcome was explored"
 
 
 # ---------------------------------------------------------------------------

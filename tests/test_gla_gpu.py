@@ -281,18 +281,22 @@ def test_workspace_reuse_and_no_fault(gtr):
     assert torch.equal(results[0], results[3])
 
 
-@pytest.mark.parametrize("name,heads,want,parts", [
-    ("kbench", None, "inline", 1), ("tiny", None, "inline", 1), ("op1600", None, "inline", 1),
-    ("op256", None, "inline", 2), ("kbench", 4, "inline", 2), ("op1600", 2, "inline", 2),
-    ("directions", None, ("inline", "fused"), 1), ("batched", None, "fused", 1), ("highres", None, "fused", 1),
-    ("op16k", None, "fused", 1), ("tiny", 1100, "staged", 1)])
-def test_auto_schedule(gtr, name, heads, want, parts):
+@pytest.mark.parametrize("name,heads,want,parts,chunk", [
+    ("kbench", None, "inline", 1, None), ("tiny", None, "inline", 1, None), ("op1600", None, "inline", 1, None),
+    ("op256", None, "inline", 2, None), ("kbench", 4, "inline", 2, None), ("op1600", 2, "inline", 2, None),
+    ("directions", None, ("inline", "fused"), 1, None), ("batched", None, "fused", 1, None),
+    ("highres", None, "staged", 1, None), ("highres", None, "fused", 1, 128), ("op16k", None, "staged", 1, None),
+    ("tiny", 1100, "staged", 1, None)])
+def test_auto_schedule(gtr, name, heads, want, parts, chunk):
     """AUTO's choice (the length-aware dispatch) as gtr_gla_schedule reports it:
-    INLINE up to 32 chunks while the whole grid is resident (two work-groups per
-    CU: 512), FUSED up to 256 chunks and 1024 sequences, STAGED beyond; the value
-    split where the doubled grid gives every work-group its own CU (4 x 25
-    chunks x 2 = 200 work-groups split, 6 x 25 x 2 = 300 do not)."""
+    INLINE up to 32 chunks while the whole grid is resident, FUSED up to 64
+    chunks and 1024 sequences, STAGED beyond (80x80 at chunk 64: 100 chunks;
+    at chunk 128: 50); the value split where the doubled grid gives every
+    work-group its own CU (4 x 25 chunks x 2 = 200 work-groups split, 6 x 25 x 2
+    = 300 do not)."""
     wl = WORKLOADS[name] if heads is None else WORKLOADS[name].with_(heads=heads)
+    if chunk is not None:
+        wl = wl.with_(chunk=chunk)
     dev = torch.device("cuda")
     mk = lambda d: torch.empty((wl.B, wl.heads, wl.L, d), dtype=torch_dtype(wl.dtype), device=dev)
     s0 = torch.empty((wl.B, wl.heads, wl.dk, wl.dv), device=dev) if wl.s0_std is not None else None
@@ -310,11 +314,13 @@ def test_paths_agree(gtr):
     for scan in wl.scans:
         a, _ = run_gpu(gtr, wl, scan, 64, "fused")
         b, _ = run_gpu(gtr, wl, scan, 64, "staged")
-        # the same arithmetic except the order in which the boundary state is
-        # summed (look-back nearest first against the scan's chunk order), so an
-        # fp16 rounding of S can flip: well below the 2e-3 parity bar that each
-        # schedule meets against the oracle on its own
-        assert rel_err(a, b.double().cpu().numpy()) <= 2e-4
+        # the one-launch kernel for 16-bit inputs forms its fp16 operands in
+        # another order than the staged kernels (key rows rounded before the
+        # chunk-level factor, outputs accumulated transposed) and sums the
+        # boundary state nearest first: two independent rounding sequences,
+        # each within 2e-3 of the oracle on its own (about 5e-4 measured), so
+        # they agree to the sum of their errors, well inside 1e-3
+        assert rel_err(a, b.double().cpu().numpy()) <= 1e-3
 
 
 def test_graph_replays_match_eager(gtr):
