@@ -104,15 +104,21 @@ typedef enum {
 typedef enum {
   GTR_PATH_AUTO = 0,   /* the library picks (gtr_gla_schedule reports the choice):
                           INLINE for sequences of at most 32 chunks whose chunks
-                          are all resident at once, FUSED for sequences of at
-                          most 64 chunks, STAGED beyond (or for more than 1024
-                          sequences).                                               */
+                          are all resident at once; FUSED otherwise, up to 256
+                          chunks for 16-bit inputs at chunk 64 and up to 64
+                          chunks for the rest; STAGED beyond (or for more than
+                          1024 sequences).                                          */
   GTR_PATH_FUSED = 1,  /* one launch, boundary states by look-back: each chunk
                           hands over its summary, finds S_[c] from the summaries
                           of the chunks before it back to the nearest chunk that
                           has handed over its inclusive state S_[j+1], and hands
                           over S_[c+1] in turn (the scan co-runs with the
-                          outputs). At most 1024 sequences of 256 chunks.          */
+                          outputs). For 16-bit inputs at chunk 64 and sequences
+                          of more than 32 chunks the look-back goes by groups of
+                          8 chunks: the last chunk of each group also hands over
+                          the group's aggregate, and a chunk sums the summaries
+                          of its own group and then one aggregate per earlier
+                          group. At most 1024 sequences of 256 chunks.              */
   GTR_PATH_STAGED = 2, /* three launches: summaries, boundary-state scan, outputs;
                           no waits between work-groups                             */
   GTR_PATH_INLINE = 3  /* one launch, each chunk rebuilds its boundary state from

@@ -22,6 +22,14 @@ constexpr unsigned kFlagLocal = 4u;        // the summary and record went to the
 // inclusive state S_[c+1]; a look-back sums at most about that many summaries
 // before it meets one, and the other chunks skip the store.
 constexpr int kPublishEvery = 4;
+// Grouped look-back (16-bit kernel, long sequences): the chunks form groups of
+// kGroup; the last chunk e of a group stores the group's aggregate
+//   A_g = sum_{j in group} (prod_{j<l<=e} Diag(d_l)) U_j,  D_g = prod_{j in group} d_j,
+// so a chunk sums the summaries of its own group and then one aggregate per
+// earlier group instead of every summary. Inclusive states are then stored at
+// group ends only.
+constexpr int kGroup = 8;
+constexpr unsigned kFlagGroup = 8u;        // chunk flag (group ends): the group aggregate and its record are stored
 constexpr float kF16Safe = 65504.f;        // bf16 inputs must stay within the fp16 range
 
 // fault word bits (the workspace's first word; sticky until the workspace is
@@ -64,6 +72,7 @@ struct GlaParams {
   int publish;  // one launch: store inclusive states
   int nxcd;     // one launch, 16-bit kernel: XCDs of the sequence-per-XCD grid (0: plain chunk-major grid)
   unsigned spin;  // polls of a bounded wait
+  int group;      // one launch, 16-bit kernel: grouped look-back (kGroup chunks per group)
 };
 
 constexpr int tile_threads(int chunk) { return chunk / 16 * kWave; }
@@ -304,55 +313,73 @@ __device__ __forceinline__ int lookback_base(const GlaParams& P, const T& ch, in
   return -1;
 }
 
-template <class T>
-__device__ __forceinline__ void lookback_sum(const GlaParams& P, const T& ch, int seq, int c, int base,
-                                             float (&acc)[T::SPER][8]) {
+// Adds n look-back items to acc, nearest first, continuing the decay product
+// `run` (per row i: the product of d_l[i] over the chunks already passed). Item
+// k is the summary of chunk first - k, or (AGG) the aggregate of group
+// first - k, which sits with its record (D_g, scale) in the state slot of the
+// group's second-to-last chunk (a chunk that never stores an inclusive state).
+// The tiles go in batches of B with every load of a batch issued before any is
+// used; inside a batch nothing branches: a tile past the n items (and every
+// tile for a thread without a piece) is read at an offset past the
+// descriptors' ranges, which returns zeros, and the decay product skips it.
+template <class T, bool AGG>
+__device__ __forceinline__ void sum_items(const GlaParams& P, int seq, int first, int n,
+                                          float (&acc)[T::SPER][8], float& run) {
   constexpr int DK = T::kDK, DV = T::kDV, SPER = T::SPER, RS = T::RS;
   constexpr bool F16 = T::F16;
+  static_assert(!AGG || F16, "group aggregates are fp16 tiles");
   // tiles per batch: about 80 registers of loads per batch
   constexpr int B = 80 / (SPER * (F16 ? 4 : 8) + 2) < 1 ? 1 : 80 / (SPER * (F16 ? 4 : 8) + 2);
   const int NC = P.nchunks;
   const uint32_t tile = DK * DV * (F16 ? 2 : 4);
+  const uint32_t slot = DK * DV * 4;  // a state slot (bytes)
   const __amdgpu_buffer_rsrc_t ar =
-      make_rsrc(static_cast<char*>(P.agg) + (size_t)seq * NC * tile, (uint32_t)NC * tile);
-  const __amdgpu_buffer_rsrc_t rr = make_rsrc(P.rec + (size_t)seq * NC * RS, (uint32_t)NC * RS * 4);
-  const __amdgpu_buffer_rsrc_t sr = make_rsrc(P.states + (size_t)seq * NC * (DK * DV), (uint32_t)NC * DK * DV * 4);
+      AGG ? make_rsrc(P.states + (size_t)seq * NC * (DK * DV), (uint32_t)NC * slot)
+          : make_rsrc(static_cast<char*>(P.agg) + (size_t)seq * NC * tile, (uint32_t)NC * tile);
+  const __amdgpu_buffer_rsrc_t rr =
+      AGG ? ar : make_rsrc(P.rec + (size_t)seq * NC * RS, (uint32_t)NC * RS * 4);
   const bool mine = T::piece_ok(0);
   const uint32_t row = (uint32_t)T::piece_i(0);
-  float run = 1.f;
-#pragma unroll
-  for (int m = 0; m < SPER; ++m)
-#pragma unroll
-    for (int e = 0; e < 8; ++e) acc[m][e] = 0.f;
-  // summaries j = c - 1 down to base + 1 in batches of B (every load of a
-  // batch issued before any is used). Inside a batch nothing branches: a tile
-  // at or below `base` (and every tile for a thread without a piece) is read
-  // at an offset past the descriptors' ranges, which returns zeros, and the
-  // decay product skips it.
-  for (int j1 = c - 1; j1 > base; j1 -= B) {
+  for (int k1 = 0; k1 < n; k1 += B) {
     Piece<F16> u[B][SPER];
     f2 r[B];
 #pragma unroll
     for (int b = 0; b < B; ++b) {
-      const int j = j1 - b;
-      const bool in = j > base && mine;
-      r[b] = __builtin_bit_cast(f2, __builtin_amdgcn_raw_buffer_load_b64(
-                                        rr, in ? (uint32_t)(j * RS + 2 * (int)row) * 4 : kOutOfRange, 0, kAgentCoherent));
+      const int j = first - k1 - b;
+      const bool in = k1 + b < n && mine;
+      const uint32_t s = (uint32_t)(j * kGroup + kGroup - 2);  // AGG: the slot of group j
+      const uint32_t roff = AGG ? s * slot + tile + row * 8 : (uint32_t)(j * RS + 2 * (int)row) * 4;
+      r[b] = __builtin_bit_cast(f2, __builtin_amdgcn_raw_buffer_load_b64(rr, in ? roff : kOutOfRange, 0,
+                                                                         kAgentCoherent));
+      const uint32_t e0 = AGG ? s * (slot / 2) : (uint32_t)j * (DK * DV);
 #pragma unroll
       for (int mm = 0; mm < SPER; ++mm)
-        u[b][mm].load(ar, in ? (uint32_t)j * (DK * DV) + T::piece_elem(mm) : kOutOfRange / (F16 ? 2 : 4));
+        u[b][mm].load(ar, in ? e0 + T::piece_elem(mm) : kOutOfRange / (F16 ? 2 : 4));
     }
 #pragma unroll
     for (int b = 0; b < B; ++b) {
-      const bool in = j1 - b > base;
+      const bool in = k1 + b < n;
       const float wt = run * (F16 ? r[b][1] : 1.f);  // 0 for a tile read as zeros
 #pragma unroll
       for (int mm = 0; mm < SPER; ++mm) u[b][mm].fma_into(acc[mm], wt);
       run = in ? run * r[b][0] : run;
     }
   }
+}
+
+// Ends a look-back: adds the inclusive state S_[base+1] that chunk `base`
+// stored (base >= 0), or S_0 (base = -1, if there is one), with the decay
+// product `run` of the chunks in between.
+template <class T>
+__device__ __forceinline__ void add_base(const GlaParams& P, int seq, int base, float run,
+                                         float (&acc)[T::SPER][8]) {
+  constexpr int DK = T::kDK, DV = T::kDV, SPER = T::SPER;
+  const int NC = P.nchunks;
+  const bool mine = T::piece_ok(0);
+  const uint32_t row = (uint32_t)T::piece_i(0);
   if (base >= 0) {
-    // the inclusive state S_[base+1] that chunk `base` stored
+    const __amdgpu_buffer_rsrc_t sr =
+        make_rsrc(P.states + (size_t)seq * NC * (DK * DV), (uint32_t)NC * DK * DV * 4);
     Piece32 st[SPER];
 #pragma unroll
     for (int mm = 0; mm < SPER; ++mm)
@@ -374,6 +401,69 @@ __device__ __forceinline__ void lookback_sum(const GlaParams& P, const T& ch, in
         acc[mm][e + 4] = fmaf(run, hi4[e], acc[mm][e + 4]);
       }
     }
+  }
+}
+
+template <class T>
+__device__ __forceinline__ void lookback_sum(const GlaParams& P, const T& ch, int seq, int c, int base,
+                                             float (&acc)[T::SPER][8]) {
+#pragma unroll
+  for (int m = 0; m < T::SPER; ++m)
+#pragma unroll
+    for (int e = 0; e < 8; ++e) acc[m][e] = 0.f;
+  float run = 1.f;
+  sum_items<T, false>(P, seq, c - 1, c - 1 - base, acc, run);
+  add_base<T>(P, seq, base, run, acc);
+}
+
+// Grouped look-back, own group: polls the summary flags of the chunks lo..c-1
+// (fewer than kGroup, none with an inclusive state) until every one is set.
+// Returns 0, or -2 (the wait ran out) / -3 (a summary sits in another XCD's L2).
+template <class T>
+__device__ __forceinline__ int wait_own_group(const GlaParams& P, const T& ch, int seq, int lo, int c, unsigned xcc) {
+  const unsigned* fl = P.flags + (size_t)seq * kMaxChainChunks;
+  const int n = c - lo;
+  if (n <= 0) return 0;
+  const uint64_t need = (1ull << n) - 1ull;
+  for (unsigned cnt = 0;;) {
+    const unsigned f =
+        ch.lane < n ? __hip_atomic_load(&fl[c - 1 - ch.lane], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) : 0u;
+    const uint64_t rdy = __builtin_amdgcn_ballot_w64((f & kFlagSummary) != 0);
+    if ((rdy & need) == need) {
+      const uint64_t far = __builtin_amdgcn_ballot_w64((f & kFlagLocal) != 0 && ((f >> 8) & 15u) != xcc);
+      return (far & need) ? -3 : 0;
+    }
+    if (++cnt >= P.spin) return -2;
+    __builtin_amdgcn_s_sleep(1);
+  }
+}
+
+// Grouped look-back, earlier groups: lane l watches the end chunk of group
+// gc - 1 - l and the wait lasts until every group after the nearest inclusive
+// state has its aggregate. Returns the chunk whose inclusive state ends the sum
+// (-1: none, S_0) with `naggs` aggregates before it, or -2 (the wait ran out).
+// Aggregates and inclusive states go through memory (agent-coherent stores),
+// so their placement does not matter.
+template <class T>
+__device__ __forceinline__ int wait_groups(const GlaParams& P, const T& ch, int seq, int gc, int& naggs) {
+  const unsigned* fl = P.flags + (size_t)seq * kMaxChainChunks;
+  naggs = 0;
+  if (gc <= 0) return -1;
+  const int n = gc;  // kMaxChainChunks / kGroup <= 64 groups
+  for (unsigned cnt = 0;;) {
+    const unsigned f = ch.lane < n ? __hip_atomic_load(&fl[(gc - 1 - ch.lane) * kGroup + kGroup - 1],
+                                                       __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)
+                                   : 0u;
+    const uint64_t inc = __builtin_amdgcn_ballot_w64((f & kFlagInclusive) != 0);
+    const uint64_t agg = __builtin_amdgcn_ballot_w64((f & kFlagGroup) != 0);
+    const int m = inc ? (int)__builtin_ctzll(inc) : n;
+    const uint64_t need = m >= 64 ? ~0ull : (1ull << m) - 1ull;
+    if ((agg & need) == need) {
+      naggs = m;
+      return m < n ? (gc - 1 - m) * kGroup + kGroup - 1 : -1;
+    }
+    if (++cnt >= P.spin) return -2;
+    __builtin_amdgcn_s_sleep(1);
   }
 }
 

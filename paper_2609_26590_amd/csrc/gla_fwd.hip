@@ -1058,6 +1058,7 @@ struct Plan {
   int vparts;   // value split of the one-launch schedules
   int desc;     // chunks in descending order (every work-group resident at once)
   int nxcd;     // sequence-per-XCD grid of the 16-bit kernel (0: chunk-major grid)
+  int group;    // grouped look-back (16-bit kernel, FUSED)
   int64_t blocks;
 };
 
@@ -1068,21 +1069,29 @@ struct Plan {
 //     most kMaxChainChunks chunks); INLINE (every chunk reads all summaries
 //     before it, no inclusive states) while a sequence has at most
 //     kInlineMaxChunks chunks and the whole grid is resident at once, FUSED
-//     (look-back to the nearest inclusive state) otherwise;
+//     (look-back to the nearest inclusive state) otherwise: up to
+//     kFusedMaxChunks chunks on the float32 kernel (STAGED beyond), up to
+//     kMaxChainChunks on the 16-bit kernel at chunk 64, which looks back by
+//     groups of kGroup chunks once a sequence is longer than kInlineMaxChunks;
 //   * the value split (d_v = 64 in two halves, no output gate: its RMSNorm needs
 //     whole rows) when the doubled grid still gives every work-group a CU of
 //     its own;
 //   * the chunk-major grid, in descending chunk order when every work-group is
-//     resident at once.
+//     resident at once (ascending for the grouped look-back).
 // An explicit path that does not fit is GTR_ERR_UNSUPPORTED; STAGED always fits.
 constexpr int64_t kInlineMaxChunks = 32;
-constexpr int64_t kFusedMaxChunks = 64;  // longer sequences: the staged kernels are faster
+constexpr int64_t kFusedMaxChunks = 64;  // longer sequences: the staged kernels are faster (float32 kernel)
+// FUSED, 16-bit kernel: the grouped look-back for sequences longer than this
+// (shorter ones, which are not all resident, find an inclusive state within
+// kPublishEvery chunks)
+constexpr int64_t kGroupMinChunks = kInlineMaxChunks + 1;
 
 static gtr_status plan_call(const GlaShape& s, int path, bool gate, const KernelSet& ks, Plan* pl) {
   pl->sched = GTR_PATH_STAGED;
   pl->vparts = 1;
   pl->desc = 0;
   pl->nxcd = 0;
+  pl->group = 0;
   pl->blocks = 0;
   if (path == GTR_PATH_STAGED) return GTR_OK;
   const bool fits = s.nchunks <= kMaxChainChunks && s.BH <= kSyncSeqs;
@@ -1113,7 +1122,7 @@ static gtr_status plan_call(const GlaShape& s, int path, bool gate, const Kernel
     if (all_resident && s.nchunks <= kInlineMaxChunks)
       pl->sched = GTR_PATH_INLINE;
     else
-      pl->sched = s.nchunks <= kFusedMaxChunks ? GTR_PATH_FUSED : GTR_PATH_STAGED;
+      pl->sched = s.nchunks <= (ks.lean ? kMaxChainChunks : kFusedMaxChunks) ? GTR_PATH_FUSED : GTR_PATH_STAGED;
   } else {
     pl->sched = path;
   }
@@ -1122,7 +1131,12 @@ static gtr_status plan_call(const GlaShape& s, int path, bool gate, const Kernel
     pl->nxcd = 0;
     return GTR_OK;
   }
-  pl->desc = all_resident ? 1 : 0;
+  const bool lean = (pl->vparts > 1 ? ks.lean_split : ks.lean) != nullptr;
+  pl->group = pl->sched == GTR_PATH_FUSED && lean && s.nchunks >= kGroupMinChunks ? 1 : 0;
+  // descending chunk order when every work-group is resident (the chunks that
+  // wait longest start first), except for the grouped look-back, whose
+  // aggregates come from the low chunks
+  pl->desc = all_resident && !pl->group ? 1 : 0;
   pl->blocks = pl->nxcd > 1 ? (int64_t)pl->nxcd * ((ns + pl->nxcd - 1) / pl->nxcd) * s.nchunks : ns * s.nchunks;
   return GTR_OK;
 }
@@ -1220,6 +1234,7 @@ static gtr_status gla_launch(const gtr_gla_args* a, const GlaShape& s, hipStream
   P.publish = pl.sched == GTR_PATH_FUSED;
   P.nxcd = pl.nxcd;
   P.spin = a->spin_limit ? a->spin_limit : kSpinDefault;
+  P.group = pl.group;
 
   void* kargs[] = {&P};
   hipError_t err;

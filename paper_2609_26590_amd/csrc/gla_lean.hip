@@ -452,6 +452,59 @@ struct Lean {
     }
   }
 
+  // Grouped look-back, at the last chunk c of a group: the group aggregate
+  // A = Diag(d_c) acc + U_c (acc: the summaries of the group's other chunks,
+  // decayed to chunk c) and D = run d_c go to the state slot of chunk c - 1 as
+  // an fp16 tile with a power-of-two scale per row, and the record (D[i],
+  // scale[i]) after it; then the chunk's kFlagGroup. `ok` false (the own
+  // group's wait ran out) stores NaN, which poisons every chunk that uses it.
+  template <class S>
+  __device__ __forceinline__ void publish_aggregate(const GlaParams& P, S& sm, int seq, int c, const void* U,
+                                                    const float (&acc)[SPER][8], float run, bool ok,
+                                                    unsigned* flag) const {
+    const __amdgpu_buffer_rsrc_t ur = make_rsrc(U, DK * DV * 2);
+    const __amdgpu_buffer_rsrc_t sr =
+        make_rsrc(P.states + ((size_t)seq * P.nchunks + c - 1) * (DK * DV), DK * DV * 4);
+    const bool mine = piece_ok(0);
+    const int row = mine ? piece_i(0) : 0;
+    const float dc = sm.dc[row];
+    Piece<true> own[SPER];
+#pragma unroll
+    for (int m = 0; m < SPER; ++m)
+      if (mine) own[m].load(ur, piece_elem(m));
+    float a[SPER][8];
+    float mx = 0.f;
+#pragma unroll
+    for (int m = 0; m < SPER; ++m) {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) a[m][e] = ok ? acc[m][e] * dc : __builtin_nanf("");
+      if (mine) own[m].fma_into(a[m], usc);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) mx = fmaxf(mx, fabsf(a[m][e]));
+    }
+    // the row's largest |A| over its TPR neighbouring lanes
+#pragma unroll
+    for (int o = 1; o < TPR; o <<= 1) mx = fmaxf(mx, __shfl_xor(mx, o, kWave));
+    const int ex = fp16_exponent(mx);
+    const float inv = exp2i(-ex);
+    if (mine) {
+#pragma unroll
+      for (int m = 0; m < SPER; ++m) {
+        h8 h;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) h[e] = (_Float16)(a[m][e] * inv);
+        __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, h), sr, (int)piece_elem(m) * 2, 0,
+                                               kAgentCoherent);
+      }
+      if ((int)threadIdx.x % TPR == 0)
+        __builtin_amdgcn_raw_buffer_store_b64(__builtin_bit_cast(u32x2, f2{run * dc, exp2i(ex)}), sr,
+                                              DK * DV * 2 + row * 8, 0, kAgentCoherent);
+    }
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    __syncthreads();
+    if (threadIdx.x == 0) __hip_atomic_fetch_or(flag, kFlagGroup, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  }
+
   // S_[c] pieces -> the shared state tile (rows i, fp16 of S / tsc, tsc = 2^e
   // from the largest |S_[c]| of the work-group). No barrier.
   template <class S>
@@ -568,8 +621,10 @@ struct Lean {
 // The kernel: same grid, flags, look-back, poison and hand-off protocol as
 // gla_chain_kernel in gla_fwd.hip.
 // ---------------------------------------------------------------------------
+// At most 168 registers: three work-groups per CU.
 template <int DK, int DV, int C, int IN>
-__global__ void __launch_bounds__(tile_threads(C)) gla_lean_kernel(GlaParams P) {
+__global__ void __launch_bounds__(tile_threads(C)) __attribute__((amdgpu_waves_per_eu(3)))
+gla_lean_kernel(GlaParams P) {
   typedef Lean<DK, DV, C, IN> T;
   __shared__ typename T::Smem sm;
   const int NC = P.nchunks;
@@ -633,8 +688,30 @@ __global__ void __launch_bounds__(tile_threads(C)) gla_lean_kernel(GlaParams P) 
                           __HIP_MEMORY_SCOPE_AGENT);
 
   float acc[T::SPER][8];
-  const int base = lookback_base(P, ch, seq, c, xcc);
-  if (base >= -1) lookback_sum(P, ch, seq, c, base, acc);
+  int base;
+  if (P.group) {
+    // grouped: the summaries of the own group, then (at a group's last chunk)
+    // the group's aggregate, then one aggregate per earlier group back to the
+    // nearest inclusive state
+    const int lo = c - c % kGroup;
+    const int st = wait_own_group(P, ch, seq, lo, c, xcc);
+#pragma unroll
+    for (int m = 0; m < T::SPER; ++m)
+#pragma unroll
+      for (int e = 0; e < 8; ++e) acc[m][e] = 0.f;
+    float run = 1.f;
+    if (st == 0) sum_items<T, false>(P, seq, c - 1, c - lo, acc, run);
+    if (c % kGroup == kGroup - 1 && c < NC - 1) ch.publish_aggregate(P, sm, seq, c, U, acc, run, st == 0, flag);
+    int naggs = 0;
+    base = st == 0 ? wait_groups(P, ch, seq, c / kGroup, naggs) : st;
+    if (base >= -1) {
+      sum_items<T, true>(P, seq, c / kGroup - 1, naggs, acc, run);
+      add_base<T>(P, seq, base, run, acc);
+    }
+  } else {
+    base = lookback_base(P, ch, seq, c, xcc);
+    if (base >= -1) lookback_sum(P, ch, seq, c, base, acc);
+  }
   const bool okw = base >= -1;
   // one exchange makes the outcome uniform (a wait that ran out, or a NaN
   // state handed over by a poisoned chunk before it, poisons everything this
@@ -677,7 +754,8 @@ __global__ void __launch_bounds__(tile_threads(C)) gla_lean_kernel(GlaParams P) 
 
   // S_[c+1] = Diag(d_c) S_[c] + U_c for the chunks after this one (FUSED), or
   // S_final after the last chunk; U_c is read back from the acknowledged stores
-  const bool next = c < NC - 1 ? P.publish != 0 && c % kPublishEvery == kPublishEvery - 1 : P.s_final != nullptr;
+  const int every = P.group ? kGroup : kPublishEvery;
+  const bool next = c < NC - 1 ? P.publish != 0 && c % every == every - 1 : P.s_final != nullptr;
   if (next) {
     Piece<true> own[T::SPER];
     const __amdgpu_buffer_rsrc_t ur = make_rsrc(U, DK * DV * 2);

@@ -626,6 +626,17 @@ def set_scc(w, val, opaque=False, d=True):
     w.scc = (1 if val else 0, bool(opaque), d)
 
 
+def _sbfe(a, b, signed):
+    """Scalar bit-field extract: offset b[4:0], width b[22:16] (sign-extended if signed)."""
+    off, wid = b & 31, (b >> 16) & 127
+    if wid == 0:
+        return 0
+    x = (a >> off) & ((1 << min(wid, 32)) - 1)
+    if signed and wid < 32 and (x >> (wid - 1)) & 1:
+        x -= 1 << wid
+    return x & M32
+
+
 def salu32(fn, scc_mode=None):
     def h(w, i):
         a = [w.s32(t, i) for t in i.ops[1:]]
@@ -693,6 +704,8 @@ HANDLERS.update({
     's_not_b32': salu32(lambda a: (~a & M32, (~a & M32) != 0)),
     's_andn2_b32': salu32(lambda a, b: (a & ~b & M32, (a & ~b & M32) != 0)),
     's_orn2_b32': salu32(lambda a, b: ((a | ~b) & M32, ((a | ~b) & M32) != 0)),
+    's_bfe_u32': salu32(lambda a, b: (_sbfe(a, b, False), _sbfe(a, b, False) != 0)),
+    's_bfe_i32': salu32(lambda a, b: (_sbfe(a, b, True), _sbfe(a, b, True) != 0)),
     's_lshl_b64': salu64_shift(lambda a, b: ((a << (b & 63)) & M64, ((a << (b & 63)) & M64) != 0)),
     's_lshr_b64': salu64_shift(lambda a, b: (a >> (b & 63), (a >> (b & 63)) != 0)),
 })
@@ -1173,6 +1186,12 @@ def _cvtfu(w, i):
 def _cvtfi(w, i):
     a = w.v32(i.ops[1], i)
     w.vwrite(i.ops[0], vres(fo(a.v.view(np.int32).astype(np.float32)), a))
+
+
+@handler('v_cvt_f32_ubyte0_e32', 'v_cvt_f32_ubyte0_e64')
+def _cvtub0(w, i):
+    a = w.v32(i.ops[1], i)
+    w.vwrite(i.ops[0], vres(fo((a.v & np.uint32(0xff)).astype(np.float32)), a))
 
 
 @handler('v_cvt_u32_f32_e32', 'v_cvt_u32_f32_e64')

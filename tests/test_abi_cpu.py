@@ -99,7 +99,8 @@ def test_workspace_size_formula(lib):
 def test_schedule_query_without_device(lib):
     """gtr_gla_schedule: -1 for invalid arguments. AUTO is length-aware: INLINE
     up to 32 chunks per sequence when the whole grid is resident at once, FUSED
-    up to 64 chunks, STAGED beyond; an explicit one-launch path that does not
+    up to 64 chunks (256 for 16-bit inputs at chunk 64), STAGED beyond; an
+    explicit one-launch path that does not
     fit (more than 256 chunks) reports -1. Without a usable device residency is
     unknown (so AUTO takes FUSED) and the value split is off."""
     assert lib.gtr_gla_schedule(None) == -1
@@ -110,11 +111,14 @@ def test_schedule_query_without_device(lib):
     a.path = 0
     a.H, a.W = 40, 80  # 50 chunks
     assert lib.gtr_gla_schedule(ctypes.byref(a)) == 1
-    a.H = a.W = 80  # 100 chunks
+    a.H = a.W = 80  # 100 chunks: FUSED (grouped look-back) for 16-bit inputs at chunk 64
+    assert lib.gtr_gla_schedule(ctypes.byref(a)) == 1
+    a.qkv_dtype = a.g_dtype = a.o_dtype = gtr.F32  # STAGED for float32
     assert lib.gtr_gla_schedule(ctypes.byref(a)) == 2
     a.path = 1  # an explicit one-launch path still fits
     assert lib.gtr_gla_schedule(ctypes.byref(a)) == 1
     a.path = 0
+    a.qkv_dtype = a.g_dtype = a.o_dtype = gtr.F16
     a.H = a.W = 200  # 625 chunks
     assert lib.gtr_gla_schedule(ctypes.byref(a)) == 2
     a.path = 1

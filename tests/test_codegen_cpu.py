@@ -185,10 +185,13 @@ class Launch:
     chunk flag reads as (FLAG_SUMMARY: summaries only, the look-back walks back
     to the start; FLAG_ALL: inclusive states everywhere as well, it stops at the
     nearest; FLAG_NONE: nothing is ever ready, every wait runs out after the
-    spin limit) and the XCDs of the sequence-per-XCD grid (0: chunk-major)."""
+    spin limit), the XCDs of the sequence-per-XCD grid (0: chunk-major) and the
+    grouped look-back of the 16-bit kernel (FLAG_GROUP: every group aggregate
+    is stored)."""
 
-    def __init__(self, vparts=1, desc=0, publish=1, flag=1, nxcd=0):
+    def __init__(self, vparts=1, desc=0, publish=1, flag=1, nxcd=0, group=0):
         self.vparts, self.desc, self.publish, self.flag, self.nxcd = vparts, desc, publish, flag, nxcd
+        self.group = group
 
 
 def kernel_args(c: Shape, ln: Launch = Launch()):
@@ -228,11 +231,11 @@ def kernel_args(c: Shape, ln: Launch = Launch()):
     regions.insert(0, emu.Region("sync", ws + sync, ns * 16, "rw"))
     regions.insert(0, emu.Region("fault", ws, 256, "rw"))
     regions.append(emu.Region("kernarg", emu.KERNARG_BASE, KERNARG_BYTES, "r"))
-    kern = struct.pack("<7Q6iqifi4x6Qif2Qif6iI4x", q, k, v, g, o, s0, sf, DT[c.dt][0], DT[c.gdt][0],
+    kern = struct.pack("<7Q6iqifi4x6Qif2Qif6iIi", q, k, v, g, o, s0, sf, DT[c.dt][0], DT[c.gdt][0],
                        DT[c.odt][0], c.BH, c.H, c.W, c.L, c.NC, c.dk ** -0.5, SCAN[c.scan],
                        ws + agg, ws + rec, ws + states, ws + sync, ws + flags, ws,
                        1 if c.logits else 0, 1.0 / 16, z, nw, DT[c.zdt][0] if c.zdt else 0, 1e-5,
-                       c.dv, ln.vparts, ns, ln.desc, ln.publish, ln.nxcd, 8)
+                       c.dv, ln.vparts, ns, ln.desc, ln.publish, ln.nxcd, 8, ln.group)
     assert len(kern) == KERNARG_BYTES
     return kern, regions
 
@@ -255,10 +258,11 @@ def mangled(kind: str, c: Shape) -> str:
 
 
 def work_groups(kind: str, c: Shape, ln: Launch):
-    """First, second and last chunk of the first and last sequence (+ one block
-    of the XCD-ordered grid that has no sequence)."""
+    """First, second and last chunk of the first and last sequence (+ the last
+    chunk of the first group for the grouped look-back, + one block of the
+    XCD-ordered grid that has no sequence)."""
     nw = c.chunk // 16
-    cs = sorted({0, 1 % c.NC, c.NC - 1})
+    cs = sorted({0, 1 % c.NC, c.NC - 1} | ({7} if ln.group and c.NC > 8 else set()))  # 7: a group's last chunk
     bhs = sorted({0, c.BH - 1})
     if kind in ("summary", "output"):
         return [((cc, bh, 0), nw) for cc in cs for bh in bhs]
@@ -288,11 +292,11 @@ def work_groups(kind: str, c: Shape, ln: Launch):
 # and (16-bit kernel) the sequence-per-XCD grid
 CHAIN = ("chain", "chain_x", "chain_i")
 # the 16-bit kernel at chunk 64: every launch variant on one shape, one variant on the others
-LEAN = ("lean", "lean_n", "lean_x", "lean_i", "lean_xcd", "lean_split")
+LEAN = ("lean", "lean_n", "lean_x", "lean_i", "lean_xcd", "lean_split", "lean_g", "lean_gs")
 CHECKS = [
     (Shape(1, 12, 40, 40, 64, 64, 64, "bf16", "bf16", "f32", "row", False, False),
      ("summary", "scan", "output") + CHAIN + ("chain_split",) + LEAN),
-    (Shape(8, 12, 40, 40, 64, 64, 64, "bf16", "bf16", "f32", "col_rev", True, True), ("output",) + CHAIN + ("lean_x",)),
+    (Shape(8, 12, 40, 40, 64, 64, 64, "bf16", "bf16", "f32", "col_rev", True, True), ("output",) + CHAIN + ("lean_x", "lean_g")),
     (Shape(2, 9, 12, 20, 32, 32, 32, "bf16", "f32", "f32", "col", True, True), ("summary", "output") + CHAIN),
     (Shape(1, 2, 20, 20, 32, 64, 128, "bf16", "bf16", "bf16", "row_rev", False, False), ("output",) + CHAIN),
     (Shape(1, 6, 40, 40, 64, 64, 64, "f16", "f16", "f16", "row", False, False),
@@ -302,7 +306,7 @@ CHECKS = [
     (Shape(1, 3, 7, 9, 64, 64, 128, "f16", "f32", "f32", "col", True, True), ("output",) + CHAIN + ("chain_split",)),
     (Shape(1, 2, 13, 11, 64, 64, 32, "f32", "f32", "f32", "row_rev", True, True), CHAIN + ("chain_split",)),
     (Shape(1, 2, 13, 11, 32, 32, 32, "f32", "f32", "f32", "row", False, True), ("summary", "output") + CHAIN),
-    (Shape(1, 6, 80, 80, 64, 64, 64, "f16", "f16", "f16", "row", False, False), ("scan",) + CHAIN + ("lean",)),
+    (Shape(1, 6, 80, 80, 64, 64, 64, "f16", "f16", "f16", "row", False, False), ("scan",) + CHAIN + ("lean", "lean_g")),
     # gate fusion and the output-gate epilogue
     (Shape(1, 12, 40, 40, 64, 64, 64, "bf16", "bf16", "f32", "col", True, True, True, "bf16", True),
      ("summary", "output") + CHAIN + ("lean_i",)),
@@ -312,7 +316,8 @@ CHECKS = [
 ]
 
 
-FLAG_SUMMARY, FLAG_ALL, FLAG_NONE = 1, 3, 0  # summaries only; summaries and inclusive states; nothing
+# summaries only; summaries and inclusive states; nothing; summaries and group aggregates
+FLAG_SUMMARY, FLAG_ALL, FLAG_NONE, FLAG_GROUP = 1, 3, 0, 9
 
 
 def launches(kind: str, c: Shape):
@@ -337,7 +342,19 @@ def launches(kind: str, c: Shape):
         return [Launch(desc=1, flag=FLAG_SUMMARY, nxcd=8)]
     if kind == "lean_split":
         return [Launch(vparts=2, desc=1, flag=FLAG_ALL, nxcd=8)]
+    if kind == "lean_g":  # grouped look-back: aggregates back to the start; inclusive states; nothing ready
+        return [Launch(group=1, flag=FLAG_GROUP), Launch(group=1, desc=1, flag=FLAG_ALL | FLAG_GROUP),
+                Launch(group=1, flag=FLAG_NONE)]
+    if kind == "lean_gs":  # grouped look-back with the value split
+        return [Launch(vparts=2, group=1, flag=FLAG_GROUP)]
     return [Launch()]
+
+
+def split_name(kind):
+    """The kernel a kind runs: the value-split instantiation for the split kinds."""
+    if kind in ("chain_split", "lean_split", "lean_gs"):
+        return "lean_split" if kind.startswith("lean") else kind
+    return kind.split("_")[0]
 
 
 @pytest.fixture(scope="module")
@@ -374,7 +391,7 @@ def test_gla_kernel_addresses(asm_text, case):
     names = set(emu.kernel_names(asm_text))
     jobs, keys = [], []
     for kind in kinds:
-        name = mangled(kind if kind in ("chain_split", "lean_split") else kind.split("_")[0], c)
+        name = mangled(split_name(kind), c)
         assert name in names, f"no kernel {name} in the listing"
         if name not in _JOBS:
             _JOBS[name] = emu.parse_kernel(asm_text, name)

@@ -155,6 +155,39 @@ def test_value_split_parity(gtr, case):
             assert rel_err(sf, sf_ref) <= tol_for(dtype, "f32"), (path, rel_err(sf, sf_ref))
 
 
+# FUSED with the grouped look-back (16-bit inputs at chunk 64, sequences longer
+# than 32 chunks, groups of 8 chunks): ragged last groups and chunks, S0 and
+# S_final, the value split, 256 chunks (32 groups), every dims pair
+GROUPED = [
+    (1, 2, 48, 48, 64, 64, 64, "bf16", "bf16", "f32", "col", True, True),       # 36 chunks, value split
+    (1, 3, 50, 41, 32, 64, 64, "f16", "f32", "f16", "row_rev", False, True),    # 33 chunks, 2-token tail
+    (2, 5, 40, 80, 64, 64, 64, "f16", "f16", "f16", "row", True, False),        # 50 chunks, 10 sequences
+    (1, 1, 128, 128, 32, 32, 64, "bf16", "bf16", "bf16", "col_rev", True, True),  # 256 chunks
+]
+
+
+@pytest.mark.parametrize("case", range(len(GROUPED)))
+def test_grouped_lookback_parity(gtr, case):
+    B, heads, H, W, dk, dv, chunk, dtype, gdtype, odtype, scan, s0, final = GROUPED[case]
+    wl = edge_workload(B, heads, H, W, dk, dv, chunk, dtype, gdtype, odtype, scan, s0, final, 4000 + case)
+    inp = make_inputs(wl)
+    if gdtype != dtype:
+        inp["g"] = inp["g"].float()
+    dev = torch.device("cuda")
+    q, k, v, g = (inp[n].to(dev) for n in ("q", "k", "v", "g"))
+    s0t = None if inp["s0"] is None else inp["s0"].to(dev)
+    kw = dict(H=H, W=W, chunk=chunk, scan=scan, s0=s0t, want_final=final, o_dtype=torch_dtype(odtype))
+    assert gtr.gtr_gla_schedule(q, k, v, g, **kw) == "fused"
+    o_ref, sf_ref = oracle.gla(inp["q"], inp["k"], inp["v"], inp["g"], inp["s0"], scale=wl.scale, H=H, W=W,
+                               scan=scan)
+    tol = tol_for(dtype, odtype)
+    for path in ("auto", "fused"):
+        o, sf = run_gpu(gtr, wl, scan, chunk, path, inp)
+        assert rel_err(o, o_ref) <= tol, (path, rel_err(o, o_ref))
+        if final:
+            assert rel_err(sf, sf_ref) <= tol_for(dtype, "f32"), (path, rel_err(sf, sf_ref))
+
+
 @pytest.mark.parametrize("path", PATHS)
 @pytest.mark.parametrize("case", range(len(EDGE)))
 def test_edge_parity(gtr, case, path):
@@ -285,13 +318,15 @@ def test_workspace_reuse_and_no_fault(gtr):
     ("kbench", None, "inline", 1, None), ("tiny", None, "inline", 1, None), ("op1600", None, "inline", 1, None),
     ("op256", None, "inline", 2, None), ("kbench", 4, "inline", 2, None), ("op1600", 2, "inline", 2, None),
     ("directions", None, ("inline", "fused"), 1, None), ("batched", None, "fused", 1, None),
-    ("highres", None, "staged", 1, None), ("highres", None, "fused", 1, 128), ("op16k", None, "staged", 1, None),
+    ("highres", None, "fused", 1, None), ("highres", None, "fused", 1, 128), ("highres", None, "staged", 1, 32),
+    ("op16k", None, "fused", 1, None),
     ("tiny", 1100, "staged", 1, None)])
 def test_auto_schedule(gtr, name, heads, want, parts, chunk):
     """AUTO's choice (the length-aware dispatch) as gtr_gla_schedule reports it:
-    INLINE up to 32 chunks while the whole grid is resident, FUSED up to 64
-    chunks and 1024 sequences, STAGED beyond (80x80 at chunk 64: 100 chunks;
-    at chunk 128: 50); the value split where the doubled grid gives every
+    INLINE up to 32 chunks while the whole grid is resident, FUSED up to 1024
+    sequences of 64 chunks (of 256 for 16-bit inputs at chunk 64: 80x80 gives
+    100 chunks, the 16K-token operator shape 256), STAGED beyond (80x80 at
+    chunk 32: 200 chunks); the value split where the doubled grid gives every
     work-group its own CU (4 x 25 chunks x 2 = 200 work-groups split, 6 x 25 x 2
     = 300 do not)."""
     wl = WORKLOADS[name] if heads is None else WORKLOADS[name].with_(heads=heads)
