@@ -659,8 +659,6 @@ gla_lean_kernel(GlaParams P) {
 
   T ch;
   ch.load(P, sm, bh, c);
-  Raw rz[T::VB];
-  if (P.gate) ch.prefetch_gate(P, bh, c, rz);
   ch.factors(sm);
   // the chunk record (d_c, the summary's scale) for the chunks after this one
   if (ch.w == 0 && ch.lane < DK) {
@@ -712,6 +710,10 @@ gla_lean_kernel(GlaParams P) {
     base = lookback_base(P, ch, seq, c, xcc);
     if (base >= -1) lookback_sum(P, ch, seq, c, base, acc);
   }
+  // the output gate's loads overlap the exchange, the state tile and the
+  // readout (issued earlier they would hold registers through every phase)
+  Raw rz[T::VB];
+  if (P.gate) ch.prefetch_gate(P, bh, c, rz);
   const bool okw = base >= -1;
   // one exchange makes the outcome uniform (a wait that ran out, or a NaN
   // state handed over by a poisoned chunk before it, poisons everything this
