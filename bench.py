@@ -251,6 +251,34 @@ def swiglu_detail():
     return res
 
 
+def block_detail():
+    """One GTR block (Sec. 3.1: projections, GLA with the fused gate and output
+    gate, W_o, Spatial SwiGLU, residuals) with random weights on the 40x40 grid,
+    fp16, row scan: GTR-S and GTR-L widths. FLOPs: the products (2 M N K each)
+    plus the GLA's chunkwise arithmetic."""
+    from paper_2609_26590_amd import block
+    from paper_2609_26590_amd.workloads import BLOCK_SIZES, make_block
+    res = {}
+    dev = torch.device("cuda")
+    for name in ("gtr_s", "gtr_l"):
+        d, heads = BLOCK_SIZES[name]
+        x, p = make_block(name, 40, 40)
+        x = x.to(dev)
+        pd = block.prepare({k: v.to(dev) for k, v in p.items()})
+
+        def step(i=0):
+            block.forward(x, pd, H=40, W=40, heads=heads, scan="row")
+
+        step()
+        torch.cuda.synchronize()
+        t, _ = time_graph(step, 100, 10)
+        M, h, dh = 1600, 4 * d, d // heads
+        flops = 2.0 * M * (4 * d * d + 64 * d + 64 * d + d * d + 3 * h * d) + heads * M * (2 * dh * 65 + 4 * dh * dh)
+        res[f"block {name.upper().replace('_', '-')} d{d} 40x40"] = {
+            "us_per_call": t * 1e6, "tflops": flops / t / 1e12, "tokens_per_s": M / t}
+    return res
+
+
 def cpu_model() -> str:
     try:
         for line in open("/proc/cpuinfo"):
@@ -391,6 +419,7 @@ def detail(path, steps, warmup):
         det[f"{name}+fusions"] = {"us_per_call": t * 1e6, "tokens_per_s": wl.B * wl.L / t,
                                   "hbm_frac": b2 / t / 1e9 / HBM_PEAK_GBS}
     det.update(swiglu_detail())
+    det.update(block_detail())
     return det
 
 

@@ -305,6 +305,69 @@ size_t gtr_spatial_swiglu_workspace_size(const gtr_swiglu_args* args);
 gtr_status gtr_spatial_swiglu(const gtr_swiglu_args* args, hipStream_t stream);
 
 /*
+ * The remaining entry points serve one GTR block (Sec. 3.1: projections, the
+ * key-only gated recurrence with its output gate, head concat and W_o, then
+ * Spatial SwiGLU), composed from them and the calls above.
+ *
+ * gtr_gemm: C = A B^T (+ bias) (+ res), the block's projections.
+ * a       : [M, K] row-major, a_dtype (GTR_F16 or GTR_BF16)
+ * b       : [N, K] row-major (linear-layer weight layout, output features
+ *           first), b_dtype = a_dtype
+ * c       : [M, N] row-major, c_dtype (GTR_F32, GTR_F16 or GTR_BF16); must not
+ *           overlap a, b or bias
+ * bias    : [N] float32 added to every row, or NULL
+ * res     : [M, N] in c_dtype added elementwise (a residual), or NULL; may be c
+ *           itself (in place), must not overlap it otherwise
+ * N and K multiples of 64, every pointer 16-byte aligned. The products
+ * accumulate in float32 (MFMA on the input dtype) and are rounded once into c.
+ * Errors as for gtr_gla_fwd; every check runs before the launch.
+ */
+typedef struct {
+  const void* a;
+  const void* b;
+  void* c;
+  const float* bias;
+  const void* res;
+  gtr_dtype a_dtype, b_dtype, c_dtype;
+  int64_t M;
+  int32_t N, K;
+} gtr_gemm_args;
+
+gtr_status gtr_gemm(const gtr_gemm_args* args, hipStream_t stream);
+
+/*
+ * gtr_layernorm: y[m] = (x[m] - mean) / sqrt(var + eps) * w + b over the d
+ * channels of every row m (mean and biased variance of the row, in float32).
+ * x, y : [M, d] dtype (GTR_F16 or GTR_BF16); y may be x (in place).
+ * w, b : [d] float32; NULL stands for ones / zeros.
+ * d a multiple of 8 and at most 2048; x, y 16-byte aligned.
+ */
+gtr_status gtr_layernorm(const void* x, const float* w, const float* b, void* y, int64_t M, int32_t d, float eps,
+                         gtr_dtype dtype, hipStream_t stream);
+
+/*
+ * gtr_heads_split: the columns of a token-major product into head-major
+ * tensors, as the GLA call takes them.
+ *   src : [B*L, ld] dtype; part p, head h is columns p*H*dh + h*dh .. + dh - 1
+ *   dst : [parts][B][H][L][dh] dtype, contiguous
+ * gtr_heads_merge: the reverse for one part: src [B][H][L][dh] ->
+ *   dst [B*L][H*dh].
+ * dtype GTR_F16 or GTR_BF16; dh a multiple of 8; ld >= parts*H*dh and a
+ * multiple of 8; src and dst 16-byte aligned and not overlapping.
+ */
+gtr_status gtr_heads_split(const void* src, void* dst, int32_t parts, int32_t B, int32_t H, int64_t L, int32_t dh,
+                           int64_t ld, gtr_dtype dtype, hipStream_t stream);
+gtr_status gtr_heads_merge(const void* src, void* dst, int32_t B, int32_t H, int64_t L, int32_t dh, gtr_dtype dtype,
+                           hipStream_t stream);
+
+/*
+ * gtr_add: y = a + b elementwise over n elements (a residual), rounded once
+ * into dtype (GTR_F16 or GTR_BF16). n a multiple of 8; pointers 16-byte
+ * aligned; y may be a or b.
+ */
+gtr_status gtr_add(const void* a, const void* b, void* y, int64_t n, gtr_dtype dtype, hipStream_t stream);
+
+/*
  * gtr_gla_fwd_noalloc - gtr_gla_fwd for callers that cannot allocate device
  * memory (code under HIP graph capture, serving loops, harnesses that forbid
  * hipMalloc). Same arguments, results and schedules as gtr_gla_fwd, except

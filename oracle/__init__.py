@@ -209,3 +209,51 @@ def spatial_swiglu(x, w_gate, w_value, w_out, conv_w, conv_b=None, *, H: int, W:
     v = x @ _f64(w_value).T
     hidden = (g / (1.0 + np.exp(-g))) * dwconv3x3(v, conv_w, conv_b, H=H, W=W)
     return hidden @ _f64(w_out).T
+
+
+def layer_norm(x, weight=None, bias=None, eps: float = 1e-6) -> np.ndarray:
+    """Layer normalisation over the last axis: (x - mean) / sqrt(var + eps) * w + b,
+    mean and variance (biased, divided by d) of each row. The block's
+    normalisation before the token mixer and before the Spatial SwiGLU (the
+    paper names neither; see the block's reading of Sec. 3.1)."""
+    x = _f64(x)
+    d = x.shape[-1]
+    w = np.ones(d) if weight is None else _f64(weight)
+    b = np.zeros(d) if bias is None else _f64(bias)
+    mean = np.mean(x, axis=-1, keepdims=True)
+    var = np.mean((x - mean) ** 2, axis=-1, keepdims=True)
+    return (x - mean) / np.sqrt(var + float(eps)) * w + b
+
+
+def gtr_block(x, p: dict, *, H: int, W: int, heads: int, scan: str, tau: float = 16.0, ln_eps: float = 1e-6,
+              norm_eps: float = 1e-5) -> np.ndarray:
+    """One GTR block (Sec. 3.1), float64, composed from the functions above:
+        n1 = LN1(x);  q, k, v, z = n1 W_q^T, n1 W_k^T, n1 W_v^T, n1 W_r^T
+        a  = (n1 W_a1^T) W_a2^T + b_a                 (gate logits, low rank)
+        o  = GLA(q, k, v, log gamma = logsigmoid(a) / tau) per head, in ``scan``
+             order, scale d_k^-1/2
+        u  = SiLU(z) * RMSNorm(o) per head (weight norm_w)
+        x1 = x + concat_heads(u) W_o^T
+        x2 = x1 + SpatialSwiGLU(LN2(x1))
+    x [B, H*W, d] in spatial order; ``p`` holds the weights in linear-layer
+    layout (output features first): w_qkvr [4d, d] (rows q, k, v, r), w_a1 [r, d],
+    w_a2 [d, r], b_a [d], norm_w [d / heads], w_o [d, d], ln1_w, ln1_b, ln2_w, ln2_b
+    [d], and the Spatial SwiGLU's w_g, w_v [h, d], w_out [d, h], conv_w [h, 3, 3],
+    conv_b [h]."""
+    x = _f64(x)
+    B, L, d = x.shape
+    dh = d // heads
+    n1 = layer_norm(x, p["ln1_w"], p["ln1_b"], ln_eps)
+    proj = n1 @ _f64(p["w_qkvr"]).T  # [B, L, 4d]
+
+    def split(t):  # [B, L, heads * dh] -> [B, heads, L, dh]
+        return t.reshape(B, L, heads, dh).transpose(0, 2, 1, 3)
+
+    q, k, v, z = (split(proj[..., i * d:(i + 1) * d]) for i in range(4))
+    a = (n1 @ _f64(p["w_a1"]).T) @ _f64(p["w_a2"]).T + _f64(p["b_a"])
+    g = log_decay_from_logits(split(a), tau)
+    o, _ = gla(q, k, v, g, None, scale=dh ** -0.5, H=H, W=W, scan=scan, want_final=False)
+    u = output_gate(o, z, p["norm_w"], norm_eps)  # [B, heads, L, dh]
+    x1 = x + u.transpose(0, 2, 1, 3).reshape(B, L, d) @ _f64(p["w_o"]).T
+    n2 = layer_norm(x1, p["ln2_w"], p["ln2_b"], ln_eps)
+    return x1 + spatial_swiglu(n2, p["w_g"], p["w_v"], p["w_out"], p["conv_w"], p["conv_b"], H=H, W=W)

@@ -40,7 +40,7 @@ _DT_BACK = {F32: torch.float32, F16: torch.float16, BF16: torch.bfloat16}
 
 EXPORTS = ("gtr_scan_permute", "gtr_gla_workspace_size", "gtr_gla_workspace_init", "gtr_gla_fwd", "gtr_gla_fwd_noalloc",
            "gtr_gla_schedule", "gtr_gla_value_parts", "gtr_gla_workspace_fault", "gtr_status_string", "gtr_spatial_swiglu_workspace_size",
-           "gtr_spatial_swiglu")
+           "gtr_spatial_swiglu", "gtr_gemm", "gtr_layernorm", "gtr_heads_split", "gtr_heads_merge", "gtr_add")
 
 
 class GtrError(RuntimeError):
@@ -75,6 +75,15 @@ class SwigluArgs(ctypes.Structure):
         ("y", ctypes.c_void_p), ("dtype", ctypes.c_int), ("y_dtype", ctypes.c_int),
         ("B", ctypes.c_int32), ("H", ctypes.c_int32), ("W", ctypes.c_int32), ("d", ctypes.c_int32),
         ("hidden", ctypes.c_int32), ("workspace", ctypes.c_void_p), ("workspace_bytes", ctypes.c_size_t),
+    ]
+
+
+class GemmArgs(ctypes.Structure):
+    """Mirror of ``gtr_gemm_args`` (include/gtr.h)."""
+    _fields_ = [
+        ("a", ctypes.c_void_p), ("b", ctypes.c_void_p), ("c", ctypes.c_void_p), ("bias", ctypes.c_void_p),
+        ("res", ctypes.c_void_p), ("a_dtype", ctypes.c_int), ("b_dtype", ctypes.c_int), ("c_dtype", ctypes.c_int),
+        ("M", ctypes.c_int64), ("N", ctypes.c_int32), ("K", ctypes.c_int32),
     ]
 
 
@@ -114,6 +123,16 @@ def load(path: Optional[str] = None) -> ctypes.CDLL:
     lib.gtr_spatial_swiglu_workspace_size.restype = ctypes.c_size_t
     lib.gtr_spatial_swiglu.argtypes = [ctypes.POINTER(SwigluArgs), P]
     lib.gtr_spatial_swiglu.restype = ctypes.c_int
+    lib.gtr_gemm.argtypes = [ctypes.POINTER(GemmArgs), P]
+    lib.gtr_gemm.restype = ctypes.c_int
+    lib.gtr_layernorm.argtypes = [P, P, P, P, I64, I32, ctypes.c_float, ctypes.c_int, P]
+    lib.gtr_layernorm.restype = ctypes.c_int
+    lib.gtr_heads_split.argtypes = [P, P, I32, I32, I32, I64, I32, I64, ctypes.c_int, P]
+    lib.gtr_heads_split.restype = ctypes.c_int
+    lib.gtr_heads_merge.argtypes = [P, P, I32, I32, I64, I32, ctypes.c_int, P]
+    lib.gtr_heads_merge.restype = ctypes.c_int
+    lib.gtr_add.argtypes = [P, P, P, I64, ctypes.c_int, P]
+    lib.gtr_add.restype = ctypes.c_int
     _lib = lib
     return lib
 
@@ -375,4 +394,91 @@ def gtr_spatial_swiglu(x: torch.Tensor, w_gate: torch.Tensor, w_value: torch.Ten
     st = lib.gtr_spatial_swiglu(ctypes.byref(a), _stream_ptr(stream))
     if st:
         raise GtrError("gtr_spatial_swiglu", st)
+    return y
+
+
+# ---------------------------------------------------------------------------
+# the small calls of one GTR block (gtr_gemm, gtr_layernorm, gtr_heads_split /
+# gtr_heads_merge, gtr_add): argument marshalling only
+# ---------------------------------------------------------------------------
+def _dev_contig(name: str, t: torch.Tensor) -> None:
+    if not t.is_cuda or not t.is_contiguous():
+        raise ValueError(f"{name} must be a contiguous device tensor")
+
+
+def gtr_gemm(a: torch.Tensor, b: torch.Tensor, *, bias: Optional[torch.Tensor] = None,
+             res: Optional[torch.Tensor] = None, out_dtype: Optional[torch.dtype] = None,
+             out: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
+    """c = a b^T (+ bias) (+ res): a [M, K], b [N, K] (fp16 or bf16, same dtype),
+    bias [N] float32, res [M, N] in the output dtype (may be ``out``)."""
+    for name, t in (("a", a), ("b", b)) + ((("bias", bias),) if bias is not None else ()) + \
+            ((("res", res),) if res is not None else ()):
+        _dev_contig(name, t)
+    M, K = a.shape
+    N = b.shape[0]
+    if b.shape[1] != K:
+        raise ValueError(f"b has {b.shape[1]} columns, a has {K}")
+    c = out if out is not None else torch.empty((M, N), dtype=out_dtype or a.dtype, device=a.device)
+    _check("out", c, (M, N), (torch.float32, torch.float16, torch.bfloat16), a.device)
+    _check("bias", bias, (N,), (torch.float32,), a.device)
+    _check("res", res, (M, N), (c.dtype,), a.device)
+    g = GemmArgs()
+    g.a, g.b, g.c, g.bias, g.res = _ptr(a), _ptr(b), _ptr(c), _ptr(bias), _ptr(res)
+    g.a_dtype, g.b_dtype, g.c_dtype = _DT[a.dtype], _DT[b.dtype], _DT[c.dtype]
+    g.M, g.N, g.K = M, N, K
+    st = load().gtr_gemm(ctypes.byref(g), _stream_ptr(stream))
+    if st:
+        raise GtrError("gtr_gemm", st)
+    return c
+
+
+def gtr_layernorm(x: torch.Tensor, weight: Optional[torch.Tensor] = None, bias: Optional[torch.Tensor] = None, *,
+                  eps: float = 1e-6, out: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
+    """Layer normalisation over the last dimension of x (fp16 or bf16)."""
+    _dev_contig("x", x)
+    d = x.shape[-1]
+    y = out if out is not None else torch.empty_like(x)
+    _check("out", y, tuple(x.shape), (x.dtype,), x.device)
+    _check("weight", weight, (d,), (torch.float32,), x.device)
+    _check("bias", bias, (d,), (torch.float32,), x.device)
+    st = load().gtr_layernorm(_ptr(x), _ptr(weight), _ptr(bias), _ptr(y), x.numel() // d, d, float(eps), _DT[x.dtype],
+                              _stream_ptr(stream))
+    if st:
+        raise GtrError("gtr_layernorm", st)
+    return y
+
+
+def gtr_heads_split(x: torch.Tensor, *, parts: int, B: int, heads: int, dh: int, stream=None) -> torch.Tensor:
+    """x [B*L, ld] (token-major product; part p, head h at columns
+    (p*heads + h)*dh ...) -> [parts, B, heads, L, dh]."""
+    _dev_contig("x", x)
+    M, ld = x.shape
+    L = M // B
+    y = torch.empty((parts, B, heads, L, dh), dtype=x.dtype, device=x.device)
+    st = load().gtr_heads_split(_ptr(x), _ptr(y), parts, B, heads, L, dh, ld, _DT[x.dtype], _stream_ptr(stream))
+    if st:
+        raise GtrError("gtr_heads_split", st)
+    return y
+
+
+def gtr_heads_merge(u: torch.Tensor, stream=None) -> torch.Tensor:
+    """u [B, heads, L, dh] -> [B*L, heads*dh] (the head concat)."""
+    _dev_contig("u", u)
+    B, H, L, dh = u.shape
+    y = torch.empty((B * L, H * dh), dtype=u.dtype, device=u.device)
+    st = load().gtr_heads_merge(_ptr(u), _ptr(y), B, H, L, dh, _DT[u.dtype], _stream_ptr(stream))
+    if st:
+        raise GtrError("gtr_heads_merge", st)
+    return y
+
+
+def gtr_add(a: torch.Tensor, b: torch.Tensor, *, out: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
+    """a + b elementwise (fp16 or bf16, same shape); ``out`` may be a or b."""
+    _dev_contig("a", a)
+    _check("b", b, tuple(a.shape), (a.dtype,), a.device)
+    y = out if out is not None else torch.empty_like(a)
+    _check("out", y, tuple(a.shape), (a.dtype,), a.device)
+    st = load().gtr_add(_ptr(a), _ptr(b), _ptr(y), a.numel(), _DT[a.dtype], _stream_ptr(stream))
+    if st:
+        raise GtrError("gtr_add", st)
     return y

@@ -18,7 +18,7 @@ INCLUDE = os.path.join(ROOT, "include")
 BUILD = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libgtr.so")
 
-SOURCES = ["gtr_host.cpp", "permute.hip", "gla_fwd.hip", "gla_lean.hip", "swiglu.hip"]
+SOURCES = ["gtr_host.cpp", "permute.hip", "gla_fwd.hip", "gla_lean.hip", "swiglu.hip", "block.hip"]
 
 HIPCC_FLAGS = [
     "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-Wall",

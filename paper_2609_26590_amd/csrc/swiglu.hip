@@ -84,7 +84,27 @@ struct GemmArgs {
   int M, N, K;
   int cdt;     // dtype of C (GTR_F32 / GTR_F16 / GTR_BF16)
   int ksplit;  // number of K slices (1: none)
+  const float* bias;  // [N] float32 added to every row, or null (ksplit = 1 only)
+  const void* res;    // [M][N] in C's dtype added elementwise (a residual), or null (ksplit = 1 only)
 };
+
+// 4 consecutive elements of dtype dt at element offset off, as floats.
+__device__ __forceinline__ void load4(const void* base, int dt, int64_t off, float (&x)[4]) {
+  if (dt == GTR_F32) {
+    const f4 v = *reinterpret_cast<const f4*>(static_cast<const float*>(base) + off);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) x[e] = v[e];
+  } else if (dt == GTR_F16) {
+    const h4 v = *reinterpret_cast<const h4*>(static_cast<const _Float16*>(base) + off);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) x[e] = (float)v[e];
+  } else {
+    typedef unsigned short u16x4 __attribute__((ext_vector_type(4)));
+    const u16x4 v = *reinterpret_cast<const u16x4*>(static_cast<const unsigned short*>(base) + off);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) x[e] = bf16_bits_to_f32(v[e]);
+  }
+}
 
 constexpr int KB = 4;     // minimum 64-wide K-steps per slice when splitting K
 // LDS tiles: rows of 32 K elements (64 bytes, no padding); the 16-byte piece
@@ -213,8 +233,20 @@ __global__ void __launch_bounds__(256) gemm_nt_kernel(GemmArgs g) {
     if (m >= g.M) continue;
 #pragma unroll
     for (int j = 0; j < TJ; ++j) {
-      const int64_t off = (int64_t)m * g.N + nb + wn + 16 * j + 4 * kq;
-      const float x[4] = {acc[i][j][0], acc[i][j][1], acc[i][j][2], acc[i][j][3]};
+      const int n0 = nb + wn + 16 * j + 4 * kq;
+      const int64_t off = (int64_t)m * g.N + n0;
+      float x[4] = {acc[i][j][0], acc[i][j][1], acc[i][j][2], acc[i][j][3]};
+      if (g.ksplit == 1 && g.bias) {
+        const f4 bv = *reinterpret_cast<const f4*>(g.bias + n0);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) x[e] += bv[e];
+      }
+      if (g.ksplit == 1 && g.res) {
+        float rv[4];
+        load4(g.res, cdt, off, rv);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) x[e] += rv[e];
+      }
       store_n<4>(C, cdt, off, x);
     }
   }
@@ -576,5 +608,47 @@ extern "C" gtr_status gtr_spatial_swiglu(const gtr_swiglu_args* a, hipStream_t s
     hipLaunchKernelGGL(ksplit_reduce_kernel, dim3((unsigned)((n4 + 255) / 256)), dim3(256), 0, stream, part, a->y,
                        n4, ks, (int)a->y_dtype);
   }
+  return hipGetLastError() == hipSuccess ? GTR_OK : GTR_ERR_HIP;
+}
+
+// ---------------------------------------------------------------------------
+// gtr_gemm: C = A B^T (+ bias) (+ res) on gemm_nt_kernel, 128 x 64 tiles, no
+// K split (the block's products have K = d or 64).
+// ---------------------------------------------------------------------------
+static gtr_status gemm_check(const gtr_gemm_args* a) {
+  if (a->M <= 0 || a->N <= 0 || a->K <= 0) return GTR_ERR_SHAPE;
+  if (a->N % 64 || a->K % 64) return GTR_ERR_UNSUPPORTED;
+  if ((a->a_dtype != GTR_F16 && a->a_dtype != GTR_BF16) || a->b_dtype != a->a_dtype) return GTR_ERR_UNSUPPORTED;
+  if (a->c_dtype != GTR_F16 && a->c_dtype != GTR_BF16 && a->c_dtype != GTR_F32) return GTR_ERR_UNSUPPORTED;
+  if (a->M > 0x7fffffff - 128 || ((a->M + 127) / 128) * (a->N / 64) > 0x7fffffff) return GTR_ERR_SHAPE;
+  if (!a->a || !a->b || !a->c) return GTR_ERR_NULL;
+  const uintptr_t mis = reinterpret_cast<uintptr_t>(a->a) | reinterpret_cast<uintptr_t>(a->b) |
+                        reinterpret_cast<uintptr_t>(a->c) | reinterpret_cast<uintptr_t>(a->bias) |
+                        reinterpret_cast<uintptr_t>(a->res);
+  if (mis & 15u) return GTR_ERR_UNSUPPORTED;
+  const size_t es = dtype_size(a->a_dtype);
+  auto ovl = [](const void* p, size_t pb, const void* q, size_t qb) {
+    const uintptr_t x = reinterpret_cast<uintptr_t>(p), y = reinterpret_cast<uintptr_t>(q);
+    return q && x < y + qb && y < x + pb;
+  };
+  const size_t cb = (size_t)a->M * a->N * dtype_size(a->c_dtype);
+  // C may be res itself (an in-place residual: each element is read, then
+  // written, by one thread), not any other input
+  if (ovl(a->c, cb, a->a, (size_t)a->M * a->K * es) || ovl(a->c, cb, a->b, (size_t)a->N * a->K * es) ||
+      ovl(a->c, cb, a->bias, (size_t)a->N * 4) || (a->res != a->c && ovl(a->c, cb, a->res, cb)))
+    return GTR_ERR_ALIAS;
+  return GTR_OK;
+}
+
+extern "C" gtr_status gtr_gemm(const gtr_gemm_args* a, hipStream_t stream) {
+  if (!a) return GTR_ERR_NULL;
+  const gtr_status st = gemm_check(a);
+  if (st != GTR_OK) return st;
+  GemmArgs g{a->a, a->b, a->c, nullptr, (int)a->M, a->N, a->K, (int)a->c_dtype, 1, a->bias, a->res};
+  const dim3 grid((unsigned)(((a->M + 127) / 128) * (a->N / 64)));
+  if (a->a_dtype == GTR_BF16)
+    hipLaunchKernelGGL((gemm_nt_kernel<GTR_BF16, GTR_BF16, GTR_BF16, 128, 64>), grid, dim3(256), 0, stream, g);
+  else
+    hipLaunchKernelGGL((gemm_nt_kernel<GTR_F16, GTR_F16, GTR_F16, 128, 64>), grid, dim3(256), 0, stream, g);
   return hipGetLastError() == hipSuccess ? GTR_OK : GTR_ERR_HIP;
 }

@@ -165,3 +165,39 @@ def algorithmic_bytes(wl: Workload) -> float:
     if wl.want_final:
         total += seq_state
     return total
+
+
+# ---------------------------------------------------------------------------
+# One GTR block with random weights (GTR-S: d 192, 3 heads; GTR-L: d 384, 6
+# heads; head width 64, Spatial SwiGLU expansion 4, gate rank 16). Draw order:
+# x, then the weights in the order of BLOCK_WEIGHTS; projections N(0, 1/fan_in),
+# layer-norm and RMSNorm weights 1 + N(0, 0.1), biases N(0, 0.1), the gate bias
+# N(2, 0.5) (decays between about 0.995 and 0.9999 per token after the
+# temperature), depthwise conv weights N(0, 1/9). Every tensor is cast to its
+# dtype once; fp16 / bf16 weights and float32 norm weights and biases.
+# ---------------------------------------------------------------------------
+BLOCK_SIZES = {"gtr_s": (192, 3), "gtr_l": (384, 6)}
+GATE_RANK = 16
+
+
+def make_block(name: str, H: int, W: int, B: int = 1, dtype: str = "f16", seed: int = 11) -> tuple:
+    """(x [B, H*W, d], weights dict) for one block; see the recipe above."""
+    d, heads = BLOCK_SIZES[name]
+    hidden = 4 * d
+    rng = np.random.Generator(np.random.PCG64(seed))
+    n = lambda *shape, std=1.0, mu=0.0: mu + std * rng.standard_normal(shape)
+    x = _cast(n(B, H * W, d), dtype)
+    p = {
+        "ln1_w": n(d, std=0.1, mu=1.0), "ln1_b": n(d, std=0.1),
+        "w_qkvr": n(4 * d, d, std=d ** -0.5),
+        "w_a1": n(GATE_RANK, d, std=d ** -0.5), "w_a2": n(d, GATE_RANK, std=GATE_RANK ** -0.5),
+        "b_a": n(d, std=0.5, mu=2.0),
+        "norm_w": n(d // heads, std=0.1, mu=1.0),
+        "w_o": n(d, d, std=d ** -0.5),
+        "ln2_w": n(d, std=0.1, mu=1.0), "ln2_b": n(d, std=0.1),
+        "w_g": n(hidden, d, std=d ** -0.5), "w_v": n(hidden, d, std=d ** -0.5),
+        "w_out": n(d, hidden, std=hidden ** -0.5),
+        "conv_w": n(hidden, 3, 3, std=1.0 / 3), "conv_b": n(hidden, std=0.1),
+    }
+    f32 = ("ln1_w", "ln1_b", "b_a", "norm_w", "ln2_w", "ln2_b", "conv_w", "conv_b")
+    return x, {k: _cast(v, "f32" if k in f32 else dtype) for k, v in p.items()}

@@ -450,20 +450,26 @@ def check_kernel(text, name, kern, regions, wgs, waves=4):
     assert "INFO-PATHLIMIT" not in rep.counts
 
 
-@pytest.mark.parametrize("adt,bdt,mt,bn,M,N,K,cdt,ks", [(1, 2, 1, 64, 126, 256, 64, 0, 1),
-                                                        (1, 1, 1, 64, 1600, 384, 1536, 1, 4),
-                                                        (1, 2, 1, 64, 63, 64, 128, 2, 1),
-                                                        (1, 1, 1, 64, 200, 192, 192, 1, 2)])
-def test_swiglu_gemm_addresses(adt, bdt, mt, bn, M, N, K, cdt, ks):
+@pytest.mark.parametrize("adt,bdt,mt,bn,M,N,K,cdt,ks,epi", [(1, 2, 1, 64, 126, 256, 64, 0, 1, 0),
+                                                            (1, 1, 1, 64, 1600, 384, 1536, 1, 4, 0),
+                                                            (1, 2, 1, 64, 63, 64, 128, 2, 1, 0),
+                                                            (1, 1, 1, 64, 200, 192, 192, 1, 2, 0),
+                                                            # gtr_gemm: bias and residual epilogue
+                                                            (1, 1, 1, 64, 1600, 1536, 384, 1, 1, 3),
+                                                            (2, 2, 2, 64, 37, 64, 64, 0, 1, 1),
+                                                            (2, 2, 2, 64, 1, 384, 64, 2, 1, 2)])
+def test_swiglu_gemm_addresses(adt, bdt, mt, bn, M, N, K, cdt, ks, epi):
+    """epi: bit 0 a bias, bit 1 a residual (gtr_gemm's epilogue)."""
     text = swiglu_asm()
     base = 0x1000_0000_0000
     es = {0: 4, 1: 2, 2: 2}
-    A, B, C, P = (base + i * 0x10_0000_0000 for i in range(4))
+    A, B, C, P, BI, R = (base + i * 0x10_0000_0000 for i in range(6))
     regions = [emu.Region("A", A, M * K * 2, "r"), emu.Region("B", B, N * K * 2, "r"),
                emu.Region("C", C, M * N * es[cdt], "w"),
                emu.Region("part", P, ks * M * N * 4, "w"),  # K-split partials are float32
+               emu.Region("bias", BI, N * 4, "r"), emu.Region("res", R, M * N * es[cdt], "r"),
                emu.Region("kernarg", emu.KERNARG_BASE, 64, "r")]
-    kern = struct.pack("<QQQQiiiii4x", A, B, C, P, M, N, K, cdt, ks)
+    kern = struct.pack("<QQQQiiiii4xQQ", A, B, C, P, M, N, K, cdt, ks, BI if epi & 1 else 0, R if epi & 2 else 0)
     name = f"_ZN3gtr14gemm_nt_kernelILi{adt}ELi{bdt}ELi{mt}ELi128ELi{bn}EEEvNS_8GemmArgsE"
     assert name in emu.kernel_names(text)
     gx, gy = (M + 127) // 128, N // bn
@@ -531,3 +537,73 @@ def test_swiglu_ksplit_reduce_addresses(cdt):
     name = [n for n in emu.kernel_names(text) if "ksplit_reduce_kernel" in n][0]
     nblk = (n4 + 255) // 256
     check_kernel(text, name, kern, regions, [(0, 0, 0), (nblk - 1, 0, 0)])
+
+
+# ---------------------------------------------------------------------------
+# the block's small kernels (block.hip)
+# ---------------------------------------------------------------------------
+def block_asm() -> str:
+    from paper_2609_26590_amd import build as b
+    h = hashlib.sha256()
+    for f in ("block.hip", "gtr_device.h", "gtr_internal.h"):
+        with open(os.path.join(CSRC, f), "rb") as fh:
+            h.update(fh.read())
+    with open(os.path.join(ROOT, "include", "gtr.h"), "rb") as fh:
+        h.update(fh.read())
+    h.update(" ".join(b.HIPCC_FLAGS).encode())
+    os.makedirs(BUILD, exist_ok=True)
+    path = os.path.join(BUILD, f"block.gfx950.{h.hexdigest()[:16]}.s")
+    if not os.path.exists(path):
+        tmp = path + f".tmp{os.getpid()}"
+        r = subprocess.run([b._hipcc(), *b.HIPCC_FLAGS, "-S", "--cuda-device-only", os.path.join(CSRC, "block.hip"),
+                            "-o", tmp], capture_output=True, text=True)
+        assert r.returncode == 0, r.stderr[-2000:]
+        os.replace(tmp, path)
+    with open(path) as fh:
+        return fh.read()
+
+
+def _kname(text, sub):
+    return [n for n in emu.kernel_names(text) if sub in n][0]
+
+
+@pytest.mark.parametrize("M,d,dt,affine", [(1600, 384, 1, True), (33, 192, 2, False), (5, 2048, 1, True),
+                                           (4, 8, 2, True)])
+def test_block_layernorm_addresses(M, d, dt, affine):
+    text = block_asm()
+    base = 0x1000_0000_0000
+    X, Wt, Bt, Y = (base + i * 0x10_0000_0000 for i in range(4))
+    regions = [emu.Region("x", X, M * d * 2, "r"), emu.Region("w", Wt, d * 4, "r"), emu.Region("b", Bt, d * 4, "r"),
+               emu.Region("y", Y, M * d * 2, "w"), emu.Region("kernarg", emu.KERNARG_BASE, 64, "r")]
+    kern = struct.pack("<QQQQqifi4x", X, Wt if affine else 0, Bt if affine else 0, Y, M, d, 1e-6, dt)
+    nb = (M + 3) // 4
+    check_kernel(text, _kname(text, "layernorm_kernel"), kern, regions, [(0, 0, 0), (nb - 1, 0, 0)])
+
+
+@pytest.mark.parametrize("parts,B,H,L,dh,pad,merge", [(4, 1, 6, 1600, 64, 0, 0), (2, 3, 2, 5, 8, 8, 0),
+                                                      (1, 2, 3, 37, 64, 0, 1), (1, 3, 2, 5, 8, 0, 1)])
+def test_block_heads_addresses(parts, B, H, L, dh, pad, merge):
+    text = block_asm()
+    base = 0x1000_0000_0000
+    S, D = base, base + 0x10_0000_0000
+    ld = parts * H * dh + pad
+    n = parts * B * H * L * dh
+    src_elems = n if merge else B * L * ld
+    regions = [emu.Region("src", S, src_elems * 2, "r"), emu.Region("dst", D, n * 2, "w"),
+               emu.Region("kernarg", emu.KERNARG_BASE, 64, "r")]
+    total = n // 8
+    kern = struct.pack("<QQqiiqi4xqii", S, D, total, B, H, L, dh // 8, ld // 8, parts, merge)
+    nb = (total + 255) // 256
+    check_kernel(text, _kname(text, "heads_kernel"), kern, regions, sorted({(0, 0, 0), (nb - 1, 0, 0)}))
+
+
+@pytest.mark.parametrize("n,dt", [(614400, 1), (8, 2), (2056, 1)])
+def test_block_add_addresses(n, dt):
+    text = block_asm()
+    base = 0x1000_0000_0000
+    A, Bv, Y = (base + i * 0x10_0000_0000 for i in range(3))
+    regions = [emu.Region("a", A, n * 2, "r"), emu.Region("b", Bv, n * 2, "r"), emu.Region("y", Y, n * 2, "w"),
+               emu.Region("kernarg", emu.KERNARG_BASE, 64, "r")]
+    kern = struct.pack("<QQQqi4x", A, Bv, Y, n // 8, dt)
+    nb = (n // 8 + 255) // 256
+    check_kernel(text, _kname(text, "add_kernel"), kern, regions, sorted({(0, 0, 0), (nb - 1, 0, 0)}))

@@ -575,3 +575,106 @@ def test_spatial_swiglu_python_copy_passes_the_composition_pin():
 @pytest.mark.parametrize("mistake", ["conv_on_gate", "conv_after_gating", "no_bias"])
 def test_spatial_swiglu_composition_pin_rejects_planted_mistakes(mistake):
     assert not swiglu_composition_pin(lambda *a, **kw: py_spatial_swiglu(*a, mistake=mistake, **kw))
+
+
+# ---------------------------------------------------------------------------
+# One GTR block (Sec. 3.1): layer normalisation and the block's composition
+# ---------------------------------------------------------------------------
+def layer_norm_pins(fn) -> bool:
+    """True when ``fn(x, w, b, eps)`` behaves as a layer normalisation over the last axis."""
+    rng = np.random.default_rng(21)
+    x = rng.normal(size=(4, 6, 48)) * rng.uniform(0.1, 10.0, size=(4, 6, 1)) + rng.normal(size=(4, 6, 1)) * 5
+    w = rng.uniform(0.5, 2.0, size=48)
+    b = rng.normal(size=48)
+    y = fn(x, None, None, 0.0)
+    pins = [
+        np.allclose(y.mean(axis=-1), 0.0, atol=1e-12),                        # zero mean per row
+        np.allclose((y * y).mean(axis=-1), 1.0, rtol=1e-12),                  # unit (biased) variance per row
+        np.allclose(fn(x, w, b, 0.0), y * w + b, rtol=1e-12, atol=1e-12),    # affine per channel
+        np.allclose(fn(x * 3.0 + 7.0, None, None, 0.0), y, rtol=1e-10, atol=1e-10),  # shift / scale invariant
+    ]
+    # epsilon under the root: the row (-1, 1, -1, 1, ...) has variance 1 -> 1 / sqrt(1 + eps)
+    alt = np.tile([-1.0, 1.0], 24)[None]
+    pins.append(np.allclose(fn(alt, None, None, 3.0), alt / 2.0, rtol=1e-12))
+    # a constant row maps to the bias
+    pins.append(np.allclose(fn(np.full((1, 48), 4.0), w, b, 1e-6), b, rtol=1e-12))
+    return all(pins)
+
+
+def py_layer_norm(x, w, b, eps, mistake=None):
+    w = np.ones(x.shape[-1]) if w is None else w
+    b = np.zeros(x.shape[-1]) if b is None else b
+    axis = -2 if mistake == "axis" else -1
+    mean = 0.0 if mistake == "no_center" else np.mean(x, axis=axis, keepdims=True)
+    var = np.var(x, axis=axis, keepdims=True, ddof=1 if mistake == "unbiased" else 0)
+    den = np.sqrt(var) + eps if mistake == "eps_outside" else np.sqrt(var + eps)
+    return (x - mean) / den * w + b
+
+
+def test_layer_norm_oracle_passes_its_pins():
+    assert layer_norm_pins(lambda x, w, b, eps: oracle.layer_norm(x, w, b, eps))
+
+
+@pytest.mark.parametrize("mistake", ["axis", "no_center", "unbiased", "eps_outside"])
+def test_layer_norm_pins_reject_planted_mistakes(mistake):
+    assert not layer_norm_pins(lambda x, w, b, eps: py_layer_norm(x, w, b, eps, mistake))
+
+
+def test_layer_norm_python_copy_passes_pins():
+    assert layer_norm_pins(lambda x, w, b, eps: py_layer_norm(x, w, b, eps))
+
+
+def _small_block(seed=5):
+    """A GTR block at d = 16, 2 heads, hidden 64 on a 4 x 5 grid, float64 weights."""
+    rng = np.random.default_rng(seed)
+    d, heads, hidden, r = 16, 2, 64, 4
+    n = lambda *s, std=1.0, mu=0.0: mu + std * rng.normal(size=s)
+    p = {"ln1_w": n(d, std=0.1, mu=1.0), "ln1_b": n(d, std=0.1), "w_qkvr": n(4 * d, d, std=d ** -0.5),
+         "w_a1": n(r, d, std=d ** -0.5), "w_a2": n(d, r, std=r ** -0.5), "b_a": n(d, mu=2.0, std=0.5),
+         "norm_w": n(d // heads, mu=1.0, std=0.1), "w_o": n(d, d, std=d ** -0.5), "ln2_w": n(d, std=0.1, mu=1.0),
+         "ln2_b": n(d, std=0.1), "w_g": n(hidden, d, std=d ** -0.5), "w_v": n(hidden, d, std=d ** -0.5),
+         "w_out": n(d, hidden, std=hidden ** -0.5), "conv_w": n(hidden, 3, 3, std=1 / 3), "conv_b": n(hidden, std=0.1)}
+    return n(2, 20, d), p, heads
+
+
+@pytest.mark.parametrize("scan", ["row", "col_rev"])
+def test_block_reduces_to_its_parts(scan):
+    """Pins of the composition: with W_o = 0 and the Spatial SwiGLU's W_out = 0
+    the block is the identity; with W_out = 0 alone it is x + the token mixer,
+    which matches per-head scalar loops over the recurrence (gate from the
+    logits, output gate); with zero query weights the mixer vanishes and the
+    block is x + SpatialSwiGLU(LN2(x))."""
+    x, p, heads = _small_block()
+    H, W = 4, 5
+    q = dict(p, w_o=np.zeros_like(p["w_o"]), w_out=np.zeros_like(p["w_out"]))
+    assert np.array_equal(oracle.gtr_block(x, q, H=H, W=W, heads=heads, scan=scan), x)
+    # the mixer by scalar loops, in scan order
+    q = dict(p, w_out=np.zeros_like(p["w_out"]))
+    got = oracle.gtr_block(x, q, H=H, W=W, heads=heads, scan=scan) - x
+    d = x.shape[-1]
+    dh = d // heads
+    n1 = oracle.layer_norm(x, p["ln1_w"], p["ln1_b"], 1e-6)
+    proj = n1 @ p["w_qkvr"].T
+    a = n1 @ p["w_a1"].T @ p["w_a2"].T + p["b_a"]
+    order = oracle.scan_order(H, W, scan)
+    u = np.zeros_like(x)
+    for bb in range(x.shape[0]):
+        for h in range(heads):
+            cols = slice(h * dh, (h + 1) * dh)
+            S = np.zeros((dh, dh))
+            for t in order:
+                qt, kt, vt = proj[bb, t, cols], proj[bb, t, d:2 * d][cols], proj[bb, t, 2 * d:3 * d][cols]
+                zt = proj[bb, t, 3 * d:][cols]
+                gam = (1.0 / (1.0 + np.exp(-a[bb, t, cols]))) ** (1.0 / 16.0)
+                S = gam[:, None] * S + np.outer(kt, vt)
+                o = dh ** -0.5 * qt @ S
+                rms = np.sqrt(np.mean(o * o) + 1e-5)
+                u[bb, t, cols] = zt / (1.0 + np.exp(-zt)) * o / rms * p["norm_w"]
+    assert np.allclose(got, u @ p["w_o"].T, rtol=1e-10, atol=1e-12)
+    # zero query weights: the GLA output, hence the gated output, is zero
+    wq = p["w_qkvr"].copy()
+    wq[:d] = 0.0
+    q = dict(p, w_qkvr=wq)
+    want = x + oracle.spatial_swiglu(oracle.layer_norm(x, p["ln2_w"], p["ln2_b"], 1e-6), p["w_g"], p["w_v"],
+                                     p["w_out"], p["conv_w"], p["conv_b"], H=H, W=W)
+    assert np.allclose(oracle.gtr_block(x, q, H=H, W=W, heads=heads, scan=scan), want, rtol=1e-12, atol=1e-12)
