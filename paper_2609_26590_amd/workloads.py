@@ -172,7 +172,7 @@ def algorithmic_bytes(wl: Workload) -> float:
 # heads; head width 64, Spatial SwiGLU expansion 4, gate rank 16). Draw order:
 # x, then the weights in the order of BLOCK_WEIGHTS; projections N(0, 1/fan_in),
 # layer-norm and RMSNorm weights 1 + N(0, 0.1), biases N(0, 0.1), the gate bias
-# N(2, 0.5) (decays between about 0.995 and 0.9999 per token after the
+# N(2, 0.5) (decays of about 0.98 to 0.998 per token after the
 # temperature), depthwise conv weights N(0, 1/9). Every tensor is cast to its
 # dtype once; fp16 / bf16 weights and float32 norm weights and biases.
 # ---------------------------------------------------------------------------
