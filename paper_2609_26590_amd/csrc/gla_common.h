@@ -328,8 +328,9 @@ __device__ __forceinline__ void sum_items(const GlaParams& P, int seq, int first
   constexpr int DK = T::kDK, DV = T::kDV, SPER = T::SPER, RS = T::RS;
   constexpr bool F16 = T::F16;
   static_assert(!AGG || F16, "group aggregates are fp16 tiles");
-  // tiles per batch: about 80 registers of loads per batch
-  constexpr int B = 80 / (SPER * (F16 ? 4 : 8) + 2) < 1 ? 1 : 80 / (SPER * (F16 ? 4 : 8) + 2);
+  // tiles per batch: about T::kLookRegs registers of loads per batch
+  constexpr int R = T::kLookRegs;
+  constexpr int B = R / (SPER * (F16 ? 4 : 8) + 2) < 1 ? 1 : R / (SPER * (F16 ? 4 : 8) + 2);
   const int NC = P.nchunks;
   const uint32_t tile = DK * DV * (F16 ? 2 : 4);
   const uint32_t slot = DK * DV * 4;  // a state slot (bytes)
@@ -470,6 +471,14 @@ __device__ __forceinline__ int wait_groups(const GlaParams& P, const T& ch, int 
 // The one-launch kernels for 16-bit inputs at chunk 64 (gla_lean.hip): the
 // whole-width kernel and the value-split one (d_v / 2 columns; null unless
 // d_v = 64). Returns false (both null) for every other shape or dtype.
-bool lean_kernels(int qdt, int dk, int dv, int chunk, const void** whole, const void** split);
+// occ3: at most 168 registers (three work-groups per CU), look-back batches of
+// about 80 registers; occ4: at most 128 (four per CU), batches of about 40.
+struct LeanKernels {
+  const void* whole3;
+  const void* split3;
+  const void* whole4;
+  const void* split4;
+};
+bool lean_kernels(int qdt, int dk, int dv, int chunk, LeanKernels* out);
 
 }  // namespace gtr

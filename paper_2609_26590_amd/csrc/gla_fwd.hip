@@ -69,6 +69,7 @@ namespace gtr {
 // columns of this work-group (d_v, or d_v / 2 under the value split).
 template <int DK, int DV, int C, int IN>
 struct Chunk {
+  static constexpr int kLookRegs = 80;  // registers of loads per look-back batch
   static constexpr bool F16 = IN != GTR_F32;  // matrix operands: fp16 (else float32)
   static constexpr int kDK = DK, kDV = DV;
   static constexpr int NW = C / 16;
@@ -955,11 +956,16 @@ struct KernelSet {
   const void* chain;
   const void* chain_split;  // one launch with d_v split in two (d_v = 64 only), else null
   int threads;
-  const void* lean;        // one launch for 16-bit inputs at chunk 64 (gla_lean.hip), else null
-  const void* lean_split;  // the same with d_v split in two, else null
-  // the one-launch kernels that run: the lean ones where they exist
-  const void* one() const { return lean ? lean : chain; }
-  const void* one_split() const { return lean_split ? lean_split : chain_split; }
+  const void* lean;         // one launch for 16-bit inputs at chunk 64 (gla_lean.hip), else null
+  const void* lean_split;   // the same with d_v split in two, else null
+  const void* lean4;        // the same at four work-groups per CU
+  const void* lean4_split;
+  // the one-launch kernels that run: the lean ones where they exist (occ4:
+  // the four-per-CU instantiation)
+  const void* one(bool occ4 = false) const { return lean ? (occ4 ? lean4 : lean) : chain; }
+  const void* one_split(bool occ4 = false) const {
+    return lean_split ? (occ4 ? lean4_split : lean_split) : chain_split;
+  }
 };
 
 template <int DK, int DV, int C, int IN>
@@ -998,7 +1004,14 @@ static bool select_kernels(const GlaShape& s, KernelSet* ks) {
     case GTR_BF16: ok = pick_dims<GTR_BF16>(s.dk, s.dv, s.chunk, ks); break;
     default: return false;
   }
-  if (ok) lean_kernels(s.qdt, s.dk, s.dv, s.chunk, &ks->lean, &ks->lean_split);
+  if (ok) {
+    LeanKernels lk;
+    lean_kernels(s.qdt, s.dk, s.dv, s.chunk, &lk);
+    ks->lean = lk.whole3;
+    ks->lean_split = lk.split3;
+    ks->lean4 = lk.whole4;
+    ks->lean4_split = lk.split4;
+  }
   return ok;
 }
 
@@ -1059,6 +1072,7 @@ struct Plan {
   int desc;     // chunks in descending order (every work-group resident at once)
   int nxcd;     // sequence-per-XCD grid of the 16-bit kernel (0: chunk-major grid)
   int group;    // grouped look-back (16-bit kernel, FUSED)
+  int occ4;     // 16-bit kernel at four work-groups per CU
   int64_t blocks;
 };
 
@@ -1092,6 +1106,7 @@ static gtr_status plan_call(const GlaShape& s, int path, bool gate, const Kernel
   pl->desc = 0;
   pl->nxcd = 0;
   pl->group = 0;
+  pl->occ4 = 0;
   pl->blocks = 0;
   if (path == GTR_PATH_STAGED) return GTR_OK;
   const bool fits = s.nchunks <= kMaxChainChunks && s.BH <= kSyncSeqs;
@@ -1133,6 +1148,10 @@ static gtr_status plan_call(const GlaShape& s, int path, bool gate, const Kernel
   }
   const bool lean = (pl->vparts > 1 ? ks.lean_split : ks.lean) != nullptr;
   pl->group = pl->sched == GTR_PATH_FUSED && lean && s.nchunks >= kGroupMinChunks ? 1 : 0;
+  // four work-groups per CU (shorter look-back batches) where the grid is more
+  // than one round of work-groups or the key width is 32; the inline schedule
+  // at d_k = 64, whose look-backs are the longest, keeps the longer batches
+  pl->occ4 = lean && (pl->sched == GTR_PATH_FUSED || s.dk == 32) ? 1 : 0;
   // descending chunk order when every work-group is resident (the chunks that
   // wait longest start first), except for the grouped look-back, whose
   // aggregates come from the low chunks
@@ -1239,7 +1258,7 @@ static gtr_status gla_launch(const gtr_gla_args* a, const GlaShape& s, hipStream
   void* kargs[] = {&P};
   hipError_t err;
   if (pl.sched != GTR_PATH_STAGED) {
-    const void* k = pl.vparts > 1 ? ks.one_split() : ks.one();
+    const void* k = pl.vparts > 1 ? ks.one_split(pl.occ4) : ks.one(pl.occ4);
     err = hipLaunchKernel(k, dim3((unsigned)pl.blocks), dim3(ks.threads), kargs, 0, stream);
   } else {
     err = hipLaunchKernel(ks.summary, dim3((unsigned)s.nchunks, (unsigned)s.BH), dim3(ks.threads), kargs, 0, stream);

@@ -44,11 +44,12 @@ __device__ __forceinline__ h4 ld_tr(const _Float16* p) {
 __device__ __forceinline__ h8 cat(const h4& a, const h4& b) { return __builtin_shufflevector(a, b, 0, 1, 2, 3, 4, 5, 6, 7); }
 __device__ __forceinline__ float fexp2(float x) { return __builtin_amdgcn_exp2f(x); }
 
-template <int DK, int DV, int C, int IN>
+template <int DK, int DV, int C, int IN, int OCC>
 struct Lean {
   static_assert(IN == GTR_F16 || IN == GTR_BF16, "16-bit inputs only");
   static_assert(C == 64, "chunk 64 only");
   static constexpr bool F16 = true;  // fp16 products and fp16 summaries (shared look-back)
+  static constexpr int kLookRegs = OCC >= 4 ? 40 : 80;  // registers of loads per look-back batch
   static constexpr int kDK = DK, kDV = DV;
   static constexpr int NW = C / 16;
   static constexpr int NT = NW * kWave;
@@ -621,11 +622,12 @@ struct Lean {
 // The kernel: same grid, flags, look-back, poison and hand-off protocol as
 // gla_chain_kernel in gla_fwd.hip.
 // ---------------------------------------------------------------------------
-// At most 168 registers: three work-groups per CU.
-template <int DK, int DV, int C, int IN>
-__global__ void __launch_bounds__(tile_threads(C)) __attribute__((amdgpu_waves_per_eu(3)))
+// OCC work-groups per CU: at most 168 registers for 3 (look-back batches of
+// about 80 registers), 128 for 4 (batches of about 40).
+template <int DK, int DV, int C, int IN, int OCC>
+__global__ void __launch_bounds__(tile_threads(C)) __attribute__((amdgpu_waves_per_eu(OCC)))
 gla_lean_kernel(GlaParams P) {
-  typedef Lean<DK, DV, C, IN> T;
+  typedef Lean<DK, DV, C, IN, OCC> T;
   __shared__ typename T::Smem sm;
   const int NC = P.nchunks;
   const int b = blockIdx.x;
@@ -815,25 +817,28 @@ gla_lean_kernel(GlaParams P) {
 }
 
 template <int DK, int DV, int IN>
-static void lean_pair(const void** whole, const void** split) {
-  *whole = reinterpret_cast<const void*>(&gla_lean_kernel<DK, DV, 64, IN>);
-  if constexpr (DV == 64) *split = reinterpret_cast<const void*>(&gla_lean_kernel<DK, 32, 64, IN>);
+static void lean_set(LeanKernels* o) {
+  o->whole3 = reinterpret_cast<const void*>(&gla_lean_kernel<DK, DV, 64, IN, 3>);
+  o->whole4 = reinterpret_cast<const void*>(&gla_lean_kernel<DK, DV, 64, IN, 4>);
+  if constexpr (DV == 64) {
+    o->split3 = reinterpret_cast<const void*>(&gla_lean_kernel<DK, 32, 64, IN, 3>);
+    o->split4 = reinterpret_cast<const void*>(&gla_lean_kernel<DK, 32, 64, IN, 4>);
+  }
 }
 
 template <int IN>
-static bool lean_dims(int dk, int dv, const void** whole, const void** split) {
-  if (dk == 64 && dv == 64) return lean_pair<64, 64, IN>(whole, split), true;
-  if (dk == 32 && dv == 64) return lean_pair<32, 64, IN>(whole, split), true;
-  if (dk == 32 && dv == 32) return lean_pair<32, 32, IN>(whole, split), true;
+static bool lean_dims(int dk, int dv, LeanKernels* o) {
+  if (dk == 64 && dv == 64) return lean_set<64, 64, IN>(o), true;
+  if (dk == 32 && dv == 64) return lean_set<32, 64, IN>(o), true;
+  if (dk == 32 && dv == 32) return lean_set<32, 32, IN>(o), true;
   return false;
 }
 
-bool lean_kernels(int qdt, int dk, int dv, int chunk, const void** whole, const void** split) {
-  *whole = nullptr;
-  *split = nullptr;
+bool lean_kernels(int qdt, int dk, int dv, int chunk, LeanKernels* o) {
+  *o = LeanKernels{nullptr, nullptr, nullptr, nullptr};
   if (chunk != 64) return false;
-  if (qdt == GTR_F16) return lean_dims<GTR_F16>(dk, dv, whole, split);
-  if (qdt == GTR_BF16) return lean_dims<GTR_BF16>(dk, dv, whole, split);
+  if (qdt == GTR_F16) return lean_dims<GTR_F16>(dk, dv, o);
+  if (qdt == GTR_BF16) return lean_dims<GTR_BF16>(dk, dv, o);
   return false;
 }
 

@@ -544,6 +544,17 @@ def _nop(w, i):
     return False
 
 
+@handler('s_bitset1_b32', 's_bitset0_b32')
+def _bitset(w, i):
+    # sdst[ssrc & 31] = 1 (bitset1) or 0 (bitset0); the other bits keep their value
+    r = w.sreg_index(i.ops[0])
+    bit, bo, bd = w.s32(i.ops[1], i)
+    old, oo, od = w.s32(i.ops[0], i)
+    m = 1 << (bit & 31)
+    val = (old | m) if i.op == 's_bitset1_b32' else (old & ~m & M32)
+    w.sset(r, val, (oo | (M32 if bo else 0)) & M32, od and bd)
+
+
 HWREG_VALUE = 0  # what s_getreg_b32 reads: the emulated wave runs on XCC 0
 
 

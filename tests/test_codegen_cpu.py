@@ -250,17 +250,21 @@ def mangled(kind: str, c: Shape) -> str:
         return f"_ZN3gtr15gla_scan_kernelILi{c.dk}ELi{c.dv}ELb{int(c.dt != 'f32')}EEEvNS_9GlaParamsE"
     if kind == "chain_split":  # d_v / 2 columns per work-group
         return f"_ZN3gtr16gla_chain_kernelILi{c.dk}ELi{c.dv // 2}ELi{c.chunk}ELi{DT[c.dt][0]}EEEvNS_9GlaParamsE"
-    if kind == "lean_split":
-        return f"_ZN3gtr15gla_lean_kernelILi{c.dk}ELi{c.dv // 2}ELi{c.chunk}ELi{DT[c.dt][0]}EEEvNS_9GlaParamsE"
-    if kind == "lean":
-        return f"_ZN3gtr15gla_lean_kernel{t}EEvNS_9GlaParamsE"
+    if kind in ("lean_split", "lean4_split"):
+        occ = 4 if kind.startswith("lean4") else 3
+        return f"_ZN3gtr15gla_lean_kernelILi{c.dk}ELi{c.dv // 2}ELi{c.chunk}ELi{DT[c.dt][0]}ELi{occ}EEEvNS_9GlaParamsE"
+    if kind in ("lean", "lean4"):
+        occ = 4 if kind == "lean4" else 3
+        return f"_ZN3gtr15gla_lean_kernelILi{c.dk}ELi{c.dv}ELi{c.chunk}ELi{DT[c.dt][0]}ELi{occ}EEEvNS_9GlaParamsE"
     return f"_ZN3gtr16gla_chain_kernel{t}EEvNS_9GlaParamsE"
 
 
 def work_groups(kind: str, c: Shape, ln: Launch):
-    """First, second and last chunk of the first and last sequence (+ the last
-    chunk of the first group for the grouped look-back, + one block of the
-    XCD-ordered grid that has no sequence)."""
+    """Staged kernels: first, second and last chunk of the first and last
+    sequence. One-launch kernels: first and second chunk of the first sequence
+    and the last chunk of the last (+ the last chunk of the first group for the
+    grouped look-back, + one block of the XCD-ordered grid that has no
+    sequence)."""
     nw = c.chunk // 16
     cs = sorted({0, 1 % c.NC, c.NC - 1} | ({7} if ln.group and c.NC > 8 else set()))  # 7: a group's last chunk
     bhs = sorted({0, c.BH - 1})
@@ -270,20 +274,22 @@ def work_groups(kind: str, c: Shape, ln: Launch):
         eb = (c.dk * c.dv + 255) // 256
         return [((x, bh, 0), 2) for x in sorted({0, eb - 1}) for bh in bhs]  # 128 threads
     ns = c.BH * ln.vparts
-    seqs = sorted({0, ns - 1})
-    rows = sorted({(c.NC - 1 - cc) if ln.desc else cc for cc in cs})
+    # one-launch kernels: the first chunks (and a group's last) of the first
+    # sequence, the last chunk of the last sequence
+    pairs = sorted({(cc, 0) for cc in cs if cc != c.NC - 1 or c.NC == 1} | {(c.NC - 1, ns - 1)})
+    row = lambda cc: (c.NC - 1 - cc) if ln.desc else cc
     if ln.nxcd > 1:
         # sequence-per-XCD grid: block (row * nx + j) * nxcd + x runs sequence
         # x + nxcd * j, nx = the sequences of XCD x; blocks past an XCD's share return
         nx = lambda x: (ns - x + ln.nxcd - 1) // ln.nxcd
         blocks = ln.nxcd * ((ns + ln.nxcd - 1) // ln.nxcd) * c.NC
-        out = [(((r * nx(sq % ln.nxcd) + sq // ln.nxcd) * ln.nxcd + sq % ln.nxcd, 0, 0), nw)
-               for r in rows for sq in seqs]
+        out = [(((row(cc) * nx(sq % ln.nxcd) + sq // ln.nxcd) * ln.nxcd + sq % ln.nxcd, 0, 0), nw)
+               for cc, sq in pairs]
         pad = [(nx(x) * c.NC) * ln.nxcd + x for x in range(ln.nxcd)]
         out += [((bb, 0, 0), nw) for bb in pad if bb < blocks][:1]
         return out
     # chunk-major grid: block row * ns + seq, row = chunk (or NC - 1 - chunk)
-    return [((r * ns + sq, 0, 0), nw) for r in rows for sq in seqs]
+    return [((row(cc) * ns + sq, 0, 0), nw) for cc, sq in pairs]
 
 
 # (shape, kernels): the bf16 instantiations, float32 gates with 16-bit inputs,
@@ -292,7 +298,7 @@ def work_groups(kind: str, c: Shape, ln: Launch):
 # and (16-bit kernel) the sequence-per-XCD grid
 CHAIN = ("chain", "chain_x", "chain_i")
 # the 16-bit kernel at chunk 64: every launch variant on one shape, one variant on the others
-LEAN = ("lean", "lean_n", "lean_x", "lean_i", "lean_xcd", "lean_split", "lean_g", "lean_gs")
+LEAN = ("lean", "lean_n", "lean_x", "lean_i", "lean_xcd", "lean_split", "lean_g", "lean_gs", "lean4")
 CHECKS = [
     (Shape(1, 12, 40, 40, 64, 64, 64, "bf16", "bf16", "f32", "row", False, False),
      ("summary", "scan", "output") + CHAIN + ("chain_split",) + LEAN),
@@ -301,12 +307,12 @@ CHECKS = [
     (Shape(1, 2, 20, 20, 32, 64, 128, "bf16", "bf16", "bf16", "row_rev", False, False), ("output",) + CHAIN),
     (Shape(1, 6, 40, 40, 64, 64, 64, "f16", "f16", "f16", "row", False, False),
      CHAIN + ("chain_split", "lean_split")),
-    (Shape(1, 5, 9, 23, 32, 64, 64, "f16", "f32", "f32", "row_rev", True, True), ("lean", "lean_split")),
+    (Shape(1, 5, 9, 23, 32, 64, 64, "f16", "f32", "f32", "row_rev", True, True), ("lean", "lean_split", "lean4", "lean4_gs")),
     (Shape(3, 3, 16, 16, 32, 32, 64, "bf16", "f32", "bf16", "col", False, True), ("lean_xcd",)),
     (Shape(1, 3, 7, 9, 64, 64, 128, "f16", "f32", "f32", "col", True, True), ("output",) + CHAIN + ("chain_split",)),
     (Shape(1, 2, 13, 11, 64, 64, 32, "f32", "f32", "f32", "row_rev", True, True), CHAIN + ("chain_split",)),
     (Shape(1, 2, 13, 11, 32, 32, 32, "f32", "f32", "f32", "row", False, True), ("summary", "output") + CHAIN),
-    (Shape(1, 6, 80, 80, 64, 64, 64, "f16", "f16", "f16", "row", False, False), ("scan",) + CHAIN + ("lean", "lean_g")),
+    (Shape(1, 6, 80, 80, 64, 64, 64, "f16", "f16", "f16", "row", False, False), ("scan",) + CHAIN + ("lean", "lean_g", "lean4_g")),
     # gate fusion and the output-gate epilogue
     (Shape(1, 12, 40, 40, 64, 64, 64, "bf16", "bf16", "f32", "col", True, True, True, "bf16", True),
      ("summary", "output") + CHAIN + ("lean_i",)),
@@ -347,13 +353,20 @@ def launches(kind: str, c: Shape):
                 Launch(group=1, flag=FLAG_NONE)]
     if kind == "lean_gs":  # grouped look-back with the value split
         return [Launch(vparts=2, group=1, flag=FLAG_GROUP)]
+    if kind == "lean4":  # four work-groups per CU: summaries back to the start, inclusive states
+        return [Launch(flag=FLAG_SUMMARY), Launch(desc=1, flag=FLAG_ALL)]
+    if kind == "lean4_g":
+        return [Launch(group=1, flag=FLAG_GROUP), Launch(group=1, flag=FLAG_NONE)]
+    if kind == "lean4_gs":
+        return [Launch(vparts=2, group=1, flag=FLAG_GROUP | FLAG_ALL)]
     return [Launch()]
 
 
 def split_name(kind):
-    """The kernel a kind runs: the value-split instantiation for the split kinds."""
-    if kind in ("chain_split", "lean_split", "lean_gs"):
-        return "lean_split" if kind.startswith("lean") else kind
+    """The kernel a kind runs: the value-split instantiation for the split kinds
+    (lean4: the four-per-CU instantiation of the 16-bit kernel)."""
+    if kind in ("chain_split", "lean_split", "lean_gs", "lean4_gs"):
+        return kind if kind == "chain_split" else kind.split("_")[0] + "_split"
     return kind.split("_")[0]
 
 
