@@ -273,7 +273,8 @@ def block_detail():
         torch.cuda.synchronize()
         t, _ = time_graph(step, 100, 10)
         M, h, dh = 1600, 4 * d, d // heads
-        flops = 2.0 * M * (4 * d * d + 64 * d + 64 * d + d * d + 3 * h * d) + heads * M * (2 * dh * 65 + 4 * dh * dh)
+        # products: the five-part projection (q, k, v, z, gate logits), W_o, the Spatial SwiGLU's three
+        flops = 2.0 * M * (5 * d * d + d * d + 3 * h * d) + heads * M * (2 * dh * 65 + 4 * dh * dh)
         res[f"block {name.upper().replace('_', '-')} d{d} 40x40"] = {
             "us_per_call": t * 1e6, "tflops": flops / t / 1e12, "tokens_per_s": M / t}
     return res

@@ -273,7 +273,8 @@ int gtr_gla_value_parts(const gtr_gla_args* args);
  *                                 grid offset (u - 1, v - 1)
  * conv_b  : [hidden] float32 or NULL
  * y       : [B, H*W, d]           y_dtype (dtype or GTR_F32); must not overlap
- *                                 the inputs or the workspace
+ *                                 the inputs or the workspace; y = residual + Y
+ *                                 when residual (below) is not NULL
  * dtype   : GTR_F16 or GTR_BF16; d and hidden multiples of 64; every pointer
  *           16-byte aligned.
  * The products accumulate in float32; X W_g and X W_v are rounded to fp16 on
@@ -299,6 +300,7 @@ typedef struct {
   int32_t B, H, W, d, hidden;
   void* workspace;
   size_t workspace_bytes;
+  const void* residual;  /* [B, H*W, d] in y_dtype added to y (a block's residual), or NULL; may be y itself */
 } gtr_swiglu_args;
 
 size_t gtr_spatial_swiglu_workspace_size(const gtr_swiglu_args* args);
@@ -309,7 +311,8 @@ gtr_status gtr_spatial_swiglu(const gtr_swiglu_args* args, hipStream_t stream);
  * key-only gated recurrence with its output gate, head concat and W_o, then
  * Spatial SwiGLU), composed from them and the calls above.
  *
- * gtr_gemm: C = A B^T (+ bias) (+ res), the block's projections.
+ * gtr_gemm: C = A B^T (+ bias) (+ res), the block's projections. a and c may
+ * be head-major (a_tokens, c_tokens below; zero for row-major).
  * a       : [M, K] row-major, a_dtype (GTR_F16 or GTR_BF16)
  * b       : [N, K] row-major (linear-layer weight layout, output features
  *           first), b_dtype = a_dtype
@@ -331,6 +334,13 @@ typedef struct {
   gtr_dtype a_dtype, b_dtype, c_dtype;
   int64_t M;
   int32_t N, K;
+  int64_t a_tokens;    /* 0, or a head-major a: [M / a_tokens][K / 64][a_tokens][64], row m = token m % a_tokens
+                          of image m / a_tokens, columns 64 h .. 64 h + 63 = head h (a head concat read in
+                          place; M a multiple of a_tokens) */
+  int64_t c_tokens;    /* 0, or a head-major c: [N / (c_heads c_head_dim)][M / c_tokens][c_heads][c_tokens]
+                          [c_head_dim] (projections split into heads as they are stored; M a multiple of
+                          c_tokens, N of c_heads c_head_dim, c_head_dim of 4, res NULL) */
+  int32_t c_heads, c_head_dim;
 } gtr_gemm_args;
 
 gtr_status gtr_gemm(const gtr_gemm_args* args, hipStream_t stream);

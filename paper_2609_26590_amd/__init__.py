@@ -75,6 +75,7 @@ class SwigluArgs(ctypes.Structure):
         ("y", ctypes.c_void_p), ("dtype", ctypes.c_int), ("y_dtype", ctypes.c_int),
         ("B", ctypes.c_int32), ("H", ctypes.c_int32), ("W", ctypes.c_int32), ("d", ctypes.c_int32),
         ("hidden", ctypes.c_int32), ("workspace", ctypes.c_void_p), ("workspace_bytes", ctypes.c_size_t),
+        ("residual", ctypes.c_void_p),
     ]
 
 
@@ -84,6 +85,8 @@ class GemmArgs(ctypes.Structure):
         ("a", ctypes.c_void_p), ("b", ctypes.c_void_p), ("c", ctypes.c_void_p), ("bias", ctypes.c_void_p),
         ("res", ctypes.c_void_p), ("a_dtype", ctypes.c_int), ("b_dtype", ctypes.c_int), ("c_dtype", ctypes.c_int),
         ("M", ctypes.c_int64), ("N", ctypes.c_int32), ("K", ctypes.c_int32),
+        ("a_tokens", ctypes.c_int64), ("c_tokens", ctypes.c_int64), ("c_heads", ctypes.c_int32),
+        ("c_head_dim", ctypes.c_int32),
     ]
 
 
@@ -365,12 +368,14 @@ def gtr_gla_value_parts(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, g: to
 def gtr_spatial_swiglu(x: torch.Tensor, w_gate: torch.Tensor, w_value: torch.Tensor, w_out: torch.Tensor,
                        conv_w: torch.Tensor, conv_b: Optional[torch.Tensor] = None, *, H: int, W: int,
                        y_dtype: Optional[torch.dtype] = None, out: Optional[torch.Tensor] = None,
+                       residual: Optional[torch.Tensor] = None,
                        workspace: Optional["Workspace"] = None, stream=None) -> torch.Tensor:
     """Spatial SwiGLU (Sec. 3.1): y = [SiLU(x W_g^T) * DWConv3x3(x W_v^T)] W_o^T.
 
     x [B, H*W, d] (fp16/bf16, spatial order), w_gate/w_value [hidden, d],
     w_out [d, hidden] (same dtype), conv_w [hidden, 3, 3] and conv_b [hidden]
-    float32. Returns y [B, H*W, d] in ``y_dtype`` (default: x's dtype).
+    float32. Returns y [B, H*W, d] in ``y_dtype`` (default: x's dtype), plus
+    ``residual`` ([B, H*W, d] in that dtype, may be ``out``) when given.
     """
     for name, t in (("x", x), ("w_gate", w_gate), ("w_value", w_value), ("w_out", w_out), ("conv_w", conv_w)) + \
             ((("conv_b", conv_b),) if conv_b is not None else ()):
@@ -383,6 +388,9 @@ def gtr_spatial_swiglu(x: torch.Tensor, w_gate: torch.Tensor, w_value: torch.Ten
     a.conv_w, a.conv_b, a.y = _ptr(conv_w), _ptr(conv_b), _ptr(y)
     a.dtype, a.y_dtype = _DT[x.dtype], _DT[y.dtype]
     a.B, a.H, a.W, a.d, a.hidden = B, H, W, d, w_gate.shape[0]
+    if residual is not None:  # y = residual + SwiGLU(x)
+        _check("residual", residual, (B, L, d), (y.dtype,), x.device)
+        a.residual = _ptr(residual)
     lib = load()
     need = int(lib.gtr_spatial_swiglu_workspace_size(ctypes.byref(a)))
     if need == 0:
@@ -408,24 +416,43 @@ def _dev_contig(name: str, t: torch.Tensor) -> None:
 
 def gtr_gemm(a: torch.Tensor, b: torch.Tensor, *, bias: Optional[torch.Tensor] = None,
              res: Optional[torch.Tensor] = None, out_dtype: Optional[torch.dtype] = None,
-             out: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
+             out: Optional[torch.Tensor] = None, heads_out: Optional[tuple] = None, stream=None) -> torch.Tensor:
     """c = a b^T (+ bias) (+ res): a [M, K], b [N, K] (fp16 or bf16, same dtype),
-    bias [N] float32, res [M, N] in the output dtype (may be ``out``)."""
+    bias [N] float32, res [M, N] in the output dtype (may be ``out``).
+
+    a may also be head-major [B, K / 64, L, 64] (a head concat read in place:
+    M = B * L). ``heads_out = (L, heads, dh)`` stores c head-major as
+    [N / (heads * dh), M / L, heads, L, dh] instead of [M, N]."""
     for name, t in (("a", a), ("b", b)) + ((("bias", bias),) if bias is not None else ()) + \
             ((("res", res),) if res is not None else ()):
         _dev_contig(name, t)
-    M, K = a.shape
+    a_tokens = 0
+    if a.dim() == 4:
+        Bi, nh, L, w = a.shape
+        if w != 64:
+            raise ValueError("a head-major operand has heads of width 64")
+        M, K, a_tokens = Bi * L, nh * 64, L
+    else:
+        M, K = a.shape
     N = b.shape[0]
     if b.shape[1] != K:
         raise ValueError(f"b has {b.shape[1]} columns, a has {K}")
-    c = out if out is not None else torch.empty((M, N), dtype=out_dtype or a.dtype, device=a.device)
-    _check("out", c, (M, N), (torch.float32, torch.float16, torch.bfloat16), a.device)
+    if heads_out is not None:
+        L, nh, dh = heads_out
+        shape = (N // (nh * dh), M // L, nh, L, dh)
+    else:
+        shape = (M, N)
+    c = out if out is not None else torch.empty(shape, dtype=out_dtype or a.dtype, device=a.device)
+    _check("out", c, shape, (torch.float32, torch.float16, torch.bfloat16), a.device)
     _check("bias", bias, (N,), (torch.float32,), a.device)
     _check("res", res, (M, N), (c.dtype,), a.device)
     g = GemmArgs()
     g.a, g.b, g.c, g.bias, g.res = _ptr(a), _ptr(b), _ptr(c), _ptr(bias), _ptr(res)
     g.a_dtype, g.b_dtype, g.c_dtype = _DT[a.dtype], _DT[b.dtype], _DT[c.dtype]
     g.M, g.N, g.K = M, N, K
+    g.a_tokens = a_tokens
+    if heads_out is not None:
+        g.c_tokens, g.c_heads, g.c_head_dim = heads_out
     st = load().gtr_gemm(ctypes.byref(g), _stream_ptr(stream))
     if st:
         raise GtrError("gtr_gemm", st)

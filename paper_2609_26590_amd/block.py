@@ -1,39 +1,45 @@
 """One GTR block (paper Sec. 3.1) as a sequence of libgtr calls.
 
     n1 = LN1(x)                                   gtr_layernorm
-    [q k v z] = n1 W_qkvr^T                       gtr_gemm, then gtr_heads_split
-    a = (n1 W_a1^T) W_a2^T + b_a                  gtr_gemm x 2 (low-rank gate logits), gtr_heads_split
+    [q k v z a] = n1 [W_qkvr; W_a]^T + [0; b_a]   one gtr_gemm, stored head-major (W_a = W_a2 W_a1: the
+                                                  low-rank gate's factors multiplied once, in ``prepare``)
     u = SiLU(z) * RMSNorm(GLA(q, k, v; a))        gtr_gla_fwd: gate fusion (tau) and the output-gate epilogue
-    x1 = x + concat_heads(u) W_o^T                gtr_heads_merge, gtr_gemm with the residual
-    x2 = x1 + SpatialSwiGLU(LN2(x1))              gtr_layernorm, gtr_spatial_swiglu, gtr_add
+    x1 = x + concat_heads(u) W_o^T                gtr_gemm reading u head-major, the residual in its epilogue
+    x2 = x1 + SpatialSwiGLU(LN2(x1))              gtr_layernorm, gtr_spatial_swiglu with the residual
 
 Every step runs in the library's kernels; this module only marshals
 arguments. The block's normalisation and residual placement are a reading of
 the paper (it names the parts of the block, not their order): pre-norm layer
 normalisation before the token mixer and before the Spatial SwiGLU, a residual
-around each. The gate's rank-16 projection pair is zero-padded to 64 once,
-when the weights are prepared (the product kernel takes K and N in multiples
-of 64; the padding adds exact zeros).
+around each. The gate's rank-16 factors are multiplied into one d x d matrix
+when the weights are prepared: the same logits in real arithmetic, with the
+product's fp16 rounding in place of the rank-16 intermediate's.
 """
 from __future__ import annotations
 
 import torch
 
-from . import (gtr_add, gtr_gemm, gtr_gla_fwd, gtr_heads_merge, gtr_heads_split, gtr_layernorm,
-               gtr_spatial_swiglu)
+from . import gtr_gemm, gtr_gla_fwd, gtr_layernorm, gtr_spatial_swiglu
 
 GATE_PAD = 64
 
 
 def prepare(p: dict) -> dict:
-    """Device weights for ``forward``: the gate's rank-16 pair padded to 64."""
-    q = dict(p)
+    """Device weights for ``forward`` (once per block): the gate's rank-16
+    factors multiplied into one d x d matrix W_a = W_a2 W_a1 (on the device,
+    through gtr_gemm, the rank zero-padded to 64) and appended to the
+    projections as a fifth part, with the gate bias as that part's bias, so one
+    product gives q, k, v, z and the gate logits."""
     r, d = p["w_a1"].shape
-    a1 = torch.zeros((GATE_PAD, d), dtype=p["w_a1"].dtype, device=p["w_a1"].device)
-    a1[:r] = p["w_a1"]
-    a2 = torch.zeros((d, GATE_PAD), dtype=p["w_a2"].dtype, device=p["w_a2"].device)
+    dev, dt = p["w_a1"].device, p["w_a1"].dtype
+    a2 = torch.zeros((d, GATE_PAD), dtype=dt, device=dev)
     a2[:, :r] = p["w_a2"]
-    q["w_a1"], q["w_a2"] = a1, a2.contiguous()
+    a1t = torch.zeros((d, GATE_PAD), dtype=dt, device=dev)
+    a1t[:, :r] = p["w_a1"].t()
+    w_a = gtr_gemm(a2, a1t)  # [d, d] = W_a2 W_a1
+    q = dict(p)
+    q["w_proj"] = torch.cat([p["w_qkvr"], w_a]).contiguous()
+    q["b_proj"] = torch.cat([torch.zeros(4 * d, device=dev), p["b_a"].float()]).contiguous()
     return q
 
 
@@ -46,17 +52,14 @@ def forward(x: torch.Tensor, p: dict, *, H: int, W: int, heads: int, scan: str, 
     M = B * L
     x2d = x.reshape(M, d)
     n1 = gtr_layernorm(x2d, p["ln1_w"], p["ln1_b"], eps=ln_eps, stream=stream)
-    proj = gtr_gemm(n1, p["w_qkvr"], stream=stream)                       # [M, 4d]
-    qkvz = gtr_heads_split(proj, parts=4, B=B, heads=heads, dh=dh, stream=stream)
-    a1 = gtr_gemm(n1, p["w_a1"], stream=stream)                           # [M, 64]
-    a = gtr_gemm(a1, p["w_a2"], bias=p["b_a"], stream=stream)             # [M, d]
-    g = gtr_heads_split(a, parts=1, B=B, heads=heads, dh=dh, stream=stream)[0]
-    u, _ = gtr_gla_fwd(qkvz[0], qkvz[1], qkvz[2], g, H=H, W=W, scale=dh ** -0.5, scan=scan,
-                       gate_tau=tau, out_gate=qkvz[3], norm_weight=p["norm_w"],
+    # one product, stored head-major ([5, B, heads, L, dh]: q, k, v, z, gate logits)
+    proj = gtr_gemm(n1, p["w_proj"], bias=p["b_proj"], heads_out=(L, heads, dh), stream=stream)
+    u, _ = gtr_gla_fwd(proj[0], proj[1], proj[2], proj[4], H=H, W=W, scale=dh ** -0.5, scan=scan,
+                       gate_tau=tau, out_gate=proj[3], norm_weight=p["norm_w"],
                        norm_eps=norm_eps, stream=stream)
-    um = gtr_heads_merge(u, stream=stream)                               # [M, d]
-    x1 = gtr_gemm(um, p["w_o"], res=x2d, stream=stream)
+    # the head concat read in place by W_o, the residual in its epilogue
+    x1 = gtr_gemm(u, p["w_o"], res=x2d, stream=stream)
     n2 = gtr_layernorm(x1, p["ln2_w"], p["ln2_b"], eps=ln_eps, stream=stream)
-    y = gtr_spatial_swiglu(n2.reshape(B, L, d), p["w_g"], p["w_v"], p["w_out"], p["conv_w"], p["conv_b"],
-                           H=H, W=W, stream=stream)
-    return gtr_add(x1.reshape(B, L, d), y, stream=stream)
+    x1 = x1.reshape(B, L, d)
+    return gtr_spatial_swiglu(n2.reshape(B, L, d), p["w_g"], p["w_v"], p["w_out"], p["conv_w"], p["conv_b"],
+                              H=H, W=W, residual=x1, stream=stream)

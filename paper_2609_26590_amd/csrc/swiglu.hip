@@ -86,6 +86,11 @@ struct GemmArgs {
   int ksplit;  // number of K slices (1: none)
   const float* bias;  // [N] float32 added to every row, or null (ksplit = 1 only)
   const void* res;    // [M][N] in C's dtype added elementwise (a residual), or null (ksplit = 1 only)
+  // head-major operands (ksplit = 1 only; 0: row-major):
+  int64_t a_tokens;   // A is [M / a_tokens][K / 64][a_tokens][64]: row m = (image m / a_tokens, token
+                      // m % a_tokens), K step s = head s (a head concat read in place)
+  int64_t c_tokens;   // C is written [N / (c_heads c_dim)][M / c_tokens][c_heads][c_tokens][c_dim]
+  int c_heads, c_dim;
 };
 
 // 4 consecutive elements of dtype dt at element offset off, as floats.
@@ -157,7 +162,9 @@ __global__ void __launch_bounds__(256) gemm_nt_kernel(GemmArgs g) {
 #pragma unroll
   for (int q = 0; q < PA; ++q) {
     const int p = threadIdx.x + 256 * q, row = p >> 3, col = p & 7;
-    ga[q] = reinterpret_cast<const w4*>(A + (int64_t)min(mb + row, g.M - 1) * K + 8 * col);
+    const unsigned m = (unsigned)min(mb + row, g.M - 1), at = g.a_tokens ? (unsigned)g.a_tokens : 1u;
+    ga[q] = reinterpret_cast<const w4*>(
+        A + (g.a_tokens ? ((int64_t)(m / at) * (K / 64) * at + m % at) * 64 : (int64_t)m * K) + 8 * col);
     la[q] = row * kPitch64 + 8 * (col ^ kSwz64(row));
   }
 #pragma unroll
@@ -176,10 +183,11 @@ __global__ void __launch_bounds__(256) gemm_nt_kernel(GemmArgs g) {
   // to LDS the step before it is multiplied (the loop is unrolled by D so
   // every slot index is a compile-time constant)
   constexpr int D = 4;
+  const int64_t ast = g.a_tokens ? 8 * g.a_tokens : 8;  // 16-byte pieces from one K step of A to the next
   w4 ra[D][PA], rb[D][PB];
   auto fetch = [&](int st, w4 (&a)[PA], w4 (&b)[PB]) {
 #pragma unroll
-    for (int q = 0; q < PA; ++q) a[q] = ga[q][8 * st];
+    for (int q = 0; q < PA; ++q) a[q] = ga[q][ast * st];
 #pragma unroll
     for (int q = 0; q < PB; ++q) b[q] = gb[q][8 * st];
   };
@@ -189,35 +197,52 @@ __global__ void __launch_bounds__(256) gemm_nt_kernel(GemmArgs g) {
 #pragma unroll
     for (int q = 0; q < PB; ++q) *reinterpret_cast<w4*>(&Bs[buf][lb[q]]) = b[q];
   };
+  auto mma = [&](int buf) {
 #pragma unroll
-  for (int q = 0; q < D; ++q)
-    if (s0 + q < s1) fetch(s0 + q, ra[q], rb[q]);
-  if (s0 < s1) stage(0, ra[0], rb[0]);
-  __syncthreads();
-  for (int sb = s0; sb < s1; sb += D) {
+    for (int h = 0; h < 2; ++h) {  // the two 32-deep halves of the step
+      const int pc = (4 * h + kq) ^ kSwz64(r16);
+      typename OA::T fa[TI];
+      typename OB::T fb[TJ];
 #pragma unroll
-    for (int q = 0; q < D; ++q) {
-      const int st = sb + q;
+      for (int i = 0; i < TI; ++i)
+        fa[i] = OA::get(*reinterpret_cast<const w4*>(&As[buf][(wm + 16 * i + r16) * kPitch64 + 8 * pc]));
+#pragma unroll
+      for (int j = 0; j < TJ; ++j)
+        fb[j] = OB::get(*reinterpret_cast<const w4*>(&Bs[buf][(wn + 16 * j + r16) * kPitch64 + 8 * pc]));
+#pragma unroll
+      for (int i = 0; i < TI; ++i)
+#pragma unroll
+        for (int j = 0; j < TJ; ++j) acc[i][j] = mfma(fb[j], fa[i], acc[i][j]);  // C^T tiles
+    }
+  };
+  // The loop runs whole groups of D steps in which every step issues the same
+  // loads (past the slice's last step they re-read that step, never used):
+  // with no load under a branch the compiler's waits count exactly, so a step
+  // waits for the loads of the step it stages, not for the newer ones (which
+  // matters where few work-groups run, each a chain of K steps). The last
+  // (steps mod D) steps follow with their loads already in flight.
+  if (s1 > s0) {
+#pragma unroll
+    for (int q = 0; q < D; ++q) fetch(min(s0 + q, s1 - 1), ra[q], rb[q]);
+    stage(0, ra[0], rb[0]);
+    __syncthreads();
+    int sb = s0;
+    for (; sb + D <= s1; sb += D) {
+#pragma unroll
+      for (int q = 0; q < D; ++q) {
+        const int st = sb + q, buf = (st - s0) & 1;
+        fetch(min(st + D, s1 - 1), ra[q], rb[q]);  // slot q was staged before this step
+        mma(buf);
+        stage(buf ^ 1, ra[(q + 1) % D], rb[(q + 1) % D]);  // nobody reads buf ^ 1 now
+        __syncthreads();
+      }
+    }
+#pragma unroll
+    for (int q = 0; q < D - 1; ++q) {
+      const int st = sb + q, buf = (st - s0) & 1;
       if (st < s1) {
-        const int buf = (st - s0) & 1;
-        if (st + D < s1) fetch(st + D, ra[q], rb[q]);  // slot q was staged before this step
-#pragma unroll
-        for (int h = 0; h < 2; ++h) {  // the two 32-deep halves of the step
-          const int pc = (4 * h + kq) ^ kSwz64(r16);
-          typename OA::T fa[TI];
-          typename OB::T fb[TJ];
-#pragma unroll
-          for (int i = 0; i < TI; ++i)
-            fa[i] = OA::get(*reinterpret_cast<const w4*>(&As[buf][(wm + 16 * i + r16) * kPitch64 + 8 * pc]));
-#pragma unroll
-          for (int j = 0; j < TJ; ++j)
-            fb[j] = OB::get(*reinterpret_cast<const w4*>(&Bs[buf][(wn + 16 * j + r16) * kPitch64 + 8 * pc]));
-#pragma unroll
-          for (int i = 0; i < TI; ++i)
-#pragma unroll
-            for (int j = 0; j < TJ; ++j) acc[i][j] = mfma(fb[j], fa[i], acc[i][j]);  // C^T tiles
-        }
-        if (st + 1 < s1) stage(buf ^ 1, ra[(q + 1) % D], rb[(q + 1) % D]);  // nobody reads buf ^ 1 now
+        mma(buf);
+        if (st + 1 < s1) stage(buf ^ 1, ra[(q + 1) % D], rb[(q + 1) % D]);
         __syncthreads();
       }
     }
@@ -227,6 +252,24 @@ __global__ void __launch_bounds__(256) gemm_nt_kernel(GemmArgs g) {
   // wave's block (the products above are C^T tiles): one 4-element store each
   void* C = g.ksplit > 1 ? static_cast<void*>(g.part + (int64_t)bz * g.M * g.N) : g.C;
   const int cdt = g.ksplit > 1 ? (int)GTR_F32 : g.cdt;
+  // head-major C: element (m, n) at (((p img + b) heads + h) tokens + t) dim + c
+  // with m = b tokens + t, n = (p heads + h) dim + c; the divisions are 32-bit
+  // (the host keeps M below 2^31) and taken once per row and column block
+  const bool hmc = g.ksplit == 1 && g.c_tokens != 0;
+  const unsigned tokens = hmc ? (unsigned)g.c_tokens : 1u, cdim = hmc ? (unsigned)g.c_dim : 1u;
+  const unsigned hd = hmc ? (unsigned)(g.c_heads * g.c_dim) : 1u, img = (unsigned)g.M / tokens;
+  int64_t rowoff[TI], coloff[TJ];
+#pragma unroll
+  for (int i = 0; i < TI; ++i) {
+    const unsigned m = (unsigned)(mb + wm + 16 * i + r16);
+    rowoff[i] = hmc ? ((int64_t)(m / tokens) * g.c_heads * tokens + m % tokens) * cdim : (int64_t)m * g.N;
+  }
+#pragma unroll
+  for (int j = 0; j < TJ; ++j) {
+    const unsigned n0 = (unsigned)(nb + wn + 16 * j + 4 * kq);
+    const unsigned p = n0 / hd, r = n0 - p * hd, h = r / cdim;
+    coloff[j] = hmc ? ((int64_t)p * img * g.c_heads * tokens + (int64_t)h * tokens) * cdim + (r - h * cdim) : n0;
+  }
 #pragma unroll
   for (int i = 0; i < TI; ++i) {
     const int m = mb + wm + 16 * i + r16;
@@ -234,14 +277,14 @@ __global__ void __launch_bounds__(256) gemm_nt_kernel(GemmArgs g) {
 #pragma unroll
     for (int j = 0; j < TJ; ++j) {
       const int n0 = nb + wn + 16 * j + 4 * kq;
-      const int64_t off = (int64_t)m * g.N + n0;
+      const int64_t off = rowoff[i] + coloff[j];
       float x[4] = {acc[i][j][0], acc[i][j][1], acc[i][j][2], acc[i][j][3]};
       if (g.ksplit == 1 && g.bias) {
         const f4 bv = *reinterpret_cast<const f4*>(g.bias + n0);
 #pragma unroll
         for (int e = 0; e < 4; ++e) x[e] += bv[e];
       }
-      if (g.ksplit == 1 && g.res) {
+      if (g.ksplit == 1 && g.res) {  // (row-major C)
         float rv[4];
         load4(g.res, cdt, off, rv);
 #pragma unroll
@@ -255,11 +298,17 @@ __global__ void __launch_bounds__(256) gemm_nt_kernel(GemmArgs g) {
 // C = sum over the ksplit float32 partial products, converted to C's dtype;
 // 4 elements per thread.
 __global__ void __launch_bounds__(256) ksplit_reduce_kernel(const float* part, void* C, int64_t n4, int ksplit,
-                                                            int cdt) {
+                                                            int cdt, const void* res) {
   const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
   if (i >= n4) return;
   f4 s = reinterpret_cast<const f4*>(part)[i];
   for (int z = 1; z < ksplit; ++z) s += reinterpret_cast<const f4*>(part)[(int64_t)z * n4 + i];
+  if (res) {  // a residual in C's dtype
+    float r[4];
+    load4(res, cdt, 4 * i, r);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) s[e] += r[e];
+  }
   if (cdt == GTR_F32) {
     reinterpret_cast<f4*>(C)[i] = s;
   } else {
@@ -562,6 +611,11 @@ static gtr_status swiglu_check(const gtr_swiglu_args* a, int64_t* M_out, bool ch
   for (const R& r : ins)
     if (ovl(ry, r) || ovl(rw, r)) return GTR_ERR_ALIAS;
   if (ovl(ry, rw)) return GTR_ERR_ALIAS;
+  if (a->residual) {  // read-only like the inputs, or y itself (each element read, then written, by one thread)
+    if (reinterpret_cast<uintptr_t>(a->residual) & 15u) return GTR_ERR_UNSUPPORTED;
+    const R rr = rng(a->residual, (size_t)M * a->d * dtype_size(a->y_dtype));
+    if ((a->residual != a->y && ovl(rr, ry)) || ovl(rr, rw)) return GTR_ERR_ALIAS;
+  }
   return GTR_OK;
 }
 
@@ -596,7 +650,7 @@ extern "C" gtr_status gtr_spatial_swiglu(const gtr_swiglu_args* a, hipStream_t s
 
   const int ks = out_ksplit(M, a->d, a->hidden);
   float* part = reinterpret_cast<float*>(ws + lay.part_off);
-  GemmArgs g3{Hb, a->w_out, a->y, part, (int)M, a->d, a->hidden, a->y_dtype, ks};
+  GemmArgs g3{Hb, a->w_out, a->y, part, (int)M, a->d, a->hidden, a->y_dtype, ks, nullptr, ks == 1 ? a->residual : nullptr};
   const dim3 grid3((unsigned)(((M + 127) / 128) * (a->d / kOutBN) * ks));
   if (bf)
     hipLaunchKernelGGL((gemm_nt_kernel<GTR_F16, GTR_BF16, GTR_F16, 128, kOutBN>), grid3, dim3(256), 0, stream, g3);
@@ -606,7 +660,7 @@ extern "C" gtr_status gtr_spatial_swiglu(const gtr_swiglu_args* a, hipStream_t s
   if (ks > 1) {
     const int64_t n4 = M * a->d / 4;
     hipLaunchKernelGGL(ksplit_reduce_kernel, dim3((unsigned)((n4 + 255) / 256)), dim3(256), 0, stream, part, a->y,
-                       n4, ks, (int)a->y_dtype);
+                       n4, ks, (int)a->y_dtype, a->residual);
   }
   return hipGetLastError() == hipSuccess ? GTR_OK : GTR_ERR_HIP;
 }
@@ -616,8 +670,13 @@ extern "C" gtr_status gtr_spatial_swiglu(const gtr_swiglu_args* a, hipStream_t s
 // K split (the block's products have K = d or 64).
 // ---------------------------------------------------------------------------
 static gtr_status gemm_check(const gtr_gemm_args* a) {
-  if (a->M <= 0 || a->N <= 0 || a->K <= 0) return GTR_ERR_SHAPE;
+  if (a->M <= 0 || a->N <= 0 || a->K <= 0 || a->a_tokens < 0 || a->c_tokens < 0) return GTR_ERR_SHAPE;
   if (a->N % 64 || a->K % 64) return GTR_ERR_UNSUPPORTED;
+  if (a->a_tokens && a->M % a->a_tokens) return GTR_ERR_SHAPE;
+  if (a->c_tokens) {
+    if (a->c_heads <= 0 || a->c_head_dim <= 0 || a->M % a->c_tokens) return GTR_ERR_SHAPE;
+    if (a->c_head_dim % 4 || a->N % ((int64_t)a->c_heads * a->c_head_dim) || a->res) return GTR_ERR_UNSUPPORTED;
+  }
   if ((a->a_dtype != GTR_F16 && a->a_dtype != GTR_BF16) || a->b_dtype != a->a_dtype) return GTR_ERR_UNSUPPORTED;
   if (a->c_dtype != GTR_F16 && a->c_dtype != GTR_BF16 && a->c_dtype != GTR_F32) return GTR_ERR_UNSUPPORTED;
   if (a->M > 0x7fffffff - 128 || ((a->M + 127) / 128) * (a->N / 64) > 0x7fffffff) return GTR_ERR_SHAPE;
@@ -644,7 +703,8 @@ extern "C" gtr_status gtr_gemm(const gtr_gemm_args* a, hipStream_t stream) {
   if (!a) return GTR_ERR_NULL;
   const gtr_status st = gemm_check(a);
   if (st != GTR_OK) return st;
-  GemmArgs g{a->a, a->b, a->c, nullptr, (int)a->M, a->N, a->K, (int)a->c_dtype, 1, a->bias, a->res};
+  GemmArgs g{a->a, a->b, a->c, nullptr, (int)a->M, a->N, a->K, (int)a->c_dtype, 1, a->bias, a->res,
+             a->a_tokens, a->c_tokens, a->c_tokens ? a->c_heads : 0, a->c_tokens ? a->c_head_dim : 0};
   const dim3 grid((unsigned)(((a->M + 127) / 128) * (a->N / 64)));
   if (a->a_dtype == GTR_BF16)
     hipLaunchKernelGGL((gemm_nt_kernel<GTR_BF16, GTR_BF16, GTR_BF16, 128, 64>), grid, dim3(256), 0, stream, g);

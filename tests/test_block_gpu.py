@@ -68,6 +68,50 @@ def test_gemm_residual_in_place():
 
 
 @pytest.mark.parametrize("dtype", [torch.float16, torch.bfloat16])
+@pytest.mark.parametrize("B,L,heads,parts", [(1, 1600, 6, 4), (2, 207, 3, 1)])
+def test_gemm_head_major_operands(dtype, B, L, heads, parts):
+    """gtr_gemm storing c head-major and reading a head-major a: the same
+    products, placed as a reshape and transpose of the row-major ones."""
+    rng = np.random.default_rng(L + parts)
+    d = 64 * heads
+    a = rnd(rng, B * L, d, dtype=dtype).to(DEV)
+    w = rnd(rng, parts * d, d, std=d ** -0.5, dtype=dtype).to(DEV)
+    bias = rnd(rng, parts * d, dtype=torch.float32).to(DEV)
+    plain = gtr.gtr_gemm(a, w, bias=bias)
+    hm = gtr.gtr_gemm(a, w, bias=bias, heads_out=(L, heads, 64))
+    torch.cuda.synchronize()
+    assert torch.equal(hm, plain.reshape(B, L, parts, heads, 64).permute(2, 0, 3, 1, 4))
+    # a head-major a (as the GLA output) against its head concat
+    u = hm[0].contiguous()                       # [B, heads, L, 64]
+    wo = rnd(rng, d, d, std=d ** -0.5, dtype=dtype).to(DEV)
+    got = gtr.gtr_gemm(u, wo, res=a)
+    want = gtr.gtr_gemm(u.permute(0, 2, 1, 3).reshape(B * L, d).contiguous(), wo, res=a)
+    torch.cuda.synchronize()
+    assert torch.equal(got, want)
+
+
+@pytest.mark.parametrize("B,H,W", [(1, 40, 40), (2, 9, 23)])
+def test_spatial_swiglu_residual(B, H, W):
+    """y = residual + SwiGLU(x), in place on the residual too."""
+    rng = np.random.default_rng(H * W)
+    d, h = 192, 768
+    x = rnd(rng, B, H * W, d).to(DEV)
+    wg, wv = rnd(rng, h, d, std=d ** -0.5).to(DEV), rnd(rng, h, d, std=d ** -0.5).to(DEV)
+    wo = rnd(rng, d, h, std=h ** -0.5).to(DEV)
+    cw = rnd(rng, h, 3, 3, std=1 / 3, dtype=torch.float32).to(DEV)
+    r = rnd(rng, B, H * W, d).to(DEV)
+    y0 = gtr.gtr_spatial_swiglu(x, wg, wv, wo, cw, H=H, W=W, y_dtype=torch.float32)
+    y1 = gtr.gtr_spatial_swiglu(x, wg, wv, wo, cw, H=H, W=W, residual=r)
+    y2 = r.clone()
+    gtr.gtr_spatial_swiglu(x, wg, wv, wo, cw, H=H, W=W, residual=y2, out=y2)
+    torch.cuda.synchronize()
+    want = (y0.double() + r.double()).cpu().numpy()
+    tol = 2.0 ** -11 * np.abs(want) + 1e-6
+    assert np.all(np.abs(y1.double().cpu().numpy() - want) <= tol)
+    assert torch.equal(y1, y2)
+
+
+@pytest.mark.parametrize("dtype", [torch.float16, torch.bfloat16])
 @pytest.mark.parametrize("M,d,affine", [(1600, 384, True), (33, 192, False), (5, 2048, True), (4, 8, True)])
 def test_layernorm_parity(dtype, M, d, affine):
     rng = np.random.default_rng(M * d)

@@ -470,9 +470,13 @@ def check_kernel(text, name, kern, regions, wgs, waves=4):
                                                             # gtr_gemm: bias and residual epilogue
                                                             (1, 1, 1, 64, 1600, 1536, 384, 1, 1, 3),
                                                             (2, 2, 2, 64, 37, 64, 64, 0, 1, 1),
-                                                            (2, 2, 2, 64, 1, 384, 64, 2, 1, 2)])
+                                                            (2, 2, 2, 64, 1, 384, 64, 2, 1, 2),
+                                                            # head-major operands (the block's projections)
+                                                            (1, 1, 1, 64, 1600, 1536, 384, 1, 1, 8),
+                                                            (1, 1, 1, 64, 3200, 384, 384, 1, 1, 6),
+                                                            (2, 2, 2, 64, 414, 384, 64, 2, 1, 9)])
 def test_swiglu_gemm_addresses(adt, bdt, mt, bn, M, N, K, cdt, ks, epi):
-    """epi: bit 0 a bias, bit 1 a residual (gtr_gemm's epilogue)."""
+    """epi: bit 0 a bias, bit 1 a residual (gtr_gemm's epilogue), bits 2 / 3 head-major A / C."""
     text = swiglu_asm()
     base = 0x1000_0000_0000
     es = {0: 4, 1: 2, 2: 2}
@@ -482,7 +486,11 @@ def test_swiglu_gemm_addresses(adt, bdt, mt, bn, M, N, K, cdt, ks, epi):
                emu.Region("part", P, ks * M * N * 4, "w"),  # K-split partials are float32
                emu.Region("bias", BI, N * 4, "r"), emu.Region("res", R, M * N * es[cdt], "r"),
                emu.Region("kernarg", emu.KERNARG_BASE, 64, "r")]
-    kern = struct.pack("<QQQQiiiii4xQQ", A, B, C, P, M, N, K, cdt, ks, BI if epi & 1 else 0, R if epi & 2 else 0)
+    # epi bit 2: head-major A, bit 3: head-major C (6 heads of 64), two images of M / 2 tokens (one if M is odd)
+    at = (M // 2 if M % 2 == 0 else M) if epi & 4 else 0
+    ct = (M // 2 if M % 2 == 0 else M) if epi & 8 else 0
+    kern = struct.pack("<QQQQiiiii4xQQqqii", A, B, C, P, M, N, K, cdt, ks, BI if epi & 1 else 0,
+                       R if epi & 2 else 0, at, ct, 6 if ct else 0, 64 if ct else 0)
     name = f"_ZN3gtr14gemm_nt_kernelILi{adt}ELi{bdt}ELi{mt}ELi128ELi{bn}EEEvNS_8GemmArgsE"
     assert name in emu.kernel_names(text)
     gx, gy = (M + 127) // 128, N // bn
@@ -545,8 +553,10 @@ def test_swiglu_ksplit_reduce_addresses(cdt):
     base = 0x1000_0000_0000
     P, C = base, base + 0x10_0000_0000
     regions = [emu.Region("part", P, ks * M * N * 4, "r"), emu.Region("C", C, M * N * es[cdt], "w"),
-               emu.Region("kernarg", emu.KERNARG_BASE, 32, "r")]
-    kern = struct.pack("<QQqii", P, C, n4, ks, cdt)
+               emu.Region("kernarg", emu.KERNARG_BASE, 40, "r")]
+    R = base + 0x20_0000_0000
+    regions.append(emu.Region("res", R, M * N * es[cdt], "r"))
+    kern = struct.pack("<QQqiiQ", P, C, n4, ks, cdt, R if cdt else 0)
     name = [n for n in emu.kernel_names(text) if "ksplit_reduce_kernel" in n][0]
     nblk = (n4 + 255) // 256
     check_kernel(text, name, kern, regions, [(0, 0, 0), (nblk - 1, 0, 0)])
