@@ -112,6 +112,8 @@ def parse():
                    help="only measure the achievable copy bandwidth and fp16 GEMM rate and print them")
     p.add_argument("--swiglu-only", action="store_true",
                    help="only time the Spatial SwiGLU (GTR-L and GTR-X widths) and print its JSON line")
+    p.add_argument("--block-only", action="store_true",
+                   help="only time one GTR block (GTR-S and GTR-L widths, 40x40) and print its JSON line")
     p.add_argument("--calibrate-copy", type=float, default=0.0, metavar="MB",
                    help="only run a device-to-device copy of MB megabytes --steps times")
     return p.parse_args()
@@ -439,6 +441,9 @@ def main():
     gtr.load()
     if a.swiglu_only:
         print(json.dumps(swiglu_detail()), flush=True)
+        return
+    if a.block_only:
+        print(json.dumps(block_detail()), flush=True)
         return
     if a.peaks:
         print(json.dumps(measured_peaks()), flush=True)
