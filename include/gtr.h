@@ -115,7 +115,7 @@ typedef enum {
                           over S_[c+1] in turn (the scan co-runs with the
                           outputs). For 16-bit inputs at chunk 64 and sequences
                           of more than 32 chunks the look-back goes by groups of
-                          8 chunks: the last chunk of each group also hands over
+                          16 chunks: the last chunk of each group also hands over
                           the group's aggregate, and a chunk sums the summaries
                           of its own group and then one aggregate per earlier
                           group. At most 1024 sequences of 256 chunks.              */

@@ -21,14 +21,14 @@ constexpr unsigned kFlagLocal = 4u;        // the summary and record went to the
 // FUSED schedule: every kPublishEvery-th chunk (and no other) stores its
 // inclusive state S_[c+1]; a look-back sums at most about that many summaries
 // before it meets one, and the other chunks skip the store.
-constexpr int kPublishEvery = 4;
+constexpr int kPublishEvery = 8;
 // Grouped look-back (16-bit kernel, long sequences): the chunks form groups of
 // kGroup; the last chunk e of a group stores the group's aggregate
 //   A_g = sum_{j in group} (prod_{j<l<=e} Diag(d_l)) U_j,  D_g = prod_{j in group} d_j,
 // so a chunk sums the summaries of its own group and then one aggregate per
 // earlier group instead of every summary. Inclusive states are then stored at
 // group ends only.
-constexpr int kGroup = 8;
+constexpr int kGroup = 16;
 constexpr unsigned kFlagGroup = 8u;        // chunk flag (group ends): the group aggregate and its record are stored
 constexpr float kF16Safe = 65504.f;        // bf16 inputs must stay within the fp16 range
 

@@ -266,7 +266,7 @@ def work_groups(kind: str, c: Shape, ln: Launch):
     grouped look-back, + one block of the XCD-ordered grid that has no
     sequence)."""
     nw = c.chunk // 16
-    cs = sorted({0, 1 % c.NC, c.NC - 1} | ({7} if ln.group and c.NC > 8 else set()))  # 7: a group's last chunk
+    cs = sorted({0, 1 % c.NC, c.NC - 1} | ({15} if ln.group and c.NC > 16 else set()))  # 15: a group's last chunk
     bhs = sorted({0, c.BH - 1})
     if kind in ("summary", "output"):
         return [((cc, bh, 0), nw) for cc in cs for bh in bhs]

@@ -156,8 +156,8 @@ def test_value_split_parity(gtr, case):
 
 
 # FUSED with the grouped look-back (16-bit inputs at chunk 64, sequences longer
-# than 32 chunks, groups of 8 chunks): ragged last groups and chunks, S0 and
-# S_final, the value split, 256 chunks (32 groups), every dims pair
+# than 32 chunks, groups of 16 chunks): ragged last groups and chunks, S0 and
+# S_final, the value split, 256 chunks (16 groups), every dims pair
 GROUPED = [
     (1, 2, 48, 48, 64, 64, 64, "bf16", "bf16", "f32", "col", True, True),       # 36 chunks, value split
     (1, 3, 50, 41, 32, 64, 64, "f16", "f32", "f16", "row_rev", False, True),    # 33 chunks, 2-token tail
