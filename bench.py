@@ -497,6 +497,10 @@ def main():
     }
     if a.detail:
         out["detail"] = detail(a.path, a.steps, a.warmup)
+    elif only is None:
+        # the rows beyond the GLA call, timed in every default run: the Spatial
+        # SwiGLU and one GTR block (warm, us per image / per block)
+        out["beyond_gla"] = {**swiglu_detail(), **block_detail()}
     if not a.no_cpu:
         out["cpu_baseline"] = cpu_baseline(wl, a.cpu_seconds)
     print(json.dumps(out), flush=True)
