@@ -540,16 +540,19 @@ __global__ void __launch_bounds__(256) gated_conv_kernel(GatedConvArgs f) {
 }
 
 // The output product uses 128 x 64 work-group tiles (d is small next to
-// hidden) and splits K into the fewest slices that give one work-group per CU
-// (256) when M x d alone does not: every slice costs a float32 partial product
-// and its share of the reduction. Measured at GTR-L width, one image (product +
-// reduction, microseconds): 128 x 64 tiles with 1 / 2 / 4 / 8 slices 21.5 /
-// 16.5 / 15.8 / 17.1, 128 x 128 tiles 20.7 / 19.0 / 16.5 / 18.7.
+// hidden) and splits K into the fewest slices that give 128 work-groups when
+// M x d alone does not: every slice costs a float32 partial product and its
+// share of the reduction. Measured at GTR-L width, one image (product +
+// reduction, microseconds), with a K loop that waited for all its loads at
+// every step: 128 x 64 tiles with 1 / 2 / 4 / 8 slices 21.5 / 16.5 / 15.8 /
+// 17.1, 128 x 128 tiles 20.7 / 19.0 / 16.5 / 18.7; with the pipelined K loop,
+// the whole Spatial SwiGLU at 78 / 156 / 312 work-groups (1 / 2 / 4 slices)
+// 32.2 / 30.0 / 30.9 at GTR-L and 46.2 / 41.4 / 42.5 at GTR-X.
 constexpr int kOutBN = 64;
 static int out_ksplit(int64_t M, int d, int hidden) {
   const int64_t wgs = ((M + 127) / 128) * (d / kOutBN);
   int s = 1;
-  while (wgs * s < 256 && s < 8 && hidden / 64 >= 2 * s * KB) s *= 2;
+  while (wgs * s < 128 && s < 8 && hidden / 64 >= 2 * s * KB) s *= 2;
   return s;
 }
 

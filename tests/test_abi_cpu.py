@@ -328,14 +328,13 @@ def test_swiglu_workspace_size(lib):
     a = swiglu_args(B=2, H=40, W=40, d=384, hidden=1536)
     M = 2 * 1600
     a256 = lambda x: (x + 255) // 256 * 256
-    # H in fp16 (G and V stay on chip), then 2 float32 partial products of the
-    # output product split over K: 25 x 6 work-groups of 128 x 64 alone would
-    # leave CUs idle, two slices give 300 >= 256.
+    # H in fp16 (G and V stay on chip); the output product splits K only when
+    # its 128 x 64 tiles give fewer than 128 work-groups: 25 x 6 = 150 do not
     base = a256(M * 1536 * 2)
-    assert lib.gtr_spatial_swiglu_workspace_size(ctypes.byref(a)) == a256(base + 2 * M * 384 * 4)
-    one = swiglu_args(B=1, H=40, W=40, d=384, hidden=1536)  # 13 x 6 work-groups: 4 slices
+    assert lib.gtr_spatial_swiglu_workspace_size(ctypes.byref(a)) == base
+    one = swiglu_args(B=1, H=40, W=40, d=384, hidden=1536)  # 13 x 6 work-groups: 2 slices
     assert lib.gtr_spatial_swiglu_workspace_size(ctypes.byref(one)) == \
-        a256(a256(1600 * 1536 * 2) + 4 * 1600 * 384 * 4)
+        a256(a256(1600 * 1536 * 2) + 2 * 1600 * 384 * 4)
     big = swiglu_args(B=8, H=40, W=40, d=384, hidden=1536)  # 100 x 6 work-groups: no split
     assert lib.gtr_spatial_swiglu_workspace_size(ctypes.byref(big)) == a256(12800 * 1536 * 2)
 
