@@ -151,13 +151,13 @@ def test_add_parity(dtype):
     assert np.all(np.abs(y.double().cpu().numpy() - want) <= ulp * np.abs(want) + 1e-7)
 
 
-def run_block(name, scan, H=40, W=40, B=1):
-    x, p = make_block(name, H, W, B=B)
+def run_block(name, scan, H=40, W=40, B=1, dtype="f16"):
+    x, p = make_block(name, H, W, B=B, dtype=dtype)
     heads = {"gtr_s": 3, "gtr_l": 6}[name]
     pd = block.prepare({k: v.to(DEV) for k, v in p.items()})
     y = block.forward(x.to(DEV), pd, H=H, W=W, heads=heads, scan=scan)
     torch.cuda.synchronize()
-    want = oracle.gtr_block(x.numpy(), {k: v.double().numpy() for k, v in p.items()}, H=H, W=W, heads=heads,
+    want = oracle.gtr_block(x.double().numpy(), {k: v.double().numpy() for k, v in p.items()}, H=H, W=W, heads=heads,
                             scan=scan)
     return x.double().numpy(), y.double().cpu().numpy(), want
 
@@ -178,3 +178,16 @@ def test_block_ragged_grid_two_images():
     x, got, want = run_block("gtr_s", "col", H=9, W=23, B=2)
     err = np.max(np.abs(got - want))
     assert err <= 5e-3 * np.max(np.abs(want - x)), err
+
+
+@pytest.mark.parametrize("scan", ["row_rev", "col"])
+def test_block_parity_bf16(scan):
+    """bf16 activations and weights (the products on bf16 MFMA, the GLA on fp16
+    operands with its range check): one bf16 rounding (2^-8 relative) per
+    stored intermediate, so the bars are 8x the fp16 ones."""
+    x, got, want = run_block("gtr_l", scan, dtype="bf16")
+    err = np.max(np.abs(got - want))
+    inc = np.max(np.abs(want - x))
+    print(f"gtr_l bf16 {scan}: max err {err:.3e}, max |increment| {inc:.3e}")
+    assert err <= 4e-2 * inc, (err, inc)
+    assert err <= 1.6e-2 * np.max(np.abs(want)), err
