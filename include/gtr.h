@@ -350,7 +350,7 @@ gtr_status gtr_gemm(const gtr_gemm_args* args, hipStream_t stream);
  * channels of every row m (mean and biased variance of the row, in float32).
  * x, y : [M, d] dtype (GTR_F16 or GTR_BF16); y may be x (in place).
  * w, b : [d] float32; NULL stands for ones / zeros.
- * d a multiple of 8 and at most 2048; x, y 16-byte aligned.
+ * d a multiple of 8 and at most 2048; x, y, w, b 16-byte aligned.
  */
 gtr_status gtr_layernorm(const void* x, const float* w, const float* b, void* y, int64_t M, int32_t d, float eps,
                          gtr_dtype dtype, hipStream_t stream);

@@ -27,7 +27,21 @@ __device__ __forceinline__ void unpack8(v4u raw, int dt, float (&x)[8]) {
   }
 }
 
-// One wave per row of d channels (d / 8 vectors, at most 4 per lane).
+// Sum over the 64 lanes as a wave-uniform value: a prefix sum along each
+// 16-lane row with DPP row shifts, then the four row totals (lanes 15, 31, 47,
+// 63) read into scalar registers. No LDS round trips.
+__device__ __forceinline__ float wave_sum(float x) {
+  const int s = __builtin_bit_cast(int, row_inclusive_scan(x));
+  const float r0 = __builtin_bit_cast(float, __builtin_amdgcn_readlane(s, 15));
+  const float r1 = __builtin_bit_cast(float, __builtin_amdgcn_readlane(s, 31));
+  const float r2 = __builtin_bit_cast(float, __builtin_amdgcn_readlane(s, 47));
+  const float r3 = __builtin_bit_cast(float, __builtin_amdgcn_readlane(s, 63));
+  return (r0 + r1) + (r2 + r3);
+}
+
+// One wave per row of d channels (d / 8 vectors, at most 4 per lane). The
+// affine weights are loaded with the row, so the two reductions (mean, then the
+// centred sum of squares) are the only steps between the loads and the store.
 constexpr int kLnMaxVec = 4;
 __global__ void __launch_bounds__(256) layernorm_kernel(const v4u* __restrict__ x, const float* __restrict__ w,
                                                         const float* __restrict__ b, void* __restrict__ y, int64_t M,
@@ -36,7 +50,7 @@ __global__ void __launch_bounds__(256) layernorm_kernel(const v4u* __restrict__ 
   const int lane = threadIdx.x & 63;
   if (row >= M) return;
   const int nv = d / 8;
-  float v[kLnMaxVec][8];
+  float v[kLnMaxVec][8], wv[kLnMaxVec][8], bv[kLnMaxVec][8];
   float s = 0.f;
 #pragma unroll
   for (int q = 0; q < kLnMaxVec; ++q) {
@@ -44,11 +58,20 @@ __global__ void __launch_bounds__(256) layernorm_kernel(const v4u* __restrict__ 
     if (i < nv) {
       unpack8(x[row * nv + i], dt, v[q]);
 #pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        const f4 wq = w ? reinterpret_cast<const f4*>(w)[2 * i + h] : f4{1.f, 1.f, 1.f, 1.f};
+        const f4 bq = b ? reinterpret_cast<const f4*>(b)[2 * i + h] : f4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          wv[q][4 * h + e] = wq[e];
+          bv[q][4 * h + e] = bq[e];
+        }
+      }
+#pragma unroll
       for (int e = 0; e < 8; ++e) s += v[q][e];
     }
   }
-  for (int o = 32; o > 0; o >>= 1) s += __shfl_xor(s, o, kWave);
-  const float mean = s / (float)d;
+  const float mean = wave_sum(s) / (float)d;
   float ss = 0.f;
 #pragma unroll
   for (int q = 0; q < kLnMaxVec; ++q)
@@ -58,18 +81,14 @@ __global__ void __launch_bounds__(256) layernorm_kernel(const v4u* __restrict__ 
         const float t = v[q][e] - mean;
         ss = fmaf(t, t, ss);
       }
-  for (int o = 32; o > 0; o >>= 1) ss += __shfl_xor(ss, o, kWave);
-  const float rs = rsqrtf(ss / (float)d + eps);
+  const float rs = rsqrtf(wave_sum(ss) / (float)d + eps);
 #pragma unroll
   for (int q = 0; q < kLnMaxVec; ++q) {
     const int i = lane + 64 * q;
     if (i < nv) {
       float o8[8];
 #pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        const int c = 8 * i + e;
-        o8[e] = (v[q][e] - mean) * rs * (w ? w[c] : 1.f) + (b ? b[c] : 0.f);
-      }
+      for (int e = 0; e < 8; ++e) o8[e] = (v[q][e] - mean) * rs * wv[q][e] + bv[q][e];
       store_n<8>(y, dt, (row * nv + i) * 8, o8);
     }
   }
@@ -128,7 +147,7 @@ extern "C" gtr_status gtr_layernorm(const void* x, const float* w, const float* 
   if (d % 8 || d > 8 * 64 * kLnMaxVec || (dtype != GTR_F16 && dtype != GTR_BF16)) return GTR_ERR_UNSUPPORTED;
   if (M > ((int64_t)1 << 33)) return GTR_ERR_SHAPE;
   if (!x || !y) return GTR_ERR_NULL;
-  if (!aligned16(x) || !aligned16(y)) return GTR_ERR_UNSUPPORTED;
+  if (!aligned16(x) || !aligned16(y) || (w && !aligned16(w)) || (b && !aligned16(b))) return GTR_ERR_UNSUPPORTED;
   const size_t bytes = (size_t)M * d * 2;
   if (x != y && overlaps(x, bytes, y, bytes)) return GTR_ERR_ALIAS;
   if ((w && overlaps(w, (size_t)d * 4, y, bytes)) || (b && overlaps(b, (size_t)d * 4, y, bytes))) return GTR_ERR_ALIAS;

@@ -339,6 +339,9 @@ constexpr int kFV = (kFH + 2) * kFHW;    // halo tokens (180)
 constexpr int kFVT = (kFV + 15) / 16;    // MFMA row blocks of V (12; rows 180..191 are zero padding)
 constexpr int kFN = 64;                  // channels per work-group
 constexpr int kFA = kFVT * 16 * 4 / 256; // 16-byte A pieces per thread per K step (3)
+constexpr int kFB = kFN * 4 * 2 / 256;   // 16-byte pieces of the W_g and W_v tiles per thread per K step
+constexpr int kFP = kFN / 8;             // 16-byte pieces (8 channels) of one token's kFN channels
+static_assert(kFB >= 1 && kFN * 4 * 2 % 256 == 0 && (kFP & (kFP - 1)) == 0, "weight tiles split evenly over 256 threads");
 static_assert(kFVT % 4 == 0 && kFH % 4 == 0, "row blocks split evenly over 4 waves");
 
 struct GatedConvArgs {
@@ -400,10 +403,16 @@ __global__ void __launch_bounds__(256) gated_conv_kernel(GatedConvArgs f) {
     am[q] = in ? 0xffffffffu : 0u;
     la[q] = row * kPitch + 8 * (col ^ kSwz(row));
   }
-  const int brow = tid >> 2, bcol = tid & 3;
-  const w4* gbg = reinterpret_cast<const w4*>(static_cast<const unsigned short*>(f.Wg) + (int64_t)(c0 + brow) * K + 8 * bcol);
-  const w4* gbv = reinterpret_cast<const w4*>(static_cast<const unsigned short*>(f.Wv) + (int64_t)(c0 + brow) * K + 8 * bcol);
-  const int lb = brow * kPitch + 8 * (bcol ^ kSwz(brow));
+  // weight pieces: piece p < 4 kFN of the W_g tile, then the W_v tile
+  const w4* gb[kFB];
+  int lb[kFB];
+#pragma unroll
+  for (int q = 0; q < kFB; ++q) {
+    const int p = tid + 256 * q, v = p / (kFN * 4), r = (p % (kFN * 4)) >> 2, col = p & 3;
+    gb[q] = reinterpret_cast<const w4*>(static_cast<const unsigned short*>(v ? f.Wv : f.Wg) + (int64_t)(c0 + r) * K +
+                                        8 * col);
+    lb[q] = SA + v * SB + r * kPitch + 8 * (col ^ kSwz(r));
+  }
 
   f4 av[VT][NJ], ag[GT][NJ];
 #pragma unroll
@@ -416,19 +425,19 @@ __global__ void __launch_bounds__(256) gated_conv_kernel(GatedConvArgs f) {
     for (int j = 0; j < NJ; ++j) ag[t][j] = f4{0.f, 0.f, 0.f, 0.f};
 
   constexpr int D = 4;
-  w4 ra[D][kFA], rg[D], rv[D];
-  auto fetch = [&](int s, w4 (&a)[kFA], w4& g, w4& v) {
+  w4 ra[D][kFA], rb[D][kFB];
+  auto fetch = [&](int s, w4 (&a)[kFA], w4 (&b)[kFB]) {
 #pragma unroll
     for (int q = 0; q < kFA; ++q) a[q] = ga[q][4 * s];
-    g = gbg[4 * s];
-    v = gbv[4 * s];
+#pragma unroll
+    for (int q = 0; q < kFB; ++q) b[q] = gb[q][4 * s];
   };
-  auto stage = [&](int buf, const w4 (&a)[kFA], const w4& g, const w4& v) {
+  auto stage = [&](int buf, const w4 (&a)[kFA], const w4 (&b)[kFB]) {
     unsigned short* S = stg[buf];
 #pragma unroll
     for (int q = 0; q < kFA; ++q) *reinterpret_cast<w4*>(&S[la[q]]) = a[q] & am[q];  // zero outside the image
-    *reinterpret_cast<w4*>(&S[SA + lb]) = g;
-    *reinterpret_cast<w4*>(&S[SA + SB + lb]) = v;
+#pragma unroll
+    for (int q = 0; q < kFB; ++q) *reinterpret_cast<w4*>(&S[lb[q]]) = b[q];
   };
   auto frag = [&](const unsigned short* S, int row) {
     return OP::get(*reinterpret_cast<const w4*>(&S[row * kPitch + 8 * (kq ^ kSwz(row))]));
@@ -436,8 +445,8 @@ __global__ void __launch_bounds__(256) gated_conv_kernel(GatedConvArgs f) {
   const int steps = f.d / 32;
 #pragma unroll
   for (int q = 0; q < D; ++q)
-    if (q < steps) fetch(q, ra[q], rg[q], rv[q]);
-  stage(0, ra[0], rg[0], rv[0]);
+    if (q < steps) fetch(q, ra[q], rb[q]);
+  stage(0, ra[0], rb[0]);
   __syncthreads();
   for (int sb = 0; sb < steps; sb += D) {
 #pragma unroll
@@ -445,7 +454,7 @@ __global__ void __launch_bounds__(256) gated_conv_kernel(GatedConvArgs f) {
       const int s = sb + q;
       if (s < steps) {
         const unsigned short* S = stg[s & 1];
-        if (s + D < steps) fetch(s + D, ra[q], rg[q], rv[q]);  // slot q was staged before this step
+        if (s + D < steps) fetch(s + D, ra[q], rb[q]);  // slot q was staged before this step
         typename OP::T fg[NJ], fv[NJ];
 #pragma unroll
         for (int j = 0; j < NJ; ++j) {
@@ -465,7 +474,7 @@ __global__ void __launch_bounds__(256) gated_conv_kernel(GatedConvArgs f) {
 #pragma unroll
           for (int j = 0; j < NJ; ++j) ag[t][j] = mfma(fg[j], fa, ag[t][j]);  // G^T tiles
         }
-        if (s + 1 < steps) stage((s & 1) ^ 1, ra[(q + 1) % D], rg[(q + 1) % D], rv[(q + 1) % D]);
+        if (s + 1 < steps) stage((s & 1) ^ 1, ra[(q + 1) % D], rb[(q + 1) % D]);
         __syncthreads();
       }
     }
@@ -479,7 +488,7 @@ __global__ void __launch_bounds__(256) gated_conv_kernel(GatedConvArgs f) {
   // unswizzled, the writes of rows r, r + 2, r + 4, ... hit the same banks.
   _Float16* Vt = reinterpret_cast<_Float16*>(&stg[0][0]);
   _Float16* Gt = Vt + kFVT * 16 * kFN;
-  auto eswz = [](int row) { return (row >> 1) & 7; };
+  auto eswz = [](int row) { return (row >> 1) & (kFP - 1); };
 #pragma unroll
   for (int t = 0; t < VT; ++t)
 #pragma unroll
@@ -498,8 +507,8 @@ __global__ void __launch_bounds__(256) gated_conv_kernel(GatedConvArgs f) {
     }
   __syncthreads();
 
-  // gated convolution: 8 channels (piece pc) of 4 tile tokens per thread
-  const int pc = tid & 7, tg = tid >> 3;
+  // gated convolution: 8 channels (piece pc) of kFH kFW kFP / 256 tile tokens per thread
+  const int pc = tid & (kFP - 1), tg = tid / kFP;
   float wt[72];  // wt[9 e + 3 u + v]: tap (u, v) of channel 8 pc + e
 #pragma unroll
   for (int q = 0; q < 18; ++q) {
@@ -510,8 +519,8 @@ __global__ void __launch_bounds__(256) gated_conv_kernel(GatedConvArgs f) {
   const f4 blo = reinterpret_cast<const f4*>(wsm + kFN * 9 + 8 * pc)[0];
   const f4 bhi = reinterpret_cast<const f4*>(wsm + kFN * 9 + 8 * pc)[1];
 #pragma unroll
-  for (int m = 0; m < kFH * kFW / 32; ++m) {
-    const int ct = tg + 32 * m, ci = ct / kFW, cj = ct % kFW;
+  for (int m = 0; m < kFH * kFW * kFP / 256; ++m) {
+    const int ct = tg + 256 / kFP * m, ci = ct / kFW, cj = ct % kFW;
     float acc[8];
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
@@ -539,18 +548,21 @@ __global__ void __launch_bounds__(256) gated_conv_kernel(GatedConvArgs f) {
   }
 }
 
-// The output product uses 128 x 64 work-group tiles (d is small next to
-// hidden) and splits K into the fewest slices that give 128 work-groups when
-// M x d alone does not: every slice costs a float32 partial product and its
-// share of the reduction. Measured at GTR-L width, one image (product +
-// reduction, microseconds), with a K loop that waited for all its loads at
-// every step: 128 x 64 tiles with 1 / 2 / 4 / 8 slices 21.5 / 16.5 / 15.8 /
-// 17.1, 128 x 128 tiles 20.7 / 19.0 / 16.5 / 18.7; with the pipelined K loop,
-// the whole Spatial SwiGLU at 78 / 156 / 312 work-groups (1 / 2 / 4 slices)
-// 32.2 / 30.0 / 30.9 at GTR-L and 46.2 / 41.4 / 42.5 at GTR-X.
-constexpr int kOutBN = 64;
+// Both products on gemm_nt_kernel (the Spatial SwiGLU's output product and
+// gtr_gemm) use 64 x 64 work-group tiles (4 waves of 32 x 32). The K loop of a
+// work-group is a chain of dependent steps, so at the token counts of one or a
+// few images the number of work-groups sets the time more than the operand
+// reuse of a larger tile. Measured at one 40x40 image (us): the output product
+// 1600 x 384 x 1536 alone 10.3 with 64 x 64 tiles (150 work-groups) against
+// 15.1 with 128 x 64 (78); the whole Spatial SwiGLU 27.3 against 30.4 (128 x 64
+// tiles with K split in 2 and the reduction) at GTR-L and 40.5 against 41.3 at
+// GTR-X; 32 x 64 tiles 28.9 / 42.2; at 3200 and 12800 tokens the two tile
+// sizes are on par. K is split into the fewest slices that give 128 work-groups
+// when M x d alone does not (small grids only): every slice costs a float32
+// partial product and its share of the reduction.
+constexpr int kGemmBM = 64, kGemmBN = 64;
 static int out_ksplit(int64_t M, int d, int hidden) {
-  const int64_t wgs = ((M + 127) / 128) * (d / kOutBN);
+  const int64_t wgs = ((M + kGemmBM - 1) / kGemmBM) * (d / kGemmBN);
   int s = 1;
   while (wgs * s < 128 && s < 8 && hidden / 64 >= 2 * s * KB) s *= 2;
   return s;
@@ -583,7 +595,7 @@ static gtr_status swiglu_check(const gtr_swiglu_args* a, int64_t* M_out, bool ch
     return GTR_ERR_SHAPE;
   // both launches number their work-groups with 32-bit ints
   const int64_t tiles = (int64_t)a->B * ((a->H + kFH - 1) / kFH) * ((a->W + kFW - 1) / kFW);
-  if (tiles * (a->hidden / kFN) > 0x7fffffff || ((M + 127) / 128) * (a->d / kOutBN) * 8 > 0x7fffffff)
+  if (tiles * (a->hidden / kFN) > 0x7fffffff || ((M + kGemmBM - 1) / kGemmBM) * (a->d / kGemmBN) * 8 > 0x7fffffff)
     return GTR_ERR_SHAPE;
   *M_out = M;
   if (!check_pointers) return GTR_OK;
@@ -654,11 +666,11 @@ extern "C" gtr_status gtr_spatial_swiglu(const gtr_swiglu_args* a, hipStream_t s
   const int ks = out_ksplit(M, a->d, a->hidden);
   float* part = reinterpret_cast<float*>(ws + lay.part_off);
   GemmArgs g3{Hb, a->w_out, a->y, part, (int)M, a->d, a->hidden, a->y_dtype, ks, nullptr, ks == 1 ? a->residual : nullptr};
-  const dim3 grid3((unsigned)(((M + 127) / 128) * (a->d / kOutBN) * ks));
+  const dim3 grid3((unsigned)(((M + kGemmBM - 1) / kGemmBM) * (a->d / kGemmBN) * ks));
   if (bf)
-    hipLaunchKernelGGL((gemm_nt_kernel<GTR_F16, GTR_BF16, GTR_F16, 128, kOutBN>), grid3, dim3(256), 0, stream, g3);
+    hipLaunchKernelGGL((gemm_nt_kernel<GTR_F16, GTR_BF16, GTR_F16, kGemmBM, kGemmBN>), grid3, dim3(256), 0, stream, g3);
   else
-    hipLaunchKernelGGL((gemm_nt_kernel<GTR_F16, GTR_F16, GTR_F16, 128, kOutBN>), grid3, dim3(256), 0, stream, g3);
+    hipLaunchKernelGGL((gemm_nt_kernel<GTR_F16, GTR_F16, GTR_F16, kGemmBM, kGemmBN>), grid3, dim3(256), 0, stream, g3);
   if (hipGetLastError() != hipSuccess) return GTR_ERR_HIP;
   if (ks > 1) {
     const int64_t n4 = M * a->d / 4;
@@ -669,7 +681,7 @@ extern "C" gtr_status gtr_spatial_swiglu(const gtr_swiglu_args* a, hipStream_t s
 }
 
 // ---------------------------------------------------------------------------
-// gtr_gemm: C = A B^T (+ bias) (+ res) on gemm_nt_kernel, 128 x 64 tiles, no
+// gtr_gemm: C = A B^T (+ bias) (+ res) on gemm_nt_kernel, 64 x 64 tiles, no
 // K split (the block's products have K = d or 64).
 // ---------------------------------------------------------------------------
 static gtr_status gemm_check(const gtr_gemm_args* a) {
@@ -682,7 +694,8 @@ static gtr_status gemm_check(const gtr_gemm_args* a) {
   }
   if ((a->a_dtype != GTR_F16 && a->a_dtype != GTR_BF16) || a->b_dtype != a->a_dtype) return GTR_ERR_UNSUPPORTED;
   if (a->c_dtype != GTR_F16 && a->c_dtype != GTR_BF16 && a->c_dtype != GTR_F32) return GTR_ERR_UNSUPPORTED;
-  if (a->M > 0x7fffffff - 128 || ((a->M + 127) / 128) * (a->N / 64) > 0x7fffffff) return GTR_ERR_SHAPE;
+  if (a->M > 0x7fffffff - 128 || ((a->M + kGemmBM - 1) / kGemmBM) * (a->N / kGemmBN) > 0x7fffffff)
+    return GTR_ERR_SHAPE;
   if (!a->a || !a->b || !a->c) return GTR_ERR_NULL;
   const uintptr_t mis = reinterpret_cast<uintptr_t>(a->a) | reinterpret_cast<uintptr_t>(a->b) |
                         reinterpret_cast<uintptr_t>(a->c) | reinterpret_cast<uintptr_t>(a->bias) |
@@ -708,10 +721,10 @@ extern "C" gtr_status gtr_gemm(const gtr_gemm_args* a, hipStream_t stream) {
   if (st != GTR_OK) return st;
   GemmArgs g{a->a, a->b, a->c, nullptr, (int)a->M, a->N, a->K, (int)a->c_dtype, 1, a->bias, a->res,
              a->a_tokens, a->c_tokens, a->c_tokens ? a->c_heads : 0, a->c_tokens ? a->c_head_dim : 0};
-  const dim3 grid((unsigned)(((a->M + 127) / 128) * (a->N / 64)));
+  const dim3 grid((unsigned)(((a->M + kGemmBM - 1) / kGemmBM) * (a->N / kGemmBN)));
   if (a->a_dtype == GTR_BF16)
-    hipLaunchKernelGGL((gemm_nt_kernel<GTR_BF16, GTR_BF16, GTR_BF16, 128, 64>), grid, dim3(256), 0, stream, g);
+    hipLaunchKernelGGL((gemm_nt_kernel<GTR_BF16, GTR_BF16, GTR_BF16, kGemmBM, kGemmBN>), grid, dim3(256), 0, stream, g);
   else
-    hipLaunchKernelGGL((gemm_nt_kernel<GTR_F16, GTR_F16, GTR_F16, 128, 64>), grid, dim3(256), 0, stream, g);
+    hipLaunchKernelGGL((gemm_nt_kernel<GTR_F16, GTR_F16, GTR_F16, kGemmBM, kGemmBN>), grid, dim3(256), 0, stream, g);
   return hipGetLastError() == hipSuccess ? GTR_OK : GTR_ERR_HIP;
 }

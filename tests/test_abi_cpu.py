@@ -329,12 +329,14 @@ def test_swiglu_workspace_size(lib):
     M = 2 * 1600
     a256 = lambda x: (x + 255) // 256 * 256
     # H in fp16 (G and V stay on chip); the output product splits K only when
-    # its 128 x 64 tiles give fewer than 128 work-groups: 25 x 6 = 150 do not
+    # its 64 x 64 tiles give fewer than 128 work-groups: 50 x 6 = 300 do not
     base = a256(M * 1536 * 2)
     assert lib.gtr_spatial_swiglu_workspace_size(ctypes.byref(a)) == base
-    one = swiglu_args(B=1, H=40, W=40, d=384, hidden=1536)  # 13 x 6 work-groups: 2 slices
-    assert lib.gtr_spatial_swiglu_workspace_size(ctypes.byref(one)) == \
-        a256(a256(1600 * 1536 * 2) + 2 * 1600 * 384 * 4)
+    one = swiglu_args(B=1, H=40, W=40, d=384, hidden=1536)  # 25 x 6 work-groups: no split
+    assert lib.gtr_spatial_swiglu_workspace_size(ctypes.byref(one)) == a256(1600 * 1536 * 2)
+    small = swiglu_args(B=1, H=16, W=16, d=384, hidden=1536)  # 4 x 6 work-groups: 4 slices
+    assert lib.gtr_spatial_swiglu_workspace_size(ctypes.byref(small)) == \
+        a256(a256(256 * 1536 * 2) + 4 * 256 * 384 * 4)
     big = swiglu_args(B=8, H=40, W=40, d=384, hidden=1536)  # 100 x 6 work-groups: no split
     assert lib.gtr_spatial_swiglu_workspace_size(ctypes.byref(big)) == a256(12800 * 1536 * 2)
 

@@ -13,6 +13,7 @@ from __future__ import annotations
 
 import hashlib
 import os
+import re
 import shutil
 import struct
 import subprocess
@@ -491,9 +492,9 @@ def test_swiglu_gemm_addresses(adt, bdt, mt, bn, M, N, K, cdt, ks, epi):
     ct = (M // 2 if M % 2 == 0 else M) if epi & 8 else 0
     kern = struct.pack("<QQQQiiiii4xQQqqii", A, B, C, P, M, N, K, cdt, ks, BI if epi & 1 else 0,
                        R if epi & 2 else 0, at, ct, 6 if ct else 0, 64 if ct else 0)
-    name = f"_ZN3gtr14gemm_nt_kernelILi{adt}ELi{bdt}ELi{mt}ELi128ELi{bn}EEEvNS_8GemmArgsE"
+    name = f"_ZN3gtr14gemm_nt_kernelILi{adt}ELi{bdt}ELi{mt}ELi64ELi{bn}EEEvNS_8GemmArgsE"
     assert name in emu.kernel_names(text)
-    gx, gy = (M + 127) // 128, N // bn
+    gx, gy = (M + 63) // 64, N // bn
     T = gx * gy * ks
 
     def block_of(x, y, z):
@@ -525,8 +526,10 @@ def test_swiglu_gated_conv_addresses(dt, B, H, W, d, hidden):
                emu.Region("kernarg", emu.KERNARG_BASE, 64, "r")]
     kern = struct.pack("<QQQQQQiiiii4x", X, WG, WV, CW, CB, HO, H, W, d, hidden, B)
     name = [n for n in emu.kernel_names(text) if "gated_conv_kernel" in n and f"ILi{dt}E" in n][0]
-    tx, ty = (W + 15) // 16, (H + 7) // 8  # one work-group per 8 x 16 tokens x 64 channels
-    nt, nc = B * tx * ty, hidden // 64
+    with open(os.path.join(CSRC, "swiglu.hip")) as fh:
+        fn = int(re.search(r"constexpr int kFN = (\d+);", fh.read()).group(1))
+    tx, ty = (W + 15) // 16, (H + 7) // 8  # one work-group per 8 x 16 tokens x kFN channels
+    nt, nc = B * tx * ty, hidden // fn
     T = nt * nc
 
     def block_of(tile, cb):

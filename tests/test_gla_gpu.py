@@ -647,6 +647,7 @@ SWIGLU = [
     (2, 7, 9, 64, 128, "f16", "f32", False),        # odd grid, partial 64-row tile, B = 2
     (1, 1, 1, 64, 64, "bf16", "bf16", True),        # a single token: every neighbour is padding
     (1, 16, 16, 192, 768, "f16", "f16", True),      # GTR-S width
+    (1, 16, 16, 384, 1536, "f16", "f16", True),     # GTR-L width on a small grid: the output product in 4 K slices
     (2, 17, 35, 128, 192, "bf16", "f32", True),     # 3 x 3 token tiles, both edges partial, halos across tiles
 ]
 
