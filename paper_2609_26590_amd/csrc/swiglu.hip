@@ -128,16 +128,22 @@ __device__ __forceinline__ int kSwz(int r) { return (r >> 2) & 2; }
 constexpr int kPitch64 = 64;
 __device__ __forceinline__ int kSwz64(int r) { return ((r >> 2) & 3) << 1; }
 
-template <int ADT, int BDT, int MT, int BM, int BN>
-__global__ void __launch_bounds__(256) gemm_nt_kernel(GemmArgs g) {
+template <int ADT, int BDT, int MT, int BM, int BN, int KW>
+__global__ void __launch_bounds__(256 * KW) gemm_nt_kernel(GemmArgs g) {
   typedef Operand<ADT, MT> OA;
   typedef Operand<BDT, MT> OB;
+  constexpr int NT = 256 * KW;                // threads
   constexpr int TI = BM / 32, TJ = BN / 32;   // MFMA tiles per wave
-  constexpr int PA = BM * 8 / 256, PB = BN * 8 / 256;  // 16-byte pieces per thread per step
+  constexpr int PA = BM * 8 / NT, PB = BN * 8 / NT;  // 16-byte pieces per thread per step
+  static_assert((KW == 1 || KW == 2) && PA >= 1 && PB >= 1 && BM * 8 % NT == 0 && BN * 8 % NT == 0,
+                "tiles split evenly over the threads");
+  static_assert(KW == 1 || BM * BN * 4 <= 2 * BM * kPitch64 * 2, "the K halves' partial sums fit in As");
   __shared__ __attribute__((aligned(16))) unsigned short As[2][BM * kPitch64];
   __shared__ __attribute__((aligned(16))) unsigned short Bs[2][BN * kPitch64];
 
-  const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  // wave w of the 2 x 2 grid over the tile; with KW = 2 the waves kh = 0 and
+  // kh = 1 take the first and the second 32-deep half of every K step
+  const int w = (threadIdx.x >> 6) & 3, kh = threadIdx.x >> 8, lane = threadIdx.x & 63;
   const int r16 = lane & 15, kq = lane >> 4;
   // tile of this work-group: XCD k = b % 8 takes positions [start_k, start_k +
   // count_k) of the tile order, count_k = ceil((T - k) / 8)
@@ -161,7 +167,7 @@ __global__ void __launch_bounds__(256) gemm_nt_kernel(GemmArgs g) {
   int la[PA], lb[PB];
 #pragma unroll
   for (int q = 0; q < PA; ++q) {
-    const int p = threadIdx.x + 256 * q, row = p >> 3, col = p & 7;
+    const int p = threadIdx.x + NT * q, row = p >> 3, col = p & 7;
     const unsigned m = (unsigned)min(mb + row, g.M - 1), at = g.a_tokens ? (unsigned)g.a_tokens : 1u;
     ga[q] = reinterpret_cast<const w4*>(
         A + (g.a_tokens ? ((int64_t)(m / at) * (K / 64) * at + m % at) * 64 : (int64_t)m * K) + 8 * col);
@@ -169,7 +175,7 @@ __global__ void __launch_bounds__(256) gemm_nt_kernel(GemmArgs g) {
   }
 #pragma unroll
   for (int q = 0; q < PB; ++q) {
-    const int p = threadIdx.x + 256 * q, row = p >> 3, col = p & 7;
+    const int p = threadIdx.x + NT * q, row = p >> 3, col = p & 7;
     gb[q] = reinterpret_cast<const w4*>(B + (int64_t)(nb + row) * K + 8 * col);
     lb[q] = row * kPitch64 + 8 * (col ^ kSwz64(row));
   }
@@ -199,7 +205,8 @@ __global__ void __launch_bounds__(256) gemm_nt_kernel(GemmArgs g) {
   };
   auto mma = [&](int buf) {
 #pragma unroll
-    for (int h = 0; h < 2; ++h) {  // the two 32-deep halves of the step
+    for (int hh = 0; hh < 2 / KW; ++hh) {  // the 32-deep halves of the step this wave takes
+      const int h = KW == 1 ? hh : kh;
       const int pc = (4 * h + kq) ^ kSwz64(r16);
       typename OA::T fa[TI];
       typename OB::T fb[TJ];
@@ -246,6 +253,23 @@ __global__ void __launch_bounds__(256) gemm_nt_kernel(GemmArgs g) {
         __syncthreads();
       }
     }
+  }
+
+  if (KW == 2) {  // the second K half's sums join the first's through LDS
+    f4* red = reinterpret_cast<f4*>(&As[0][0]);
+    __syncthreads();  // every wave is past the K loop's last LDS read
+    if (kh == 1) {
+#pragma unroll
+      for (int i = 0; i < TI; ++i)
+#pragma unroll
+        for (int j = 0; j < TJ; ++j) red[((w * TI + i) * TJ + j) * 64 + lane] = acc[i][j];
+    }
+    __syncthreads();
+    if (kh == 1) return;
+#pragma unroll
+    for (int i = 0; i < TI; ++i)
+#pragma unroll
+      for (int j = 0; j < TJ; ++j) acc[i][j] += red[((w * TI + i) * TJ + j) * 64 + lane];
   }
 
   // lane holds C[row 16i + r16][columns 16j + 4kq .. 16j + 4kq + 3] of this
@@ -561,6 +585,23 @@ __global__ void __launch_bounds__(256) gated_conv_kernel(GatedConvArgs f) {
 // when M x d alone does not (small grids only): every slice costs a float32
 // partial product and its share of the reduction.
 constexpr int kGemmBM = 64, kGemmBN = 64;
+
+// A grid of fewer tiles than the chip's 256 compute units leaves CUs idle, and
+// each work-group's K loop is a chain of dependent steps: there, 8 waves per
+// tile (the two 32-deep halves of every K step on separate waves, their sums
+// joined through LDS at the end) run the chain faster. Larger grids keep 4
+// waves per tile. Measured (us): 1600 x 384 x 1536 (150 tiles) 9.5 against
+// 10.1, 1600 x 384 x 384 5.0 against 5.3, the Spatial SwiGLU 26.4 / 38.5
+// against 27.2 / 40.6 (GTR-L / GTR-X); 1600 x 1920 x 384 (750 tiles) 10.8
+// against 9.3, 12800 x 384 x 1536 37.4 against 36.5.
+constexpr int kKHalvesBelow = 256;
+template <int ADT, int BDT, int MT>
+static void launch_gemm(const GemmArgs& g, unsigned tiles, hipStream_t stream) {
+  if (tiles < (unsigned)kKHalvesBelow)
+    hipLaunchKernelGGL((gemm_nt_kernel<ADT, BDT, MT, kGemmBM, kGemmBN, 2>), dim3(tiles), dim3(512), 0, stream, g);
+  else
+    hipLaunchKernelGGL((gemm_nt_kernel<ADT, BDT, MT, kGemmBM, kGemmBN, 1>), dim3(tiles), dim3(256), 0, stream, g);
+}
 static int out_ksplit(int64_t M, int d, int hidden) {
   const int64_t wgs = ((M + kGemmBM - 1) / kGemmBM) * (d / kGemmBN);
   int s = 1;
@@ -666,11 +707,11 @@ extern "C" gtr_status gtr_spatial_swiglu(const gtr_swiglu_args* a, hipStream_t s
   const int ks = out_ksplit(M, a->d, a->hidden);
   float* part = reinterpret_cast<float*>(ws + lay.part_off);
   GemmArgs g3{Hb, a->w_out, a->y, part, (int)M, a->d, a->hidden, a->y_dtype, ks, nullptr, ks == 1 ? a->residual : nullptr};
-  const dim3 grid3((unsigned)(((M + kGemmBM - 1) / kGemmBM) * (a->d / kGemmBN) * ks));
+  const unsigned tiles3 = (unsigned)(((M + kGemmBM - 1) / kGemmBM) * (a->d / kGemmBN) * ks);
   if (bf)
-    hipLaunchKernelGGL((gemm_nt_kernel<GTR_F16, GTR_BF16, GTR_F16, kGemmBM, kGemmBN>), grid3, dim3(256), 0, stream, g3);
+    launch_gemm<GTR_F16, GTR_BF16, GTR_F16>(g3, tiles3, stream);
   else
-    hipLaunchKernelGGL((gemm_nt_kernel<GTR_F16, GTR_F16, GTR_F16, kGemmBM, kGemmBN>), grid3, dim3(256), 0, stream, g3);
+    launch_gemm<GTR_F16, GTR_F16, GTR_F16>(g3, tiles3, stream);
   if (hipGetLastError() != hipSuccess) return GTR_ERR_HIP;
   if (ks > 1) {
     const int64_t n4 = M * a->d / 4;
@@ -721,10 +762,10 @@ extern "C" gtr_status gtr_gemm(const gtr_gemm_args* a, hipStream_t stream) {
   if (st != GTR_OK) return st;
   GemmArgs g{a->a, a->b, a->c, nullptr, (int)a->M, a->N, a->K, (int)a->c_dtype, 1, a->bias, a->res,
              a->a_tokens, a->c_tokens, a->c_tokens ? a->c_heads : 0, a->c_tokens ? a->c_head_dim : 0};
-  const dim3 grid((unsigned)(((a->M + kGemmBM - 1) / kGemmBM) * (a->N / kGemmBN)));
+  const unsigned tiles = (unsigned)(((a->M + kGemmBM - 1) / kGemmBM) * (a->N / kGemmBN));
   if (a->a_dtype == GTR_BF16)
-    hipLaunchKernelGGL((gemm_nt_kernel<GTR_BF16, GTR_BF16, GTR_BF16, kGemmBM, kGemmBN>), grid, dim3(256), 0, stream, g);
+    launch_gemm<GTR_BF16, GTR_BF16, GTR_BF16>(g, tiles, stream);
   else
-    hipLaunchKernelGGL((gemm_nt_kernel<GTR_F16, GTR_F16, GTR_F16, kGemmBM, kGemmBN>), grid, dim3(256), 0, stream, g);
+    launch_gemm<GTR_F16, GTR_F16, GTR_F16>(g, tiles, stream);
   return hipGetLastError() == hipSuccess ? GTR_OK : GTR_ERR_HIP;
 }

@@ -475,7 +475,10 @@ def check_kernel(text, name, kern, regions, wgs, waves=4):
                                                             # head-major operands (the block's projections)
                                                             (1, 1, 1, 64, 1600, 1536, 384, 1, 1, 8),
                                                             (1, 1, 1, 64, 3200, 384, 384, 1, 1, 6),
-                                                            (2, 2, 2, 64, 414, 384, 64, 2, 1, 9)])
+                                                            (2, 2, 2, 64, 414, 384, 64, 2, 1, 9),
+                                                            # 4 waves per tile at 256 tiles and more
+                                                            (2, 2, 2, 64, 3200, 384, 64, 2, 1, 1),
+                                                            (1, 2, 1, 64, 4096, 384, 128, 0, 1, 0)])
 def test_swiglu_gemm_addresses(adt, bdt, mt, bn, M, N, K, cdt, ks, epi):
     """epi: bit 0 a bias, bit 1 a residual (gtr_gemm's epilogue), bits 2 / 3 head-major A / C."""
     text = swiglu_asm()
@@ -492,7 +495,9 @@ def test_swiglu_gemm_addresses(adt, bdt, mt, bn, M, N, K, cdt, ks, epi):
     ct = (M // 2 if M % 2 == 0 else M) if epi & 8 else 0
     kern = struct.pack("<QQQQiiiii4xQQqqii", A, B, C, P, M, N, K, cdt, ks, BI if epi & 1 else 0,
                        R if epi & 2 else 0, at, ct, 6 if ct else 0, 64 if ct else 0)
-    name = f"_ZN3gtr14gemm_nt_kernelILi{adt}ELi{bdt}ELi{mt}ELi64ELi{bn}EEEvNS_8GemmArgsE"
+    # 8 waves per tile below 256 tiles (the K halves on separate waves), 4 above
+    kw = 2 if ((M + 63) // 64) * (N // bn) * ks < 256 else 1
+    name = f"_ZN3gtr14gemm_nt_kernelILi{adt}ELi{bdt}ELi{mt}ELi64ELi{bn}ELi{kw}EEEvNS_8GemmArgsE"
     assert name in emu.kernel_names(text)
     gx, gy = (M + 63) // 64, N // bn
     T = gx * gy * ks
@@ -510,7 +515,7 @@ def test_swiglu_gemm_addresses(adt, bdt, mt, bn, M, N, K, cdt, ks, epi):
     ids = sorted({block_of(x, y, z) for x in sorted({0, gx - 1}) for y in sorted({0, gy - 1})
                   for z in sorted({0, ks - 1})})
     assert all(0 <= b < T for b in ids)
-    check_kernel(text, name, kern, regions, [(b, 0, 0) for b in ids])
+    check_kernel(text, name, kern, regions, [(b, 0, 0) for b in ids], waves=4 * kw)
 
 
 @pytest.mark.parametrize("dt,B,H,W,d,hidden", [(1, 2, 7, 9, 64, 128), (2, 1, 40, 40, 384, 192),
