@@ -321,6 +321,13 @@ gtr_status gtr_spatial_swiglu(const gtr_swiglu_args* args, hipStream_t stream);
  * bias    : [N] float32 added to every row, or NULL
  * res     : [M, N] in c_dtype added elementwise (a residual), or NULL; may be c
  *           itself (in place), must not overlap it otherwise
+ * row_norm: 0, or 1 to normalise every row of a over its K columns first:
+ *           C = ((A - mu) / sqrt(var + row_norm_eps)) B^T (+ bias) (+ res),
+ *           mu and var the mean and biased variance of the row (float32). A
+ *           layer normalisation with weights gamma, beta before a linear layer
+ *           W, bias c is this call with b = W diag(gamma) and bias = c + W beta
+ *           (Sec. 3.1's pre-norm block). Needs a row-major a (a_tokens 0) and
+ *           0 <= row_norm_eps < 1e30.
  * N and K multiples of 64, every pointer 16-byte aligned. The products
  * accumulate in float32 (MFMA on the input dtype) and are rounded once into c.
  * Errors as for gtr_gla_fwd; every check runs before the launch.
@@ -341,6 +348,8 @@ typedef struct {
                           [c_head_dim] (projections split into heads as they are stored; M a multiple of
                           c_tokens, N of c_heads c_head_dim, c_head_dim of 4, res NULL) */
   int32_t c_heads, c_head_dim;
+  float row_norm_eps;  /* the row normalisation's epsilon (row_norm 1) */
+  int32_t row_norm;    /* 0, or 1: normalise the rows of a (above) */
 } gtr_gemm_args;
 
 gtr_status gtr_gemm(const gtr_gemm_args* args, hipStream_t stream);

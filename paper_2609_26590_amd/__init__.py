@@ -86,7 +86,7 @@ class GemmArgs(ctypes.Structure):
         ("res", ctypes.c_void_p), ("a_dtype", ctypes.c_int), ("b_dtype", ctypes.c_int), ("c_dtype", ctypes.c_int),
         ("M", ctypes.c_int64), ("N", ctypes.c_int32), ("K", ctypes.c_int32),
         ("a_tokens", ctypes.c_int64), ("c_tokens", ctypes.c_int64), ("c_heads", ctypes.c_int32),
-        ("c_head_dim", ctypes.c_int32),
+        ("c_head_dim", ctypes.c_int32), ("row_norm_eps", ctypes.c_float), ("row_norm", ctypes.c_int32),
     ]
 
 
@@ -416,9 +416,14 @@ def _dev_contig(name: str, t: torch.Tensor) -> None:
 
 def gtr_gemm(a: torch.Tensor, b: torch.Tensor, *, bias: Optional[torch.Tensor] = None,
              res: Optional[torch.Tensor] = None, out_dtype: Optional[torch.dtype] = None,
-             out: Optional[torch.Tensor] = None, heads_out: Optional[tuple] = None, stream=None) -> torch.Tensor:
+             out: Optional[torch.Tensor] = None, heads_out: Optional[tuple] = None,
+             row_norm_eps: Optional[float] = None, stream=None) -> torch.Tensor:
     """c = a b^T (+ bias) (+ res): a [M, K], b [N, K] (fp16 or bf16, same dtype),
     bias [N] float32, res [M, N] in the output dtype (may be ``out``).
+
+    ``row_norm_eps`` set: every row of a is first normalised over its K
+    columns, (a - mean) / sqrt(var + row_norm_eps) (a layer normalisation whose
+    weights the caller folds into b and bias).
 
     a may also be head-major [B, K / 64, L, 64] (a head concat read in place:
     M = B * L). ``heads_out = (L, heads, dh)`` stores c head-major as
@@ -451,6 +456,8 @@ def gtr_gemm(a: torch.Tensor, b: torch.Tensor, *, bias: Optional[torch.Tensor] =
     g.a_dtype, g.b_dtype, g.c_dtype = _DT[a.dtype], _DT[b.dtype], _DT[c.dtype]
     g.M, g.N, g.K = M, N, K
     g.a_tokens = a_tokens
+    if row_norm_eps is not None:
+        g.row_norm, g.row_norm_eps = 1, float(row_norm_eps)
     if heads_out is not None:
         g.c_tokens, g.c_heads, g.c_head_dim = heads_out
     st = load().gtr_gemm(ctypes.byref(g), _stream_ptr(stream))

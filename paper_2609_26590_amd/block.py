@@ -1,8 +1,9 @@
 """One GTR block (paper Sec. 3.1) as a sequence of libgtr calls.
 
-    n1 = LN1(x)                                   gtr_layernorm
-    [q k v z a] = n1 [W_qkvr; W_a]^T + [0; b_a]   one gtr_gemm, stored head-major (W_a = W_a2 W_a1: the
-                                                  low-rank gate's factors multiplied once, in ``prepare``)
+    [q k v z a] = LN1(x) [W_qkvr; W_a]^T + [0; b_a]   one gtr_gemm that normalises the rows of x inside the
+                                                  product (LN1's weights folded into the matrix and the bias
+                                                  in ``prepare``), stored head-major; W_a = W_a2 W_a1, the
+                                                  low-rank gate's factors multiplied once in ``prepare``
     u = SiLU(z) * RMSNorm(GLA(q, k, v; a))        gtr_gla_fwd: gate fusion (tau) and the output-gate epilogue
     x1 = x + concat_heads(u) W_o^T                gtr_gemm reading u head-major, the residual in its epilogue
     x2 = x1 + SpatialSwiGLU(LN2(x1))              gtr_layernorm, gtr_spatial_swiglu with the residual
@@ -13,7 +14,10 @@ the paper (it names the parts of the block, not their order): pre-norm layer
 normalisation before the token mixer and before the Spatial SwiGLU, a residual
 around each. The gate's rank-16 factors are multiplied into one d x d matrix
 when the weights are prepared: the same logits in real arithmetic, with the
-product's fp16 rounding in place of the rank-16 intermediate's.
+product's fp16 rounding in place of the rank-16 intermediate's. LN1's weights
+gamma, beta are folded the usual way, LN1(x) W^T + c = norm(x) (W diag(gamma))^T
++ (c + W beta): the same values in real arithmetic, with the folded matrix
+rounded to the input dtype in place of the rounding of LN1(x).
 """
 from __future__ import annotations
 
@@ -25,11 +29,12 @@ GATE_PAD = 64
 
 
 def prepare(p: dict) -> dict:
-    """Device weights for ``forward`` (once per block): the gate's rank-16
-    factors multiplied into one d x d matrix W_a = W_a2 W_a1 (on the device,
-    through gtr_gemm, the rank zero-padded to 64) and appended to the
+    """Device weights for ``forward`` (once per block), all products through
+    gtr_gemm: the gate's rank-16 factors multiplied into one d x d matrix
+    W_a = W_a2 W_a1 (the rank zero-padded to 64) and appended to the
     projections as a fifth part, with the gate bias as that part's bias, so one
-    product gives q, k, v, z and the gate logits."""
+    product gives q, k, v, z and the gate logits; then LN1's weights folded
+    into that matrix and bias: W diag(gamma) and c + W beta."""
     r, d = p["w_a1"].shape
     dev, dt = p["w_a1"].device, p["w_a1"].dtype
     a2 = torch.zeros((d, GATE_PAD), dtype=dt, device=dev)
@@ -37,9 +42,13 @@ def prepare(p: dict) -> dict:
     a1t = torch.zeros((d, GATE_PAD), dtype=dt, device=dev)
     a1t[:, :r] = p["w_a1"].t()
     w_a = gtr_gemm(a2, a1t)  # [d, d] = W_a2 W_a1
+    w_proj = torch.cat([p["w_qkvr"], w_a]).contiguous()
+    b_proj = torch.cat([torch.zeros(4 * d, device=dev), p["b_a"].float()]).contiguous()
+    gamma = torch.diag(p["ln1_w"].float()).to(dt).contiguous()
     q = dict(p)
-    q["w_proj"] = torch.cat([p["w_qkvr"], w_a]).contiguous()
-    q["b_proj"] = torch.cat([torch.zeros(4 * d, device=dev), p["b_a"].float()]).contiguous()
+    q["w_proj"] = gtr_gemm(w_proj, gamma)  # W diag(gamma)
+    beta = p["ln1_b"].to(dt).reshape(1, d).contiguous()
+    q["b_proj"] = gtr_gemm(beta, w_proj, bias=b_proj, out_dtype=torch.float32).reshape(-1)  # c + W beta
     return q
 
 
@@ -51,9 +60,10 @@ def forward(x: torch.Tensor, p: dict, *, H: int, W: int, heads: int, scan: str, 
     dh = d // heads
     M = B * L
     x2d = x.reshape(M, d)
-    n1 = gtr_layernorm(x2d, p["ln1_w"], p["ln1_b"], eps=ln_eps, stream=stream)
-    # one product, stored head-major ([5, B, heads, L, dh]: q, k, v, z, gate logits)
-    proj = gtr_gemm(n1, p["w_proj"], bias=p["b_proj"], heads_out=(L, heads, dh), stream=stream)
+    # one product over the normalised rows of x, stored head-major ([5, B, heads, L, dh]: q, k, v, z and
+    # the gate logits)
+    proj = gtr_gemm(x2d, p["w_proj"], bias=p["b_proj"], heads_out=(L, heads, dh), row_norm_eps=ln_eps,
+                    stream=stream)
     u, _ = gtr_gla_fwd(proj[0], proj[1], proj[2], proj[4], H=H, W=W, scale=dh ** -0.5, scan=scan,
                        gate_tau=tau, out_gate=proj[3], norm_weight=p["norm_w"],
                        norm_eps=norm_eps, stream=stream)

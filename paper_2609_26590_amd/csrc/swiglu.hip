@@ -91,7 +91,25 @@ struct GemmArgs {
                       // m % a_tokens), K step s = head s (a head concat read in place)
   int64_t c_tokens;   // C is written [N / (c_heads c_dim)][M / c_tokens][c_heads][c_tokens][c_dim]
   int c_heads, c_dim;
+  float ln_eps;       // the row normalisation's epsilon (kernels with LN = 1)
+  int pad_;
 };
+
+// 8 consecutive 16-bit elements of dtype DT (one 16-byte piece) as floats.
+template <int DT>
+__device__ __forceinline__ void unpack_piece(const w4& v, float (&x)[8]) {
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    const unsigned u = v[e];
+    if (DT == GTR_F16) {
+      x[2 * e] = (float)__builtin_bit_cast(_Float16, (unsigned short)(u & 0xffffu));
+      x[2 * e + 1] = (float)__builtin_bit_cast(_Float16, (unsigned short)(u >> 16));
+    } else {
+      x[2 * e] = __builtin_bit_cast(float, u << 16);
+      x[2 * e + 1] = __builtin_bit_cast(float, u & 0xffff0000u);
+    }
+  }
+}
 
 // 4 consecutive elements of dtype dt at element offset off, as floats.
 __device__ __forceinline__ void load4(const void* base, int dt, int64_t off, float (&x)[4]) {
@@ -128,7 +146,16 @@ __device__ __forceinline__ int kSwz(int r) { return (r >> 2) & 2; }
 constexpr int kPitch64 = 64;
 __device__ __forceinline__ int kSwz64(int r) { return ((r >> 2) & 3) << 1; }
 
-template <int ADT, int BDT, int MT, int BM, int BN, int KW>
+// With LN = 1 every row of A is normalised over its K columns (A' = (A - mu)
+// / sqrt(var + eps), a layer normalisation without affine weights, which the
+// caller folds into B and the bias) inside the product: the MFMAs multiply the
+// raw A, the row sums and squares of A and the row sums of B (colsum of B^T)
+// are taken from the pieces as they pass through registers on their way to
+// LDS, and the epilogue forms rs_m (C_mn - mu_m colsum_n), which is A' B^T in
+// real arithmetic. The squares are taken about a shift (the row's first
+// element) so that a row mean large next to its spread costs no precision.
+// LN = 1 needs K in one slice and a row-major A.
+template <int ADT, int BDT, int MT, int BM, int BN, int KW, int LN>
 __global__ void __launch_bounds__(256 * KW) gemm_nt_kernel(GemmArgs g) {
   typedef Operand<ADT, MT> OA;
   typedef Operand<BDT, MT> OB;
@@ -140,6 +167,8 @@ __global__ void __launch_bounds__(256 * KW) gemm_nt_kernel(GemmArgs g) {
   static_assert(KW == 1 || BM * BN * 4 <= 2 * BM * kPitch64 * 2, "the K halves' partial sums fit in As");
   __shared__ __attribute__((aligned(16))) unsigned short As[2][BM * kPitch64];
   __shared__ __attribute__((aligned(16))) unsigned short Bs[2][BN * kPitch64];
+  __shared__ float lnst[LN ? 2 * BM : 1];  // per tile row: mean, 1 / sqrt(var + eps)
+  __shared__ float lncs[LN ? BN : 1];      // per tile column: the row sum of B
 
   // wave w of the 2 x 2 grid over the tile; with KW = 2 the waves kh = 0 and
   // kh = 1 take the first and the second 32-deep half of every K step
@@ -203,6 +232,35 @@ __global__ void __launch_bounds__(256 * KW) gemm_nt_kernel(GemmArgs g) {
 #pragma unroll
     for (int q = 0; q < PB; ++q) *reinterpret_cast<w4*>(&Bs[buf][lb[q]]) = b[q];
   };
+  // row statistics (LN = 1) of the steps staged so far: per piece of A the
+  // sum and the sum of squares about the row's shift, per piece of B its sum
+  float sh[PA], sa[PA], sq[PA], cb[PB];
+#pragma unroll
+  for (int q = 0; q < PA; ++q) sh[q] = sa[q] = sq[q] = 0.f;
+#pragma unroll
+  for (int q = 0; q < PB; ++q) cb[q] = 0.f;
+  auto stats = [&](const w4 (&a)[PA], const w4 (&b)[PB]) {
+    if constexpr (LN != 0) {
+#pragma unroll
+      for (int q = 0; q < PA; ++q) {
+        float x[8];
+        unpack_piece<ADT>(a[q], x);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          const float d = x[e] - sh[q];
+          sa[q] += d;
+          sq[q] = fmaf(d, d, sq[q]);
+        }
+      }
+#pragma unroll
+      for (int q = 0; q < PB; ++q) {
+        float x[8];
+        unpack_piece<BDT>(b[q], x);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) cb[q] += x[e];
+      }
+    }
+  };
   auto mma = [&](int buf) {
 #pragma unroll
     for (int hh = 0; hh < 2 / KW; ++hh) {  // the 32-deep halves of the step this wave takes
@@ -231,7 +289,16 @@ __global__ void __launch_bounds__(256 * KW) gemm_nt_kernel(GemmArgs g) {
   if (s1 > s0) {
 #pragma unroll
     for (int q = 0; q < D; ++q) fetch(min(s0 + q, s1 - 1), ra[q], rb[q]);
+    if constexpr (LN != 0) {  // the shift of each row: its first element, from the row's column-0 lane
+#pragma unroll
+      for (int q = 0; q < PA; ++q) {
+        float x[8];
+        unpack_piece<ADT>(ra[0][q], x);
+        sh[q] = __shfl(x[0], lane & ~7, kWave);
+      }
+    }
     stage(0, ra[0], rb[0]);
+    stats(ra[0], rb[0]);
     __syncthreads();
     int sb = s0;
     for (; sb + D <= s1; sb += D) {
@@ -241,6 +308,7 @@ __global__ void __launch_bounds__(256 * KW) gemm_nt_kernel(GemmArgs g) {
         fetch(min(st + D, s1 - 1), ra[q], rb[q]);  // slot q was staged before this step
         mma(buf);
         stage(buf ^ 1, ra[(q + 1) % D], rb[(q + 1) % D]);  // nobody reads buf ^ 1 now
+        if (st + 1 < s1) stats(ra[(q + 1) % D], rb[(q + 1) % D]);  // past the last step: a re-read
         __syncthreads();
       }
     }
@@ -249,12 +317,40 @@ __global__ void __launch_bounds__(256 * KW) gemm_nt_kernel(GemmArgs g) {
       const int st = sb + q, buf = (st - s0) & 1;
       if (st < s1) {
         mma(buf);
-        if (st + 1 < s1) stage(buf ^ 1, ra[(q + 1) % D], rb[(q + 1) % D]);
+        if (st + 1 < s1) {
+          stage(buf ^ 1, ra[(q + 1) % D], rb[(q + 1) % D]);
+          stats(ra[(q + 1) % D], rb[(q + 1) % D]);
+        }
         __syncthreads();
       }
     }
   }
 
+  if constexpr (LN != 0) {  // the 8 lanes of a row combine; lane 0 of each stores
+#pragma unroll
+    for (int o = 1; o < 8; o <<= 1) {
+#pragma unroll
+      for (int q = 0; q < PA; ++q) {
+        sa[q] += __shfl_xor(sa[q], o, kWave);
+        sq[q] += __shfl_xor(sq[q], o, kWave);
+      }
+#pragma unroll
+      for (int q = 0; q < PB; ++q) cb[q] += __shfl_xor(cb[q], o, kWave);
+    }
+    if ((lane & 7) == 0) {
+      const float inv = 1.f / (float)g.K;
+#pragma unroll
+      for (int q = 0; q < PA; ++q) {
+        const int row = (threadIdx.x + NT * q) >> 3;
+        const float m1 = sa[q] * inv;
+        lnst[2 * row] = sh[q] + m1;
+        lnst[2 * row + 1] = rsqrtf(fmaxf(sq[q] * inv - m1 * m1, 0.f) + g.ln_eps);
+      }
+#pragma unroll
+      for (int q = 0; q < PB; ++q) lncs[(threadIdx.x + NT * q) >> 3] = cb[q];
+    }
+    if (KW == 1) __syncthreads();
+  }
   if (KW == 2) {  // the second K half's sums join the first's through LDS
     f4* red = reinterpret_cast<f4*>(&As[0][0]);
     __syncthreads();  // every wave is past the K loop's last LDS read
@@ -303,6 +399,12 @@ __global__ void __launch_bounds__(256 * KW) gemm_nt_kernel(GemmArgs g) {
       const int n0 = nb + wn + 16 * j + 4 * kq;
       const int64_t off = rowoff[i] + coloff[j];
       float x[4] = {acc[i][j][0], acc[i][j][1], acc[i][j][2], acc[i][j][3]};
+      if constexpr (LN != 0) {
+        const int lr = wm + 16 * i + r16, lc = wn + 16 * j + 4 * kq;
+        const float mu = lnst[2 * lr], rs = lnst[2 * lr + 1];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) x[e] = rs * (x[e] - mu * lncs[lc + e]);
+      }
       if (g.ksplit == 1 && g.bias) {
         const f4 bv = *reinterpret_cast<const f4*>(g.bias + n0);
 #pragma unroll
@@ -595,12 +697,12 @@ constexpr int kGemmBM = 64, kGemmBN = 64;
 // against 27.2 / 40.6 (GTR-L / GTR-X); 1600 x 1920 x 384 (750 tiles) 10.8
 // against 9.3, 12800 x 384 x 1536 37.4 against 36.5.
 constexpr int kKHalvesBelow = 256;
-template <int ADT, int BDT, int MT>
+template <int ADT, int BDT, int MT, int LN>
 static void launch_gemm(const GemmArgs& g, unsigned tiles, hipStream_t stream) {
   if (tiles < (unsigned)kKHalvesBelow)
-    hipLaunchKernelGGL((gemm_nt_kernel<ADT, BDT, MT, kGemmBM, kGemmBN, 2>), dim3(tiles), dim3(512), 0, stream, g);
+    hipLaunchKernelGGL((gemm_nt_kernel<ADT, BDT, MT, kGemmBM, kGemmBN, 2, LN>), dim3(tiles), dim3(512), 0, stream, g);
   else
-    hipLaunchKernelGGL((gemm_nt_kernel<ADT, BDT, MT, kGemmBM, kGemmBN, 1>), dim3(tiles), dim3(256), 0, stream, g);
+    hipLaunchKernelGGL((gemm_nt_kernel<ADT, BDT, MT, kGemmBM, kGemmBN, 1, LN>), dim3(tiles), dim3(256), 0, stream, g);
 }
 static int out_ksplit(int64_t M, int d, int hidden) {
   const int64_t wgs = ((M + kGemmBM - 1) / kGemmBM) * (d / kGemmBN);
@@ -709,9 +811,9 @@ extern "C" gtr_status gtr_spatial_swiglu(const gtr_swiglu_args* a, hipStream_t s
   GemmArgs g3{Hb, a->w_out, a->y, part, (int)M, a->d, a->hidden, a->y_dtype, ks, nullptr, ks == 1 ? a->residual : nullptr};
   const unsigned tiles3 = (unsigned)(((M + kGemmBM - 1) / kGemmBM) * (a->d / kGemmBN) * ks);
   if (bf)
-    launch_gemm<GTR_F16, GTR_BF16, GTR_F16>(g3, tiles3, stream);
+    launch_gemm<GTR_F16, GTR_BF16, GTR_F16, 0>(g3, tiles3, stream);
   else
-    launch_gemm<GTR_F16, GTR_F16, GTR_F16>(g3, tiles3, stream);
+    launch_gemm<GTR_F16, GTR_F16, GTR_F16, 0>(g3, tiles3, stream);
   if (hipGetLastError() != hipSuccess) return GTR_ERR_HIP;
   if (ks > 1) {
     const int64_t n4 = M * a->d / 4;
@@ -735,6 +837,8 @@ static gtr_status gemm_check(const gtr_gemm_args* a) {
   }
   if ((a->a_dtype != GTR_F16 && a->a_dtype != GTR_BF16) || a->b_dtype != a->a_dtype) return GTR_ERR_UNSUPPORTED;
   if (a->c_dtype != GTR_F16 && a->c_dtype != GTR_BF16 && a->c_dtype != GTR_F32) return GTR_ERR_UNSUPPORTED;
+  if (a->row_norm && (a->row_norm != 1 || a->a_tokens || !(a->row_norm_eps >= 0.f && a->row_norm_eps < 1e30f)))
+    return GTR_ERR_UNSUPPORTED;
   if (a->M > 0x7fffffff - 128 || ((a->M + kGemmBM - 1) / kGemmBM) * (a->N / kGemmBN) > 0x7fffffff)
     return GTR_ERR_SHAPE;
   if (!a->a || !a->b || !a->c) return GTR_ERR_NULL;
@@ -761,11 +865,19 @@ extern "C" gtr_status gtr_gemm(const gtr_gemm_args* a, hipStream_t stream) {
   const gtr_status st = gemm_check(a);
   if (st != GTR_OK) return st;
   GemmArgs g{a->a, a->b, a->c, nullptr, (int)a->M, a->N, a->K, (int)a->c_dtype, 1, a->bias, a->res,
-             a->a_tokens, a->c_tokens, a->c_tokens ? a->c_heads : 0, a->c_tokens ? a->c_head_dim : 0};
+             a->a_tokens, a->c_tokens, a->c_tokens ? a->c_heads : 0, a->c_tokens ? a->c_head_dim : 0,
+             a->row_norm ? a->row_norm_eps : 0.f, 0};
   const unsigned tiles = (unsigned)(((a->M + kGemmBM - 1) / kGemmBM) * (a->N / kGemmBN));
-  if (a->a_dtype == GTR_BF16)
-    launch_gemm<GTR_BF16, GTR_BF16, GTR_BF16>(g, tiles, stream);
-  else
-    launch_gemm<GTR_F16, GTR_F16, GTR_F16>(g, tiles, stream);
+  if (a->a_dtype == GTR_BF16) {
+    if (a->row_norm)
+      launch_gemm<GTR_BF16, GTR_BF16, GTR_BF16, 1>(g, tiles, stream);
+    else
+      launch_gemm<GTR_BF16, GTR_BF16, GTR_BF16, 0>(g, tiles, stream);
+  } else {
+    if (a->row_norm)
+      launch_gemm<GTR_F16, GTR_F16, GTR_F16, 1>(g, tiles, stream);
+    else
+      launch_gemm<GTR_F16, GTR_F16, GTR_F16, 0>(g, tiles, stream);
+  }
   return hipGetLastError() == hipSuccess ? GTR_OK : GTR_ERR_HIP;
 }

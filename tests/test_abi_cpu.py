@@ -394,3 +394,25 @@ def test_noalloc_validation(lib):
     a = base_args(B=1, heads=6, H=40, W=40)
     a.workspace, a.workspace_bytes = None, 0  # ignored by this entry point
     assert lib.gtr_gla_workspace_size(ctypes.byref(a)) <= 32 << 20
+
+
+# ---------------------------------------------------------------------------
+# gtr_gemm: the row normalisation's argument checks (before any HIP call)
+# ---------------------------------------------------------------------------
+
+def gemm_args(M=200, N=128, K=192):
+    g = gtr.GemmArgs()
+    step = 1 << 30
+    g.a, g.b, g.c = FAKE, FAKE + step, FAKE + 2 * step
+    g.a_dtype = g.b_dtype = g.c_dtype = gtr.F16
+    g.M, g.N, g.K = M, N, K
+    g.row_norm, g.row_norm_eps = 1, 1e-6
+    return g
+
+
+@pytest.mark.parametrize("field,val", [("a_tokens", 100), ("row_norm_eps", -1.0), ("row_norm_eps", float("nan")),
+                                       ("row_norm", 2)])
+def test_gemm_row_norm_rejects(lib, field, val):
+    g = gemm_args()
+    setattr(g, field, val)
+    assert lib.gtr_gemm(ctypes.byref(g), None) == UNSUP

@@ -68,6 +68,28 @@ def test_gemm_residual_in_place():
 
 
 @pytest.mark.parametrize("dtype", [torch.float16, torch.bfloat16])
+@pytest.mark.parametrize("M,N,K,offset", [(1600, 1920, 384, 1.0), (200, 128, 192, 40.0), (37, 64, 64, 0.0),
+                                          (1, 384, 384, 5.0), (3200, 384, 192, 300.0)])
+def test_gemm_row_norm(dtype, M, N, K, offset):
+    """gtr_gemm with row_norm: the layer normalisation (no affine weights) of
+    every row of a, then the product, against the float64 oracle's
+    layer_norm. Row means up to 300 times the spread check the shifted
+    squares; grids below and above 256 tiles run both kernel shapes."""
+    rng = np.random.default_rng(M + K)
+    a = (rnd(rng, M, K, dtype=torch.float32) * 3 + torch.from_numpy(rng.uniform(-1, 1, (M, 1)) * offset).float())
+    a = a.to(dtype)
+    b = rnd(rng, N, K, std=K ** -0.5, dtype=dtype)
+    bi = rnd(rng, N, dtype=torch.float32)
+    c = gtr.gtr_gemm(a.to(DEV), b.to(DEV), bias=bi.to(DEV), row_norm_eps=1e-6)
+    torch.cuda.synchronize()
+    want = oracle.layer_norm(a.double().numpy(), None, None, 1e-6) @ b.double().numpy().T + bi.double().numpy()
+    got = c.double().cpu().numpy()
+    ulp = 2.0 ** -8 if dtype == torch.bfloat16 else 2.0 ** -11
+    err = np.max(np.abs(got - want) / (np.abs(want) * ulp + 1e-3 * np.max(np.abs(want))))
+    assert err <= 1.0, err
+
+
+@pytest.mark.parametrize("dtype", [torch.float16, torch.bfloat16])
 @pytest.mark.parametrize("B,L,heads,parts", [(1, 1600, 6, 4), (2, 207, 3, 1)])
 def test_gemm_head_major_operands(dtype, B, L, heads, parts):
     """gtr_gemm storing c head-major and reading a head-major a: the same

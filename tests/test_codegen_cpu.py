@@ -478,9 +478,14 @@ def check_kernel(text, name, kern, regions, wgs, waves=4):
                                                             (2, 2, 2, 64, 414, 384, 64, 2, 1, 9),
                                                             # 4 waves per tile at 256 tiles and more
                                                             (2, 2, 2, 64, 3200, 384, 64, 2, 1, 1),
-                                                            (1, 2, 1, 64, 4096, 384, 128, 0, 1, 0)])
+                                                            (1, 2, 1, 64, 4096, 384, 128, 0, 1, 0),
+                                                            # rows of A normalised (the block's first layer norm)
+                                                            (1, 1, 1, 64, 1600, 1920, 384, 1, 1, 16 | 8 | 1),
+                                                            (2, 2, 2, 64, 37, 128, 192, 2, 1, 16 | 2),
+                                                            (1, 1, 1, 64, 200, 384, 64, 0, 1, 16)])
 def test_swiglu_gemm_addresses(adt, bdt, mt, bn, M, N, K, cdt, ks, epi):
-    """epi: bit 0 a bias, bit 1 a residual (gtr_gemm's epilogue), bits 2 / 3 head-major A / C."""
+    """epi: bit 0 a bias, bit 1 a residual (gtr_gemm's epilogue), bits 2 / 3 head-major A / C, bit 4 the
+    rows of A normalised."""
     text = swiglu_asm()
     base = 0x1000_0000_0000
     es = {0: 4, 1: 2, 2: 2}
@@ -493,11 +498,11 @@ def test_swiglu_gemm_addresses(adt, bdt, mt, bn, M, N, K, cdt, ks, epi):
     # epi bit 2: head-major A, bit 3: head-major C (6 heads of 64), two images of M / 2 tokens (one if M is odd)
     at = (M // 2 if M % 2 == 0 else M) if epi & 4 else 0
     ct = (M // 2 if M % 2 == 0 else M) if epi & 8 else 0
-    kern = struct.pack("<QQQQiiiii4xQQqqii", A, B, C, P, M, N, K, cdt, ks, BI if epi & 1 else 0,
-                       R if epi & 2 else 0, at, ct, 6 if ct else 0, 64 if ct else 0)
+    kern = struct.pack("<QQQQiiiii4xQQqqiifi", A, B, C, P, M, N, K, cdt, ks, BI if epi & 1 else 0,
+                       R if epi & 2 else 0, at, ct, 6 if ct else 0, 64 if ct else 0, 1e-6 if epi & 16 else 0.0, 0)
     # 8 waves per tile below 256 tiles (the K halves on separate waves), 4 above
     kw = 2 if ((M + 63) // 64) * (N // bn) * ks < 256 else 1
-    name = f"_ZN3gtr14gemm_nt_kernelILi{adt}ELi{bdt}ELi{mt}ELi64ELi{bn}ELi{kw}EEEvNS_8GemmArgsE"
+    name = f"_ZN3gtr14gemm_nt_kernelILi{adt}ELi{bdt}ELi{mt}ELi64ELi{bn}ELi{kw}ELi{1 if epi & 16 else 0}EEEvNS_8GemmArgsE"
     assert name in emu.kernel_names(text)
     gx, gy = (M + 63) // 64, N // bn
     T = gx * gy * ks
