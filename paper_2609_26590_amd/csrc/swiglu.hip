@@ -683,9 +683,11 @@ __global__ void __launch_bounds__(256) gated_conv_kernel(GatedConvArgs f) {
 // 15.1 with 128 x 64 (78); the whole Spatial SwiGLU 27.3 against 30.4 (128 x 64
 // tiles with K split in 2 and the reduction) at GTR-L and 40.5 against 41.3 at
 // GTR-X; 32 x 64 tiles 28.9 / 42.2; at 3200 and 12800 tokens the two tile
-// sizes are on par. K is split into the fewest slices that give 128 work-groups
+// sizes are on par. K is split into the fewest slices that give 64 work-groups
 // when M x d alone does not (small grids only): every slice costs a float32
-// partial product and its share of the reduction.
+// partial product and its share of the reduction. (With 8-wave tiles below 256
+// tiles, a target of 64 against 128 took the GTR-S block from 48.9 to 47.3 us:
+// its 75-tile output product no longer splits; 256 was slower at every width.)
 constexpr int kGemmBM = 64, kGemmBN = 64;
 
 // A grid of fewer tiles than the chip's 256 compute units leaves CUs idle, and
@@ -707,7 +709,7 @@ static void launch_gemm(const GemmArgs& g, unsigned tiles, hipStream_t stream) {
 static int out_ksplit(int64_t M, int d, int hidden) {
   const int64_t wgs = ((M + kGemmBM - 1) / kGemmBM) * (d / kGemmBN);
   int s = 1;
-  while (wgs * s < 128 && s < 8 && hidden / 64 >= 2 * s * KB) s *= 2;
+  while (wgs * s < 64 && s < 8 && hidden / 64 >= 2 * s * KB) s *= 2;
   return s;
 }
 

@@ -329,7 +329,7 @@ def test_swiglu_workspace_size(lib):
     M = 2 * 1600
     a256 = lambda x: (x + 255) // 256 * 256
     # H in fp16 (G and V stay on chip); the output product splits K only when
-    # its 64 x 64 tiles give fewer than 128 work-groups: 50 x 6 = 300 do not
+    # its 64 x 64 tiles give fewer than 64 work-groups: 50 x 6 = 300 do not
     base = a256(M * 1536 * 2)
     assert lib.gtr_spatial_swiglu_workspace_size(ctypes.byref(a)) == base
     one = swiglu_args(B=1, H=40, W=40, d=384, hidden=1536)  # 25 x 6 work-groups: no split
@@ -337,6 +337,9 @@ def test_swiglu_workspace_size(lib):
     small = swiglu_args(B=1, H=16, W=16, d=384, hidden=1536)  # 4 x 6 work-groups: 4 slices
     assert lib.gtr_spatial_swiglu_workspace_size(ctypes.byref(small)) == \
         a256(a256(256 * 1536 * 2) + 4 * 256 * 384 * 4)
+    tiny = swiglu_args(B=1, H=8, W=8, d=64, hidden=2048)  # 1 work-group: 8 slices (the most)
+    assert lib.gtr_spatial_swiglu_workspace_size(ctypes.byref(tiny)) == \
+        a256(a256(64 * 2048 * 2) + 8 * 64 * 64 * 4)
     big = swiglu_args(B=8, H=40, W=40, d=384, hidden=1536)  # 100 x 6 work-groups: no split
     assert lib.gtr_spatial_swiglu_workspace_size(ctypes.byref(big)) == a256(12800 * 1536 * 2)
 
