@@ -74,9 +74,11 @@ def test_gemm_row_norm(dtype, M, N, K, offset):
     """gtr_gemm with row_norm: the layer normalisation (no affine weights) of
     every row of a, then the product, against the float64 oracle's
     layer_norm. Row means up to 300 times the spread check the shifted
-    squares; grids below and above 256 tiles run both kernel shapes."""
+    squares; every seventh row is constant (variance zero, the result is the
+    bias alone); grids below and above 256 tiles run both kernel shapes."""
     rng = np.random.default_rng(M + K)
     a = (rnd(rng, M, K, dtype=torch.float32) * 3 + torch.from_numpy(rng.uniform(-1, 1, (M, 1)) * offset).float())
+    a[::7] = torch.from_numpy(rng.uniform(-4, 4, (len(range(0, M, 7)), 1))).float()  # constant rows: zero spread
     a = a.to(dtype)
     b = rnd(rng, N, K, std=K ** -0.5, dtype=dtype)
     bi = rnd(rng, N, dtype=torch.float32)
